@@ -1,0 +1,210 @@
+/*
+ * mi355svm.h -- C ABI of a kernel-SVM dual solver for one AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The library trains C-SVC and eps-SVR models with the RBF kernel by the
+ * working-set decomposition of Wang et al., "Rgtsvm: Support Vector Machines
+ * on a GPU in R" (arXiv 1706.05544), and evaluates their decision function.
+ * Everything that computes runs in hand-written HIP kernels; this header
+ * only moves pointers and sizes.
+ *
+ * Problem (Section 3, Eq. 2):
+ *     min_a  1/2 a^T Q a + p^T a   s.t.  y^T a = 0,  0 <= a_t <= C,
+ *     Q_ts = y_t y_s K(x_smp(t), x_smp(s)),  K(u,v) = exp(-gamma |u - v|^2).
+ *   C-SVC:   one variable per sample, y_t = label in {+1,-1}, p_t = -1.
+ *   eps-SVR: two variables per sample (Section 3, "positive and negative
+ *            copy"; Eq. 1): copy (i,+) with y = +1, p = eps - z_i and copy
+ *            (i,-) with y = -1, p = eps + z_i.
+ * Decision function: D(x) = sum_i c_i K(x_i, x) + b with c_i = y_i a_i
+ * (C-SVC) or c_i = a_(i,+) - a_(i,-) (eps-SVR).
+ *
+ * Conventions shared by every call:
+ *   - status: 0 OK, > 0 warning (result valid), < 0 error (nothing written,
+ *     *out set to NULL where there is one).  svm_last_error() returns a
+ *     thread-local message for the last non-OK status.
+ *   - All argument validation happens before any device call, so invalid
+ *     arguments are reported even on a machine without a GPU.
+ *   - Host inputs are read during the call and copied once to the device;
+ *     they are never retained.  Device inputs (on_device = 1) are borrowed
+ *     for the duration of the call and used on params->stream.
+ *   - Calls are synchronous: they return after the device work they queued
+ *     has finished.  Models and solvers are not shared between threads
+ *     without external locking.
+ */
+#ifndef MI355SVM_H
+#define MI355SVM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SVM_OK = 0,
+    SVM_W_MAX_ITER = 1,        /* max_iter reached; model valid, gap > tol */
+    SVM_E_INVALID = -1,        /* bad argument (message says which) */
+    SVM_E_UNSUPPORTED = -2,    /* valid but not implemented (e.g. kernel) */
+    SVM_E_NOMEM = -3,          /* device or host allocation failed */
+    SVM_E_DEVICE = -4,         /* no usable GPU, or a HIP runtime error */
+    SVM_E_INTERNAL = -5
+} svm_status;
+
+typedef enum { SVM_C_SVC = 0, SVM_EPS_SVR = 1 } svm_type;
+
+/* Section 3 lists four kernels; RBF is implemented, the others return
+ * SVM_E_UNSUPPORTED. */
+typedef enum {
+    SVM_KERNEL_LINEAR = 0,
+    SVM_KERNEL_POLY = 1,
+    SVM_KERNEL_RBF = 2,
+    SVM_KERNEL_SIGMOID = 3
+} svm_kernel;
+
+typedef enum { SVM_DENSE = 0, SVM_CSR = 1 } svm_layout;
+
+/* A feature matrix of n rows and d columns.
+ *   dense: values[i*ld + k], fp32, ld >= d.
+ *   CSR:   row_ptr[0..n] (row_ptr[0] = 0, nondecreasing, row_ptr[n] = nnz),
+ *          col_idx[nnz] sorted and unique within each row, in [0, d),
+ *          values[nnz].
+ * on_device = 1: every pointer is device memory of params->device. */
+typedef struct {
+    int32_t layout;
+    int32_t on_device;
+    int64_t n, d;
+    const float *values;
+    int64_t ld;
+    const int64_t *row_ptr;
+    const int32_t *col_idx;
+    int64_t nnz;
+} svm_matrix;
+
+typedef struct {
+    int32_t type;          /* svm_type */
+    int32_t kernel;        /* svm_kernel */
+    double C;              /* > 0 */
+    double epsilon;        /* >= 0, eps-SVR tube half-width */
+    double gamma;          /* >= 0; 0 means 1/d (the e1071 default) */
+    double tol;            /* > 0; stop when max_{I_up} v - min_{I_low} v <= tol */
+    int64_t max_iter;      /* outer iterations; <= 0: max(1e7, 100 N) */
+    int32_t working_set;   /* q, even, in [2, 64]; 16 as in Section 3 */
+    int32_t device;        /* HIP device ordinal */
+    int64_t cache_bytes;   /* kernel-row cache budget; 0 default, < 0 off */
+    void *stream;          /* hipStream_t; NULL: a stream of the library */
+    int32_t check_every;   /* outer iterations between host polls (0: 64) */
+    double inner_ratio;    /* subproblem stops at local gap <= max(ratio *
+                              global gap, tol/2); 0: 0.1 */
+    int32_t max_inner;     /* subproblem step cap; 0: 8 q */
+    int32_t profile;       /* 1: time the row/update kernel with events */
+} svm_params;
+
+/* Per-output statistics of a trained model. */
+typedef struct {
+    int32_t type;          /* svm_type */
+    int32_t n_outputs;     /* 1, or the number of classes (one-vs-rest) */
+    int64_t n_train;       /* training samples */
+    int64_t n_features;
+    int64_t n_sv;          /* support rows stored (union over outputs) */
+    double gamma;          /* resolved gamma */
+    /* the rest refers to the output asked for */
+    int32_t status;        /* SVM_OK or SVM_W_MAX_ITER */
+    int64_t n_sv_output;   /* samples with non-zero coefficient */
+    int64_t n_bounded;     /* variables at C */
+    int64_t iters;         /* outer iterations (working sets optimised) */
+    double gap;            /* final m - M */
+    double b;              /* bias */
+    double dual_obj;       /* f(a) of Eq. 2 */
+    int64_t kernel_rows;   /* kernel rows K(x_s, X) evaluated */
+    int64_t cache_hits;    /* kernel rows served by the row cache */
+    double train_ms;       /* device time from solver start to model ready */
+    double row_kernel_ms;  /* summed row/update kernel time (profile = 1) */
+    int64_t row_kernel_launches; /* launches included in row_kernel_ms */
+    int64_t row_kernel_rows;     /* rows processed by those launches */
+} svm_model_info;
+
+typedef struct svm_model svm_model;  /* opaque, owned by the library */
+
+/* Defaults: C-SVC, RBF, C = 1, eps = 0.1, gamma = 0 (1/d), tol = 1e-3,
+ * working_set = 16, device 0, NULL stream. */
+void svm_params_default(svm_params *p);
+
+/* Train a binary C-SVC (y = labels, each +1 or -1, both present) or an
+ * eps-SVR (y = targets z).  y has n entries in the memory space of X.
+ * On success *out receives a model the caller frees with svm_model_free. */
+svm_status svm_train(const svm_matrix *X, const float *y,
+                     const svm_params *p, svm_model **out);
+
+/* One-vs-rest multi-class C-SVC (Section 3, multi-class classification):
+ * labels in [0, n_classes), n_classes >= 2; one binary problem per class
+ * (class c against the rest), all sharing X on the device. */
+svm_status svm_train_ovr(const svm_matrix *X, const int32_t *labels,
+                         int32_t n_classes, const svm_params *p,
+                         svm_model **out);
+
+/* Decision values D (m x n_outputs, row-major, fp64) for the m rows of X,
+ * written to `decision` in the memory space of X (caller-owned). */
+svm_status svm_predict(const svm_model *m, const svm_matrix *X,
+                       double *decision);
+
+/* Labels: +1 / -1 (D >= 0 gives +1) for C-SVC, argmax over classes (ties to
+ * the lowest class) for one-vs-rest.  eps-SVR models: SVM_E_INVALID. */
+svm_status svm_predict_labels(const svm_model *m, const svm_matrix *X,
+                              int32_t *labels);
+
+svm_status svm_model_get_info(const svm_model *m, int32_t output,
+                              svm_model_info *info);
+
+/* Host copies of one output: sv_idx[n_sv_output] (training-row indices,
+ * increasing) and coef[n_sv_output]; alpha[N] (N = n or 2n) may be NULL. */
+svm_status svm_model_get(const svm_model *m, int32_t output, int32_t *sv_idx,
+                         double *coef, double *alpha);
+
+void svm_model_free(svm_model *m);
+
+const char *svm_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * Test hooks: a solver whose state can be set and stepped one phase at a
+ * time, so the tests can compare single steps with the CPU oracle from an
+ * identical state.  Not needed for training.  Host pointers only.
+ * ---------------------------------------------------------------------- */
+typedef struct svm_solver svm_solver;
+
+svm_status svm_test_solver_create(const svm_matrix *X, const float *y,
+                                  const svm_params *p, svm_solver **out);
+void svm_test_solver_free(svm_solver *s);
+
+/* Replace the state: alpha[N] and responses F[n] (fp64). */
+svm_status svm_test_set_state(svm_solver *s, const double *alpha,
+                              const double *F);
+svm_status svm_test_get_state(svm_solver *s, double *alpha, double *F);
+
+/* Working-set selection on the current state: the q/2 largest keys of I_up
+ * interleaved with the q/2 smallest of I_low, ties to the lowest index:
+ * B[<= q] variable indices, *nB, and m = max_{I_up} v, M = min_{I_low} v. */
+svm_status svm_test_select(svm_solver *s, int32_t *B, int32_t *nB, double *m,
+                           double *M);
+
+/* Kernel rows K(x_samples[j], X) for k <= 64 samples: out[j*n + i], fp32. */
+svm_status svm_test_rows(svm_solver *s, const int32_t *samples, int32_t k,
+                         float *out);
+
+/* Solve the subproblem on B from the current state; returns the new
+ * alpha_B and the number of inner steps (state unchanged). */
+svm_status svm_test_subproblem(svm_solver *s, const int32_t *B, int32_t nB,
+                               double inner_tol, int32_t max_inner,
+                               double *alpha_B_new, int32_t *steps);
+
+/* Set alpha_B to the given values and update F with the row/update kernel. */
+svm_status svm_test_apply(svm_solver *s, const int32_t *B, int32_t nB,
+                          const double *alpha_B_new);
+
+/* Run up to k full outer iterations; *iters gets the count, *gap the gap. */
+svm_status svm_test_iterate(svm_solver *s, int64_t k, int64_t *iters,
+                            double *gap);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MI355SVM_H */

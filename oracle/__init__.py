@@ -242,7 +242,7 @@ def responses(X, y, p: Params, alpha) -> np.ndarray:
 
 
 def select(y, p: Params, alpha, F, q: int, d: int = 1):
-    """Working set (reading R3) -> (B, m, M)."""
+    """Working set of at most q variables -> (B, m, M)."""
     y = np.ascontiguousarray(y, dtype=np.float32)
     alpha = np.ascontiguousarray(alpha, dtype=np.float64)
     F = np.ascontiguousarray(F, dtype=np.float64)
@@ -264,7 +264,7 @@ def sample_of(type_: int, n: int, t):
 
 def subproblem(X, y, p: Params, alpha, F, B, inner_tol: float,
                max_inner: int, KBB=None):
-    """Inner maximal-violating-pair solve on B (reading R4).
+    """Inner maximal-violating-pair solve on the working set B.
 
     KBB defaults to the fp64 kernel block over the samples of B.
     Returns (alpha_B_new, steps)."""
@@ -318,7 +318,7 @@ def model_decision(X, y, p: Params, res: Result, Xt, threads: int = 0):
 
 
 def train_ovr(X, labels, n_classes: int, p: Params):
-    """One-vs-rest (reading R14): one binary C-SVC per class."""
+    """One-vs-rest multi-class: one binary C-SVC per class."""
     labels = np.asarray(labels)
     out = []
     for c in range(n_classes):

@@ -30,7 +30,8 @@
 #include <omp.h>
 #endif
 
-#define TAU 1e-12 /* step denominator floor for a degenerate pair (R7) */
+#define TAU 1e-12 /* curvature floor for a pair of coincident points (the
+                     * paper is silent; LIBSVM uses the same floor) */
 
 /* ---------------------------------------------------------------------- */
 /* kernel                                                                 */
@@ -136,8 +137,9 @@ static double yv(int32_t type, int64_t n, const float *y, int64_t t)
     return y[t] > 0.0f ? 1.0 : -1.0;
 }
 
-/* linear term p_t of Eq. 2: -1 for C-SVC (R1); eps - z_i for the positive
- * copy and eps + z_i for the negative copy (Eq. 1 substituted, R2). */
+/* linear term p_t of Eq. 2: -1 for C-SVC (the paper's "all-one" vector with
+ * the sign that makes Eq. 2 a minimisation, as in LIBSVM); eps - z_i for the
+ * positive copy and eps + z_i for the negative copy (Eq. 1 substituted). */
 static double pv(int32_t type, int64_t n, const float *y, double eps, int64_t t)
 {
     if (type == ORC_EPS_SVR) {
@@ -209,7 +211,8 @@ int orc_state_summary(int64_t n, const float *y, const orc_params *p,
     res->M = M;
     res->gap = (i < 0 || j < 0) ? 0.0 : m - M;
 
-    /* bias: mean key over free variables, else the midpoint (R6) */
+    /* bias (not defined in the paper): mean key over free variables, else
+     * the midpoint of m and M, as in LIBSVM */
     double sum = 0.0;
     int64_t nfree = 0;
     for (int64_t t = 0; t < N; ++t) {
@@ -348,7 +351,7 @@ int orc_responses(const orc_mat *X, const float *y, const orc_params *p,
 }
 
 /* ---------------------------------------------------------------------- */
-/* working set of q variables and its subproblem (readings R3, R4)        */
+/* working set of q variables and its subproblem (Section 3)              */
 /* ---------------------------------------------------------------------- */
 
 typedef struct { double k; int64_t t; } kv;

@@ -11,17 +11,19 @@
  *       s.t.  y^T a = 0,  0 <= a_t <= C,
  *     with Q_ts = y_t y_s K(x_smp(t), x_smp(s)) (Section 3, text after Eq. 1);
  *   - C-SVC: one variable per sample, p_t = -1 (Eq. 2 with the "all-one"
- *     linear term read as LIBSVM's -e, reading R1);
+ *     linear term taken with the sign that makes Eq. 2 a minimisation, as
+ *     in LIBSVM);
  *   - eps-SVR: two copies per sample (Section 3, "positive and negative
  *     copy"), copy (i,+) has y = +1 and p = eps - z_i, copy (i,-) has
- *     y = -1 and p = eps + z_i (Eq. 1 substituted into Eq. 2, reading R2);
+ *     y = -1 and p = eps + z_i (Eq. 1 substituted into Eq. 2; the only
+ *     assignment under which a free positive copy lies on f(x) = z - eps);
  *   - RBF kernel K(a,b) = exp(-gamma * sum_k (a_k - b_k)^2)  (Section 3,
  *     "radial basis function", e1071 parameterisation).
  *
  * Solver: maximal-violating-pair SMO (Chang & Lin 2011, cited in Section 1
  * and Section 3 for Eq. 1), no shrinking, kernel values from the direct
  * definition in fp64, stop when m - M <= tol (Section 3: iterate "until
- * convergence"; the KKT-gap reading R5).
+ * convergence", read as the KKT gap of LIBSVM).
  *
  * Notation used throughout (identical in the tests):
  *   F_i   = sum_t y_t a_t K(x_i, x_smp(t))      ("responses", Section 3)
@@ -62,7 +64,7 @@ typedef struct {
     int64_t iters;      /* SMO steps taken by this call */
     double gap;         /* m - M at exit */
     double m, M;
-    double b;           /* bias (reading R6) */
+    double b;           /* bias: mean v over free variables, else (m+M)/2 */
     double obj;         /* dual objective f(a) */
     int64_t n_sv;       /* samples with non-zero coefficient */
     int64_t n_free;     /* variables with 0 < a < C */
@@ -99,12 +101,14 @@ int orc_responses(const orc_mat *X, const float *y, const orc_params *p,
 
 /* Working set of size <= q (q even): interleave the q/2 largest keys of I_up
  * with the q/2 smallest keys of I_low, ties to the lowest variable index,
- * dropping repeats (reading R3).  Returns |B| in *nB; also m and M. */
+ * dropping repeats (Section 3: the working set is chosen by the largest
+ * partial derivatives under the constraints).  Returns |B| in *nB, m, M. */
 int orc_select(int64_t n, const float *y, const orc_params *p,
                const double *alpha, const double *F, int32_t q,
                int32_t *B, int32_t *nB, double *m, double *M);
 
-/* Subproblem on B (reading R4): maximal-violating-pair steps restricted to B,
+/* Subproblem on B (Section 3: the working set is optimised from the local
+ * gradient): maximal-violating-pair steps restricted to B,
  * starting from keys v_B = r_B - F_smp(B), using the kernel block KBB
  * (nB x nB, KBB[a*nB+b] = K(x_smp(B_a), x_smp(B_b))).  Stops when the local
  * gap <= inner_tol or after max_inner steps.  Writes the new alpha_B. */

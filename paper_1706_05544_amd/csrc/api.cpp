@@ -1,0 +1,497 @@
+// C ABI of the MI355X kernel-SVM library: argument validation, status codes,
+// the thread-local error message, and dispatch to the solver.  Nothing here
+// computes on the data; all arithmetic runs in the HIP kernels.
+#include <cmath>
+#include <cstring>
+#include <memory>
+#include <new>
+#include <string>
+
+#include "solver.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+svm_status fail(svm_status st, const std::string& msg)
+{
+    g_err = msg;
+    return st;
+}
+
+bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
+
+svm_status check_params(const svm_params* p)
+{
+    if (!p) return fail(SVM_E_INVALID, "params is NULL");
+    if (p->type != SVM_C_SVC && p->type != SVM_EPS_SVR)
+        return fail(SVM_E_INVALID, "type must be SVM_C_SVC or SVM_EPS_SVR");
+    if (p->kernel != SVM_KERNEL_RBF) {
+        if (p->kernel >= SVM_KERNEL_LINEAR && p->kernel <= SVM_KERNEL_SIGMOID)
+            return fail(SVM_E_UNSUPPORTED, "only the RBF kernel is implemented");
+        return fail(SVM_E_INVALID, "unknown kernel");
+    }
+    if (!finite_pos(p->C)) return fail(SVM_E_INVALID, "C must be finite and > 0");
+    if (!std::isfinite(p->epsilon) || p->epsilon < 0)
+        return fail(SVM_E_INVALID, "epsilon must be finite and >= 0");
+    if (!std::isfinite(p->gamma) || p->gamma < 0)
+        return fail(SVM_E_INVALID, "gamma must be finite and >= 0");
+    if (!finite_pos(p->tol)) return fail(SVM_E_INVALID, "tol must be finite and > 0");
+    if (p->working_set < 2 || p->working_set > msvm::kMaxQ ||
+        (p->working_set & 1))
+        return fail(SVM_E_INVALID, "working_set must be even and in [2, 64]");
+    if (p->device < 0) return fail(SVM_E_INVALID, "device must be >= 0");
+    if (p->check_every < 0) return fail(SVM_E_INVALID, "check_every must be >= 0");
+    if (!std::isfinite(p->inner_ratio) || p->inner_ratio < 0 ||
+        p->inner_ratio >= 1)
+        return fail(SVM_E_INVALID, "inner_ratio must be in [0, 1)");
+    if (p->max_inner < 0) return fail(SVM_E_INVALID, "max_inner must be >= 0");
+    return SVM_OK;
+}
+
+svm_status check_matrix(const svm_matrix* X, int64_t min_rows)
+{
+    if (!X) return fail(SVM_E_INVALID, "X is NULL");
+    if (X->layout != SVM_DENSE && X->layout != SVM_CSR)
+        return fail(SVM_E_INVALID, "unknown layout");
+    if (X->n < min_rows)
+        return fail(SVM_E_INVALID, min_rows > 1
+                                       ? "X needs at least 2 rows"
+                                       : "X rows must be >= 0");
+    if (X->d < 1 || X->d > (int64_t)1 << 30)
+        return fail(SVM_E_INVALID, "d must be in [1, 2^30]");
+    if (X->layout == SVM_CSR)
+        return fail(SVM_E_UNSUPPORTED, "CSR input is not implemented yet");
+    if (X->n > 0 && !X->values) return fail(SVM_E_INVALID, "X values is NULL");
+    if (X->ld < X->d) return fail(SVM_E_INVALID, "ld must be >= d");
+    if (X->n > ((int64_t)1 << 31) - 1)
+        return fail(SVM_E_INVALID, "n must be < 2^31");
+    return SVM_OK;
+}
+
+svm_status check_device(int dev)
+{
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || count <= 0)
+        return fail(SVM_E_DEVICE, "no HIP device available");
+    if (dev >= count) return fail(SVM_E_INVALID, "device ordinal out of range");
+    return SVM_OK;
+}
+
+svm_status check_host_labels(const float* y, int64_t n, int32_t type)
+{
+    if (type == SVM_EPS_SVR) {
+        for (int64_t i = 0; i < n; ++i)
+            if (!std::isfinite(y[i]))
+                return fail(SVM_E_INVALID, "targets must be finite");
+        return SVM_OK;
+    }
+    bool pos = false, neg = false;
+    for (int64_t i = 0; i < n; ++i) {
+        if (y[i] == 1.0f) pos = true;
+        else if (y[i] == -1.0f) neg = true;
+        else return fail(SVM_E_INVALID, "labels must be +1 or -1");
+    }
+    if (!pos || !neg) return fail(SVM_E_INVALID, "both classes must be present");
+    return SVM_OK;
+}
+
+void fill_info(svm_model_info& in, const svm_model& m,
+               const msvm::SolveResult& r)
+{
+    std::memset(&in, 0, sizeof(in));
+    in.type = m.type;
+    in.n_outputs = m.n_out;
+    in.n_train = m.n_train;
+    in.n_features = m.d;
+    in.gamma = m.gamma;
+    in.status = r.status;
+    in.n_sv_output = r.n_sv;
+    in.n_bounded = r.n_bounded;
+    in.iters = r.iters;
+    in.gap = r.gap;
+    in.b = r.b;
+    in.dual_obj = r.obj;
+    in.kernel_rows = r.kernel_rows;
+    in.cache_hits = 0;
+    in.train_ms = r.train_ms;
+    in.row_kernel_ms = r.row_ms;
+    in.row_kernel_launches = r.row_launches;
+    in.row_kernel_rows = r.row_rows;
+}
+
+#define GUARD_BEGIN try {
+#define GUARD_END                                                      \
+    }                                                                  \
+    catch (const msvm::Error& e) { return fail(e.status, e.msg); }     \
+    catch (const std::bad_alloc&) {                                    \
+        return fail(SVM_E_NOMEM, "host allocation failed");            \
+    }                                                                  \
+    catch (const std::exception& e) { return fail(SVM_E_INTERNAL, e.what()); } \
+    catch (...) { return fail(SVM_E_INTERNAL, "unknown error"); }
+
+}  // namespace
+
+namespace msvm {
+void set_error(svm_status st, const std::string& msg)
+{
+    (void)st;
+    g_err = msg;
+}
+}  // namespace msvm
+
+struct svm_solver {
+    std::unique_ptr<msvm::Context> cx;
+    msvm::Features f;
+    msvm::DevBuf<float> y;
+    std::unique_ptr<msvm::Solver> s;
+};
+
+extern "C" {
+
+const char* svm_last_error(void) { return g_err.c_str(); }
+
+void svm_params_default(svm_params* p)
+{
+    if (!p) return;
+    std::memset(p, 0, sizeof(*p));
+    p->type = SVM_C_SVC;
+    p->kernel = SVM_KERNEL_RBF;
+    p->C = 1.0;
+    p->epsilon = 0.1;
+    p->gamma = 0.0;
+    p->tol = 1e-3;
+    p->max_iter = 0;
+    p->working_set = 16;
+    p->device = 0;
+    p->cache_bytes = 0;
+    p->stream = nullptr;
+    p->check_every = 0;
+    p->inner_ratio = 0.0;
+    p->max_inner = 0;
+    p->profile = 0;
+}
+
+svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
+                     svm_model** out)
+{
+    if (!out) return fail(SVM_E_INVALID, "out is NULL");
+    *out = nullptr;
+    svm_status st;
+    if ((st = check_params(p)) != SVM_OK) return st;
+    if ((st = check_matrix(X, 2)) != SVM_OK) return st;
+    if (!y) return fail(SVM_E_INVALID, "y is NULL");
+    if (!X->on_device && (st = check_host_labels(y, X->n, p->type)) != SVM_OK)
+        return st;
+    if ((st = check_device(p->device)) != SVM_OK) return st;
+    GUARD_BEGIN
+    msvm::Context cx(p->device, p->stream);
+    msvm::Features f;
+    msvm::load_features(X, f, cx);
+    msvm::DevBuf<float> yd((size_t)X->n);
+    HIP_TRY(hipMemcpyAsync(yd.p, y, (size_t)X->n * sizeof(float),
+                           X->on_device ? hipMemcpyDeviceToDevice
+                                        : hipMemcpyHostToDevice,
+                           cx.stream));
+    msvm::SolveOptions o = msvm::make_options(p, X->n, X->d);
+    msvm::Solver s(cx, f, yd.p, o);
+    msvm::SolveResult r = s.train();
+
+    auto m = std::make_unique<svm_model>();
+    m->type = p->type;
+    m->n_out = 1;
+    m->n_train = X->n;
+    m->d = X->d;
+    m->ldp = f.ldp;
+    m->gamma = o.gamma;
+    m->gexp = (float)(o.gamma * 1.4426950408889634);
+    m->device = p->device;
+    m->b.assign(1, r.b);
+    msvm::DevBuf<double> coef((size_t)X->n);
+    s.coefficients(coef.p, 1, 0);
+    msvm::build_model(*m, cx, f, coef.p, 1);
+    m->alpha.resize(1);
+    m->alpha[0].resize((size_t)s.N());
+    s.get_alpha(m->alpha[0].data());
+    m->info.resize(1);
+    fill_info(m->info[0], *m, r);
+    *out = m.release();
+    if (r.status == SVM_W_MAX_ITER)
+        return fail(SVM_W_MAX_ITER, "max_iter reached before the gap met tol");
+    return SVM_OK;
+    GUARD_END
+}
+
+svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
+                         int32_t n_classes, const svm_params* p,
+                         svm_model** out)
+{
+    if (!out) return fail(SVM_E_INVALID, "out is NULL");
+    *out = nullptr;
+    svm_status st;
+    if ((st = check_params(p)) != SVM_OK) return st;
+    if (p->type != SVM_C_SVC)
+        return fail(SVM_E_INVALID, "one-vs-rest needs type SVM_C_SVC");
+    if ((st = check_matrix(X, 2)) != SVM_OK) return st;
+    if (!labels) return fail(SVM_E_INVALID, "labels is NULL");
+    if (n_classes < 2 || n_classes > 16)
+        return fail(SVM_E_INVALID, "n_classes must be in [2, 16]");
+    if (!X->on_device) {
+        std::vector<int64_t> cnt((size_t)n_classes, 0);
+        for (int64_t i = 0; i < X->n; ++i) {
+            if (labels[i] < 0 || labels[i] >= n_classes)
+                return fail(SVM_E_INVALID, "labels must be in [0, n_classes)");
+            cnt[(size_t)labels[i]]++;
+        }
+        for (int32_t c = 0; c < n_classes; ++c)
+            if (cnt[(size_t)c] == 0)
+                return fail(SVM_E_INVALID, "every class needs a sample");
+    }
+    if ((st = check_device(p->device)) != SVM_OK) return st;
+    GUARD_BEGIN
+    msvm::Context cx(p->device, p->stream);
+    msvm::Features f;
+    msvm::load_features(X, f, cx);
+    const int64_t n = X->n;
+    msvm::DevBuf<int32_t> ld((size_t)n);
+    HIP_TRY(hipMemcpyAsync(ld.p, labels, (size_t)n * sizeof(int32_t),
+                           X->on_device ? hipMemcpyDeviceToDevice
+                                        : hipMemcpyHostToDevice,
+                           cx.stream));
+    if (X->on_device) {
+        msvm::DevBuf<int32_t> bad(1);
+        HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
+        msvm::launch_check_labels(ld.p, n, n_classes, bad.p, cx.stream);
+        int32_t hb = 0;
+        HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t),
+                               hipMemcpyDeviceToHost, cx.stream));
+        cx.sync();
+        if (hb) return fail(SVM_E_INVALID, "labels must be in [0, n_classes)");
+    }
+    msvm::SolveOptions o = msvm::make_options(p, n, X->d);
+    auto m = std::make_unique<svm_model>();
+    m->type = SVM_C_SVC;
+    m->n_out = n_classes;
+    m->n_train = n;
+    m->d = X->d;
+    m->ldp = f.ldp;
+    m->gamma = o.gamma;
+    m->gexp = (float)(o.gamma * 1.4426950408889634);
+    m->device = p->device;
+    m->b.assign((size_t)n_classes, 0.0);
+    m->alpha.resize((size_t)n_classes);
+    m->info.resize((size_t)n_classes);
+    msvm::DevBuf<double> coef((size_t)(n * n_classes));
+    msvm::DevBuf<float> yc((size_t)n);
+    std::vector<msvm::SolveResult> res((size_t)n_classes);
+    svm_status worst = SVM_OK;
+    for (int32_t c = 0; c < n_classes; ++c) {
+        msvm::launch_ovr_labels(ld.p, n, c, yc.p, cx.stream);
+        msvm::Solver s(cx, f, yc.p, o);
+        res[(size_t)c] = s.train();
+        s.coefficients(coef.p, n_classes, c);
+        m->b[(size_t)c] = res[(size_t)c].b;
+        m->alpha[(size_t)c].resize((size_t)s.N());
+        s.get_alpha(m->alpha[(size_t)c].data());
+        if (res[(size_t)c].status != SVM_OK) worst = res[(size_t)c].status;
+    }
+    msvm::build_model(*m, cx, f, coef.p, n_classes);
+    for (int32_t c = 0; c < n_classes; ++c)
+        fill_info(m->info[(size_t)c], *m, res[(size_t)c]);
+    *out = m.release();
+    if (worst == SVM_W_MAX_ITER)
+        return fail(SVM_W_MAX_ITER, "max_iter reached for at least one class");
+    return SVM_OK;
+    GUARD_END
+}
+
+static svm_status predict_impl(const svm_model* mdl, const svm_matrix* X,
+                               double* decision, int32_t* labels)
+{
+    if (!mdl) return fail(SVM_E_INVALID, "model is NULL");
+    svm_status st;
+    if ((st = check_matrix(X, 0)) != SVM_OK) return st;
+    if (X->d != mdl->d)
+        return fail(SVM_E_INVALID, "X has a different number of features");
+    if (X->n > 0 && !decision && !labels)
+        return fail(SVM_E_INVALID, "output is NULL");
+    if (labels && mdl->type == SVM_EPS_SVR)
+        return fail(SVM_E_INVALID, "labels are undefined for eps-SVR");
+    if (X->n == 0) return SVM_OK;
+    if ((st = check_device(mdl->device)) != SVM_OK) return st;
+    GUARD_BEGIN
+    msvm::Context cx(mdl->device, nullptr);
+    msvm::Features t;
+    msvm::load_features(X, t, cx);
+    const int64_t m = X->n;
+    msvm::DevBuf<double> D((size_t)(m * mdl->n_out));
+    msvm::predict_device(*mdl, cx, t, D.p);
+    const hipMemcpyKind kind =
+        X->on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+    if (decision) {
+        HIP_TRY(hipMemcpyAsync(decision, D.p,
+                               (size_t)(m * mdl->n_out) * sizeof(double), kind,
+                               cx.stream));
+    } else {
+        msvm::DevBuf<int32_t> L((size_t)m);
+        msvm::launch_argmax_labels(D.p, m, mdl->n_out, mdl->type, L.p,
+                                   cx.stream);
+        HIP_TRY(hipMemcpyAsync(labels, L.p, (size_t)m * sizeof(int32_t), kind,
+                               cx.stream));
+        cx.sync();
+    }
+    cx.sync();
+    return SVM_OK;
+    GUARD_END
+}
+
+svm_status svm_predict(const svm_model* m, const svm_matrix* X,
+                       double* decision)
+{
+    if (X && X->n > 0 && !decision)
+        return fail(SVM_E_INVALID, "decision is NULL");
+    return predict_impl(m, X, decision, nullptr);
+}
+
+svm_status svm_predict_labels(const svm_model* m, const svm_matrix* X,
+                              int32_t* labels)
+{
+    if (X && X->n > 0 && !labels) return fail(SVM_E_INVALID, "labels is NULL");
+    if (m && m->type == SVM_EPS_SVR)
+        return fail(SVM_E_INVALID, "labels are undefined for eps-SVR");
+    return predict_impl(m, X, nullptr, labels);
+}
+
+svm_status svm_model_get_info(const svm_model* m, int32_t output,
+                              svm_model_info* info)
+{
+    if (!m || !info) return fail(SVM_E_INVALID, "model or info is NULL");
+    if (output < 0 || output >= m->n_out)
+        return fail(SVM_E_INVALID, "output out of range");
+    *info = m->info[(size_t)output];
+    info->n_sv = m->n_sv;
+    return SVM_OK;
+}
+
+svm_status svm_model_get(const svm_model* m, int32_t output, int32_t* sv_idx,
+                         double* coef, double* alpha)
+{
+    if (!m) return fail(SVM_E_INVALID, "model is NULL");
+    if (output < 0 || output >= m->n_out)
+        return fail(SVM_E_INVALID, "output out of range");
+    int64_t k = 0;
+    for (int64_t j = 0; j < m->n_sv; ++j) {
+        double c = m->coef[(size_t)(j * m->n_out + output)];
+        if (c == 0.0) continue;
+        if (sv_idx) sv_idx[k] = m->sv_idx[(size_t)j];
+        if (coef) coef[k] = c;
+        ++k;
+    }
+    if (alpha) {
+        const auto& a = m->alpha[(size_t)output];
+        std::memcpy(alpha, a.data(), a.size() * sizeof(double));
+    }
+    return SVM_OK;
+}
+
+void svm_model_free(svm_model* m) { delete m; }
+
+svm_status svm_test_solver_create(const svm_matrix* X, const float* y,
+                                  const svm_params* p, svm_solver** out)
+{
+    if (!out) return fail(SVM_E_INVALID, "out is NULL");
+    *out = nullptr;
+    svm_status st;
+    if ((st = check_params(p)) != SVM_OK) return st;
+    if ((st = check_matrix(X, 2)) != SVM_OK) return st;
+    if (X->on_device) return fail(SVM_E_INVALID, "test hooks take host data");
+    if (!y) return fail(SVM_E_INVALID, "y is NULL");
+    if ((st = check_host_labels(y, X->n, p->type)) != SVM_OK) return st;
+    if ((st = check_device(p->device)) != SVM_OK) return st;
+    GUARD_BEGIN
+    auto s = std::make_unique<svm_solver>();
+    s->cx = std::make_unique<msvm::Context>(p->device, p->stream);
+    msvm::load_features(X, s->f, *s->cx);
+    s->y.alloc((size_t)X->n);
+    HIP_TRY(hipMemcpyAsync(s->y.p, y, (size_t)X->n * sizeof(float),
+                           hipMemcpyHostToDevice, s->cx->stream));
+    s->s = std::make_unique<msvm::Solver>(
+        *s->cx, s->f, s->y.p, msvm::make_options(p, X->n, X->d));
+    *out = s.release();
+    return SVM_OK;
+    GUARD_END
+}
+
+void svm_test_solver_free(svm_solver* s) { delete s; }
+
+#define SOLVER_CALL(body)                                        \
+    if (!s) return fail(SVM_E_INVALID, "solver is NULL");        \
+    GUARD_BEGIN body; return SVM_OK;                             \
+    GUARD_END
+
+svm_status svm_test_set_state(svm_solver* s, const double* alpha,
+                              const double* F)
+{
+    if (!alpha || !F) return fail(SVM_E_INVALID, "alpha or F is NULL");
+    SOLVER_CALL(s->s->set_state(alpha, F))
+}
+
+svm_status svm_test_get_state(svm_solver* s, double* alpha, double* F)
+{
+    SOLVER_CALL(s->s->get_state(alpha, F))
+}
+
+svm_status svm_test_select(svm_solver* s, int32_t* B, int32_t* nB, double* m,
+                           double* M)
+{
+    if (!B || !nB || !m || !M) return fail(SVM_E_INVALID, "NULL output");
+    SOLVER_CALL(s->s->select(B, nB, m, M))
+}
+
+svm_status svm_test_rows(svm_solver* s, const int32_t* samples, int32_t k,
+                         float* out)
+{
+    if (!samples || !out || k < 1 || k > msvm::kMaxQ)
+        return fail(SVM_E_INVALID, "need 1..64 samples and an output");
+    if (s)
+        for (int32_t j = 0; j < k; ++j)
+            if (samples[j] < 0 || samples[j] >= s->f.n)
+                return fail(SVM_E_INVALID, "sample index out of range");
+    SOLVER_CALL(s->s->rows(samples, k, out))
+}
+
+svm_status svm_test_subproblem(svm_solver* s, const int32_t* B, int32_t nB,
+                               double inner_tol, int32_t max_inner,
+                               double* alpha_B_new, int32_t* steps)
+{
+    if (!B || !alpha_B_new || !steps || nB < 1 || nB > msvm::kMaxQ)
+        return fail(SVM_E_INVALID, "need 1..64 variables and outputs");
+    if (s)
+        for (int32_t j = 0; j < nB; ++j)
+            if (B[j] < 0 || B[j] >= s->s->N())
+                return fail(SVM_E_INVALID, "variable index out of range");
+    SOLVER_CALL(s->s->subproblem(B, nB, inner_tol, max_inner, alpha_B_new,
+                                 steps))
+}
+
+svm_status svm_test_apply(svm_solver* s, const int32_t* B, int32_t nB,
+                          const double* alpha_B_new)
+{
+    if (!B || !alpha_B_new || nB < 1 || nB > msvm::kMaxQ)
+        return fail(SVM_E_INVALID, "need 1..64 variables");
+    if (s)
+        for (int32_t j = 0; j < nB; ++j)
+            if (B[j] < 0 || B[j] >= s->s->N())
+                return fail(SVM_E_INVALID, "variable index out of range");
+    SOLVER_CALL(s->s->apply(B, nB, alpha_B_new))
+}
+
+svm_status svm_test_iterate(svm_solver* s, int64_t k, int64_t* iters,
+                            double* gap)
+{
+    if (!iters || !gap || k < 0) return fail(SVM_E_INVALID, "bad arguments");
+    SOLVER_CALL(s->s->iterate(k, iters, gap))
+}
+
+}  // extern "C"

@@ -1,0 +1,198 @@
+// Internal declarations of the MI355X kernel-SVM library (not installed).
+//
+// Data layout in HBM (one device):
+//   X    n x ldp fp32, row-major, ldp = d rounded up to a multiple of 4 and
+//        zero-padded, so that every lane can load aligned float4 pieces.
+//   sq   n fp32 squared norms |x_i|^2 (summed in fp64, rounded once).
+//   F    n fp64 responses F_i = sum_t y_t a_t K(x_i, x_smp(t)).
+//   a    N fp64 dual variables; st N bytes of state (label sign, I_up, I_low).
+//   z    n fp32 targets (eps-SVR only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "../../include/mi355svm.h"
+
+namespace msvm {
+
+constexpr int kMaxQ = 64;          // largest working set
+constexpr int kMaxHalf = kMaxQ / 2;
+constexpr int kRowThreads = 256;   // row/update kernel: 4 waves
+constexpr int kSelThreads = 1024;  // select/solve kernel: one block
+constexpr int kSelPerThread = 8;   // candidates per side held per thread
+constexpr double kTau = 1e-12;     // curvature floor of a degenerate pair
+
+// state byte of a dual variable
+constexpr uint8_t ST_YPOS = 1;  // y_t = +1
+constexpr uint8_t ST_UP = 2;    // t in I_up
+constexpr uint8_t ST_LOW = 4;   // t in I_low
+
+// Device-resident description of the current working set.  Written by the
+// select/solve kernel, read by the row/update kernel of the same iteration.
+struct WorkingSet {
+    int32_t done;      // 0 running, 1 converged (gap <= tol), 2 iteration cap
+    int32_t nB;        // variables in B
+    int32_t nS;        // distinct samples of B (slots)
+    int32_t pad0;
+    int64_t iter;      // outer iterations performed
+    int64_t rows;      // kernel rows evaluated (sum of nS)
+    double gap, m, M;
+    int32_t B[kMaxQ];
+    int32_t S[kMaxQ];     // sample of each slot
+    int32_t slotB[kMaxQ]; // slot of each variable of B
+    float sS[kMaxQ];      // squared norm of each slot's sample
+    double coef[kMaxQ];   // change of the expansion coefficient per slot
+    double alphaB[kMaxQ]; // new alpha_B (written by the solve)
+    int32_t steps;        // inner steps of the last subproblem
+    int32_t pad1;
+};
+
+// Final reductions of a state (bias and objective).
+struct Summary {
+    double sum_free_v;  // sum of v_t over free variables
+    double obj2;        // sum_t a_t y_t (r_t + v_t); f = -obj2 / 2
+    int64_t n_free;
+    int64_t n_bounded;
+};
+
+// row/update kernel modes
+enum : int32_t {
+    RU_UPDATE = 1,      // F += sum_s coef_s K(x_i, x_s)
+    RU_ROWS = 2,        // write K(x_s, x_i) to rows_out (tests)
+    RU_CAND = 4,        // keys and per-block candidates
+    RU_CHECK_DONE = 8   // return at once if the solve has finished
+};
+
+// select/solve kernel modes
+enum : int32_t {
+    SS_SOLVE = 1,       // build B, solve, write the new working set
+    SS_CHECK_DONE = 2,
+    SS_GIVEN_B = 4,     // B is taken from ws->B (tests)
+    SS_NO_WRITE = 8,    // leave alpha/state untouched (tests)
+    SS_SET_ALPHA = 16   // alpha_B taken from ws->alphaB instead of solved
+};
+
+struct RowArgs {
+    const float* X;
+    const float* sq;
+    double* F;
+    const uint8_t* st;
+    const float* z;
+    const WorkingSet* ws;
+    const float* xS;      // kMaxQ x ldp rows of the working-set samples
+    double* cand_key;     // [nb][2][half]: up scores v, low scores -v
+    int32_t* cand_idx;
+    float* rows_out;      // nS x n (tests)
+    int64_t n, ldp;
+    double eps;
+    float gexp;           // gamma * log2(e)
+    int32_t half;
+    int32_t tiles;        // 16-row tiles per wave
+    int32_t mode;
+    int32_t nS_override;  // >= 0: use this many slots (tests), else ws->nS
+};
+
+struct SelArgs {
+    const double* cand_key;
+    const int32_t* cand_idx;
+    int32_t nb, half;
+    WorkingSet* ws;
+    double* alpha;
+    uint8_t* st;
+    const double* F;
+    const float* z;
+    const float* X;
+    const float* sq;
+    float* xS;
+    int64_t n, ldp;
+    double C, eps, tol;
+    float gexp;
+    double inner_ratio;
+    double inner_tol_override;  // >= 0: fixed inner tolerance (tests)
+    int32_t max_inner;
+    int64_t max_iter;
+    int32_t mode;
+};
+
+struct PredictArgs {
+    const float* Xt;      // m x ldp test rows
+    const float* sqt;
+    int64_t m, ldp;
+    const float* SV;      // nsv x ldp support rows
+    const float* sqsv;
+    int64_t nsv;
+    const double* coef;   // nsv x n_out
+    const double* b;      // n_out or nullptr
+    int32_t n_out;
+    const int32_t* sv_train_idx;  // with self_match: K(x_i, x_i) = 1 exactly
+    int32_t self_match;
+    double* out;          // m x n_out
+    float gexp;
+};
+
+// ---- launch wrappers (kernels.hip / predict.hip) ----
+void launch_pad_copy(const float* src, int64_t ld, int64_t n, int64_t d,
+                     float* dst, int64_t ldp, hipStream_t s);
+void launch_norms(const float* X, int64_t n, int64_t ldp, float* sq,
+                  int32_t* bad_flag, hipStream_t s);
+void launch_init_state(int32_t type, const float* y, int64_t n, uint8_t* st,
+                       int32_t* bad_flag, hipStream_t s);
+void launch_ovr_labels(const int32_t* labels, int64_t n, int32_t cls,
+                       float* y, hipStream_t s);
+void launch_check_labels(const int32_t* labels, int64_t n, int32_t ncls,
+                         int32_t* bad_flag, hipStream_t s);
+void launch_check_finite(const float* v, int64_t n, int32_t* bad_flag,
+                         hipStream_t s);
+void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
+                 hipStream_t s);
+size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr);
+void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
+void launch_state_from_alpha(int32_t type, const float* y, const double* a,
+                             int64_t n, double C, uint8_t* st, hipStream_t s);
+void launch_coef(int32_t type, const double* a, const uint8_t* st, int64_t n,
+                 double* c, hipStream_t s);
+void launch_coef_strided(int32_t type, const double* a, const uint8_t* st,
+                         int64_t n, double* c, int32_t stride, int32_t off,
+                         hipStream_t s);
+void launch_summary(int32_t type, const double* a, const uint8_t* st,
+                    const double* F, const float* z, int64_t n, double C,
+                    double eps, Summary* out, hipStream_t s);
+// compaction of rows with any non-zero coefficient over n_out columns
+void launch_compact(const double* coef, int64_t n, int32_t n_out,
+                    int32_t* blk_cnt, int32_t* idx_out, double* coef_out,
+                    int64_t* count_out, hipStream_t s);
+void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
+                        const int32_t* idx, int64_t k, float* out,
+                        float* sq_out, hipStream_t s);
+void launch_predict(const PredictArgs& a, hipStream_t s);
+void launch_argmax_labels(const double* D, int64_t m, int32_t n_out,
+                          int32_t type, int32_t* labels, hipStream_t s);
+void launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
+
+int64_t compact_blocks(int64_t n);
+
+// ---- errors ----
+struct Error {
+    svm_status status;
+    std::string msg;
+};
+
+void set_error(svm_status st, const std::string& msg);
+
+#define HIP_TRY(expr)                                                     \
+    do {                                                                  \
+        hipError_t e_ = (expr);                                           \
+        if (e_ != hipSuccess) {                                           \
+            throw ::msvm::Error{e_ == hipErrorOutOfMemory ? SVM_E_NOMEM   \
+                                                          : SVM_E_DEVICE, \
+                                std::string(#expr) + ": " +               \
+                                    hipGetErrorString(e_)};               \
+        }                                                                 \
+    } while (0)
+
+}  // namespace msvm

@@ -1,0 +1,98 @@
+// Device helpers shared by the HIP kernels of the library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+
+namespace msvm {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// One 16x16x4 fp32 matrix-core step.  Lane l supplies A[l%16][l/16] and
+// B[l/16][l%16]; lane l, register v of the result holds D[4(l/16)+v][l%16].
+__device__ __forceinline__ floatx4 mfma4(float a, float b, floatx4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Accumulate the dot products of 16 A rows with 16 B rows over ldp features
+// in the fixed order used by every kernel of the library: 16-feature chunks
+// in increasing order, lane group g = lane/16 covering features
+// c0 + 4g .. c0 + 4g + 3 of each chunk, one MFMA per component.  Using one
+// order everywhere makes every K value computed for a pair bitwise equal,
+// whichever kernel computes it.
+__device__ __forceinline__ floatx4 mfma_chunk(floatx4 acc, float4 a, float4 b)
+{
+    acc = mfma4(a.x, b.x, acc);
+    acc = mfma4(a.y, b.y, acc);
+    acc = mfma4(a.z, b.z, acc);
+    acc = mfma4(a.w, b.w, acc);
+    return acc;
+}
+
+// RBF kernel value from the expansion |a|^2 + |b|^2 - 2 a.b, clamped at 0
+// (fp32 cancellation can make it slightly negative), as 2^(-gexp * d2)
+// with gexp = gamma * log2(e).
+__device__ __forceinline__ float rbf_from_dot(float sa, float sb, float dot,
+                                              float gexp)
+{
+    float d2 = fmaf(-2.0f, dot, sa + sb);
+    d2 = fmaxf(d2, 0.0f);
+    return __builtin_amdgcn_exp2f(-gexp * d2);
+}
+
+// Order "largest key first, lowest index on ties".
+__device__ __forceinline__ bool better(double k1, int32_t i1, double k2,
+                                       int32_t i2)
+{
+    return k1 > k2 || (k1 == k2 && i1 < i2);
+}
+
+// (k1,i1) comes strictly after (k2,i2) in that order.
+__device__ __forceinline__ bool after(double k1, int32_t i1, double k2,
+                                      int32_t i2)
+{
+    return k1 < k2 || (k1 == k2 && i1 > i2);
+}
+
+// Wave-wide best (key, index); every lane ends with the result.
+__device__ __forceinline__ void wave_best(double& k, int32_t& i)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        double ok = __shfl_xor(k, off);
+        int32_t oi = __shfl_xor(i, off);
+        if (better(ok, oi, k, i)) {
+            k = ok;
+            i = oi;
+        }
+    }
+}
+
+__device__ __forceinline__ float4 ld4(const float* p)
+{
+    return *reinterpret_cast<const float4*>(p);
+}
+
+__device__ __forceinline__ float4 zero4()
+{
+    return make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+}
+
+__device__ __forceinline__ double pick4(const double (&v)[4], int k)
+{
+    return k == 0 ? v[0] : k == 1 ? v[1] : k == 2 ? v[2] : v[3];
+}
+
+__device__ __forceinline__ uint8_t state_bits(double y, double a, double C)
+{
+    uint8_t s = y > 0 ? 1 : 0;
+    bool up = (y > 0 && a < C) || (y < 0 && a > 0);
+    bool lo = (y > 0 && a > 0) || (y < 0 && a < C);
+    return (uint8_t)(s | (up ? 2 : 0) | (lo ? 4 : 0));
+}
+
+}  // namespace msvm

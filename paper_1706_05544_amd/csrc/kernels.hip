@@ -1,0 +1,995 @@
+// HIP kernels of the working-set dual solve (gfx950).
+//
+// One outer iteration of the decomposition (Section 3: pick a working set
+// of 16 coefficients by the largest partial derivatives under the
+// constraints, optimise them from the local gradient, update the responses)
+// is two launches:
+//
+//   k_select  one block of 1024 threads.  Merges the per-block candidates of
+//             the previous k_rows into the global working set B (the q/2
+//             largest keys of I_up interleaved with the q/2 smallest keys of
+//             I_low), tests the gap m - M against tol, computes the kernel
+//             block K_BB on the matrix cores and solves the subproblem on B
+//             with maximal-violating-pair steps.  Writes the new alpha_B, the
+//             state bytes and the coefficient change of each distinct sample.
+//   k_rows    the whole grid.  Streams X once: for each 16-row tile, the dot
+//             products with the (at most 16 per column block) working-set
+//             samples on the matrix cores (16x16x4 fp32), the RBF epilogue,
+//             F_i += sum_s dc_s K(x_i, x_s) in fp64, the keys v of the
+//             variables of the tile and the per-block top-q/2 candidates of
+//             each side for the next k_select.
+#include "common.hpp"
+#include "device.hpp"
+
+namespace msvm {
+
+// ---------------------------------------------------------------------------
+// feature store
+// ---------------------------------------------------------------------------
+
+__global__ void k_pad_copy(const float* src, int64_t ld, int64_t n, int64_t d,
+                           float* dst, int64_t ldp)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t total = n * ldp;
+    for (; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t r = i / ldp, c = i - r * ldp;
+        dst[i] = c < d ? src[r * ld + c] : 0.0f;
+    }
+}
+
+void launch_pad_copy(const float* src, int64_t ld, int64_t n, int64_t d,
+                     float* dst, int64_t ldp, hipStream_t s)
+{
+    if (n <= 0) return;
+    int64_t blocks = (n * ldp + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    k_pad_copy<<<(unsigned)blocks, 256, 0, s>>>(src, ld, n, d, dst, ldp);
+}
+
+// Squared norms: 16 lanes per row, fp64 partial sums, fixed reduction order.
+// A non-finite row (NaN, Inf, or a square that overflows) sets *bad.
+__global__ void k_norms(const float* X, int64_t n, int64_t ldp, float* sq,
+                        int32_t* bad)
+{
+    int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+    int sub = threadIdx.x & 15;
+    if (row >= n) return;
+    const float* x = X + row * ldp;
+    double acc = 0.0;
+    for (int64_t k = sub; k < ldp; k += 16) {
+        double v = (double)x[k];
+        acc += v * v;
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 16);
+    if (sub == 0) {
+        float f = (float)acc;
+        sq[row] = f;
+        if (!isfinite(f)) atomicOr(bad, 1);
+    }
+}
+
+void launch_norms(const float* X, int64_t n, int64_t ldp, float* sq,
+                  int32_t* bad, hipStream_t s)
+{
+    if (n <= 0) return;
+    int64_t blocks = (n * 16 + 255) / 256;
+    k_norms<<<(unsigned)blocks, 256, 0, s>>>(X, n, ldp, sq, bad);
+}
+
+__global__ void k_check_finite(const float* v, int64_t n, int32_t* bad)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n && !isfinite(v[i])) atomicOr(bad, 1);
+}
+
+void launch_check_finite(const float* v, int64_t n, int32_t* bad,
+                         hipStream_t s)
+{
+    if (n <= 0) return;
+    k_check_finite<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(v, n, bad);
+}
+
+// Initial state bytes for alpha = 0.  C-SVC: label +1 -> I_up, -1 -> I_low;
+// a label other than +-1 sets bit 0 of *bad, each class seen sets bit 1
+// (+1) or bit 2 (-1).  eps-SVR: positive copies in I_up, negative in I_low.
+__global__ void k_init_state(int32_t type, const float* y, int64_t n,
+                             uint8_t* st, int32_t* bad)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    if (type == SVM_C_SVC) {
+        float v = y[i];
+        if (v == 1.0f) {
+            st[i] = ST_YPOS | ST_UP;
+            atomicOr(bad, 2);
+        } else if (v == -1.0f) {
+            st[i] = ST_LOW;
+            atomicOr(bad, 4);
+        } else {
+            st[i] = 0;
+            atomicOr(bad, 1);
+        }
+    } else {
+        st[i] = ST_YPOS | ST_UP;
+        st[n + i] = ST_LOW;
+        if (!isfinite(y[i])) atomicOr(bad, 1);
+    }
+}
+
+void launch_init_state(int32_t type, const float* y, int64_t n, uint8_t* st,
+                       int32_t* bad, hipStream_t s)
+{
+    k_init_state<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(type, y, n, st,
+                                                             bad);
+}
+
+__global__ void k_ovr_labels(const int32_t* labels, int64_t n, int32_t cls,
+                             float* y)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) y[i] = labels[i] == cls ? 1.0f : -1.0f;
+}
+
+void launch_ovr_labels(const int32_t* labels, int64_t n, int32_t cls,
+                       float* y, hipStream_t s)
+{
+    k_ovr_labels<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(labels, n, cls,
+                                                             y);
+}
+
+__global__ void k_check_labels(const int32_t* labels, int64_t n,
+                               int32_t ncls, int32_t* bad)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n && (labels[i] < 0 || labels[i] >= ncls)) atomicOr(bad, 1);
+}
+
+void launch_check_labels(const int32_t* labels, int64_t n, int32_t ncls,
+                         int32_t* bad, hipStream_t s)
+{
+    k_check_labels<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(labels, n,
+                                                               ncls, bad);
+}
+
+__global__ void k_fill_i32(int32_t* p, int32_t v, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+void launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s)
+{
+    if (n <= 0) return;
+    k_fill_i32<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p, v, n);
+}
+
+// State bytes from a given alpha (test hooks).
+__global__ void k_state_from_alpha(int32_t type, const float* y,
+                                   const double* a, int64_t n, double C,
+                                   uint8_t* st)
+{
+    int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t N = type == SVM_EPS_SVR ? 2 * n : n;
+    if (t >= N) return;
+    double yt = type == SVM_EPS_SVR ? (t < n ? 1.0 : -1.0)
+                                    : (y[t] > 0.0f ? 1.0 : -1.0);
+    st[t] = state_bits(yt, a[t], C);
+}
+
+void launch_state_from_alpha(int32_t type, const float* y, const double* a,
+                             int64_t n, double C, uint8_t* st, hipStream_t s)
+{
+    int64_t N = type == SVM_EPS_SVR ? 2 * n : n;
+    k_state_from_alpha<<<(unsigned)((N + 255) / 256), 256, 0, s>>>(
+        type, y, a, n, C, st);
+}
+
+// ---------------------------------------------------------------------------
+// row / update kernel
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int32_t local_var(int e, int64_t R, int64_t rblk,
+                                             int64_t n)
+{
+    return (int32_t)(e < R ? rblk + e : n + rblk + (e - R));
+}
+
+// Block-level top-`half` of both sides from keys staged in LDS, in the order
+// "largest score first, lowest variable index on ties"; `half` rounds, each
+// one a block-wide best over the entries after the previous winner.
+template <int NT>
+__device__ void block_topk(const double* ku, const double* kl, int count,
+                           int64_t R, int64_t rblk, int64_t n, int half,
+                           double* out_key, int32_t* out_idx)
+{
+    constexpr int NW = NT / 64;
+    __shared__ double rk[2][2][NW];
+    __shared__ int32_t ri[2][2][NW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    double pk0 = INFINITY, pk1 = INFINITY;
+    int32_t pi0 = -1, pi1 = -1;
+    for (int k = 0; k < half; ++k) {
+        double bk0 = -INFINITY, bk1 = -INFINITY;
+        int32_t bi0 = INT_MAX, bi1 = INT_MAX;
+        for (int e = tid; e < count; e += NT) {
+            int32_t t = local_var(e, R, rblk, n);
+            double u = ku[e], l = kl[e];
+            if (after(u, t, pk0, pi0) && better(u, t, bk0, bi0)) {
+                bk0 = u;
+                bi0 = t;
+            }
+            if (after(l, t, pk1, pi1) && better(l, t, bk1, bi1)) {
+                bk1 = l;
+                bi1 = t;
+            }
+        }
+        wave_best(bk0, bi0);
+        wave_best(bk1, bi1);
+        const int p = k & 1;
+        if (lane == 0) {
+            rk[p][0][wave] = bk0;
+            ri[p][0][wave] = bi0;
+            rk[p][1][wave] = bk1;
+            ri[p][1][wave] = bi1;
+        }
+        __syncthreads();
+        bk0 = rk[p][0][0];
+        bi0 = ri[p][0][0];
+        bk1 = rk[p][1][0];
+        bi1 = ri[p][1][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) {
+            if (better(rk[p][0][w], ri[p][0][w], bk0, bi0)) {
+                bk0 = rk[p][0][w];
+                bi0 = ri[p][0][w];
+            }
+            if (better(rk[p][1][w], ri[p][1][w], bk1, bi1)) {
+                bk1 = rk[p][1][w];
+                bi1 = ri[p][1][w];
+            }
+        }
+        pk0 = bk0;
+        pi0 = bi0;
+        pk1 = bk1;
+        pi1 = bi1;
+        if (tid == 0) {
+            out_key[k] = bk0;
+            out_idx[k] = bi0;
+            out_key[half + k] = bk1;
+            out_idx[half + k] = bi1;
+        }
+    }
+}
+
+size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
+{
+    size_t xs = (size_t)nblk_cols * 16 * (size_t)(ldp + 4) * sizeof(float);
+    size_t keys = (size_t)(svr ? 2 : 1) * 64 * tiles * 2 * sizeof(double);
+    return xs + keys;
+}
+
+template <bool SVR, int NBLK>
+__global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const WorkingSet* ws = a.ws;
+    if ((a.mode & RU_CHECK_DONE) && ws->done) return;
+
+    constexpr int NV = SVR ? 2 : 1;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, nl = lane & 15;
+    const int T = a.tiles;
+    const int64_t n = a.n, ldp = a.ldp;
+    const int64_t R = 64LL * T;
+    const int64_t rblk = (int64_t)blockIdx.x * R;
+    const int lstride = (int)ldp + 4;
+    float* xsl = reinterpret_cast<float*>(smem);
+    double* kup = reinterpret_cast<double*>(
+        smem + (size_t)NBLK * 16 * lstride * sizeof(float));
+    double* klo = kup + NV * R;
+
+    const bool want_rows = (a.mode & (RU_UPDATE | RU_ROWS)) != 0;
+    int nS = 0;
+    if (want_rows) nS = a.nS_override >= 0 ? a.nS_override : ws->nS;
+
+    if (nS > 0) {
+        const int q4 = (int)(ldp >> 2);
+        const int total = NBLK * 16 * q4;
+        for (int e = tid; e < total; e += kRowThreads) {
+            int slot = e / q4, c4 = e - slot * q4;
+            float4 v = slot < nS ? ld4(a.xS + (int64_t)slot * ldp + 4 * c4)
+                                 : zero4();
+            *reinterpret_cast<float4*>(xsl + slot * lstride + 4 * c4) = v;
+        }
+    }
+    if (a.mode & RU_CAND) {
+        for (int e = tid; e < NV * R; e += kRowThreads) {
+            kup[e] = -INFINITY;
+            klo[e] = -INFINITY;
+        }
+    }
+    __syncthreads();
+
+    double cf[NBLK];
+    float ssl[NBLK];
+    int32_t sidx[NBLK];
+#pragma unroll
+    for (int b = 0; b < NBLK; ++b) {
+        int slot = b * 16 + nl;
+        bool ok = slot < nS;
+        cf[b] = (ok && (a.mode & RU_UPDATE)) ? ws->coef[slot] : 0.0;
+        ssl[b] = ok ? ws->sS[slot] : 0.0f;
+        sidx[b] = ok ? ws->S[slot] : -1;
+    }
+
+    for (int ti = 0; ti < T; ++ti) {
+        const int64_t r0 = rblk + ((int64_t)wave * T + ti) * 16;
+        if (r0 >= n) break;
+        const int64_t orow = r0 + 4 * g + nl;  // row owned by lanes nl < 4
+        const bool owner = nl < 4 && orow < n;
+        double Fn = 0.0;
+        if (owner && (a.mode & (RU_UPDATE | RU_CAND))) Fn = a.F[orow];
+
+        if (nS > 0) {
+            floatx4 acc[NBLK];
+#pragma unroll
+            for (int b = 0; b < NBLK; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+            const int64_t arow = r0 + nl;
+            const bool rv = arow < n;
+            const float* xr = a.X + (rv ? arow : 0) * ldp;
+#pragma unroll 4
+            for (int64_t c0 = 0; c0 < ldp; c0 += 16) {
+                const int64_t col = c0 + 4 * g;
+                const bool cv = col < ldp;
+                float4 av = (rv && cv) ? ld4(xr + col) : zero4();
+#pragma unroll
+                for (int b = 0; b < NBLK; ++b) {
+                    float4 bv = cv ? ld4(xsl + (b * 16 + nl) * lstride + col)
+                                   : zero4();
+                    acc[b] = mfma_chunk(acc[b], av, bv);
+                }
+            }
+            float sqr[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                int64_t rr = r0 + 4 * g + v;
+                sqr[v] = rr < n ? a.sq[rr] : 0.0f;
+            }
+            double part[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+            for (int b = 0; b < NBLK; ++b) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    int64_t rr = r0 + 4 * g + v;
+                    float kv = rbf_from_dot(sqr[v], ssl[b], acc[b][v], a.gexp);
+                    if (rr == (int64_t)sidx[b]) kv = 1.0f;
+                    part[v] = fma(cf[b], (double)kv, part[v]);
+                    if ((a.mode & RU_ROWS) && b * 16 + nl < nS && rr < n)
+                        a.rows_out[(int64_t)(b * 16 + nl) * n + rr] = kv;
+                }
+            }
+            if (a.mode & RU_UPDATE) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+#pragma unroll
+                    for (int off = 8; off > 0; off >>= 1)
+                        part[v] += __shfl_xor(part[v], off, 16);
+                }
+                Fn += pick4(part, nl & 3);
+                if (owner) a.F[orow] = Fn;
+            }
+        }
+
+        if ((a.mode & RU_CAND) && owner) {
+            const int64_t loc = orow - rblk;
+            const uint8_t s0 = a.st[orow];
+            const double rr0 = SVR ? (double)a.z[orow] - a.eps
+                                   : ((s0 & ST_YPOS) ? 1.0 : -1.0);
+            const double v0 = rr0 - Fn;
+            kup[loc] = (s0 & ST_UP) ? v0 : -INFINITY;
+            klo[loc] = (s0 & ST_LOW) ? -v0 : -INFINITY;
+            if (SVR) {
+                const uint8_t s1 = a.st[n + orow];
+                const double v1 = ((double)a.z[orow] + a.eps) - Fn;
+                kup[R + loc] = (s1 & ST_UP) ? v1 : -INFINITY;
+                klo[R + loc] = (s1 & ST_LOW) ? -v1 : -INFINITY;
+            }
+        }
+    }
+
+    if (!(a.mode & RU_CAND)) return;
+    __syncthreads();
+    block_topk<kRowThreads>(kup, klo, (int)(NV * R), R, rblk, n, a.half,
+                            a.cand_key + (size_t)blockIdx.x * 2 * a.half,
+                            a.cand_idx + (size_t)blockIdx.x * 2 * a.half);
+}
+
+template <bool SVR, int NBLK>
+static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s)
+{
+    size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipFuncSetAttribute((const void*)k_rows<SVR, NBLK>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            160 * 1024);
+        attr_set = true;
+    }
+    k_rows<SVR, NBLK><<<nblocks, kRowThreads, lds, s>>>(a);
+}
+
+void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
+                 hipStream_t s)
+{
+    if (nblocks <= 0) return;
+    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
+        case 2: rows_dispatch<false, 1>(a, nblocks, s); break;
+        case 3: rows_dispatch<true, 1>(a, nblocks, s); break;
+        case 4: rows_dispatch<false, 2>(a, nblocks, s); break;
+        case 5: rows_dispatch<true, 2>(a, nblocks, s); break;
+        case 8: rows_dispatch<false, 4>(a, nblocks, s); break;
+        case 9: rows_dispatch<true, 4>(a, nblocks, s); break;
+        default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
+    }
+}
+
+// ---------------------------------------------------------------------------
+// select / solve kernel
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int64_t sample_of(bool svr, int64_t t, int64_t n)
+{
+    return (svr && t >= n) ? t - n : t;
+}
+
+template <bool SVR, int NBLK>
+__global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
+{
+    WorkingSet* ws = a.ws;
+    if ((a.mode & SS_CHECK_DONE) && ws->done) return;
+
+    constexpr int NW = kSelThreads / 64;
+    constexpr int QS = NBLK * 16;  // slots covered by K_SS
+    __shared__ double upk[kMaxHalf], lok[kMaxHalf];
+    __shared__ int32_t upi[kMaxHalf], loi[kMaxHalf];
+    __shared__ double rk[2][2][NW];
+    __shared__ int32_t ri[2][2][NW];
+    __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
+    __shared__ float shsS[kMaxQ];
+    __shared__ float KSS[QS][QS + 1];
+    __shared__ double shDc[kMaxQ];
+    __shared__ int32_t shNB, shNS, shGo;
+    __shared__ double shGap;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int half = a.half;
+    const int64_t n = a.n, ldp = a.ldp;
+    const bool given = (a.mode & SS_GIVEN_B) != 0;
+
+    if (!given) {
+        // merge the per-block candidates of both sides
+        const int cnt = a.nb * half;
+        double ku[kSelPerThread], kl[kSelPerThread];
+        int32_t iu[kSelPerThread], il[kSelPerThread];
+#pragma unroll
+        for (int j = 0; j < kSelPerThread; ++j) {
+            int e = tid + j * kSelThreads;
+            if (e < cnt) {
+                int blk = e / half, k = e - blk * half;
+                size_t bu = (size_t)blk * 2 * half;
+                ku[j] = a.cand_key[bu + k];
+                iu[j] = a.cand_idx[bu + k];
+                kl[j] = a.cand_key[bu + half + k];
+                il[j] = a.cand_idx[bu + half + k];
+            } else {
+                ku[j] = kl[j] = -INFINITY;
+                iu[j] = il[j] = INT_MAX;
+            }
+        }
+        double pk0 = INFINITY, pk1 = INFINITY;
+        int32_t pi0 = -1, pi1 = -1;
+        for (int k = 0; k < half; ++k) {
+            double bk0 = -INFINITY, bk1 = -INFINITY;
+            int32_t bi0 = INT_MAX, bi1 = INT_MAX;
+#pragma unroll
+            for (int j = 0; j < kSelPerThread; ++j) {
+                if (after(ku[j], iu[j], pk0, pi0) &&
+                    better(ku[j], iu[j], bk0, bi0)) {
+                    bk0 = ku[j];
+                    bi0 = iu[j];
+                }
+                if (after(kl[j], il[j], pk1, pi1) &&
+                    better(kl[j], il[j], bk1, bi1)) {
+                    bk1 = kl[j];
+                    bi1 = il[j];
+                }
+            }
+            wave_best(bk0, bi0);
+            wave_best(bk1, bi1);
+            const int p = k & 1;
+            if (lane == 0) {
+                rk[p][0][wave] = bk0;
+                ri[p][0][wave] = bi0;
+                rk[p][1][wave] = bk1;
+                ri[p][1][wave] = bi1;
+            }
+            __syncthreads();
+            bk0 = rk[p][0][0];
+            bi0 = ri[p][0][0];
+            bk1 = rk[p][1][0];
+            bi1 = ri[p][1][0];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) {
+                if (better(rk[p][0][w], ri[p][0][w], bk0, bi0)) {
+                    bk0 = rk[p][0][w];
+                    bi0 = ri[p][0][w];
+                }
+                if (better(rk[p][1][w], ri[p][1][w], bk1, bi1)) {
+                    bk1 = rk[p][1][w];
+                    bi1 = ri[p][1][w];
+                }
+            }
+            pk0 = bk0;
+            pi0 = bi0;
+            pk1 = bk1;
+            pi1 = bi1;
+            if (tid == 0) {
+                upk[k] = bk0;
+                upi[k] = bi0;
+                lok[k] = bk1;
+                loi[k] = bi1;
+            }
+        }
+        __syncthreads();
+    }
+
+    if (tid == 0) {
+        int go = 0, nB = 0, nS = 0;
+        double gap = 0.0;
+        if (!given) {
+            const bool valid = upk[0] != -INFINITY && lok[0] != -INFINITY;
+            const double m = upk[0], M = -lok[0];
+            gap = valid ? m - M : 0.0;
+            ws->gap = gap;
+            ws->m = valid ? m : 0.0;
+            ws->M = valid ? M : 0.0;
+            if (a.mode & SS_SOLVE) {
+                if (!valid || gap <= a.tol) {
+                    ws->done = 1;
+                } else if (ws->iter >= a.max_iter) {
+                    ws->done = 2;
+                } else {
+                    for (int k = 0; k < half; ++k) {
+                        for (int side = 0; side < 2; ++side) {
+                            double key = side ? lok[k] : upk[k];
+                            int32_t t = side ? loi[k] : upi[k];
+                            if (key == -INFINITY) continue;
+                            bool dup = false;
+                            for (int c = 0; c < nB; ++c) dup |= (shB[c] == t);
+                            if (!dup) shB[nB++] = t;
+                        }
+                    }
+                    go = 1;
+                }
+            } else {
+                // selection only: publish B for inspection
+                for (int k = 0; k < half; ++k) {
+                    for (int side = 0; side < 2; ++side) {
+                        double key = side ? lok[k] : upk[k];
+                        int32_t t = side ? loi[k] : upi[k];
+                        if (key == -INFINITY) continue;
+                        bool dup = false;
+                        for (int c = 0; c < nB; ++c) dup |= (ws->B[c] == t);
+                        if (!dup) ws->B[nB++] = t;
+                    }
+                }
+                ws->nB = nB;
+            }
+        } else {
+            nB = ws->nB;
+            for (int c = 0; c < nB; ++c) shB[c] = ws->B[c];
+            gap = ws->gap;
+            go = (a.mode & SS_SOLVE) ? 1 : 0;
+        }
+        if (go) {
+            for (int c = 0; c < nB; ++c) {
+                int32_t s = (int32_t)sample_of(SVR, shB[c], n);
+                int j = 0;
+                while (j < nS && shS[j] != s) ++j;
+                if (j == nS) shS[nS++] = s;
+                shSlot[c] = j;
+            }
+        }
+        shGo = go;
+        shNB = nB;
+        shNS = nS;
+        shGap = gap;
+    }
+    __syncthreads();
+    if (!shGo) return;
+    const int nB = shNB, nS = shNS;
+
+    // copy the working-set rows for the next k_rows; norms
+    {
+        const int q4 = (int)(ldp >> 2);
+        for (int e = tid; e < nS * q4; e += kSelThreads) {
+            int slot = e / q4, c4 = e - slot * q4;
+            *reinterpret_cast<float4*>(a.xS + (int64_t)slot * ldp + 4 * c4) =
+                ld4(a.X + (int64_t)shS[slot] * ldp + 4 * c4);
+        }
+        if (tid < nS) shsS[tid] = a.sq[shS[tid]];
+    }
+    __syncthreads();
+
+    // K_SS on the matrix cores, same operand order as k_rows
+    if (wave < NBLK * NBLK) {
+        const int g = lane >> 4, nl = lane & 15;
+        const int bi = wave / NBLK, bj = wave - bi * NBLK;
+        const int sa = bi * 16 + nl, sb = bj * 16 + nl;
+        const bool va = sa < nS, vb = sb < nS;
+        const float* xa = a.X + (int64_t)(va ? shS[sa] : 0) * ldp;
+        const float* xb = a.X + (int64_t)(vb ? shS[sb] : 0) * ldp;
+        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int64_t c0 = 0; c0 < ldp; c0 += 16) {
+            const int64_t col = c0 + 4 * g;
+            const bool cv = col < ldp;
+            float4 av = (va && cv) ? ld4(xa + col) : zero4();
+            float4 bv = (vb && cv) ? ld4(xb + col) : zero4();
+            acc = mfma_chunk(acc, av, bv);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            int ia = bi * 16 + 4 * g + v, ib = bj * 16 + nl;
+            if (ia < nS && ib < nS)
+                KSS[ia][ib] = ia == ib ? 1.0f
+                                       : rbf_from_dot(shsS[ia], shsS[ib],
+                                                      acc[v], a.gexp);
+        }
+    }
+    __syncthreads();
+
+    if (wave != 0) return;
+
+    // subproblem: maximal-violating-pair steps restricted to B
+    const bool act = lane < nB;
+    const int32_t t = act ? shB[lane] : INT_MAX;
+    const int sl = act ? shSlot[lane] : 0;
+    const int64_t sm = act ? sample_of(SVR, t, n) : 0;
+    double al = act ? a.alpha[t] : 0.0;
+    const double a0 = al;
+    if ((a.mode & SS_SET_ALPHA) && act) al = ws->alphaB[lane];
+    double yv, rv;
+    if (SVR) {
+        yv = t < n ? 1.0 : -1.0;
+        rv = act ? (t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps)
+                 : 0.0;
+    } else {
+        yv = act ? ((a.st[t] & ST_YPOS) ? 1.0 : -1.0) : 1.0;
+        rv = yv;
+    }
+    double v = act ? rv - a.F[sm] : 0.0;
+    const double C = a.C;
+    const double itol = a.inner_tol_override >= 0.0
+                            ? a.inner_tol_override
+                            : fmax(a.inner_ratio * shGap, 0.5 * a.tol);
+    int steps = 0;
+    for (; steps < a.max_inner; ++steps) {
+        const bool up = act && ((yv > 0 && al < C) || (yv < 0 && al > 0));
+        const bool lo = act && ((yv > 0 && al > 0) || (yv < 0 && al < C));
+        double bu = up ? v : -INFINITY, bl = lo ? -v : -INFINITY;
+        int32_t iu = up ? t : INT_MAX, il = lo ? t : INT_MAX;
+        wave_best(bu, iu);
+        wave_best(bl, il);
+        if (bu == -INFINITY || bl == -INFINITY) break;
+        const double vi = bu, vj = -bl;
+        if (!(vi - vj > itol)) break;
+        const int Li = __ffsll((unsigned long long)__ballot(act && t == iu)) - 1;
+        const int Lj = __ffsll((unsigned long long)__ballot(act && t == il)) - 1;
+        const double ali = __shfl(al, Li), alj = __shfl(al, Lj);
+        const double yi = __shfl(yv, Li), yj = __shfl(yv, Lj);
+        const int si = __shfl(sl, Li), sj = __shfl(sl, Lj);
+        double a2 = (double)KSS[si][si] + (double)KSS[sj][sj] -
+                    2.0 * (double)KSS[si][sj];
+        if (a2 <= 0.0) a2 = kTau;
+        double s = (vi - vj) / a2;
+        const double Ui = yi > 0 ? C - ali : ali;
+        const double Lb = yj > 0 ? alj : C - alj;
+        bool ci = false, cj = false;
+        if (Ui <= s) {
+            s = Ui;
+            ci = true;
+        }
+        if (Lb <= s) {
+            s = Lb;
+            cj = true;
+            ci = (Ui == s);
+        }
+        if (lane == Li) {
+            al += yi * s;
+            if (ci) al = yi > 0 ? C : 0.0;
+        }
+        if (lane == Lj) {
+            al -= yj * s;
+            if (cj) al = yj > 0 ? 0.0 : C;
+        }
+        if (act) v -= s * ((double)KSS[sl][si] - (double)KSS[sl][sj]);
+    }
+
+    if (act) ws->alphaB[lane] = al;
+    if (!(a.mode & SS_NO_WRITE)) {
+        if (act) {
+            a.alpha[t] = al;
+            a.st[t] = state_bits(yv, al, C);
+        }
+        shDc[lane] = act ? yv * (al - a0) : 0.0;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (lane < nS) {
+            double c = 0.0;
+            for (int b = 0; b < nB; ++b)
+                if (shSlot[b] == lane) c += shDc[b];
+            ws->coef[lane] = c;
+            ws->S[lane] = shS[lane];
+            ws->sS[lane] = shsS[lane];
+        }
+        if (act) {
+            ws->B[lane] = t;
+            ws->slotB[lane] = sl;
+        }
+        if (lane == 0) {
+            ws->nB = nB;
+            ws->nS = nS;
+            if (!given) ws->iter += 1;
+            ws->rows += nS;
+        }
+    }
+    if (lane == 0) ws->steps = steps;
+}
+
+void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s)
+{
+    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
+        case 2: k_select<false, 1><<<1, kSelThreads, 0, s>>>(a); break;
+        case 3: k_select<true, 1><<<1, kSelThreads, 0, s>>>(a); break;
+        case 4: k_select<false, 2><<<1, kSelThreads, 0, s>>>(a); break;
+        case 5: k_select<true, 2><<<1, kSelThreads, 0, s>>>(a); break;
+        case 8: k_select<false, 4><<<1, kSelThreads, 0, s>>>(a); break;
+        case 9: k_select<true, 4><<<1, kSelThreads, 0, s>>>(a); break;
+        default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
+    }
+}
+
+// ---------------------------------------------------------------------------
+// coefficients, summary, compaction
+// ---------------------------------------------------------------------------
+
+// c_i = y_i a_i (C-SVC) or a_(i,+) - a_(i,-) (eps-SVR), written with a
+// stride so that several outputs can share one n x n_out matrix.
+__global__ void k_coef(int32_t type, const double* a, const uint8_t* st,
+                       int64_t n, double* c, int32_t stride, int32_t off)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    double v;
+    if (type == SVM_EPS_SVR) v = a[i] - a[n + i];
+    else v = (st[i] & ST_YPOS) ? a[i] : -a[i];
+    c[i * stride + off] = v;
+}
+
+void launch_coef(int32_t type, const double* a, const uint8_t* st, int64_t n,
+                 double* c, hipStream_t s)
+{
+    k_coef<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(type, a, st, n, c, 1,
+                                                       0);
+}
+
+void launch_coef_strided(int32_t type, const double* a, const uint8_t* st,
+                         int64_t n, double* c, int32_t stride, int32_t off,
+                         hipStream_t s)
+{
+    k_coef<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(type, a, st, n, c,
+                                                       stride, off);
+}
+
+// Bias and objective ingredients, one block, fixed reduction order.
+__global__ __launch_bounds__(1024) void k_summary(int32_t type,
+                                                  const double* a,
+                                                  const uint8_t* st,
+                                                  const double* F,
+                                                  const float* z, int64_t n,
+                                                  double C, double eps,
+                                                  Summary* out)
+{
+    __shared__ double s_v[1024], s_o[1024];
+    __shared__ int64_t s_f[1024], s_b[1024];
+    const int tid = threadIdx.x;
+    const int64_t N = type == SVM_EPS_SVR ? 2 * n : n;
+    double sv = 0.0, so = 0.0;
+    int64_t nf = 0, nbd = 0;
+    for (int64_t t = tid; t < N; t += 1024) {
+        const int64_t sm = t >= n ? t - n : t;
+        double yv, rv;
+        if (type == SVM_EPS_SVR) {
+            yv = t < n ? 1.0 : -1.0;
+            rv = t < n ? (double)z[sm] - eps : (double)z[sm] + eps;
+        } else {
+            yv = (st[t] & ST_YPOS) ? 1.0 : -1.0;
+            rv = yv;
+        }
+        const double at = a[t];
+        const double v = rv - F[sm];
+        if (at > 0.0 && at < C) {
+            sv += v;
+            ++nf;
+        }
+        if (at == C) ++nbd;
+        so += at * yv * (rv + v);
+    }
+    s_v[tid] = sv;
+    s_o[tid] = so;
+    s_f[tid] = nf;
+    s_b[tid] = nbd;
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+        if (tid < w) {
+            s_v[tid] += s_v[tid + w];
+            s_o[tid] += s_o[tid + w];
+            s_f[tid] += s_f[tid + w];
+            s_b[tid] += s_b[tid + w];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        out->sum_free_v = s_v[0];
+        out->obj2 = s_o[0];
+        out->n_free = s_f[0];
+        out->n_bounded = s_b[0];
+    }
+}
+
+void launch_summary(int32_t type, const double* a, const uint8_t* st,
+                    const double* F, const float* z, int64_t n, double C,
+                    double eps, Summary* out, hipStream_t s)
+{
+    k_summary<<<1, 1024, 0, s>>>(type, a, st, F, z, n, C, eps, out);
+}
+
+constexpr int kCompactThreads = 1024;
+
+int64_t compact_blocks(int64_t n)
+{
+    return (n + kCompactThreads - 1) / kCompactThreads;
+}
+
+__device__ __forceinline__ bool row_nonzero(const double* coef, int64_t i,
+                                            int32_t n_out)
+{
+    bool nz = false;
+    for (int o = 0; o < n_out; ++o) nz |= coef[i * n_out + o] != 0.0;
+    return nz;
+}
+
+__global__ __launch_bounds__(kCompactThreads) void k_compact_count(
+    const double* coef, int64_t n, int32_t n_out, int32_t* blk_cnt)
+{
+    __shared__ int32_t wc[kCompactThreads / 64];
+    const int64_t i = (int64_t)blockIdx.x * kCompactThreads + threadIdx.x;
+    const bool f = i < n && row_nonzero(coef, i, n_out);
+    const unsigned long long m = __ballot(f);
+    if ((threadIdx.x & 63) == 0) wc[threadIdx.x >> 6] = __popcll(m);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t c = 0;
+        for (int w = 0; w < kCompactThreads / 64; ++w) c += wc[w];
+        blk_cnt[blockIdx.x] = c;
+    }
+}
+
+__global__ void k_compact_scan(int32_t* blk_cnt, int64_t nblk,
+                               int64_t* total)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int64_t acc = 0;
+    for (int64_t b = 0; b < nblk; ++b) {
+        int32_t c = blk_cnt[b];
+        blk_cnt[b] = (int32_t)acc;
+        acc += c;
+    }
+    *total = acc;
+}
+
+__global__ __launch_bounds__(kCompactThreads) void k_compact_scatter(
+    const double* coef, int64_t n, int32_t n_out, const int32_t* blk_off,
+    int32_t* idx_out, double* coef_out)
+{
+    __shared__ int32_t wc[kCompactThreads / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * kCompactThreads + threadIdx.x;
+    const bool f = i < n && row_nonzero(coef, i, n_out);
+    const unsigned long long m = __ballot(f);
+    if (lane == 0) wc[wave] = __popcll(m);
+    __syncthreads();
+    int32_t base = blk_off[blockIdx.x];
+    for (int w = 0; w < wave; ++w) base += wc[w];
+    const unsigned long long below =
+        lane == 0 ? 0ull : (m & ((1ull << lane) - 1ull));
+    if (f) {
+        int32_t pos = base + __popcll(below);
+        idx_out[pos] = (int32_t)i;
+        for (int o = 0; o < n_out; ++o)
+            coef_out[(int64_t)pos * n_out + o] = coef[i * n_out + o];
+    }
+}
+
+void launch_compact(const double* coef, int64_t n, int32_t n_out,
+                    int32_t* blk_cnt, int32_t* idx_out, double* coef_out,
+                    int64_t* count_out, hipStream_t s)
+{
+    int64_t nblk = compact_blocks(n);
+    if (nblk == 0) return;
+    k_compact_count<<<(unsigned)nblk, kCompactThreads, 0, s>>>(coef, n, n_out,
+                                                               blk_cnt);
+    k_compact_scan<<<1, 64, 0, s>>>(blk_cnt, nblk, count_out);
+    k_compact_scatter<<<(unsigned)nblk, kCompactThreads, 0, s>>>(
+        coef, n, n_out, blk_cnt, idx_out, coef_out);
+}
+
+__global__ void k_gather_rows(const float* X, const float* sq, int64_t ldp,
+                              const int32_t* idx, int64_t k, float* out,
+                              float* sq_out)
+{
+    const int64_t q4 = ldp >> 2;
+    int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; e < k * q4; e += (int64_t)gridDim.x * blockDim.x) {
+        int64_t r = e / q4, c4 = e - r * q4;
+        int64_t src = idx[r];
+        *reinterpret_cast<float4*>(out + r * ldp + 4 * c4) =
+            ld4(X + src * ldp + 4 * c4);
+        if (c4 == 0) sq_out[r] = sq[src];
+    }
+}
+
+void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
+                        const int32_t* idx, int64_t k, float* out,
+                        float* sq_out, hipStream_t s)
+{
+    if (k <= 0) return;
+    int64_t blocks = (k * (ldp >> 2) + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    k_gather_rows<<<(unsigned)blocks, 256, 0, s>>>(X, sq, ldp, idx, k, out,
+                                                   sq_out);
+}
+
+__global__ void k_labels(const double* D, int64_t m, int32_t n_out,
+                         int32_t* labels)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= m) return;
+    if (n_out == 1) {
+        labels[i] = D[i] >= 0.0 ? 1 : -1;
+        return;
+    }
+    int32_t best = 0;
+    double bv = D[i * n_out];
+    for (int o = 1; o < n_out; ++o) {
+        double v = D[i * n_out + o];
+        if (v > bv) {
+            bv = v;
+            best = o;
+        }
+    }
+    labels[i] = best;
+}
+
+void launch_argmax_labels(const double* D, int64_t m, int32_t n_out,
+                          int32_t type, int32_t* labels, hipStream_t s)
+{
+    (void)type;
+    if (m <= 0) return;
+    k_labels<<<(unsigned)((m + 255) / 256), 256, 0, s>>>(D, m, n_out, labels);
+}
+
+}  // namespace msvm

@@ -1,0 +1,689 @@
+// Host side of the working-set dual solve: buffers, the iteration loop,
+// the final recompute of the responses, bias, objective and the model.
+#include "solver.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+namespace msvm {
+
+// ---------------------------------------------------------------------------
+// context and features
+// ---------------------------------------------------------------------------
+
+Context::Context(int dev, void* s) : device(dev)
+{
+    HIP_TRY(hipSetDevice(dev));
+    stream = (hipStream_t)s;  // NULL: the device's default stream
+}
+
+Context::~Context()
+{
+    if (own_stream && stream) {
+        (void)hipStreamSynchronize(stream);
+        (void)hipStreamDestroy(stream);
+    }
+}
+
+void Context::sync() { HIP_TRY(hipStreamSynchronize(stream)); }
+
+int64_t padded_ld(int64_t d) { return (d + 3) / 4 * 4; }
+
+void load_features(const svm_matrix* M, Features& f, Context& cx)
+{
+    f.n = M->n;
+    f.d = M->d;
+    f.ldp = padded_ld(M->d);
+    f.X.alloc((size_t)(f.n * f.ldp));
+    f.sq.alloc((size_t)f.n);
+    const hipMemcpyKind kind =
+        M->on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    if (f.n > 0) {
+        if (f.ldp == f.d && M->ld == f.d) {
+            HIP_TRY(hipMemcpyAsync(f.X.p, M->values,
+                                   (size_t)(f.n * f.d) * sizeof(float), kind,
+                                   cx.stream));
+        } else if (M->on_device) {
+            launch_pad_copy(M->values, M->ld, f.n, f.d, f.X.p, f.ldp,
+                            cx.stream);
+        } else {
+            HIP_TRY(hipMemsetAsync(f.X.p, 0, f.X.bytes(), cx.stream));
+            HIP_TRY(hipMemcpy2DAsync(f.X.p, (size_t)f.ldp * sizeof(float),
+                                     M->values, (size_t)M->ld * sizeof(float),
+                                     (size_t)f.d * sizeof(float),
+                                     (size_t)f.n, kind, cx.stream));
+        }
+    }
+    DevBuf<int32_t> bad(1);
+    HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
+    launch_norms(f.X.p, f.n, f.ldp, f.sq.p, bad.p, cx.stream);
+    int32_t hb = 0;
+    HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t),
+                           hipMemcpyDeviceToHost, cx.stream));
+    cx.sync();
+    if (hb)
+        throw Error{SVM_E_INVALID,
+                    "X holds a value that is not finite (or whose square "
+                    "overflows fp32)"};
+}
+
+SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
+{
+    SolveOptions o{};
+    o.type = p->type;
+    o.C = p->C;
+    o.eps = p->type == SVM_EPS_SVR ? p->epsilon : 0.0;
+    o.gamma = p->gamma > 0 ? p->gamma : 1.0 / (double)d;
+    o.tol = p->tol;
+    const int64_t N = p->type == SVM_EPS_SVR ? 2 * n : n;
+    o.max_iter = p->max_iter > 0 ? p->max_iter
+                                 : std::max<int64_t>(10000000, 100 * N);
+    o.q = p->working_set;
+    o.check_every = p->check_every > 0 ? p->check_every : 64;
+    o.inner_ratio = p->inner_ratio > 0 ? p->inner_ratio : 0.1;
+    o.max_inner = p->max_inner > 0 ? p->max_inner : 8 * p->working_set;
+    o.profile = p->profile != 0;
+    return o;
+}
+
+// ---------------------------------------------------------------------------
+// solver
+// ---------------------------------------------------------------------------
+
+Solver::Solver(Context& cx, const Features& f, const float* y_dev,
+               const SolveOptions& o)
+    : cx_(cx), f_(f), o_(o)
+{
+    n_ = f.n;
+    N_ = o.type == SVM_EPS_SVR ? 2 * n_ : n_;
+    gexp_ = (float)(o.gamma * 1.4426950408889634);
+    half_ = o.q / 2;
+    nblk_cols_ = o.q <= 16 ? 1 : (o.q <= 32 ? 2 : 4);
+    tiles_ = 1;
+    const int64_t cap = (int64_t)kSelThreads * kSelPerThread;
+    while (((n_ + 64LL * tiles_ - 1) / (64LL * tiles_)) * half_ > cap)
+        tiles_ *= 2;
+    nb_ = (int)((n_ + 64LL * tiles_ - 1) / (64LL * tiles_));
+    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, o.type == SVM_EPS_SVR) >
+        160 * 1024)
+        throw Error{SVM_E_UNSUPPORTED,
+                    "too many features for the dense row kernel's LDS tile"};
+
+    F_.alloc((size_t)n_);
+    alpha_.alloc((size_t)N_);
+    st_.alloc((size_t)N_);
+    y_.alloc((size_t)n_);
+    ws_.alloc(1);
+    xS_.alloc((size_t)kMaxQ * f.ldp);
+    ckey_.alloc((size_t)nb_ * 2 * half_);
+    cidx_.alloc((size_t)nb_ * 2 * half_);
+    sum_.alloc(1);
+    cvec_.alloc((size_t)n_);
+    cblk_.alloc((size_t)compact_blocks(n_));
+    sv_idx_.alloc((size_t)n_);
+    sv_coef_.alloc((size_t)n_);
+    sv_cnt_.alloc(1);
+
+    hipStream_t s = cx_.stream;
+    HIP_TRY(hipMemcpyAsync(y_.p, y_dev, (size_t)n_ * sizeof(float),
+                           hipMemcpyDeviceToDevice, s));
+    HIP_TRY(hipMemsetAsync(F_.p, 0, F_.bytes(), s));
+    HIP_TRY(hipMemsetAsync(alpha_.p, 0, alpha_.bytes(), s));
+    HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
+    HIP_TRY(hipMemsetAsync(xS_.p, 0, xS_.bytes(), s));
+    DevBuf<int32_t> bad(1);
+    HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), s));
+    launch_init_state(o.type, y_.p, n_, st_.p, bad.p, s);
+    int32_t hb = 0;
+    HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t), hipMemcpyDeviceToHost,
+                           s));
+    cx_.sync();
+    if (o.type == SVM_C_SVC) {
+        if (hb & 1) throw Error{SVM_E_INVALID, "labels must be +1 or -1"};
+        if ((hb & 6) != 6)
+            throw Error{SVM_E_INVALID, "both classes must be present"};
+    } else if (hb & 1) {
+        throw Error{SVM_E_INVALID, "targets must be finite"};
+    }
+}
+
+void Solver::launch_keys()
+{
+    RowArgs a{};
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.F = F_.p;
+    a.st = st_.p;
+    a.z = y_.p;
+    a.ws = ws_.p;
+    a.xS = xS_.p;
+    a.cand_key = ckey_.p;
+    a.cand_idx = cidx_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.eps = o_.eps;
+    a.gexp = gexp_;
+    a.half = half_;
+    a.tiles = tiles_;
+    a.mode = RU_CAND;
+    a.nS_override = 0;
+    launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
+}
+
+void Solver::launch_hot_rows()
+{
+    RowArgs a{};
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.F = F_.p;
+    a.st = st_.p;
+    a.z = y_.p;
+    a.ws = ws_.p;
+    a.xS = xS_.p;
+    a.cand_key = ckey_.p;
+    a.cand_idx = cidx_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.eps = o_.eps;
+    a.gexp = gexp_;
+    a.half = half_;
+    a.tiles = tiles_;
+    a.mode = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
+    a.nS_override = -1;
+    launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
+}
+
+void Solver::launch_solve(int32_t mode)
+{
+    SelArgs a{};
+    a.cand_key = ckey_.p;
+    a.cand_idx = cidx_.p;
+    a.nb = nb_;
+    a.half = half_;
+    a.ws = ws_.p;
+    a.alpha = alpha_.p;
+    a.st = st_.p;
+    a.F = F_.p;
+    a.z = y_.p;
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.xS = xS_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.C = o_.C;
+    a.eps = o_.eps;
+    a.tol = o_.tol;
+    a.gexp = gexp_;
+    a.inner_ratio = o_.inner_ratio;
+    a.inner_tol_override = -1.0;
+    a.max_inner = o_.max_inner;
+    a.max_iter = o_.max_iter;
+    a.mode = mode;
+    launch_select(a, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
+}
+
+void Solver::launch_select_only() { launch_solve(0); }
+
+void Solver::read_ws(WorkingSet& w)
+{
+    HIP_TRY(hipMemcpyAsync(&w, ws_.p, sizeof(WorkingSet),
+                           hipMemcpyDeviceToHost, cx_.stream));
+    cx_.sync();
+}
+
+// Queue chunks of `check_every` iterations, two chunks in flight, and poll
+// the done flag of the older chunk.  Iterations queued after convergence
+// return at their first instruction.
+bool Solver::run_loop(SolveResult& r)
+{
+    const int K = o_.check_every;
+    HostBuf<WorkingSet> hs(2);
+    hipEvent_t ev[2];
+    HIP_TRY(hipEventCreateWithFlags(&ev[0], hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&ev[1], hipEventDisableTiming));
+    std::vector<hipEvent_t> pe;
+    if (o_.profile) {
+        pe.resize((size_t)4 * K);
+        for (auto& e : pe) HIP_TRY(hipEventCreate(&e));
+    }
+    WorkingSet w0;
+    read_ws(w0);
+    int64_t last_iter = w0.iter;
+
+    auto enqueue = [&](int slot) {
+        for (int k = 0; k < K; ++k) {
+            launch_solve(SS_SOLVE | SS_CHECK_DONE);
+            if (o_.profile)
+                HIP_TRY(hipEventRecord(pe[(size_t)(slot * K + k) * 2],
+                                       cx_.stream));
+            launch_hot_rows();
+            if (o_.profile)
+                HIP_TRY(hipEventRecord(pe[(size_t)(slot * K + k) * 2 + 1],
+                                       cx_.stream));
+        }
+        HIP_TRY(hipMemcpyAsync(&hs.p[slot], ws_.p, sizeof(WorkingSet),
+                               hipMemcpyDeviceToHost, cx_.stream));
+        HIP_TRY(hipEventRecord(ev[slot], cx_.stream));
+    };
+
+    enqueue(0);
+    enqueue(1);
+    int cur = 0;
+    for (;;) {
+        HIP_TRY(hipEventSynchronize(ev[cur]));
+        const WorkingSet& w = hs.p[cur];
+        if (o_.profile) {
+            int64_t real = std::min<int64_t>(w.iter - last_iter, K);
+            for (int64_t k = 0; k < real; ++k) {
+                float ms = 0.f;
+                HIP_TRY(hipEventElapsedTime(
+                    &ms, pe[(size_t)(cur * K + k) * 2],
+                    pe[(size_t)(cur * K + k) * 2 + 1]));
+                row_ms_ += ms;
+                row_launches_ += 1;
+                row_rows_ += n_;
+            }
+        }
+        if (w.done) break;
+        if (w.iter == last_iter) {
+            cx_.sync();
+            for (auto& e : pe) (void)hipEventDestroy(e);
+            (void)hipEventDestroy(ev[0]);
+            (void)hipEventDestroy(ev[1]);
+            throw Error{SVM_E_INTERNAL, "solver state made no progress"};
+        }
+        last_iter = w.iter;
+        enqueue(cur);
+        cur ^= 1;
+    }
+    cx_.sync();
+    for (auto& e : pe) (void)hipEventDestroy(e);
+    (void)hipEventDestroy(ev[0]);
+    (void)hipEventDestroy(ev[1]);
+    WorkingSet w;
+    read_ws(w);
+    r.iters = w.iter;
+    r.gap = w.gap;
+    r.m = w.m;
+    r.M = w.M;
+    r.kernel_rows = w.rows;
+    r.status = w.done == 2 ? SVM_W_MAX_ITER : SVM_OK;
+    return w.done == 1;
+}
+
+void Solver::recompute_responses()
+{
+    hipStream_t s = cx_.stream;
+    launch_coef(o_.type, alpha_.p, st_.p, n_, cvec_.p, s);
+    launch_compact(cvec_.p, n_, 1, cblk_.p, sv_idx_.p, sv_coef_.p,
+                   sv_cnt_.p, s);
+    int64_t nsv = 0;
+    HIP_TRY(hipMemcpyAsync(&nsv, sv_cnt_.p, sizeof(int64_t),
+                           hipMemcpyDeviceToHost, s));
+    cx_.sync();
+    if (nsv == 0) {
+        HIP_TRY(hipMemsetAsync(F_.p, 0, F_.bytes(), s));
+        return;
+    }
+    if (sv_rows_.count < (size_t)(nsv * f_.ldp)) {
+        sv_rows_.alloc((size_t)(nsv * f_.ldp));
+        sv_sq_.alloc((size_t)nsv);
+    }
+    launch_gather_rows(f_.X.p, f_.sq.p, f_.ldp, sv_idx_.p, nsv, sv_rows_.p,
+                       sv_sq_.p, s);
+    PredictArgs a{};
+    a.Xt = f_.X.p;
+    a.sqt = f_.sq.p;
+    a.m = n_;
+    a.ldp = f_.ldp;
+    a.SV = sv_rows_.p;
+    a.sqsv = sv_sq_.p;
+    a.nsv = nsv;
+    a.coef = sv_coef_.p;
+    a.b = nullptr;
+    a.n_out = 1;
+    a.sv_train_idx = sv_idx_.p;
+    a.self_match = 1;
+    a.out = F_.p;
+    a.gexp = gexp_;
+    launch_predict(a, s);
+}
+
+SolveResult Solver::train()
+{
+    SolveResult r;
+    hipEvent_t t0, t1;
+    HIP_TRY(hipEventCreate(&t0));
+    HIP_TRY(hipEventCreate(&t1));
+    HIP_TRY(hipEventRecord(t0, cx_.stream));
+
+    launch_keys();
+    bool conv = run_loop(r);
+    // The incremental responses accumulate rounding over many updates:
+    // recompute them from alpha and re-test the gap before accepting.
+    for (int pass = 0; pass < 4 && conv; ++pass) {
+        recompute_responses();
+        launch_keys();
+        launch_select_only();
+        WorkingSet w;
+        read_ws(w);
+        r.gap = w.gap;
+        r.m = w.m;
+        r.M = w.M;
+        if (w.gap <= o_.tol) break;
+        launch_fill_i32(&ws_.p->done, 0, 1, cx_.stream);
+        conv = run_loop(r);
+        if (!conv) break;
+    }
+    if (!conv) recompute_responses();
+
+    launch_summary(o_.type, alpha_.p, st_.p, F_.p, y_.p, n_, o_.C, o_.eps,
+                   sum_.p, cx_.stream);
+    Summary sm;
+    HIP_TRY(hipMemcpyAsync(&sm, sum_.p, sizeof(Summary),
+                           hipMemcpyDeviceToHost, cx_.stream));
+    int64_t nsv = 0;
+    HIP_TRY(hipMemcpyAsync(&nsv, sv_cnt_.p, sizeof(int64_t),
+                           hipMemcpyDeviceToHost, cx_.stream));
+    HIP_TRY(hipEventRecord(t1, cx_.stream));
+    cx_.sync();
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, t0, t1));
+    (void)hipEventDestroy(t0);
+    (void)hipEventDestroy(t1);
+
+    r.n_free = sm.n_free;
+    r.n_bounded = sm.n_bounded;
+    r.b = sm.n_free > 0 ? sm.sum_free_v / (double)sm.n_free
+                        : 0.5 * (r.m + r.M);
+    r.obj = -0.5 * sm.obj2;
+    r.n_sv = nsv;
+    r.train_ms = ms;
+    r.row_ms = row_ms_;
+    r.row_launches = row_launches_;
+    r.row_rows = row_rows_;
+    WorkingSet w;
+    read_ws(w);
+    r.kernel_rows = w.rows;
+    r.iters = w.iter;
+    return r;
+}
+
+void Solver::coefficients(double* c, int32_t stride, int32_t off)
+{
+    launch_coef_strided(o_.type, alpha_.p, st_.p, n_, c, stride, off,
+                        cx_.stream);
+}
+
+void Solver::get_alpha(double* out)
+{
+    HIP_TRY(hipMemcpyAsync(out, alpha_.p, (size_t)N_ * sizeof(double),
+                           hipMemcpyDeviceToHost, cx_.stream));
+    cx_.sync();
+}
+
+// ---- test hooks ----
+
+void Solver::set_state(const double* alpha_h, const double* F_h)
+{
+    hipStream_t s = cx_.stream;
+    HIP_TRY(hipMemcpyAsync(alpha_.p, alpha_h, (size_t)N_ * sizeof(double),
+                           hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(F_.p, F_h, (size_t)n_ * sizeof(double),
+                           hipMemcpyHostToDevice, s));
+    launch_state_from_alpha(o_.type, y_.p, alpha_.p, n_, o_.C, st_.p, s);
+    HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
+    cx_.sync();
+}
+
+void Solver::get_state(double* alpha_h, double* F_h)
+{
+    if (alpha_h)
+        HIP_TRY(hipMemcpyAsync(alpha_h, alpha_.p, (size_t)N_ * sizeof(double),
+                               hipMemcpyDeviceToHost, cx_.stream));
+    if (F_h)
+        HIP_TRY(hipMemcpyAsync(F_h, F_.p, (size_t)n_ * sizeof(double),
+                               hipMemcpyDeviceToHost, cx_.stream));
+    cx_.sync();
+}
+
+void Solver::select(int32_t* B, int32_t* nB, double* m, double* M)
+{
+    launch_keys();
+    launch_select_only();
+    WorkingSet w;
+    read_ws(w);
+    *nB = w.nB;
+    for (int i = 0; i < w.nB; ++i) B[i] = w.B[i];
+    *m = w.m;
+    *M = w.M;
+}
+
+void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
+{
+    hipStream_t s = cx_.stream;
+    WorkingSet w;
+    read_ws(w);
+    w.nS = k;
+    for (int j = 0; j < k; ++j) {
+        w.S[j] = samples[j];
+        HIP_TRY(hipMemcpyAsync(&w.sS[j], f_.sq.p + samples[j], sizeof(float),
+                               hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(xS_.p + (size_t)j * f_.ldp,
+                               f_.X.p + (size_t)samples[j] * f_.ldp,
+                               (size_t)f_.ldp * sizeof(float),
+                               hipMemcpyDeviceToDevice, s));
+    }
+    cx_.sync();
+    HIP_TRY(hipMemcpyAsync(ws_.p, &w, sizeof(WorkingSet),
+                           hipMemcpyHostToDevice, s));
+    cx_.sync();
+    if (rows_out_.count < (size_t)(k * n_)) rows_out_.alloc((size_t)(k * n_));
+    RowArgs a{};
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.F = F_.p;
+    a.st = st_.p;
+    a.z = y_.p;
+    a.ws = ws_.p;
+    a.xS = xS_.p;
+    a.rows_out = rows_out_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.eps = o_.eps;
+    a.gexp = gexp_;
+    a.half = half_;
+    a.tiles = tiles_;
+    a.mode = RU_ROWS;
+    a.nS_override = k;
+    int nbc = k <= 16 ? 1 : (k <= 32 ? 2 : 4);
+    if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR) >
+        160 * 1024)
+        throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
+    launch_rows(a, nb_, nbc, o_.type == SVM_EPS_SVR, s);
+    HIP_TRY(hipMemcpyAsync(out_h, rows_out_.p,
+                           (size_t)(k * n_) * sizeof(float),
+                           hipMemcpyDeviceToHost, s));
+    cx_.sync();
+}
+
+void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
+                        int32_t max_inner, double* alpha_B, int32_t* steps)
+{
+    hipStream_t s = cx_.stream;
+    WorkingSet w;
+    read_ws(w);
+    w.nB = nB;
+    for (int i = 0; i < nB; ++i) w.B[i] = B[i];
+    w.done = 0;
+    HIP_TRY(hipMemcpyAsync(ws_.p, &w, sizeof(WorkingSet),
+                           hipMemcpyHostToDevice, s));
+    cx_.sync();
+    SelArgs a{};
+    a.ws = ws_.p;
+    a.alpha = alpha_.p;
+    a.st = st_.p;
+    a.F = F_.p;
+    a.z = y_.p;
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.xS = xS_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.C = o_.C;
+    a.eps = o_.eps;
+    a.tol = o_.tol;
+    a.gexp = gexp_;
+    a.inner_ratio = o_.inner_ratio;
+    a.inner_tol_override = inner_tol;
+    a.max_inner = max_inner;
+    a.max_iter = o_.max_iter;
+    a.half = half_;
+    a.mode = SS_GIVEN_B | SS_SOLVE | SS_NO_WRITE;
+    int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
+    launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
+    read_ws(w);
+    for (int i = 0; i < nB; ++i) alpha_B[i] = w.alphaB[i];
+    *steps = w.steps;
+}
+
+void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
+{
+    hipStream_t s = cx_.stream;
+    WorkingSet w;
+    read_ws(w);
+    w.nB = nB;
+    w.done = 0;
+    for (int i = 0; i < nB; ++i) {
+        w.B[i] = B[i];
+        w.alphaB[i] = alpha_B[i];
+    }
+    HIP_TRY(hipMemcpyAsync(ws_.p, &w, sizeof(WorkingSet),
+                           hipMemcpyHostToDevice, s));
+    cx_.sync();
+    SelArgs a{};
+    a.ws = ws_.p;
+    a.alpha = alpha_.p;
+    a.st = st_.p;
+    a.F = F_.p;
+    a.z = y_.p;
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.xS = xS_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.C = o_.C;
+    a.eps = o_.eps;
+    a.tol = o_.tol;
+    a.gexp = gexp_;
+    a.inner_ratio = o_.inner_ratio;
+    a.inner_tol_override = 0.0;
+    a.max_inner = 0;
+    a.max_iter = o_.max_iter;
+    a.half = half_;
+    a.mode = SS_GIVEN_B | SS_SOLVE | SS_SET_ALPHA;
+    int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
+    launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
+    RowArgs r{};
+    r.X = f_.X.p;
+    r.sq = f_.sq.p;
+    r.F = F_.p;
+    r.st = st_.p;
+    r.z = y_.p;
+    r.ws = ws_.p;
+    r.xS = xS_.p;
+    r.cand_key = ckey_.p;
+    r.cand_idx = cidx_.p;
+    r.n = n_;
+    r.ldp = f_.ldp;
+    r.eps = o_.eps;
+    r.gexp = gexp_;
+    r.half = half_;
+    r.tiles = tiles_;
+    r.mode = RU_UPDATE;
+    r.nS_override = -1;
+    if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR) >
+        160 * 1024)
+        throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
+    launch_rows(r, nb_, nbc, o_.type == SVM_EPS_SVR, s);
+    cx_.sync();
+}
+
+void Solver::iterate(int64_t k, int64_t* iters, double* gap)
+{
+    launch_keys();
+    for (int64_t i = 0; i < k; ++i) {
+        launch_solve(SS_SOLVE | SS_CHECK_DONE);
+        launch_hot_rows();
+    }
+    WorkingSet w;
+    read_ws(w);
+    *iters = w.iter;
+    *gap = w.gap;
+}
+
+// ---------------------------------------------------------------------------
+// model
+// ---------------------------------------------------------------------------
+
+void build_model(svm_model& m, Context& cx, const Features& f,
+                 const double* coef_dev, int32_t n_out)
+{
+    hipStream_t s = cx.stream;
+    const int64_t n = f.n;
+    DevBuf<int32_t> blk((size_t)compact_blocks(n)), idx((size_t)n);
+    DevBuf<double> cc((size_t)(n * n_out));
+    DevBuf<int64_t> cnt(1);
+    launch_compact(coef_dev, n, n_out, blk.p, idx.p, cc.p, cnt.p, s);
+    int64_t nsv = 0;
+    HIP_TRY(hipMemcpyAsync(&nsv, cnt.p, sizeof(int64_t),
+                           hipMemcpyDeviceToHost, s));
+    cx.sync();
+    m.n_sv = nsv;
+    m.SV.alloc((size_t)(nsv * f.ldp));
+    m.sqsv.alloc((size_t)nsv);
+    m.coef_dev.alloc((size_t)(nsv * n_out));
+    m.b_dev.alloc((size_t)n_out);
+    launch_gather_rows(f.X.p, f.sq.p, f.ldp, idx.p, nsv, m.SV.p, m.sqsv.p, s);
+    m.sv_idx.resize((size_t)nsv);
+    m.coef.resize((size_t)(nsv * n_out));
+    if (nsv > 0) {
+        HIP_TRY(hipMemcpyAsync(m.coef_dev.p, cc.p,
+                               (size_t)(nsv * n_out) * sizeof(double),
+                               hipMemcpyDeviceToDevice, s));
+        HIP_TRY(hipMemcpyAsync(m.sv_idx.data(), idx.p,
+                               (size_t)nsv * sizeof(int32_t),
+                               hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(m.coef.data(), cc.p,
+                               (size_t)(nsv * n_out) * sizeof(double),
+                               hipMemcpyDeviceToHost, s));
+    }
+    HIP_TRY(hipMemcpyAsync(m.b_dev.p, m.b.data(),
+                           (size_t)n_out * sizeof(double),
+                           hipMemcpyHostToDevice, s));
+    cx.sync();
+}
+
+void predict_device(const svm_model& mdl, Context& cx, const Features& t,
+                    double* out)
+{
+    PredictArgs a{};
+    a.Xt = t.X.p;
+    a.sqt = t.sq.p;
+    a.m = t.n;
+    a.ldp = t.ldp;
+    a.SV = mdl.SV.p;
+    a.sqsv = mdl.sqsv.p;
+    a.nsv = mdl.n_sv;
+    a.coef = mdl.coef_dev.p;
+    a.b = mdl.b_dev.p;
+    a.n_out = mdl.n_out;
+    a.sv_train_idx = nullptr;
+    a.self_match = 0;
+    a.out = out;
+    a.gexp = mdl.gexp;
+    launch_predict(a, cx.stream);
+}
+
+}  // namespace msvm

@@ -1,0 +1,191 @@
+// Host-side solver state of the MI355X kernel-SVM library.
+#pragma once
+
+#include <memory>
+
+#include "common.hpp"
+
+namespace msvm {
+
+// RAII device buffer.
+template <class T>
+struct DevBuf {
+    T* p = nullptr;
+    size_t count = 0;
+    DevBuf() = default;
+    explicit DevBuf(size_t n) { alloc(n); }
+    DevBuf(const DevBuf&) = delete;
+    DevBuf& operator=(const DevBuf&) = delete;
+    ~DevBuf() { release(); }
+    void alloc(size_t n)
+    {
+        release();
+        if (n == 0) n = 1;
+        HIP_TRY(hipMalloc((void**)&p, n * sizeof(T)));
+        count = n;
+    }
+    void release()
+    {
+        if (p) (void)hipFree(p);
+        p = nullptr;
+        count = 0;
+    }
+    size_t bytes() const { return count * sizeof(T); }
+};
+
+// Pinned host buffer.
+template <class T>
+struct HostBuf {
+    T* p = nullptr;
+    explicit HostBuf(size_t n)
+    {
+        HIP_TRY(hipHostMalloc((void**)&p, (n ? n : 1) * sizeof(T),
+                              hipHostMallocDefault));
+    }
+    HostBuf(const HostBuf&) = delete;
+    HostBuf& operator=(const HostBuf&) = delete;
+    ~HostBuf()
+    {
+        if (p) (void)hipHostFree(p);
+    }
+};
+
+// The device and stream of one call.
+struct Context {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+    Context(int dev, void* stream);
+    ~Context();
+    void sync();
+};
+
+// Dense feature store: X zero-padded to ldp columns, plus squared norms.
+struct Features {
+    int64_t n = 0, d = 0, ldp = 0;
+    DevBuf<float> X, sq;
+};
+
+// Uploads X (host or device) into the padded layout and computes norms.
+// Throws Error{SVM_E_INVALID} if a value is not finite.
+void load_features(const svm_matrix* M, Features& f, Context& cx);
+
+int64_t padded_ld(int64_t d);
+
+struct SolveOptions {
+    int32_t type;
+    double C, eps, gamma, tol;
+    int64_t max_iter;
+    int32_t q;
+    int32_t check_every;
+    double inner_ratio;
+    int32_t max_inner;
+    bool profile;
+};
+
+SolveOptions make_options(const svm_params* p, int64_t n, int64_t d);
+
+// Result of one binary (or SVR) solve.
+struct SolveResult {
+    svm_status status = SVM_OK;
+    int64_t iters = 0;
+    double gap = 0, m = 0, M = 0, b = 0, obj = 0;
+    int64_t n_free = 0, n_bounded = 0, n_sv = 0;
+    int64_t kernel_rows = 0;
+    double train_ms = 0;
+    double row_ms = 0;
+    int64_t row_launches = 0, row_rows = 0;
+};
+
+class Solver {
+public:
+    // y: device pointer to n labels (+-1) or targets.  Features are shared.
+    Solver(Context& cx, const Features& f, const float* y_dev,
+           const SolveOptions& o);
+
+    // Full training run: initial keys, iterations, final recompute, bias.
+    SolveResult train();
+
+    // Expansion coefficients c_i over all n samples, written to
+    // c[i * stride + off] (device).
+    void coefficients(double* c, int32_t stride, int32_t off);
+
+    // Host copy of alpha (N values).
+    void get_alpha(double* out);
+
+    // ---- test hooks ----
+    void set_state(const double* alpha_h, const double* F_h);
+    void get_state(double* alpha_h, double* F_h);
+    void select(int32_t* B, int32_t* nB, double* m, double* M);
+    void rows(const int32_t* samples, int32_t k, float* out_h);
+    void subproblem(const int32_t* B, int32_t nB, double inner_tol,
+                    int32_t max_inner, double* alpha_B, int32_t* steps);
+    void apply(const int32_t* B, int32_t nB, const double* alpha_B);
+    void iterate(int64_t k, int64_t* iters, double* gap);
+
+    int64_t N() const { return N_; }
+
+private:
+    void launch_keys();
+    void launch_hot_rows();
+    void launch_solve(int32_t mode);
+    void launch_select_only();
+    bool run_loop(SolveResult& r);
+    void recompute_responses();
+    void read_ws(WorkingSet& w);
+
+    Context& cx_;
+    const Features& f_;
+    SolveOptions o_;
+    int64_t n_, N_;
+    float gexp_;
+    int half_, nblk_cols_, tiles_, nb_;
+    DevBuf<double> F_, alpha_;
+    DevBuf<uint8_t> st_;
+    DevBuf<float> y_;
+    DevBuf<WorkingSet> ws_;
+    DevBuf<float> xS_;
+    DevBuf<double> ckey_;
+    DevBuf<int32_t> cidx_;
+    DevBuf<Summary> sum_;
+    DevBuf<double> cvec_;
+    DevBuf<int32_t> cblk_, sv_idx_;
+    DevBuf<double> sv_coef_;
+    DevBuf<int64_t> sv_cnt_;
+    DevBuf<float> sv_rows_, sv_sq_;
+    DevBuf<float> rows_out_;
+    double row_ms_ = 0;
+    int64_t row_launches_ = 0, row_rows_ = 0;
+};
+
+}  // namespace msvm
+
+// The opaque model of the C ABI.
+struct svm_model {
+    int32_t type = 0;
+    int32_t n_out = 1;
+    int64_t n_train = 0, d = 0, ldp = 0;
+    double gamma = 0;
+    float gexp = 0;
+    int device = 0;
+    int64_t n_sv = 0;
+    msvm::DevBuf<float> SV, sqsv;
+    msvm::DevBuf<double> coef_dev, b_dev;
+    std::vector<int32_t> sv_idx;             // union, increasing
+    std::vector<double> coef;                // n_sv x n_out
+    std::vector<double> b;                   // n_out
+    std::vector<std::vector<double>> alpha;  // per output, N values
+    std::vector<svm_model_info> info;        // per output
+};
+
+namespace msvm {
+
+// Builds the model arrays from the n x n_out coefficient matrix (device).
+void build_model(svm_model& m, Context& cx, const Features& f,
+                 const double* coef_dev, int32_t n_out);
+
+// Decision values for X (m x n_out) into `out` (device).
+void predict_device(const svm_model& mdl, Context& cx, const Features& t,
+                    double* out);
+
+}  // namespace msvm

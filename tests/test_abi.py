@@ -1,0 +1,154 @@
+"""C ABI: the library loads here (no GPU), exports every declared symbol,
+its ctypes mirror matches the C layout, and argument validation reports
+errors before any device call; with valid arguments and no GPU it returns
+SVM_E_DEVICE cleanly."""
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_1706_05544_amd import native as nv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mi355svm.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(svm_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = nv.load()
+    names = _declared()
+    assert len(names) >= 15
+    assert set(names) == set(nv.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", nv.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (svm_\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(lib, n)
+
+
+def test_struct_layout_matches_header(tmp_path):
+    prog = tmp_path / "layout.c"
+    prog.write_text(r'''
+#include <stdio.h>
+#include <stddef.h>
+#include "mi355svm.h"
+int main(void) {
+  printf("%zu %zu %zu\n", sizeof(svm_matrix), sizeof(svm_params),
+         sizeof(svm_model_info));
+  printf("%zu %zu %zu %zu\n", offsetof(svm_params, stream),
+         offsetof(svm_params, profile), offsetof(svm_model_info, train_ms),
+         offsetof(svm_matrix, nnz));
+  return 0;
+}
+''')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.dirname(HEADER),
+                    str(prog), "-o", str(exe)], check=True)
+    a, b = subprocess.run([str(exe)], capture_output=True, text=True,
+                          check=True).stdout.split("\n")[:2]
+    import ctypes as ct
+    assert [int(x) for x in a.split()] == [
+        ct.sizeof(nv.svm_matrix), ct.sizeof(nv.svm_params),
+        ct.sizeof(nv.svm_model_info)]
+    assert [int(x) for x in b.split()] == [
+        nv.svm_params.stream.offset, nv.svm_params.profile.offset,
+        nv.svm_model_info.train_ms.offset, nv.svm_matrix.nnz.offset]
+
+
+def test_params_default():
+    p = nv.svm_params_default()
+    assert p.type == nv.SVM_C_SVC and p.kernel == nv.SVM_KERNEL_RBF
+    assert p.C == 1.0 and p.epsilon == 0.1 and p.gamma == 0.0
+    assert p.tol == 1e-3 and p.working_set == 16 and p.device == 0
+
+
+def _x(n=8, d=3):
+    return np.random.default_rng(0).standard_normal((n, d)).astype(np.float32)
+
+
+def _y(n=8):
+    return np.where(np.arange(n) % 2 == 0, 1.0, -1.0).astype(np.float32)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(C=0.0), nv.SVM_E_INVALID),
+    (dict(C=float("nan")), nv.SVM_E_INVALID),
+    (dict(tol=0.0), nv.SVM_E_INVALID),
+    (dict(gamma=-1.0), nv.SVM_E_INVALID),
+    (dict(epsilon=-0.1), nv.SVM_E_INVALID),
+    (dict(working_set=3), nv.SVM_E_INVALID),
+    (dict(working_set=66), nv.SVM_E_INVALID),
+    (dict(working_set=0), nv.SVM_E_INVALID),
+    (dict(type=7), nv.SVM_E_INVALID),
+    (dict(kernel=nv.SVM_KERNEL_POLY), nv.SVM_E_UNSUPPORTED),
+    (dict(kernel=9), nv.SVM_E_INVALID),
+    (dict(inner_ratio=1.5), nv.SVM_E_INVALID),
+])
+def test_invalid_params(kw, code):
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(), _y(), **kw)
+    assert e.value.status == code
+    assert nv.svm_last_error()
+
+
+def test_invalid_labels_and_shapes():
+    y = _y()
+    y[3] = 0.5
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(), y)
+    assert e.value.status == nv.SVM_E_INVALID and "+1 or -1" in str(e.value)
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(), np.ones(8, np.float32))
+    assert "both classes" in str(e.value)
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(1, 3), np.ones(1, np.float32))
+    assert e.value.status == nv.SVM_E_INVALID
+    z = _y()
+    z[0] = np.inf
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(), z, type=nv.SVM_EPS_SVR)
+    assert "finite" in str(e.value)
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train_ovr(_x(), np.array([0, 1, 2, 0, 1, 2, 0, 5]), 3)
+    assert e.value.status == nv.SVM_E_INVALID
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train_ovr(_x(), np.zeros(8, np.int32), 3)
+    assert "every class" in str(e.value)
+
+
+def test_null_arguments_are_rejected():
+    lib = nv.load()
+    import ctypes as ct
+    out = ct.c_void_p()
+    p = nv.svm_params_default()
+    assert lib.svm_train(None, None, ct.byref(p), ct.byref(out)) == \
+        nv.SVM_E_INVALID
+    M = nv._Mat(_x())
+    assert lib.svm_train(ct.byref(M.s), None, ct.byref(p), ct.byref(out)) \
+        == nv.SVM_E_INVALID
+    assert lib.svm_predict(None, ct.byref(M.s), None) == nv.SVM_E_INVALID
+    assert lib.svm_model_get_info(None, 0, None) == nv.SVM_E_INVALID
+    lib.svm_model_free(None)
+
+
+def test_csr_is_reported_unsupported():
+    import scipy.sparse as sp
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(sp.csr_matrix(_x()), _y())
+    assert e.value.status == nv.SVM_E_UNSUPPORTED
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU is present")
+def test_no_device_is_a_clean_error():
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(), _y())
+    assert e.value.status == nv.SVM_E_DEVICE
+    assert "device" in nv.svm_last_error()

@@ -1,4 +1,4 @@
-"""Pins for the oracle's working-set selection and subproblem (R3, R4).
+"""Pins for the oracle's working-set selection and subproblem (Section 3).
 
 The selection is checked against a direct sort of keys computed here from
 scikit-learn's kernel; the subproblem against (a) one maximal-violating-pair
