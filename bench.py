@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark of the kernel-SVM hot path on one MI355X.
+
+One step = one complete pass of the method on the C3 workload (binary
+C-SVC, RBF, dense n = 100000, d = 128, x = y*0.2*1 + N(0, I), C = 1,
+gamma = 1/128, tol = 1e-3, working set q = 16): feature store and norms,
+the working-set iterations to the KKT tolerance, the final recompute of the
+responses, bias and model extraction, then the decision function on the
+20000 test points.  Inputs are resident in HBM (torch tensors) before the
+timed region starts.
+
+Prints one JSON line.  `value` is kernel rows per second: rows K(x_s, X)
+(length n) evaluated by the working-set iterations, over the wall time of
+the timed steps.  `roofline` is for the row/update kernel (k_rows), timed
+with HIP events on the stream it runs on; `cpu_baseline` is the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("train time to KKT tol 1e-3; kernel rows/s and % of HBM/MFMA peak")
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg: str) -> None:
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def row_bytes_per_launch(n: int, d: int, svr: bool) -> int:
+    """Algorithmic HBM bytes of one k_rows launch (dense layout): per row the
+    features (4d), the squared norm (4), F read and written (16), one state
+    byte per variable and, for eps-SVR, the fp32 target (4)."""
+    per = 4 * d + 4 + 16 + (2 + 4 if svr else 1)
+    return n * per
+
+
+def cpu_baseline(w, target_s: float) -> dict:
+    """The oracle (untuned) on a bounded sample: maximal-violating-pair SMO
+    steps from alpha = 0 on the full training set; 2 kernel rows per step."""
+    import numpy as np
+
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    if threads <= 0:
+        threads = len(os.sched_getaffinity(0))
+    p = oracle.Params(w.type, C=w.C, eps=w.eps, gamma=w.gamma, tol=w.tol,
+                      threads=threads)
+    N = oracle.num_vars(w.type, w.n)
+    X = oracle.Matrix(w.X)
+    a0 = np.zeros(N)
+    F0 = np.zeros(w.n)
+    t0 = time.perf_counter()
+    r = oracle.solve(X, w.y, p, a0, F0, max_steps=10)
+    dt = time.perf_counter() - t0
+    steps = max(10, int(10 * target_s / max(dt, 1e-6)))
+    log("cpu baseline: %d oracle steps (calibration %.3f s / 10 steps)"
+        % (steps, dt))
+    t0 = time.perf_counter()
+    r = oracle.solve(X, w.y, p, a0, F0, max_steps=steps)
+    dt = time.perf_counter() - t0
+    rows = 2 * r.iters
+    return {"value": rows / dt, "unit": "kernel rows/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d maximal-violating-pair SMO steps from alpha=0 on the "
+                      "full %s training set (%d x %d), 2 kernel rows of "
+                      "length n per step, fp64, %.1f s" % (
+                          r.iters, w.name, w.n, w.d, dt)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="C3")
+    ap.add_argument("--working-set", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only; --gpus %d is not "
+              "supported (the multi-GPU design is described in DESIGN.md)"
+              % args.gpus, file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_1706_05544_amd import native as nv
+    from paper_1706_05544_amd import workloads
+
+    nv.load()
+    w = workloads.make(args.workload)
+    if w.type != workloads.C_SVC and w.type != workloads.EPS_SVR:
+        raise SystemExit("unsupported workload")
+    log("workload %s: n=%d d=%d n_test=%d" % (w.name, w.n, w.d,
+                                             w.Xt.shape[0]))
+    dev = torch.device("cuda:0")
+    X = torch.from_numpy(w.X).to(dev)
+    y = torch.from_numpy(w.y).to(dev)
+    Xt = torch.from_numpy(w.Xt).to(dev)
+    torch.cuda.synchronize()
+    kw = dict(type=w.type, C=w.C, epsilon=w.eps, gamma=w.gamma, tol=w.tol,
+              working_set=args.working_set)
+
+    def step(profile: int):
+        m = nv.svm_train(X, y, profile=profile, **kw)
+        t1 = time.perf_counter()
+        D = nv.svm_predict(m, Xt)
+        return m, D, t1
+
+    for i in range(args.warmup):
+        m, _, _ = step(0)
+        log("warmup %d: iters=%d" % (i, m.info()["iters"]))
+
+    infos = []
+    pred_s = 0.0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ts = time.perf_counter()
+        m, D, t1 = step(1)
+        torch.cuda.synchronize()
+        te = time.perf_counter()
+        info = m.info()
+        infos.append(info)
+        pred_s += te - t1
+        log("step %d: %.1f ms (train %.1f ms device, iters %d, rows %d)"
+            % (i, 1e3 * (te - ts), info["train_ms"], info["iters"],
+               info["kernel_rows"]))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    rows = sum(i["kernel_rows"] for i in infos)
+    launches = sum(i["row_kernel_launches"] for i in infos)
+    row_ms = sum(i["row_kernel_ms"] for i in infos)
+    avg_ms = row_ms / max(launches, 1)
+    bytes_launch = row_bytes_per_launch(w.n, w.d, w.type == workloads.EPS_SVR)
+    achieved = bytes_launch / (avg_ms * 1e-3) / 1e9 if launches else 0.0
+
+    last = infos[-1]
+    Dn = D.cpu().numpy()
+    if w.type == workloads.C_SVC:
+        acc = float(np.mean(np.where(Dn >= 0, 1.0, -1.0) == w.yt))
+        quality = {"test_accuracy": acc}
+    else:
+        quality = {"test_mse": float(np.mean((Dn - w.yt) ** 2))}
+
+    out = {
+        "metric": METRIC,
+        "value": rows / wall,
+        "unit": "kernel rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * wall / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: %s RBF, dense n=%d d=%d, C=%g, gamma=%g, "
+                        "tol=%g, q=%d; predict %d points"
+                        % (w.name, "C-SVC" if w.type == 0 else "eps-SVR",
+                           w.n, w.d, w.C, w.gamma, w.tol, args.working_set,
+                           w.Xt.shape[0]),
+            "n": w.n, "d": w.d, "n_test": int(w.Xt.shape[0]),
+            "working_set": args.working_set,
+        },
+        "train_ms_device": sum(i["train_ms"] for i in infos) / len(infos),
+        "predict_ms_wall": 1e3 * pred_s / len(infos),
+        "iters": last["iters"],
+        "n_sv": last["n_sv_output"],
+        "dual_obj": last["dual_obj"],
+        "gap": last["gap"],
+        **quality,
+        "roofline": {
+            "kernel": "k_rows (kernel rows + gradient update + candidates)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "avg_launch_us": 1e3 * avg_ms,
+            "bytes_per_launch": bytes_launch,
+            "launches_timed": launches,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -121,7 +121,16 @@ void fill_info(svm_model_info& in, const svm_model& m,
     in.row_kernel_rows = r.row_rows;
 }
 
-#define GUARD_BEGIN try {
+// Leaves HIP's per-thread last-error slot clean on every exit, so that an
+// error the library handled (or ignored while freeing) is not reported later
+// by a caller's own error check.
+struct ClearHipError {
+    ~ClearHipError() { (void)hipGetLastError(); }
+};
+
+#define GUARD_BEGIN \
+    ClearHipError clear_hip_error_on_exit_; \
+    try {
 #define GUARD_END                                                      \
     }                                                                  \
     catch (const msvm::Error& e) { return fail(e.status, e.msg); }     \

@@ -410,12 +410,17 @@ template <bool SVR, int NBLK>
 static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s)
 {
     size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipFuncSetAttribute((const void*)k_rows<SVR, NBLK>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize,
-                            160 * 1024);
-        attr_set = true;
+    static size_t lds_allowed = 64 * 1024;
+    if (lds > lds_allowed) {
+        hipError_t e = hipFuncSetAttribute(
+            (const void*)k_rows<SVR, NBLK>,
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            throw Error{SVM_E_UNSUPPORTED,
+                        "row tile needs more LDS than the device allows"};
+        }
+        lds_allowed = lds;
     }
     k_rows<SVR, NBLK><<<nblocks, kRowThreads, lds, s>>>(a);
 }
