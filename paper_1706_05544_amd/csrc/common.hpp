@@ -25,6 +25,7 @@ constexpr int kMaxHalf = kMaxQ / 2;
 constexpr int kRowThreads = 256;   // row/update kernel: 4 waves
 constexpr int kSelThreads = 1024;  // select/solve kernel: one block
 constexpr int kSelPerThread = 8;   // candidates per side held per thread
+constexpr int kBlockTop = 2;       // candidates per side kept per row block
 constexpr double kTau = 1e-12;     // curvature floor of a degenerate pair
 
 // state byte of a dual variable
@@ -50,6 +51,10 @@ struct WorkingSet {
     double alphaB[kMaxQ]; // new alpha_B (written by the solve)
     int32_t steps;        // inner steps of the last subproblem
     int32_t pad1;
+    int64_t inner_total;  // inner steps summed over iterations
+    int64_t rescans;      // iterations that rescanned exhausted blocks
+    int64_t slow_selects; // iterations that fell back to a full scan
+    int64_t prof[8];      // select/solve phase times (wall-clock ticks)
 };
 
 // Final reductions of a state (bias and objective).
@@ -117,6 +122,7 @@ struct SelArgs {
     int32_t max_inner;
     int64_t max_iter;
     int32_t mode;
+    int32_t tiles;        // tiles per wave of k_rows (rows per block / 64)
 };
 
 struct PredictArgs {
@@ -149,7 +155,8 @@ void launch_check_labels(const int32_t* labels, int64_t n, int32_t ncls,
 void launch_check_finite(const float* v, int64_t n, int32_t* bad_flag,
                          hipStream_t s);
 void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
-                 hipStream_t s);
+                 hipStream_t s, hipEvent_t e0 = nullptr,
+                 hipEvent_t e1 = nullptr);
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
 void launch_state_from_alpha(int32_t type, const float* y, const double* a,

@@ -72,6 +72,77 @@ __device__ __forceinline__ void wave_best(double& k, int32_t& i)
     }
 }
 
+// ---- fast cross-lane reductions (DPP row rotates + readlane) ----
+
+constexpr int kDppRor1 = 0x121, kDppRor2 = 0x122, kDppRor4 = 0x124,
+              kDppRor8 = 0x128;
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v)
+{
+    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    int lo = dpp_i32<CTRL>(__double2loint(v));
+    int hi = dpp_i32<CTRL>(__double2hiint(v));
+    return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ double rl_f64(double v, int lane)
+{
+    int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
+    int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
+    return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ int rl_i32(int v, int lane)
+{
+    return __builtin_amdgcn_readlane(v, lane);
+}
+
+// every lane of each 16-lane row receives the row maximum / minimum
+__device__ __forceinline__ double row_max_f64(double v)
+{
+    v = fmax(v, dpp_f64<kDppRor8>(v));
+    v = fmax(v, dpp_f64<kDppRor4>(v));
+    v = fmax(v, dpp_f64<kDppRor2>(v));
+    v = fmax(v, dpp_f64<kDppRor1>(v));
+    return v;
+}
+
+__device__ __forceinline__ int row_min_i32(int v)
+{
+    v = min(v, dpp_i32<kDppRor8>(v));
+    v = min(v, dpp_i32<kDppRor4>(v));
+    v = min(v, dpp_i32<kDppRor2>(v));
+    v = min(v, dpp_i32<kDppRor1>(v));
+    return v;
+}
+
+// Best (key, index) of a 16-lane row, in the order of better(); every lane
+// of the row receives its row's result.
+__device__ __forceinline__ void row_best(double& k, int32_t& i)
+{
+    const double M = row_max_f64(k);
+    i = row_min_i32(k == M ? i : INT_MAX);
+    k = M;
+}
+
+// Best (key, index) of the wave; the result is wave-uniform.
+__device__ __forceinline__ void wave_best_fast(double& k, int32_t& i)
+{
+    double M = row_max_f64(k);
+    M = fmax(fmax(rl_f64(M, 0), rl_f64(M, 16)),
+             fmax(rl_f64(M, 32), rl_f64(M, 48)));
+    int c = row_min_i32(k == M ? i : INT_MAX);
+    c = min(min(rl_i32(c, 0), rl_i32(c, 16)), min(rl_i32(c, 32), rl_i32(c, 48)));
+    k = M;
+    i = c;
+}
+
 __device__ __forceinline__ float4 ld4(const float* p)
 {
     return *reinterpret_cast<const float4*>(p);

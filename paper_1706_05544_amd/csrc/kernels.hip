@@ -18,6 +18,8 @@
 //             F_i += sum_s dc_s K(x_i, x_s) in fp64, the keys v of the
 //             variables of the tile and the per-block top-q/2 candidates of
 //             each side for the next k_select.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "device.hpp"
 
@@ -196,73 +198,6 @@ __device__ __forceinline__ int32_t local_var(int e, int64_t R, int64_t rblk,
     return (int32_t)(e < R ? rblk + e : n + rblk + (e - R));
 }
 
-// Block-level top-`half` of both sides from keys staged in LDS, in the order
-// "largest score first, lowest variable index on ties"; `half` rounds, each
-// one a block-wide best over the entries after the previous winner.
-template <int NT>
-__device__ void block_topk(const double* ku, const double* kl, int count,
-                           int64_t R, int64_t rblk, int64_t n, int half,
-                           double* out_key, int32_t* out_idx)
-{
-    constexpr int NW = NT / 64;
-    __shared__ double rk[2][2][NW];
-    __shared__ int32_t ri[2][2][NW];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    double pk0 = INFINITY, pk1 = INFINITY;
-    int32_t pi0 = -1, pi1 = -1;
-    for (int k = 0; k < half; ++k) {
-        double bk0 = -INFINITY, bk1 = -INFINITY;
-        int32_t bi0 = INT_MAX, bi1 = INT_MAX;
-        for (int e = tid; e < count; e += NT) {
-            int32_t t = local_var(e, R, rblk, n);
-            double u = ku[e], l = kl[e];
-            if (after(u, t, pk0, pi0) && better(u, t, bk0, bi0)) {
-                bk0 = u;
-                bi0 = t;
-            }
-            if (after(l, t, pk1, pi1) && better(l, t, bk1, bi1)) {
-                bk1 = l;
-                bi1 = t;
-            }
-        }
-        wave_best(bk0, bi0);
-        wave_best(bk1, bi1);
-        const int p = k & 1;
-        if (lane == 0) {
-            rk[p][0][wave] = bk0;
-            ri[p][0][wave] = bi0;
-            rk[p][1][wave] = bk1;
-            ri[p][1][wave] = bi1;
-        }
-        __syncthreads();
-        bk0 = rk[p][0][0];
-        bi0 = ri[p][0][0];
-        bk1 = rk[p][1][0];
-        bi1 = ri[p][1][0];
-#pragma unroll
-        for (int w = 1; w < NW; ++w) {
-            if (better(rk[p][0][w], ri[p][0][w], bk0, bi0)) {
-                bk0 = rk[p][0][w];
-                bi0 = ri[p][0][w];
-            }
-            if (better(rk[p][1][w], ri[p][1][w], bk1, bi1)) {
-                bk1 = rk[p][1][w];
-                bi1 = ri[p][1][w];
-            }
-        }
-        pk0 = bk0;
-        pi0 = bi0;
-        pk1 = bk1;
-        pi1 = bi1;
-        if (tid == 0) {
-            out_key[k] = bk0;
-            out_idx[k] = bi0;
-            out_key[half + k] = bk1;
-            out_idx[half + k] = bi1;
-        }
-    }
-}
-
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
 {
     size_t xs = (size_t)nblk_cols * 16 * (size_t)(ldp + 4) * sizeof(float);
@@ -274,6 +209,8 @@ template <bool SVR, int NBLK>
 __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ double wk[2][kRowThreads / 64][kBlockTop];
+    __shared__ int32_t wi[2][kRowThreads / 64][kBlockTop];
     const WorkingSet* ws = a.ws;
     if ((a.mode & RU_CHECK_DONE) && ws->done) return;
 
@@ -401,13 +338,87 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 
     if (!(a.mode & RU_CAND)) return;
     __syncthreads();
-    block_topk<kRowThreads>(kup, klo, (int)(NV * R), R, rblk, n, a.half,
-                            a.cand_key + (size_t)blockIdx.x * 2 * a.half,
-                            a.cand_idx + (size_t)blockIdx.x * 2 * a.half);
+
+    // Per-wave best kBlockTop of each side over the wave's own rows (no
+    // block barrier), then wave 0 merges the four lists.  Only the top
+    // kBlockTop per block are kept: the global top q/2 lie in the blocks
+    // whose lists they exhaust, which k_select then rescans.
+    {
+        const int E = 16 * T;
+        const int wbase = wave * E;
+        double pk0 = INFINITY, pk1 = INFINITY;
+        int32_t pi0 = -1, pi1 = -1;
+        for (int k = 0; k < kBlockTop; ++k) {
+            double bk0 = -INFINITY, bk1 = -INFINITY;
+            int32_t bi0 = INT_MAX, bi1 = INT_MAX;
+            for (int j = lane; j < NV * E; j += 64) {
+                const int loc = j < E ? wbase + j : (int)R + wbase + (j - E);
+                const int32_t t = local_var(loc, R, rblk, n);
+                const double u = kup[loc], l = klo[loc];
+                if (after(u, t, pk0, pi0) && better(u, t, bk0, bi0)) {
+                    bk0 = u;
+                    bi0 = t;
+                }
+                if (after(l, t, pk1, pi1) && better(l, t, bk1, bi1)) {
+                    bk1 = l;
+                    bi1 = t;
+                }
+            }
+            wave_best_fast(bk0, bi0);
+            wave_best_fast(bk1, bi1);
+            pk0 = bk0;
+            pi0 = bi0;
+            pk1 = bk1;
+            pi1 = bi1;
+            if (lane == 0) {
+                wk[0][wave][k] = bk0;
+                wi[0][wave][k] = bi0;
+                wk[1][wave][k] = bk1;
+                wi[1][wave][k] = bi1;
+            }
+        }
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    {
+        constexpr int NW = kRowThreads / 64;
+        double e0 = -INFINITY, e1 = -INFINITY;
+        int32_t j0 = INT_MAX, j1 = INT_MAX;
+        if (lane < NW * kBlockTop) {
+            const int w = lane / kBlockTop, k = lane - w * kBlockTop;
+            e0 = wk[0][w][k];
+            j0 = wi[0][w][k];
+            e1 = wk[1][w][k];
+            j1 = wi[1][w][k];
+        }
+        double* ok = a.cand_key + (size_t)blockIdx.x * 2 * kBlockTop;
+        int32_t* oi = a.cand_idx + (size_t)blockIdx.x * 2 * kBlockTop;
+        double pk0 = INFINITY, pk1 = INFINITY;
+        int32_t pi0 = -1, pi1 = -1;
+        for (int k = 0; k < kBlockTop; ++k) {
+            double bk0 = after(e0, j0, pk0, pi0) ? e0 : -INFINITY;
+            int32_t bi0 = after(e0, j0, pk0, pi0) ? j0 : INT_MAX;
+            double bk1 = after(e1, j1, pk1, pi1) ? e1 : -INFINITY;
+            int32_t bi1 = after(e1, j1, pk1, pi1) ? j1 : INT_MAX;
+            wave_best_fast(bk0, bi0);
+            wave_best_fast(bk1, bi1);
+            pk0 = bk0;
+            pi0 = bi0;
+            pk1 = bk1;
+            pi1 = bi1;
+            if (lane == 0) {
+                ok[k] = bk0;
+                oi[k] = bi0;
+                ok[kBlockTop + k] = bk1;
+                oi[kBlockTop + k] = bi1;
+            }
+        }
+    }
 }
 
 template <bool SVR, int NBLK>
-static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s)
+static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
+                          hipEvent_t e0, hipEvent_t e1)
 {
     size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
     static size_t lds_allowed = 64 * 1024;
@@ -422,20 +433,26 @@ static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s)
         }
         lds_allowed = lds;
     }
-    k_rows<SVR, NBLK><<<nblocks, kRowThreads, lds, s>>>(a);
+    if (e0) {
+        hipExtLaunchKernelGGL(k_rows<SVR, NBLK>, dim3(nblocks),
+                              dim3(kRowThreads), (uint32_t)lds, s, e0, e1, 0,
+                              a);
+    } else {
+        k_rows<SVR, NBLK><<<nblocks, kRowThreads, lds, s>>>(a);
+    }
 }
 
 void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
-                 hipStream_t s)
+                 hipStream_t s, hipEvent_t e0, hipEvent_t e1)
 {
     if (nblocks <= 0) return;
     switch (nblk_cols * 2 + (svr ? 1 : 0)) {
-        case 2: rows_dispatch<false, 1>(a, nblocks, s); break;
-        case 3: rows_dispatch<true, 1>(a, nblocks, s); break;
-        case 4: rows_dispatch<false, 2>(a, nblocks, s); break;
-        case 5: rows_dispatch<true, 2>(a, nblocks, s); break;
-        case 8: rows_dispatch<false, 4>(a, nblocks, s); break;
-        case 9: rows_dispatch<true, 4>(a, nblocks, s); break;
+        case 2: rows_dispatch<false, 1>(a, nblocks, s, e0, e1); break;
+        case 3: rows_dispatch<true, 1>(a, nblocks, s, e0, e1); break;
+        case 4: rows_dispatch<false, 2>(a, nblocks, s, e0, e1); break;
+        case 5: rows_dispatch<true, 2>(a, nblocks, s, e0, e1); break;
+        case 8: rows_dispatch<false, 4>(a, nblocks, s, e0, e1); break;
+        case 9: rows_dispatch<true, 4>(a, nblocks, s, e0, e1); break;
         default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
     }
 }
@@ -449,186 +466,408 @@ __device__ __forceinline__ int64_t sample_of(bool svr, int64_t t, int64_t n)
     return (svr && t >= n) ? t - n : t;
 }
 
+// Scores of variable t on both sides, recomputed from the responses exactly
+// as k_rows computes them: up = v (t in I_up), low = -v (t in I_low).
+template <bool SVR>
+__device__ __forceinline__ void var_scores(const SelArgs& a, int64_t t,
+                                           double& up, double& lo)
+{
+    const int64_t n = a.n;
+    const int64_t sm = sample_of(SVR, t, n);
+    const uint8_t s = a.st[t];
+    double r;
+    if (SVR) r = t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps;
+    else r = (s & ST_YPOS) ? 1.0 : -1.0;
+    const double v = r - a.F[sm];
+    up = (s & ST_UP) ? v : -INFINITY;
+    lo = (s & ST_LOW) ? -v : -INFINITY;
+}
+
+// Survivor-list capacity per side of the threshold filter in k_select.
+constexpr int kSurv = 1024;
+
+// Top-`half` of entries (k[0..M), i[0..M)) by rank: entry e goes to slot
+// rank(e) = #{f : f better than e}; entries are distinct (key, index) pairs
+// so ranks are unique.  Run by threads [tl, tl+nt).
+__device__ __forceinline__ void rank_select(const double* k, const int32_t* i,
+                                            int M, int half, double* ok,
+                                            int32_t* oi, int tl, int nt)
+{
+    for (int e = tl; e < M; e += nt) {
+        const double ke = k[e];
+        const int32_t ie = i[e];
+        if (ke == -INFINITY) continue;
+        int r = 0;
+        for (int f = 0; f < M; ++f) r += better(k[f], i[f], ke, ie) ? 1 : 0;
+        if (r < half) {
+            ok[r] = ke;
+            oi[r] = ie;
+        }
+    }
+}
+
+__device__ __forceinline__ int lanes_below(unsigned long long m)
+{
+    return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((unsigned)m, 0));
+}
+
 template <bool SVR, int NBLK>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 {
     WorkingSet* ws = a.ws;
     if ((a.mode & SS_CHECK_DONE) && ws->done) return;
+    const uint64_t t_start = wall_clock64();
 
     constexpr int NW = kSelThreads / 64;
     constexpr int QS = NBLK * 16;  // slots covered by K_SS
     __shared__ double upk[kMaxHalf], lok[kMaxHalf];
     __shared__ int32_t upi[kMaxHalf], loi[kMaxHalf];
-    __shared__ double rk[2][2][NW];
-    __shared__ int32_t ri[2][2][NW];
+    __shared__ double rmax[2][NW * 4];
+    __shared__ double theta[2];
+    __shared__ double svk[2][kSurv];
+    __shared__ int32_t svi[2][kSurv];
+    __shared__ int32_t nsv[2];
+    __shared__ int32_t exb[2][kMaxHalf];
+    __shared__ int32_t nex[2];
+    __shared__ double rk[2][NW];
+    __shared__ int32_t ri[2][NW];
     __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
     __shared__ float shsS[kMaxQ];
     __shared__ float KSS[QS][QS + 1];
     __shared__ double shDc[kMaxQ];
-    __shared__ int32_t shNB, shNS, shGo;
+    __shared__ int32_t shNB, shNS, shGo, shSlow;
     __shared__ double shGap;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int half = a.half;
     const int64_t n = a.n, ldp = a.ldp;
     const bool given = (a.mode & SS_GIVEN_B) != 0;
+    const int rshift = 6 + __builtin_ctz((unsigned)a.tiles);  // row block
 
     if (!given) {
-        // merge the per-block candidates of both sides
-        const int cnt = a.nb * half;
+        // (1) the per-block candidates
+        const int cnt = a.nb * kBlockTop;
         double ku[kSelPerThread], kl[kSelPerThread];
         int32_t iu[kSelPerThread], il[kSelPerThread];
 #pragma unroll
         for (int j = 0; j < kSelPerThread; ++j) {
-            int e = tid + j * kSelThreads;
+            const int e = tid + j * kSelThreads;
             if (e < cnt) {
-                int blk = e / half, k = e - blk * half;
-                size_t bu = (size_t)blk * 2 * half;
+                const int blk = e / kBlockTop, k = e - blk * kBlockTop;
+                const size_t bu = (size_t)blk * 2 * kBlockTop;
                 ku[j] = a.cand_key[bu + k];
                 iu[j] = a.cand_idx[bu + k];
-                kl[j] = a.cand_key[bu + half + k];
-                il[j] = a.cand_idx[bu + half + k];
+                kl[j] = a.cand_key[bu + kBlockTop + k];
+                il[j] = a.cand_idx[bu + kBlockTop + k];
             } else {
                 ku[j] = kl[j] = -INFINITY;
                 iu[j] = il[j] = INT_MAX;
             }
         }
-        double pk0 = INFINITY, pk1 = INFINITY;
-        int32_t pi0 = -1, pi1 = -1;
-        for (int k = 0; k < half; ++k) {
-            double bk0 = -INFINITY, bk1 = -INFINITY;
-            int32_t bi0 = INT_MAX, bi1 = INT_MAX;
+        // (2) maxima of every 16-lane row: distinct candidates, so the
+        // half-th largest of them bounds the half-th best key from below
+        double mu = -INFINITY, ml = -INFINITY;
 #pragma unroll
-            for (int j = 0; j < kSelPerThread; ++j) {
-                if (after(ku[j], iu[j], pk0, pi0) &&
-                    better(ku[j], iu[j], bk0, bi0)) {
-                    bk0 = ku[j];
-                    bi0 = iu[j];
-                }
-                if (after(kl[j], il[j], pk1, pi1) &&
-                    better(kl[j], il[j], bk1, bi1)) {
-                    bk1 = kl[j];
-                    bi1 = il[j];
-                }
-            }
-            wave_best(bk0, bi0);
-            wave_best(bk1, bi1);
-            const int p = k & 1;
-            if (lane == 0) {
-                rk[p][0][wave] = bk0;
-                ri[p][0][wave] = bi0;
-                rk[p][1][wave] = bk1;
-                ri[p][1][wave] = bi1;
-            }
-            __syncthreads();
-            bk0 = rk[p][0][0];
-            bi0 = ri[p][0][0];
-            bk1 = rk[p][1][0];
-            bi1 = ri[p][1][0];
-#pragma unroll
-            for (int w = 1; w < NW; ++w) {
-                if (better(rk[p][0][w], ri[p][0][w], bk0, bi0)) {
-                    bk0 = rk[p][0][w];
-                    bi0 = ri[p][0][w];
-                }
-                if (better(rk[p][1][w], ri[p][1][w], bk1, bi1)) {
-                    bk1 = rk[p][1][w];
-                    bi1 = ri[p][1][w];
-                }
-            }
-            pk0 = bk0;
-            pi0 = bi0;
-            pk1 = bk1;
-            pi1 = bi1;
-            if (tid == 0) {
-                upk[k] = bk0;
-                upi[k] = bi0;
-                lok[k] = bk1;
-                loi[k] = bi1;
+        for (int j = 0; j < kSelPerThread; ++j) {
+            mu = fmax(mu, ku[j]);
+            ml = fmax(ml, kl[j]);
+        }
+        mu = row_max_f64(mu);
+        ml = row_max_f64(ml);
+        if ((lane & 15) == 0) {
+            rmax[0][wave * 4 + (lane >> 4)] = mu;
+            rmax[1][wave * 4 + (lane >> 4)] = ml;
+        }
+        if (tid < 2) nsv[tid] = 0;
+        if (tid < kMaxHalf) {
+            upk[tid] = lok[tid] = -INFINITY;
+            upi[tid] = loi[tid] = INT_MAX;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            // lane l holds row maximum l; theta = the largest x_l with at
+            // least `half` row maxima >= x_l (-inf if there is none)
+            for (int side = 0; side < 2; ++side) {
+                const double x = rmax[side][lane];
+                int c = 0;
+                for (int j = 0; j < NW * 4; ++j) c += rmax[side][j] >= x;
+                double th = (c >= half && x != -INFINITY) ? x : -INFINITY;
+                th = fmax(fmax(rl_f64(row_max_f64(th), 0),
+                               rl_f64(row_max_f64(th), 16)),
+                          fmax(rl_f64(row_max_f64(th), 32),
+                               rl_f64(row_max_f64(th), 48)));
+                if (lane == 0) theta[side] = th;
             }
         }
         __syncthreads();
+        // (3) keep the candidates at or above the bound
+        {
+            const double th0 = theta[0], th1 = theta[1];
+#pragma unroll
+            for (int j = 0; j < kSelPerThread; ++j) {
+                for (int side = 0; side < 2; ++side) {
+                    const double kv = side ? kl[j] : ku[j];
+                    const int32_t iv = side ? il[j] : iu[j];
+                    const double th = side ? th1 : th0;
+                    const bool keep = kv != -INFINITY && kv >= th;
+                    const unsigned long long m = __ballot(keep);
+                    if (m == 0) continue;
+                    int base = 0;
+                    if (lane == 0) base = atomicAdd(&nsv[side], __popcll(m));
+                    base = __builtin_amdgcn_readfirstlane(base);
+                    const int pos = base + lanes_below(m);
+                    if (keep && pos < kSurv) {
+                        svk[side][pos] = kv;
+                        svi[side][pos] = iv;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        const int M0 = nsv[0], M1 = nsv[1];
+        bool slow = M0 > kSurv || M1 > kSurv;
+        // (4) rank the survivors: side 0 on threads [0,512), side 1 on the rest
+        if (!slow) {
+            const int hs = kSelThreads / 2;
+            if (tid < hs) rank_select(svk[0], svi[0], M0, half, upk, upi, tid, hs);
+            else rank_select(svk[1], svi[1], M1, half, lok, loi, tid - hs, hs);
+        }
+        __syncthreads();
+        // (5) blocks whose whole candidate list was taken may hold more:
+        // wave 0 finds them (lane-parallel)
+        if (!slow && wave == 0) {
+            for (int side = 0; side < 2; ++side) {
+                const double* kk = side ? lok : upk;
+                const int32_t* ii = side ? loi : upi;
+                const bool valid = lane < half && kk[lane] != -INFINITY;
+                const int32_t b =
+                    valid ? (int32_t)(sample_of(SVR, ii[lane], n) >> rshift)
+                          : -1 - lane;
+                int c = 0;
+                bool first = true;
+                for (int j = 0; j < half; ++j) {
+                    const int32_t bj = rl_i32(b, j);
+                    c += bj == b;
+                    first &= !(j < lane && bj == b);
+                }
+                const bool ex = valid && c >= kBlockTop && first;
+                const unsigned long long m = __ballot(ex);
+                if (ex) exb[side][lanes_below(m)] = b;
+                if (lane == 0) nex[side] = __popcll(m);
+            }
+        }
+        __syncthreads();
+        if (!slow && nex[0] + nex[1] > 0) {
+            // (6) rare: drop those blocks' candidates, add all their
+            // variables with keys recomputed from F, rank again
+            const int64_t R = 1LL << rshift;
+            const int NV = SVR ? 2 : 1;
+            for (int side = 0; side < 2; ++side) {
+                const int ne = nex[side];
+                if (ne == 0) continue;
+                const int M = side ? M1 : M0;
+                const int64_t per = R * NV;
+                if (M + ne * per > kSurv) {
+                    slow = true;
+                    break;
+                }
+                for (int e = tid; e < M; e += kSelThreads) {
+                    const int32_t b =
+                        (int32_t)(sample_of(SVR, svi[side][e], n) >> rshift);
+                    bool drop = false;
+                    for (int x = 0; x < ne; ++x) drop |= exb[side][x] == b;
+                    if (drop) svk[side][e] = -INFINITY;
+                }
+                for (int64_t q = tid; q < ne * per; q += kSelThreads) {
+                    const int x = (int)(q / per);
+                    const int64_t o = q - (int64_t)x * per;
+                    const int64_t row = ((int64_t)exb[side][x] << rshift) + (o % R);
+                    double u = -INFINITY, l = -INFINITY;
+                    int32_t tt = INT_MAX;
+                    if (row < n) {
+                        tt = (int32_t)(o < R ? row : n + row);
+                        var_scores<SVR>(a, tt, u, l);
+                    }
+                    svk[side][M + q] = side ? l : u;
+                    svi[side][M + q] = tt;
+                }
+                __syncthreads();
+                if (tid < half) {
+                    if (side) { lok[tid] = -INFINITY; loi[tid] = INT_MAX; }
+                    else { upk[tid] = -INFINITY; upi[tid] = INT_MAX; }
+                }
+                __syncthreads();
+                rank_select(svk[side], svi[side], (int)(M + ne * per), half,
+                            side ? lok : upk, side ? loi : upi, tid,
+                            kSelThreads);
+                __syncthreads();
+            }
+            if (tid == 0) ws->rescans += 1;
+        }
+        if (slow) {
+            // (7) fallback: exact rounds over every variable's key
+            const int64_t N = SVR ? 2 * n : n;
+            for (int side = 0; side < 2; ++side) {
+                double pk = INFINITY;
+                int32_t pi = -1;
+                for (int k = 0; k < half; ++k) {
+                    double bk = -INFINITY;
+                    int32_t bi = INT_MAX;
+                    for (int64_t t = tid; t < N; t += kSelThreads) {
+                        double u, l;
+                        var_scores<SVR>(a, t, u, l);
+                        const double key = side ? l : u;
+                        if (after(key, (int32_t)t, pk, pi) &&
+                            better(key, (int32_t)t, bk, bi)) {
+                            bk = key;
+                            bi = (int32_t)t;
+                        }
+                    }
+                    wave_best_fast(bk, bi);
+                    if (lane == 0) {
+                        rk[k & 1][wave] = bk;
+                        ri[k & 1][wave] = bi;
+                    }
+                    __syncthreads();
+                    bk = rk[k & 1][0];
+                    bi = ri[k & 1][0];
+                    for (int w = 1; w < NW; ++w)
+                        if (better(rk[k & 1][w], ri[k & 1][w], bk, bi)) {
+                            bk = rk[k & 1][w];
+                            bi = ri[k & 1][w];
+                        }
+                    pk = bk;
+                    pi = bi;
+                    if (tid == 0) {
+                        if (side) { lok[k] = bk; loi[k] = bi; }
+                        else { upk[k] = bk; upi[k] = bi; }
+                    }
+                }
+            }
+            if (tid == 0) ws->slow_selects += 1;
+            __syncthreads();
+        }
     }
+    const uint64_t t_merge = wall_clock64();
 
-    if (tid == 0) {
-        int go = 0, nB = 0, nS = 0;
+    // (8) working set, distinct samples (wave 0, lane-parallel)
+    if (wave == 0) {
+        int go = 0, nB = 0;
         double gap = 0.0;
         if (!given) {
             const bool valid = upk[0] != -INFINITY && lok[0] != -INFINITY;
             const double m = upk[0], M = -lok[0];
             gap = valid ? m - M : 0.0;
-            ws->gap = gap;
-            ws->m = valid ? m : 0.0;
-            ws->M = valid ? M : 0.0;
+            bool build = true;
             if (a.mode & SS_SOLVE) {
                 if (!valid || gap <= a.tol) {
-                    ws->done = 1;
+                    if (lane == 0) ws->done = 1;
+                    build = false;
                 } else if (ws->iter >= a.max_iter) {
-                    ws->done = 2;
-                } else {
-                    for (int k = 0; k < half; ++k) {
-                        for (int side = 0; side < 2; ++side) {
-                            double key = side ? lok[k] : upk[k];
-                            int32_t t = side ? loi[k] : upi[k];
-                            if (key == -INFINITY) continue;
-                            bool dup = false;
-                            for (int c = 0; c < nB; ++c) dup |= (shB[c] == t);
-                            if (!dup) shB[nB++] = t;
-                        }
-                    }
-                    go = 1;
+                    if (lane == 0) ws->done = 2;
+                    build = false;
                 }
-            } else {
-                // selection only: publish B for inspection
-                for (int k = 0; k < half; ++k) {
-                    for (int side = 0; side < 2; ++side) {
-                        double key = side ? lok[k] : upk[k];
-                        int32_t t = side ? loi[k] : upi[k];
-                        if (key == -INFINITY) continue;
-                        bool dup = false;
-                        for (int c = 0; c < nB; ++c) dup |= (ws->B[c] == t);
-                        if (!dup) ws->B[nB++] = t;
+            }
+            if (lane == 0) {
+                ws->gap = gap;
+                ws->m = valid ? m : 0.0;
+                ws->M = valid ? M : 0.0;
+            }
+            if (build) {
+                // lanes [0,half): up list, [half,2half): low list; position
+                // in the interleaved order U0 L0 U1 L1 ...
+                const bool isU = lane < half;
+                const bool inL = lane >= half && lane < 2 * half;
+                const int k = isU ? lane : lane - half;
+                const double key = isU ? upk[k] : (inL ? lok[k] : -INFINITY);
+                const int32_t idx = isU ? upi[k] : (inL ? loi[k] : INT_MAX);
+                bool keep = (isU || inL) && key != -INFINITY;
+                if (keep) {
+                    // drop a variable already placed earlier in the order
+                    if (isU) {
+                        for (int j = 0; j < k; ++j)
+                            keep &= !(lok[j] != -INFINITY && loi[j] == idx);
+                    } else {
+                        for (int j = 0; j <= k; ++j)
+                            keep &= !(upk[j] != -INFINITY && upi[j] == idx);
                     }
                 }
-                ws->nB = nB;
+                const unsigned long long m = __ballot(keep);
+                const unsigned long long mu = m & ((1ull << half) - 1ull);
+                const unsigned long long ml = (m >> half) & ((1ull << half) - 1ull);
+                const unsigned long long below = (1ull << k) - 1ull;
+                int pos = __popcll(mu & below) + __popcll(ml & below);
+                if (!isU) pos += (int)((mu >> k) & 1ull);
+                int32_t* dst = (a.mode & SS_SOLVE) ? shB : ws->B;
+                if (keep) dst[pos] = idx;
+                nB = __popcll(m);
+                if (a.mode & SS_SOLVE) go = 1;
+                else if (lane == 0) ws->nB = nB;
             }
         } else {
             nB = ws->nB;
-            for (int c = 0; c < nB; ++c) shB[c] = ws->B[c];
+            if (lane < nB) shB[lane] = ws->B[lane];
             gap = ws->gap;
             go = (a.mode & SS_SOLVE) ? 1 : 0;
         }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        int nS = 0;
         if (go) {
-            for (int c = 0; c < nB; ++c) {
-                int32_t s = (int32_t)sample_of(SVR, shB[c], n);
-                int j = 0;
-                while (j < nS && shS[j] != s) ++j;
-                if (j == nS) shS[nS++] = s;
-                shSlot[c] = j;
+            // slot of each variable: rank of the first occurrence of its
+            // sample (eps-SVR: both copies of a sample share one slot)
+            const bool act = lane < nB;
+            const int32_t s = act ? (int32_t)sample_of(SVR, shB[lane], n) : -1;
+            int firstpos = lane;
+            if (SVR && act)
+                for (int j = lane - 1; j >= 0; --j)
+                    if ((int32_t)sample_of(SVR, shB[j], n) == s) firstpos = j;
+            const unsigned long long fm = __ballot(act && firstpos == lane);
+            const unsigned long long bl =
+                firstpos >= 64 ? ~0ull : ((1ull << firstpos) - 1ull);
+            const int slot = __popcll(fm & bl);
+            if (act) {
+                shSlot[lane] = slot;
+                if (firstpos == lane) shS[slot] = s;
             }
+            nS = __popcll(fm);
         }
-        shGo = go;
-        shNB = nB;
-        shNS = nS;
-        shGap = gap;
+        if (lane == 0) {
+            shGo = go;
+            shNB = nB;
+            shNS = nS;
+            shGap = gap;
+        }
     }
     __syncthreads();
-    if (!shGo) return;
+    if (!shGo) {
+        if (tid == 0) ws->prof[0] += (int64_t)(t_merge - t_start);
+        return;
+    }
     const int nB = shNB, nS = shNS;
 
-    // copy the working-set rows for the next k_rows; norms
-    {
-        const int q4 = (int)(ldp >> 2);
-        for (int e = tid; e < nS * q4; e += kSelThreads) {
-            int slot = e / q4, c4 = e - slot * q4;
-            *reinterpret_cast<float4*>(a.xS + (int64_t)slot * ldp + 4 * c4) =
-                ld4(a.X + (int64_t)shS[slot] * ldp + 4 * c4);
+    // (9) state of B for the subproblem (wave 0, loads issued early)
+    const bool act = wave == 0 && lane < nB;
+    const int32_t t = act ? shB[lane] : INT_MAX;
+    const int sl = act ? shSlot[lane] : 0;
+    const int64_t sm = act ? sample_of(SVR, t, n) : 0;
+    double al = act ? a.alpha[t] : 0.0;
+    double yv = 1.0, rv = 0.0, v = 0.0;
+    if (act) {
+        if (SVR) {
+            yv = t < n ? 1.0 : -1.0;
+            rv = t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps;
+        } else {
+            yv = (a.st[t] & ST_YPOS) ? 1.0 : -1.0;
+            rv = yv;
         }
-        if (tid < nS) shsS[tid] = a.sq[shS[tid]];
+        v = rv - a.F[sm];
     }
-    __syncthreads();
 
-    // K_SS on the matrix cores, same operand order as k_rows
+    // (10) K_SS on the matrix cores (same operand order as k_rows) while
+    // the other waves copy the working-set rows for the next k_rows
     if (wave < NBLK * NBLK) {
         const int g = lane >> 4, nl = lane & 15;
         const int bi = wave / NBLK, bj = wave - bi * NBLK;
@@ -636,6 +875,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         const bool va = sa < nS, vb = sb < nS;
         const float* xa = a.X + (int64_t)(va ? shS[sa] : 0) * ldp;
         const float* xb = a.X + (int64_t)(vb ? shS[sb] : 0) * ldp;
+        float sqa[4];
+#pragma unroll
+        for (int vv = 0; vv < 4; ++vv) {
+            const int ia = bi * 16 + 4 * g + vv;
+            sqa[vv] = ia < nS ? a.sq[shS[ia]] : 0.0f;
+        }
+        const float sqb = vb ? a.sq[shS[sb]] : 0.0f;
         floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
         for (int64_t c0 = 0; c0 < ldp; c0 += 16) {
             const int64_t col = c0 + 4 * g;
@@ -645,36 +891,39 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             acc = mfma_chunk(acc, av, bv);
         }
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            int ia = bi * 16 + 4 * g + v, ib = bj * 16 + nl;
+        for (int vv = 0; vv < 4; ++vv) {
+            const int ia = bi * 16 + 4 * g + vv, ib = bj * 16 + nl;
             if (ia < nS && ib < nS)
                 KSS[ia][ib] = ia == ib ? 1.0f
-                                       : rbf_from_dot(shsS[ia], shsS[ib],
-                                                      acc[v], a.gexp);
+                                       : rbf_from_dot(sqa[vv], sqb, acc[vv],
+                                                      a.gexp);
+        }
+        if (bi == 0 && bj == 0 && g == 0 && vb) shsS[sb] = sqb;
+        if (NBLK > 1 && bi == 0 && g == 0 && vb) shsS[sb] = sqb;
+    }
+    {
+        // copy by the waves without a K_SS block (by every wave if all of
+        // them have one)
+        constexpr int GW = NBLK * NBLK < NW ? NBLK * NBLK : 0;
+        if (wave >= GW) {
+            const int q4 = (int)(ldp >> 2);
+            const int nt = (NW - GW) * 64;
+            for (int e = tid - GW * 64; e < nS * q4; e += nt) {
+                const int slot = e / q4, c4 = e - slot * q4;
+                *reinterpret_cast<float4*>(a.xS + (int64_t)slot * ldp +
+                                           4 * c4) =
+                    ld4(a.X + (int64_t)shS[slot] * ldp + 4 * c4);
+            }
         }
     }
     __syncthreads();
+    const uint64_t t_kss = wall_clock64();
 
     if (wave != 0) return;
 
-    // subproblem: maximal-violating-pair steps restricted to B
-    const bool act = lane < nB;
-    const int32_t t = act ? shB[lane] : INT_MAX;
-    const int sl = act ? shSlot[lane] : 0;
-    const int64_t sm = act ? sample_of(SVR, t, n) : 0;
-    double al = act ? a.alpha[t] : 0.0;
+    // (11) subproblem: maximal-violating-pair steps restricted to B
     const double a0 = al;
     if ((a.mode & SS_SET_ALPHA) && act) al = ws->alphaB[lane];
-    double yv, rv;
-    if (SVR) {
-        yv = t < n ? 1.0 : -1.0;
-        rv = act ? (t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps)
-                 : 0.0;
-    } else {
-        yv = act ? ((a.st[t] & ST_YPOS) ? 1.0 : -1.0) : 1.0;
-        rv = yv;
-    }
-    double v = act ? rv - a.F[sm] : 0.0;
     const double C = a.C;
     const double itol = a.inner_tol_override >= 0.0
                             ? a.inner_tol_override
@@ -685,18 +934,30 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         const bool lo = act && ((yv > 0 && al > 0) || (yv < 0 && al < C));
         double bu = up ? v : -INFINITY, bl = lo ? -v : -INFINITY;
         int32_t iu = up ? t : INT_MAX, il = lo ? t : INT_MAX;
-        wave_best(bu, iu);
-        wave_best(bl, il);
+        if (NBLK == 1) {
+            row_best(bu, iu);
+            row_best(bl, il);
+            bu = rl_f64(bu, 0);
+            iu = rl_i32(iu, 0);
+            bl = rl_f64(bl, 0);
+            il = rl_i32(il, 0);
+        } else {
+            wave_best_fast(bu, iu);
+            wave_best_fast(bl, il);
+        }
         if (bu == -INFINITY || bl == -INFINITY) break;
         const double vi = bu, vj = -bl;
         if (!(vi - vj > itol)) break;
-        const int Li = __ffsll((unsigned long long)__ballot(act && t == iu)) - 1;
-        const int Lj = __ffsll((unsigned long long)__ballot(act && t == il)) - 1;
-        const double ali = __shfl(al, Li), alj = __shfl(al, Lj);
-        const double yi = __shfl(yv, Li), yj = __shfl(yv, Lj);
-        const int si = __shfl(sl, Li), sj = __shfl(sl, Lj);
-        double a2 = (double)KSS[si][si] + (double)KSS[sj][sj] -
-                    2.0 * (double)KSS[si][sj];
+        const int Li =
+            __ffsll((unsigned long long)__ballot(act && t == iu)) - 1;
+        const int Lj =
+            __ffsll((unsigned long long)__ballot(act && t == il)) - 1;
+        const double ali = rl_f64(al, Li), alj = rl_f64(al, Lj);
+        const double yi = rl_f64(yv, Li), yj = rl_f64(yv, Lj);
+        const int si = rl_i32(sl, Li), sj = rl_i32(sl, Lj);
+        const double kij = (double)KSS[si][sj];
+        const double kai = (double)KSS[sl][si], kaj = (double)KSS[sl][sj];
+        double a2 = (double)KSS[si][si] + (double)KSS[sj][sj] - 2.0 * kij;
         if (a2 <= 0.0) a2 = kTau;
         double s = (vi - vj) / a2;
         const double Ui = yi > 0 ? C - ali : ali;
@@ -719,8 +980,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             al -= yj * s;
             if (cj) al = yj > 0 ? 0.0 : C;
         }
-        if (act) v -= s * ((double)KSS[sl][si] - (double)KSS[sl][sj]);
+        if (act) v -= s * (kai - kaj);
     }
+    const uint64_t t_inner = wall_clock64();
 
     if (act) ws->alphaB[lane] = al;
     if (!(a.mode & SS_NO_WRITE)) {
@@ -751,7 +1013,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             ws->rows += nS;
         }
     }
-    if (lane == 0) ws->steps = steps;
+    if (lane == 0) {
+        ws->steps = steps;
+        ws->inner_total += steps;
+        ws->prof[0] += (int64_t)(t_merge - t_start);
+        ws->prof[1] += (int64_t)(t_kss - t_merge);
+        ws->prof[2] += (int64_t)(t_inner - t_kss);
+        ws->prof[3] += (int64_t)(wall_clock64() - t_inner);
+        ws->prof[4] += 1;
+    }
 }
 
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s)

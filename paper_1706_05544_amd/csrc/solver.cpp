@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 
 namespace msvm {
@@ -100,9 +101,14 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     gexp_ = (float)(o.gamma * 1.4426950408889634);
     half_ = o.q / 2;
     nblk_cols_ = o.q <= 16 ? 1 : (o.q <= 32 ? 2 : 4);
-    tiles_ = 1;
+    tiles_ = 2;
+    if (const char* e = getenv("SVM_TILES")) {  // tuning: a power of two
+        const int v = std::max(1, std::min(64, atoi(e)));
+        tiles_ = 1;
+        while (tiles_ * 2 <= v) tiles_ *= 2;
+    }
     const int64_t cap = (int64_t)kSelThreads * kSelPerThread;
-    while (((n_ + 64LL * tiles_ - 1) / (64LL * tiles_)) * half_ > cap)
+    while (((n_ + 64LL * tiles_ - 1) / (64LL * tiles_)) * kBlockTop > cap)
         tiles_ *= 2;
     nb_ = (int)((n_ + 64LL * tiles_ - 1) / (64LL * tiles_));
     if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, o.type == SVM_EPS_SVR) >
@@ -116,8 +122,8 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     y_.alloc((size_t)n_);
     ws_.alloc(1);
     xS_.alloc((size_t)kMaxQ * f.ldp);
-    ckey_.alloc((size_t)nb_ * 2 * half_);
-    cidx_.alloc((size_t)nb_ * 2 * half_);
+    ckey_.alloc((size_t)nb_ * 2 * kBlockTop);
+    cidx_.alloc((size_t)nb_ * 2 * kBlockTop);
     sum_.alloc(1);
     cvec_.alloc((size_t)n_);
     cblk_.alloc((size_t)compact_blocks(n_));
@@ -171,7 +177,7 @@ void Solver::launch_keys()
     launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
 }
 
-void Solver::launch_hot_rows()
+void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
 {
     RowArgs a{};
     a.X = f_.X.p;
@@ -191,7 +197,8 @@ void Solver::launch_hot_rows()
     a.tiles = tiles_;
     a.mode = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
     a.nS_override = -1;
-    launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
+    launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream, e0,
+                e1);
 }
 
 void Solver::launch_solve(int32_t mode)
@@ -220,6 +227,7 @@ void Solver::launch_solve(int32_t mode)
     a.max_inner = o_.max_inner;
     a.max_iter = o_.max_iter;
     a.mode = mode;
+    a.tiles = tiles_;
     launch_select(a, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
 }
 
@@ -254,13 +262,13 @@ bool Solver::run_loop(SolveResult& r)
     auto enqueue = [&](int slot) {
         for (int k = 0; k < K; ++k) {
             launch_solve(SS_SOLVE | SS_CHECK_DONE);
+            // profiling: the events are part of the kernel's own dispatch,
+            // so they bracket its execution, not the queue around it
             if (o_.profile)
-                HIP_TRY(hipEventRecord(pe[(size_t)(slot * K + k) * 2],
-                                       cx_.stream));
-            launch_hot_rows();
-            if (o_.profile)
-                HIP_TRY(hipEventRecord(pe[(size_t)(slot * K + k) * 2 + 1],
-                                       cx_.stream));
+                launch_hot_rows(pe[(size_t)(slot * K + k) * 2],
+                                pe[(size_t)(slot * K + k) * 2 + 1]);
+            else
+                launch_hot_rows();
         }
         HIP_TRY(hipMemcpyAsync(&hs.p[slot], ws_.p, sizeof(WorkingSet),
                                hipMemcpyDeviceToHost, cx_.stream));
@@ -407,6 +415,24 @@ SolveResult Solver::train()
     read_ws(w);
     r.kernel_rows = w.rows;
     r.iters = w.iter;
+    if (const char* e = getenv("SVM_LOG")) {
+        if (atoi(e) > 0 && w.prof[4] > 0) {
+            const double k = 10.0 / (double)w.prof[4];  // 100 MHz ticks -> ns
+            fprintf(stderr,
+                    "[mi355svm] iters=%lld rows=%lld inner=%.1f/iter "
+                    "rescans=%lld slow=%lld select(us): merge %.2f kss %.2f "
+                    "inner %.2f "
+                    "write %.2f; rows kernel %.2f us/launch (%lld timed)\n",
+                    (long long)w.iter, (long long)w.rows,
+                    (double)w.inner_total / (double)w.prof[4],
+                    (long long)w.rescans, (long long)w.slow_selects,
+                    1e-3 * k * w.prof[0],
+                    1e-3 * k * w.prof[1], 1e-3 * k * w.prof[2],
+                    1e-3 * k * w.prof[3],
+                    row_launches_ ? 1e3 * row_ms_ / row_launches_ : 0.0,
+                    (long long)row_launches_);
+        }
+    }
     return r;
 }
 
@@ -540,6 +566,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.max_inner = max_inner;
     a.max_iter = o_.max_iter;
     a.half = half_;
+    a.tiles = tiles_;
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_NO_WRITE;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
@@ -582,6 +609,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.max_inner = 0;
     a.max_iter = o_.max_iter;
     a.half = half_;
+    a.tiles = tiles_;
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_SET_ALPHA;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);

@@ -127,7 +127,7 @@ public:
 
 private:
     void launch_keys();
-    void launch_hot_rows();
+    void launch_hot_rows(hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
     void launch_solve(int32_t mode);
     void launch_select_only();
     bool run_loop(SolveResult& r);
