@@ -24,8 +24,8 @@ constexpr int kMaxQ = 64;          // largest working set
 constexpr int kMaxHalf = kMaxQ / 2;
 constexpr int kRowThreads = 256;   // row/update kernel: 4 waves
 constexpr int kSelThreads = 1024;  // select/solve kernel: one block
-constexpr int kSelPerThread = 8;   // candidates per side held per thread
-constexpr int kBlockTop = 2;       // candidates per side kept per row block
+constexpr int kSelPerThread = 16;  // candidates per side held per thread
+constexpr int kBlockTop = 2;       // candidates per side kept per row group
 constexpr double kTau = 1e-12;     // curvature floor of a degenerate pair
 
 // state byte of a dual variable
@@ -105,7 +105,7 @@ struct RowArgs {
 struct SelArgs {
     const double* cand_key;
     const int32_t* cand_idx;
-    int32_t nb, half;
+    int32_t nb, half;     // nb: candidate lists (one per k_rows wave)
     WorkingSet* ws;
     double* alpha;
     uint8_t* st;

@@ -122,6 +122,16 @@ __device__ __forceinline__ int row_min_i32(int v)
     return v;
 }
 
+// every lane of each 16-lane row receives the row sum (fixed order)
+__device__ __forceinline__ double row_sum_f64(double v)
+{
+    v += dpp_f64<kDppRor8>(v);
+    v += dpp_f64<kDppRor4>(v);
+    v += dpp_f64<kDppRor2>(v);
+    v += dpp_f64<kDppRor1>(v);
+    return v;
+}
+
 // Best (key, index) of a 16-lane row, in the order of better(); every lane
 // of the row receives its row's result.
 __device__ __forceinline__ void row_best(double& k, int32_t& i)
@@ -141,6 +151,27 @@ __device__ __forceinline__ void wave_best_fast(double& k, int32_t& i)
     c = min(min(rl_i32(c, 0), rl_i32(c, 16)), min(rl_i32(c, 32), rl_i32(c, 48)));
     k = M;
     i = c;
+}
+
+// Two independent wave-wide best searches, interleaved.
+__device__ __forceinline__ void wave_best_pair(double& k0, int32_t& i0,
+                                               double& k1, int32_t& i1)
+{
+    double M0 = row_max_f64(k0), M1 = row_max_f64(k1);
+    M0 = fmax(fmax(rl_f64(M0, 0), rl_f64(M0, 16)),
+              fmax(rl_f64(M0, 32), rl_f64(M0, 48)));
+    M1 = fmax(fmax(rl_f64(M1, 0), rl_f64(M1, 16)),
+              fmax(rl_f64(M1, 32), rl_f64(M1, 48)));
+    int c0 = row_min_i32(k0 == M0 ? i0 : INT_MAX);
+    int c1 = row_min_i32(k1 == M1 ? i1 : INT_MAX);
+    c0 = min(min(rl_i32(c0, 0), rl_i32(c0, 16)),
+             min(rl_i32(c0, 32), rl_i32(c0, 48)));
+    c1 = min(min(rl_i32(c1, 0), rl_i32(c1, 16)),
+             min(rl_i32(c1, 32), rl_i32(c1, 48)));
+    k0 = M0;
+    i0 = c0;
+    k1 = M1;
+    i1 = c1;
 }
 
 __device__ __forceinline__ float4 ld4(const float* p)

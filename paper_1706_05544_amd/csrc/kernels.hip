@@ -192,29 +192,82 @@ void launch_state_from_alpha(int32_t type, const float* y, const double* a,
 // row / update kernel
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ int32_t local_var(int e, int64_t R, int64_t rblk,
-                                             int64_t n)
-{
-    return (int32_t)(e < R ? rblk + e : n + rblk + (e - R));
-}
 
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
 {
-    size_t xs = (size_t)nblk_cols * 16 * (size_t)(ldp + 4) * sizeof(float);
-    size_t keys = (size_t)(svr ? 2 : 1) * 64 * tiles * 2 * sizeof(double);
-    return xs + keys;
+    (void)tiles;
+    (void)svr;
+    return (size_t)nblk_cols * 16 * (size_t)(ldp + 4) * sizeof(float);
+}
+
+// Running best two (score, variable) of one lane, in the order of better().
+struct Top2 {
+    double k1 = -INFINITY, k2 = -INFINITY;
+    int32_t i1 = INT_MAX, i2 = INT_MAX;
+    __device__ __forceinline__ void push(double k, int32_t i)
+    {
+        if (better(k, i, k1, i1)) {
+            k2 = k1;
+            i2 = i1;
+            k1 = k;
+            i1 = i;
+        } else if (better(k, i, k2, i2)) {
+            k2 = k;
+            i2 = i;
+        }
+    }
+};
+
+// Wave-level best two of the lanes' Top2 lists; lane 0 writes them.
+__device__ __forceinline__ void wave_top2(Top2 t, double* ok, int32_t* oi)
+{
+    double k = t.k1;
+    int32_t i = t.i1;
+    wave_best_fast(k, i);
+    const bool mine = t.i1 == i && t.k1 == k;
+    double k2 = mine ? t.k2 : t.k1;
+    int32_t i2 = mine ? t.i2 : t.i1;
+    wave_best_fast(k2, i2);
+    if ((threadIdx.x & 63) == 0) {
+        ok[0] = k;
+        oi[0] = i;
+        ok[1] = k2;
+        oi[1] = i2;
+    }
+}
+
+// Both sides at once (independent chains interleave): writes up[0..1] to
+// ok[0..1] and low[0..1] to ok[2..3].
+__device__ __forceinline__ void wave_top2_pair(Top2 u, Top2 l, double* ok,
+                                               int32_t* oi)
+{
+    double ku = u.k1, kl = l.k1;
+    int32_t iu = u.i1, il = l.i1;
+    wave_best_pair(ku, iu, kl, il);
+    const bool mu = u.i1 == iu && u.k1 == ku;
+    const bool ml = l.i1 == il && l.k1 == kl;
+    double ku2 = mu ? u.k2 : u.k1, kl2 = ml ? l.k2 : l.k1;
+    int32_t iu2 = mu ? u.i2 : u.i1, il2 = ml ? l.i2 : l.i1;
+    wave_best_pair(ku2, iu2, kl2, il2);
+    if ((threadIdx.x & 63) == 0) {
+        ok[0] = ku;
+        oi[0] = iu;
+        ok[1] = ku2;
+        oi[1] = iu2;
+        ok[2] = kl;
+        oi[2] = il;
+        ok[3] = kl2;
+        oi[3] = il2;
+    }
 }
 
 template <bool SVR, int NBLK>
 __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 {
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ double wk[2][kRowThreads / 64][kBlockTop];
-    __shared__ int32_t wi[2][kRowThreads / 64][kBlockTop];
     const WorkingSet* ws = a.ws;
     if ((a.mode & RU_CHECK_DONE) && ws->done) return;
 
-    constexpr int NV = SVR ? 2 : 1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, nl = lane & 15;
     const int T = a.tiles;
@@ -223,31 +276,22 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     const int64_t rblk = (int64_t)blockIdx.x * R;
     const int lstride = (int)ldp + 4;
     float* xsl = reinterpret_cast<float*>(smem);
-    double* kup = reinterpret_cast<double*>(
-        smem + (size_t)NBLK * 16 * lstride * sizeof(float));
-    double* klo = kup + NV * R;
 
     const bool want_rows = (a.mode & (RU_UPDATE | RU_ROWS)) != 0;
-    int nS = 0;
-    if (want_rows) nS = a.nS_override >= 0 ? a.nS_override : ws->nS;
-
-    if (nS > 0) {
+    // Stage all slots of the working-set rows without waiting for nS (the
+    // buffer always holds finite values; unused slots get coefficient 0).
+    if (want_rows) {
         const int q4 = (int)(ldp >> 2);
         const int total = NBLK * 16 * q4;
         for (int e = tid; e < total; e += kRowThreads) {
             int slot = e / q4, c4 = e - slot * q4;
-            float4 v = slot < nS ? ld4(a.xS + (int64_t)slot * ldp + 4 * c4)
-                                 : zero4();
-            *reinterpret_cast<float4*>(xsl + slot * lstride + 4 * c4) = v;
+            *reinterpret_cast<float4*>(xsl + slot * lstride + 4 * c4) =
+                ld4(a.xS + (int64_t)slot * ldp + 4 * c4);
         }
     }
-    if (a.mode & RU_CAND) {
-        for (int e = tid; e < NV * R; e += kRowThreads) {
-            kup[e] = -INFINITY;
-            klo[e] = -INFINITY;
-        }
-    }
-    __syncthreads();
+    int nS = 0;
+    if (want_rows) nS = a.nS_override >= 0 ? a.nS_override : ws->nS;
+    if (want_rows) __syncthreads();
 
     double cf[NBLK];
     float ssl[NBLK];
@@ -261,159 +305,126 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         sidx[b] = ok ? ws->S[slot] : -1;
     }
 
-    for (int ti = 0; ti < T; ++ti) {
-        const int64_t r0 = rblk + ((int64_t)wave * T + ti) * 16;
-        if (r0 >= n) break;
-        const int64_t orow = r0 + 4 * g + nl;  // row owned by lanes nl < 4
-        const bool owner = nl < 4 && orow < n;
-        double Fn = 0.0;
-        if (owner && (a.mode & (RU_UPDATE | RU_CAND))) Fn = a.F[orow];
+    // Rows of this wave: tiles ti = 0..Tw-1, rows rw0 + 16 ti + 0..15.
+    const int64_t rw0 = rblk + (int64_t)wave * T * 16;
+    const int Tw = rw0 >= n ? 0 : (int)min((int64_t)T, (n - rw0 + 15) / 16);
 
-        if (nS > 0) {
-            floatx4 acc[NBLK];
+    Top2 up, lo;  // this lane's best candidates of each side
+    auto push_keys = [&](int ti, double Fn, uint8_t s0, uint8_t s1, float zr) {
+        const int64_t orow = rw0 + 16 * ti + 4 * g + nl;
+        if (nl >= 4 || orow >= n) return;
+        const double rr0 = SVR ? (double)zr - a.eps
+                               : ((s0 & ST_YPOS) ? 1.0 : -1.0);
+        const double v0 = rr0 - Fn;
+        if (s0 & ST_UP) up.push(v0, (int32_t)orow);
+        if (s0 & ST_LOW) lo.push(-v0, (int32_t)orow);
+        if (SVR) {
+            const double v1 = ((double)zr + a.eps) - Fn;
+            if (s1 & ST_UP) up.push(v1, (int32_t)(n + orow));
+            if (s1 & ST_LOW) lo.push(-v1, (int32_t)(n + orow));
+        }
+    };
+    // Per-tile row data: norms of rows 4g..4g+3 (all lanes), and for the
+    // owner lanes (nl < 4) the response, state bytes and target.
+    struct Aux {
+        float sq[4];
+        double F;
+        uint8_t s0, s1;
+        float z;
+    };
+    auto load_aux = [&](int ti, Aux& x) {
+        const int64_t base = rw0 + 16 * ti + 4 * g;
 #pragma unroll
-            for (int b = 0; b < NBLK; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
-            const int64_t arow = r0 + nl;
-            const bool rv = arow < n;
-            const float* xr = a.X + (rv ? arow : 0) * ldp;
-#pragma unroll 4
-            for (int64_t c0 = 0; c0 < ldp; c0 += 16) {
-                const int64_t col = c0 + 4 * g;
-                const bool cv = col < ldp;
-                float4 av = (rv && cv) ? ld4(xr + col) : zero4();
-#pragma unroll
-                for (int b = 0; b < NBLK; ++b) {
-                    float4 bv = cv ? ld4(xsl + (b * 16 + nl) * lstride + col)
-                                   : zero4();
-                    acc[b] = mfma_chunk(acc[b], av, bv);
-                }
+        for (int v = 0; v < 4; ++v)
+            x.sq[v] = (nS > 0 && base + v < n) ? a.sq[base + v] : 0.0f;
+        const int64_t orow = base + nl;
+        const bool own = nl < 4 && orow < n;
+        x.F = (own && (a.mode & (RU_UPDATE | RU_CAND))) ? a.F[orow] : 0.0;
+        x.s0 = (own && (a.mode & RU_CAND)) ? a.st[orow] : 0;
+        x.s1 = (SVR && own && (a.mode & RU_CAND)) ? a.st[n + orow] : 0;
+        x.z = (SVR && own && (a.mode & RU_CAND)) ? a.z[orow] : 0.0f;
+    };
+
+    if (nS == 0) {
+        if (a.mode & RU_CAND) {
+            for (int ti = 0; ti < Tw; ++ti) {
+                Aux x;
+                load_aux(ti, x);
+                push_keys(ti, x.F, x.s0, x.s1, x.z);
             }
-            float sqr[4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                int64_t rr = r0 + 4 * g + v;
-                sqr[v] = rr < n ? a.sq[rr] : 0.0f;
-            }
+        }
+    } else {
+        // Tiles in pairs: the feature chunks of both tiles stream through
+        // the matrix cores against one LDS read of the working-set operand.
+        // No register prefetch: a low register count keeps every wave of the
+        // grid resident, and that many waves in flight hide the HBM latency.
+        const int nch = (int)((ldp + 15) >> 4);
+        auto epilogue = [&](int ti, const floatx4 (&acc)[NBLK], const Aux& xc) {
+            const int64_t r0 = rw0 + 16 * ti;
             double part[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int b = 0; b < NBLK; ++b) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    int64_t rr = r0 + 4 * g + v;
-                    float kv = rbf_from_dot(sqr[v], ssl[b], acc[b][v], a.gexp);
+                    const int64_t rr = r0 + 4 * g + v;
+                    float kv = rbf_from_dot(xc.sq[v], ssl[b], acc[b][v], a.gexp);
                     if (rr == (int64_t)sidx[b]) kv = 1.0f;
                     part[v] = fma(cf[b], (double)kv, part[v]);
                     if ((a.mode & RU_ROWS) && b * 16 + nl < nS && rr < n)
                         a.rows_out[(int64_t)(b * 16 + nl) * n + rr] = kv;
                 }
             }
+            double Fn = xc.F;
             if (a.mode & RU_UPDATE) {
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-#pragma unroll
-                    for (int off = 8; off > 0; off >>= 1)
-                        part[v] += __shfl_xor(part[v], off, 16);
-                }
+                for (int v = 0; v < 4; ++v) part[v] = row_sum_f64(part[v]);
                 Fn += pick4(part, nl & 3);
-                if (owner) a.F[orow] = Fn;
+                const int64_t orow = r0 + 4 * g + nl;
+                if (nl < 4 && orow < n) a.F[orow] = Fn;
             }
-        }
-
-        if ((a.mode & RU_CAND) && owner) {
-            const int64_t loc = orow - rblk;
-            const uint8_t s0 = a.st[orow];
-            const double rr0 = SVR ? (double)a.z[orow] - a.eps
-                                   : ((s0 & ST_YPOS) ? 1.0 : -1.0);
-            const double v0 = rr0 - Fn;
-            kup[loc] = (s0 & ST_UP) ? v0 : -INFINITY;
-            klo[loc] = (s0 & ST_LOW) ? -v0 : -INFINITY;
-            if (SVR) {
-                const uint8_t s1 = a.st[n + orow];
-                const double v1 = ((double)a.z[orow] + a.eps) - Fn;
-                kup[R + loc] = (s1 & ST_UP) ? v1 : -INFINITY;
-                klo[R + loc] = (s1 & ST_LOW) ? -v1 : -INFINITY;
+            if (a.mode & RU_CAND) push_keys(ti, Fn, xc.s0, xc.s1, xc.z);
+        };
+        for (int ti = 0; ti < Tw; ti += 2) {
+            const bool two = ti + 1 < Tw;
+            Aux x0, x1;
+            load_aux(ti, x0);
+            if (two) load_aux(ti + 1, x1);
+            const int64_t ar0 = rw0 + 16 * ti + nl, ar1 = ar0 + 16;
+            const bool rv0 = ar0 < n, rv1 = two && ar1 < n;
+            const float* xr0 = a.X + (rv0 ? ar0 : 0) * ldp;
+            const float* xr1 = a.X + (rv1 ? ar1 : 0) * ldp;
+            floatx4 acc0[NBLK], acc1[NBLK];
+#pragma unroll
+            for (int b = 0; b < NBLK; ++b) {
+                acc0[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+                acc1[b] = floatx4{0.f, 0.f, 0.f, 0.f};
             }
+#pragma unroll 4
+            for (int ch = 0; ch < nch; ++ch) {
+                const int col = ch * 16 + 4 * g;
+                const bool cv = col < ldp;
+                const float4 av0 = (rv0 && cv) ? ld4(xr0 + col) : zero4();
+                const float4 av1 = (rv1 && cv) ? ld4(xr1 + col) : zero4();
+#pragma unroll
+                for (int b = 0; b < NBLK; ++b) {
+                    float4 bv = cv ? ld4(xsl + (b * 16 + nl) * lstride + col)
+                                   : zero4();
+                    acc0[b] = mfma_chunk(acc0[b], av0, bv);
+                    if (two) acc1[b] = mfma_chunk(acc1[b], av1, bv);
+                }
+            }
+            epilogue(ti, acc0, x0);
+            if (two) epilogue(ti + 1, acc1, x1);
         }
     }
 
     if (!(a.mode & RU_CAND)) return;
-    __syncthreads();
-
-    // Per-wave best kBlockTop of each side over the wave's own rows (no
-    // block barrier), then wave 0 merges the four lists.  Only the top
-    // kBlockTop per block are kept: the global top q/2 lie in the blocks
-    // whose lists they exhaust, which k_select then rescans.
-    {
-        const int E = 16 * T;
-        const int wbase = wave * E;
-        double pk0 = INFINITY, pk1 = INFINITY;
-        int32_t pi0 = -1, pi1 = -1;
-        for (int k = 0; k < kBlockTop; ++k) {
-            double bk0 = -INFINITY, bk1 = -INFINITY;
-            int32_t bi0 = INT_MAX, bi1 = INT_MAX;
-            for (int j = lane; j < NV * E; j += 64) {
-                const int loc = j < E ? wbase + j : (int)R + wbase + (j - E);
-                const int32_t t = local_var(loc, R, rblk, n);
-                const double u = kup[loc], l = klo[loc];
-                if (after(u, t, pk0, pi0) && better(u, t, bk0, bi0)) {
-                    bk0 = u;
-                    bi0 = t;
-                }
-                if (after(l, t, pk1, pi1) && better(l, t, bk1, bi1)) {
-                    bk1 = l;
-                    bi1 = t;
-                }
-            }
-            wave_best_fast(bk0, bi0);
-            wave_best_fast(bk1, bi1);
-            pk0 = bk0;
-            pi0 = bi0;
-            pk1 = bk1;
-            pi1 = bi1;
-            if (lane == 0) {
-                wk[0][wave][k] = bk0;
-                wi[0][wave][k] = bi0;
-                wk[1][wave][k] = bk1;
-                wi[1][wave][k] = bi1;
-            }
-        }
-    }
-    __syncthreads();
-    if (wave != 0) return;
-    {
-        constexpr int NW = kRowThreads / 64;
-        double e0 = -INFINITY, e1 = -INFINITY;
-        int32_t j0 = INT_MAX, j1 = INT_MAX;
-        if (lane < NW * kBlockTop) {
-            const int w = lane / kBlockTop, k = lane - w * kBlockTop;
-            e0 = wk[0][w][k];
-            j0 = wi[0][w][k];
-            e1 = wk[1][w][k];
-            j1 = wi[1][w][k];
-        }
-        double* ok = a.cand_key + (size_t)blockIdx.x * 2 * kBlockTop;
-        int32_t* oi = a.cand_idx + (size_t)blockIdx.x * 2 * kBlockTop;
-        double pk0 = INFINITY, pk1 = INFINITY;
-        int32_t pi0 = -1, pi1 = -1;
-        for (int k = 0; k < kBlockTop; ++k) {
-            double bk0 = after(e0, j0, pk0, pi0) ? e0 : -INFINITY;
-            int32_t bi0 = after(e0, j0, pk0, pi0) ? j0 : INT_MAX;
-            double bk1 = after(e1, j1, pk1, pi1) ? e1 : -INFINITY;
-            int32_t bi1 = after(e1, j1, pk1, pi1) ? j1 : INT_MAX;
-            wave_best_fast(bk0, bi0);
-            wave_best_fast(bk1, bi1);
-            pk0 = bk0;
-            pi0 = bi0;
-            pk1 = bk1;
-            pi1 = bi1;
-            if (lane == 0) {
-                ok[k] = bk0;
-                oi[k] = bi0;
-                ok[kBlockTop + k] = bk1;
-                oi[kBlockTop + k] = bi1;
-            }
-        }
-    }
+    // the best two of each side over this wave's rows; a variable outside
+    // the global top q/2 never needs more (k_select rescans a row group
+    // whose two candidates were both taken)
+    const size_t wid = (size_t)blockIdx.x * (kRowThreads / 64) + wave;
+    wave_top2_pair(up, lo, a.cand_key + wid * 2 * kBlockTop,
+                   a.cand_idx + wid * 2 * kBlockTop);
 }
 
 template <bool SVR, int NBLK>
@@ -543,10 +554,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     const int half = a.half;
     const int64_t n = a.n, ldp = a.ldp;
     const bool given = (a.mode & SS_GIVEN_B) != 0;
-    const int rshift = 6 + __builtin_ctz((unsigned)a.tiles);  // row block
+    // candidate lists come from row groups of 16 * tiles rows (one wave)
+    const int rshift = 4 + __builtin_ctz((unsigned)a.tiles);
 
     if (!given) {
-        // (1) the per-block candidates
+        // (1) the per-group candidates
         const int cnt = a.nb * kBlockTop;
         double ku[kSelPerThread], kl[kSelPerThread];
         int32_t iu[kSelPerThread], il[kSelPerThread];

@@ -108,9 +108,12 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
         while (tiles_ * 2 <= v) tiles_ *= 2;
     }
     const int64_t cap = (int64_t)kSelThreads * kSelPerThread;
-    while (((n_ + 64LL * tiles_ - 1) / (64LL * tiles_)) * kBlockTop > cap)
+    constexpr int kWaves = kRowThreads / 64;
+    while (((n_ + 64LL * tiles_ - 1) / (64LL * tiles_)) * kWaves * kBlockTop >
+           cap)
         tiles_ *= 2;
     nb_ = (int)((n_ + 64LL * tiles_ - 1) / (64LL * tiles_));
+    ncand_ = nb_ * kWaves;
     if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, o.type == SVM_EPS_SVR) >
         160 * 1024)
         throw Error{SVM_E_UNSUPPORTED,
@@ -122,8 +125,8 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     y_.alloc((size_t)n_);
     ws_.alloc(1);
     xS_.alloc((size_t)kMaxQ * f.ldp);
-    ckey_.alloc((size_t)nb_ * 2 * kBlockTop);
-    cidx_.alloc((size_t)nb_ * 2 * kBlockTop);
+    ckey_.alloc((size_t)ncand_ * 2 * kBlockTop);
+    cidx_.alloc((size_t)ncand_ * 2 * kBlockTop);
     sum_.alloc(1);
     cvec_.alloc((size_t)n_);
     cblk_.alloc((size_t)compact_blocks(n_));
@@ -206,7 +209,7 @@ void Solver::launch_solve(int32_t mode)
     SelArgs a{};
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
-    a.nb = nb_;
+    a.nb = ncand_;
     a.half = half_;
     a.ws = ws_.p;
     a.alpha = alpha_.p;

@@ -139,7 +139,7 @@ private:
     SolveOptions o_;
     int64_t n_, N_;
     float gexp_;
-    int half_, nblk_cols_, tiles_, nb_;
+    int half_, nblk_cols_, tiles_, nb_, ncand_;
     DevBuf<double> F_, alpha_;
     DevBuf<uint8_t> st_;
     DevBuf<float> y_;
