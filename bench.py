@@ -43,6 +43,41 @@ def row_bytes_per_launch(n: int, d: int, svr: bool) -> int:
     return n * per
 
 
+KERNEL_SOURCES = ("paper_1706_05544_amd/csrc/kernels.hip",
+                  "paper_1706_05544_amd/csrc/device.hpp",
+                  "paper_1706_05544_amd/csrc/common.hpp")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per k_rows launch from the committed counter runs
+    (FETCH_SIZE and WRITE_SIZE, scaled by a copy of known size), or None
+    when the kernel sources changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", "k_rows_%s_hbm_counters.md"
+                        % workload)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(("#", "|", " ", "`")):
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w, target_s: float) -> dict:
     """The oracle (untuned) on a bounded sample: maximal-violating-pair SMO
     steps from alpha = 0 on the full training set; 2 kernel rows per step."""
@@ -85,6 +120,9 @@ def main() -> int:
     ap.add_argument("--working-set", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain device copy of 256 MiB (the "
+                         "reference kernel for the HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -118,6 +156,16 @@ def main() -> int:
         t1 = time.perf_counter()
         D = nv.svm_predict(m, Xt)
         return m, D, t1
+
+    if args.copy_calibration:
+        src = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device=dev)
+        src.fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("copy calibration: 3 copies of 256 MiB")
 
     for i in range(args.warmup):
         m, _, _ = step(0)
@@ -192,7 +240,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": measured_traffic(w.name),
             "avg_launch_us": 1e3 * avg_ms,
             "bytes_per_launch": bytes_launch,
             "launches_timed": launches,

@@ -256,7 +256,10 @@ bool Solver::run_loop(SolveResult& r)
     std::vector<hipEvent_t> pe;
     if (o_.profile) {
         pe.resize((size_t)4 * K);
-        for (auto& e : pe) HIP_TRY(hipEventCreate(&e));
+        // device-scope release only: the events time the kernel, not a
+        // flush of the caches to host-visible memory
+        for (auto& e : pe)
+            HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
     }
     WorkingSet w0;
     read_ws(w0);
