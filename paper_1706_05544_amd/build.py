@@ -20,12 +20,12 @@ ARCH = "gfx950"
 DEVICE_SOURCES = ["kernels.hip", "predict.hip"]
 HOST_SOURCES = ["solver.cpp", "api.cpp"]
 
+# Packed fp32 instructions are disabled for every compilation that has a
+# device pass (hipcc runs one for the .cpp sources too).
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",
-          "-I" + INCLUDE]
-# Packed fp32 instructions are disabled for all device code.
-DEVICE_FLAGS = ["-x", "hip", "--offload-arch=" + ARCH, "-Xclang",
-                "-target-feature", "-Xclang", "-packed-fp32-ops",
-                "-munsafe-fp-atomics"]
+          "--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang",
+          "-packed-fp32-ops", "-I" + INCLUDE]
+DEVICE_FLAGS = ["-x", "hip", "-munsafe-fp-atomics"]
 
 
 def _hipcc() -> str:

@@ -122,7 +122,7 @@ struct SelArgs {
     int32_t max_inner;
     int64_t max_iter;
     int32_t mode;
-    int32_t tiles;        // tiles per wave of k_rows (rows per block / 64)
+    int32_t group_rows;   // rows behind one candidate list (one k_rows wave)
 };
 
 struct PredictArgs {
@@ -158,6 +158,7 @@ void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
                  hipStream_t s, hipEvent_t e0 = nullptr,
                  hipEvent_t e1 = nullptr);
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr);
+int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
 void launch_state_from_alpha(int32_t type, const float* y, const double* a,
                              int64_t n, double C, uint8_t* st, hipStream_t s);

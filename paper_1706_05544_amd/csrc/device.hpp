@@ -179,6 +179,53 @@ __device__ __forceinline__ float4 ld4(const float* p)
     return *reinterpret_cast<const float4*>(p);
 }
 
+// ---- raw buffer accesses ----
+// A buffer resource covers `bytes` bytes from a base address.  A load at an
+// offset at or past the end returns zero without touching memory and a store
+// there is dropped, so ragged tails need no branch around the access (a
+// branch around a load also keeps the compiler from counting the loads in
+// flight).  Offsets are byte offsets below 2^31; kOob lies past every range.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcRaw32 = 0x00020000;  // word 3: 32-bit data format
+constexpr uint32_t kOob = 0x80000000u;
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* p, int64_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0,
+                                             (int)bytes, kRsrcRaw32);
+}
+
+__device__ __forceinline__ float4 bld_f4(Rsrc r, uint32_t off)
+{
+    const floatx4 v = __builtin_bit_cast(
+        floatx4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+    return make_float4(v[0], v[1], v[2], v[3]);
+}
+
+__device__ __forceinline__ float bld_f32(Rsrc r, uint32_t off)
+{
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+
+__device__ __forceinline__ double bld_f64(Rsrc r, uint32_t off)
+{
+    return __builtin_bit_cast(
+        double, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
+
+__device__ __forceinline__ uint8_t bld_u8(Rsrc r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
+}
+
+__device__ __forceinline__ void bst_f64(Rsrc r, uint32_t off, double v)
+{
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), r,
+                                          (int)off, 0, 0);
+}
+
 __device__ __forceinline__ float4 zero4()
 {
     return make_float4(0.0f, 0.0f, 0.0f, 0.0f);

@@ -193,11 +193,36 @@ void launch_state_from_alpha(int32_t type, const float* y, const double* a,
 // ---------------------------------------------------------------------------
 
 
+// LDS row stride of the per-wave feature slab buffer (64 columns + pad)
+constexpr int kSlabStride = 68;
+// feature slabs in flight per wave of k_rows
+constexpr int kRing = 4;
+constexpr int kRowWaves = kRowThreads / 64;
+
+// LDS row stride of a staged working-set sample: ldp rounded up to whole
+// 16-feature chunks (zero-filled) plus a pad of 4 against bank conflicts.
+__host__ __device__ inline int rows_xs_stride(int64_t ldp)
+{
+    return (int)(((ldp + 15) & ~(int64_t)15) + 4);
+}
+
+// Per-wave LDS bytes for the row data of 16 * tiles rows: F (fp64), the
+// squared norm, for eps-SVR the target, and the state byte of each copy.
+__host__ __device__ inline int rows_aux_bytes(int tiles, bool svr)
+{
+    return ((16 * tiles * (svr ? 18 : 13)) + 15) & ~15;
+}
+
+__host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp)
+{
+    return (size_t)nblk_cols * 16 * rows_xs_stride(ldp) * sizeof(float) +
+           (size_t)kRowWaves * 16 * kSlabStride * sizeof(float);
+}
+
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
 {
-    (void)tiles;
-    (void)svr;
-    return (size_t)nblk_cols * 16 * (size_t)(ldp + 4) * sizeof(float);
+    return rows_aux_offset(nblk_cols, ldp) +
+           (size_t)kRowWaves * rows_aux_bytes(tiles, svr);
 }
 
 // Running best two (score, variable) of one lane, in the order of better().
@@ -218,26 +243,8 @@ struct Top2 {
     }
 };
 
-// Wave-level best two of the lanes' Top2 lists; lane 0 writes them.
-__device__ __forceinline__ void wave_top2(Top2 t, double* ok, int32_t* oi)
-{
-    double k = t.k1;
-    int32_t i = t.i1;
-    wave_best_fast(k, i);
-    const bool mine = t.i1 == i && t.k1 == k;
-    double k2 = mine ? t.k2 : t.k1;
-    int32_t i2 = mine ? t.i2 : t.i1;
-    wave_best_fast(k2, i2);
-    if ((threadIdx.x & 63) == 0) {
-        ok[0] = k;
-        oi[0] = i;
-        ok[1] = k2;
-        oi[1] = i2;
-    }
-}
-
-// Both sides at once (independent chains interleave): writes up[0..1] to
-// ok[0..1] and low[0..1] to ok[2..3].
+// Both sides at once (independent chains interleave): writes the wave's best
+// two up scores to ok[0..1] and best two low scores to ok[2..3].
 __device__ __forceinline__ void wave_top2_pair(Top2 u, Top2 l, double* ok,
                                                int32_t* oi)
 {
@@ -261,181 +268,287 @@ __device__ __forceinline__ void wave_top2_pair(Top2 u, Top2 l, double* ok,
     }
 }
 
-template <bool SVR, int NBLK>
+// Row/update kernel.  Each wave owns 16 * tiles consecutive rows.
+//
+// Its row data (F, norms, state bytes, targets) is read once into a
+// wave-private LDS area, updated there and F is written back, coalesced, at
+// the end: the feature stream is then the only global traffic in the main
+// loop, and every load in it is unconditional (buffer range checks give the
+// zeros of ragged tails), so the loads stay in flight across slabs.
+//
+// Features go through 64-column slabs: the global loads are row-contiguous
+// (16 lanes cover 256 B of one row, 4 rows per instruction) and run kRing
+// slabs ahead; each slab passes through a wave-private LDS buffer and is read
+// back in the matrix-core operand layout (lane (g, nl): row nl, columns
+// 16c + 4g .. +3 of chunk c), which is the library-wide chunk order, so every
+// K value matches the other kernels bitwise.
+template <bool SVR, int NBLK, int MODE>
 __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 {
+    constexpr bool UPD = (MODE & RU_UPDATE) != 0;
+    constexpr bool ROWS = (MODE & RU_ROWS) != 0;
+    constexpr bool CAND = (MODE & RU_CAND) != 0;
+    constexpr bool XS = UPD || ROWS;  // the working-set samples are needed
+    constexpr int kXsEarly = 2;       // staging loads issued with the stream
     extern __shared__ __align__(16) unsigned char smem[];
     const WorkingSet* ws = a.ws;
-    if ((a.mode & RU_CHECK_DONE) && ws->done) return;
+    if ((MODE & RU_CHECK_DONE) && ws->done) return;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform by construction; said so, so that the buffer resources
+    // built from it live in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, nl = lane & 15;
-    const int T = a.tiles;
-    const int64_t n = a.n, ldp = a.ldp;
-    const int64_t R = 64LL * T;
-    const int64_t rblk = (int64_t)blockIdx.x * R;
-    const int lstride = (int)ldp + 4;
+    const int T = a.tiles, RW = 16 * T;
+    const int64_t n = a.n;
+    const int ldp = (int)a.ldp;
+    const int xstride = rows_xs_stride(ldp);
     float* xsl = reinterpret_cast<float*>(smem);
 
-    const bool want_rows = (a.mode & (RU_UPDATE | RU_ROWS)) != 0;
-    // Stage all slots of the working-set rows without waiting for nS (the
-    // buffer always holds finite values; unused slots get coefficient 0).
-    if (want_rows) {
-        const int q4 = (int)(ldp >> 2);
-        const int total = NBLK * 16 * q4;
-        for (int e = tid; e < total; e += kRowThreads) {
-            int slot = e / q4, c4 = e - slot * q4;
-            *reinterpret_cast<float4*>(xsl + slot * lstride + 4 * c4) =
-                ld4(a.xS + (int64_t)slot * ldp + 4 * c4);
-        }
-    }
-    int nS = 0;
-    if (want_rows) nS = a.nS_override >= 0 ? a.nS_override : ws->nS;
-    if (want_rows) __syncthreads();
-
+    // working-set slot b * 16 + nl of this lane (slots past nS contribute 0)
+    const int nS = XS ? (a.nS_override >= 0 ? a.nS_override : ws->nS) : 0;
     double cf[NBLK];
     float ssl[NBLK];
     int32_t sidx[NBLK];
 #pragma unroll
     for (int b = 0; b < NBLK; ++b) {
-        int slot = b * 16 + nl;
-        bool ok = slot < nS;
-        cf[b] = (ok && (a.mode & RU_UPDATE)) ? ws->coef[slot] : 0.0;
-        ssl[b] = ok ? ws->sS[slot] : 0.0f;
-        sidx[b] = ok ? ws->S[slot] : -1;
+        const int slot = b * 16 + nl;  // < kMaxQ: always inside the arrays
+        const bool ok = slot < nS;
+        const double c = ws->coef[slot];
+        const float s = ws->sS[slot];
+        const int32_t i = ws->S[slot];
+        cf[b] = (ok && UPD) ? c : 0.0;
+        ssl[b] = ok ? s : 0.0f;
+        sidx[b] = ok ? i : -1;
     }
 
-    // Rows of this wave: tiles ti = 0..Tw-1, rows rw0 + 16 ti + 0..15.
-    const int64_t rw0 = rblk + (int64_t)wave * T * 16;
-    const int Tw = rw0 >= n ? 0 : (int)min((int64_t)T, (n - rw0 + 15) / 16);
+    // rows of this wave: rw0 .. rw0 + nw - 1, in Tw tiles of 16
+    const int64_t rw0 = ((int64_t)blockIdx.x * kRowWaves + wave) * RW;
+    const int nw = rw0 >= n ? 0 : (int)min((int64_t)RW, n - rw0);
+    const int Tw = (nw + 15) >> 4;
+    unsigned char* aux =
+        smem + rows_aux_offset(NBLK, ldp) + wave * rows_aux_bytes(T, SVR);
+    double* Fw = reinterpret_cast<double*>(aux);
+    float* sqw = reinterpret_cast<float*>(aux + 8 * RW);
+    float* zw = reinterpret_cast<float*>(aux + 12 * RW);
+    uint8_t* stw = aux + (SVR ? 16 : 12) * RW;  // copy (i,-) at stw[RW + r]
 
-    Top2 up, lo;  // this lane's best candidates of each side
-    auto push_keys = [&](int ti, double Fn, uint8_t s0, uint8_t s1, float zr) {
-        const int64_t orow = rw0 + 16 * ti + 4 * g + nl;
-        if (nl >= 4 || orow >= n) return;
-        const double rr0 = SVR ? (double)zr - a.eps
-                               : ((s0 & ST_YPOS) ? 1.0 : -1.0);
-        const double v0 = rr0 - Fn;
-        if (s0 & ST_UP) up.push(v0, (int32_t)orow);
-        if (s0 & ST_LOW) lo.push(-v0, (int32_t)orow);
-        if (SVR) {
-            const double v1 = ((double)zr + a.eps) - Fn;
-            if (s1 & ST_UP) up.push(v1, (int32_t)(n + orow));
-            if (s1 & ST_LOW) lo.push(-v1, (int32_t)(n + orow));
+    // row data of rows k0 .. k0 + 255 of the wave: issue, then store to LDS
+    struct AuxRegs {
+        double f[4];
+        float q[4], z[4];
+        uint8_t s0[4], s1[4];
+    };
+    const Rsrc rF = make_rsrc(a.F + rw0, (int64_t)nw * 8);
+    auto aux_issue = [&](int k0, AuxRegs& x) {
+        const Rsrc rQ = make_rsrc(a.sq + rw0, (int64_t)nw * 4);
+        const Rsrc rS0 = make_rsrc(a.st + rw0, nw);
+        const Rsrc rS1 = make_rsrc(a.st + n + rw0, SVR ? nw : 0);
+        const Rsrc rZ = make_rsrc(a.z + rw0, SVR ? (int64_t)nw * 4 : 0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t r = (uint32_t)(k0 + 64 * j + lane);
+            x.f[j] = (UPD || CAND) ? bld_f64(rF, 8 * r) : 0.0;
+            x.q[j] = XS ? bld_f32(rQ, 4 * r) : 0.0f;
+            x.s0[j] = CAND ? bld_u8(rS0, r) : 0;
+            x.s1[j] = (SVR && CAND) ? bld_u8(rS1, r) : 0;
+            x.z[j] = (SVR && CAND) ? bld_f32(rZ, 4 * r) : 0.0f;
         }
     };
-    // Per-tile row data: norms of rows 4g..4g+3 (all lanes), and for the
-    // owner lanes (nl < 4) the response, state bytes and target.
-    struct Aux {
-        float sq[4];
-        double F;
-        uint8_t s0, s1;
-        float z;
-    };
-    auto load_aux = [&](int ti, Aux& x) {
-        const int64_t base = rw0 + 16 * ti + 4 * g;
+    auto aux_store = [&](int k0, const AuxRegs& x) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-            x.sq[v] = (nS > 0 && base + v < n) ? a.sq[base + v] : 0.0f;
-        const int64_t orow = base + nl;
-        const bool own = nl < 4 && orow < n;
-        x.F = (own && (a.mode & (RU_UPDATE | RU_CAND))) ? a.F[orow] : 0.0;
-        x.s0 = (own && (a.mode & RU_CAND)) ? a.st[orow] : 0;
-        x.s1 = (SVR && own && (a.mode & RU_CAND)) ? a.st[n + orow] : 0;
-        x.z = (SVR && own && (a.mode & RU_CAND)) ? a.z[orow] : 0.0f;
-    };
-
-    if (nS == 0) {
-        if (a.mode & RU_CAND) {
-            for (int ti = 0; ti < Tw; ++ti) {
-                Aux x;
-                load_aux(ti, x);
-                push_keys(ti, x.F, x.s0, x.s1, x.z);
+        for (int j = 0; j < 4; ++j) {
+            const int r = k0 + 64 * j + lane;
+            if (r < RW) {
+                Fw[r] = x.f[j];
+                sqw[r] = x.q[j];
+                stw[r] = x.s0[j];
+                if (SVR) {
+                    stw[RW + r] = x.s1[j];
+                    zw[r] = x.z[j];
+                }
             }
         }
-    } else {
-        // Tiles in pairs: the feature chunks of both tiles stream through
-        // the matrix cores against one LDS read of the working-set operand.
-        // No register prefetch: a low register count keeps every wave of the
-        // grid resident, and that many waves in flight hide the HBM latency.
-        const int nch = (int)((ldp + 15) >> 4);
-        auto epilogue = [&](int ti, const floatx4 (&acc)[NBLK], const Aux& xc) {
-            const int64_t r0 = rw0 + 16 * ti;
+    };
+
+    Top2 up, lo;  // this lane's best candidates of each side
+    auto push = [&](int lr, double Fn) {
+        const int32_t row = (int32_t)(rw0 + lr);
+        const uint8_t s0 = stw[lr];
+        const double r0 = SVR ? (double)zw[lr] - a.eps
+                              : ((s0 & ST_YPOS) ? 1.0 : -1.0);
+        const double v0 = r0 - Fn;
+        if (s0 & ST_UP) up.push(v0, row);
+        if (s0 & ST_LOW) lo.push(-v0, row);
+        if (SVR) {
+            const uint8_t s1 = stw[RW + lr];
+            const double v1 = ((double)zw[lr] + a.eps) - Fn;
+            if (s1 & ST_UP) up.push(v1, (int32_t)(n + row));
+            if (s1 & ST_LOW) lo.push(-v1, (int32_t)(n + row));
+        }
+    };
+
+    if (XS) {
+        // Staged working-set rows: every slot (finite values past nS),
+        // zero-filled to whole 16-feature chunks.
+        const int q4 = (xstride - 4) >> 2;  // float4 per staged row
+        const int xs_total = NBLK * 16 * q4;
+        const Rsrc rXs = make_rsrc(a.xS, (int64_t)NBLK * 16 * ldp * 4);
+        auto xs_off = [&](int e) -> uint32_t {
+            const int slot = e / q4, c4 = e - slot * q4;
+            return (e < xs_total && 4 * c4 < ldp)
+                       ? (uint32_t)((slot * ldp + 4 * c4) * 4)
+                       : kOob;
+        };
+        auto xs_put = [&](int e, float4 v) {
+            const int slot = e / q4, c4 = e - slot * q4;
+            if (e < xs_total)
+                *reinterpret_cast<float4*>(xsl + slot * xstride + 4 * c4) = v;
+        };
+
+        const int nslab = (ldp + 63) >> 6;
+        const Rsrc rX = make_rsrc(a.X + rw0 * ldp, (int64_t)nw * ldp * 4);
+        float* wbuf = xsl + NBLK * 16 * xstride + wave * (16 * kSlabStride);
+        const uint32_t step4 = (uint32_t)(16 * ldp);  // 4 rows, in bytes
+        int fti = 0, fsl = 0;  // next slab to fetch
+        auto fetch = [&](float4 (&v)[4]) {
+            const int col = fsl * 64 + 4 * nl;
+            const bool ok = fti < Tw && col < ldp;
+            const uint32_t o = (uint32_t)(((16 * fti + g) * ldp + col) * 4);
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                v[rr] = bld_f4(rX, ok ? o + rr * step4 : kOob);
+            if (++fsl == nslab) {
+                fsl = 0;
+                ++fti;
+            }
+        };
+
+        // Everything the first slabs need is requested at once: the first
+        // staging loads, the row data and kRing feature slabs.
+        float4 xv[kXsEarly];
+#pragma unroll
+        for (int i = 0; i < kXsEarly; ++i)
+            xv[i] = bld_f4(rXs, xs_off(tid + i * kRowThreads));
+        AuxRegs ar;
+        aux_issue(0, ar);
+        float4 ring[kRing][4];
+#pragma unroll
+        for (int j = 0; j < kRing; ++j) fetch(ring[j]);
+#pragma unroll
+        for (int i = 0; i < kXsEarly; ++i) xs_put(tid + i * kRowThreads, xv[i]);
+        aux_store(0, ar);
+        for (int k0 = 256; k0 < RW; k0 += 256) {
+            aux_issue(k0, ar);
+            aux_store(k0, ar);
+        }
+        for (int e = tid + kXsEarly * kRowThreads; e < xs_total;
+             e += kRowThreads)
+            xs_put(e, bld_f4(rXs, xs_off(e)));
+        __syncthreads();
+
+        floatx4 acc[NBLK];
+        auto epilogue = [&](int ti) {
+            const int lr = 16 * ti + 4 * g;
+            const float4 q4v = *reinterpret_cast<const float4*>(sqw + lr);
+            const float qv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
             double part[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int b = 0; b < NBLK; ++b) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int64_t rr = r0 + 4 * g + v;
-                    float kv = rbf_from_dot(xc.sq[v], ssl[b], acc[b][v], a.gexp);
-                    if (rr == (int64_t)sidx[b]) kv = 1.0f;
+                    float kv = rbf_from_dot(qv[v], ssl[b], acc[b][v], a.gexp);
+                    if (rw0 + lr + v == (int64_t)sidx[b]) kv = 1.0f;
                     part[v] = fma(cf[b], (double)kv, part[v]);
-                    if ((a.mode & RU_ROWS) && b * 16 + nl < nS && rr < n)
-                        a.rows_out[(int64_t)(b * 16 + nl) * n + rr] = kv;
+                    if (ROWS && b * 16 + nl < nS && lr + v < nw)
+                        a.rows_out[(int64_t)(b * 16 + nl) * n + rw0 + lr + v] =
+                            kv;
                 }
             }
-            double Fn = xc.F;
-            if (a.mode & RU_UPDATE) {
+            const int orl = lr + (nl & 3);  // row owned by lanes nl < 4
+            double Fn = 0.0;
+            if (UPD || CAND) Fn = Fw[orl];
+            if (UPD) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) part[v] = row_sum_f64(part[v]);
                 Fn += pick4(part, nl & 3);
-                const int64_t orow = r0 + 4 * g + nl;
-                if (nl < 4 && orow < n) a.F[orow] = Fn;
+                if (nl < 4) Fw[orl] = Fn;
             }
-            if (a.mode & RU_CAND) push_keys(ti, Fn, xc.s0, xc.s1, xc.z);
+            if (CAND && nl < 4 && orl < nw) push(orl, Fn);
         };
-        for (int ti = 0; ti < Tw; ti += 2) {
-            const bool two = ti + 1 < Tw;
-            Aux x0, x1;
-            load_aux(ti, x0);
-            if (two) load_aux(ti + 1, x1);
-            const int64_t ar0 = rw0 + 16 * ti + nl, ar1 = ar0 + 16;
-            const bool rv0 = ar0 < n, rv1 = two && ar1 < n;
-            const float* xr0 = a.X + (rv0 ? ar0 : 0) * ldp;
-            const float* xr1 = a.X + (rv1 ? ar1 : 0) * ldp;
-            floatx4 acc0[NBLK], acc1[NBLK];
+
+        int pti = 0, psl = 0;  // slab being processed
+        for (int s0 = 0; s0 < Tw * nslab; s0 += kRing) {
+            // all kRing slots every trip (slabs past the end are zeros and
+            // touch no memory), so the loads in flight are countable
 #pragma unroll
-            for (int b = 0; b < NBLK; ++b) {
-                acc0[b] = floatx4{0.f, 0.f, 0.f, 0.f};
-                acc1[b] = floatx4{0.f, 0.f, 0.f, 0.f};
-            }
-#pragma unroll 4
-            for (int ch = 0; ch < nch; ++ch) {
-                const int col = ch * 16 + 4 * g;
-                const bool cv = col < ldp;
-                const float4 av0 = (rv0 && cv) ? ld4(xr0 + col) : zero4();
-                const float4 av1 = (rv1 && cv) ? ld4(xr1 + col) : zero4();
+            for (int j = 0; j < kRing; ++j) {
+                if (psl == 0) {
 #pragma unroll
-                for (int b = 0; b < NBLK; ++b) {
-                    float4 bv = cv ? ld4(xsl + (b * 16 + nl) * lstride + col)
-                                   : zero4();
-                    acc0[b] = mfma_chunk(acc0[b], av0, bv);
-                    if (two) acc1[b] = mfma_chunk(acc1[b], av1, bv);
+                    for (int b = 0; b < NBLK; ++b)
+                        acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    *reinterpret_cast<float4*>(
+                        wbuf + (4 * rr + g) * kSlabStride + 4 * nl) =
+                        ring[j][rr];
+                fetch(ring[j]);  // refill the slot kRing slabs ahead
+                __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int ch = psl * 4 + c;
+                    if (ch * 16 < ldp) {  // chunk present (uniform)
+                        const float4 av =
+                            ld4(wbuf + nl * kSlabStride + c * 16 + 4 * g);
+#pragma unroll
+                        for (int b = 0; b < NBLK; ++b) {
+                            const float4 bv = ld4(xsl + (b * 16 + nl) * xstride +
+                                                  ch * 16 + 4 * g);
+                            acc[b] = mfma_chunk(acc[b], av, bv);
+                        }
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
+                if (psl == nslab - 1 && pti < Tw) epilogue(pti);
+                if (++psl == nslab) {
+                    psl = 0;
+                    ++pti;
                 }
             }
-            epilogue(ti, acc0, x0);
-            if (two) epilogue(ti + 1, acc1, x1);
+        }
+        if (UPD)
+            for (int r = lane; r < nw; r += 64) bst_f64(rF, 8 * r, Fw[r]);
+    } else if (CAND) {
+        AuxRegs ar;
+        for (int k0 = 0; k0 < RW; k0 += 256) {
+            aux_issue(k0, ar);
+            aux_store(k0, ar);
+        }
+        for (int ti = 0; ti < Tw; ++ti) {
+            const int orl = 16 * ti + 4 * g + (nl & 3);
+            if (nl < 4 && orl < nw) push(orl, Fw[orl]);
         }
     }
 
-    if (!(a.mode & RU_CAND)) return;
+    if (!CAND) return;
     // the best two of each side over this wave's rows; a variable outside
     // the global top q/2 never needs more (k_select rescans a row group
     // whose two candidates were both taken)
-    const size_t wid = (size_t)blockIdx.x * (kRowThreads / 64) + wave;
+    const size_t wid = (size_t)blockIdx.x * kRowWaves + wave;
     wave_top2_pair(up, lo, a.cand_key + wid * 2 * kBlockTop,
                    a.cand_idx + wid * 2 * kBlockTop);
 }
 
-template <bool SVR, int NBLK>
+template <bool SVR, int NBLK, int MODE>
 static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
                           hipEvent_t e0, hipEvent_t e1)
 {
-    size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
+    const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
     static size_t lds_allowed = 64 * 1024;
     if (lds > lds_allowed) {
         hipError_t e = hipFuncSetAttribute(
-            (const void*)k_rows<SVR, NBLK>,
+            (const void*)k_rows<SVR, NBLK, MODE>,
             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -445,11 +558,60 @@ static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
         lds_allowed = lds;
     }
     if (e0) {
-        hipExtLaunchKernelGGL(k_rows<SVR, NBLK>, dim3(nblocks),
+        hipExtLaunchKernelGGL(k_rows<SVR, NBLK, MODE>, dim3(nblocks),
                               dim3(kRowThreads), (uint32_t)lds, s, e0, e1, 0,
                               a);
     } else {
-        k_rows<SVR, NBLK><<<nblocks, kRowThreads, lds, s>>>(a);
+        k_rows<SVR, NBLK, MODE><<<nblocks, kRowThreads, lds, s>>>(a);
+    }
+}
+
+constexpr int kModeHot = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
+
+template <bool SVR, int NBLK>
+static void rows_mode(const RowArgs& a, int nblocks, hipStream_t s,
+                      hipEvent_t e0, hipEvent_t e1)
+{
+    switch (a.mode) {
+        case kModeHot:
+            rows_dispatch<SVR, NBLK, kModeHot>(a, nblocks, s, e0, e1);
+            break;
+        case RU_CAND:
+            rows_dispatch<SVR, NBLK, RU_CAND>(a, nblocks, s, e0, e1);
+            break;
+        case RU_ROWS:
+            rows_dispatch<SVR, NBLK, RU_ROWS>(a, nblocks, s, e0, e1);
+            break;
+        case RU_UPDATE:
+            rows_dispatch<SVR, NBLK, RU_UPDATE>(a, nblocks, s, e0, e1);
+            break;
+        default: throw Error{SVM_E_INTERNAL, "bad row kernel mode"};
+    }
+}
+
+template <bool SVR, int NBLK>
+static int rows_occupancy(size_t lds)
+{
+    int bpc = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &bpc, (const void*)k_rows<SVR, NBLK, kModeHot>, kRowThreads,
+            lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 1;
+    }
+    return bpc > 0 ? bpc : 1;
+}
+
+int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds)
+{
+    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
+        case 2: return rows_occupancy<false, 1>(lds);
+        case 3: return rows_occupancy<true, 1>(lds);
+        case 4: return rows_occupancy<false, 2>(lds);
+        case 5: return rows_occupancy<true, 2>(lds);
+        case 8: return rows_occupancy<false, 4>(lds);
+        case 9: return rows_occupancy<true, 4>(lds);
+        default: return 1;
     }
 }
 
@@ -457,13 +619,16 @@ void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
                  hipStream_t s, hipEvent_t e0, hipEvent_t e1)
 {
     if (nblocks <= 0) return;
+    // byte offsets inside one wave's rows must stay below 2^31
+    if ((int64_t)16 * a.tiles * a.ldp * 4 >= ((int64_t)1 << 31))
+        throw Error{SVM_E_UNSUPPORTED, "row group too large for the row kernel"};
     switch (nblk_cols * 2 + (svr ? 1 : 0)) {
-        case 2: rows_dispatch<false, 1>(a, nblocks, s, e0, e1); break;
-        case 3: rows_dispatch<true, 1>(a, nblocks, s, e0, e1); break;
-        case 4: rows_dispatch<false, 2>(a, nblocks, s, e0, e1); break;
-        case 5: rows_dispatch<true, 2>(a, nblocks, s, e0, e1); break;
-        case 8: rows_dispatch<false, 4>(a, nblocks, s, e0, e1); break;
-        case 9: rows_dispatch<true, 4>(a, nblocks, s, e0, e1); break;
+        case 2: rows_mode<false, 1>(a, nblocks, s, e0, e1); break;
+        case 3: rows_mode<true, 1>(a, nblocks, s, e0, e1); break;
+        case 4: rows_mode<false, 2>(a, nblocks, s, e0, e1); break;
+        case 5: rows_mode<true, 2>(a, nblocks, s, e0, e1); break;
+        case 8: rows_mode<false, 4>(a, nblocks, s, e0, e1); break;
+        case 9: rows_mode<true, 4>(a, nblocks, s, e0, e1); break;
         default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
     }
 }
@@ -523,6 +688,53 @@ __device__ __forceinline__ int lanes_below(unsigned long long m)
                                      __builtin_amdgcn_mbcnt_lo((unsigned)m, 0));
 }
 
+// Exact top-`half` over `count` entries produced by get(e, key, index), by
+// `half` block-wide rounds (each: the best entry after the previous winner).
+// All threads of the block take part; thread 0 writes ok/oi.
+template <class Get>
+__device__ void block_rounds(int64_t count, Get get, int half, double* ok,
+                             int32_t* oi, double (*rk)[kSelThreads / 64],
+                             int32_t (*ri)[kSelThreads / 64])
+{
+    constexpr int NW = kSelThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    double pk = INFINITY;
+    int32_t pi = -1;
+    for (int k = 0; k < half; ++k) {
+        double bk = -INFINITY;
+        int32_t bi = INT_MAX;
+        for (int64_t e = tid; e < count; e += kSelThreads) {
+            double key;
+            int32_t t;
+            get(e, key, t);
+            if (after(key, t, pk, pi) && better(key, t, bk, bi)) {
+                bk = key;
+                bi = t;
+            }
+        }
+        wave_best_fast(bk, bi);
+        if (lane == 0) {
+            rk[k & 1][wave] = bk;
+            ri[k & 1][wave] = bi;
+        }
+        __syncthreads();
+        bk = rk[k & 1][0];
+        bi = ri[k & 1][0];
+        for (int w = 1; w < NW; ++w)
+            if (better(rk[k & 1][w], ri[k & 1][w], bk, bi)) {
+                bk = rk[k & 1][w];
+                bi = ri[k & 1][w];
+            }
+        pk = bk;
+        pi = bi;
+        if (tid == 0) {
+            ok[k] = bk;
+            oi[k] = bi;
+        }
+    }
+    __syncthreads();
+}
+
 template <bool SVR, int NBLK>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 {
@@ -541,6 +753,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     __shared__ int32_t nsv[2];
     __shared__ int32_t exb[2][kMaxHalf];
     __shared__ int32_t nex[2];
+    __shared__ double keepk[kMaxHalf];
+    __shared__ int32_t keepi[kMaxHalf];
+    __shared__ int32_t nkeep;
     __shared__ double rk[2][NW];
     __shared__ int32_t ri[2][NW];
     __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
@@ -554,8 +769,6 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     const int half = a.half;
     const int64_t n = a.n, ldp = a.ldp;
     const bool given = (a.mode & SS_GIVEN_B) != 0;
-    // candidate lists come from row groups of 16 * tiles rows (one wave)
-    const int rshift = 4 + __builtin_ctz((unsigned)a.tiles);
 
     if (!given) {
         // (1) the per-group candidates
@@ -638,23 +851,40 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         }
         __syncthreads();
         const int M0 = nsv[0], M1 = nsv[1];
-        bool slow = M0 > kSurv || M1 > kSurv;
-        // (4) rank the survivors: side 0 on threads [0,512), side 1 on the rest
-        if (!slow) {
+        const bool overflow = M0 > kSurv || M1 > kSurv;
+        if (!overflow) {
+            // (4) rank the survivors: side 0 on threads [0,512), side 1 on
+            // the rest
             const int hs = kSelThreads / 2;
             if (tid < hs) rank_select(svk[0], svi[0], M0, half, upk, upi, tid, hs);
             else rank_select(svk[1], svi[1], M1, half, lok, loi, tid - hs, hs);
+            __syncthreads();
+        } else {
+            // (4') too many ties at the bound (e.g. alpha = 0): exact block
+            // rounds over all candidates
+            for (int side = 0; side < 2; ++side) {
+                auto get = [&](int64_t e, double& key, int32_t& t) {
+                    const int64_t blk = e / kBlockTop, k = e - blk * kBlockTop;
+                    const size_t o = (size_t)blk * 2 * kBlockTop +
+                                     (side ? kBlockTop : 0) + k;
+                    key = a.cand_key[o];
+                    t = a.cand_idx[o];
+                };
+                block_rounds(cnt, get, half, side ? lok : upk,
+                             side ? loi : upi, rk, ri);
+            }
+            if (tid == 0) ws->slow_selects += 1;
         }
-        __syncthreads();
-        // (5) blocks whose whole candidate list was taken may hold more:
-        // wave 0 finds them (lane-parallel)
-        if (!slow && wave == 0) {
+        // (5) row groups whose whole candidate list was taken may hold
+        // more: wave 0 finds them (lane-parallel)
+        const uint32_t grows = (uint32_t)a.group_rows;
+        if (wave == 0) {
             for (int side = 0; side < 2; ++side) {
                 const double* kk = side ? lok : upk;
                 const int32_t* ii = side ? loi : upi;
                 const bool valid = lane < half && kk[lane] != -INFINITY;
                 const int32_t b =
-                    valid ? (int32_t)(sample_of(SVR, ii[lane], n) >> rshift)
+                    valid ? (int32_t)((uint32_t)sample_of(SVR, ii[lane], n) / grows)
                           : -1 - lane;
                 int c = 0;
                 bool first = true;
@@ -670,95 +900,57 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             }
         }
         __syncthreads();
-        if (!slow && nex[0] + nex[1] > 0) {
-            // (6) rare: drop those blocks' candidates, add all their
-            // variables with keys recomputed from F, rank again
-            const int64_t R = 1LL << rshift;
-            const int NV = SVR ? 2 : 1;
+        if (nex[0] + nex[1] > 0) {
+            // (6) rare: exact block rounds over the winners outside those
+            // groups plus every variable of the groups (keys from F)
+            const uint32_t NV = SVR ? 2 : 1;
             for (int side = 0; side < 2; ++side) {
                 const int ne = nex[side];
                 if (ne == 0) continue;
-                const int M = side ? M1 : M0;
-                const int64_t per = R * NV;
-                if (M + ne * per > kSurv) {
-                    slow = true;
-                    break;
-                }
-                for (int e = tid; e < M; e += kSelThreads) {
-                    const int32_t b =
-                        (int32_t)(sample_of(SVR, svi[side][e], n) >> rshift);
-                    bool drop = false;
-                    for (int x = 0; x < ne; ++x) drop |= exb[side][x] == b;
-                    if (drop) svk[side][e] = -INFINITY;
-                }
-                for (int64_t q = tid; q < ne * per; q += kSelThreads) {
-                    const int x = (int)(q / per);
-                    const int64_t o = q - (int64_t)x * per;
-                    const int64_t row = ((int64_t)exb[side][x] << rshift) + (o % R);
-                    double u = -INFINITY, l = -INFINITY;
-                    int32_t tt = INT_MAX;
-                    if (row < n) {
-                        tt = (int32_t)(o < R ? row : n + row);
-                        var_scores<SVR>(a, tt, u, l);
+                double* kk = side ? lok : upk;
+                int32_t* ii = side ? loi : upi;
+                if (tid == 0) {
+                    int c = 0;
+                    for (int k = 0; k < half; ++k) {
+                        if (kk[k] == -INFINITY) continue;
+                        const int32_t b =
+                            (int32_t)((uint32_t)sample_of(SVR, ii[k], n) / grows);
+                        bool ex = false;
+                        for (int x = 0; x < ne; ++x) ex |= exb[side][x] == b;
+                        if (!ex) {
+                            keepk[c] = kk[k];
+                            keepi[c] = ii[k];
+                            ++c;
+                        }
                     }
-                    svk[side][M + q] = side ? l : u;
-                    svi[side][M + q] = tt;
+                    nkeep = c;
                 }
                 __syncthreads();
-                if (tid < half) {
-                    if (side) { lok[tid] = -INFINITY; loi[tid] = INT_MAX; }
-                    else { upk[tid] = -INFINITY; upi[tid] = INT_MAX; }
-                }
-                __syncthreads();
-                rank_select(svk[side], svi[side], (int)(M + ne * per), half,
-                            side ? lok : upk, side ? loi : upi, tid,
-                            kSelThreads);
-                __syncthreads();
+                const int nk = nkeep;
+                const uint32_t per = grows * NV;
+                auto get = [&](int64_t e, double& key, int32_t& t) {
+                    if (e < nk) {
+                        key = keepk[e];
+                        t = keepi[e];
+                        return;
+                    }
+                    const uint32_t q = (uint32_t)(e - nk);
+                    const uint32_t x = q / per, o = q - x * per;
+                    const int64_t row = (int64_t)exb[side][x] * grows + (o % grows);
+                    key = -INFINITY;
+                    t = INT_MAX;
+                    if (row < n) {
+                        const int64_t tt = o < grows ? row : n + row;
+                        double u, l;
+                        var_scores<SVR>(a, tt, u, l);
+                        key = side ? l : u;
+                        t = (int32_t)tt;
+                    }
+                };
+                block_rounds((int64_t)nk + (int64_t)ne * per, get, half, kk, ii,
+                             rk, ri);
             }
             if (tid == 0) ws->rescans += 1;
-        }
-        if (slow) {
-            // (7) fallback: exact rounds over every variable's key
-            const int64_t N = SVR ? 2 * n : n;
-            for (int side = 0; side < 2; ++side) {
-                double pk = INFINITY;
-                int32_t pi = -1;
-                for (int k = 0; k < half; ++k) {
-                    double bk = -INFINITY;
-                    int32_t bi = INT_MAX;
-                    for (int64_t t = tid; t < N; t += kSelThreads) {
-                        double u, l;
-                        var_scores<SVR>(a, t, u, l);
-                        const double key = side ? l : u;
-                        if (after(key, (int32_t)t, pk, pi) &&
-                            better(key, (int32_t)t, bk, bi)) {
-                            bk = key;
-                            bi = (int32_t)t;
-                        }
-                    }
-                    wave_best_fast(bk, bi);
-                    if (lane == 0) {
-                        rk[k & 1][wave] = bk;
-                        ri[k & 1][wave] = bi;
-                    }
-                    __syncthreads();
-                    bk = rk[k & 1][0];
-                    bi = ri[k & 1][0];
-                    for (int w = 1; w < NW; ++w)
-                        if (better(rk[k & 1][w], ri[k & 1][w], bk, bi)) {
-                            bk = rk[k & 1][w];
-                            bi = ri[k & 1][w];
-                        }
-                    pk = bk;
-                    pi = bi;
-                    if (tid == 0) {
-                        if (side) { lok[k] = bk; loi[k] = bi; }
-                        else { upk[k] = bk; upi[k] = bi; }
-                    }
-                }
-            }
-            if (tid == 0) ws->slow_selects += 1;
-            __syncthreads();
         }
     }
     const uint64_t t_merge = wall_clock64();

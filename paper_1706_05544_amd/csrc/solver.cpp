@@ -101,23 +101,42 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     gexp_ = (float)(o.gamma * 1.4426950408889634);
     half_ = o.q / 2;
     nblk_cols_ = o.q <= 16 ? 1 : (o.q <= 32 ? 2 : 4);
-    tiles_ = 2;
-    if (const char* e = getenv("SVM_TILES")) {  // tuning: a power of two
-        const int v = std::max(1, std::min(64, atoi(e)));
-        tiles_ = 1;
-        while (tiles_ * 2 <= v) tiles_ *= 2;
-    }
-    const int64_t cap = (int64_t)kSelThreads * kSelPerThread;
+    // Grid: every wave of k_rows resident at once (occupancy from the
+    // runtime), each wave owning `tiles_` consecutive 16-row tiles.
     constexpr int kWaves = kRowThreads / 64;
-    while (((n_ + 64LL * tiles_ - 1) / (64LL * tiles_)) * kWaves * kBlockTop >
-           cap)
-        tiles_ *= 2;
-    nb_ = (int)((n_ + 64LL * tiles_ - 1) / (64LL * tiles_));
-    ncand_ = nb_ * kWaves;
-    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, o.type == SVM_EPS_SVR) >
-        160 * 1024)
+    const bool svr = o.type == SVM_EPS_SVR;
+    constexpr size_t kLdsMax = 160 * 1024;
+    if (rows_lds_bytes(nblk_cols_, f.ldp, 1, svr) > kLdsMax)
         throw Error{SVM_E_UNSUPPORTED,
                     "too many features for the dense row kernel's LDS tile"};
+    int cus = 0;
+    HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
+                                  cx.device));
+    const int64_t tiles_total = (n_ + 15) / 16;
+    // The LDS of a block grows with the tiles per wave (row data is staged),
+    // and the resident blocks shrink with the LDS: iterate to a fixed point
+    // (tiles only grow, so this ends).
+    tiles_ = 1;
+    for (int it = 0; it < 8; ++it) {
+        const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr);
+        const int64_t cap =
+            (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds) * kWaves;
+        const int t = (int)std::max<int64_t>(1, (tiles_total + cap - 1) / cap);
+        if (t <= tiles_) break;
+        tiles_ = t;
+    }
+    if (const char* e = getenv("SVM_TILES"))  // tuning override
+        tiles_ = std::max(1, std::min(4096, atoi(e)));
+    const int64_t cand_cap = (int64_t)kSelThreads * kSelPerThread;
+    while (((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_)) * kWaves *
+               kBlockTop > cand_cap)
+        ++tiles_;
+    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr) > kLdsMax ||
+        (int64_t)16 * tiles_ * f.ldp * 4 >= ((int64_t)1 << 31))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "training set too large for the dense row kernel"};
+    nb_ = (int)((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_));
+    ncand_ = nb_ * kWaves;
 
     F_.alloc((size_t)n_);
     alpha_.alloc((size_t)N_);
@@ -230,7 +249,7 @@ void Solver::launch_solve(int32_t mode)
     a.max_inner = o_.max_inner;
     a.max_iter = o_.max_iter;
     a.mode = mode;
-    a.tiles = tiles_;
+    a.group_rows = 16 * tiles_;
     launch_select(a, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
 }
 
@@ -572,7 +591,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.max_inner = max_inner;
     a.max_iter = o_.max_iter;
     a.half = half_;
-    a.tiles = tiles_;
+    a.group_rows = 16 * tiles_;
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_NO_WRITE;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
@@ -615,7 +634,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.max_inner = 0;
     a.max_iter = o_.max_iter;
     a.half = half_;
-    a.tiles = tiles_;
+    a.group_rows = 16 * tiles_;
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_SET_ALPHA;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
