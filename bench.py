@@ -43,7 +43,7 @@ def row_bytes_per_launch(n: int, d: int, svr: bool) -> int:
     return n * per
 
 
-KERNEL_SOURCES = ("paper_1706_05544_amd/csrc/kernels.hip",
+KERNEL_SOURCES = ("paper_1706_05544_amd/csrc/rows.hip",
                   "paper_1706_05544_amd/csrc/device.hpp",
                   "paper_1706_05544_amd/csrc/common.hpp")
 

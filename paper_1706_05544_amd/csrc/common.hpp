@@ -26,6 +26,8 @@ constexpr int kRowThreads = 256;   // row/update kernel: 4 waves
 constexpr int kSelThreads = 1024;  // select/solve kernel: one block
 constexpr int kSelPerThread = 16;  // candidates per side held per thread
 constexpr int kBlockTop = 2;       // candidates per side kept per row group
+constexpr int kListCap = 1024;     // threshold list entries per side
+constexpr int kWaveList = 16;      // threshold list entries per side per wave
 constexpr double kTau = 1e-12;     // curvature floor of a degenerate pair
 
 // state byte of a dual variable
@@ -54,7 +56,10 @@ struct WorkingSet {
     int64_t inner_total;  // inner steps summed over iterations
     int64_t rescans;      // iterations that rescanned exhausted blocks
     int64_t slow_selects; // iterations that fell back to a full scan
-    int64_t prof[8];      // select/solve phase times (wall-clock ticks)
+    int64_t list_hits;    // iterations selected from the threshold list
+    double theta[2];      // list thresholds for the next row kernel (up, low)
+    double spread[2];     // distance of each threshold below the q/2-th key
+    int64_t prof[12];     // select/solve phase times (wall-clock ticks)
 };
 
 // Final reductions of a state (bias and objective).
@@ -93,6 +98,9 @@ struct RowArgs {
     double* cand_key;     // [nb][2][half]: up scores v, low scores -v
     int32_t* cand_idx;
     float* rows_out;      // nS x n (tests)
+    double* list_key;     // [2][kListCap] keys at or above ws->theta
+    int32_t* list_idx;
+    int32_t* list_cnt;    // [2] entries appended (> kListCap: overflow)
     int64_t n, ldp;
     double eps;
     float gexp;           // gamma * log2(e)
@@ -105,6 +113,9 @@ struct RowArgs {
 struct SelArgs {
     const double* cand_key;
     const int32_t* cand_idx;
+    const double* list_key;  // threshold list of the previous row kernel
+    const int32_t* list_idx;
+    int32_t* list_cnt;       // read, then cleared (nullptr: no list)
     int32_t nb, half;     // nb: candidate lists (one per k_rows wave)
     WorkingSet* ws;
     double* alpha;
@@ -123,6 +134,7 @@ struct SelArgs {
     int64_t max_iter;
     int32_t mode;
     int32_t group_rows;   // rows behind one candidate list (one k_rows wave)
+    int32_t slice;        // features per LDS slice of the working-set rows
 };
 
 struct PredictArgs {

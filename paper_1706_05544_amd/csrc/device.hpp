@@ -132,6 +132,16 @@ __device__ __forceinline__ double row_sum_f64(double v)
     return v;
 }
 
+// every lane of each 16-lane row receives the row sum
+__device__ __forceinline__ int row_sum_i32(int v)
+{
+    v += dpp_i32<kDppRor8>(v);
+    v += dpp_i32<kDppRor4>(v);
+    v += dpp_i32<kDppRor2>(v);
+    v += dpp_i32<kDppRor1>(v);
+    return v;
+}
+
 // Best (key, index) of a 16-lane row, in the order of better(); every lane
 // of the row receives its row's result.
 __device__ __forceinline__ void row_best(double& k, int32_t& i)
@@ -172,6 +182,13 @@ __device__ __forceinline__ void wave_best_pair(double& k0, int32_t& i0,
     i0 = c0;
     k1 = M1;
     i1 = c1;
+}
+
+// number of set bits of m below this lane
+__device__ __forceinline__ int lanes_below(unsigned long long m)
+{
+    return __builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((unsigned)m, 0));
 }
 
 __device__ __forceinline__ float4 ld4(const float* p)

@@ -1,0 +1,522 @@
+// Row/update kernel of the working-set dual solve (gfx950).
+//
+// k_rows runs on the whole grid once per outer iteration (Section 3: the
+// responses are updated after the working set has been optimised).  It
+// streams X once: for each 16-row tile, the dot products with the (at most
+// 16 per column block) working-set samples on the matrix cores (16x16x4
+// fp32), the RBF epilogue, F_i += sum_s dc_s K(x_i, x_s) in fp64, the keys v
+// of the variables of the tile and per-wave candidates of each side for the
+// next selection.
+#include <hip/hip_ext.h>
+
+#include "common.hpp"
+#include "device.hpp"
+
+namespace msvm {
+
+// ---------------------------------------------------------------------------
+// row / update kernel
+// ---------------------------------------------------------------------------
+
+
+// LDS row stride of the per-wave feature slab buffer (64 columns + pad)
+constexpr int kSlabStride = 68;
+// feature slabs in flight per wave of k_rows
+constexpr int kRing = 4;
+constexpr int kRowWaves = kRowThreads / 64;
+
+// LDS row stride of a staged working-set sample: ldp rounded up to whole
+// 16-feature chunks (zero-filled) plus a pad of 4 against bank conflicts.
+__host__ __device__ inline int rows_xs_stride(int64_t ldp)
+{
+    return (int)(((ldp + 15) & ~(int64_t)15) + 4);
+}
+
+// Per-wave LDS bytes for the row data of 16 * tiles rows: F (fp64), the
+// squared norm, for eps-SVR the target, and the state byte of each copy.
+__host__ __device__ inline int rows_aux_bytes(int tiles, bool svr)
+{
+    return ((16 * tiles * (svr ? 18 : 13)) + 15) & ~15;
+}
+
+__host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp)
+{
+    return (size_t)nblk_cols * 16 * rows_xs_stride(ldp) * sizeof(float) +
+           (size_t)kRowWaves * 16 * kSlabStride * sizeof(float);
+}
+
+// per-wave threshold list: kWaveList (key, index) pairs per side
+constexpr int kWaveListBytes = 2 * kWaveList * (8 + 4);
+
+size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
+{
+    return rows_aux_offset(nblk_cols, ldp) +
+           (size_t)kRowWaves * (rows_aux_bytes(tiles, svr) + kWaveListBytes);
+}
+
+// Running best two (score, variable) of one lane, in the order of better().
+struct Top2 {
+    double k1 = -INFINITY, k2 = -INFINITY;
+    int32_t i1 = INT_MAX, i2 = INT_MAX;
+    __device__ __forceinline__ void push(double k, int32_t i)
+    {
+        if (better(k, i, k1, i1)) {
+            k2 = k1;
+            i2 = i1;
+            k1 = k;
+            i1 = i;
+        } else if (better(k, i, k2, i2)) {
+            k2 = k;
+            i2 = i;
+        }
+    }
+};
+
+// Both sides at once (independent chains interleave): writes the wave's best
+// two up scores to ok[0..1] and best two low scores to ok[2..3].
+__device__ __forceinline__ void wave_top2_pair(Top2 u, Top2 l, double* ok,
+                                               int32_t* oi)
+{
+    double ku = u.k1, kl = l.k1;
+    int32_t iu = u.i1, il = l.i1;
+    wave_best_pair(ku, iu, kl, il);
+    const bool mu = u.i1 == iu && u.k1 == ku;
+    const bool ml = l.i1 == il && l.k1 == kl;
+    double ku2 = mu ? u.k2 : u.k1, kl2 = ml ? l.k2 : l.k1;
+    int32_t iu2 = mu ? u.i2 : u.i1, il2 = ml ? l.i2 : l.i1;
+    wave_best_pair(ku2, iu2, kl2, il2);
+    if ((threadIdx.x & 63) == 0) {
+        ok[0] = ku;
+        oi[0] = iu;
+        ok[1] = ku2;
+        oi[1] = iu2;
+        ok[2] = kl;
+        oi[2] = il;
+        ok[3] = kl2;
+        oi[3] = il2;
+    }
+}
+
+// Row/update kernel.  Each wave owns 16 * tiles consecutive rows.
+//
+// Its row data (F, norms, state bytes, targets) is read once into a
+// wave-private LDS area, updated there and F is written back, coalesced, at
+// the end: the feature stream is then the only global traffic in the main
+// loop, and every load in it is unconditional (buffer range checks give the
+// zeros of ragged tails), so the loads stay in flight across slabs.
+//
+// Features go through 64-column slabs: the global loads are row-contiguous
+// (16 lanes cover 256 B of one row, 4 rows per instruction) and run kRing
+// slabs ahead; each slab passes through a wave-private LDS buffer and is read
+// back in the matrix-core operand layout (lane (g, nl): row nl, columns
+// 16c + 4g .. +3 of chunk c), which is the library-wide chunk order, so every
+// K value matches the other kernels bitwise.
+template <bool SVR, int NBLK, int MODE>
+__global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
+{
+    constexpr bool UPD = (MODE & RU_UPDATE) != 0;
+    constexpr bool ROWS = (MODE & RU_ROWS) != 0;
+    constexpr bool CAND = (MODE & RU_CAND) != 0;
+    constexpr bool XS = UPD || ROWS;  // the working-set samples are needed
+    // hot mode: also list every variable whose key reaches the threshold
+    // of its side (the selection then ranks that short list only)
+    constexpr bool LIST = UPD && CAND;
+    constexpr int kXsEarly = 2;       // staging loads issued with the stream
+    extern __shared__ __align__(16) unsigned char smem[];
+    const WorkingSet* ws = a.ws;
+    if ((MODE & RU_CHECK_DONE) && ws->done) return;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform by construction; said so, so that the buffer resources
+    // built from it live in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, nl = lane & 15;
+    const int T = a.tiles, RW = 16 * T;
+    const int64_t n = a.n;
+    const int ldp = (int)a.ldp;
+    const int xstride = rows_xs_stride(ldp);
+    float* xsl = reinterpret_cast<float*>(smem);
+
+    // working-set slot b * 16 + nl of this lane (slots past nS contribute 0)
+    const int nS = XS ? (a.nS_override >= 0 ? a.nS_override : ws->nS) : 0;
+    double cf[NBLK];
+    float ssl[NBLK];
+    int32_t sidx[NBLK];
+#pragma unroll
+    for (int b = 0; b < NBLK; ++b) {
+        const int slot = b * 16 + nl;  // < kMaxQ: always inside the arrays
+        const bool ok = slot < nS;
+        const double c = ws->coef[slot];
+        const float s = ws->sS[slot];
+        const int32_t i = ws->S[slot];
+        cf[b] = (ok && UPD) ? c : 0.0;
+        ssl[b] = ok ? s : 0.0f;
+        sidx[b] = ok ? i : -1;
+    }
+
+    // rows of this wave: rw0 .. rw0 + nw - 1, in Tw tiles of 16
+    const int64_t rw0 = ((int64_t)blockIdx.x * kRowWaves + wave) * RW;
+    const int nw = rw0 >= n ? 0 : (int)min((int64_t)RW, n - rw0);
+    const int Tw = (nw + 15) >> 4;
+    unsigned char* aux =
+        smem + rows_aux_offset(NBLK, ldp) + wave * rows_aux_bytes(T, SVR);
+    double* Fw = reinterpret_cast<double*>(aux);
+    float* sqw = reinterpret_cast<float*>(aux + 8 * RW);
+    float* zw = reinterpret_cast<float*>(aux + 12 * RW);
+    uint8_t* stw = aux + (SVR ? 16 : 12) * RW;  // copy (i,-) at stw[RW + r]
+    unsigned char* wl = smem + rows_aux_offset(NBLK, ldp) +
+                        kRowWaves * rows_aux_bytes(T, SVR) +
+                        wave * kWaveListBytes;
+    double* wlk = reinterpret_cast<double*>(wl);              // [2][kWaveList]
+    int32_t* wli = reinterpret_cast<int32_t*>(wl + 16 * kWaveList);
+    double th[2] = {INFINITY, INFINITY};
+    if (LIST) {
+        th[0] = ws->theta[0];
+        th[1] = ws->theta[1];
+    }
+    int nlist[2] = {0, 0};  // wave-uniform entry counts
+
+    // row data of rows k0 .. k0 + 255 of the wave: issue, then store to LDS
+    struct AuxRegs {
+        double f[4];
+        float q[4], z[4];
+        uint8_t s0[4], s1[4];
+    };
+    const Rsrc rF = make_rsrc(a.F + rw0, (int64_t)nw * 8);
+    auto aux_issue = [&](int k0, AuxRegs& x) {
+        const Rsrc rQ = make_rsrc(a.sq + rw0, (int64_t)nw * 4);
+        const Rsrc rS0 = make_rsrc(a.st + rw0, nw);
+        const Rsrc rS1 = make_rsrc(a.st + n + rw0, SVR ? nw : 0);
+        const Rsrc rZ = make_rsrc(a.z + rw0, SVR ? (int64_t)nw * 4 : 0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t r = (uint32_t)(k0 + 64 * j + lane);
+            x.f[j] = (UPD || CAND) ? bld_f64(rF, 8 * r) : 0.0;
+            x.q[j] = XS ? bld_f32(rQ, 4 * r) : 0.0f;
+            x.s0[j] = CAND ? bld_u8(rS0, r) : 0;
+            x.s1[j] = (SVR && CAND) ? bld_u8(rS1, r) : 0;
+            x.z[j] = (SVR && CAND) ? bld_f32(rZ, 4 * r) : 0.0f;
+        }
+    };
+    auto aux_store = [&](int k0, const AuxRegs& x) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = k0 + 64 * j + lane;
+            if (r < RW) {
+                Fw[r] = x.f[j];
+                sqw[r] = x.q[j];
+                stw[r] = x.s0[j];
+                if (SVR) {
+                    stw[RW + r] = x.s1[j];
+                    zw[r] = x.z[j];
+                }
+            }
+        }
+    };
+
+    Top2 up, lo;  // this lane's best candidates of each side
+    // (called by the whole wave) appends the passing lanes' entries
+    auto append = [&](int side, bool pass, double key, int32_t idx) {
+        const unsigned long long m = __ballot(pass);
+        if (m == 0) return;
+        const int pos = nlist[side] + lanes_below(m);
+        if (pass && pos < kWaveList) {
+            wlk[side * kWaveList + pos] = key;
+            wli[side * kWaveList + pos] = idx;
+        }
+        nlist[side] += __popcll(m);
+    };
+    // keys of the variables of row lr (only lanes with own = true hold one)
+    auto push = [&](int lr, double Fn, bool own) {
+        const int32_t row = (int32_t)(rw0 + lr);
+        const uint8_t s0 = stw[lr];
+        const double r0 = SVR ? (double)zw[lr] - a.eps
+                              : ((s0 & ST_YPOS) ? 1.0 : -1.0);
+        const double v0 = r0 - Fn;
+        const bool u0 = own && (s0 & ST_UP), l0 = own && (s0 & ST_LOW);
+        if (u0) up.push(v0, row);
+        if (l0) lo.push(-v0, row);
+        if (LIST) {
+            append(0, u0 && v0 >= th[0], v0, row);
+            append(1, l0 && -v0 >= th[1], -v0, row);
+        }
+        if (SVR) {
+            const uint8_t s1 = stw[RW + lr];
+            const double v1 = ((double)zw[lr] + a.eps) - Fn;
+            const bool u1 = own && (s1 & ST_UP), l1 = own && (s1 & ST_LOW);
+            if (u1) up.push(v1, (int32_t)(n + row));
+            if (l1) lo.push(-v1, (int32_t)(n + row));
+            if (LIST) {
+                append(0, u1 && v1 >= th[0], v1, (int32_t)(n + row));
+                append(1, l1 && -v1 >= th[1], -v1, (int32_t)(n + row));
+            }
+        }
+    };
+
+    if (XS) {
+        // Staged working-set rows: every slot (finite values past nS),
+        // zero-filled to whole 16-feature chunks.
+        const int q4 = (xstride - 4) >> 2;  // float4 per staged row
+        const int xs_total = NBLK * 16 * q4;
+        const Rsrc rXs = make_rsrc(a.xS, (int64_t)NBLK * 16 * ldp * 4);
+        auto xs_off = [&](int e) -> uint32_t {
+            const int slot = e / q4, c4 = e - slot * q4;
+            return (e < xs_total && 4 * c4 < ldp)
+                       ? (uint32_t)((slot * ldp + 4 * c4) * 4)
+                       : kOob;
+        };
+        auto xs_put = [&](int e, float4 v) {
+            const int slot = e / q4, c4 = e - slot * q4;
+            if (e < xs_total)
+                *reinterpret_cast<float4*>(xsl + slot * xstride + 4 * c4) = v;
+        };
+
+        const int nslab = (ldp + 63) >> 6;
+        const Rsrc rX = make_rsrc(a.X + rw0 * ldp, (int64_t)nw * ldp * 4);
+        float* wbuf = xsl + NBLK * 16 * xstride + wave * (16 * kSlabStride);
+        const uint32_t step4 = (uint32_t)(16 * ldp);  // 4 rows, in bytes
+        int fti = 0, fsl = 0;  // next slab to fetch
+        auto fetch = [&](float4 (&v)[4]) {
+            const int col = fsl * 64 + 4 * nl;
+            const bool ok = fti < Tw && col < ldp;
+            const uint32_t o = (uint32_t)(((16 * fti + g) * ldp + col) * 4);
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                v[rr] = bld_f4(rX, ok ? o + rr * step4 : kOob);
+            if (++fsl == nslab) {
+                fsl = 0;
+                ++fti;
+            }
+        };
+
+        // Everything the first slabs need is requested at once: the first
+        // staging loads, the row data and kRing feature slabs.
+        float4 xv[kXsEarly];
+#pragma unroll
+        for (int i = 0; i < kXsEarly; ++i)
+            xv[i] = bld_f4(rXs, xs_off(tid + i * kRowThreads));
+        AuxRegs ar;
+        aux_issue(0, ar);
+        float4 ring[kRing][4];
+#pragma unroll
+        for (int j = 0; j < kRing; ++j) fetch(ring[j]);
+#pragma unroll
+        for (int i = 0; i < kXsEarly; ++i) xs_put(tid + i * kRowThreads, xv[i]);
+        aux_store(0, ar);
+        for (int k0 = 256; k0 < RW; k0 += 256) {
+            aux_issue(k0, ar);
+            aux_store(k0, ar);
+        }
+        for (int e = tid + kXsEarly * kRowThreads; e < xs_total;
+             e += kRowThreads)
+            xs_put(e, bld_f4(rXs, xs_off(e)));
+        __syncthreads();
+
+        floatx4 acc[NBLK];
+        auto epilogue = [&](int ti) {
+            const int lr = 16 * ti + 4 * g;
+            const float4 q4v = *reinterpret_cast<const float4*>(sqw + lr);
+            const float qv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
+            double part[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+            for (int b = 0; b < NBLK; ++b) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    float kv = rbf_from_dot(qv[v], ssl[b], acc[b][v], a.gexp);
+                    if (rw0 + lr + v == (int64_t)sidx[b]) kv = 1.0f;
+                    part[v] = fma(cf[b], (double)kv, part[v]);
+                    if (ROWS && b * 16 + nl < nS && lr + v < nw)
+                        a.rows_out[(int64_t)(b * 16 + nl) * n + rw0 + lr + v] =
+                            kv;
+                }
+            }
+            const int orl = lr + (nl & 3);  // row owned by lanes nl < 4
+            double Fn = 0.0;
+            if (UPD || CAND) Fn = Fw[orl];
+            if (UPD) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) part[v] = row_sum_f64(part[v]);
+                Fn += pick4(part, nl & 3);
+                if (nl < 4) Fw[orl] = Fn;
+            }
+            if (CAND) push(orl, Fn, nl < 4 && orl < nw);
+        };
+
+        int pti = 0, psl = 0;  // slab being processed
+        for (int s0 = 0; s0 < Tw * nslab; s0 += kRing) {
+            // all kRing slots every trip (slabs past the end are zeros and
+            // touch no memory), so the loads in flight are countable
+#pragma unroll
+            for (int j = 0; j < kRing; ++j) {
+                if (psl == 0) {
+#pragma unroll
+                    for (int b = 0; b < NBLK; ++b)
+                        acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+                }
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    *reinterpret_cast<float4*>(
+                        wbuf + (4 * rr + g) * kSlabStride + 4 * nl) =
+                        ring[j][rr];
+                fetch(ring[j]);  // refill the slot kRing slabs ahead
+                __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int ch = psl * 4 + c;
+                    if (ch * 16 < ldp) {  // chunk present (uniform)
+                        const float4 av =
+                            ld4(wbuf + nl * kSlabStride + c * 16 + 4 * g);
+#pragma unroll
+                        for (int b = 0; b < NBLK; ++b) {
+                            const float4 bv = ld4(xsl + (b * 16 + nl) * xstride +
+                                                  ch * 16 + 4 * g);
+                            acc[b] = mfma_chunk(acc[b], av, bv);
+                        }
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
+                if (psl == nslab - 1 && pti < Tw) epilogue(pti);
+                if (++psl == nslab) {
+                    psl = 0;
+                    ++pti;
+                }
+            }
+        }
+        if (UPD)
+            for (int r = lane; r < nw; r += 64) bst_f64(rF, 8 * r, Fw[r]);
+    } else if (CAND) {
+        AuxRegs ar;
+        for (int k0 = 0; k0 < RW; k0 += 256) {
+            aux_issue(k0, ar);
+            aux_store(k0, ar);
+        }
+        for (int ti = 0; ti < Tw; ++ti) {
+            const int orl = 16 * ti + 4 * g + (nl & 3);
+            push(orl, Fw[orl], nl < 4 && orl < nw);
+        }
+    }
+
+    if (LIST) {
+        // reserve room in the global list (a wave that saw more entries
+        // than it keeps pushes the count past the capacity: overflow)
+#pragma unroll
+        for (int side = 0; side < 2; ++side) {
+            const int c = nlist[side];
+            if (c == 0) continue;
+            int base = 0;
+            if (lane == 0)
+                base = atomicAdd(a.list_cnt + side,
+                                 c > kWaveList ? kListCap + 1 : c);
+            base = __builtin_amdgcn_readfirstlane(base);
+            if (c <= kWaveList && lane < c && base + lane < kListCap) {
+                a.list_key[side * kListCap + base + lane] =
+                    wlk[side * kWaveList + lane];
+                a.list_idx[side * kListCap + base + lane] =
+                    wli[side * kWaveList + lane];
+            }
+        }
+    }
+
+    if (!CAND) return;
+    // the best two of each side over this wave's rows; a variable outside
+    // the global top q/2 never needs more (k_select rescans a row group
+    // whose two candidates were both taken)
+    const size_t wid = (size_t)blockIdx.x * kRowWaves + wave;
+    wave_top2_pair(up, lo, a.cand_key + wid * 2 * kBlockTop,
+                   a.cand_idx + wid * 2 * kBlockTop);
+}
+
+template <bool SVR, int NBLK, int MODE>
+static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
+                          hipEvent_t e0, hipEvent_t e1)
+{
+    const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
+    static size_t lds_allowed = 64 * 1024;
+    if (lds > lds_allowed) {
+        hipError_t e = hipFuncSetAttribute(
+            (const void*)k_rows<SVR, NBLK, MODE>,
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            throw Error{SVM_E_UNSUPPORTED,
+                        "row tile needs more LDS than the device allows"};
+        }
+        lds_allowed = lds;
+    }
+    if (e0) {
+        hipExtLaunchKernelGGL(k_rows<SVR, NBLK, MODE>, dim3(nblocks),
+                              dim3(kRowThreads), (uint32_t)lds, s, e0, e1, 0,
+                              a);
+    } else {
+        k_rows<SVR, NBLK, MODE><<<nblocks, kRowThreads, lds, s>>>(a);
+    }
+}
+
+constexpr int kModeHot = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
+
+template <bool SVR, int NBLK>
+static void rows_mode(const RowArgs& a, int nblocks, hipStream_t s,
+                      hipEvent_t e0, hipEvent_t e1)
+{
+    switch (a.mode) {
+        case kModeHot:
+            rows_dispatch<SVR, NBLK, kModeHot>(a, nblocks, s, e0, e1);
+            break;
+        case RU_CAND:
+            rows_dispatch<SVR, NBLK, RU_CAND>(a, nblocks, s, e0, e1);
+            break;
+        case RU_ROWS:
+            rows_dispatch<SVR, NBLK, RU_ROWS>(a, nblocks, s, e0, e1);
+            break;
+        case RU_UPDATE:
+            rows_dispatch<SVR, NBLK, RU_UPDATE>(a, nblocks, s, e0, e1);
+            break;
+        default: throw Error{SVM_E_INTERNAL, "bad row kernel mode"};
+    }
+}
+
+template <bool SVR, int NBLK>
+static int rows_occupancy(size_t lds)
+{
+    int bpc = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &bpc, (const void*)k_rows<SVR, NBLK, kModeHot>, kRowThreads,
+            lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 1;
+    }
+    return bpc > 0 ? bpc : 1;
+}
+
+int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds)
+{
+    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
+        case 2: return rows_occupancy<false, 1>(lds);
+        case 3: return rows_occupancy<true, 1>(lds);
+        case 4: return rows_occupancy<false, 2>(lds);
+        case 5: return rows_occupancy<true, 2>(lds);
+        case 8: return rows_occupancy<false, 4>(lds);
+        case 9: return rows_occupancy<true, 4>(lds);
+        default: return 1;
+    }
+}
+
+void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
+                 hipStream_t s, hipEvent_t e0, hipEvent_t e1)
+{
+    if (nblocks <= 0) return;
+    // byte offsets inside one wave's rows must stay below 2^31
+    if ((int64_t)16 * a.tiles * a.ldp * 4 >= ((int64_t)1 << 31))
+        throw Error{SVM_E_UNSUPPORTED, "row group too large for the row kernel"};
+    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
+        case 2: rows_mode<false, 1>(a, nblocks, s, e0, e1); break;
+        case 3: rows_mode<true, 1>(a, nblocks, s, e0, e1); break;
+        case 4: rows_mode<false, 2>(a, nblocks, s, e0, e1); break;
+        case 5: rows_mode<true, 2>(a, nblocks, s, e0, e1); break;
+        case 8: rows_mode<false, 4>(a, nblocks, s, e0, e1); break;
+        case 9: rows_mode<true, 4>(a, nblocks, s, e0, e1); break;
+        default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
+    }
+}
+
+}  // namespace msvm

@@ -1,0 +1,965 @@
+// Select/solve kernel of the working-set dual solve (gfx950).
+//
+// k_select is one block of 1024 threads per outer iteration (Section 3: pick
+// a working set of 16 coefficients by the largest partial derivatives under
+// the constraints and optimise them from the local gradient).  It merges the
+// per-wave candidates of the previous k_rows into the global working set B
+// (the q/2 largest keys of I_up interleaved with the q/2 smallest keys of
+// I_low), tests the gap m - M against tol, computes the kernel block K_BB on
+// the matrix cores and solves the subproblem on B with maximal-violating-pair
+// steps.  It writes the new alpha_B, the state bytes, the coefficient change
+// of each distinct sample and the working-set rows for the next k_rows.
+#include <hip/hip_ext.h>
+
+#include <algorithm>
+
+#include "common.hpp"
+#include "device.hpp"
+
+namespace msvm {
+
+// ---------------------------------------------------------------------------
+// select / solve kernel
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int64_t sample_of(bool svr, int64_t t, int64_t n)
+{
+    return (svr && t >= n) ? t - n : t;
+}
+
+// Scores of variable t on both sides, recomputed from the responses exactly
+// as k_rows computes them: up = v (t in I_up), low = -v (t in I_low).
+template <bool SVR>
+__device__ __forceinline__ void var_scores(const SelArgs& a, int64_t t,
+                                           double& up, double& lo)
+{
+    const int64_t n = a.n;
+    const int64_t sm = sample_of(SVR, t, n);
+    const uint8_t s = a.st[t];
+    double r;
+    if (SVR) r = t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps;
+    else r = (s & ST_YPOS) ? 1.0 : -1.0;
+    const double v = r - a.F[sm];
+    up = (s & ST_UP) ? v : -INFINITY;
+    lo = (s & ST_LOW) ? -v : -INFINITY;
+}
+
+// Survivor-list capacity per side of the threshold filter in k_select.
+constexpr int kSurv = 1024;
+
+// Top `half` of (k[0..M), i[0..M)) in the order of better(), by `half`
+// rounds over one wave (entries are distinct (key, index) pairs); lane 0
+// writes ok/oi.  The first 256 entries are held in registers.
+__device__ void wave_top(const double* k, const int32_t* i, int M, int half,
+                         double* ok, int32_t* oi)
+{
+    const int lane = threadIdx.x & 63;
+    double ck[4];
+    int32_t ci[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int e = lane + 64 * j;
+        ck[j] = e < M ? k[e] : -INFINITY;
+        ci[j] = e < M ? i[e] : INT_MAX;
+    }
+    double pk = INFINITY;
+    int32_t pi = -1;
+    for (int r = 0; r < half; ++r) {
+        double bk = -INFINITY;
+        int32_t bi = INT_MAX;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (after(ck[j], ci[j], pk, pi) && better(ck[j], ci[j], bk, bi)) {
+                bk = ck[j];
+                bi = ci[j];
+            }
+        for (int e = lane + 256; e < M; e += 64) {
+            const double ke = k[e];
+            const int32_t ie = i[e];
+            if (after(ke, ie, pk, pi) && better(ke, ie, bk, bi)) {
+                bk = ke;
+                bi = ie;
+            }
+        }
+        wave_best_fast(bk, bi);
+        if (lane == 0) {
+            ok[r] = bk;
+            oi[r] = bi;
+        }
+        pk = bk;
+        pi = bi;
+    }
+}
+
+// Largest list (per side) ranked by pairs in one pass.
+constexpr int kPairMax = 256;
+
+// Top `half` of each side's entries (k[s][0..M_s), i[s][0..M_s)), M_s <=
+// kSelThreads / LPE, by ranks computed all at once: LPE threads share one
+// entry, each compares it with a slice of the others, and a sum over the
+// LPE threads gives its rank (the number of entries before it in the order
+// of better(); entries are distinct, so ranks are unique).  Run by the
+// whole block.
+template <int LPE>
+__device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
+                                              const int32_t (*i)[kSurv],
+                                              int M0, int M1, int half,
+                                              double* ku, int32_t* iu,
+                                              double* kl, int32_t* il)
+{
+    constexpr int E = kSelThreads / LPE;  // entries covered
+    constexpr int F = E / LPE;            // comparisons per thread
+    const int tid = threadIdx.x;
+    const int e = tid / LPE, f0 = (tid % LPE) * F;
+#pragma unroll
+    for (int side = 0; side < 2; ++side) {
+        const int M = side ? M1 : M0;
+        const bool ve = e < M;
+        const double ke = k[side][ve ? e : 0];
+        const int32_t ie = i[side][ve ? e : 0];
+        int c = 0;
+#pragma unroll 8
+        for (int j = 0; j < F; ++j) {
+            const int f = f0 + j;
+            const double kf = k[side][f];
+            const int32_t iff = i[side][f];
+            c += (f < M && better(kf, iff, ke, ie)) ? 1 : 0;
+        }
+        if (LPE == 16) {
+            c = row_sum_i32(c);
+        } else {
+#pragma unroll
+            for (int o = 1; o < LPE; o <<= 1) c += __shfl_xor(c, o);
+        }
+        if (ve && tid % LPE == 0 && c < half) {
+            (side ? kl : ku)[c] = ke;
+            (side ? il : iu)[c] = ie;
+        }
+    }
+}
+
+// Threshold of the next list of one side, from this selection's best key
+// K1 and half-th key Kh and the entries c the list held (c < 0: the list
+// was not consulted).  The spread below Kh adapts so that the list keeps a
+// few times `half` entries: an empty or short list widens it, a long or
+// overflowing one narrows it.
+__device__ __forceinline__ double next_threshold(double K1, double Kh, int c,
+                                                 int half, double& spread)
+{
+    const int hi = max(6 * half, min(kPairMax / 2, 12 * half));
+    if (c < half) spread = fmax(2.0 * spread, K1 - Kh);
+    else if (c > kListCap) spread *= 0.25;
+    else if (c > hi) spread *= 0.5;
+    else if (c < 3 * half) spread *= 1.5;
+    if (!(spread > 0.0) || !(spread < INFINITY))
+        spread = 1e-6 * fmax(1.0, fabs(Kh));
+    return Kh == -INFINITY ? INFINITY : Kh - spread;
+}
+
+// Exact top-`half` over `count` entries produced by get(e, key, index), by
+// `half` block-wide rounds (each: the best entry after the previous winner).
+// All threads of the block take part; thread 0 writes ok/oi.
+template <class Get>
+__device__ void block_rounds(int64_t count, Get get, int half, double* ok,
+                             int32_t* oi, double (*rk)[kSelThreads / 64],
+                             int32_t (*ri)[kSelThreads / 64])
+{
+    constexpr int NW = kSelThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    double pk = INFINITY;
+    int32_t pi = -1;
+    for (int k = 0; k < half; ++k) {
+        double bk = -INFINITY;
+        int32_t bi = INT_MAX;
+        for (int64_t e = tid; e < count; e += kSelThreads) {
+            double key;
+            int32_t t;
+            get(e, key, t);
+            if (after(key, t, pk, pi) && better(key, t, bk, bi)) {
+                bk = key;
+                bi = t;
+            }
+        }
+        wave_best_fast(bk, bi);
+        if (lane == 0) {
+            rk[k & 1][wave] = bk;
+            ri[k & 1][wave] = bi;
+        }
+        __syncthreads();
+        bk = rk[k & 1][0];
+        bi = ri[k & 1][0];
+        for (int w = 1; w < NW; ++w)
+            if (better(rk[k & 1][w], ri[k & 1][w], bk, bi)) {
+                bk = rk[k & 1][w];
+                bi = ri[k & 1][w];
+            }
+        pk = bk;
+        pi = bi;
+        if (tid == 0) {
+            ok[k] = bk;
+            oi[k] = bi;
+        }
+    }
+    __syncthreads();
+}
+
+// Best (key, lane) of each side over a 16-lane row (NBLK = 1) or the wave,
+// both sides interleaved; results are wave-uniform.  Ties go to the lowest
+// lane.
+template <int NBLK>
+__device__ __forceinline__ void best_two_sides(double& ku, int& lu, double& kl,
+                                               int& ll)
+{
+    if (NBLK == 1) {
+        const double mu = row_max_f64(ku), ml = row_max_f64(kl);
+        const int cu = row_min_i32(ku == mu ? lu : INT_MAX);
+        const int cl = row_min_i32(kl == ml ? ll : INT_MAX);
+        ku = rl_f64(mu, 0);
+        kl = rl_f64(ml, 0);
+        lu = rl_i32(cu, 0);
+        ll = rl_i32(cl, 0);
+    } else {
+        wave_best_pair(ku, lu, kl, ll);
+    }
+}
+
+// Features per LDS slice of the working-set rows in k_select.
+int select_slice(int nblk_cols, int64_t ldp)
+{
+    const int64_t ldp16 = (ldp + 15) & ~(int64_t)15;
+    const int64_t budget = 96 * 1024;  // bytes of dynamic LDS
+    int64_t w = (budget / ((int64_t)nblk_cols * 16 * 4) - 4) & ~(int64_t)15;
+    w = std::min<int64_t>(w, ldp16);
+    return (int)std::max<int64_t>(16, w);
+}
+
+static size_t select_lds_bytes(int nblk_cols, int slice)
+{
+    return (size_t)nblk_cols * 16 * (slice + 4) * sizeof(float);
+}
+
+template <bool SVR, int NBLK>
+__global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
+{
+    WorkingSet* ws = a.ws;
+    if ((a.mode & SS_CHECK_DONE) && ws->done) return;
+    const uint64_t t_start = wall_clock64();
+
+    constexpr int NW = kSelThreads / 64;
+    constexpr int QS = NBLK * 16;  // slots covered by K_SS
+    __shared__ double upk[kMaxHalf], lok[kMaxHalf];
+    __shared__ int32_t upi[kMaxHalf], loi[kMaxHalf];
+    __shared__ double rmax[2][NW * 4];
+    __shared__ double theta[2];
+    __shared__ double thnext[2];
+    __shared__ double svk[2][kSurv];
+    __shared__ int32_t svi[2][kSurv];
+    __shared__ int32_t nsv[2];
+    __shared__ int32_t exb[2][kMaxHalf];
+    __shared__ int32_t nex[2];
+    __shared__ double keepk[kMaxHalf];
+    __shared__ int32_t keepi[kMaxHalf];
+    __shared__ int32_t nkeep;
+    __shared__ double rk[2][NW];
+    __shared__ int32_t ri[2][NW];
+    __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
+    __shared__ int32_t shPos[kMaxQ];  // position in B of the i-th smallest
+    __shared__ float shsS[kMaxQ];
+    __shared__ float KSS[QS][QS + 1];
+    __shared__ double shDc[kMaxQ];
+    __shared__ int32_t shNB, shNS, shGo, shDone;
+    __shared__ double shGap, shMx, shMn;
+    extern __shared__ __align__(16) float xst[];  // QS x (slice + 4)
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int half = a.half;
+    const int64_t n = a.n, ldp = a.ldp;
+    const bool given = (a.mode & SS_GIVEN_B) != 0;
+    const int64_t iter0 = ws->iter;  // issued early, used in (8)
+    // Counters: read now and written back once by thread 0 at the exit, so
+    // that no read-modify-write of global memory waits on the way.  Global
+    // stores are likewise left to the exit: a barrier after a store waits
+    // for it.
+    int64_t c_rows = 0, c_inner = 0, c_resc = 0, c_slow = 0, c_hits = 0;
+    int64_t c_prof[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    uint64_t t_l1 = 0, t_l2 = 0;  // (list path) entries staged, ranked
+    double spr[2] = {0.0, 0.0};
+    if (tid == 0) {
+        spr[0] = ws->spread[0];
+        spr[1] = ws->spread[1];
+        c_rows = ws->rows;
+        c_inner = ws->inner_total;
+        c_resc = ws->rescans;
+        c_slow = ws->slow_selects;
+        c_hits = ws->list_hits;
+#pragma unroll
+        for (int k = 0; k < 12; ++k) c_prof[k] = ws->prof[k];
+    }
+    if (tid == 0) shDone = 0;
+    bool fastp = false;  // (thread 0) this selection used the list
+
+    if (!given) {
+        if (tid < kMaxHalf) {
+            upk[tid] = lok[tid] = -INFINITY;
+            upi[tid] = loi[tid] = INT_MAX;
+        }
+        if (tid < 2) thnext[tid] = INFINITY;
+        // (0) the threshold list: every variable whose key reached the
+        // threshold of its side.  With at least `half` of them on a side,
+        // the top `half` of the side are among them (exact).  Its entries
+        // are loaded together with the counts.
+        int lc0 = 0, lc1 = 0;
+        double lk0 = 0.0, lk1 = 0.0;
+        int32_t li0 = 0, li1 = 0;
+        if (a.list_cnt) {
+            lc0 = a.list_cnt[0];
+            lc1 = a.list_cnt[1];
+            lk0 = a.list_key[tid];
+            li0 = a.list_idx[tid];
+            lk1 = a.list_key[kListCap + tid];
+            li1 = a.list_idx[kListCap + tid];
+        }
+        const bool fast = lc0 >= half && lc1 >= half && lc0 <= kListCap &&
+                          lc1 <= kListCap;
+        if (fast) {
+            if (tid < lc0) {
+                svk[0][tid] = lk0;
+                svi[0][tid] = li0;
+            }
+            if (tid < lc1) {
+                svk[1][tid] = lk1;
+                svi[1][tid] = li1;
+            }
+            __syncthreads();
+            t_l1 = wall_clock64();
+            const int lm = max(lc0, lc1);
+            if (lm <= 64) {
+                pair_rank_top<16>(svk, svi, lc0, lc1, half, upk, upi, lok, loi);
+            } else if (lm <= 128) {
+                pair_rank_top<8>(svk, svi, lc0, lc1, half, upk, upi, lok, loi);
+            } else if (lm <= kPairMax) {
+                pair_rank_top<4>(svk, svi, lc0, lc1, half, upk, upi, lok, loi);
+            } else {
+                if (wave == 0) wave_top(svk[0], svi[0], lc0, half, upk, upi);
+                if (wave == 1) wave_top(svk[1], svi[1], lc1, half, lok, loi);
+            }
+            __syncthreads();
+            t_l2 = wall_clock64();
+            if (tid == 0) {
+                c_hits += 1;
+                fastp = true;
+            }
+        } else {
+            // (1) the per-group candidates
+            const int cnt = a.nb * kBlockTop;
+            double ku[kSelPerThread], kl[kSelPerThread];
+            int32_t iu[kSelPerThread], il[kSelPerThread];
+#pragma unroll
+            for (int j = 0; j < kSelPerThread; ++j) {
+                // unconditional loads (a valid entry when unused)
+                const int e = tid + j * kSelThreads;
+                const int ec = min(e, cnt - 1);
+                const int blk = ec / kBlockTop, k = ec - blk * kBlockTop;
+                const size_t bu = (size_t)blk * 2 * kBlockTop;
+                ku[j] = a.cand_key[bu + k];
+                iu[j] = a.cand_idx[bu + k];
+                kl[j] = a.cand_key[bu + kBlockTop + k];
+                il[j] = a.cand_idx[bu + kBlockTop + k];
+            }
+#pragma unroll
+            for (int j = 0; j < kSelPerThread; ++j) {
+                if (tid + j * kSelThreads >= cnt) {
+                    ku[j] = kl[j] = -INFINITY;
+                    iu[j] = il[j] = INT_MAX;
+                }
+            }
+            // (2) maxima of every 16-lane row: distinct candidates, so the
+            // half-th largest of them bounds the half-th best key from below
+            double mu = -INFINITY, ml = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < kSelPerThread; ++j) {
+                mu = fmax(mu, ku[j]);
+                ml = fmax(ml, kl[j]);
+            }
+            mu = row_max_f64(mu);
+            ml = row_max_f64(ml);
+            if ((lane & 15) == 0) {
+                rmax[0][wave * 4 + (lane >> 4)] = mu;
+                rmax[1][wave * 4 + (lane >> 4)] = ml;
+            }
+            if (tid < 2) nsv[tid] = 0;
+            __syncthreads();
+            if (wave == 0) {
+                // lane l holds row maximum l; theta = the largest x_l with at
+                // least `half` row maxima >= x_l (-inf if there is none)
+                for (int side = 0; side < 2; ++side) {
+                    const double x = rmax[side][lane];
+                    int c = 0;
+#pragma unroll 16
+                    for (int j = 0; j < NW * 4; ++j) c += rmax[side][j] >= x;
+                    double th = (c >= half && x != -INFINITY) ? x : -INFINITY;
+                    th = row_max_f64(th);
+                    th = fmax(fmax(rl_f64(th, 0), rl_f64(th, 16)),
+                              fmax(rl_f64(th, 32), rl_f64(th, 48)));
+                    if (lane == 0) theta[side] = th;
+                }
+            }
+            __syncthreads();
+            // (3) keep the candidates at or above the bound
+            {
+                const double th0 = theta[0], th1 = theta[1];
+#pragma unroll
+                for (int j = 0; j < kSelPerThread; ++j) {
+                    for (int side = 0; side < 2; ++side) {
+                        const double kv = side ? kl[j] : ku[j];
+                        const int32_t iv = side ? il[j] : iu[j];
+                        const double th = side ? th1 : th0;
+                        const bool keep = kv != -INFINITY && kv >= th;
+                        const unsigned long long m = __ballot(keep);
+                        if (m == 0) continue;
+                        int base = 0;
+                        if (lane == 0) base = atomicAdd(&nsv[side], __popcll(m));
+                        base = __builtin_amdgcn_readfirstlane(base);
+                        const int pos = base + lanes_below(m);
+                        if (keep && pos < kSurv) {
+                            svk[side][pos] = kv;
+                            svi[side][pos] = iv;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            const int M0 = nsv[0], M1 = nsv[1];
+            const bool overflow = M0 > kSurv || M1 > kSurv;
+            if (!overflow) {
+                // (4) rank the survivors: side 0 on threads [0,512), side 1
+                // on the rest
+                if (wave == 0) wave_top(svk[0], svi[0], M0, half, upk, upi);
+                if (wave == 1) wave_top(svk[1], svi[1], M1, half, lok, loi);
+                __syncthreads();
+            } else {
+                // (4') too many ties at the bound (e.g. alpha = 0): exact
+                // block rounds over all candidates
+                for (int side = 0; side < 2; ++side) {
+                    auto get = [&](int64_t e, double& key, int32_t& t) {
+                        const int64_t blk = e / kBlockTop,
+                                      k = e - blk * kBlockTop;
+                        const size_t o = (size_t)blk * 2 * kBlockTop +
+                                         (side ? kBlockTop : 0) + k;
+                        key = a.cand_key[o];
+                        t = a.cand_idx[o];
+                    };
+                    block_rounds(cnt, get, half, side ? lok : upk,
+                                 side ? loi : upi, rk, ri);
+                }
+                if (tid == 0) c_slow += 1;
+            }
+            // (5) row groups whose whole candidate list was taken may hold
+            // more: wave 0 finds them (lane-parallel)
+            const uint32_t grows = (uint32_t)a.group_rows;
+            if (wave == 0) {
+                for (int side = 0; side < 2; ++side) {
+                    const double* kk = side ? lok : upk;
+                    const int32_t* ii = side ? loi : upi;
+                    const bool valid = lane < half && kk[lane] != -INFINITY;
+                    const int32_t b =
+                        valid ? (int32_t)((uint32_t)sample_of(SVR, ii[lane], n) /
+                                          grows)
+                              : -1 - lane;
+                    int c = 0;
+                    bool first = true;
+                    for (int j = 0; j < half; ++j) {
+                        const int32_t bj = rl_i32(b, j);
+                        c += bj == b;
+                        first &= !(j < lane && bj == b);
+                    }
+                    const bool ex = valid && c >= kBlockTop && first;
+                    const unsigned long long m = __ballot(ex);
+                    if (ex) exb[side][lanes_below(m)] = b;
+                    if (lane == 0) nex[side] = __popcll(m);
+                }
+            }
+            __syncthreads();
+            if (nex[0] + nex[1] > 0) {
+                // (6) rare: exact block rounds over the winners outside those
+                // groups plus every variable of the groups (keys from F)
+                const uint32_t NV = SVR ? 2 : 1;
+                for (int side = 0; side < 2; ++side) {
+                    const int ne = nex[side];
+                    if (ne == 0) continue;
+                    double* kk = side ? lok : upk;
+                    int32_t* ii = side ? loi : upi;
+                    if (tid == 0) {
+                        int c = 0;
+                        for (int k = 0; k < half; ++k) {
+                            if (kk[k] == -INFINITY) continue;
+                            const int32_t b = (int32_t)(
+                                (uint32_t)sample_of(SVR, ii[k], n) / grows);
+                            bool ex = false;
+                            for (int x = 0; x < ne; ++x) ex |= exb[side][x] == b;
+                            if (!ex) {
+                                keepk[c] = kk[k];
+                                keepi[c] = ii[k];
+                                ++c;
+                            }
+                        }
+                        nkeep = c;
+                    }
+                    __syncthreads();
+                    const int nk = nkeep;
+                    const uint32_t per = grows * NV;
+                    auto get = [&](int64_t e, double& key, int32_t& t) {
+                        if (e < nk) {
+                            key = keepk[e];
+                            t = keepi[e];
+                            return;
+                        }
+                        const uint32_t q = (uint32_t)(e - nk);
+                        const uint32_t x = q / per, o = q - x * per;
+                        const int64_t row =
+                            (int64_t)exb[side][x] * grows + (o % grows);
+                        key = -INFINITY;
+                        t = INT_MAX;
+                        if (row < n) {
+                            const int64_t tt = o < grows ? row : n + row;
+                            double u, l;
+                            var_scores<SVR>(a, tt, u, l);
+                            key = side ? l : u;
+                            t = (int32_t)tt;
+                        }
+                    };
+                    block_rounds((int64_t)nk + (int64_t)ne * per, get, half, kk,
+                                 ii, rk, ri);
+                }
+                if (tid == 0) c_resc += 1;
+            }
+        }
+        if (tid == 0) {
+            thnext[0] = next_threshold(upk[0], upk[half - 1],
+                                       a.list_cnt ? lc0 : -1, half, spr[0]);
+            thnext[1] = next_threshold(lok[0], lok[half - 1],
+                                       a.list_cnt ? lc1 : -1, half, spr[1]);
+        }
+    }
+    const uint64_t t_merge = wall_clock64();
+
+    // (8) working set, distinct samples (wave 0, lane-parallel)
+    if (wave == 0) {
+        int go = 0, nB = 0;
+        double gap = 0.0;
+        if (!given) {
+            const bool valid = upk[0] != -INFINITY && lok[0] != -INFINITY;
+            const double m = upk[0], M = -lok[0];
+            gap = valid ? m - M : 0.0;
+            bool build = true;
+            if (a.mode & SS_SOLVE) {
+                if (!valid || gap <= a.tol) {
+                    if (lane == 0) shDone = 1;
+                    build = false;
+                } else if (iter0 >= a.max_iter) {
+                    if (lane == 0) shDone = 2;
+                    build = false;
+                }
+            }
+            if (lane == 0) {
+                shMx = valid ? m : 0.0;
+                shMn = valid ? M : 0.0;
+            }
+            if (build) {
+                // lanes [0,half): up list, [half,2half): low list; position
+                // in the interleaved order U0 L0 U1 L1 ...
+                const bool isU = lane < half;
+                const bool inL = lane >= half && lane < 2 * half;
+                const int k = isU ? lane : lane - half;
+                const double key = isU ? upk[k] : (inL ? lok[k] : -INFINITY);
+                const bool ent = (isU || inL) && key != -INFINITY;
+                const int32_t idx =
+                    ent ? (isU ? upi[k] : loi[k]) : INT_MAX;  // none: no match
+                bool keep = ent;
+                // drop a variable already placed earlier in the order: up
+                // entry k follows low entries 0..k-1, low entry k follows up
+                // entries 0..k (entries compared through registers)
+                for (int j = 0; j < half; ++j) {
+                    const int32_t uj = rl_i32(idx, j), lj = rl_i32(idx, half + j);
+                    if (isU && j < k && lj == idx) keep = false;
+                    if (inL && j <= k && uj == idx) keep = false;
+                }
+                const unsigned long long m = __ballot(keep);
+                const unsigned long long mu = m & ((1ull << half) - 1ull);
+                const unsigned long long ml = (m >> half) & ((1ull << half) - 1ull);
+                const unsigned long long below = (1ull << k) - 1ull;
+                int pos = __popcll(mu & below) + __popcll(ml & below);
+                if (!isU) pos += (int)((mu >> k) & 1ull);
+                int32_t* dst = (a.mode & SS_SOLVE) ? shB : ws->B;
+                if (keep) dst[pos] = idx;
+                nB = __popcll(m);
+                if (a.mode & SS_SOLVE) go = 1;
+                else if (lane == 0) ws->nB = nB;
+            }
+        } else {
+            nB = ws->nB;
+            if (lane < nB) shB[lane] = ws->B[lane];
+            gap = ws->gap;
+            go = (a.mode & SS_SOLVE) ? 1 : 0;
+        }
+        __builtin_amdgcn_wave_barrier();
+        int nS = 0;
+        if (go) {
+            // slot of each variable: rank of the first occurrence of its
+            // sample (eps-SVR: both copies of a sample share one slot)
+            const bool act = lane < nB;
+            const int32_t t = act ? shB[lane] : INT_MAX;
+            const int32_t s = act ? (int32_t)sample_of(SVR, t, n) : -1;
+            int firstpos = lane;
+            if (SVR)
+                for (int j = 0; j < nB; ++j) {
+                    const int32_t sj = rl_i32(s, j);
+                    if (act && j < firstpos && sj == s) firstpos = j;
+                }
+            const unsigned long long fm = __ballot(act && firstpos == lane);
+            const unsigned long long bl =
+                firstpos >= 64 ? ~0ull : ((1ull << firstpos) - 1ull);
+            const int slot = __popcll(fm & bl);
+            // order of the variable among B by index (the subproblem runs
+            // its variables in increasing index order: lowest lane = lowest
+            // index on ties)
+            int p = 0;
+            for (int j = 0; j < nB; ++j) p += rl_i32(t, j) < t ? 1 : 0;
+            if (act) {
+                shSlot[lane] = slot;
+                if (firstpos == lane) shS[slot] = s;
+                shPos[p] = lane;
+            }
+            nS = __popcll(fm);
+        }
+        if (lane == 0) {
+            shGo = go;
+            shNB = nB;
+            shNS = nS;
+            shGap = gap;
+        }
+    }
+    __syncthreads();
+    const uint64_t t_build = wall_clock64();
+    // state written at every exit (threads 0 and 1)
+    auto finish = [&](int64_t t_end) {
+        if (tid < 2) {
+            if (a.list_cnt) a.list_cnt[tid] = 0;
+            if (!given) ws->theta[tid] = thnext[tid];
+        }
+        if (tid == 0) {
+            if (!given) {
+                ws->spread[0] = spr[0];
+                ws->spread[1] = spr[1];
+                if (shDone) ws->done = shDone;
+                ws->gap = shGap;
+                ws->m = shMx;
+                ws->M = shMn;
+            }
+            ws->list_hits = c_hits;
+            ws->slow_selects = c_slow;
+            ws->rescans = c_resc;
+            (void)t_end;
+        }
+    };
+    if (!shGo) {
+        finish(0);
+        if (tid == 0) ws->prof[0] = c_prof[0] + (int64_t)(t_merge - t_start);
+        return;
+    }
+    const int nB = shNB, nS = shNS;
+
+    // (9) state of B for the subproblem (wave 0, loads issued early).  The
+    // variable of rank p by index sits in lane p; with q <= 16 it sits in
+    // lane p of both row 0 (its up side) and row 1 (its low side), so that
+    // one row reduction serves both sides of a step.
+    constexpr bool DUP = NBLK == 1;
+    const int p = DUP ? (lane & 15) : lane;
+    const int prow = lane >> 4;
+    const bool act = wave == 0 && p < nB && (!DUP || prow < 2);
+    const bool own = act && (!DUP || prow == 0);  // writes the results
+    const int bpos = act ? shPos[p] : 0;          // position in B
+    const int32_t t = act ? shB[bpos] : INT_MAX;
+    const int sl = act ? shSlot[bpos] : 0;
+    const int64_t sm = act ? sample_of(SVR, t, n) : 0;
+    double al = act ? a.alpha[t] : 0.0;
+    double yv = 1.0, rv = 0.0, v = 0.0;
+    if (act) {
+        if (SVR) {
+            yv = t < n ? 1.0 : -1.0;
+            rv = t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps;
+        } else {
+            yv = (a.st[t] & ST_YPOS) ? 1.0 : -1.0;
+            rv = yv;
+        }
+        v = rv - a.F[sm];
+    }
+
+    uint64_t t_stage = 0;
+    // (10) K_SS on the matrix cores (same operand order as k_rows).  The
+    // working-set rows pass through LDS in feature slices: every thread
+    // loads a piece into LDS; then the NBLK^2 matrix-core waves accumulate
+    // the slice while the other waves copy it to xS (the rows of the next
+    // k_rows).
+    {
+        const int g = lane >> 4, nl = lane & 15;
+        const int bi = wave / NBLK, bj = wave - bi * NBLK;
+        const int sa = bi * 16 + nl, sb = bj * 16 + nl;
+        const bool mw = wave < NBLK * NBLK;
+        const bool va = mw && sa < nS, vb = mw && sb < nS;
+        float sqa[4] = {0.f, 0.f, 0.f, 0.f};
+        float sqb = 0.f;
+        if (mw) {
+#pragma unroll
+            for (int vv = 0; vv < 4; ++vv) {
+                const int ia = bi * 16 + 4 * g + vv;
+                sqa[vv] = a.sq[ia < nS ? shS[ia] : 0];
+            }
+            sqb = a.sq[vb ? shS[sb] : 0];
+        }
+        const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
+        const int W = a.slice, wst = W + 4;
+        // copy waves: those without a K_SS block, or all of them.  With a
+        // single slice the copy waits until after the last barrier (waves
+        // 1.. copy while wave 0 solves), so that no barrier waits for it.
+        constexpr int GW = NBLK * NBLK < NW ? NBLK * NBLK : 0;
+        const bool one_slice = W >= ldp16;
+        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+        t_stage = wall_clock64();
+        for (int c0 = 0; c0 < ldp16; c0 += W) {
+            const int wc = min(W, ldp16 - c0), q4 = wc >> 2, tot = nS * q4;
+            for (int e0 = tid; e0 < tot; e0 += 4 * kSelThreads) {
+                float4 xv[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int e = e0 + j * kSelThreads;
+                    const bool in = e < tot;
+                    const int slot = in ? e / q4 : 0;
+                    const int c4 = e - slot * q4;
+                    const int64_t col = c0 + 4 * c4;
+                    const bool ok = in && col < ldp;
+                    // unconditional loads (an address inside X when unused)
+                    xv[j] = ld4(a.X + (ok ? (int64_t)shS[slot] * ldp + col : 0));
+                    if (!ok) xv[j] = zero4();
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int e = e0 + j * kSelThreads;
+                    if (e < tot) {
+                        const int slot = e / q4, c4 = e - slot * q4;
+                        *reinterpret_cast<float4*>(xst + slot * wst + 4 * c4) =
+                            xv[j];
+                    }
+                }
+            }
+            __syncthreads();
+            if (c0 == 0) t_stage = wall_clock64();
+            if (mw) {
+                for (int cc = 0; cc < wc; cc += 16) {
+                    float4 av = ld4(xst + sa * wst + cc + 4 * g);
+                    float4 bv = ld4(xst + sb * wst + cc + 4 * g);
+                    if (!va) av = zero4();
+                    if (!vb) bv = zero4();
+                    acc = mfma_chunk(acc, av, bv);
+                }
+            }
+            if (!one_slice) {
+                if (wave >= GW) {
+                    for (int e = tid - GW * 64; e < tot;
+                         e += kSelThreads - GW * 64) {
+                        const int slot = e / q4, c4 = e - slot * q4;
+                        const int64_t col = c0 + 4 * c4;
+                        if (col < ldp)
+                            *reinterpret_cast<float4*>(
+                                a.xS + (int64_t)slot * ldp + col) =
+                                ld4(xst + slot * wst + 4 * c4);
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        if (mw) {
+#pragma unroll
+            for (int vv = 0; vv < 4; ++vv) {
+                const int ia = bi * 16 + 4 * g + vv, ib = bj * 16 + nl;
+                if (ia < nS && ib < nS)
+                    KSS[ia][ib] = ia == ib ? 1.0f
+                                           : rbf_from_dot(sqa[vv], sqb, acc[vv],
+                                                          a.gexp);
+            }
+            if (bi == 0 && g == 0 && vb) shsS[sb] = sqb;
+        }
+    }
+    __syncthreads();
+    const uint64_t t_kss = wall_clock64();
+
+    if (wave != 0) {
+        const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
+        const int W = a.slice;
+        if (W >= ldp16) {
+            const int q4 = ldp16 >> 2, wst = W + 4;
+            for (int e = tid - 64; e < nS * q4; e += kSelThreads - 64) {
+                const int slot = e / q4, c4 = e - slot * q4;
+                const int64_t col = 4 * c4;
+                if (col < ldp)
+                    *reinterpret_cast<float4*>(a.xS + (int64_t)slot * ldp +
+                                               col) =
+                        ld4(xst + slot * wst + 4 * c4);
+            }
+        }
+        return;
+    }
+
+    // (11) subproblem: maximal-violating-pair steps restricted to B
+    const double a0 = al;
+    if ((a.mode & SS_SET_ALPHA) && act) al = ws->alphaB[bpos];
+    const double C = a.C;
+    const double itol = a.inner_tol_override >= 0.0
+                            ? a.inner_tol_override
+                            : fmax(a.inner_ratio * shGap, 0.5 * a.tol);
+    int steps = 0;
+    for (; steps < a.max_inner; ++steps) {
+        const bool up = act && ((yv > 0 && al < C) || (yv < 0 && al > 0));
+        const bool lo = act && ((yv > 0 && al > 0) || (yv < 0 && al < C));
+        double bu, bl;
+        int Li, Lj;
+        if (DUP) {
+            // row 0: up scores v, row 1: low scores -v; ties to the lowest
+            // lane = the lowest index
+            const bool lside = prow == 1;
+            const double key =
+                lside ? (lo ? -v : -INFINITY) : (up ? v : -INFINITY);
+            const int idx = (lside ? lo : up) ? p : INT_MAX;
+            const double M = row_max_f64(key);
+            const unsigned long long hit = __ballot(key == M && idx != INT_MAX);
+            bu = rl_f64(M, 0);
+            bl = rl_f64(M, 16);
+            Li = __builtin_ctzll((hit & 0xFFFFull) | 0x10000ull);
+            Lj = __builtin_ctzll(((hit >> 16) & 0xFFFFull) | 0x10000ull);
+        } else {
+            bu = up ? v : -INFINITY;
+            bl = lo ? -v : -INFINITY;
+            Li = up ? lane : INT_MAX;
+            Lj = lo ? lane : INT_MAX;
+            wave_best_pair(bu, Li, bl, Lj);
+        }
+        if (bu == -INFINITY || bl == -INFINITY) break;
+        const double vi = bu, vj = -bl;
+        if (!(vi - vj > itol)) break;
+        const double ali = rl_f64(al, Li), alj = rl_f64(al, Lj);
+        const double yi = rl_f64(yv, Li), yj = rl_f64(yv, Lj);
+        const int si = rl_i32(sl, Li), sj = rl_i32(sl, Lj);
+        const double kij = (double)KSS[si][sj];
+        const double kai = (double)KSS[sl][si], kaj = (double)KSS[sl][sj];
+        double a2 = (double)KSS[si][si] + (double)KSS[sj][sj] - 2.0 * kij;
+        if (a2 <= 0.0) a2 = kTau;
+        double s = (vi - vj) / a2;
+        const double Ui = yi > 0 ? C - ali : ali;
+        const double Lb = yj > 0 ? alj : C - alj;
+        bool ci = false, cj = false;
+        if (Ui <= s) {
+            s = Ui;
+            ci = true;
+        }
+        if (Lb <= s) {
+            s = Lb;
+            cj = true;
+            ci = (Ui == s);
+        }
+        if (act && p == Li) {
+            al += yi * s;
+            if (ci) al = yi > 0 ? C : 0.0;
+        }
+        if (act && p == Lj) {
+            al -= yj * s;
+            if (cj) al = yj > 0 ? 0.0 : C;
+        }
+        if (act) v -= s * (kai - kaj);
+    }
+    const uint64_t t_inner = wall_clock64();
+
+    if (own) ws->alphaB[bpos] = al;
+    if (!(a.mode & SS_NO_WRITE)) {
+        const double dc = own ? yv * (al - a0) : 0.0;
+        if (own) {
+            a.alpha[t] = al;
+            a.st[t] = state_bits(yv, al, C);
+            shDc[p] = dc;
+        }
+        // the change of the coefficient of each slot: the one variable of
+        // the slot, or (eps-SVR) the sum of both copies of its sample
+        int partner = -1;
+        if (SVR)
+            for (int j = 0; j < nB; ++j)
+                if (j != p && rl_i32(sl, j) == sl) partner = j;
+        __builtin_amdgcn_wave_barrier();
+        if (own && (partner < 0 || p < partner))
+            ws->coef[sl] = dc + (partner >= 0 ? shDc[partner] : 0.0);
+        if (lane < nS) {
+            ws->S[lane] = shS[lane];
+            ws->sS[lane] = shsS[lane];
+        }
+        if (lane < nB) {
+            ws->B[lane] = shB[lane];
+            ws->slotB[lane] = shSlot[lane];
+        }
+        if (lane == 0) {
+            ws->nB = nB;
+            ws->nS = nS;
+            if (!given) ws->iter = iter0 + 1;
+            ws->rows = c_rows + nS;
+        }
+    }
+    finish(0);
+    if (lane == 0) {
+        ws->steps = steps;
+        ws->inner_total = c_inner + steps;
+        ws->prof[0] = c_prof[0] + (int64_t)(t_merge - t_start);
+        ws->prof[1] = c_prof[1] + (int64_t)(t_kss - t_merge);
+        ws->prof[2] = c_prof[2] + (int64_t)(t_inner - t_kss);
+        ws->prof[3] = c_prof[3] + (int64_t)(wall_clock64() - t_inner);
+        ws->prof[4] = c_prof[4] + 1;
+        ws->prof[5] = c_prof[5] + (fastp ? (int64_t)(t_merge - t_start) : 0);
+        ws->prof[6] = c_prof[6] + (int64_t)(t_build - t_merge);
+        ws->prof[7] = c_prof[7] + (int64_t)(t_stage - t_build);
+        ws->prof[8] = c_prof[8] + (fastp ? (int64_t)(t_l1 - t_start) : 0);
+        ws->prof[9] = c_prof[9] + (fastp ? (int64_t)(t_l2 - t_l1) : 0);
+        ws->prof[10] = c_prof[10] + (fastp ? (int64_t)(t_merge - t_l2) : 0);
+    }
+}
+
+template <bool SVR, int NBLK>
+static void select_dispatch(const SelArgs& a, hipStream_t s)
+{
+    const size_t lds = select_lds_bytes(NBLK, a.slice);
+    static size_t lds_allowed = 32 * 1024;
+    if (lds > lds_allowed) {
+        hipError_t e = hipFuncSetAttribute(
+            (const void*)k_select<SVR, NBLK>,
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            throw Error{SVM_E_UNSUPPORTED,
+                        "select tile needs more LDS than the device allows"};
+        }
+        lds_allowed = lds;
+    }
+    k_select<SVR, NBLK><<<1, kSelThreads, lds, s>>>(a);
+}
+
+void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)
+{
+    SelArgs a = a0;
+    if (a.slice <= 0) a.slice = select_slice(nblk_cols, a.ldp);
+    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
+        case 2: select_dispatch<false, 1>(a, s); break;
+        case 3: select_dispatch<true, 1>(a, s); break;
+        case 4: select_dispatch<false, 2>(a, s); break;
+        case 5: select_dispatch<true, 2>(a, s); break;
+        case 8: select_dispatch<false, 4>(a, s); break;
+        case 9: select_dispatch<true, 4>(a, s); break;
+        default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
+    }
+}
+
+}  // namespace msvm

@@ -146,6 +146,9 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     xS_.alloc((size_t)kMaxQ * f.ldp);
     ckey_.alloc((size_t)ncand_ * 2 * kBlockTop);
     cidx_.alloc((size_t)ncand_ * 2 * kBlockTop);
+    lkey_.alloc((size_t)2 * kListCap);
+    lidx_.alloc((size_t)2 * kListCap);
+    lcnt_.alloc(2);
     sum_.alloc(1);
     cvec_.alloc((size_t)n_);
     cblk_.alloc((size_t)compact_blocks(n_));
@@ -159,6 +162,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     HIP_TRY(hipMemsetAsync(F_.p, 0, F_.bytes(), s));
     HIP_TRY(hipMemsetAsync(alpha_.p, 0, alpha_.bytes(), s));
     HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
+    HIP_TRY(hipMemsetAsync(lcnt_.p, 0, lcnt_.bytes(), s));
     HIP_TRY(hipMemsetAsync(xS_.p, 0, xS_.bytes(), s));
     DevBuf<int32_t> bad(1);
     HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), s));
@@ -188,6 +192,9 @@ void Solver::launch_keys()
     a.xS = xS_.p;
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
+    a.list_key = lkey_.p;
+    a.list_idx = lidx_.p;
+    a.list_cnt = lcnt_.p;
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
@@ -211,6 +218,9 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
     a.xS = xS_.p;
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
+    a.list_key = lkey_.p;
+    a.list_idx = lidx_.p;
+    a.list_cnt = lcnt_.p;
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
@@ -228,6 +238,9 @@ void Solver::launch_solve(int32_t mode)
     SelArgs a{};
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
+    a.list_key = lkey_.p;
+    a.list_idx = lidx_.p;
+    a.list_cnt = lcnt_.p;
     a.nb = ncand_;
     a.half = half_;
     a.ws = ws_.p;
@@ -445,15 +458,24 @@ SolveResult Solver::train()
             const double k = 10.0 / (double)w.prof[4];  // 100 MHz ticks -> ns
             fprintf(stderr,
                     "[mi355svm] iters=%lld rows=%lld inner=%.1f/iter "
-                    "rescans=%lld slow=%lld select(us): merge %.2f kss %.2f "
+                    "rescans=%lld slow=%lld list=%lld select(us): merge %.2f "
+                    "kss %.2f "
                     "inner %.2f "
-                    "write %.2f; rows kernel %.2f us/launch (%lld timed)\n",
+                    "write %.2f (list merge %.2f = %.2f + %.2f + %.2f, build "
+                    "%.2f stage %.2f); "
+                    "rows kernel %.2f us/launch (%lld timed)\n",
                     (long long)w.iter, (long long)w.rows,
                     (double)w.inner_total / (double)w.prof[4],
                     (long long)w.rescans, (long long)w.slow_selects,
+                    (long long)w.list_hits,
                     1e-3 * k * w.prof[0],
                     1e-3 * k * w.prof[1], 1e-3 * k * w.prof[2],
                     1e-3 * k * w.prof[3],
+                    w.list_hits ? 1e-2 * w.prof[5] / (double)w.list_hits : 0.0,
+                    w.list_hits ? 1e-2 * w.prof[8] / (double)w.list_hits : 0.0,
+                    w.list_hits ? 1e-2 * w.prof[9] / (double)w.list_hits : 0.0,
+                    w.list_hits ? 1e-2 * w.prof[10] / (double)w.list_hits : 0.0,
+                    1e-3 * k * w.prof[6], 1e-3 * k * w.prof[7],
                     row_launches_ ? 1e3 * row_ms_ / row_launches_ : 0.0,
                     (long long)row_launches_);
         }
@@ -485,6 +507,7 @@ void Solver::set_state(const double* alpha_h, const double* F_h)
                            hipMemcpyHostToDevice, s));
     launch_state_from_alpha(o_.type, y_.p, alpha_.p, n_, o_.C, st_.p, s);
     HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
+    HIP_TRY(hipMemsetAsync(lcnt_.p, 0, lcnt_.bytes(), s));
     cx_.sync();
 }
 
@@ -648,6 +671,9 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     r.xS = xS_.p;
     r.cand_key = ckey_.p;
     r.cand_idx = cidx_.p;
+    r.list_key = lkey_.p;
+    r.list_idx = lidx_.p;
+    r.list_cnt = lcnt_.p;
     r.n = n_;
     r.ldp = f_.ldp;
     r.eps = o_.eps;

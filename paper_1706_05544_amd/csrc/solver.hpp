@@ -147,6 +147,9 @@ private:
     DevBuf<float> xS_;
     DevBuf<double> ckey_;
     DevBuf<int32_t> cidx_;
+    DevBuf<double> lkey_;   // threshold list (2 x kListCap)
+    DevBuf<int32_t> lidx_;
+    DevBuf<int32_t> lcnt_;  // 2 counters
     DevBuf<Summary> sum_;
     DevBuf<double> cvec_;
     DevBuf<int32_t> cblk_, sv_idx_;
