@@ -60,6 +60,7 @@ struct WorkingSet {
     double theta[2];      // list thresholds for the next row kernel (up, low)
     double spread[2];     // distance of each threshold below the q/2-th key
     int64_t prof[12];     // select/solve phase times (wall-clock ticks)
+    int64_t stat[8];      // selection statistics (threshold list use)
 };
 
 // Final reductions of a state (bias and objective).

@@ -124,7 +124,10 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     constexpr int kXsEarly = 2;       // staging loads issued with the stream
     extern __shared__ __align__(16) unsigned char smem[];
     const WorkingSet* ws = a.ws;
-    if ((MODE & RU_CHECK_DONE) && ws->done) return;
+    // (RU_CHECK_DONE) the test of ws->done waits until the first loads are
+    // in flight, so that its round trip overlaps theirs
+    const int32_t done = (MODE & RU_CHECK_DONE) ? ws->done : 0;
+    if (!XS && done) return;
 
     const int tid = threadIdx.x, lane = tid & 63;
     // wave-uniform by construction; said so, so that the buffer resources
@@ -300,6 +303,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         float4 ring[kRing][4];
 #pragma unroll
         for (int j = 0; j < kRing; ++j) fetch(ring[j]);
+        if (done) return;  // uniform over the block
 #pragma unroll
         for (int i = 0; i < kXsEarly; ++i) xs_put(tid + i * kRowThreads, xv[i]);
         aux_store(0, ar);

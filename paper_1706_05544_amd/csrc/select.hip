@@ -92,7 +92,7 @@ __device__ void wave_top(const double* k, const int32_t* i, int M, int half,
 }
 
 // Largest list (per side) ranked by pairs in one pass.
-constexpr int kPairMax = 256;
+constexpr int kPairSmall = 64;
 
 // Top `half` of each side's entries (k[s][0..M_s), i[s][0..M_s)), M_s <=
 // kSelThreads / LPE, by ranks computed all at once: LPE threads share one
@@ -138,6 +138,67 @@ __device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
     }
 }
 
+// Exact top `half` of each side's entries (k[s][0..M_s), i[s][0..M_s)),
+// M_s <= kSurv, into (ku, iu) and (kl, il).  A list longer than one pair
+// pass ranks cheaply is cut first: the half-th best of its first 64
+// entries bounds the half-th best of the whole list from below, so the
+// entries at or above it (at least `half` of them) hold the top `half`;
+// they are compacted in place and ranked.  Run by the whole block; k and i
+// are overwritten.
+__device__ void top_half(double (*k)[kSurv], int32_t (*i)[kSurv], int M0,
+                         int M1, int half, double* ku, int32_t* iu, double* kl,
+                         int32_t* il, int32_t* shM)
+{
+    const int tid = threadIdx.x, lane = tid & 63;
+    if (M0 > kPairSmall || M1 > kPairSmall) {
+        pair_rank_top<16>(k, i, min(M0, kPairSmall), min(M1, kPairSmall), half,
+                          ku, iu, kl, il);
+        if (tid < 2) shM[tid] = 0;
+        __syncthreads();
+        double ke[2];
+        int32_t ie[2];
+        bool keep[2];
+#pragma unroll
+        for (int side = 0; side < 2; ++side) {
+            const int M = side ? M1 : M0;
+            const double bk = (side ? kl : ku)[half - 1];
+            const int32_t bi = (side ? il : iu)[half - 1];
+            const bool in = tid < M;
+            ke[side] = in ? k[side][tid] : -INFINITY;
+            ie[side] = in ? i[side][tid] : INT_MAX;
+            keep[side] = in && (M <= kPairSmall || !after(ke[side], ie[side], bk, bi));
+        }
+        __syncthreads();  // every entry read before the in-place writes
+#pragma unroll
+        for (int side = 0; side < 2; ++side) {
+            const unsigned long long m = __ballot(keep[side]);
+            if (m == 0) continue;
+            int base = 0;
+            if (lane == 0) base = atomicAdd(&shM[side], __popcll(m));
+            base = __builtin_amdgcn_readfirstlane(base);
+            if (keep[side]) {
+                const int pos = base + lanes_below(m);
+                k[side][pos] = ke[side];
+                i[side][pos] = ie[side];
+            }
+        }
+        __syncthreads();
+        M0 = shM[0];
+        M1 = shM[1];
+    }
+    const int lm = max(M0, M1);
+    if (lm <= kPairSmall) {
+        pair_rank_top<16>(k, i, M0, M1, half, ku, iu, kl, il);
+    } else if (lm <= 2 * kPairSmall) {
+        pair_rank_top<8>(k, i, M0, M1, half, ku, iu, kl, il);
+    } else {
+        const int wave = tid >> 6;
+        if (wave == 0) wave_top(k[0], i[0], M0, half, ku, iu);
+        if (wave == 1) wave_top(k[1], i[1], M1, half, kl, il);
+    }
+    __syncthreads();
+}
+
 // Threshold of the next list of one side, from this selection's best key
 // K1 and half-th key Kh and the entries c the list held (c < 0: the list
 // was not consulted).  The spread below Kh adapts so that the list keeps a
@@ -146,10 +207,9 @@ __device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
 __device__ __forceinline__ double next_threshold(double K1, double Kh, int c,
                                                  int half, double& spread)
 {
-    const int hi = max(6 * half, min(kPairMax / 2, 12 * half));
     if (c < half) spread = fmax(2.0 * spread, K1 - Kh);
     else if (c > kListCap) spread *= 0.25;
-    else if (c > hi) spread *= 0.5;
+    else if (c > max(4 * kPairSmall, 8 * half)) spread *= 0.5;
     else if (c < 3 * half) spread *= 1.5;
     if (!(spread > 0.0) || !(spread < INFINITY))
         spread = 1e-6 * fmax(1.0, fabs(Kh));
@@ -242,7 +302,8 @@ template <bool SVR, int NBLK>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 {
     WorkingSet* ws = a.ws;
-    if ((a.mode & SS_CHECK_DONE) && ws->done) return;
+    // (SS_CHECK_DONE) ws->done is tested once the list loads are in flight
+    const int32_t done0 = (a.mode & SS_CHECK_DONE) ? ws->done : 0;
     const uint64_t t_start = wall_clock64();
 
     constexpr int NW = kSelThreads / 64;
@@ -275,6 +336,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     const int half = a.half;
     const int64_t n = a.n, ldp = a.ldp;
     const bool given = (a.mode & SS_GIVEN_B) != 0;
+    if (given && done0) return;
     const int64_t iter0 = ws->iter;  // issued early, used in (8)
     // Counters: read now and written back once by thread 0 at the exit, so
     // that no read-modify-write of global memory waits on the way.  Global
@@ -284,9 +346,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     int64_t c_prof[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     uint64_t t_l1 = 0, t_l2 = 0;  // (list path) entries staged, ranked
     double spr[2] = {0.0, 0.0};
+    int64_t c_stat[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (tid == 0) {
         spr[0] = ws->spread[0];
         spr[1] = ws->spread[1];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) c_stat[k] = ws->stat[k];
         c_rows = ws->rows;
         c_inner = ws->inner_total;
         c_resc = ws->rescans;
@@ -319,8 +384,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             lk1 = a.list_key[kListCap + tid];
             li1 = a.list_idx[kListCap + tid];
         }
+        if (done0) return;  // uniform over the block
         const bool fast = lc0 >= half && lc1 >= half && lc0 <= kListCap &&
                           lc1 <= kListCap;
+        if (tid == 0 && a.list_cnt) {
+            c_stat[0] += lc0 < half;
+            c_stat[1] += lc1 < half;
+            c_stat[2] += lc0 > kListCap;
+            c_stat[3] += lc1 > kListCap;
+            c_stat[4] += lc0 > kPairSmall && lc0 <= kListCap;
+            c_stat[5] += lc1 > kPairSmall && lc1 <= kListCap;
+            if (fast) {
+                c_stat[6] += lc0;
+                c_stat[7] += lc1;
+            }
+        }
         if (fast) {
             if (tid < lc0) {
                 svk[0][tid] = lk0;
@@ -332,18 +410,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             }
             __syncthreads();
             t_l1 = wall_clock64();
-            const int lm = max(lc0, lc1);
-            if (lm <= 64) {
-                pair_rank_top<16>(svk, svi, lc0, lc1, half, upk, upi, lok, loi);
-            } else if (lm <= 128) {
-                pair_rank_top<8>(svk, svi, lc0, lc1, half, upk, upi, lok, loi);
-            } else if (lm <= kPairMax) {
-                pair_rank_top<4>(svk, svi, lc0, lc1, half, upk, upi, lok, loi);
-            } else {
-                if (wave == 0) wave_top(svk[0], svi[0], lc0, half, upk, upi);
-                if (wave == 1) wave_top(svk[1], svi[1], lc1, half, lok, loi);
-            }
-            __syncthreads();
+            top_half(svk, svi, lc0, lc1, half, upk, upi, lok, loi, nsv);
             t_l2 = wall_clock64();
             if (tid == 0) {
                 c_hits += 1;
@@ -434,9 +501,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             if (!overflow) {
                 // (4) rank the survivors: side 0 on threads [0,512), side 1
                 // on the rest
-                if (wave == 0) wave_top(svk[0], svi[0], M0, half, upk, upi);
-                if (wave == 1) wave_top(svk[1], svi[1], M1, half, lok, loi);
-                __syncthreads();
+                top_half(svk, svi, M0, M1, half, upk, upi, lok, loi, nsv);
             } else {
                 // (4') too many ties at the bound (e.g. alpha = 0): exact
                 // block rounds over all candidates
@@ -657,6 +722,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 ws->M = shMn;
             }
             ws->list_hits = c_hits;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) ws->stat[k] = c_stat[k];
             ws->slow_selects = c_slow;
             ws->rescans = c_resc;
             (void)t_end;

@@ -478,6 +478,12 @@ SolveResult Solver::train()
                     1e-3 * k * w.prof[6], 1e-3 * k * w.prof[7],
                     row_launches_ ? 1e3 * row_ms_ / row_launches_ : 0.0,
                     (long long)row_launches_);
+            if (atoi(e) > 1) {
+                fprintf(stderr, "[mi355svm] lists:");
+                for (int k = 0; k < 8; ++k)
+                    fprintf(stderr, " %lld", (long long)w.stat[k]);
+                fprintf(stderr, "\n");
+            }
         }
     }
     return r;
