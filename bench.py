@@ -196,7 +196,10 @@ def main() -> int:
         per = infos_of(m)
         info = dict(per[0])
         for k in ("train_ms", "iters", "kernel_rows", "row_kernel_ms",
-                  "row_kernel_launches", "n_sv_output"):
+                  "row_kernel_launches", "row_kernel_bytes",
+                  "cached_kernel_ms", "cached_kernel_launches",
+                  "cached_kernel_bytes", "cache_hits", "cache_fills",
+                  "n_sv_output"):
             info[k] = sum(x[k] for x in per)
         info["dual_obj"] = sum(x["dual_obj"] for x in per)
         info["gap"] = max(x["gap"] for x in per)
@@ -209,11 +212,19 @@ def main() -> int:
     wall = time.perf_counter() - t0
 
     rows = sum(i["kernel_rows"] for i in infos)
+    # roofline of the row/update kernel over its launches that compute the
+    # rows from X (launches served from the row cache are reported apart):
+    # algorithmic bytes (features, norm, F, state; plus the rows written to
+    # the cache) over the kernel's own time
     launches = sum(i["row_kernel_launches"] for i in infos)
     row_ms = sum(i["row_kernel_ms"] for i in infos)
+    row_bytes = sum(i["row_kernel_bytes"] for i in infos)
     avg_ms = row_ms / max(launches, 1)
-    bytes_launch = row_bytes_per_launch(w.n, w.d, w.type == workloads.EPS_SVR)
-    achieved = bytes_launch / (avg_ms * 1e-3) / 1e9 if launches else 0.0
+    bytes_launch = row_bytes / max(launches, 1)
+    achieved = row_bytes / (row_ms * 1e-3) / 1e9 if row_ms > 0 else 0.0
+    c_launches = sum(i["cached_kernel_launches"] for i in infos)
+    c_ms = sum(i["cached_kernel_ms"] for i in infos)
+    c_bytes = sum(i["cached_kernel_bytes"] for i in infos)
 
     last = infos[-1]
     Dn = D.cpu().numpy()
@@ -267,7 +278,17 @@ def main() -> int:
             "traffic": measured_traffic(w.name),
             "avg_launch_us": 1e3 * avg_ms,
             "bytes_per_launch": bytes_launch,
+            "bytes_per_launch_no_cache_fill": row_bytes_per_launch(
+                w.n, w.d, w.type == workloads.EPS_SVR),
             "launches_timed": launches,
+        },
+        "row_cache": {
+            "rows_served": last["cache_hits"],
+            "rows_filled": last["cache_fills"],
+            "rows_used": last["kernel_rows"],
+            "cached_launches": c_launches,
+            "cached_avg_launch_us": 1e3 * c_ms / max(c_launches, 1),
+            "cached_GBps": c_bytes / (c_ms * 1e-3) / 1e9 if c_ms > 0 else 0.0,
         },
     }
     if not args.no_cpu_baseline:

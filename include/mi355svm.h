@@ -115,12 +115,19 @@ typedef struct {
     double gap;            /* final m - M */
     double b;              /* bias */
     double dual_obj;       /* f(a) of Eq. 2 */
-    int64_t kernel_rows;   /* kernel rows K(x_s, X) evaluated */
+    int64_t kernel_rows;   /* kernel rows K(x_s, X) used (computed + cached) */
     int64_t cache_hits;    /* kernel rows served by the row cache */
+    int64_t cache_fills;   /* kernel rows written to the row cache */
     double train_ms;       /* device time from solver start to model ready */
-    double row_kernel_ms;  /* summed row/update kernel time (profile = 1) */
+    /* profile = 1: row/update kernel launches that computed the rows from X */
+    double row_kernel_ms;        /* summed kernel time */
     int64_t row_kernel_launches; /* launches included in row_kernel_ms */
-    int64_t row_kernel_rows;     /* rows processed by those launches */
+    int64_t row_kernel_rows;     /* rows of X processed by those launches */
+    double row_kernel_bytes;     /* their algorithmic HBM bytes */
+    /* profile = 1: launches served entirely from the row cache */
+    double cached_kernel_ms;
+    int64_t cached_kernel_launches;
+    double cached_kernel_bytes;
 } svm_model_info;
 
 typedef struct svm_model svm_model;  /* opaque, owned by the library */

@@ -114,11 +114,16 @@ void fill_info(svm_model_info& in, const svm_model& m,
     in.b = r.b;
     in.dual_obj = r.obj;
     in.kernel_rows = r.kernel_rows;
-    in.cache_hits = 0;
+    in.cache_hits = r.cache_served;
+    in.cache_fills = r.cache_filled;
     in.train_ms = r.train_ms;
     in.row_kernel_ms = r.row_ms;
     in.row_kernel_launches = r.row_launches;
     in.row_kernel_rows = r.row_rows;
+    in.row_kernel_bytes = r.row_bytes;
+    in.cached_kernel_ms = r.cached_ms;
+    in.cached_kernel_launches = r.cached_launches;
+    in.cached_kernel_bytes = r.cached_bytes;
 }
 
 // Leaves HIP's per-thread last-error slot clean on every exit, so that an
@@ -204,7 +209,9 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
                                         : hipMemcpyHostToDevice,
                            cx.stream));
     msvm::SolveOptions o = msvm::make_options(p, X->n, X->d);
-    msvm::Solver s(cx, f, yd.p, o);
+    msvm::RowCache rc;
+    msvm::cache_init(rc, X->n, p->cache_bytes, cx);
+    msvm::Solver s(cx, f, yd.p, o, &rc);
     msvm::SolveResult r = s.train();
 
     auto m = std::make_unique<svm_model>();
@@ -295,9 +302,12 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     msvm::DevBuf<float> yc((size_t)n);
     std::vector<msvm::SolveResult> res((size_t)n_classes);
     svm_status worst = SVM_OK;
+    // one row cache for all classes: the kernel rows do not depend on labels
+    msvm::RowCache rc;
+    msvm::cache_init(rc, n, p->cache_bytes, cx);
     for (int32_t c = 0; c < n_classes; ++c) {
         msvm::launch_ovr_labels(ld.p, n, c, yc.p, cx.stream);
-        msvm::Solver s(cx, f, yc.p, o);
+        msvm::Solver s(cx, f, yc.p, o, &rc);
         res[(size_t)c] = s.train();
         s.coefficients(coef.p, n_classes, c);
         m->b[(size_t)c] = res[(size_t)c].b;

@@ -30,6 +30,14 @@ constexpr int kListCap = 1024;     // threshold list entries per side
 constexpr int kWaveList = 16;      // threshold list entries per side per wave
 constexpr double kTau = 1e-12;     // curvature floor of a degenerate pair
 
+// how the row kernel of an iteration gets K(x_i, x_s) (set by the selection)
+enum : int32_t {
+    PATH_STREAM = 0,  // computed from X
+    PATH_INSERT = 1,  // computed from X; rows of missing samples go to the cache
+    PATH_CACHED = 2   // every sample of the working set is cached: rows read
+};
+constexpr int kPathLog = 256;  // iterations of path history kept (profiling)
+
 // state byte of a dual variable
 constexpr uint8_t ST_YPOS = 1;  // y_t = +1
 constexpr uint8_t ST_UP = 2;    // t in I_up
@@ -61,6 +69,16 @@ struct WorkingSet {
     double spread[2];     // distance of each threshold below the q/2-th key
     int64_t prof[12];     // select/solve phase times (wall-clock ticks)
     int64_t stat[8];      // selection statistics (threshold list use)
+    // kernel-row cache
+    int32_t path;             // PATH_* of the current iteration
+    int32_t pad2;
+    int32_t cslot[kMaxQ];     // cache slot of each working-set slot (cached:
+                              // source; insert: destination or -1)
+    int64_t cache_served;     // kernel rows read from the cache
+    int64_t cache_filled;     // kernel rows written to the cache
+    uint8_t path_log[kPathLog];  // path of iteration t at [t % kPathLog]
+    uint8_t fill_log[kPathLog];  // rows written to the cache by iteration t
+    uint8_t ns_log[kPathLog];    // distinct samples of iteration t
 };
 
 // Final reductions of a state (bias and objective).
@@ -102,6 +120,8 @@ struct RowArgs {
     double* list_key;     // [2][kListCap] keys at or above ws->theta
     int32_t* list_idx;
     int32_t* list_cnt;    // [2] entries appended (> kListCap: overflow)
+    float* cache;         // kernel-row cache rows (stride ldc), or nullptr
+    int64_t ldc;
     int64_t n, ldp;
     double eps;
     float gexp;           // gamma * log2(e)
@@ -136,6 +156,12 @@ struct SelArgs {
     int32_t mode;
     int32_t group_rows;   // rows behind one candidate list (one k_rows wave)
     int32_t slice;        // features per LDS slice of the working-set rows
+    // kernel-row cache (cache_slots == 0: none)
+    const float* cache;   // cache_slots rows of ldc floats
+    int64_t ldc, cache_slots;
+    int32_t* slot_of;     // n: cache slot of each sample, or -1
+    int32_t* owner;       // cache_slots: sample held by each slot, or -1
+    int64_t* clock;       // next replacement candidate (FIFO)
 };
 
 struct PredictArgs {

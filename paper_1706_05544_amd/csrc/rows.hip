@@ -48,10 +48,14 @@ __host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp)
 // per-wave threshold list: kWaveList (key, index) pairs per side
 constexpr int kWaveListBytes = 2 * kWaveList * (8 + 4);
 
+// per-block table of the working-set slots: norm, sample, cache slot
+constexpr int kSlotInfoBytes = kMaxQ * (4 + 4 + 4);
+
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
 {
     return rows_aux_offset(nblk_cols, ldp) +
-           (size_t)kRowWaves * (rows_aux_bytes(tiles, svr) + kWaveListBytes);
+           (size_t)kRowWaves * (rows_aux_bytes(tiles, svr) + kWaveListBytes) +
+           kSlotInfoBytes;
 }
 
 // Running best two (score, variable) of one lane, in the order of better().
@@ -143,18 +147,11 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     // working-set slot b * 16 + nl of this lane (slots past nS contribute 0)
     const int nS = XS ? (a.nS_override >= 0 ? a.nS_override : ws->nS) : 0;
     double cf[NBLK];
-    float ssl[NBLK];
-    int32_t sidx[NBLK];
 #pragma unroll
     for (int b = 0; b < NBLK; ++b) {
         const int slot = b * 16 + nl;  // < kMaxQ: always inside the arrays
-        const bool ok = slot < nS;
         const double c = ws->coef[slot];
-        const float s = ws->sS[slot];
-        const int32_t i = ws->S[slot];
-        cf[b] = (ok && UPD) ? c : 0.0;
-        ssl[b] = ok ? s : 0.0f;
-        sidx[b] = ok ? i : -1;
+        cf[b] = (slot < nS && UPD) ? c : 0.0;
     }
 
     // rows of this wave: rw0 .. rw0 + nw - 1, in Tw tiles of 16
@@ -178,6 +175,12 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         th[1] = ws->theta[1];
     }
     int nlist[2] = {0, 0};  // wave-uniform entry counts
+    // slot table (block-wide): norm, sample and cache slot of every slot
+    unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp) +
+                           kRowWaves * (rows_aux_bytes(T, SVR) + kWaveListBytes);
+    float* sl_sq = reinterpret_cast<float*>(sinfo);
+    int32_t* sl_smp = reinterpret_cast<int32_t*>(sinfo + 4 * kMaxQ);
+    int32_t* sl_cs = reinterpret_cast<int32_t*>(sinfo + 8 * kMaxQ);
 
     // row data of rows k0 .. k0 + 255 of the wave: issue, then store to LDS
     struct AuxRegs {
@@ -257,81 +260,26 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     };
 
     if (XS) {
-        // Staged working-set rows: every slot (finite values past nS),
-        // zero-filled to whole 16-feature chunks.
-        const int q4 = (xstride - 4) >> 2;  // float4 per staged row
-        const int xs_total = NBLK * 16 * q4;
-        const Rsrc rXs = make_rsrc(a.xS, (int64_t)NBLK * 16 * ldp * 4);
-        auto xs_off = [&](int e) -> uint32_t {
-            const int slot = e / q4, c4 = e - slot * q4;
-            return (e < xs_total && 4 * c4 < ldp)
-                       ? (uint32_t)((slot * ldp + 4 * c4) * 4)
-                       : kOob;
-        };
-        auto xs_put = [&](int e, float4 v) {
-            const int slot = e / q4, c4 = e - slot * q4;
-            if (e < xs_total)
-                *reinterpret_cast<float4*>(xsl + slot * xstride + 4 * c4) = v;
-        };
+        // Path of this iteration (hot mode: set by the selection; tests:
+        // always computed from X) and the cache slot of this lane's
+        // working-set slots.
+        const int32_t path = LIST ? ws->path : PATH_STREAM;
 
-        const int nslab = (ldp + 63) >> 6;
-        const Rsrc rX = make_rsrc(a.X + rw0 * ldp, (int64_t)nw * ldp * 4);
-        float* wbuf = xsl + NBLK * 16 * xstride + wave * (16 * kSlabStride);
-        const uint32_t step4 = (uint32_t)(16 * ldp);  // 4 rows, in bytes
-        int fti = 0, fsl = 0;  // next slab to fetch
-        auto fetch = [&](float4 (&v)[4]) {
-            const int col = fsl * 64 + 4 * nl;
-            const bool ok = fti < Tw && col < ldp;
-            const uint32_t o = (uint32_t)(((16 * fti + g) * ldp + col) * 4);
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                v[rr] = bld_f4(rX, ok ? o + rr * step4 : kOob);
-            if (++fsl == nslab) {
-                fsl = 0;
-                ++fti;
-            }
-        };
-
-        // Everything the first slabs need is requested at once: the first
-        // staging loads, the row data and kRing feature slabs.
-        float4 xv[kXsEarly];
-#pragma unroll
-        for (int i = 0; i < kXsEarly; ++i)
-            xv[i] = bld_f4(rXs, xs_off(tid + i * kRowThreads));
-        AuxRegs ar;
-        aux_issue(0, ar);
-        float4 ring[kRing][4];
-#pragma unroll
-        for (int j = 0; j < kRing; ++j) fetch(ring[j]);
-        if (done) return;  // uniform over the block
-#pragma unroll
-        for (int i = 0; i < kXsEarly; ++i) xs_put(tid + i * kRowThreads, xv[i]);
-        aux_store(0, ar);
-        for (int k0 = 256; k0 < RW; k0 += 256) {
-            aux_issue(k0, ar);
-            aux_store(k0, ar);
-        }
-        for (int e = tid + kXsEarly * kRowThreads; e < xs_total;
-             e += kRowThreads)
-            xs_put(e, bld_f4(rXs, xs_off(e)));
-        __syncthreads();
-
-        floatx4 acc[NBLK];
-        auto epilogue = [&](int ti) {
+        // F_i += sum_s cf_s K(x_i, x_s) for the 16 rows of tile ti, given
+        // this lane's K values kv[b][v] (row lr + v of slot b * 16 + nl),
+        // then the keys of the tile's variables.  The same code (and fp64
+        // order) whether K was computed or read from the cache.
+        auto finish_tile = [&](int ti, const float (&kv)[NBLK][4]) {
             const int lr = 16 * ti + 4 * g;
-            const float4 q4v = *reinterpret_cast<const float4*>(sqw + lr);
-            const float qv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
             double part[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int b = 0; b < NBLK; ++b) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    float kv = rbf_from_dot(qv[v], ssl[b], acc[b][v], a.gexp);
-                    if (rw0 + lr + v == (int64_t)sidx[b]) kv = 1.0f;
-                    part[v] = fma(cf[b], (double)kv, part[v]);
+                    part[v] = fma(cf[b], (double)kv[b][v], part[v]);
                     if (ROWS && b * 16 + nl < nS && lr + v < nw)
                         a.rows_out[(int64_t)(b * 16 + nl) * n + rw0 + lr + v] =
-                            kv;
+                            kv[b][v];
                 }
             }
             const int orl = lr + (nl & 3);  // row owned by lanes nl < 4
@@ -346,43 +294,206 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             if (CAND) push(orl, Fn, nl < 4 && orl < nw);
         };
 
-        int pti = 0, psl = 0;  // slab being processed
-        for (int s0 = 0; s0 < Tw * nslab; s0 += kRing) {
-            // all kRing slots every trip (slabs past the end are zeros and
-            // touch no memory), so the loads in flight are countable
+        if (LIST && path == PATH_CACHED) {
+            // Every working-set sample is cached: lane (g, nl) reads rows
+            // lr .. lr + 3 of its slot's row as one float4, kRing tiles
+            // ahead.  Unused slots read a valid address and are zeroed.
+            int32_t cs[NBLK];
 #pragma unroll
-            for (int j = 0; j < kRing; ++j) {
-                if (psl == 0) {
+            for (int b = 0; b < NBLK; ++b) {
+                const int32_t c = ws->cslot[b * 16 + nl];
+                cs[b] = b * 16 + nl < nS ? c : -1;
+            }
+            const float* crow[NBLK];
 #pragma unroll
-                    for (int b = 0; b < NBLK; ++b)
-                        acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+            for (int b = 0; b < NBLK; ++b)
+                crow[b] = a.cache + (int64_t)(cs[b] >= 0 ? cs[b] : 0) * a.ldc +
+                          (nw > 0 ? rw0 : 0);
+            auto cfetch = [&](int ti, float4 (&v)[NBLK]) {
+                const int t = min(ti, max(Tw - 1, 0));  // a valid tile
+#pragma unroll
+                for (int b = 0; b < NBLK; ++b)
+                    v[b] = ld4(crow[b] + 16 * t + 4 * g);
+            };
+            float4 ring[kRing][NBLK];
+#pragma unroll
+            for (int j = 0; j < kRing; ++j) cfetch(j, ring[j]);
+            AuxRegs ar;
+            aux_issue(0, ar);
+            if (done) return;  // uniform over the block
+            aux_store(0, ar);
+            for (int k0 = 256; k0 < RW; k0 += 256) {
+                aux_issue(k0, ar);
+                aux_store(k0, ar);
+            }
+            for (int t0 = 0; t0 < Tw; t0 += kRing) {
+#pragma unroll
+                for (int j = 0; j < kRing; ++j) {
+                    float kv[NBLK][4];
+#pragma unroll
+                    for (int b = 0; b < NBLK; ++b) {
+                        const float4 c = ring[j][b];
+                        const bool ok = cs[b] >= 0;
+                        kv[b][0] = ok ? c.x : 0.0f;
+                        kv[b][1] = ok ? c.y : 0.0f;
+                        kv[b][2] = ok ? c.z : 0.0f;
+                        kv[b][3] = ok ? c.w : 0.0f;
+                    }
+                    cfetch(t0 + j + kRing, ring[j]);
+                    if (t0 + j < Tw) finish_tile(t0 + j, kv);
                 }
+            }
+        } else {
+            // Staged working-set rows: every slot (finite values past nS),
+            // zero-filled to whole 16-feature chunks.
+            const int q4 = (xstride - 4) >> 2;  // float4 per staged row
+            const int xs_total = NBLK * 16 * q4;
+            const Rsrc rXs = make_rsrc(a.xS, (int64_t)NBLK * 16 * ldp * 4);
+            auto xs_off = [&](int e) -> uint32_t {
+                const int slot = e / q4, c4 = e - slot * q4;
+                return (e < xs_total && 4 * c4 < ldp)
+                           ? (uint32_t)((slot * ldp + 4 * c4) * 4)
+                           : kOob;
+            };
+            auto xs_put = [&](int e, float4 v) {
+                const int slot = e / q4, c4 = e - slot * q4;
+                if (e < xs_total)
+                    *reinterpret_cast<float4*>(xsl + slot * xstride + 4 * c4) =
+                        v;
+            };
+
+            const int nslab = (ldp + 63) >> 6;
+            const Rsrc rX = make_rsrc(a.X + rw0 * ldp, (int64_t)nw * ldp * 4);
+            float* wbuf = xsl + NBLK * 16 * xstride + wave * (16 * kSlabStride);
+            const uint32_t step4 = (uint32_t)(16 * ldp);  // 4 rows, in bytes
+            int fti = 0, fsl = 0;  // next slab to fetch
+            auto fetch = [&](float4 (&v)[4]) {
+                const int col = fsl * 64 + 4 * nl;
+                const bool ok = fti < Tw && col < ldp;
+                const uint32_t o = (uint32_t)(((16 * fti + g) * ldp + col) * 4);
 #pragma unroll
                 for (int rr = 0; rr < 4; ++rr)
-                    *reinterpret_cast<float4*>(
-                        wbuf + (4 * rr + g) * kSlabStride + 4 * nl) =
-                        ring[j][rr];
-                fetch(ring[j]);  // refill the slot kRing slabs ahead
-                __builtin_amdgcn_wave_barrier();
+                    v[rr] = bld_f4(rX, ok ? o + rr * step4 : kOob);
+                if (++fsl == nslab) {
+                    fsl = 0;
+                    ++fti;
+                }
+            };
+
+            // Everything the first slabs need is requested at once: the
+            // first staging loads, the slot table, the row data and kRing
+            // feature slabs.
+            float sq0 = 0.0f;
+            int32_t smp0 = -1, cs0 = -1;
+            if (tid < NBLK * 16) {
+                const float q = ws->sS[tid];
+                const int32_t i = ws->S[tid], c = ws->cslot[tid];
+                sq0 = tid < nS ? q : 0.0f;
+                smp0 = tid < nS ? i : -1;
+                cs0 = (LIST && tid < nS) ? c : -1;
+            }
+            float4 xv[kXsEarly];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int ch = psl * 4 + c;
-                    if (ch * 16 < ldp) {  // chunk present (uniform)
-                        const float4 av =
-                            ld4(wbuf + nl * kSlabStride + c * 16 + 4 * g);
+            for (int i = 0; i < kXsEarly; ++i)
+                xv[i] = bld_f4(rXs, xs_off(tid + i * kRowThreads));
+            AuxRegs ar;
+            aux_issue(0, ar);
+            float4 ring[kRing][4];
 #pragma unroll
-                        for (int b = 0; b < NBLK; ++b) {
-                            const float4 bv = ld4(xsl + (b * 16 + nl) * xstride +
-                                                  ch * 16 + 4 * g);
-                            acc[b] = mfma_chunk(acc[b], av, bv);
+            for (int j = 0; j < kRing; ++j) fetch(ring[j]);
+            if (done) return;  // uniform over the block
+#pragma unroll
+            for (int i = 0; i < kXsEarly; ++i)
+                xs_put(tid + i * kRowThreads, xv[i]);
+            aux_store(0, ar);
+            if (tid < NBLK * 16) {
+                sl_sq[tid] = sq0;
+                sl_smp[tid] = smp0;
+                sl_cs[tid] = cs0;
+            }
+            for (int k0 = 256; k0 < RW; k0 += 256) {
+                aux_issue(k0, ar);
+                aux_store(k0, ar);
+            }
+            for (int e = tid + kXsEarly * kRowThreads; e < xs_total;
+                 e += kRowThreads)
+                xs_put(e, bld_f4(rXs, xs_off(e)));
+            __syncthreads();
+
+            // The slab loop; on the insert path the rows of the samples
+            // missing from the cache also go to their new cache slots.
+            {
+                const bool INS = LIST && path == PATH_INSERT;
+                floatx4 acc[NBLK];
+                int pti = 0, psl = 0;  // slab being processed
+                for (int s0 = 0; s0 < Tw * nslab; s0 += kRing) {
+                    // all kRing slots every trip (slabs past the end are
+                    // zeros and touch no memory), so the loads in flight
+                    // are countable
+#pragma unroll
+                    for (int j = 0; j < kRing; ++j) {
+                        if (psl == 0) {
+#pragma unroll
+                            for (int b = 0; b < NBLK; ++b)
+                                acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+                        }
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr)
+                            *reinterpret_cast<float4*>(
+                                wbuf + (4 * rr + g) * kSlabStride + 4 * nl) =
+                                ring[j][rr];
+                        fetch(ring[j]);  // refill the slot kRing slabs ahead
+                        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            const int ch = psl * 4 + c;
+                            if (ch * 16 < ldp) {  // chunk present (uniform)
+                                const float4 av = ld4(wbuf + nl * kSlabStride +
+                                                      c * 16 + 4 * g);
+#pragma unroll
+                                for (int b = 0; b < NBLK; ++b) {
+                                    const float4 bv =
+                                        ld4(xsl + (b * 16 + nl) * xstride +
+                                            ch * 16 + 4 * g);
+                                    acc[b] = mfma_chunk(acc[b], av, bv);
+                                }
+                            }
+                        }
+                        __builtin_amdgcn_wave_barrier();
+                        if (psl == nslab - 1 && pti < Tw) {
+                            const int lr = 16 * pti + 4 * g;
+                            const float4 q4v =
+                                *reinterpret_cast<const float4*>(sqw + lr);
+                            const float qv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
+                            float kv[NBLK][4];
+#pragma unroll
+                            for (int b = 0; b < NBLK; ++b) {
+                                const float ssb = sl_sq[b * 16 + nl];
+                                const int32_t smb = sl_smp[b * 16 + nl];
+#pragma unroll
+                                for (int v = 0; v < 4; ++v) {
+                                    float k = rbf_from_dot(qv[v], ssb,
+                                                           acc[b][v], a.gexp);
+                                    if (rw0 + lr + v == (int64_t)smb) k = 1.0f;
+                                    kv[b][v] = k;
+                                }
+                                // rows lr .. lr+3 of a row stored padded to
+                                // ldc (a multiple of 4): in bounds when row
+                                // lr is
+                                const int32_t csb = INS ? sl_cs[b * 16 + nl] : -1;
+                                if (csb >= 0 && rw0 + lr < n)
+                                    *reinterpret_cast<float4*>(
+                                        a.cache + (int64_t)csb * a.ldc + rw0 +
+                                        lr) = make_float4(kv[b][0], kv[b][1],
+                                                          kv[b][2], kv[b][3]);
+                            }
+                            finish_tile(pti, kv);
+                        }
+                        if (++psl == nslab) {
+                            psl = 0;
+                            ++pti;
                         }
                     }
-                }
-                __builtin_amdgcn_wave_barrier();
-                if (psl == nslab - 1 && pti < Tw) epilogue(pti);
-                if (++psl == nslab) {
-                    psl = 0;
-                    ++pti;
                 }
             }
         }

@@ -329,6 +329,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     __shared__ float KSS[QS][QS + 1];
     __shared__ double shDc[kMaxQ];
     __shared__ int32_t shNB, shNS, shGo, shDone;
+
     __shared__ double shGap, shMx, shMn;
     extern __shared__ __align__(16) float xst[];  // QS x (slice + 4)
 
@@ -347,11 +348,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     uint64_t t_l1 = 0, t_l2 = 0;  // (list path) entries staged, ranked
     double spr[2] = {0.0, 0.0};
     int64_t c_stat[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+
     if (tid == 0) {
         spr[0] = ws->spread[0];
         spr[1] = ws->spread[1];
 #pragma unroll
         for (int k = 0; k < 8; ++k) c_stat[k] = ws->stat[k];
+
         c_rows = ws->rows;
         c_inner = ws->inner_total;
         c_resc = ws->rescans;
@@ -763,7 +766,22 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     }
 
     uint64_t t_stage = 0;
-    // (10) K_SS on the matrix cores (same operand order as k_rows).  The
+    // Kernel-row cache (wave 1): the slot of each working-set sample,
+    // looked up while the working-set rows load.
+    const bool use_cache =
+        a.cache_slots > 0 && (a.mode & SS_SOLVE) && !given && wave == 1;
+    int32_t hslot = -1;
+    int64_t clk0 = 0, c_served = 0, c_filled = 0;
+    if (use_cache) {
+        if (lane < nS) hslot = a.slot_of[shS[lane]];
+        clk0 = *a.clock;
+    }
+    if (wave == 1 && lane == 0) {
+        c_served = ws->cache_served;
+        c_filled = ws->cache_filled;
+    }
+
+    // (10) K_SS on the matrix cores (same operand order as k_rows): the
     // working-set rows pass through LDS in feature slices: every thread
     // loads a piece into LDS; then the NBLK^2 matrix-core waves accumulate
     // the slice while the other waves copy it to xS (the rows of the next
@@ -861,6 +879,56 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     const uint64_t t_kss = wall_clock64();
 
     if (wave != 0) {
+        if (wave == 1 && (a.mode & SS_SOLVE) && !given) {
+            // The path of this iteration's row kernel (while wave 0
+            // solves): a working set whose samples are all cached is served
+            // from the cache; otherwise each missing sample gets a slot
+            // (FIFO, never a slot this working set reads) and the row
+            // kernel fills it.
+            int path = PATH_STREAM, nfill = 0;
+            int32_t cslot = -1;
+            if (use_cache) {
+                const int32_t hs = lane < nS ? hslot : -2;
+                const unsigned long long missm = __ballot(lane < nS && hs < 0);
+                int64_t clk = clk0;
+                if (missm == 0) {
+                    path = PATH_CACHED;
+                    cslot = hs;
+                } else {
+                    path = PATH_INSERT;
+                    unsigned long long mm = missm;
+                    while (mm) {
+                        const int k = __ffsll(mm) - 1;
+                        mm &= mm - 1;
+                        int32_t v;
+                        do {
+                            v = (int32_t)clk;
+                            clk = clk + 1 >= a.cache_slots ? 0 : clk + 1;
+                        } while (__ballot(lane < nS && hs == v) != 0);
+                        if (lane == k) cslot = v;
+                    }
+                    nfill = __popcll(missm);
+                    if (lane < nS && cslot >= 0) {
+                        const int32_t smp = shS[lane];
+                        const int32_t old = a.owner[cslot];
+                        if (old >= 0) a.slot_of[old] = -1;
+                        a.owner[cslot] = smp;
+                        a.slot_of[smp] = cslot;
+                    }
+                    if (lane == 0) *a.clock = clk;
+                }
+            }
+            if (lane < nS) ws->cslot[lane] = cslot;
+            if (lane == 0) {
+                ws->path = path;
+                const int64_t t = (iter0 + 1) % kPathLog;
+                ws->path_log[t] = (uint8_t)path;
+                ws->fill_log[t] = (uint8_t)nfill;
+                ws->ns_log[t] = (uint8_t)nS;
+                ws->cache_served = c_served + (path == PATH_CACHED ? nS : 0);
+                ws->cache_filled = c_filled + nfill;
+            }
+        }
         const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
         const int W = a.slice;
         if (W >= ldp16) {

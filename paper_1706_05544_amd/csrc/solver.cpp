@@ -81,7 +81,9 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
     o.max_iter = p->max_iter > 0 ? p->max_iter
                                  : std::max<int64_t>(10000000, 100 * N);
     o.q = p->working_set;
-    o.check_every = p->check_every > 0 ? p->check_every : 64;
+    // (the per-iteration path history covers kPathLog iterations)
+    o.check_every = p->check_every > 0 ? std::min(p->check_every, kPathLog)
+                                       : 64;
     o.inner_ratio = p->inner_ratio > 0 ? p->inner_ratio : 0.1;
     o.max_inner = p->max_inner > 0 ? p->max_inner : 8 * p->working_set;
     o.profile = p->profile != 0;
@@ -92,9 +94,38 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
 // solver
 // ---------------------------------------------------------------------------
 
+void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
+{
+    c.slots = 0;
+    if (const char* e = getenv("SVM_CACHE_BYTES"))  // developer override
+        bytes = atoll(e);
+    if (bytes < 0 || n <= 0) return;
+    c.ldc = (n + 3) / 4 * 4;
+    const int64_t row = c.ldc * (int64_t)sizeof(float);
+    size_t free_b = 0, total_b = 0;
+    HIP_TRY(hipMemGetInfo(&free_b, &total_b));
+    int64_t cap = std::min<int64_t>((int64_t)(free_b / 4), (int64_t)8 << 30);
+    if (bytes > 0) cap = std::min<int64_t>(cap, bytes);
+    const int64_t slots = std::min<int64_t>(n, cap / row);
+    // a working set reads up to kMaxQ slots and the replacement needs a
+    // free one besides them
+    if (slots <= kMaxQ && slots < n) return;
+    if (slots < 2) return;
+    // (+16 floats: the row kernel reads whole 16-row tiles, up to 15 rows
+    // past the last sample, and the last row has nothing after it)
+    c.rows.alloc((size_t)(slots * c.ldc + 16));
+    c.slot_of.alloc((size_t)n);
+    c.owner.alloc((size_t)slots);
+    c.clock.alloc(1);
+    HIP_TRY(hipMemsetAsync(c.slot_of.p, 0xFF, c.slot_of.bytes(), cx.stream));
+    HIP_TRY(hipMemsetAsync(c.owner.p, 0xFF, c.owner.bytes(), cx.stream));
+    HIP_TRY(hipMemsetAsync(c.clock.p, 0, c.clock.bytes(), cx.stream));
+    c.slots = slots;
+}
+
 Solver::Solver(Context& cx, const Features& f, const float* y_dev,
-               const SolveOptions& o)
-    : cx_(cx), f_(f), o_(o)
+               const SolveOptions& o, RowCache* cache)
+    : cx_(cx), f_(f), o_(o), cache_(cache && cache->slots > 0 ? cache : nullptr)
 {
     n_ = f.n;
     N_ = o.type == SVM_EPS_SVR ? 2 * n_ : n_;
@@ -229,6 +260,10 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
     a.tiles = tiles_;
     a.mode = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
     a.nS_override = -1;
+    if (cache_) {
+        a.cache = cache_->rows.p;
+        a.ldc = cache_->ldc;
+    }
     launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream, e0,
                 e1);
 }
@@ -263,6 +298,14 @@ void Solver::launch_solve(int32_t mode)
     a.max_iter = o_.max_iter;
     a.mode = mode;
     a.group_rows = 16 * tiles_;
+    if (cache_) {
+        a.cache = cache_->rows.p;
+        a.ldc = cache_->ldc;
+        a.cache_slots = cache_->slots;
+        a.slot_of = cache_->slot_of.p;
+        a.owner = cache_->owner.p;
+        a.clock = cache_->clock.p;
+    }
     launch_select(a, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
 }
 
@@ -321,14 +364,32 @@ bool Solver::run_loop(SolveResult& r)
         const WorkingSet& w = hs.p[cur];
         if (o_.profile) {
             int64_t real = std::min<int64_t>(w.iter - last_iter, K);
+            // algorithmic bytes of a launch: computed from X, the features,
+            // norm, F read and written and the state byte(s) (eps-SVR: and
+            // the target) of every row, plus the rows written to the cache;
+            // served from the cache, the nS cached rows instead of X and
+            // the norms
+            const bool svr = o_.type == SVM_EPS_SVR;
+            const double per_row = 16.0 + (svr ? 6.0 : 1.0);
             for (int64_t k = 0; k < real; ++k) {
                 float ms = 0.f;
                 HIP_TRY(hipEventElapsedTime(
                     &ms, pe[(size_t)(cur * K + k) * 2],
                     pe[(size_t)(cur * K + k) * 2 + 1]));
-                row_ms_ += ms;
-                row_launches_ += 1;
-                row_rows_ += n_;
+                const int64_t t = (last_iter + k + 1) % kPathLog;
+                if (w.path_log[t] == PATH_CACHED) {
+                    cached_ms_ += ms;
+                    cached_launches_ += 1;
+                    cached_bytes_ +=
+                        (double)n_ * (per_row + 4.0 * (double)w.ns_log[t]);
+                } else {
+                    row_ms_ += ms;
+                    row_launches_ += 1;
+                    row_rows_ += n_;
+                    row_bytes_ +=
+                        (double)n_ * (per_row + 4.0 + 4.0 * (double)f_.d +
+                                      4.0 * (double)w.fill_log[t]);
+                }
             }
         }
         if (w.done) break;
@@ -449,22 +510,31 @@ SolveResult Solver::train()
     r.row_ms = row_ms_;
     r.row_launches = row_launches_;
     r.row_rows = row_rows_;
+    r.row_bytes = row_bytes_;
+    r.cached_ms = cached_ms_;
+    r.cached_launches = cached_launches_;
+    r.cached_bytes = cached_bytes_;
     WorkingSet w;
     read_ws(w);
     r.kernel_rows = w.rows;
+    r.cache_served = w.cache_served;
+    r.cache_filled = w.cache_filled;
     r.iters = w.iter;
     if (const char* e = getenv("SVM_LOG")) {
         if (atoi(e) > 0 && w.prof[4] > 0) {
             const double k = 10.0 / (double)w.prof[4];  // 100 MHz ticks -> ns
             fprintf(stderr,
-                    "[mi355svm] iters=%lld rows=%lld inner=%.1f/iter "
+                    "[mi355svm] iters=%lld rows=%lld (cache: served %lld "
+                    "filled %lld) inner=%.1f/iter "
                     "rescans=%lld slow=%lld list=%lld select(us): merge %.2f "
                     "kss %.2f "
                     "inner %.2f "
                     "write %.2f (list merge %.2f = %.2f + %.2f + %.2f, build "
                     "%.2f stage %.2f); "
-                    "rows kernel %.2f us/launch (%lld timed)\n",
+                    "rows kernel %.2f us/launch (%lld timed), cached %.2f "
+                    "us/launch (%lld)\n",
                     (long long)w.iter, (long long)w.rows,
+                    (long long)w.cache_served, (long long)w.cache_filled,
                     (double)w.inner_total / (double)w.prof[4],
                     (long long)w.rescans, (long long)w.slow_selects,
                     (long long)w.list_hits,
@@ -477,7 +547,10 @@ SolveResult Solver::train()
                     w.list_hits ? 1e-2 * w.prof[10] / (double)w.list_hits : 0.0,
                     1e-3 * k * w.prof[6], 1e-3 * k * w.prof[7],
                     row_launches_ ? 1e3 * row_ms_ / row_launches_ : 0.0,
-                    (long long)row_launches_);
+                    (long long)row_launches_,
+                    cached_launches_ ? 1e3 * cached_ms_ / cached_launches_
+                                     : 0.0,
+                    (long long)cached_launches_);
             if (atoi(e) > 1) {
                 fprintf(stderr, "[mi355svm] lists:");
                 for (int k = 0; k < 8; ++k)

@@ -50,6 +50,25 @@ struct HostBuf {
     }
 };
 
+struct Context;
+
+// HBM-resident cache of kernel rows K(x_s, .) over all n samples, rows
+// padded to ldc floats.  The rows do not depend on the labels, so the
+// outputs of a one-vs-rest model share one cache.  Replacement is FIFO and
+// decided on the device (slot_of / owner maps, clock).
+struct RowCache {
+    int64_t slots = 0, ldc = 0;
+    DevBuf<float> rows;
+    DevBuf<int32_t> slot_of, owner;
+    DevBuf<int64_t> clock;
+};
+
+// Sizes and clears the cache for n samples.  bytes: 0 = default (the full
+// kernel matrix if it fits a quarter of the free device memory, at most
+// 8 GiB), > 0 = at most that many bytes (clamped likewise), < 0 = no cache.
+// Leaves slots = 0 when fewer rows than a working set needs would fit.
+void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx);
+
 // The device and stream of one call.
 struct Context {
     int device = 0;
@@ -92,16 +111,19 @@ struct SolveResult {
     double gap = 0, m = 0, M = 0, b = 0, obj = 0;
     int64_t n_free = 0, n_bounded = 0, n_sv = 0;
     int64_t kernel_rows = 0;
+    int64_t cache_served = 0, cache_filled = 0;
     double train_ms = 0;
-    double row_ms = 0;
-    int64_t row_launches = 0, row_rows = 0;
+    // profiled row-kernel launches: computed from X, and served from cache
+    double row_ms = 0, cached_ms = 0;
+    int64_t row_launches = 0, row_rows = 0, cached_launches = 0;
+    double row_bytes = 0, cached_bytes = 0;
 };
 
 class Solver {
 public:
     // y: device pointer to n labels (+-1) or targets.  Features are shared.
     Solver(Context& cx, const Features& f, const float* y_dev,
-           const SolveOptions& o);
+           const SolveOptions& o, RowCache* cache = nullptr);
 
     // Full training run: initial keys, iterations, final recompute, bias.
     SolveResult train();
@@ -157,8 +179,9 @@ private:
     DevBuf<int64_t> sv_cnt_;
     DevBuf<float> sv_rows_, sv_sq_;
     DevBuf<float> rows_out_;
-    double row_ms_ = 0;
-    int64_t row_launches_ = 0, row_rows_ = 0;
+    RowCache* cache_ = nullptr;
+    double row_ms_ = 0, cached_ms_ = 0, row_bytes_ = 0, cached_bytes_ = 0;
+    int64_t row_launches_ = 0, row_rows_ = 0, cached_launches_ = 0;
 };
 
 }  // namespace msvm

@@ -75,10 +75,15 @@ class svm_model_info(ct.Structure):
                 ("n_bounded", ct.c_int64), ("iters", ct.c_int64),
                 ("gap", ct.c_double), ("b", ct.c_double),
                 ("dual_obj", ct.c_double), ("kernel_rows", ct.c_int64),
-                ("cache_hits", ct.c_int64), ("train_ms", ct.c_double),
+                ("cache_hits", ct.c_int64), ("cache_fills", ct.c_int64),
+                ("train_ms", ct.c_double),
                 ("row_kernel_ms", ct.c_double),
                 ("row_kernel_launches", ct.c_int64),
-                ("row_kernel_rows", ct.c_int64)]
+                ("row_kernel_rows", ct.c_int64),
+                ("row_kernel_bytes", ct.c_double),
+                ("cached_kernel_ms", ct.c_double),
+                ("cached_kernel_launches", ct.c_int64),
+                ("cached_kernel_bytes", ct.c_double)]
 
     def as_dict(self) -> dict:
         return {k: getattr(self, k) for k, _ in self._fields_}
