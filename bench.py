@@ -146,9 +146,19 @@ def main() -> int:
     log("workload %s: n=%d d=%d n_test=%d" % (w.name, w.n, w.d,
                                              w.Xt.shape[0]))
     dev = torch.device("cuda:0")
-    X = torch.from_numpy(w.X).to(dev)
+
+    def to_device(A):
+        if hasattr(A, "indptr"):  # scipy CSR -> torch sparse CSR in HBM
+            return torch.sparse_csr_tensor(
+                torch.from_numpy(A.indptr.astype(np.int64)),
+                torch.from_numpy(A.indices.astype(np.int64)),
+                torch.from_numpy(A.data.astype(np.float32)), size=A.shape,
+                device=dev)
+        return torch.from_numpy(A).to(dev)
+
+    X = to_device(w.X)
     y = torch.from_numpy(w.y).to(dev)
-    Xt = torch.from_numpy(w.Xt).to(dev)
+    Xt = to_device(w.Xt)
     torch.cuda.synchronize()
     kw = dict(type=w.type, C=w.C, epsilon=w.eps, gamma=w.gamma, tol=w.tol,
               working_set=args.working_set)
@@ -251,11 +261,13 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "%s: %s RBF, dense n=%d d=%d, C=%g, gamma=%g, "
+            "workload": "%s: %s RBF, %s n=%d d=%d, C=%g, gamma=%g, "
                         "tol=%g, q=%d; predict %d points"
                         % (w.name, ("one-vs-rest %d-class C-SVC" % w.n_classes)
                            if multi else
                            ("C-SVC" if w.type == 0 else "eps-SVR"),
+                           ("CSR (%d nonzeros)" % w.X.nnz)
+                           if hasattr(w.X, "indptr") else "dense",
                            w.n, w.d, w.C, w.gamma, w.tol, args.working_set,
                            w.Xt.shape[0]),
             "n": w.n, "d": w.d, "n_test": int(w.Xt.shape[0]),
@@ -278,8 +290,9 @@ def main() -> int:
             "traffic": measured_traffic(w.name),
             "avg_launch_us": 1e3 * avg_ms,
             "bytes_per_launch": bytes_launch,
-            "bytes_per_launch_no_cache_fill": row_bytes_per_launch(
-                w.n, w.d, w.type == workloads.EPS_SVR),
+            "bytes_per_launch_no_cache_fill": (
+                row_bytes_per_launch(w.n, w.d, w.type == workloads.EPS_SVR)
+                if not hasattr(w.X, "indptr") else None),
             "launches_timed": launches,
         },
         "row_cache": {

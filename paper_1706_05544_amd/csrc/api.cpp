@@ -60,10 +60,16 @@ svm_status check_matrix(const svm_matrix* X, int64_t min_rows)
                                        : "X rows must be >= 0");
     if (X->d < 1 || X->d > (int64_t)1 << 30)
         return fail(SVM_E_INVALID, "d must be in [1, 2^30]");
-    if (X->layout == SVM_CSR)
-        return fail(SVM_E_UNSUPPORTED, "CSR input is not implemented yet");
-    if (X->n > 0 && !X->values) return fail(SVM_E_INVALID, "X values is NULL");
-    if (X->ld < X->d) return fail(SVM_E_INVALID, "ld must be >= d");
+    if (X->layout == SVM_CSR) {
+        if (!X->row_ptr) return fail(SVM_E_INVALID, "CSR row_ptr is NULL");
+        if (X->nnz < 0) return fail(SVM_E_INVALID, "CSR nnz must be >= 0");
+        if (X->nnz > 0 && (!X->col_idx || !X->values))
+            return fail(SVM_E_INVALID, "CSR col_idx or values is NULL");
+    } else {
+        if (X->n > 0 && !X->values)
+            return fail(SVM_E_INVALID, "X values is NULL");
+        if (X->ld < X->d) return fail(SVM_E_INVALID, "ld must be >= d");
+    }
     if (X->n > ((int64_t)1 << 31) - 1)
         return fail(SVM_E_INVALID, "n must be < 2^31");
     return SVM_OK;

@@ -107,7 +107,10 @@ enum : int32_t {
 };
 
 struct RowArgs {
-    const float* X;
+    const float* X;       // dense rows, or nullptr for CSR
+    const int64_t* rp;    // CSR rows (rp == nullptr: dense)
+    const int32_t* ci;
+    const float* cv;
     const float* sq;
     double* F;
     const uint8_t* st;
@@ -143,7 +146,10 @@ struct SelArgs {
     uint8_t* st;
     const double* F;
     const float* z;
-    const float* X;
+    const float* X;       // dense rows, or nullptr for CSR
+    const int64_t* rp;    // CSR rows (rp == nullptr: dense)
+    const int32_t* ci;
+    const float* cv;
     const float* sq;
     float* xS;
     int64_t n, ldp;
@@ -176,6 +182,7 @@ struct PredictArgs {
     int32_t n_out;
     const int32_t* sv_train_idx;  // with self_match: K(x_i, x_i) = 1 exactly
     int32_t self_match;
+    int64_t row_base;     // training-set index of query row 0 (self_match)
     double* out;          // m x n_out
     float gexp;
 };
@@ -196,8 +203,9 @@ void launch_check_finite(const float* v, int64_t n, int32_t* bad_flag,
 void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
                  hipStream_t s, hipEvent_t e0 = nullptr,
                  hipEvent_t e1 = nullptr);
-size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr);
-int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds);
+size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
+                      bool csr);
+int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
 void launch_state_from_alpha(int32_t type, const float* y, const double* a,
                              int64_t n, double C, uint8_t* st, hipStream_t s);
@@ -217,6 +225,15 @@ void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
                         const int32_t* idx, int64_t k, float* out,
                         float* sq_out, hipStream_t s);
 void launch_predict(const PredictArgs& a, hipStream_t s);
+void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,
+                            const float* cv, int64_t n, int64_t d,
+                            int64_t nnz, float* sq, int32_t* bad,
+                            hipStream_t s);
+// dense copies of CSR rows (idx == nullptr: rows r0 .. r0 + k - 1)
+void launch_gather_rows_csr(const int64_t* rp, const int32_t* ci,
+                            const float* cv, const float* sq, int64_t ldp,
+                            const int32_t* idx, int64_t r0, int64_t k,
+                            float* out, float* sq_out, hipStream_t s);
 void launch_argmax_labels(const double* D, int64_t m, int32_t n_out,
                           int32_t type, int32_t* labels, hipStream_t s);
 void launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);

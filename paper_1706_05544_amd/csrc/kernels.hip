@@ -356,7 +356,7 @@ __global__ void k_gather_rows(const float* X, const float* sq, int64_t ldp,
         int64_t src = idx[r];
         *reinterpret_cast<float4*>(out + r * ldp + 4 * c4) =
             ld4(X + src * ldp + 4 * c4);
-        if (c4 == 0) sq_out[r] = sq[src];
+        if (c4 == 0 && sq_out) sq_out[r] = sq[src];
     }
 }
 
@@ -369,6 +369,84 @@ void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
     if (blocks > 65536) blocks = 65536;
     k_gather_rows<<<(unsigned)blocks, 256, 0, s>>>(X, sq, ldp, idx, k, out,
                                                    sq_out);
+}
+
+// ---------------------------------------------------------------------------
+// CSR feature store
+// ---------------------------------------------------------------------------
+
+// Checks the CSR structure of row i and computes its squared norm (fp64
+// sum, rounded once).  bad |= 1: a value not finite (or a norm past fp32),
+// 2: row pointers, 4: column indices out of range, unsorted or repeated.
+__global__ void k_csr_check_norms(const int64_t* rp, const int32_t* ci,
+                                  const float* cv, int64_t n, int64_t d,
+                                  int64_t nnz, float* sq, int32_t* bad)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0 && (rp[0] != 0 || rp[n] != nnz)) atomicOr(bad, 2);
+    if (i >= n) return;
+    const int64_t p0 = rp[i], p1 = rp[i + 1];
+    int32_t flags = 0;
+    double s = 0.0;
+    if (p0 < 0 || p1 < p0 || p1 > nnz) {
+        flags |= 2;  // (the entries are not read)
+    } else {
+        int32_t prev = -1;
+        for (int64_t k = p0; k < p1; ++k) {
+            const int32_t c = ci[k];
+            const float v = cv[k];
+            if (c < 0 || (int64_t)c >= d || c <= prev) flags |= 4;
+            prev = c;
+            if (!isfinite(v)) flags |= 1;
+            s += (double)v * (double)v;
+        }
+    }
+    const float f = (float)s;
+    if (!isfinite(f)) flags |= 1;
+    sq[i] = f;
+    if (flags) atomicOr(bad, flags);
+}
+
+void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,
+                            const float* cv, int64_t n, int64_t d,
+                            int64_t nnz, float* sq, int32_t* bad,
+                            hipStream_t s)
+{
+    const int64_t blocks = (n + 255) / 256;
+    k_csr_check_norms<<<(unsigned)(blocks > 0 ? blocks : 1), 256, 0, s>>>(
+        rp, ci, cv, n, d, nnz, sq, bad);
+}
+
+// Dense rows (ldp wide, zero-filled) of CSR rows: row r of the output is
+// source row idx[r] (idx == nullptr: row r0 + r), with its norm.  One block
+// per output row.
+__global__ void k_gather_rows_csr(const int64_t* rp, const int32_t* ci,
+                                  const float* cv, const float* sq,
+                                  int64_t ldp, const int32_t* idx, int64_t r0,
+                                  int64_t k, float* out, float* sq_out)
+{
+    for (int64_t r = blockIdx.x; r < k; r += gridDim.x) {
+        const int64_t src = idx ? (int64_t)idx[r] : r0 + r;
+        float* row = out + r * ldp;
+        for (int64_t c = threadIdx.x; c < ldp; c += blockDim.x) row[c] = 0.0f;
+        __syncthreads();
+        const int64_t p0 = rp[src], p1 = rp[src + 1];
+        for (int64_t q = p0 + threadIdx.x; q < p1; q += blockDim.x)
+            row[ci[q]] = cv[q];
+        if (threadIdx.x == 0 && sq_out) sq_out[r] = sq[src];
+        __syncthreads();
+    }
+}
+
+void launch_gather_rows_csr(const int64_t* rp, const int32_t* ci,
+                            const float* cv, const float* sq, int64_t ldp,
+                            const int32_t* idx, int64_t r0, int64_t k,
+                            float* out, float* sq_out, hipStream_t s)
+{
+    if (k <= 0) return;
+    const int64_t blocks = k < 65536 ? k : 65536;
+    k_gather_rows_csr<<<(unsigned)blocks, 256, 0, s>>>(rp, ci, cv, sq, ldp, idx,
+                                                       r0, k, out, sq_out);
 }
 
 __global__ void k_labels(const double* D, int64_t m, int32_t n_out,

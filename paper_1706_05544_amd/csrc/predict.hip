@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 float kv = rbf_from_dot(sqr[v], ssv, acc[cb][v], a.gexp);
-                if (st == rid[v]) kv = 1.0f;
+                if (st == rid[v] + a.row_base) kv = 1.0f;
 #pragma unroll
                 for (int o = 0; o < NOUT; ++o)
                     part[o][v] = fma(cf[o], (double)kv, part[o][v]);

@@ -39,10 +39,20 @@ __host__ __device__ inline int rows_aux_bytes(int tiles, bool svr)
     return ((16 * tiles * (svr ? 18 : 13)) + 15) & ~15;
 }
 
-__host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp)
+// Floats of the per-wave buffer: a feature slab (dense), or the K values of
+// 64 rows x 16 * nblk_cols slots with one pad column (CSR).
+__host__ __device__ inline int rows_wave_buf(int nblk_cols, bool csr)
+{
+    return csr ? 64 * (16 * nblk_cols + 1) : 16 * kSlabStride;
+}
+
+// The staged working-set rows take nblk_cols * 16 rows of rows_xs_stride
+// floats (dense), or the same samples feature-major (CSR, no more room).
+__host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp,
+                                                  bool csr)
 {
     return (size_t)nblk_cols * 16 * rows_xs_stride(ldp) * sizeof(float) +
-           (size_t)kRowWaves * 16 * kSlabStride * sizeof(float);
+           (size_t)kRowWaves * rows_wave_buf(nblk_cols, csr) * sizeof(float);
 }
 
 // per-wave threshold list: kWaveList (key, index) pairs per side
@@ -51,9 +61,10 @@ constexpr int kWaveListBytes = 2 * kWaveList * (8 + 4);
 // per-block table of the working-set slots: norm, sample, cache slot
 constexpr int kSlotInfoBytes = kMaxQ * (4 + 4 + 4);
 
-size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr)
+size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
+                      bool csr)
 {
-    return rows_aux_offset(nblk_cols, ldp) +
+    return rows_aux_offset(nblk_cols, ldp, csr) +
            (size_t)kRowWaves * (rows_aux_bytes(tiles, svr) + kWaveListBytes) +
            kSlotInfoBytes;
 }
@@ -115,7 +126,7 @@ __device__ __forceinline__ void wave_top2_pair(Top2 u, Top2 l, double* ok,
 // back in the matrix-core operand layout (lane (g, nl): row nl, columns
 // 16c + 4g .. +3 of chunk c), which is the library-wide chunk order, so every
 // K value matches the other kernels bitwise.
-template <bool SVR, int NBLK, int MODE>
+template <bool SVR, int NBLK, int MODE, bool CSR>
 __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 {
     constexpr bool UPD = (MODE & RU_UPDATE) != 0;
@@ -159,12 +170,12 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     const int nw = rw0 >= n ? 0 : (int)min((int64_t)RW, n - rw0);
     const int Tw = (nw + 15) >> 4;
     unsigned char* aux =
-        smem + rows_aux_offset(NBLK, ldp) + wave * rows_aux_bytes(T, SVR);
+        smem + rows_aux_offset(NBLK, ldp, CSR) + wave * rows_aux_bytes(T, SVR);
     double* Fw = reinterpret_cast<double*>(aux);
     float* sqw = reinterpret_cast<float*>(aux + 8 * RW);
     float* zw = reinterpret_cast<float*>(aux + 12 * RW);
     uint8_t* stw = aux + (SVR ? 16 : 12) * RW;  // copy (i,-) at stw[RW + r]
-    unsigned char* wl = smem + rows_aux_offset(NBLK, ldp) +
+    unsigned char* wl = smem + rows_aux_offset(NBLK, ldp, CSR) +
                         kRowWaves * rows_aux_bytes(T, SVR) +
                         wave * kWaveListBytes;
     double* wlk = reinterpret_cast<double*>(wl);              // [2][kWaveList]
@@ -176,7 +187,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     }
     int nlist[2] = {0, 0};  // wave-uniform entry counts
     // slot table (block-wide): norm, sample and cache slot of every slot
-    unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp) +
+    unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp, CSR) +
                            kRowWaves * (rows_aux_bytes(T, SVR) + kWaveListBytes);
     float* sl_sq = reinterpret_cast<float*>(sinfo);
     int32_t* sl_smp = reinterpret_cast<int32_t*>(sinfo + 4 * kMaxQ);
@@ -343,6 +354,121 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                     if (t0 + j < Tw) finish_tile(t0 + j, kv);
                 }
             }
+        } else if (CSR) {
+            // CSR rows.  The working-set samples sit feature-major in LDS
+            // (xsT[j * QS + s] = x_s[j]); one lane per row walks the row's
+            // nonzeros in column order and, per nonzero, gathers the QS
+            // samples' values: K(x_i, x_s) sums the products of the common
+            // nonzeros in increasing column order (every CSR kernel of the
+            // library sums them so).  The K values of 64 rows go through a
+            // wave buffer into the 16-row tile layout of the epilogue.
+            constexpr int QS = NBLK * 16, QP = QS + 1;
+            float* xsT = xsl;
+            float* tb = xsl + NBLK * 16 * xstride + wave * rows_wave_buf(NBLK, true);
+            float sq0 = 0.0f;
+            int32_t smp0 = -1, cs0 = -1;
+            if (tid < NBLK * 16) {
+                const float q = ws->sS[tid];
+                const int32_t i = ws->S[tid], c = ws->cslot[tid];
+                sq0 = tid < nS ? q : 0.0f;
+                smp0 = tid < nS ? i : -1;
+                cs0 = (LIST && tid < nS) ? c : -1;
+            }
+            AuxRegs ar;
+            aux_issue(0, ar);
+            if (done) return;  // uniform over the block
+            aux_store(0, ar);
+            if (tid < NBLK * 16) {
+                sl_sq[tid] = sq0;
+                sl_smp[tid] = smp0;
+                sl_cs[tid] = cs0;
+            }
+            for (int k0 = 256; k0 < RW; k0 += 256) {
+                aux_issue(k0, ar);
+                aux_store(k0, ar);
+            }
+            const int q4 = ldp >> 2;
+            for (int e = tid; e < QS * q4; e += kRowThreads) {
+                const int slot = e % QS, c4 = e / QS;
+                float4 v = ld4(a.xS + (int64_t)slot * ldp + 4 * c4);
+                if (slot >= nS) v = zero4();
+                xsT[(4 * c4 + 0) * QS + slot] = v.x;
+                xsT[(4 * c4 + 1) * QS + slot] = v.y;
+                xsT[(4 * c4 + 2) * QS + slot] = v.z;
+                xsT[(4 * c4 + 3) * QS + slot] = v.w;
+            }
+            __syncthreads();
+
+            const bool INS = LIST && path == PATH_INSERT;
+            constexpr int KB = 8;  // nonzeros loaded per batch
+            for (int p0 = 0; p0 < Tw; p0 += 4) {
+                const int r = 16 * p0 + lane;  // this lane's row (local)
+                const bool rv = r < nw;
+                const int64_t gr = rv ? rw0 + r : 0;
+                const int64_t k0 = a.rp[gr], k1 = a.rp[gr + 1];
+                const int nz = rv ? (int)(k1 - k0) : 0;
+                int mx = nz;
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1)
+                    mx = max(mx, __shfl_xor(mx, off));
+                float acc[QS];
+#pragma unroll
+                for (int q = 0; q < QS; ++q) acc[q] = 0.0f;
+                for (int kb = 0; kb < mx; kb += KB) {
+                    int32_t cc[KB];
+                    float vv[KB];
+#pragma unroll
+                    for (int j = 0; j < KB; ++j) {
+                        // unconditional loads (a valid entry when unused)
+                        const bool ok = kb + j < nz;
+                        const int64_t pos = ok ? k0 + kb + j : 0;
+                        const int32_t c = a.ci[pos];
+                        const float v = a.cv[pos];
+                        cc[j] = ok ? c : 0;
+                        vv[j] = ok ? v : 0.0f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < KB; ++j) {
+                        const float* xr = xsT + cc[j] * QS;
+#pragma unroll
+                        for (int q = 0; q < QS; q += 4) {
+                            const float4 x = ld4(xr + q);
+                            acc[q + 0] = fmaf(vv[j], x.x, acc[q + 0]);
+                            acc[q + 1] = fmaf(vv[j], x.y, acc[q + 1]);
+                            acc[q + 2] = fmaf(vv[j], x.z, acc[q + 2]);
+                            acc[q + 3] = fmaf(vv[j], x.w, acc[q + 3]);
+                        }
+                    }
+                }
+                const float sqr = rv ? sqw[r] : 0.0f;
+#pragma unroll
+                for (int q = 0; q < QS; ++q) {
+                    float kv = rbf_from_dot(sqr, sl_sq[q], acc[q], a.gexp);
+                    if (rw0 + r == (int64_t)sl_smp[q]) kv = 1.0f;
+                    tb[lane * QP + q] = kv;
+                }
+                __builtin_amdgcn_wave_barrier();
+                for (int t = 0; t < 4; ++t) {
+                    const int ti = p0 + t;
+                    if (ti >= Tw) break;
+                    const int lr = 16 * ti + 4 * g;
+                    float kv[NBLK][4];
+#pragma unroll
+                    for (int b = 0; b < NBLK; ++b) {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            kv[b][v] = tb[(16 * t + 4 * g + v) * QP + b * 16 + nl];
+                        const int32_t csb = INS ? sl_cs[b * 16 + nl] : -1;
+                        if (csb >= 0 && rw0 + lr < n)
+                            *reinterpret_cast<float4*>(
+                                a.cache + (int64_t)csb * a.ldc + rw0 + lr) =
+                                make_float4(kv[b][0], kv[b][1], kv[b][2],
+                                            kv[b][3]);
+                    }
+                    finish_tile(ti, kv);
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
         } else {
             // Staged working-set rows: every slot (finite values past nS),
             // zero-filled to whole 16-feature chunks.
@@ -364,7 +490,8 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 
             const int nslab = (ldp + 63) >> 6;
             const Rsrc rX = make_rsrc(a.X + rw0 * ldp, (int64_t)nw * ldp * 4);
-            float* wbuf = xsl + NBLK * 16 * xstride + wave * (16 * kSlabStride);
+            float* wbuf = xsl + NBLK * 16 * xstride +
+                          wave * rows_wave_buf(NBLK, false);
             const uint32_t step4 = (uint32_t)(16 * ldp);  // 4 rows, in bytes
             int fti = 0, fsl = 0;  // next slab to fetch
             auto fetch = [&](float4 (&v)[4]) {
@@ -541,15 +668,15 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                    a.cand_idx + wid * 2 * kBlockTop);
 }
 
-template <bool SVR, int NBLK, int MODE>
+template <bool SVR, int NBLK, int MODE, bool CSR>
 static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
                           hipEvent_t e0, hipEvent_t e1)
 {
-    const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR);
+    const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR, CSR);
     static size_t lds_allowed = 64 * 1024;
     if (lds > lds_allowed) {
         hipError_t e = hipFuncSetAttribute(
-            (const void*)k_rows<SVR, NBLK, MODE>,
+            (const void*)k_rows<SVR, NBLK, MODE, CSR>,
             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -559,43 +686,43 @@ static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
         lds_allowed = lds;
     }
     if (e0) {
-        hipExtLaunchKernelGGL(k_rows<SVR, NBLK, MODE>, dim3(nblocks),
+        hipExtLaunchKernelGGL(k_rows<SVR, NBLK, MODE, CSR>, dim3(nblocks),
                               dim3(kRowThreads), (uint32_t)lds, s, e0, e1, 0,
                               a);
     } else {
-        k_rows<SVR, NBLK, MODE><<<nblocks, kRowThreads, lds, s>>>(a);
+        k_rows<SVR, NBLK, MODE, CSR><<<nblocks, kRowThreads, lds, s>>>(a);
     }
 }
 
 constexpr int kModeHot = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
 
-template <bool SVR, int NBLK>
+template <bool SVR, int NBLK, bool CSR>
 static void rows_mode(const RowArgs& a, int nblocks, hipStream_t s,
                       hipEvent_t e0, hipEvent_t e1)
 {
     switch (a.mode) {
         case kModeHot:
-            rows_dispatch<SVR, NBLK, kModeHot>(a, nblocks, s, e0, e1);
+            rows_dispatch<SVR, NBLK, kModeHot, CSR>(a, nblocks, s, e0, e1);
             break;
         case RU_CAND:
-            rows_dispatch<SVR, NBLK, RU_CAND>(a, nblocks, s, e0, e1);
+            rows_dispatch<SVR, NBLK, RU_CAND, CSR>(a, nblocks, s, e0, e1);
             break;
         case RU_ROWS:
-            rows_dispatch<SVR, NBLK, RU_ROWS>(a, nblocks, s, e0, e1);
+            rows_dispatch<SVR, NBLK, RU_ROWS, CSR>(a, nblocks, s, e0, e1);
             break;
         case RU_UPDATE:
-            rows_dispatch<SVR, NBLK, RU_UPDATE>(a, nblocks, s, e0, e1);
+            rows_dispatch<SVR, NBLK, RU_UPDATE, CSR>(a, nblocks, s, e0, e1);
             break;
         default: throw Error{SVM_E_INTERNAL, "bad row kernel mode"};
     }
 }
 
-template <bool SVR, int NBLK>
+template <bool SVR, int NBLK, bool CSR>
 static int rows_occupancy(size_t lds)
 {
     int bpc = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &bpc, (const void*)k_rows<SVR, NBLK, kModeHot>, kRowThreads,
+            &bpc, (const void*)k_rows<SVR, NBLK, kModeHot, CSR>, kRowThreads,
             lds) != hipSuccess) {
         (void)hipGetLastError();
         return 1;
@@ -603,15 +730,21 @@ static int rows_occupancy(size_t lds)
     return bpc > 0 ? bpc : 1;
 }
 
-int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds)
+// The CSR row kernel covers up to 32 working-set slots (its per-lane
+// accumulators); q = 64 with CSR input is refused by the solver.
+int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr)
 {
-    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
-        case 2: return rows_occupancy<false, 1>(lds);
-        case 3: return rows_occupancy<true, 1>(lds);
-        case 4: return rows_occupancy<false, 2>(lds);
-        case 5: return rows_occupancy<true, 2>(lds);
-        case 8: return rows_occupancy<false, 4>(lds);
-        case 9: return rows_occupancy<true, 4>(lds);
+    switch (nblk_cols * 4 + (svr ? 2 : 0) + (csr ? 1 : 0)) {
+        case 4: return rows_occupancy<false, 1, false>(lds);
+        case 5: return rows_occupancy<false, 1, true>(lds);
+        case 6: return rows_occupancy<true, 1, false>(lds);
+        case 7: return rows_occupancy<true, 1, true>(lds);
+        case 8: return rows_occupancy<false, 2, false>(lds);
+        case 9: return rows_occupancy<false, 2, true>(lds);
+        case 10: return rows_occupancy<true, 2, false>(lds);
+        case 11: return rows_occupancy<true, 2, true>(lds);
+        case 16: return rows_occupancy<false, 4, false>(lds);
+        case 18: return rows_occupancy<true, 4, false>(lds);
         default: return 1;
     }
 }
@@ -623,14 +756,21 @@ void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
     // byte offsets inside one wave's rows must stay below 2^31
     if ((int64_t)16 * a.tiles * a.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED, "row group too large for the row kernel"};
-    switch (nblk_cols * 2 + (svr ? 1 : 0)) {
-        case 2: rows_mode<false, 1>(a, nblocks, s, e0, e1); break;
-        case 3: rows_mode<true, 1>(a, nblocks, s, e0, e1); break;
-        case 4: rows_mode<false, 2>(a, nblocks, s, e0, e1); break;
-        case 5: rows_mode<true, 2>(a, nblocks, s, e0, e1); break;
-        case 8: rows_mode<false, 4>(a, nblocks, s, e0, e1); break;
-        case 9: rows_mode<true, 4>(a, nblocks, s, e0, e1); break;
-        default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
+    const bool csr = a.rp != nullptr;
+    switch (nblk_cols * 4 + (svr ? 2 : 0) + (csr ? 1 : 0)) {
+        case 4: rows_mode<false, 1, false>(a, nblocks, s, e0, e1); break;
+        case 5: rows_mode<false, 1, true>(a, nblocks, s, e0, e1); break;
+        case 6: rows_mode<true, 1, false>(a, nblocks, s, e0, e1); break;
+        case 7: rows_mode<true, 1, true>(a, nblocks, s, e0, e1); break;
+        case 8: rows_mode<false, 2, false>(a, nblocks, s, e0, e1); break;
+        case 9: rows_mode<false, 2, true>(a, nblocks, s, e0, e1); break;
+        case 10: rows_mode<true, 2, false>(a, nblocks, s, e0, e1); break;
+        case 11: rows_mode<true, 2, true>(a, nblocks, s, e0, e1); break;
+        case 16: rows_mode<false, 4, false>(a, nblocks, s, e0, e1); break;
+        case 18: rows_mode<true, 4, false>(a, nblocks, s, e0, e1); break;
+        default:
+            throw Error{SVM_E_UNSUPPORTED,
+                        "CSR input supports working sets of at most 32"};
     }
 }
 

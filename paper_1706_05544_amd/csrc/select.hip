@@ -781,12 +781,41 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         c_filled = ws->cache_filled;
     }
 
-    // (10) K_SS on the matrix cores (same operand order as k_rows): the
-    // working-set rows pass through LDS in feature slices: every thread
-    // loads a piece into LDS; then the NBLK^2 matrix-core waves accumulate
-    // the slice while the other waves copy it to xS (the rows of the next
-    // k_rows).
-    {
+    // (10) K_SS.  CSR input: every wave scatters one working-set row into
+    // a dense LDS row, and K_SS sums the products over the nonzeros of the
+    // first sample in column order (the row kernel's order, so the values
+    // are the same bits).  Dense input: on the matrix cores (same operand
+    // order as k_rows): the working-set rows pass through LDS in feature
+    // slices: every thread loads a piece into LDS; then the NBLK^2
+    // matrix-core waves accumulate the slice while the other waves copy it
+    // to xS (the rows of the next k_rows).
+    if (a.rp) {
+        const int wst = a.slice + 4;  // one slice holds a whole row (host)
+        for (int e = tid; e < nS * wst; e += kSelThreads) xst[e] = 0.0f;
+        __syncthreads();
+        for (int slot = wave; slot < nS; slot += NW) {
+            const int64_t smp = shS[slot];
+            const int64_t p0 = a.rp[smp], p1 = a.rp[smp + 1];
+            for (int64_t q = p0 + lane; q < p1; q += 64)
+                xst[slot * wst + a.ci[q]] = a.cv[q];
+        }
+        __syncthreads();
+        for (int e = tid; e < nS * nS; e += kSelThreads) {
+            const int ia = e / nS, ib = e - ia * nS;
+            float k = 1.0f;
+            if (ia != ib) {
+                const int64_t sa_ = shS[ia];
+                const int64_t p0 = a.rp[sa_], p1 = a.rp[sa_ + 1];
+                const float* xb = xst + ib * wst;
+                float acc = 0.0f;
+                for (int64_t q = p0; q < p1; ++q)
+                    acc = fmaf(a.cv[q], xb[a.ci[q]], acc);
+                k = rbf_from_dot(a.sq[sa_], a.sq[shS[ib]], acc, a.gexp);
+            }
+            KSS[ia][ib] = k;
+        }
+        if (tid < nS) shsS[tid] = a.sq[shS[tid]];
+    } else {
         const int g = lane >> 4, nl = lane & 15;
         const int bi = wave / NBLK, bj = wave - bi * NBLK;
         const int sa = bi * 16 + nl, sb = bj * 16 + nl;
@@ -1086,6 +1115,13 @@ void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)
 {
     SelArgs a = a0;
     if (a.slice <= 0) a.slice = select_slice(nblk_cols, a.ldp);
+    if (a.rp) {
+        // CSR: the dense working-set rows are whole in LDS
+        a.slice = (int)((a.ldp + 15) & ~(int64_t)15);
+        if (select_lds_bytes(nblk_cols, a.slice) > 112 * 1024)
+            throw Error{SVM_E_UNSUPPORTED,
+                        "too many features for a CSR working set in LDS"};
+    }
     switch (nblk_cols * 2 + (svr ? 1 : 0)) {
         case 2: select_dispatch<false, 1>(a, s); break;
         case 3: select_dispatch<true, 1>(a, s); break;

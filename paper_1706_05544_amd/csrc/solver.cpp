@@ -31,11 +31,57 @@ void Context::sync() { HIP_TRY(hipStreamSynchronize(stream)); }
 
 int64_t padded_ld(int64_t d) { return (d + 3) / 4 * 4; }
 
+static void load_csr(const svm_matrix* M, Features& f, Context& cx)
+{
+    f.csr = true;
+    f.nnz = M->nnz;
+    f.rp.alloc((size_t)(f.n + 1));
+    f.ci.alloc((size_t)f.nnz);
+    f.cv.alloc((size_t)f.nnz);
+    f.sq.alloc((size_t)f.n);
+    const hipMemcpyKind kind =
+        M->on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    HIP_TRY(hipMemcpyAsync(f.rp.p, M->row_ptr,
+                           (size_t)(f.n + 1) * sizeof(int64_t), kind,
+                           cx.stream));
+    if (f.nnz > 0) {
+        HIP_TRY(hipMemcpyAsync(f.ci.p, M->col_idx,
+                               (size_t)f.nnz * sizeof(int32_t), kind,
+                               cx.stream));
+        HIP_TRY(hipMemcpyAsync(f.cv.p, M->values, (size_t)f.nnz * sizeof(float),
+                               kind, cx.stream));
+    }
+    DevBuf<int32_t> bad(1);
+    HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
+    launch_csr_check_norms(f.rp.p, f.ci.p, f.cv.p, f.n, f.d, f.nnz, f.sq.p,
+                           bad.p, cx.stream);
+    int32_t hb = 0;
+    HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t), hipMemcpyDeviceToHost,
+                           cx.stream));
+    cx.sync();
+    if (hb & 2)
+        throw Error{SVM_E_INVALID,
+                    "CSR row pointers must start at 0, not decrease and end at "
+                    "nnz"};
+    if (hb & 4)
+        throw Error{SVM_E_INVALID,
+                    "CSR column indices must be in [0, d), sorted and unique "
+                    "within each row"};
+    if (hb & 1)
+        throw Error{SVM_E_INVALID,
+                    "X holds a value that is not finite (or whose square "
+                    "overflows fp32)"};
+}
+
 void load_features(const svm_matrix* M, Features& f, Context& cx)
 {
     f.n = M->n;
     f.d = M->d;
     f.ldp = padded_ld(M->d);
+    if (M->layout == SVM_CSR) {
+        load_csr(M, f, cx);
+        return;
+    }
     f.X.alloc((size_t)(f.n * f.ldp));
     f.sq.alloc((size_t)f.n);
     const hipMemcpyKind kind =
@@ -137,7 +183,10 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     constexpr int kWaves = kRowThreads / 64;
     const bool svr = o.type == SVM_EPS_SVR;
     constexpr size_t kLdsMax = 160 * 1024;
-    if (rows_lds_bytes(nblk_cols_, f.ldp, 1, svr) > kLdsMax)
+    if (f.csr && o.q > 32)
+        throw Error{SVM_E_UNSUPPORTED,
+                    "CSR input supports working sets of at most 32"};
+    if (rows_lds_bytes(nblk_cols_, f.ldp, 1, svr, f.csr) > kLdsMax)
         throw Error{SVM_E_UNSUPPORTED,
                     "too many features for the dense row kernel's LDS tile"};
     int cus = 0;
@@ -149,9 +198,9 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     // (tiles only grow, so this ends).
     tiles_ = 1;
     for (int it = 0; it < 8; ++it) {
-        const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr);
+        const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr);
         const int64_t cap =
-            (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds) * kWaves;
+            (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds, f.csr) * kWaves;
         const int t = (int)std::max<int64_t>(1, (tiles_total + cap - 1) / cap);
         if (t <= tiles_) break;
         tiles_ = t;
@@ -162,7 +211,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     while (((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_)) * kWaves *
                kBlockTop > cand_cap)
         ++tiles_;
-    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr) > kLdsMax ||
+    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr) > kLdsMax ||
         (int64_t)16 * tiles_ * f.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED,
                     "training set too large for the dense row kernel"};
@@ -215,6 +264,9 @@ void Solver::launch_keys()
 {
     RowArgs a{};
     a.X = f_.X.p;
+    a.rp = f_.rp.p;
+    a.ci = f_.ci.p;
+    a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.F = F_.p;
     a.st = st_.p;
@@ -241,6 +293,9 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
 {
     RowArgs a{};
     a.X = f_.X.p;
+    a.rp = f_.rp.p;
+    a.ci = f_.ci.p;
+    a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.F = F_.p;
     a.st = st_.p;
@@ -284,6 +339,9 @@ void Solver::launch_solve(int32_t mode)
     a.F = F_.p;
     a.z = y_.p;
     a.X = f_.X.p;
+    a.rp = f_.rp.p;
+    a.ci = f_.ci.p;
+    a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.xS = xS_.p;
     a.n = n_;
@@ -383,12 +441,16 @@ bool Solver::run_loop(SolveResult& r)
                     cached_bytes_ +=
                         (double)n_ * (per_row + 4.0 * (double)w.ns_log[t]);
                 } else {
+                    // the features: dense 4d per row, CSR 8 per nonzero and
+                    // the row pointers
+                    const double feat =
+                        f_.csr ? 8.0 * (double)f_.nnz + 8.0 * (double)(n_ + 1)
+                               : 4.0 * (double)f_.d * (double)n_;
                     row_ms_ += ms;
                     row_launches_ += 1;
                     row_rows_ += n_;
-                    row_bytes_ +=
-                        (double)n_ * (per_row + 4.0 + 4.0 * (double)f_.d +
-                                      4.0 * (double)w.fill_log[t]);
+                    row_bytes_ += feat + (double)n_ * (per_row + 4.0 +
+                                                       4.0 * w.fill_log[t]);
                 }
             }
         }
@@ -437,13 +499,8 @@ void Solver::recompute_responses()
         sv_rows_.alloc((size_t)(nsv * f_.ldp));
         sv_sq_.alloc((size_t)nsv);
     }
-    launch_gather_rows(f_.X.p, f_.sq.p, f_.ldp, sv_idx_.p, nsv, sv_rows_.p,
-                       sv_sq_.p, s);
+    gather_rows(f_, sv_idx_.p, nsv, sv_rows_.p, sv_sq_.p, s);
     PredictArgs a{};
-    a.Xt = f_.X.p;
-    a.sqt = f_.sq.p;
-    a.m = n_;
-    a.ldp = f_.ldp;
     a.SV = sv_rows_.p;
     a.sqsv = sv_sq_.p;
     a.nsv = nsv;
@@ -454,7 +511,7 @@ void Solver::recompute_responses()
     a.self_match = 1;
     a.out = F_.p;
     a.gexp = gexp_;
-    launch_predict(a, s);
+    predict_rows(a, f_, s);
 }
 
 SolveResult Solver::train()
@@ -623,11 +680,11 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
         w.S[j] = samples[j];
         HIP_TRY(hipMemcpyAsync(&w.sS[j], f_.sq.p + samples[j], sizeof(float),
                                hipMemcpyDeviceToHost, s));
-        HIP_TRY(hipMemcpyAsync(xS_.p + (size_t)j * f_.ldp,
-                               f_.X.p + (size_t)samples[j] * f_.ldp,
-                               (size_t)f_.ldp * sizeof(float),
-                               hipMemcpyDeviceToDevice, s));
     }
+    DevBuf<int32_t> sidx((size_t)k);
+    HIP_TRY(hipMemcpyAsync(sidx.p, samples, (size_t)k * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s));
+    gather_rows(f_, sidx.p, k, xS_.p, nullptr, s);
     cx_.sync();
     HIP_TRY(hipMemcpyAsync(ws_.p, &w, sizeof(WorkingSet),
                            hipMemcpyHostToDevice, s));
@@ -635,6 +692,9 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     if (rows_out_.count < (size_t)(k * n_)) rows_out_.alloc((size_t)(k * n_));
     RowArgs a{};
     a.X = f_.X.p;
+    a.rp = f_.rp.p;
+    a.ci = f_.ci.p;
+    a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.F = F_.p;
     a.st = st_.p;
@@ -651,7 +711,8 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     a.mode = RU_ROWS;
     a.nS_override = k;
     int nbc = k <= 16 ? 1 : (k <= 32 ? 2 : 4);
-    if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR) >
+    if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR,
+                       f_.csr) >
         160 * 1024)
         throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
     launch_rows(a, nb_, nbc, o_.type == SVM_EPS_SVR, s);
@@ -680,6 +741,9 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.F = F_.p;
     a.z = y_.p;
     a.X = f_.X.p;
+    a.rp = f_.rp.p;
+    a.ci = f_.ci.p;
+    a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.xS = xS_.p;
     a.n = n_;
@@ -723,6 +787,9 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.F = F_.p;
     a.z = y_.p;
     a.X = f_.X.p;
+    a.rp = f_.rp.p;
+    a.ci = f_.ci.p;
+    a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.xS = xS_.p;
     a.n = n_;
@@ -742,6 +809,9 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
     RowArgs r{};
     r.X = f_.X.p;
+    r.rp = f_.rp.p;
+    r.ci = f_.ci.p;
+    r.cv = f_.cv.p;
     r.sq = f_.sq.p;
     r.F = F_.p;
     r.st = st_.p;
@@ -761,7 +831,8 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     r.tiles = tiles_;
     r.mode = RU_UPDATE;
     r.nS_override = -1;
-    if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR) >
+    if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR,
+                       f_.csr) >
         160 * 1024)
         throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
     launch_rows(r, nb_, nbc, o_.type == SVM_EPS_SVR, s);
@@ -803,7 +874,7 @@ void build_model(svm_model& m, Context& cx, const Features& f,
     m.sqsv.alloc((size_t)nsv);
     m.coef_dev.alloc((size_t)(nsv * n_out));
     m.b_dev.alloc((size_t)n_out);
-    launch_gather_rows(f.X.p, f.sq.p, f.ldp, idx.p, nsv, m.SV.p, m.sqsv.p, s);
+    gather_rows(f, idx.p, nsv, m.SV.p, m.sqsv.p, s);
     m.sv_idx.resize((size_t)nsv);
     m.coef.resize((size_t)(nsv * n_out));
     if (nsv > 0) {
@@ -827,10 +898,6 @@ void predict_device(const svm_model& mdl, Context& cx, const Features& t,
                     double* out)
 {
     PredictArgs a{};
-    a.Xt = t.X.p;
-    a.sqt = t.sq.p;
-    a.m = t.n;
-    a.ldp = t.ldp;
     a.SV = mdl.SV.p;
     a.sqsv = mdl.sqsv.p;
     a.nsv = mdl.n_sv;
@@ -841,7 +908,50 @@ void predict_device(const svm_model& mdl, Context& cx, const Features& t,
     a.self_match = 0;
     a.out = out;
     a.gexp = mdl.gexp;
-    launch_predict(a, cx.stream);
+    predict_rows(a, t, cx.stream);
+}
+
+void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
+                 float* sq_out, hipStream_t s)
+{
+    if (f.csr)
+        launch_gather_rows_csr(f.rp.p, f.ci.p, f.cv.p, f.sq.p, f.ldp, idx, 0,
+                               k, out, sq_out, s);
+    else
+        launch_gather_rows(f.X.p, f.sq.p, f.ldp, idx, k, out, sq_out, s);
+}
+
+void predict_rows(PredictArgs a, const Features& t, hipStream_t s)
+{
+    a.ldp = t.ldp;
+    if (!t.csr) {
+        a.Xt = t.X.p;
+        a.sqt = t.sq.p;
+        a.m = t.n;
+        a.row_base = 0;
+        launch_predict(a, s);
+        return;
+    }
+    // CSR rows: dense chunks of up to 256 MB
+    const int64_t row_bytes = t.ldp * (int64_t)sizeof(float);
+    int64_t chunk = std::max<int64_t>(64, ((int64_t)256 << 20) / row_bytes);
+    chunk = std::min<int64_t>(chunk, t.n);
+    if (chunk <= 0) return;
+    DevBuf<float> buf((size_t)(chunk * t.ldp));
+    double* out0 = a.out;
+    for (int64_t r0 = 0; r0 < t.n; r0 += chunk) {
+        const int64_t k = std::min<int64_t>(chunk, t.n - r0);
+        launch_gather_rows_csr(t.rp.p, t.ci.p, t.cv.p, t.sq.p, t.ldp, nullptr,
+                               r0, k, buf.p, nullptr, s);
+        a.Xt = buf.p;
+        a.sqt = t.sq.p + r0;
+        a.m = k;
+        a.row_base = r0;
+        a.out = out0 + r0 * a.n_out;
+        launch_predict(a, s);
+    }
+    // the chunk buffer is freed when the stream has used it
+    HIP_TRY(hipStreamSynchronize(s));
 }
 
 }  // namespace msvm

@@ -80,9 +80,17 @@ struct Context {
 };
 
 // Dense feature store: X zero-padded to ldp columns, plus squared norms.
+// Feature store: dense rows zero-padded to ldp columns, or CSR (int64 row
+// pointers, int32 column indices sorted within each row, fp32 values);
+// squared norms either way.  ldp is also the width of dense copies of CSR
+// rows (the working-set rows, support vectors).
 struct Features {
-    int64_t n = 0, d = 0, ldp = 0;
+    int64_t n = 0, d = 0, ldp = 0, nnz = 0;
+    bool csr = false;
     DevBuf<float> X, sq;
+    DevBuf<int64_t> rp;
+    DevBuf<int32_t> ci;
+    DevBuf<float> cv;
 };
 
 // Uploads X (host or device) into the padded layout and computes norms.
@@ -205,6 +213,14 @@ struct svm_model {
 };
 
 namespace msvm {
+
+// Dense copies of rows idx[0..k) of f (dense or CSR) and their norms.
+void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
+                 float* sq_out, hipStream_t s);
+
+// Decision sums of a (support rows, coefficients, outputs set) for every
+// row of t: dense rows directly, CSR rows through dense chunks of rows.
+void predict_rows(PredictArgs a, const Features& t, hipStream_t s);
 
 // Builds the model arrays from the n x n_out coefficient matrix (device).
 void build_model(svm_model& m, Context& cx, const Features& f,

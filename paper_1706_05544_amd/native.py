@@ -159,6 +159,11 @@ def _is_torch(x) -> bool:
     return type(x).__module__.startswith("torch")
 
 
+def _torch_sparse_csr():
+    import torch
+    return torch.sparse_csr
+
+
 def _np_ptr(a: np.ndarray) -> int:
     return a.ctypes.data
 
@@ -170,7 +175,20 @@ class _Mat:
     def __init__(self, X):
         self.keep = []
         m = svm_matrix()
-        if _is_torch(X):
+        if _is_torch(X) and X.layout == _torch_sparse_csr():
+            import torch
+            assert X.is_cuda and X.dim() == 2
+            rp = X.crow_indices().to(torch.int64).contiguous()
+            ci = X.col_indices().to(torch.int32).contiguous()
+            cv = X.values().to(torch.float32).contiguous()
+            self.keep += [rp, ci, cv]
+            m.layout, m.on_device = SVM_CSR, 1
+            m.n, m.d = X.shape
+            m.values, m.row_ptr, m.col_idx = (cv.data_ptr(), rp.data_ptr(),
+                                              ci.data_ptr())
+            m.nnz = cv.numel()
+            self.device = True
+        elif _is_torch(X):
             import torch
             assert X.is_cuda and X.dtype == torch.float32 and X.dim() == 2
             X = X.contiguous()

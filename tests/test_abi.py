@@ -6,6 +6,8 @@ import os
 import re
 import subprocess
 
+import ctypes as ct
+
 import numpy as np
 import pytest
 
@@ -139,11 +141,21 @@ def test_null_arguments_are_rejected():
     lib.svm_model_free(None)
 
 
-def test_csr_is_reported_unsupported():
+def test_csr_arguments_are_checked_before_the_device():
+    # pointer and count checks of a CSR matrix happen on the host (its
+    # structure, sortedness and finiteness are checked on the device)
     import scipy.sparse as sp
-    with pytest.raises(nv.SvmError) as e:
-        nv.svm_train(sp.csr_matrix(_x()), _y())
-    assert e.value.status == nv.SVM_E_UNSUPPORTED
+    lib = nv.load()
+    y = np.ascontiguousarray(_y(), dtype=np.float32)
+    p = nv.svm_params_default()
+    out = ct.c_void_p()
+    for field, value in (("row_ptr", None), ("nnz", -1), ("col_idx", None),
+                         ("values", None)):
+        M = nv._Mat(sp.csr_matrix(_x()))
+        setattr(M.s, field, value)
+        st = lib.svm_train(ct.byref(M.s), y.ctypes.data, ct.byref(p),
+                           ct.byref(out))
+        assert st == nv.SVM_E_INVALID, (field, st)
 
 
 @pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="a GPU is present")
