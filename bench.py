@@ -119,6 +119,9 @@ def main() -> int:
     ap.add_argument("--workload", default="C3")
     ap.add_argument("--n", type=int, default=None,
                     help="override the workload's training-set size")
+    ap.add_argument("--layout", default=None,
+                    help="feature layout of workloads that offer both "
+                         "(C4: dense or csr)")
     ap.add_argument("--working-set", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -140,7 +143,8 @@ def main() -> int:
     from paper_1706_05544_amd import workloads
 
     nv.load()
-    w = workloads.make(args.workload, n=args.n)
+    w = workloads.make(args.workload, n=args.n,
+                       **({"layout": args.layout} if args.layout else {}))
     if w.type != workloads.C_SVC and w.type != workloads.EPS_SVR:
         raise SystemExit("unsupported workload")
     log("workload %s: n=%d d=%d n_test=%d" % (w.name, w.n, w.d,

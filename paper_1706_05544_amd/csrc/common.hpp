@@ -24,10 +24,9 @@ constexpr int kMaxQ = 64;          // largest working set
 constexpr int kMaxHalf = kMaxQ / 2;
 constexpr int kRowThreads = 256;   // row/update kernel: 4 waves
 constexpr int kSelThreads = 1024;  // select/solve kernel: one block
-constexpr int kSelPerThread = 16;  // candidates per side held per thread
 constexpr int kBlockTop = 2;       // candidates per side kept per row group
-constexpr int kListCap = 1024;     // threshold list entries per side
-constexpr int kWaveList = 16;      // threshold list entries per side per wave
+constexpr int kSelRecords = 2;     // row-group records held per thread
+constexpr int kSelPerThread = kSelRecords * kBlockTop;  // per side
 constexpr double kTau = 1e-12;     // curvature floor of a degenerate pair
 
 // how the row kernel of an iteration gets K(x_i, x_s) (set by the selection)
@@ -64,11 +63,7 @@ struct WorkingSet {
     int64_t inner_total;  // inner steps summed over iterations
     int64_t rescans;      // iterations that rescanned exhausted blocks
     int64_t slow_selects; // iterations that fell back to a full scan
-    int64_t list_hits;    // iterations selected from the threshold list
-    double theta[2];      // list thresholds for the next row kernel (up, low)
-    double spread[2];     // distance of each threshold below the q/2-th key
     int64_t prof[12];     // select/solve phase times (wall-clock ticks)
-    int64_t stat[8];      // selection statistics (threshold list use)
     // kernel-row cache
     int32_t path;             // PATH_* of the current iteration
     int32_t pad2;
@@ -117,12 +112,9 @@ struct RowArgs {
     const float* z;
     const WorkingSet* ws;
     const float* xS;      // kMaxQ x ldp rows of the working-set samples
-    double* cand_key;     // [nb][2][half]: up scores v, low scores -v
+    double* cand_key;     // [blocks][2][kBlockTop]: up scores v, low -v
     int32_t* cand_idx;
     float* rows_out;      // nS x n (tests)
-    double* list_key;     // [2][kListCap] keys at or above ws->theta
-    int32_t* list_idx;
-    int32_t* list_cnt;    // [2] entries appended (> kListCap: overflow)
     float* cache;         // kernel-row cache rows (stride ldc), or nullptr
     int64_t ldc;
     int64_t n, ldp;
@@ -137,10 +129,7 @@ struct RowArgs {
 struct SelArgs {
     const double* cand_key;
     const int32_t* cand_idx;
-    const double* list_key;  // threshold list of the previous row kernel
-    const int32_t* list_idx;
-    int32_t* list_cnt;       // read, then cleared (nullptr: no list)
-    int32_t nb, half;     // nb: candidate lists (one per k_rows wave)
+    int32_t nb, half;     // nb: candidate records (one per k_rows block)
     WorkingSet* ws;
     double* alpha;
     uint8_t* st;
@@ -160,7 +149,7 @@ struct SelArgs {
     int32_t max_inner;
     int64_t max_iter;
     int32_t mode;
-    int32_t group_rows;   // rows behind one candidate list (one k_rows wave)
+    int32_t group_rows;   // rows behind one candidate record (a k_rows block)
     int32_t slice;        // features per LDS slice of the working-set rows
     // kernel-row cache (cache_slots == 0: none)
     const float* cache;   // cache_slots rows of ldc floats

@@ -4,9 +4,9 @@
 // responses are updated after the working set has been optimised).  It
 // streams X once: for each 16-row tile, the dot products with the (at most
 // 16 per column block) working-set samples on the matrix cores (16x16x4
-// fp32), the RBF epilogue, F_i += sum_s dc_s K(x_i, x_s) in fp64, the keys v
-// of the variables of the tile and per-wave candidates of each side for the
-// next selection.
+// fp32), the RBF epilogue, F_i += sum_s dc_s K(x_i, x_s) in fp64; then the
+// keys v of the variables and per-block candidates of each side for the next
+// selection.
 #include <hip/hip_ext.h>
 
 #include "common.hpp"
@@ -55,8 +55,8 @@ __host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp,
            (size_t)kRowWaves * rows_wave_buf(nblk_cols, csr) * sizeof(float);
 }
 
-// per-wave threshold list: kWaveList (key, index) pairs per side
-constexpr int kWaveListBytes = 2 * kWaveList * (8 + 4);
+// per-block table of the waves' candidate records (see k_rows)
+constexpr int kBlockRecBytes = kRowWaves * 4 * (8 + 4);
 
 // per-block table of the working-set slots: norm, sample, cache slot
 constexpr int kSlotInfoBytes = kMaxQ * (4 + 4 + 4);
@@ -65,7 +65,7 @@ size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
                       bool csr)
 {
     return rows_aux_offset(nblk_cols, ldp, csr) +
-           (size_t)kRowWaves * (rows_aux_bytes(tiles, svr) + kWaveListBytes) +
+           (size_t)kRowWaves * rows_aux_bytes(tiles, svr) + kBlockRecBytes +
            kSlotInfoBytes;
 }
 
@@ -133,9 +133,9 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     constexpr bool ROWS = (MODE & RU_ROWS) != 0;
     constexpr bool CAND = (MODE & RU_CAND) != 0;
     constexpr bool XS = UPD || ROWS;  // the working-set samples are needed
-    // hot mode: also list every variable whose key reaches the threshold
-    // of its side (the selection then ranks that short list only)
-    constexpr bool LIST = UPD && CAND;
+    // hot mode (a training iteration): the update and the candidates, with
+    // the kernel-row cache
+    constexpr bool HOT = UPD && CAND;
     constexpr int kXsEarly = 2;       // staging loads issued with the stream
     extern __shared__ __align__(16) unsigned char smem[];
     const WorkingSet* ws = a.ws;
@@ -175,20 +175,13 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     float* sqw = reinterpret_cast<float*>(aux + 8 * RW);
     float* zw = reinterpret_cast<float*>(aux + 12 * RW);
     uint8_t* stw = aux + (SVR ? 16 : 12) * RW;  // copy (i,-) at stw[RW + r]
-    unsigned char* wl = smem + rows_aux_offset(NBLK, ldp, CSR) +
-                        kRowWaves * rows_aux_bytes(T, SVR) +
-                        wave * kWaveListBytes;
-    double* wlk = reinterpret_cast<double*>(wl);              // [2][kWaveList]
-    int32_t* wli = reinterpret_cast<int32_t*>(wl + 16 * kWaveList);
-    double th[2] = {INFINITY, INFINITY};
-    if (LIST) {
-        th[0] = ws->theta[0];
-        th[1] = ws->theta[1];
-    }
-    int nlist[2] = {0, 0};  // wave-uniform entry counts
+    unsigned char* brec = smem + rows_aux_offset(NBLK, ldp, CSR) +
+                          kRowWaves * rows_aux_bytes(T, SVR);
+    double* brk = reinterpret_cast<double*>(brec);  // [kRowWaves][4]
+    int32_t* bri = reinterpret_cast<int32_t*>(brec + kRowWaves * 32);
     // slot table (block-wide): norm, sample and cache slot of every slot
     unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp, CSR) +
-                           kRowWaves * (rows_aux_bytes(T, SVR) + kWaveListBytes);
+                           kRowWaves * rows_aux_bytes(T, SVR) + kBlockRecBytes;
     float* sl_sq = reinterpret_cast<float*>(sinfo);
     int32_t* sl_smp = reinterpret_cast<int32_t*>(sinfo + 4 * kMaxQ);
     int32_t* sl_cs = reinterpret_cast<int32_t*>(sinfo + 8 * kMaxQ);
@@ -232,17 +225,6 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     };
 
     Top2 up, lo;  // this lane's best candidates of each side
-    // (called by the whole wave) appends the passing lanes' entries
-    auto append = [&](int side, bool pass, double key, int32_t idx) {
-        const unsigned long long m = __ballot(pass);
-        if (m == 0) return;
-        const int pos = nlist[side] + lanes_below(m);
-        if (pass && pos < kWaveList) {
-            wlk[side * kWaveList + pos] = key;
-            wli[side * kWaveList + pos] = idx;
-        }
-        nlist[side] += __popcll(m);
-    };
     // keys of the variables of row lr (only lanes with own = true hold one)
     auto push = [&](int lr, double Fn, bool own) {
         const int32_t row = (int32_t)(rw0 + lr);
@@ -253,20 +235,12 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         const bool u0 = own && (s0 & ST_UP), l0 = own && (s0 & ST_LOW);
         if (u0) up.push(v0, row);
         if (l0) lo.push(-v0, row);
-        if (LIST) {
-            append(0, u0 && v0 >= th[0], v0, row);
-            append(1, l0 && -v0 >= th[1], -v0, row);
-        }
         if (SVR) {
             const uint8_t s1 = stw[RW + lr];
             const double v1 = ((double)zw[lr] + a.eps) - Fn;
             const bool u1 = own && (s1 & ST_UP), l1 = own && (s1 & ST_LOW);
             if (u1) up.push(v1, (int32_t)(n + row));
             if (l1) lo.push(-v1, (int32_t)(n + row));
-            if (LIST) {
-                append(0, u1 && v1 >= th[0], v1, (int32_t)(n + row));
-                append(1, l1 && -v1 >= th[1], -v1, (int32_t)(n + row));
-            }
         }
     };
 
@@ -274,7 +248,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         // Path of this iteration (hot mode: set by the selection; tests:
         // always computed from X) and the cache slot of this lane's
         // working-set slots.
-        const int32_t path = LIST ? ws->path : PATH_STREAM;
+        const int32_t path = HOT ? ws->path : PATH_STREAM;
 
         // F_i += sum_s cf_s K(x_i, x_s) for the 16 rows of tile ti, given
         // this lane's K values kv[b][v] (row lr + v of slot b * 16 + nl),
@@ -305,7 +279,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             if (CAND) push(orl, Fn, nl < 4 && orl < nw);
         };
 
-        if (LIST && path == PATH_CACHED) {
+        if (HOT && path == PATH_CACHED) {
             // Every working-set sample is cached: lane (g, nl) reads rows
             // lr .. lr + 3 of its slot's row as one float4, kRing tiles
             // ahead.  Unused slots read a valid address and are zeroed.
@@ -372,7 +346,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 const int32_t i = ws->S[tid], c = ws->cslot[tid];
                 sq0 = tid < nS ? q : 0.0f;
                 smp0 = tid < nS ? i : -1;
-                cs0 = (LIST && tid < nS) ? c : -1;
+                cs0 = (HOT && tid < nS) ? c : -1;
             }
             AuxRegs ar;
             aux_issue(0, ar);
@@ -399,7 +373,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             }
             __syncthreads();
 
-            const bool INS = LIST && path == PATH_INSERT;
+            const bool INS = HOT && path == PATH_INSERT;
             constexpr int KB = 8;  // nonzeros loaded per batch
             for (int p0 = 0; p0 < Tw; p0 += 4) {
                 const int r = 16 * p0 + lane;  // this lane's row (local)
@@ -517,7 +491,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 const int32_t i = ws->S[tid], c = ws->cslot[tid];
                 sq0 = tid < nS ? q : 0.0f;
                 smp0 = tid < nS ? i : -1;
-                cs0 = (LIST && tid < nS) ? c : -1;
+                cs0 = (HOT && tid < nS) ? c : -1;
             }
             float4 xv[kXsEarly];
 #pragma unroll
@@ -550,7 +524,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             // The slab loop; on the insert path the rows of the samples
             // missing from the cache also go to their new cache slots.
             {
-                const bool INS = LIST && path == PATH_INSERT;
+                const bool INS = HOT && path == PATH_INSERT;
                 floatx4 acc[NBLK];
                 int pti = 0, psl = 0;  // slab being processed
                 for (int s0 = 0; s0 < Tw * nslab; s0 += kRing) {
@@ -632,40 +606,37 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             aux_issue(k0, ar);
             aux_store(k0, ar);
         }
-        for (int ti = 0; ti < Tw; ++ti) {
-            const int orl = 16 * ti + 4 * g + (nl & 3);
-            push(orl, Fw[orl], nl < 4 && orl < nw);
-        }
-    }
-
-    if (LIST) {
-        // reserve room in the global list (a wave that saw more entries
-        // than it keeps pushes the count past the capacity: overflow)
-#pragma unroll
-        for (int side = 0; side < 2; ++side) {
-            const int c = nlist[side];
-            if (c == 0) continue;
-            int base = 0;
-            if (lane == 0)
-                base = atomicAdd(a.list_cnt + side,
-                                 c > kWaveList ? kListCap + 1 : c);
-            base = __builtin_amdgcn_readfirstlane(base);
-            if (c <= kWaveList && lane < c && base + lane < kListCap) {
-                a.list_key[side * kListCap + base + lane] =
-                    wlk[side * kWaveList + lane];
-                a.list_idx[side * kListCap + base + lane] =
-                    wli[side * kWaveList + lane];
-            }
+        // keys of the wave's variables, one row per lane
+        for (int r0 = 0; r0 < nw; r0 += 64) {
+            const int r = r0 + lane;
+            const bool own = r < nw;
+            const int rr = own ? r : 0;
+            push(rr, Fw[rr], own);
         }
     }
 
     if (!CAND) return;
-    // the best two of each side over this wave's rows; a variable outside
-    // the global top q/2 never needs more (k_select rescans a row group
-    // whose two candidates were both taken)
-    const size_t wid = (size_t)blockIdx.x * kRowWaves + wave;
-    wave_top2_pair(up, lo, a.cand_key + wid * 2 * kBlockTop,
-                   a.cand_idx + wid * 2 * kBlockTop);
+    // The best two of each side over the block's rows: every wave's best
+    // two go to the block table, then wave 0 takes the best two of those.
+    // A variable outside the global top q/2 never needs more (k_select
+    // rescans a row group whose two candidates were both taken).
+    wave_top2_pair(up, lo, brk + 4 * wave, bri + 4 * wave);
+    __syncthreads();
+    if (wave == 0) {
+        Top2 u, l;
+        if (lane < kRowWaves) {
+            u.k1 = brk[4 * lane];
+            u.k2 = brk[4 * lane + 1];
+            l.k1 = brk[4 * lane + 2];
+            l.k2 = brk[4 * lane + 3];
+            u.i1 = bri[4 * lane];
+            u.i2 = bri[4 * lane + 1];
+            l.i1 = bri[4 * lane + 2];
+            l.i2 = bri[4 * lane + 3];
+        }
+        wave_top2_pair(u, l, a.cand_key + (size_t)blockIdx.x * 2 * kBlockTop,
+                       a.cand_idx + (size_t)blockIdx.x * 2 * kBlockTop);
+    }
 }
 
 template <bool SVR, int NBLK, int MODE, bool CSR>

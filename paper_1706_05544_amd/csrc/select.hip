@@ -199,23 +199,6 @@ __device__ void top_half(double (*k)[kSurv], int32_t (*i)[kSurv], int M0,
     __syncthreads();
 }
 
-// Threshold of the next list of one side, from this selection's best key
-// K1 and half-th key Kh and the entries c the list held (c < 0: the list
-// was not consulted).  The spread below Kh adapts so that the list keeps a
-// few times `half` entries: an empty or short list widens it, a long or
-// overflowing one narrows it.
-__device__ __forceinline__ double next_threshold(double K1, double Kh, int c,
-                                                 int half, double& spread)
-{
-    if (c < half) spread = fmax(2.0 * spread, K1 - Kh);
-    else if (c > kListCap) spread *= 0.25;
-    else if (c > max(4 * kPairSmall, 8 * half)) spread *= 0.5;
-    else if (c < 3 * half) spread *= 1.5;
-    if (!(spread > 0.0) || !(spread < INFINITY))
-        spread = 1e-6 * fmax(1.0, fabs(Kh));
-    return Kh == -INFINITY ? INFINITY : Kh - spread;
-}
-
 // Exact top-`half` over `count` entries produced by get(e, key, index), by
 // `half` block-wide rounds (each: the best entry after the previous winner).
 // All threads of the block take part; thread 0 writes ok/oi.
@@ -302,7 +285,7 @@ template <bool SVR, int NBLK>
 __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 {
     WorkingSet* ws = a.ws;
-    // (SS_CHECK_DONE) ws->done is tested once the list loads are in flight
+    // (SS_CHECK_DONE) ws->done is tested once the record loads are in flight
     const int32_t done0 = (a.mode & SS_CHECK_DONE) ? ws->done : 0;
     const uint64_t t_start = wall_clock64();
 
@@ -312,7 +295,6 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     __shared__ int32_t upi[kMaxHalf], loi[kMaxHalf];
     __shared__ double rmax[2][NW * 4];
     __shared__ double theta[2];
-    __shared__ double thnext[2];
     __shared__ double svk[2][kSurv];
     __shared__ int32_t svi[2][kSurv];
     __shared__ int32_t nsv[2];
@@ -338,275 +320,252 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     const int64_t n = a.n, ldp = a.ldp;
     const bool given = (a.mode & SS_GIVEN_B) != 0;
     if (given && done0) return;
+    // (1) the candidate records of the row groups (best two up keys, best
+    // two low keys, their variables): thread t loads records t, t +
+    // kSelThreads, ... with 16-byte loads, issued before anything else
+    static_assert(kBlockTop == 2, "candidate record layout");
+    double ku[kSelPerThread], kl[kSelPerThread];
+    int32_t iu[kSelPerThread], il[kSelPerThread];
+#pragma unroll
+    for (int j = 0; j < kSelRecords; ++j) {
+        const int r = tid + j * kSelThreads;
+        double2 k01 = make_double2(-INFINITY, -INFINITY);
+        double2 k23 = k01;
+        int4 ix = make_int4(INT_MAX, INT_MAX, INT_MAX, INT_MAX);
+        if (!given && r < a.nb) {
+            const double* rk0 = a.cand_key + 4 * (size_t)r;
+            k01 = *reinterpret_cast<const double2*>(rk0);
+            k23 = *reinterpret_cast<const double2*>(rk0 + 2);
+            ix = *reinterpret_cast<const int4*>(a.cand_idx + 4 * (size_t)r);
+        }
+        ku[2 * j] = k01.x;
+        ku[2 * j + 1] = k01.y;
+        kl[2 * j] = k23.x;
+        kl[2 * j + 1] = k23.y;
+        iu[2 * j] = ix.x;
+        iu[2 * j + 1] = ix.y;
+        il[2 * j] = ix.z;
+        il[2 * j + 1] = ix.w;
+    }
     const int64_t iter0 = ws->iter;  // issued early, used in (8)
     // Counters: read now and written back once by thread 0 at the exit, so
     // that no read-modify-write of global memory waits on the way.  Global
     // stores are likewise left to the exit: a barrier after a store waits
     // for it.
-    int64_t c_rows = 0, c_inner = 0, c_resc = 0, c_slow = 0, c_hits = 0;
+    int64_t c_rows = 0, c_inner = 0, c_resc = 0, c_slow = 0;
     int64_t c_prof[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-    uint64_t t_l1 = 0, t_l2 = 0;  // (list path) entries staged, ranked
-    double spr[2] = {0.0, 0.0};
-    int64_t c_stat[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-
+    // ends of the merge phases: bound, rank, exhausted groups
+    uint64_t t_c1 = t_start, t_c2 = t_start, t_c3 = t_start;
     if (tid == 0) {
-        spr[0] = ws->spread[0];
-        spr[1] = ws->spread[1];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) c_stat[k] = ws->stat[k];
-
         c_rows = ws->rows;
         c_inner = ws->inner_total;
         c_resc = ws->rescans;
         c_slow = ws->slow_selects;
-        c_hits = ws->list_hits;
 #pragma unroll
         for (int k = 0; k < 12; ++k) c_prof[k] = ws->prof[k];
     }
     if (tid == 0) shDone = 0;
-    bool fastp = false;  // (thread 0) this selection used the list
 
     if (!given) {
         if (tid < kMaxHalf) {
             upk[tid] = lok[tid] = -INFINITY;
             upi[tid] = loi[tid] = INT_MAX;
         }
-        if (tid < 2) thnext[tid] = INFINITY;
-        // (0) the threshold list: every variable whose key reached the
-        // threshold of its side.  With at least `half` of them on a side,
-        // the top `half` of the side are among them (exact).  Its entries
-        // are loaded together with the counts.
-        int lc0 = 0, lc1 = 0;
-        double lk0 = 0.0, lk1 = 0.0;
-        int32_t li0 = 0, li1 = 0;
-        if (a.list_cnt) {
-            lc0 = a.list_cnt[0];
-            lc1 = a.list_cnt[1];
-            lk0 = a.list_key[tid];
-            li0 = a.list_idx[tid];
-            lk1 = a.list_key[kListCap + tid];
-            li1 = a.list_idx[kListCap + tid];
-        }
         if (done0) return;  // uniform over the block
-        const bool fast = lc0 >= half && lc1 >= half && lc0 <= kListCap &&
-                          lc1 <= kListCap;
-        if (tid == 0 && a.list_cnt) {
-            c_stat[0] += lc0 < half;
-            c_stat[1] += lc1 < half;
-            c_stat[2] += lc0 > kListCap;
-            c_stat[3] += lc1 > kListCap;
-            c_stat[4] += lc0 > kPairSmall && lc0 <= kListCap;
-            c_stat[5] += lc1 > kPairSmall && lc1 <= kListCap;
-            if (fast) {
-                c_stat[6] += lc0;
-                c_stat[7] += lc1;
+        const int cnt = a.nb * kBlockTop;
+        // (2) maxima of every 16-lane row: distinct candidates, so the
+        // half-th largest of them bounds the half-th best key from below
+        double mu = -INFINITY, ml = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kSelPerThread; ++j) {
+            mu = fmax(mu, ku[j]);
+            ml = fmax(ml, kl[j]);
+        }
+        mu = row_max_f64(mu);
+        ml = row_max_f64(ml);
+        if ((lane & 15) == 0) {
+            rmax[0][wave * 4 + (lane >> 4)] = mu;
+            rmax[1][wave * 4 + (lane >> 4)] = ml;
+        }
+        if (tid < 2) nsv[tid] = 0;
+        __syncthreads();
+        if (wave == 0) {
+            // lane l holds row maximum l; theta = the largest x_l with at
+            // least `half` row maxima >= x_l (-inf if there is none)
+            for (int side = 0; side < 2; ++side) {
+                const double x = rmax[side][lane];
+                int c = 0;
+#pragma unroll 16
+                for (int j = 0; j < NW * 4; ++j) c += rmax[side][j] >= x;
+                double th = (c >= half && x != -INFINITY) ? x : -INFINITY;
+                th = row_max_f64(th);
+                th = fmax(fmax(rl_f64(th, 0), rl_f64(th, 16)),
+                          fmax(rl_f64(th, 32), rl_f64(th, 48)));
+                if (lane == 0) theta[side] = th;
             }
         }
-        if (fast) {
-            if (tid < lc0) {
-                svk[0][tid] = lk0;
-                svi[0][tid] = li0;
+        __syncthreads();
+        t_c1 = wall_clock64();
+        // (3) keep the candidates at or above the bound
+        {
+            const double th0 = theta[0], th1 = theta[1];
+#pragma unroll
+            for (int j = 0; j < kSelPerThread; ++j) {
+                for (int side = 0; side < 2; ++side) {
+                    const double kv = side ? kl[j] : ku[j];
+                    const int32_t iv = side ? il[j] : iu[j];
+                    const double th = side ? th1 : th0;
+                    const bool keep = kv != -INFINITY && kv >= th;
+                    const unsigned long long m = __ballot(keep);
+                    if (m == 0) continue;
+                    int base = 0;
+                    if (lane == 0) base = atomicAdd(&nsv[side], __popcll(m));
+                    base = __builtin_amdgcn_readfirstlane(base);
+                    const int pos = base + lanes_below(m);
+                    if (keep && pos < kSurv) {
+                        svk[side][pos] = kv;
+                        svi[side][pos] = iv;
+                    }
+                }
             }
-            if (tid < lc1) {
-                svk[1][tid] = lk1;
-                svi[1][tid] = li1;
-            }
-            __syncthreads();
-            t_l1 = wall_clock64();
-            top_half(svk, svi, lc0, lc1, half, upk, upi, lok, loi, nsv);
-            t_l2 = wall_clock64();
-            if (tid == 0) {
-                c_hits += 1;
-                fastp = true;
-            }
+        }
+        __syncthreads();
+        const int M0 = nsv[0], M1 = nsv[1];
+        const bool overflow = M0 > kSurv || M1 > kSurv;
+        if (!overflow) {
+            // (4) rank the survivors: side 0 on threads [0,512), side 1
+            // on the rest
+            top_half(svk, svi, M0, M1, half, upk, upi, lok, loi, nsv);
         } else {
-            // (1) the per-group candidates
-            const int cnt = a.nb * kBlockTop;
-            double ku[kSelPerThread], kl[kSelPerThread];
-            int32_t iu[kSelPerThread], il[kSelPerThread];
-#pragma unroll
-            for (int j = 0; j < kSelPerThread; ++j) {
-                // unconditional loads (a valid entry when unused)
-                const int e = tid + j * kSelThreads;
-                const int ec = min(e, cnt - 1);
-                const int blk = ec / kBlockTop, k = ec - blk * kBlockTop;
-                const size_t bu = (size_t)blk * 2 * kBlockTop;
-                ku[j] = a.cand_key[bu + k];
-                iu[j] = a.cand_idx[bu + k];
-                kl[j] = a.cand_key[bu + kBlockTop + k];
-                il[j] = a.cand_idx[bu + kBlockTop + k];
+            // (4') too many ties at the bound (e.g. alpha = 0): exact
+            // block rounds over all candidates
+            for (int side = 0; side < 2; ++side) {
+                auto get = [&](int64_t e, double& key, int32_t& t) {
+                    const int64_t blk = e / kBlockTop,
+                                  k = e - blk * kBlockTop;
+                    const size_t o = (size_t)blk * 2 * kBlockTop +
+                                     (side ? kBlockTop : 0) + k;
+                    key = a.cand_key[o];
+                    t = a.cand_idx[o];
+                };
+                block_rounds(cnt, get, half, side ? lok : upk,
+                             side ? loi : upi, rk, ri);
             }
-#pragma unroll
-            for (int j = 0; j < kSelPerThread; ++j) {
-                if (tid + j * kSelThreads >= cnt) {
-                    ku[j] = kl[j] = -INFINITY;
-                    iu[j] = il[j] = INT_MAX;
+            if (tid == 0) c_slow += 1;
+        }
+        t_c2 = wall_clock64();
+        // (5) row groups whose whole candidate list was taken may hold
+        // more: wave 0 finds them (lane-parallel)
+        const uint32_t grows = (uint32_t)a.group_rows;
+        if (wave == 0) {
+            for (int side = 0; side < 2; ++side) {
+                const double* kk = side ? lok : upk;
+                const int32_t* ii = side ? loi : upi;
+                const bool valid = lane < half && kk[lane] != -INFINITY;
+                const int32_t b =
+                    valid ? (int32_t)((uint32_t)sample_of(SVR, ii[lane], n) /
+                                      grows)
+                          : -1 - lane;
+                int c = 0;
+                bool first = true;
+                for (int j = 0; j < half; ++j) {
+                    const int32_t bj = rl_i32(b, j);
+                    c += bj == b;
+                    first &= !(j < lane && bj == b);
                 }
+                const bool ex = valid && c >= kBlockTop && first;
+                const unsigned long long m = __ballot(ex);
+                if (ex) exb[side][lanes_below(m)] = b;
+                if (lane == 0) nex[side] = __popcll(m);
             }
-            // (2) maxima of every 16-lane row: distinct candidates, so the
-            // half-th largest of them bounds the half-th best key from below
-            double mu = -INFINITY, ml = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < kSelPerThread; ++j) {
-                mu = fmax(mu, ku[j]);
-                ml = fmax(ml, kl[j]);
-            }
-            mu = row_max_f64(mu);
-            ml = row_max_f64(ml);
-            if ((lane & 15) == 0) {
-                rmax[0][wave * 4 + (lane >> 4)] = mu;
-                rmax[1][wave * 4 + (lane >> 4)] = ml;
-            }
-            if (tid < 2) nsv[tid] = 0;
-            __syncthreads();
-            if (wave == 0) {
-                // lane l holds row maximum l; theta = the largest x_l with at
-                // least `half` row maxima >= x_l (-inf if there is none)
-                for (int side = 0; side < 2; ++side) {
-                    const double x = rmax[side][lane];
-                    int c = 0;
-#pragma unroll 16
-                    for (int j = 0; j < NW * 4; ++j) c += rmax[side][j] >= x;
-                    double th = (c >= half && x != -INFINITY) ? x : -INFINITY;
-                    th = row_max_f64(th);
-                    th = fmax(fmax(rl_f64(th, 0), rl_f64(th, 16)),
-                              fmax(rl_f64(th, 32), rl_f64(th, 48)));
-                    if (lane == 0) theta[side] = th;
-                }
-            }
-            __syncthreads();
-            // (3) keep the candidates at or above the bound
-            {
-                const double th0 = theta[0], th1 = theta[1];
-#pragma unroll
-                for (int j = 0; j < kSelPerThread; ++j) {
-                    for (int side = 0; side < 2; ++side) {
-                        const double kv = side ? kl[j] : ku[j];
-                        const int32_t iv = side ? il[j] : iu[j];
-                        const double th = side ? th1 : th0;
-                        const bool keep = kv != -INFINITY && kv >= th;
-                        const unsigned long long m = __ballot(keep);
-                        if (m == 0) continue;
-                        int base = 0;
-                        if (lane == 0) base = atomicAdd(&nsv[side], __popcll(m));
-                        base = __builtin_amdgcn_readfirstlane(base);
-                        const int pos = base + lanes_below(m);
-                        if (keep && pos < kSurv) {
-                            svk[side][pos] = kv;
-                            svi[side][pos] = iv;
-                        }
-                    }
-                }
-            }
-            __syncthreads();
-            const int M0 = nsv[0], M1 = nsv[1];
-            const bool overflow = M0 > kSurv || M1 > kSurv;
-            if (!overflow) {
-                // (4) rank the survivors: side 0 on threads [0,512), side 1
-                // on the rest
-                top_half(svk, svi, M0, M1, half, upk, upi, lok, loi, nsv);
-            } else {
-                // (4') too many ties at the bound (e.g. alpha = 0): exact
-                // block rounds over all candidates
-                for (int side = 0; side < 2; ++side) {
-                    auto get = [&](int64_t e, double& key, int32_t& t) {
-                        const int64_t blk = e / kBlockTop,
-                                      k = e - blk * kBlockTop;
-                        const size_t o = (size_t)blk * 2 * kBlockTop +
-                                         (side ? kBlockTop : 0) + k;
-                        key = a.cand_key[o];
-                        t = a.cand_idx[o];
-                    };
-                    block_rounds(cnt, get, half, side ? lok : upk,
-                                 side ? loi : upi, rk, ri);
-                }
-                if (tid == 0) c_slow += 1;
-            }
-            // (5) row groups whose whole candidate list was taken may hold
-            // more: wave 0 finds them (lane-parallel)
-            const uint32_t grows = (uint32_t)a.group_rows;
-            if (wave == 0) {
-                for (int side = 0; side < 2; ++side) {
-                    const double* kk = side ? lok : upk;
-                    const int32_t* ii = side ? loi : upi;
-                    const bool valid = lane < half && kk[lane] != -INFINITY;
+        }
+        __syncthreads();
+        t_c3 = wall_clock64();
+        if (nex[0] + nex[1] > 0) {
+            // (6) rare: the exact best `half` of the winners outside those
+            // groups plus every variable of the groups (keys from F); a
+            // side without such groups keeps its winners.  Staged and
+            // ranked like the survivors when they fit, else by rounds.
+            const uint32_t NV = SVR ? 2 : 1;
+            const uint32_t per = grows * NV;
+            if (tid < 2) {
+                const int side = tid;
+                const int ne = nex[side];
+                const double* kk = side ? lok : upk;
+                const int32_t* ii = side ? loi : upi;
+                int c = 0;
+                for (int k = 0; k < half; ++k) {
+                    if (kk[k] == -INFINITY) continue;
                     const int32_t b =
-                        valid ? (int32_t)((uint32_t)sample_of(SVR, ii[lane], n) /
-                                          grows)
-                              : -1 - lane;
-                    int c = 0;
-                    bool first = true;
-                    for (int j = 0; j < half; ++j) {
-                        const int32_t bj = rl_i32(b, j);
-                        c += bj == b;
-                        first &= !(j < lane && bj == b);
+                        (int32_t)((uint32_t)sample_of(SVR, ii[k], n) / grows);
+                    bool ex = false;
+                    for (int x = 0; x < ne; ++x) ex |= exb[side][x] == b;
+                    if (!ex) {
+                        svk[side][c] = kk[k];
+                        svi[side][c] = ii[k];
+                        ++c;
                     }
-                    const bool ex = valid && c >= kBlockTop && first;
-                    const unsigned long long m = __ballot(ex);
-                    if (ex) exb[side][lanes_below(m)] = b;
-                    if (lane == 0) nex[side] = __popcll(m);
                 }
+                nsv[side] = c;
             }
             __syncthreads();
-            if (nex[0] + nex[1] > 0) {
-                // (6) rare: exact block rounds over the winners outside those
-                // groups plus every variable of the groups (keys from F)
-                const uint32_t NV = SVR ? 2 : 1;
+            const int nk0 = nsv[0], nk1 = nsv[1];
+            const int64_t tot0 = nk0 + (int64_t)nex[0] * per;
+            const int64_t tot1 = nk1 + (int64_t)nex[1] * per;
+            // variable e - nk of the exhausted groups of a side
+            auto group_var = [&](int side, int64_t q, double& key,
+                                 int32_t& t) {
+                const uint32_t x = (uint32_t)(q / per),
+                               o = (uint32_t)(q - (int64_t)x * per);
+                const int64_t row = (int64_t)exb[side][x] * grows + (o % grows);
+                key = -INFINITY;
+                t = INT_MAX;
+                if (row < n) {
+                    const int64_t tt = o < grows ? row : n + row;
+                    double u, l;
+                    var_scores<SVR>(a, tt, u, l);
+                    key = side ? l : u;
+                    t = (int32_t)tt;
+                }
+            };
+            if (tot0 <= kSurv && tot1 <= kSurv) {
+#pragma unroll
                 for (int side = 0; side < 2; ++side) {
-                    const int ne = nex[side];
-                    if (ne == 0) continue;
-                    double* kk = side ? lok : upk;
-                    int32_t* ii = side ? loi : upi;
-                    if (tid == 0) {
-                        int c = 0;
-                        for (int k = 0; k < half; ++k) {
-                            if (kk[k] == -INFINITY) continue;
-                            const int32_t b = (int32_t)(
-                                (uint32_t)sample_of(SVR, ii[k], n) / grows);
-                            bool ex = false;
-                            for (int x = 0; x < ne; ++x) ex |= exb[side][x] == b;
-                            if (!ex) {
-                                keepk[c] = kk[k];
-                                keepi[c] = ii[k];
-                                ++c;
-                            }
-                        }
-                        nkeep = c;
+                    const int nk = side ? nk1 : nk0;
+                    const int64_t tot = side ? tot1 : tot0;
+                    if (tid >= nk && tid < tot) {
+                        double key;
+                        int32_t t;
+                        group_var(side, tid - nk, key, t);
+                        svk[side][tid] = key;
+                        svi[side][tid] = t;
+                    }
+                }
+                __syncthreads();
+                top_half(svk, svi, (int)tot0, (int)tot1, half, upk, upi, lok,
+                         loi, nsv);
+            } else {
+                for (int side = 0; side < 2; ++side) {
+                    if (nex[side] == 0) continue;
+                    const int nk = side ? nk1 : nk0;
+                    if (tid < nk) {
+                        keepk[tid] = svk[side][tid];
+                        keepi[tid] = svi[side][tid];
                     }
                     __syncthreads();
-                    const int nk = nkeep;
-                    const uint32_t per = grows * NV;
                     auto get = [&](int64_t e, double& key, int32_t& t) {
                         if (e < nk) {
                             key = keepk[e];
                             t = keepi[e];
-                            return;
-                        }
-                        const uint32_t q = (uint32_t)(e - nk);
-                        const uint32_t x = q / per, o = q - x * per;
-                        const int64_t row =
-                            (int64_t)exb[side][x] * grows + (o % grows);
-                        key = -INFINITY;
-                        t = INT_MAX;
-                        if (row < n) {
-                            const int64_t tt = o < grows ? row : n + row;
-                            double u, l;
-                            var_scores<SVR>(a, tt, u, l);
-                            key = side ? l : u;
-                            t = (int32_t)tt;
+                        } else {
+                            group_var(side, e - nk, key, t);
                         }
                     };
-                    block_rounds((int64_t)nk + (int64_t)ne * per, get, half, kk,
-                                 ii, rk, ri);
+                    block_rounds(side ? tot1 : tot0, get, half,
+                                 side ? lok : upk, side ? loi : upi, rk, ri);
                 }
-                if (tid == 0) c_resc += 1;
             }
-        }
-        if (tid == 0) {
-            thnext[0] = next_threshold(upk[0], upk[half - 1],
-                                       a.list_cnt ? lc0 : -1, half, spr[0]);
-            thnext[1] = next_threshold(lok[0], lok[half - 1],
-                                       a.list_cnt ? lc1 : -1, half, spr[1]);
+            if (tid == 0) c_resc += 1;
         }
     }
     const uint64_t t_merge = wall_clock64();
@@ -711,22 +670,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     const uint64_t t_build = wall_clock64();
     // state written at every exit (threads 0 and 1)
     auto finish = [&](int64_t t_end) {
-        if (tid < 2) {
-            if (a.list_cnt) a.list_cnt[tid] = 0;
-            if (!given) ws->theta[tid] = thnext[tid];
-        }
         if (tid == 0) {
             if (!given) {
-                ws->spread[0] = spr[0];
-                ws->spread[1] = spr[1];
                 if (shDone) ws->done = shDone;
                 ws->gap = shGap;
                 ws->m = shMx;
                 ws->M = shMn;
             }
-            ws->list_hits = c_hits;
-#pragma unroll
-            for (int k = 0; k < 8; ++k) ws->stat[k] = c_stat[k];
             ws->slow_selects = c_slow;
             ws->rescans = c_resc;
             (void)t_end;
@@ -776,7 +726,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         if (lane < nS) hslot = a.slot_of[shS[lane]];
         clk0 = *a.clock;
     }
-    if (wave == 1 && lane == 0) {
+    if (wave == 1) {
         c_served = ws->cache_served;
         c_filled = ws->cache_filled;
     }
@@ -815,6 +765,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             KSS[ia][ib] = k;
         }
         if (tid < nS) shsS[tid] = a.sq[shS[tid]];
+        t_stage = wall_clock64();
     } else {
         const int g = lane >> 4, nl = lane & 15;
         const int bi = wave / NBLK, bj = wave - bi * NBLK;
@@ -920,10 +871,14 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 const int32_t hs = lane < nS ? hslot : -2;
                 const unsigned long long missm = __ballot(lane < nS && hs < 0);
                 int64_t clk = clk0;
+                // rows stop going to a cache that serves almost nothing (a
+                // working set whose samples rarely all recur): the fills
+                // cost HBM writes and the two paths give the same bits
+                const bool fill = iter0 < 512 || c_served * 8 >= c_filled;
                 if (missm == 0) {
                     path = PATH_CACHED;
                     cslot = hs;
-                } else {
+                } else if (fill) {
                     path = PATH_INSERT;
                     unsigned long long mm = missm;
                     while (mm) {
@@ -1083,12 +1038,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         ws->prof[2] = c_prof[2] + (int64_t)(t_inner - t_kss);
         ws->prof[3] = c_prof[3] + (int64_t)(wall_clock64() - t_inner);
         ws->prof[4] = c_prof[4] + 1;
-        ws->prof[5] = c_prof[5] + (fastp ? (int64_t)(t_merge - t_start) : 0);
+        ws->prof[5] = c_prof[5] + (int64_t)(t_c1 - t_start);
         ws->prof[6] = c_prof[6] + (int64_t)(t_build - t_merge);
         ws->prof[7] = c_prof[7] + (int64_t)(t_stage - t_build);
-        ws->prof[8] = c_prof[8] + (fastp ? (int64_t)(t_l1 - t_start) : 0);
-        ws->prof[9] = c_prof[9] + (fastp ? (int64_t)(t_l2 - t_l1) : 0);
-        ws->prof[10] = c_prof[10] + (fastp ? (int64_t)(t_merge - t_l2) : 0);
+        ws->prof[8] = c_prof[8] + (int64_t)(t_c2 - t_c1);
+        ws->prof[9] = c_prof[9] + (int64_t)(t_c3 - t_c2);
+        ws->prof[10] = c_prof[10] + (int64_t)(t_merge - t_c3);
     }
 }
 

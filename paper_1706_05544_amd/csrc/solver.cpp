@@ -207,16 +207,16 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     }
     if (const char* e = getenv("SVM_TILES"))  // tuning override
         tiles_ = std::max(1, std::min(4096, atoi(e)));
-    const int64_t cand_cap = (int64_t)kSelThreads * kSelPerThread;
-    while (((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_)) * kWaves *
-               kBlockTop > cand_cap)
+    // one candidate record per block; the selection holds at most
+    // kSelRecords of them per thread
+    const int64_t rec_cap = (int64_t)kSelThreads * kSelRecords;
+    while ((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_) > rec_cap)
         ++tiles_;
     if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr) > kLdsMax ||
         (int64_t)16 * tiles_ * f.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED,
                     "training set too large for the dense row kernel"};
     nb_ = (int)((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_));
-    ncand_ = nb_ * kWaves;
 
     F_.alloc((size_t)n_);
     alpha_.alloc((size_t)N_);
@@ -224,11 +224,8 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     y_.alloc((size_t)n_);
     ws_.alloc(1);
     xS_.alloc((size_t)kMaxQ * f.ldp);
-    ckey_.alloc((size_t)ncand_ * 2 * kBlockTop);
-    cidx_.alloc((size_t)ncand_ * 2 * kBlockTop);
-    lkey_.alloc((size_t)2 * kListCap);
-    lidx_.alloc((size_t)2 * kListCap);
-    lcnt_.alloc(2);
+    ckey_.alloc((size_t)nb_ * 2 * kBlockTop);
+    cidx_.alloc((size_t)nb_ * 2 * kBlockTop);
     sum_.alloc(1);
     cvec_.alloc((size_t)n_);
     cblk_.alloc((size_t)compact_blocks(n_));
@@ -242,7 +239,6 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     HIP_TRY(hipMemsetAsync(F_.p, 0, F_.bytes(), s));
     HIP_TRY(hipMemsetAsync(alpha_.p, 0, alpha_.bytes(), s));
     HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
-    HIP_TRY(hipMemsetAsync(lcnt_.p, 0, lcnt_.bytes(), s));
     HIP_TRY(hipMemsetAsync(xS_.p, 0, xS_.bytes(), s));
     DevBuf<int32_t> bad(1);
     HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), s));
@@ -275,9 +271,6 @@ void Solver::launch_keys()
     a.xS = xS_.p;
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
-    a.list_key = lkey_.p;
-    a.list_idx = lidx_.p;
-    a.list_cnt = lcnt_.p;
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
@@ -304,9 +297,6 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
     a.xS = xS_.p;
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
-    a.list_key = lkey_.p;
-    a.list_idx = lidx_.p;
-    a.list_cnt = lcnt_.p;
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
@@ -328,10 +318,7 @@ void Solver::launch_solve(int32_t mode)
     SelArgs a{};
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
-    a.list_key = lkey_.p;
-    a.list_idx = lidx_.p;
-    a.list_cnt = lcnt_.p;
-    a.nb = ncand_;
+    a.nb = nb_;
     a.half = half_;
     a.ws = ws_.p;
     a.alpha = alpha_.p;
@@ -355,7 +342,7 @@ void Solver::launch_solve(int32_t mode)
     a.max_inner = o_.max_inner;
     a.max_iter = o_.max_iter;
     a.mode = mode;
-    a.group_rows = 16 * tiles_;
+    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // rows of a block
     if (cache_) {
         a.cache = cache_->rows.p;
         a.ldc = cache_->ldc;
@@ -582,38 +569,25 @@ SolveResult Solver::train()
             const double k = 10.0 / (double)w.prof[4];  // 100 MHz ticks -> ns
             fprintf(stderr,
                     "[mi355svm] iters=%lld rows=%lld (cache: served %lld "
-                    "filled %lld) inner=%.1f/iter "
-                    "rescans=%lld slow=%lld list=%lld select(us): merge %.2f "
-                    "kss %.2f "
-                    "inner %.2f "
-                    "write %.2f (list merge %.2f = %.2f + %.2f + %.2f, build "
-                    "%.2f stage %.2f); "
-                    "rows kernel %.2f us/launch (%lld timed), cached %.2f "
-                    "us/launch (%lld)\n",
+                    "filled %lld) inner=%.1f/iter rescans=%lld slow=%lld "
+                    "select(us): merge %.2f (bound %.2f rank %.2f groups "
+                    "%.2f rescans %.2f) kss %.2f (build %.2f stage %.2f) "
+                    "inner %.2f write %.2f; rows kernel %.2f us/launch "
+                    "(%lld timed), cached %.2f us/launch (%lld)\n",
                     (long long)w.iter, (long long)w.rows,
                     (long long)w.cache_served, (long long)w.cache_filled,
                     (double)w.inner_total / (double)w.prof[4],
                     (long long)w.rescans, (long long)w.slow_selects,
-                    (long long)w.list_hits,
-                    1e-3 * k * w.prof[0],
-                    1e-3 * k * w.prof[1], 1e-3 * k * w.prof[2],
-                    1e-3 * k * w.prof[3],
-                    w.list_hits ? 1e-2 * w.prof[5] / (double)w.list_hits : 0.0,
-                    w.list_hits ? 1e-2 * w.prof[8] / (double)w.list_hits : 0.0,
-                    w.list_hits ? 1e-2 * w.prof[9] / (double)w.list_hits : 0.0,
-                    w.list_hits ? 1e-2 * w.prof[10] / (double)w.list_hits : 0.0,
+                    1e-3 * k * w.prof[0], 1e-3 * k * w.prof[5],
+                    1e-3 * k * w.prof[8], 1e-3 * k * w.prof[9],
+                    1e-3 * k * w.prof[10], 1e-3 * k * w.prof[1],
                     1e-3 * k * w.prof[6], 1e-3 * k * w.prof[7],
+                    1e-3 * k * w.prof[2], 1e-3 * k * w.prof[3],
                     row_launches_ ? 1e3 * row_ms_ / row_launches_ : 0.0,
                     (long long)row_launches_,
                     cached_launches_ ? 1e3 * cached_ms_ / cached_launches_
                                      : 0.0,
                     (long long)cached_launches_);
-            if (atoi(e) > 1) {
-                fprintf(stderr, "[mi355svm] lists:");
-                for (int k = 0; k < 8; ++k)
-                    fprintf(stderr, " %lld", (long long)w.stat[k]);
-                fprintf(stderr, "\n");
-            }
         }
     }
     return r;
@@ -643,7 +617,6 @@ void Solver::set_state(const double* alpha_h, const double* F_h)
                            hipMemcpyHostToDevice, s));
     launch_state_from_alpha(o_.type, y_.p, alpha_.p, n_, o_.C, st_.p, s);
     HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
-    HIP_TRY(hipMemsetAsync(lcnt_.p, 0, lcnt_.bytes(), s));
     cx_.sync();
 }
 
@@ -757,7 +730,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.max_inner = max_inner;
     a.max_iter = o_.max_iter;
     a.half = half_;
-    a.group_rows = 16 * tiles_;
+    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // rows of a block
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_NO_WRITE;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
@@ -803,7 +776,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.max_inner = 0;
     a.max_iter = o_.max_iter;
     a.half = half_;
-    a.group_rows = 16 * tiles_;
+    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // rows of a block
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_SET_ALPHA;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
@@ -820,9 +793,6 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     r.xS = xS_.p;
     r.cand_key = ckey_.p;
     r.cand_idx = cidx_.p;
-    r.list_key = lkey_.p;
-    r.list_idx = lidx_.p;
-    r.list_cnt = lcnt_.p;
     r.n = n_;
     r.ldp = f_.ldp;
     r.eps = o_.eps;

@@ -169,7 +169,7 @@ private:
     SolveOptions o_;
     int64_t n_, N_;
     float gexp_;
-    int half_, nblk_cols_, tiles_, nb_, ncand_;
+    int half_, nblk_cols_, tiles_, nb_;
     DevBuf<double> F_, alpha_;
     DevBuf<uint8_t> st_;
     DevBuf<float> y_;
@@ -177,9 +177,6 @@ private:
     DevBuf<float> xS_;
     DevBuf<double> ckey_;
     DevBuf<int32_t> cidx_;
-    DevBuf<double> lkey_;   // threshold list (2 x kListCap)
-    DevBuf<int32_t> lidx_;
-    DevBuf<int32_t> lcnt_;  // 2 counters
     DevBuf<Summary> sum_;
     DevBuf<double> cvec_;
     DevBuf<int32_t> cblk_, sv_idx_;
