@@ -24,6 +24,8 @@ constexpr int kSlabStride = 68;
 // feature slabs in flight per wave of k_rows
 constexpr int kRing = 4;
 constexpr int kRowWaves = kRowThreads / 64;
+// s_waitcnt immediate (gfx9 encoding): vmcnt 0, expcnt and lgkmcnt not waited
+constexpr int kVmcnt0 = 0x0f70;
 
 // LDS row stride of a staged working-set sample: ldp rounded up to whole
 // 16-feature chunks (zero-filled) plus a pad of 4 against bank conflicts.
@@ -512,13 +514,23 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 sl_smp[tid] = smp0;
                 sl_cs[tid] = cs0;
             }
-            for (int k0 = 256; k0 < RW; k0 += 256) {
-                aux_issue(k0, ar);
-                aux_store(k0, ar);
+            // Row data past the first 256 rows and staged rows past the
+            // early loads (large tiles or many features), behind a uniform
+            // branch: their loads wait for everything in flight, the slabs
+            // included, so the common shapes do not pass through them.
+            if (RW > 256 || xs_total > kXsEarly * kRowThreads) {
+                for (int k0 = 256; k0 < RW; k0 += 256) {
+                    aux_issue(k0, ar);
+                    aux_store(k0, ar);
+                }
+                for (int e = tid + kXsEarly * kRowThreads; e < xs_total;
+                     e += kRowThreads)
+                    xs_put(e, bld_f4(rXs, xs_off(e)));
+                // nothing of these loops stays in flight (a load whose value
+                // is unused would otherwise make the slab loop wait for all
+                // loads at every slab)
+                __builtin_amdgcn_s_waitcnt(kVmcnt0);
             }
-            for (int e = tid + kXsEarly * kRowThreads; e < xs_total;
-                 e += kRowThreads)
-                xs_put(e, bld_f4(rXs, xs_off(e)));
             __syncthreads();
 
             // The slab loop; on the insert path the rows of the samples
