@@ -201,7 +201,10 @@ __device__ void top_half(double (*k)[kSurv], int32_t (*i)[kSurv], int M0,
 
 // Exact top-`half` over `count` entries produced by get(e, key, index), by
 // `half` block-wide rounds (each: the best entry after the previous winner).
-// All threads of the block take part; thread 0 writes ok/oi.
+// Up to kRoundRegs entries per thread are fetched once and kept in
+// registers; larger counts fetch in every round.  All threads of the block
+// take part; thread 0 writes ok/oi.
+constexpr int kRoundRegs = 4;
 template <class Get>
 __device__ void block_rounds(int64_t count, Get get, int half, double* ok,
                              int32_t* oi, double (*rk)[kSelThreads / 64],
@@ -209,18 +212,37 @@ __device__ void block_rounds(int64_t count, Get get, int half, double* ok,
 {
     constexpr int NW = kSelThreads / 64;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool held = count <= (int64_t)kRoundRegs * kSelThreads;
+    double hk[kRoundRegs];
+    int32_t hi[kRoundRegs];
+#pragma unroll
+    for (int j = 0; j < kRoundRegs; ++j) {
+        const int64_t e = tid + (int64_t)j * kSelThreads;
+        hk[j] = -INFINITY;
+        hi[j] = INT_MAX;
+        if (held && e < count) get(e, hk[j], hi[j]);
+    }
     double pk = INFINITY;
     int32_t pi = -1;
     for (int k = 0; k < half; ++k) {
         double bk = -INFINITY;
         int32_t bi = INT_MAX;
-        for (int64_t e = tid; e < count; e += kSelThreads) {
-            double key;
-            int32_t t;
-            get(e, key, t);
-            if (after(key, t, pk, pi) && better(key, t, bk, bi)) {
-                bk = key;
-                bi = t;
+        if (held) {
+#pragma unroll
+            for (int j = 0; j < kRoundRegs; ++j)
+                if (after(hk[j], hi[j], pk, pi) && better(hk[j], hi[j], bk, bi)) {
+                    bk = hk[j];
+                    bi = hi[j];
+                }
+        } else {
+            for (int64_t e = tid; e < count; e += kSelThreads) {
+                double key;
+                int32_t t;
+                get(e, key, t);
+                if (after(key, t, pk, pi) && better(key, t, bk, bi)) {
+                    bk = key;
+                    bi = t;
+                }
             }
         }
         wave_best_fast(bk, bi);
