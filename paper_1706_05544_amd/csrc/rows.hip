@@ -167,9 +167,14 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         cf[b] = (slot < nS && UPD) ? c : 0.0;
     }
 
-    // rows of this wave: rw0 .. rw0 + nw - 1, in Tw tiles of 16
-    const int64_t rw0 = ((int64_t)blockIdx.x * kRowWaves + wave) * RW;
-    const int nw = rw0 >= n ? 0 : (int)min((int64_t)RW, n - rw0);
+    // rows of this wave: rw0 .. rw0 + nw - 1, in Tw <= T tiles of 16 (the
+    // ceil(n / 16) tiles are shared out evenly over the grid's waves, so
+    // that no compute unit holds more of them than another)
+    const int64_t TT = (n + 15) >> 4;
+    const int64_t W = (int64_t)gridDim.x * kRowWaves;
+    const int64_t wid = (int64_t)blockIdx.x * kRowWaves + wave;
+    const int64_t rw0 = 16 * (wid * TT / W);
+    const int nw = (int)(min(16 * ((wid + 1) * TT / W), n) - rw0);
     const int Tw = (nw + 15) >> 4;
     unsigned char* aux =
         smem + rows_aux_offset(NBLK, ldp, CSR) + wave * rows_aux_bytes(T, SVR);
@@ -502,8 +507,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             AuxRegs ar;
             aux_issue(0, ar);
             float4 ring[kRing][4];
-#pragma unroll
-            for (int j = 0; j < kRing; ++j) fetch(ring[j]);
+            fetch(ring[0]);
             if (done) return;  // uniform over the block
 #pragma unroll
             for (int i = 0; i < kXsEarly; ++i)
@@ -532,6 +536,8 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 __builtin_amdgcn_s_waitcnt(kVmcnt0);
             }
             __syncthreads();
+#pragma unroll
+            for (int j = 1; j < kRing; ++j) fetch(ring[j]);
 
             // The slab loop; on the insert path the rows of the samples
             // missing from the cache also go to their new cache slots.

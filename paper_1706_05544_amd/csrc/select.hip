@@ -477,17 +477,24 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         }
         t_c2 = wall_clock64();
         // (5) row groups whose whole candidate list was taken may hold
-        // more: wave 0 finds them (lane-parallel)
+        // more: wave 0 finds them (lane-parallel).  Group b (k_rows block
+        // b) holds the tiles [b TT / nb, (b + 1) TT / nb) of the TT tiles
+        // of 16 rows; it has at most grows rows.
         const uint32_t grows = (uint32_t)a.group_rows;
+        const int64_t TT = (n + 15) >> 4, NB = a.nb;
+        auto group_of = [&](int64_t row) -> int32_t {
+            return (int32_t)((((row >> 4) + 1) * NB - 1) / TT);
+        };
+        auto group_start = [&](int64_t b) -> int64_t {
+            return 16 * (b * TT / NB);
+        };
         if (wave == 0) {
             for (int side = 0; side < 2; ++side) {
                 const double* kk = side ? lok : upk;
                 const int32_t* ii = side ? loi : upi;
                 const bool valid = lane < half && kk[lane] != -INFINITY;
                 const int32_t b =
-                    valid ? (int32_t)((uint32_t)sample_of(SVR, ii[lane], n) /
-                                      grows)
-                          : -1 - lane;
+                    valid ? group_of(sample_of(SVR, ii[lane], n)) : -1 - lane;
                 int c = 0;
                 bool first = true;
                 for (int j = 0; j < half; ++j) {
@@ -518,8 +525,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 int c = 0;
                 for (int k = 0; k < half; ++k) {
                     if (kk[k] == -INFINITY) continue;
-                    const int32_t b =
-                        (int32_t)((uint32_t)sample_of(SVR, ii[k], n) / grows);
+                    const int32_t b = group_of(sample_of(SVR, ii[k], n));
                     bool ex = false;
                     for (int x = 0; x < ne; ++x) ex |= exb[side][x] == b;
                     if (!ex) {
@@ -539,10 +545,11 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                                  int32_t& t) {
                 const uint32_t x = (uint32_t)(q / per),
                                o = (uint32_t)(q - (int64_t)x * per);
-                const int64_t row = (int64_t)exb[side][x] * grows + (o % grows);
+                const int64_t b = exb[side][x];
+                const int64_t row = group_start(b) + (o % grows);
                 key = -INFINITY;
                 t = INT_MAX;
-                if (row < n) {
+                if (row < min(n, group_start(b + 1))) {
                     const int64_t tt = o < grows ? row : n + row;
                     double u, l;
                     var_scores<SVR>(a, tt, u, l);

@@ -178,8 +178,9 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     gexp_ = (float)(o.gamma * 1.4426950408889634);
     half_ = o.q / 2;
     nblk_cols_ = o.q <= 16 ? 1 : (o.q <= 32 ? 2 : 4);
-    // Grid: every wave of k_rows resident at once (occupancy from the
-    // runtime), each wave owning `tiles_` consecutive 16-row tiles.
+    // Grid: every block of k_rows resident at once (occupancy from the
+    // runtime); the 16-row tiles are shared out evenly over the waves, at
+    // most `tiles_` per wave.
     constexpr int kWaves = kRowThreads / 64;
     const bool svr = o.type == SVM_EPS_SVR;
     constexpr size_t kLdsMax = 160 * 1024;
@@ -197,26 +198,30 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     // and the resident blocks shrink with the LDS: iterate to a fixed point
     // (tiles only grow, so this ends).
     tiles_ = 1;
+    int64_t cap_blocks = 1;
     for (int it = 0; it < 8; ++it) {
         const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr);
-        const int64_t cap =
-            (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds, f.csr) * kWaves;
+        cap_blocks = (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds, f.csr);
+        const int64_t cap = cap_blocks * kWaves;
         const int t = (int)std::max<int64_t>(1, (tiles_total + cap - 1) / cap);
         if (t <= tiles_) break;
         tiles_ = t;
     }
-    if (const char* e = getenv("SVM_TILES"))  // tuning override
-        tiles_ = std::max(1, std::min(4096, atoi(e)));
-    // one candidate record per block; the selection holds at most
-    // kSelRecords of them per thread
+    // as many blocks as are resident (fewer when there are fewer tiles);
+    // one candidate record per block, at most kSelRecords per select thread
     const int64_t rec_cap = (int64_t)kSelThreads * kSelRecords;
-    while ((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_) > rec_cap)
-        ++tiles_;
+    int64_t nb = std::min(cap_blocks, (tiles_total + kWaves - 1) / kWaves);
+    if (const char* e = getenv("SVM_TILES")) {  // tuning override
+        tiles_ = std::max(1, std::min(4096, atoi(e)));
+        nb = (tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_);
+    }
+    nb = std::max<int64_t>(1, std::min(nb, rec_cap));
+    tiles_ = (int)((tiles_total + kWaves * nb - 1) / (kWaves * nb));
     if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr) > kLdsMax ||
         (int64_t)16 * tiles_ * f.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED,
                     "training set too large for the dense row kernel"};
-    nb_ = (int)((tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_));
+    nb_ = (int)nb;
 
     F_.alloc((size_t)n_);
     alpha_.alloc((size_t)N_);
@@ -342,7 +347,7 @@ void Solver::launch_solve(int32_t mode)
     a.max_inner = o_.max_inner;
     a.max_iter = o_.max_iter;
     a.mode = mode;
-    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // rows of a block
+    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // most rows of a block
     if (cache_) {
         a.cache = cache_->rows.p;
         a.ldc = cache_->ldc;
@@ -730,7 +735,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.max_inner = max_inner;
     a.max_iter = o_.max_iter;
     a.half = half_;
-    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // rows of a block
+    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // most rows of a block
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_NO_WRITE;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
@@ -776,7 +781,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.max_inner = 0;
     a.max_iter = o_.max_iter;
     a.half = half_;
-    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // rows of a block
+    a.group_rows = (kRowThreads / 64) * 16 * tiles_;  // most rows of a block
     a.mode = SS_GIVEN_B | SS_SOLVE | SS_SET_ALPHA;
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
