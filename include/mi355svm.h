@@ -94,7 +94,7 @@ typedef struct {
     void *stream;          /* hipStream_t; NULL: a stream of the library */
     int32_t check_every;   /* outer iterations between host polls (0: 64) */
     double inner_ratio;    /* subproblem stops at local gap <= max(ratio *
-                              global gap, tol/2); 0: 0.1 */
+                              global gap, tol/2); 0: 0.3 */
     int32_t max_inner;     /* subproblem step cap; 0: 8 q */
     int32_t profile;       /* 1: time the row/update kernel with events */
 } svm_params;

@@ -130,7 +130,7 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
     // (the per-iteration path history covers kPathLog iterations)
     o.check_every = p->check_every > 0 ? std::min(p->check_every, kPathLog)
                                        : 64;
-    o.inner_ratio = p->inner_ratio > 0 ? p->inner_ratio : 0.1;
+    o.inner_ratio = p->inner_ratio > 0 ? p->inner_ratio : 0.3;
     o.max_inner = p->max_inner > 0 ? p->max_inner : 8 * p->working_set;
     o.profile = p->profile != 0;
     return o;
