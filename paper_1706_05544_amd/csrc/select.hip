@@ -328,6 +328,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     __shared__ double rk[2][NW];
     __shared__ int32_t ri[2][NW];
     __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
+    __shared__ int32_t shCandPos[kMaxQ], shSlotCand[kMaxQ];
+    __shared__ float shSqCand[kMaxQ];  // squared norm of each candidate
     __shared__ int32_t shPos[kMaxQ];  // position in B of the i-th smallest
     __shared__ float shsS[kMaxQ];
     __shared__ float KSS[QS][QS + 1];
@@ -387,6 +389,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         for (int k = 0; k < 12; ++k) c_prof[k] = ws->prof[k];
     }
     if (tid == 0) shDone = 0;
+    // (7) prefetch (dense input): waves 1.. stage the first feature slice
+    // of the winners' rows in LDS, row c for candidate c, and their norms,
+    // while wave 0 builds the working set
+    constexpr int PT = kSelThreads - 64;  // prefetching threads
+    bool pf = false;  // uniform: the winners' first slice is staged
+    const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
+    const int pq4 = min(a.slice, ldp16) >> 2;  // float4 per row of the slice
 
     if (!given) {
         if (tid < kMaxHalf) {
@@ -599,6 +608,42 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     }
     const uint64_t t_merge = wall_clock64();
 
+    // candidate c: up winner c (c < half) or low winner c - half
+    pf = !given && !a.rp && (a.mode & SS_SOLVE) && 2 * half * pq4 <= 4 * PT;
+    if (pf && wave != 0) {
+        const int pwst = a.slice + 4;
+        float4 xv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = tid - 64 + j * PT;
+            const bool in = e < 2 * half * pq4;
+            const int c = in ? e / pq4 : 0;
+            const int c4 = e - c * pq4;
+            const double key = c < half ? upk[c] : lok[c - half];
+            const int32_t idx = c < half ? upi[c] : loi[c - half];
+            const bool ok = in && key != -INFINITY && 4 * c4 < ldp;
+            // unconditional loads (an address inside X when unused)
+            xv[j] = ld4(a.X + (ok ? sample_of(SVR, idx, n) * ldp + 4 * c4 : 0));
+            if (!ok) xv[j] = zero4();
+        }
+        float q = 0.0f;
+        const int cq = tid - 64;
+        if (cq < 2 * half) {
+            const int32_t idx = cq < half ? upi[cq] : loi[cq - half];
+            const bool ok = (cq < half ? upk[cq] : lok[cq - half]) != -INFINITY;
+            q = a.sq[ok ? sample_of(SVR, idx, n) : 0];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = tid - 64 + j * PT;
+            if (e < 2 * half * pq4) {
+                const int c = e / pq4, c4 = e - c * pq4;
+                *reinterpret_cast<float4*>(xst + c * pwst + 4 * c4) = xv[j];
+            }
+        }
+        if (cq < 2 * half) shSqCand[cq] = q;
+    }
+
     // (8) working set, distinct samples (wave 0, lane-parallel)
     if (wave == 0) {
         int go = 0, nB = 0;
@@ -648,6 +693,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 if (!isU) pos += (int)((mu >> k) & 1ull);
                 int32_t* dst = (a.mode & SS_SOLVE) ? shB : ws->B;
                 if (keep) dst[pos] = idx;
+                if (lane < 2 * half) shCandPos[lane] = keep ? pos : -1;
                 nB = __popcll(m);
                 if (a.mode & SS_SOLVE) go = 1;
                 else if (lane == 0) ws->nB = nB;
@@ -687,6 +733,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 shPos[p] = lane;
             }
             nS = __popcll(fm);
+            __builtin_amdgcn_wave_barrier();
+            if (!given && lane < 2 * half) {
+                // a candidate of each slot (twins of one sample: either)
+                const int cp = shCandPos[lane];
+                if (cp >= 0) shSlotCand[shSlot[cp]] = lane;
+            }
         }
         if (lane == 0) {
             shGo = go;
@@ -803,7 +855,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         const bool va = mw && sa < nS, vb = mw && sb < nS;
         float sqa[4] = {0.f, 0.f, 0.f, 0.f};
         float sqb = 0.f;
-        if (mw) {
+        if (mw && !pf) {
 #pragma unroll
             for (int vv = 0; vv < 4; ++vv) {
                 const int ia = bi * 16 + 4 * g + vv;
@@ -811,7 +863,6 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             }
             sqb = a.sq[vb ? shS[sb] : 0];
         }
-        const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
         const int W = a.slice, wst = W + 4;
         // copy waves: those without a K_SS block, or all of them.  With a
         // single slice the copy waits until after the last barrier (waves
@@ -822,7 +873,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         t_stage = wall_clock64();
         for (int c0 = 0; c0 < ldp16; c0 += W) {
             const int wc = min(W, ldp16 - c0), q4 = wc >> 2, tot = nS * q4;
-            for (int e0 = tid; e0 < tot; e0 += 4 * kSelThreads) {
+            // the first slice is staged already when prefetched (LDS row
+            // of a slot: that of a candidate of it)
+            const bool bycand = c0 == 0 && pf;
+            for (int e0 = tid; e0 < tot && !bycand; e0 += 4 * kSelThreads) {
                 float4 xv[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -847,11 +901,23 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 }
             }
             __syncthreads();
-            if (c0 == 0) t_stage = wall_clock64();
+            if (c0 == 0) {
+                t_stage = wall_clock64();
+                if (mw && pf) {
+#pragma unroll
+                    for (int vv = 0; vv < 4; ++vv) {
+                        const int ia = bi * 16 + 4 * g + vv;
+                        sqa[vv] = shSqCand[shSlotCand[ia < nS ? ia : 0]];
+                    }
+                    sqb = shSqCand[shSlotCand[vb ? sb : 0]];
+                }
+            }
             if (mw) {
+                const int ra = bycand ? shSlotCand[va ? sa : 0] : sa;
+                const int rb = bycand ? shSlotCand[vb ? sb : 0] : sb;
                 for (int cc = 0; cc < wc; cc += 16) {
-                    float4 av = ld4(xst + sa * wst + cc + 4 * g);
-                    float4 bv = ld4(xst + sb * wst + cc + 4 * g);
+                    float4 av = ld4(xst + ra * wst + cc + 4 * g);
+                    float4 bv = ld4(xst + rb * wst + cc + 4 * g);
                     if (!va) av = zero4();
                     if (!vb) bv = zero4();
                     acc = mfma_chunk(acc, av, bv);
@@ -866,7 +932,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                         if (col < ldp)
                             *reinterpret_cast<float4*>(
                                 a.xS + (int64_t)slot * ldp + col) =
-                                ld4(xst + slot * wst + 4 * c4);
+                                ld4(xst +
+                                    (bycand ? shSlotCand[slot] : slot) * wst +
+                                    4 * c4);
                     }
                 }
                 __syncthreads();
@@ -952,7 +1020,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 if (col < ldp)
                     *reinterpret_cast<float4*>(a.xS + (int64_t)slot * ldp +
                                                col) =
-                        ld4(xst + slot * wst + 4 * c4);
+                        ld4(xst + (pf ? shSlotCand[slot] : slot) * wst + 4 * c4);
             }
         }
         return;
