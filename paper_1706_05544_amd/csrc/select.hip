@@ -491,31 +491,39 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         // of 16 rows; it has at most grows rows.
         const uint32_t grows = (uint32_t)a.group_rows;
         const int64_t TT = (n + 15) >> 4, NB = a.nb;
+        // group of a row: floor(((row / 16 + 1) NB - 1) / TT), through an
+        // fp64 quotient corrected to the exact integer
         auto group_of = [&](int64_t row) -> int32_t {
-            return (int32_t)((((row >> 4) + 1) * NB - 1) / TT);
+            const int64_t x = ((row >> 4) + 1) * NB - 1;
+            int64_t g = (int64_t)((double)x / (double)TT);
+            if (g * TT > x) --g;
+            else if ((g + 1) * TT <= x) ++g;
+            return (int32_t)g;
         };
         auto group_start = [&](int64_t b) -> int64_t {
             return 16 * (b * TT / NB);
         };
         if (wave == 0) {
-            for (int side = 0; side < 2; ++side) {
-                const double* kk = side ? lok : upk;
-                const int32_t* ii = side ? loi : upi;
-                const bool valid = lane < half && kk[lane] != -INFINITY;
-                const int32_t b =
-                    valid ? group_of(sample_of(SVR, ii[lane], n)) : -1 - lane;
-                int c = 0;
-                bool first = true;
-                for (int j = 0; j < half; ++j) {
-                    const int32_t bj = rl_i32(b, j);
-                    c += bj == b;
-                    first &= !(j < lane && bj == b);
-                }
-                const bool ex = valid && c >= kBlockTop && first;
-                const unsigned long long m = __ballot(ex);
-                if (ex) exb[side][lanes_below(m)] = b;
-                if (lane == 0) nex[side] = __popcll(m);
+            // lanes [0, 32): the up winners, [32, 64): the low winners
+            const int side = lane >> 5, k = lane & 31;
+            const double* kk = side ? lok : upk;
+            const int32_t* ii = side ? loi : upi;
+            const bool valid = k < half && kk[k] != -INFINITY;
+            const int32_t b =
+                valid ? group_of(sample_of(SVR, ii[k], n)) : -1 - lane;
+            int c = 0;
+            bool first = true;
+            for (int j = 0; j < half; ++j) {
+                const int32_t bu = rl_i32(b, j), bl = rl_i32(b, 32 + j);
+                const int32_t bj = side ? bl : bu;
+                c += bj == b;
+                first &= !(j < k && bj == b);
             }
+            const bool ex = valid && c >= kBlockTop && first;
+            const unsigned long long m = __ballot(ex);
+            const unsigned long long ms = side ? (m >> 32) : (m & 0xffffffffull);
+            if (ex) exb[side][__popcll(ms & ((1ull << k) - 1ull))] = b;
+            if (k == 0) nex[side] = __popcll(ms);
         }
         __syncthreads();
         t_c3 = wall_clock64();
