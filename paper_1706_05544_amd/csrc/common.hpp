@@ -112,6 +112,12 @@ struct RowArgs {
     const float* z;
     const WorkingSet* ws;
     const float* xS;      // kMaxQ x ldp rows of the working-set samples
+    // CSR: the working set by column (written by the selection): the column
+    // of each of csr_cols compact rows (-1: unused), and the rows
+    // (csr_cols + 1 of 16 * nblk_cols floats; unused rows and the last are 0)
+    const int32_t* xsc_cols;
+    const float* xsc;
+    int32_t csr_cols;
     double* cand_key;     // [blocks][2][kBlockTop]: up scores v, low -v
     int32_t* cand_idx;
     float* rows_out;      // nS x n (tests)
@@ -141,6 +147,9 @@ struct SelArgs {
     const float* cv;
     const float* sq;
     float* xS;
+    int32_t* xsc_cols;    // CSR: the working set by column (see RowArgs)
+    float* xsc;
+    int32_t csr_cols;
     int64_t n, ldp;
     double C, eps, tol;
     float gexp;
@@ -192,8 +201,9 @@ void launch_check_finite(const float* v, int64_t n, int32_t* bad_flag,
 void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
                  hipStream_t s, hipEvent_t e0 = nullptr,
                  hipEvent_t e1 = nullptr);
+// csr_cols < 0: dense features; else the compact working-set columns (CSR)
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
-                      bool csr);
+                      int csr_cols);
 int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
 void launch_state_from_alpha(int32_t type, const float* y, const double* a,
@@ -214,6 +224,9 @@ void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
                         const int32_t* idx, int64_t k, float* out,
                         float* sq_out, hipStream_t s);
 void launch_predict(const PredictArgs& a, hipStream_t s);
+void launch_csr_compact(const float* xS, int32_t nS, int64_t ldp,
+                        int32_t qs, int32_t csr_cols, int32_t* xsc_cols,
+                        float* xsc, hipStream_t s);
 void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,
                             const float* cv, int64_t n, int64_t d,
                             int64_t nnz, float* sq, int32_t* bad,

@@ -184,6 +184,43 @@ __device__ __forceinline__ void wave_best_pair(double& k0, int32_t& i0,
     i1 = c1;
 }
 
+// The working set by column (CSR input): every column c in [0, ldp) where
+// some of the nS slots holds a nonzero gets one compact row e (in no
+// particular order): cols[e] = c, vals[e * qs + s] = x_s[c] (0 for slots
+// past nS).  The rows after the last used one, up to csr_cols, are zero
+// with cols = -1 (row csr_cols included).  csr_cols bounds the columns used
+// (at most qs times the longest row, and ldp).  val(s, c) reads the dense
+// working-set rows.  Run by the whole block; cnt is a zeroed LDS counter.
+template <class Val>
+__device__ void compact_by_column(Val val, int nS, int64_t ldp, int qs,
+                                  int csr_cols, int32_t* cols, float* vals,
+                                  int* cnt)
+{
+    for (int64_t c = threadIdx.x; c < ldp; c += blockDim.x) {
+        bool any = false;
+        for (int s = 0; s < nS; ++s) any |= val(s, c) != 0.0f;
+        if (any) {
+            const int e = atomicAdd(cnt, 1);
+            if (e < csr_cols) {
+                cols[e] = (int32_t)c;
+                for (int s = 0; s < qs; s += 4)
+                    *reinterpret_cast<float4*>(vals + (int64_t)e * qs + s) =
+                        make_float4(s + 0 < nS ? val(s + 0, c) : 0.0f,
+                                    s + 1 < nS ? val(s + 1, c) : 0.0f,
+                                    s + 2 < nS ? val(s + 2, c) : 0.0f,
+                                    s + 3 < nS ? val(s + 3, c) : 0.0f);
+            }
+        }
+    }
+    __syncthreads();
+    const int E = min(*cnt, csr_cols);
+    for (int64_t k = (int64_t)E * qs + threadIdx.x;
+         k < (int64_t)(csr_cols + 1) * qs; k += blockDim.x)
+        vals[k] = 0.0f;
+    for (int e = E + (int)threadIdx.x; e < csr_cols; e += (int)blockDim.x)
+        cols[e] = -1;
+}
+
 // number of set bits of m below this lane
 __device__ __forceinline__ int lanes_below(unsigned long long m)
 {

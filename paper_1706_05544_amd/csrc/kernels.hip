@@ -378,6 +378,7 @@ void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
 // Checks the CSR structure of row i and computes its squared norm (fp64
 // sum, rounded once).  bad |= 1: a value not finite (or a norm past fp32),
 // 2: row pointers, 4: column indices out of range, unsorted or repeated.
+// bad[0]: flags (1 value, 2 pointers, 4 columns); bad[1]: the longest row
 __global__ void k_csr_check_norms(const int64_t* rp, const int32_t* ci,
                                   const float* cv, int64_t n, int64_t d,
                                   int64_t nnz, float* sq, int32_t* bad)
@@ -405,6 +406,30 @@ __global__ void k_csr_check_norms(const int64_t* rp, const int32_t* ci,
     if (!isfinite(f)) flags |= 1;
     sq[i] = f;
     if (flags) atomicOr(bad, flags);
+    if (!(flags & 2) && p1 > p0)
+        atomicMax(bad + 1, (int32_t)min(p1 - p0, (int64_t)INT32_MAX));
+}
+
+// The working set by column from its dense rows xS (nS rows of ldp floats):
+// see compact_by_column.  One block.
+__global__ __launch_bounds__(1024) void k_csr_compact(
+    const float* xS, int32_t nS, int64_t ldp, int32_t qs, int32_t csr_cols,
+    int32_t* xsc_cols, float* xsc)
+{
+    __shared__ int cnt;
+    if (threadIdx.x == 0) cnt = 0;
+    __syncthreads();
+    compact_by_column(
+        [&](int s, int64_t c) { return xS[(int64_t)s * ldp + c]; }, nS, ldp,
+        qs, csr_cols, xsc_cols, xsc, &cnt);
+}
+
+void launch_csr_compact(const float* xS, int32_t nS, int64_t ldp,
+                        int32_t qs, int32_t csr_cols, int32_t* xsc_cols,
+                        float* xsc, hipStream_t s)
+{
+    k_csr_compact<<<1, 1024, 0, s>>>(xS, nS, ldp, qs, csr_cols, xsc_cols,
+                                     xsc);
 }
 
 void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,

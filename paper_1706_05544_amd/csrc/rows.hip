@@ -48,13 +48,26 @@ __host__ __device__ inline int rows_wave_buf(int nblk_cols, bool csr)
     return csr ? 64 * (16 * nblk_cols + 1) : 16 * kSlabStride;
 }
 
-// The staged working-set rows take nblk_cols * 16 rows of rows_xs_stride
-// floats (dense), or the same samples feature-major (CSR, no more room).
-__host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp,
-                                                  bool csr)
+// Staged working set.  Dense: nblk_cols * 16 rows of rows_xs_stride floats.
+// CSR (csr_cols >= 0): a column map (ldp int32: the compact row of a column
+// used by the working set, or -1), then csr_cols + 1 compact rows of
+// nblk_cols * 16 floats (the samples' values at one column; the last row is
+// zero, for the columns the working set does not use).
+__host__ __device__ inline size_t rows_stage_bytes(int nblk_cols, int64_t ldp,
+                                                   int csr_cols)
 {
-    return (size_t)nblk_cols * 16 * rows_xs_stride(ldp) * sizeof(float) +
-           (size_t)kRowWaves * rows_wave_buf(nblk_cols, csr) * sizeof(float);
+    if (csr_cols < 0)
+        return (size_t)nblk_cols * 16 * rows_xs_stride(ldp) * sizeof(float);
+    return (((size_t)ldp * 4 + 15) & ~(size_t)15) +
+           (size_t)(csr_cols + 1) * nblk_cols * 16 * sizeof(float);
+}
+
+__host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp,
+                                                  int csr_cols)
+{
+    return rows_stage_bytes(nblk_cols, ldp, csr_cols) +
+           (size_t)kRowWaves * rows_wave_buf(nblk_cols, csr_cols >= 0) *
+               sizeof(float);
 }
 
 // per-block table of the waves' candidate records (see k_rows)
@@ -64,9 +77,9 @@ constexpr int kBlockRecBytes = kRowWaves * 4 * (8 + 4);
 constexpr int kSlotInfoBytes = kMaxQ * (4 + 4 + 4);
 
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
-                      bool csr)
+                      int csr_cols)
 {
-    return rows_aux_offset(nblk_cols, ldp, csr) +
+    return rows_aux_offset(nblk_cols, ldp, csr_cols) +
            (size_t)kRowWaves * rows_aux_bytes(tiles, svr) + kBlockRecBytes +
            kSlotInfoBytes;
 }
@@ -177,17 +190,17 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     const int nw = (int)(min(16 * ((wid + 1) * TT / W), n) - rw0);
     const int Tw = (nw + 15) >> 4;
     unsigned char* aux =
-        smem + rows_aux_offset(NBLK, ldp, CSR) + wave * rows_aux_bytes(T, SVR);
+        smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) + wave * rows_aux_bytes(T, SVR);
     double* Fw = reinterpret_cast<double*>(aux);
     float* sqw = reinterpret_cast<float*>(aux + 8 * RW);
     float* zw = reinterpret_cast<float*>(aux + 12 * RW);
     uint8_t* stw = aux + (SVR ? 16 : 12) * RW;  // copy (i,-) at stw[RW + r]
-    unsigned char* brec = smem + rows_aux_offset(NBLK, ldp, CSR) +
+    unsigned char* brec = smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) +
                           kRowWaves * rows_aux_bytes(T, SVR);
     double* brk = reinterpret_cast<double*>(brec);  // [kRowWaves][4]
     int32_t* bri = reinterpret_cast<int32_t*>(brec + kRowWaves * 32);
     // slot table (block-wide): norm, sample and cache slot of every slot
-    unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp, CSR) +
+    unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) +
                            kRowWaves * rows_aux_bytes(T, SVR) + kBlockRecBytes;
     float* sl_sq = reinterpret_cast<float*>(sinfo);
     int32_t* sl_smp = reinterpret_cast<int32_t*>(sinfo + 4 * kMaxQ);
@@ -336,16 +349,24 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 }
             }
         } else if (CSR) {
-            // CSR rows.  The working-set samples sit feature-major in LDS
-            // (xsT[j * QS + s] = x_s[j]); one lane per row walks the row's
-            // nonzeros in column order and, per nonzero, gathers the QS
-            // samples' values: K(x_i, x_s) sums the products of the common
-            // nonzeros in increasing column order (every CSR kernel of the
-            // library sums them so).  The K values of 64 rows go through a
-            // wave buffer into the 16-row tile layout of the epilogue.
+            // CSR rows.  The working set sits by column in LDS: colmap[j] is
+            // the compact row of column j (-1: no sample has it), xsT[e * QS
+            // + s] = x_s[cols[e]], and row CC is zero.  One lane per row
+            // walks the row's nonzeros in column order and, per nonzero,
+            // reads the QS samples' values of its column: K(x_i, x_s) sums
+            // the products of the common nonzeros in increasing column order
+            // (every CSR kernel of the library sums them so; the products
+            // with a zero add nothing, exactly).  The K values of 64 rows go
+            // through a wave buffer into the 16-row tile layout of the
+            // epilogue.
             constexpr int QS = NBLK * 16, QP = QS + 1;
-            float* xsT = xsl;
-            float* tb = xsl + NBLK * 16 * xstride + wave * rows_wave_buf(NBLK, true);
+            const int CC = a.csr_cols;
+            int32_t* colmap = reinterpret_cast<int32_t*>(smem);
+            float* xsT =
+                reinterpret_cast<float*>(smem + ((ldp * 4 + 15) & ~15));
+            float* tb = reinterpret_cast<float*>(
+                            smem + rows_stage_bytes(NBLK, ldp, CC)) +
+                        wave * rows_wave_buf(NBLK, true);
             float sq0 = 0.0f;
             int32_t smp0 = -1, cs0 = -1;
             if (tid < NBLK * 16) {
@@ -358,35 +379,77 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             AuxRegs ar;
             aux_issue(0, ar);
             if (done) return;  // uniform over the block
+            for (int e = tid; e < ldp; e += kRowThreads) colmap[e] = -1;
             aux_store(0, ar);
             if (tid < NBLK * 16) {
                 sl_sq[tid] = sq0;
                 sl_smp[tid] = smp0;
                 sl_cs[tid] = cs0;
             }
-            for (int k0 = 256; k0 < RW; k0 += 256) {
-                aux_issue(k0, ar);
-                aux_store(k0, ar);
+            if (RW > 256) {
+                for (int k0 = 256; k0 < RW; k0 += 256) {
+                    aux_issue(k0, ar);
+                    aux_store(k0, ar);
+                }
             }
-            const int q4 = ldp >> 2;
-            for (int e = tid; e < QS * q4; e += kRowThreads) {
-                const int slot = e % QS, c4 = e / QS;
-                float4 v = ld4(a.xS + (int64_t)slot * ldp + 4 * c4);
-                if (slot >= nS) v = zero4();
-                xsT[(4 * c4 + 0) * QS + slot] = v.x;
-                xsT[(4 * c4 + 1) * QS + slot] = v.y;
-                xsT[(4 * c4 + 2) * QS + slot] = v.z;
-                xsT[(4 * c4 + 3) * QS + slot] = v.w;
+            __syncthreads();  // column map cleared
+            // the compact columns and rows, 8 loads in flight per thread
+            constexpr int XB = 8;
+            for (int e0 = tid; e0 < CC; e0 += XB * kRowThreads) {
+                int32_t c[XB];
+#pragma unroll
+                for (int j = 0; j < XB; ++j)
+                    c[j] = a.xsc_cols[min(e0 + j * kRowThreads, CC - 1)];
+#pragma unroll
+                for (int j = 0; j < XB; ++j)
+                    if (e0 + j * kRowThreads < CC && c[j] >= 0)
+                        colmap[c[j]] = e0 + j * kRowThreads;
             }
+            const int n4 = (CC + 1) * QS / 4;
+            for (int e0 = tid; e0 < n4; e0 += XB * kRowThreads) {
+                float4 v[XB];
+#pragma unroll
+                for (int j = 0; j < XB; ++j)
+                    v[j] = ld4(a.xsc + 4 * min(e0 + j * kRowThreads, n4 - 1));
+#pragma unroll
+                for (int j = 0; j < XB; ++j)
+                    if (e0 + j * kRowThreads < n4)
+                        *reinterpret_cast<float4*>(
+                            xsT + 4 * (e0 + j * kRowThreads)) = v[j];
+            }
+            // nothing stays in flight (a load whose value is unused would
+            // make the row loop wait for all loads at every batch)
+            __builtin_amdgcn_s_waitcnt(kVmcnt0);
             __syncthreads();
 
             const bool INS = HOT && path == PATH_INSERT;
             constexpr int KB = 8;  // nonzeros loaded per batch
+            // row pointers of the next 64 rows requested one group ahead,
+            // and each batch of nonzeros while the previous one is summed
+            auto row_ptrs = [&](int p0, int64_t& k0, int64_t& k1) {
+                const int r = 16 * p0 + lane;
+                const int64_t gr = r < nw ? rw0 + r : 0;
+                k0 = a.rp[gr];
+                k1 = a.rp[gr + 1];
+            };
+            auto batch = [&](int kb, int nz, int64_t k0, int32_t (&cc)[KB],
+                             float (&vv)[KB]) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j) {
+                    // unconditional loads (a valid entry when unused)
+                    const bool ok = kb + j < nz;
+                    const int64_t pos = ok ? k0 + kb + j : 0;
+                    cc[j] = a.ci[pos];
+                    vv[j] = a.cv[pos];
+                }
+            };
+            int64_t nk0, nk1;
+            row_ptrs(0, nk0, nk1);
             for (int p0 = 0; p0 < Tw; p0 += 4) {
                 const int r = 16 * p0 + lane;  // this lane's row (local)
                 const bool rv = r < nw;
-                const int64_t gr = rv ? rw0 + r : 0;
-                const int64_t k0 = a.rp[gr], k1 = a.rp[gr + 1];
+                const int64_t k0 = nk0, k1 = nk1;
+                row_ptrs(p0 + 4, nk0, nk1);
                 const int nz = rv ? (int)(k1 - k0) : 0;
                 int mx = nz;
 #pragma unroll
@@ -395,22 +458,23 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 float acc[QS];
 #pragma unroll
                 for (int q = 0; q < QS; ++q) acc[q] = 0.0f;
+                int32_t ncc[KB];
+                float nvv[KB];
+                batch(0, nz, k0, ncc, nvv);
                 for (int kb = 0; kb < mx; kb += KB) {
                     int32_t cc[KB];
                     float vv[KB];
 #pragma unroll
                     for (int j = 0; j < KB; ++j) {
-                        // unconditional loads (a valid entry when unused)
                         const bool ok = kb + j < nz;
-                        const int64_t pos = ok ? k0 + kb + j : 0;
-                        const int32_t c = a.ci[pos];
-                        const float v = a.cv[pos];
-                        cc[j] = ok ? c : 0;
-                        vv[j] = ok ? v : 0.0f;
+                        cc[j] = ok ? ncc[j] : 0;
+                        vv[j] = ok ? nvv[j] : 0.0f;
                     }
+                    batch(kb + KB, nz, k0, ncc, nvv);
 #pragma unroll
                     for (int j = 0; j < KB; ++j) {
-                        const float* xr = xsT + cc[j] * QS;
+                        const int m = colmap[cc[j]];
+                        const float* xr = xsT + (m >= 0 ? m : CC) * QS;
 #pragma unroll
                         for (int q = 0; q < QS; q += 4) {
                             const float4 x = ld4(xr + q);
@@ -661,7 +725,8 @@ template <bool SVR, int NBLK, int MODE, bool CSR>
 static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
                           hipEvent_t e0, hipEvent_t e1)
 {
-    const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR, CSR);
+    const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR,
+                                      CSR ? a.csr_cols : -1);
     static size_t lds_allowed = 64 * 1024;
     if (lds > lds_allowed) {
         hipError_t e = hipFuncSetAttribute(

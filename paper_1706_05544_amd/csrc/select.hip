@@ -298,6 +298,49 @@ int select_slice(int nblk_cols, int64_t ldp)
     return (int)std::max<int64_t>(16, w);
 }
 
+// Dynamic LDS of the CSR working set in the selection: the column index
+// (ldp int32) and the by-column table ((csr_cols + 1) rows of 16 * nblk_cols
+// floats).
+static size_t select_csr_lds_bytes(int nblk_cols, int64_t ldp, int csr_cols)
+{
+    return (size_t)((ldp + 3) & ~(int64_t)3) * 4 +
+           (size_t)(csr_cols + 1) * nblk_cols * 16 * 4;
+}
+
+// In-place exclusive prefix sum of v[0..L) (non-negative ints) by the whole
+// block; returns the total.  Thread t sums a contiguous chunk.
+__device__ int block_exclusive_scan(int* v, int64_t L, int* wsum)
+{
+    constexpr int NW = kSelThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t K = (L + kSelThreads - 1) / kSelThreads;
+    const int64_t b0 = min((int64_t)tid * K, L), b1 = min(b0 + K, L);
+    int loc = 0;
+    for (int64_t i = b0; i < b1; ++i) loc += v[i];
+    int inc = loc;  // inclusive over the wave
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(inc, o);
+        if (lane >= o) inc += u;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < NW; ++w) {
+        const int x = wsum[w];
+        off += w < wave ? x : 0;
+        tot += x;
+    }
+    int run = off + inc - loc;
+    for (int64_t i = b0; i < b1; ++i) {
+        const int x = v[i];
+        v[i] = run;
+        run += x;
+    }
+    __syncthreads();
+    return tot;
+}
+
 static size_t select_lds_bytes(int nblk_cols, int slice)
 {
     return (size_t)nblk_cols * 16 * (slice + 4) * sizeof(float);
@@ -330,6 +373,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
     __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
     __shared__ int32_t shCandPos[kMaxQ], shSlotCand[kMaxQ];
     __shared__ float shSqCand[kMaxQ];  // squared norm of each candidate
+    __shared__ int shCnt;
     __shared__ int32_t shPos[kMaxQ];  // position in B of the i-th smallest
     __shared__ float shsS[kMaxQ];
     __shared__ float KSS[QS][QS + 1];
@@ -820,38 +864,102 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         c_filled = ws->cache_filled;
     }
 
-    // (10) K_SS.  CSR input: every wave scatters one working-set row into
-    // a dense LDS row, and K_SS sums the products over the nonzeros of the
-    // first sample in column order (the row kernel's order, so the values
-    // are the same bits).  Dense input: on the matrix cores (same operand
+    // (10) K_SS.  CSR input: the working set by column (below).  Dense input: on the matrix cores (same operand
     // order as k_rows): the working-set rows pass through LDS in feature
     // slices: every thread loads a piece into LDS; then the NBLK^2
     // matrix-core waves accumulate the slice while the other waves copy it
     // to xS (the rows of the next k_rows).
     if (a.rp) {
-        const int wst = a.slice + 4;  // one slice holds a whole row (host)
-        for (int e = tid; e < nS * wst; e += kSelThreads) xst[e] = 0.0f;
-        __syncthreads();
-        for (int slot = wave; slot < nS; slot += NW) {
-            const int64_t smp = shS[slot];
-            const int64_t p0 = a.rp[smp], p1 = a.rp[smp + 1];
-            for (int64_t q = p0 + lane; q < p1; q += 64)
-                xst[slot * wst + a.ci[q]] = a.cv[q];
+        // CSR: the working set by column.  cidx[c] flags, then numbers in
+        // increasing column order, the columns some sample holds; tab[e *
+        // QS + s] = x_s[column e].  K_SS sums over the columns in that
+        // order, the products that involve a zero adding nothing: these
+        // are the row kernel's sums over the nonzeros of sample ia, bit for
+        // bit.  The table (padded with zero rows to csr_cols + 1) also goes
+        // to the row kernel.
+        int* cidx = reinterpret_cast<int*>(xst);
+        float* tab = xst + ((ldp + 3) & ~(int64_t)3);
+        const int CC = a.csr_cols;
+        for (int64_t c = tid; c < ldp; c += kSelThreads) cidx[c] = 0;
+        for (int64_t e = tid; e < (int64_t)(CC + 1) * QS; e += kSelThreads)
+            tab[e] = 0.0f;
+        // sample rows: a wave per slot (two at most: nS <= 32), the first
+        // 256 nonzeros of a row held in registers from one load round,
+        // the rest of a longer row loaded again where needed
+        static_assert(NW * 2 >= 32, "two CSR slots per wave");
+        int32_t hc[2][4];
+        float hv[2][4];
+        int64_t hp0[2], hp1[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int slot = wave + k * NW;
+            const int64_t smp = slot < nS ? shS[slot] : 0;
+            hp0[k] = a.rp[smp];
+            hp1[k] = slot < nS ? a.rp[smp + 1] : hp0[k];
         }
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t q = hp0[k] + lane + 64 * j;
+                hc[k][j] = q < hp1[k] ? a.ci[q] : 0;
+                hv[k][j] = q < hp1[k] ? a.cv[q] : 0.0f;
+            }
+        auto for_rest = [&](auto fn) {  // nonzeros past the first 256
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+                for (int64_t q = hp0[k] + 256 + lane; q < hp1[k]; q += 64)
+                    fn(wave + k * NW, a.ci[q], a.cv[q]);
+        };
+        float sqa = 0.0f, sqb = 0.0f;
+        if (tid < nS * nS) {
+            const int ia = tid / nS, ib = tid - ia * nS;
+            sqa = a.sq[shS[ia]];
+            sqb = a.sq[shS[ib]];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (hp0[k] + lane + 64 * j < hp1[k]) cidx[hc[k][j]] = 1;
+        for_rest([&](int, int32_t c, float) { cidx[c] = 1; });
+        __syncthreads();
+        const int E = block_exclusive_scan(cidx, ldp, ri[0]);
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (hp0[k] + lane + 64 * j < hp1[k])
+                    tab[(int64_t)cidx[hc[k][j]] * QS + wave + k * NW] = hv[k][j];
+        for_rest([&](int slot, int32_t c, float v) {
+            tab[(int64_t)cidx[c] * QS + slot] = v;
+        });
         __syncthreads();
         for (int e = tid; e < nS * nS; e += kSelThreads) {
             const int ia = e / nS, ib = e - ia * nS;
             float k = 1.0f;
             if (ia != ib) {
-                const int64_t sa_ = shS[ia];
-                const int64_t p0 = a.rp[sa_], p1 = a.rp[sa_ + 1];
-                const float* xb = xst + ib * wst;
                 float acc = 0.0f;
-                for (int64_t q = p0; q < p1; ++q)
-                    acc = fmaf(a.cv[q], xb[a.ci[q]], acc);
-                k = rbf_from_dot(a.sq[sa_], a.sq[shS[ib]], acc, a.gexp);
+                for (int r = 0; r < E; ++r)
+                    acc = fmaf(tab[r * QS + ia], tab[r * QS + ib], acc);
+                const float qa = e == tid ? sqa : a.sq[shS[ia]];
+                const float qb = e == tid ? sqb : a.sq[shS[ib]];
+                k = rbf_from_dot(qa, qb, acc, a.gexp);
             }
             KSS[ia][ib] = k;
+        }
+        if (a.xsc) {
+            // the table and its columns for the row kernel
+            for (int64_t c = tid; c < ldp; c += kSelThreads) {
+                const int e = cidx[c];
+                const bool used = (c + 1 < ldp ? cidx[c + 1] : E) > e;
+                if (used && e < CC) a.xsc_cols[e] = (int32_t)c;
+            }
+            for (int e = E + tid; e < CC; e += kSelThreads) a.xsc_cols[e] = -1;
+            const int64_t n4 = (int64_t)(CC + 1) * QS / 4;
+            for (int64_t e = tid; e < n4; e += kSelThreads)
+                *reinterpret_cast<float4*>(a.xsc + 4 * e) = ld4(tab + 4 * e);
         }
         if (tid < nS) shsS[tid] = a.sq[shS[tid]];
         t_stage = wall_clock64();
@@ -1020,7 +1128,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         }
         const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
         const int W = a.slice;
-        if (W >= ldp16) {
+        if (!a.rp && W >= ldp16) {
             const int q4 = ldp16 >> 2, wst = W + 4;
             for (int e = tid - 64; e < nS * q4; e += kSelThreads - 64) {
                 const int slot = e / q4, c4 = e - slot * q4;
@@ -1155,7 +1263,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 template <bool SVR, int NBLK>
 static void select_dispatch(const SelArgs& a, hipStream_t s)
 {
-    const size_t lds = select_lds_bytes(NBLK, a.slice);
+    const size_t lds = a.rp ? select_csr_lds_bytes(NBLK, a.ldp, a.csr_cols)
+                            : select_lds_bytes(NBLK, a.slice);
     static size_t lds_allowed = 32 * 1024;
     if (lds > lds_allowed) {
         hipError_t e = hipFuncSetAttribute(
@@ -1176,9 +1285,9 @@ void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)
     SelArgs a = a0;
     if (a.slice <= 0) a.slice = select_slice(nblk_cols, a.ldp);
     if (a.rp) {
-        // CSR: the dense working-set rows are whole in LDS
+        // CSR: the working set by column is whole in LDS
         a.slice = (int)((a.ldp + 15) & ~(int64_t)15);
-        if (select_lds_bytes(nblk_cols, a.slice) > 112 * 1024)
+        if (select_csr_lds_bytes(nblk_cols, a.ldp, a.csr_cols) > 112 * 1024)
             throw Error{SVM_E_UNSUPPORTED,
                         "too many features for a CSR working set in LDS"};
     }

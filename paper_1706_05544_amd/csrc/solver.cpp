@@ -51,14 +51,16 @@ static void load_csr(const svm_matrix* M, Features& f, Context& cx)
         HIP_TRY(hipMemcpyAsync(f.cv.p, M->values, (size_t)f.nnz * sizeof(float),
                                kind, cx.stream));
     }
-    DevBuf<int32_t> bad(1);
-    HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
+    DevBuf<int32_t> bad(2);
+    HIP_TRY(hipMemsetAsync(bad.p, 0, 2 * sizeof(int32_t), cx.stream));
     launch_csr_check_norms(f.rp.p, f.ci.p, f.cv.p, f.n, f.d, f.nnz, f.sq.p,
                            bad.p, cx.stream);
-    int32_t hb = 0;
-    HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t), hipMemcpyDeviceToHost,
-                           cx.stream));
+    int32_t hbv[2] = {0, 0};
+    HIP_TRY(hipMemcpyAsync(hbv, bad.p, 2 * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, cx.stream));
     cx.sync();
+    const int32_t hb = hbv[0];
+    f.maxnz = hbv[1];
     if (hb & 2)
         throw Error{SVM_E_INVALID,
                     "CSR row pointers must start at 0, not decrease and end at "
@@ -187,7 +189,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     if (f.csr && o.q > 32)
         throw Error{SVM_E_UNSUPPORTED,
                     "CSR input supports working sets of at most 32"};
-    if (rows_lds_bytes(nblk_cols_, f.ldp, 1, svr, f.csr) > kLdsMax)
+    if (rows_lds_bytes(nblk_cols_, f.ldp, 1, svr, csr_cols(nblk_cols_)) > kLdsMax)
         throw Error{SVM_E_UNSUPPORTED,
                     "too many features for the dense row kernel's LDS tile"};
     int cus = 0;
@@ -200,7 +202,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     tiles_ = 1;
     int64_t cap_blocks = 1;
     for (int it = 0; it < 8; ++it) {
-        const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr);
+        const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, csr_cols(nblk_cols_));
         cap_blocks = (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds, f.csr);
         const int64_t cap = cap_blocks * kWaves;
         const int t = (int)std::max<int64_t>(1, (tiles_total + cap - 1) / cap);
@@ -217,7 +219,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     }
     nb = std::max<int64_t>(1, std::min(nb, rec_cap));
     tiles_ = (int)((tiles_total + kWaves * nb - 1) / (kWaves * nb));
-    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, f.csr) > kLdsMax ||
+    if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, csr_cols(nblk_cols_)) > kLdsMax ||
         (int64_t)16 * tiles_ * f.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED,
                     "training set too large for the dense row kernel"};
@@ -229,6 +231,10 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     y_.alloc((size_t)n_);
     ws_.alloc(1);
     xS_.alloc((size_t)kMaxQ * f.ldp);
+    if (f.csr) {
+        xsc_cols_.alloc((size_t)f.ldp);
+        xsc_.alloc((size_t)(f.ldp + 1) * kMaxQ);
+    }
     ckey_.alloc((size_t)nb_ * 2 * kBlockTop);
     cidx_.alloc((size_t)nb_ * 2 * kBlockTop);
     sum_.alloc(1);
@@ -261,6 +267,29 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     }
 }
 
+int Solver::csr_cols(int nbc) const
+{
+    if (!f_.csr) return -1;
+    // the columns of the working set: at most its samples' nonzeros and d
+    const int64_t c = std::min<int64_t>(f_.ldp,
+                                        (int64_t)16 * nbc * std::max<int64_t>(1, f_.maxnz));
+    return (int)c;
+}
+
+void Solver::set_csr(RowArgs& a, int nbc) const
+{
+    a.csr_cols = csr_cols(nbc);
+    a.xsc_cols = xsc_cols_.p;
+    a.xsc = xsc_.p;
+}
+
+void Solver::set_csr(SelArgs& a, int nbc)
+{
+    a.csr_cols = csr_cols(nbc);
+    a.xsc_cols = xsc_cols_.p;
+    a.xsc = xsc_.p;
+}
+
 void Solver::launch_keys()
 {
     RowArgs a{};
@@ -274,6 +303,7 @@ void Solver::launch_keys()
     a.z = y_.p;
     a.ws = ws_.p;
     a.xS = xS_.p;
+    set_csr(a, nblk_cols_);
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
     a.n = n_;
@@ -300,6 +330,7 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
     a.z = y_.p;
     a.ws = ws_.p;
     a.xS = xS_.p;
+    set_csr(a, nblk_cols_);
     a.cand_key = ckey_.p;
     a.cand_idx = cidx_.p;
     a.n = n_;
@@ -336,6 +367,7 @@ void Solver::launch_solve(int32_t mode)
     a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.xS = xS_.p;
+    set_csr(a, nblk_cols_);
     a.n = n_;
     a.ldp = f_.ldp;
     a.C = o_.C;
@@ -663,6 +695,10 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     HIP_TRY(hipMemcpyAsync(sidx.p, samples, (size_t)k * sizeof(int32_t),
                            hipMemcpyHostToDevice, s));
     gather_rows(f_, sidx.p, k, xS_.p, nullptr, s);
+    const int nbc = k <= 16 ? 1 : (k <= 32 ? 2 : 4);
+    if (f_.csr)
+        launch_csr_compact(xS_.p, k, f_.ldp, 16 * nbc, csr_cols(nbc),
+                           xsc_cols_.p, xsc_.p, s);
     cx_.sync();
     HIP_TRY(hipMemcpyAsync(ws_.p, &w, sizeof(WorkingSet),
                            hipMemcpyHostToDevice, s));
@@ -679,6 +715,7 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     a.z = y_.p;
     a.ws = ws_.p;
     a.xS = xS_.p;
+    set_csr(a, nbc);
     a.rows_out = rows_out_.p;
     a.n = n_;
     a.ldp = f_.ldp;
@@ -688,9 +725,8 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     a.tiles = tiles_;
     a.mode = RU_ROWS;
     a.nS_override = k;
-    int nbc = k <= 16 ? 1 : (k <= 32 ? 2 : 4);
     if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR,
-                       f_.csr) >
+                       csr_cols(nbc)) >
         160 * 1024)
         throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
     launch_rows(a, nb_, nbc, o_.type == SVM_EPS_SVR, s);
@@ -724,6 +760,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.xS = xS_.p;
+    set_csr(a, nB <= 16 ? 1 : (nB <= 32 ? 2 : 4));
     a.n = n_;
     a.ldp = f_.ldp;
     a.C = o_.C;
@@ -770,6 +807,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.cv = f_.cv.p;
     a.sq = f_.sq.p;
     a.xS = xS_.p;
+    set_csr(a, nB <= 16 ? 1 : (nB <= 32 ? 2 : 4));
     a.n = n_;
     a.ldp = f_.ldp;
     a.C = o_.C;
@@ -796,6 +834,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     r.z = y_.p;
     r.ws = ws_.p;
     r.xS = xS_.p;
+    set_csr(r, nbc);
     r.cand_key = ckey_.p;
     r.cand_idx = cidx_.p;
     r.n = n_;
@@ -807,7 +846,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     r.mode = RU_UPDATE;
     r.nS_override = -1;
     if (rows_lds_bytes(nbc, f_.ldp, tiles_, o_.type == SVM_EPS_SVR,
-                       f_.csr) >
+                       csr_cols(nbc)) >
         160 * 1024)
         throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
     launch_rows(r, nb_, nbc, o_.type == SVM_EPS_SVR, s);

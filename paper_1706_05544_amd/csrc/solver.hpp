@@ -86,6 +86,7 @@ struct Context {
 // rows (the working-set rows, support vectors).
 struct Features {
     int64_t n = 0, d = 0, ldp = 0, nnz = 0;
+    int64_t maxnz = 0;  // CSR: nonzeros of the longest row
     bool csr = false;
     DevBuf<float> X, sq;
     DevBuf<int64_t> rp;
@@ -163,6 +164,11 @@ private:
     bool run_loop(SolveResult& r);
     void recompute_responses();
     void read_ws(WorkingSet& w);
+    // CSR: compact working-set columns of a launch with nbc column blocks
+    // (-1 for dense features), and the by-column working set in the args
+    int csr_cols(int nbc) const;
+    void set_csr(RowArgs& a, int nbc) const;
+    void set_csr(SelArgs& a, int nbc);
 
     Context& cx_;
     const Features& f_;
@@ -175,6 +181,8 @@ private:
     DevBuf<float> y_;
     DevBuf<WorkingSet> ws_;
     DevBuf<float> xS_;
+    DevBuf<int32_t> xsc_cols_;  // CSR: the working set by column
+    DevBuf<float> xsc_;
     DevBuf<double> ckey_;
     DevBuf<int32_t> cidx_;
     DevBuf<Summary> sum_;
