@@ -180,14 +180,18 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         cf[b] = (slot < nS && UPD) ? c : 0.0;
     }
 
-    // rows of this wave: rw0 .. rw0 + nw - 1, in Tw <= T tiles of 16 (the
-    // ceil(n / 16) tiles are shared out evenly over the grid's waves, so
-    // that no compute unit holds more of them than another)
-    const int64_t TT = (n + 15) >> 4;
-    const int64_t W = (int64_t)gridDim.x * kRowWaves;
-    const int64_t wid = (int64_t)blockIdx.x * kRowWaves + wave;
-    const int64_t rw0 = 16 * (wid * TT / W);
-    const int nw = (int)(min(16 * ((wid + 1) * TT / W), n) - rw0);
+    // rows of this wave: rw0 .. rw0 + nw - 1, in Tw <= T tiles of 16.  The
+    // ceil(n / 32) units of 32 rows are shared out evenly over the blocks
+    // (so that no compute unit holds more of them than another, and the
+    // part of a block of every per-row fp32 array, norms and cached kernel
+    // rows, covers whole 128-byte lines: blocks sit on different L2s), and
+    // the block's 16-row tiles evenly over its waves.
+    const int64_t TU = (n + 31) >> 5, NB = gridDim.x;
+    const int64_t b0 = 32 * ((int64_t)blockIdx.x * TU / NB);
+    const int64_t b1 = min(32 * (((int64_t)blockIdx.x + 1) * TU / NB), n);
+    const int tb = (int)((b1 - b0 + 15) >> 4);
+    const int64_t rw0 = b0 + 16 * (wave * tb / kRowWaves);
+    const int nw = (int)(min(b0 + 16 * ((wave + 1) * tb / kRowWaves), b1) - rw0);
     const int Tw = (nw + 15) >> 4;
     unsigned char* aux =
         smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) + wave * rows_aux_bytes(T, SVR);

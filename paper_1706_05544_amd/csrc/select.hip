@@ -531,21 +531,21 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         t_c2 = wall_clock64();
         // (5) row groups whose whole candidate list was taken may hold
         // more: wave 0 finds them (lane-parallel).  Group b (k_rows block
-        // b) holds the tiles [b TT / nb, (b + 1) TT / nb) of the TT tiles
-        // of 16 rows; it has at most grows rows.
+        // b) holds the units [b TU / nb, (b + 1) TU / nb) of the TU units
+        // of 32 rows; it has at most grows rows.
         const uint32_t grows = (uint32_t)a.group_rows;
-        const int64_t TT = (n + 15) >> 4, NB = a.nb;
-        // group of a row: floor(((row / 16 + 1) NB - 1) / TT), through an
+        const int64_t TU = (n + 31) >> 5, NB = a.nb;
+        // group of a row: floor(((row / 32 + 1) NB - 1) / TU), through an
         // fp64 quotient corrected to the exact integer
         auto group_of = [&](int64_t row) -> int32_t {
-            const int64_t x = ((row >> 4) + 1) * NB - 1;
-            int64_t g = (int64_t)((double)x / (double)TT);
-            if (g * TT > x) --g;
-            else if ((g + 1) * TT <= x) ++g;
+            const int64_t x = ((row >> 5) + 1) * NB - 1;
+            int64_t g = (int64_t)((double)x / (double)TU);
+            if (g * TU > x) --g;
+            else if ((g + 1) * TU <= x) ++g;
             return (int32_t)g;
         };
         auto group_start = [&](int64_t b) -> int64_t {
-            return 16 * (b * TT / NB);
+            return 32 * (b * TU / NB);
         };
         if (wave == 0) {
             // lanes [0, 32): the up winners, [32, 64): the low winners

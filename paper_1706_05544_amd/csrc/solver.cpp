@@ -181,8 +181,9 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     half_ = o.q / 2;
     nblk_cols_ = o.q <= 16 ? 1 : (o.q <= 32 ? 2 : 4);
     // Grid: every block of k_rows resident at once (occupancy from the
-    // runtime); the 16-row tiles are shared out evenly over the waves, at
-    // most `tiles_` per wave.
+    // runtime); units of 32 rows (two 16-row tiles) are shared out evenly
+    // over the blocks, and a block's tiles over its waves: at most
+    // `tiles_` tiles per wave.
     constexpr int kWaves = kRowThreads / 64;
     const bool svr = o.type == SVM_EPS_SVR;
     constexpr size_t kLdsMax = 160 * 1024;
@@ -195,7 +196,13 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     int cus = 0;
     HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
                                   cx.device));
+    const int64_t units = (n_ + 31) / 32;
     const int64_t tiles_total = (n_ + 15) / 16;
+    // tiles per wave with nb blocks
+    auto wave_tiles = [&](int64_t nb) {
+        const int64_t block_tiles = 2 * ((units + nb - 1) / nb);
+        return (int)((block_tiles + kWaves - 1) / kWaves);
+    };
     // The LDS of a block grows with the tiles per wave (row data is staged),
     // and the resident blocks shrink with the LDS: iterate to a fixed point
     // (tiles only grow, so this ends).
@@ -204,8 +211,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     for (int it = 0; it < 8; ++it) {
         const size_t lds = rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, csr_cols(nblk_cols_));
         cap_blocks = (int64_t)cus * rows_blocks_per_cu(nblk_cols_, svr, lds, f.csr);
-        const int64_t cap = cap_blocks * kWaves;
-        const int t = (int)std::max<int64_t>(1, (tiles_total + cap - 1) / cap);
+        const int t = wave_tiles(std::min(cap_blocks, units));
         if (t <= tiles_) break;
         tiles_ = t;
     }
@@ -214,11 +220,11 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     const int64_t rec_cap = (int64_t)kSelThreads * kSelRecords;
     int64_t nb = std::min(cap_blocks, (tiles_total + kWaves - 1) / kWaves);
     if (const char* e = getenv("SVM_TILES")) {  // tuning override
-        tiles_ = std::max(1, std::min(4096, atoi(e)));
-        nb = (tiles_total + kWaves * tiles_ - 1) / (kWaves * tiles_);
+        const int64_t t = std::max(1, std::min(4096, atoi(e)));
+        nb = (tiles_total + kWaves * t - 1) / (kWaves * t);
     }
-    nb = std::max<int64_t>(1, std::min(nb, rec_cap));
-    tiles_ = (int)((tiles_total + kWaves * nb - 1) / (kWaves * nb));
+    nb = std::max<int64_t>(1, std::min({nb, rec_cap, units}));
+    tiles_ = wave_tiles(nb);
     if (rows_lds_bytes(nblk_cols_, f.ldp, tiles_, svr, csr_cols(nblk_cols_)) > kLdsMax ||
         (int64_t)16 * tiles_ * f.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED,
