@@ -183,6 +183,32 @@ struct PredictArgs {
     int64_t row_base;     // training-set index of query row 0 (self_match)
     double* out;          // m x n_out
     float gexp;
+    // sparse path: CSR query rows, and the support rows by column in
+    // chunks of 16 (chunk k: support rows 16k .. 16k + 15)
+    const int64_t* rpt;
+    const int32_t* cit;
+    const float* cvt;
+    const int32_t* ch_ncol;  // columns some row of the chunk holds
+    const int32_t* ch_cols;  // nchunk x ch_cap: those columns, increasing
+    const float* ch_tab;     // nchunk x ch_cap x 16: their values (0: none)
+    int32_t ch_cap;
+};
+
+// Building the support rows by column (see PredictArgs), from CSR rows:
+// support row j is CSR row idx[j] (idx == nullptr: row j).  cap bounds the
+// columns of a chunk (16 times the longest row, at most ldp).
+struct ChunkArgs {
+    const int64_t* rp;
+    const int32_t* ci;
+    const float* cv;
+    const float* sq;       // norms of the CSR rows
+    const int32_t* idx;
+    int64_t nsv, ldp;
+    int32_t cap;
+    int32_t* ncol;         // ceil(nsv / 16)
+    int32_t* cols;         // ceil(nsv / 16) x cap
+    float* tab;            // ceil(nsv / 16) x cap x 16
+    float* sq_out;         // nsv: norms of the support rows (or nullptr)
 };
 
 // ---- launch wrappers (kernels.hip / predict.hip) ----
@@ -224,6 +250,11 @@ void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
                         const int32_t* idx, int64_t k, float* out,
                         float* sq_out, hipStream_t s);
 void launch_predict(const PredictArgs& a, hipStream_t s);
+void launch_sv_chunks(const ChunkArgs& a, hipStream_t s);
+void launch_predict_sparse(const PredictArgs& a, hipStream_t s);
+// LDS of the sparse decision kernel, and whether it fits
+size_t predict_sparse_lds_bytes(int64_t ldp, int cap);
+bool predict_sparse_fits(int64_t ldp, int cap);
 void launch_csr_compact(const float* xS, int32_t nS, int64_t ldp,
                         int32_t qs, int32_t csr_cols, int32_t* xsc_cols,
                         float* xsc, hipStream_t s);

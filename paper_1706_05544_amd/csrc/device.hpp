@@ -221,6 +221,42 @@ __device__ void compact_by_column(Val val, int nS, int64_t ldp, int qs,
         cols[e] = -1;
 }
 
+// In-place exclusive prefix sum of v[0..L) (non-negative ints) by a block
+// of NT threads; returns the total.  Thread t sums a contiguous chunk;
+// wsum holds NT / 64 ints of LDS.
+template <int NT>
+__device__ int block_exclusive_scan(int* v, int64_t L, int* wsum)
+{
+    constexpr int NW = NT / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t K = (L + NT - 1) / NT;
+    const int64_t b0 = min((int64_t)tid * K, L), b1 = min(b0 + K, L);
+    int loc = 0;
+    for (int64_t i = b0; i < b1; ++i) loc += v[i];
+    int inc = loc;  // inclusive over the wave
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int u = __shfl_up(inc, o);
+        if (lane >= o) inc += u;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int w = 0; w < NW; ++w) {
+        const int x = wsum[w];
+        off += w < wave ? x : 0;
+        tot += x;
+    }
+    int run = off + inc - loc;
+    for (int64_t i = b0; i < b1; ++i) {
+        const int x = v[i];
+        v[i] = run;
+        run += x;
+    }
+    __syncthreads();
+    return tot;
+}
+
 // number of set bits of m below this lane
 __device__ __forceinline__ int lanes_below(unsigned long long m)
 {

@@ -131,3 +131,254 @@ void launch_predict(const PredictArgs& a, hipStream_t s)
 }
 
 }  // namespace msvm
+
+namespace msvm {
+
+// ---------------------------------------------------------------------------
+// Sparse decision path: CSR query rows against the support rows by column.
+//
+// With a few nonzeros per row nearly every product of the dense path is a
+// product with a zero.  The support rows are grouped in chunks of 16 and
+// stored by column (the columns some row of the chunk holds, increasing,
+// each with the 16 values).  A block owns 256 query rows, one per lane, with
+// the first kSpRegNz nonzeros of each in registers, and walks over all
+// chunks, staging chunk k + 1 in LDS (a map column -> (chunk, table row),
+// the table, the chunk's norms and coefficients) while it computes chunk k,
+// one barrier per chunk.  Per query nonzero at column c the lane looks c up
+// and, if the chunk holds it, adds v * x_s[c] to its 16 dot products: the
+// sum over the common nonzeros in the query row's column order, as every
+// CSR kernel of the library sums it (the skipped products are products with
+// a zero, which change nothing), so the K values are bitwise those of the
+// training kernels.  Per output, c_s K is accumulated in fp64 in chunk and
+// slot order: no atomics, the result does not depend on scheduling.
+
+constexpr int kSpThreads = 256;
+constexpr int kSpRegNz = 32;  // query nonzeros held in registers
+constexpr int kSpOutMax = 16;
+
+// one LDS buffer: map (int2 per column), table (cap x 16 floats), 16 norms,
+// 16 training indices, 16 x kSpOutMax coefficients
+__host__ __device__ inline size_t sp_buf_bytes(int64_t ldp, int cap)
+{
+    return (size_t)ldp * 8 + (size_t)cap * 64 + 64 + 64 +
+           16 * kSpOutMax * 8;
+}
+
+size_t predict_sparse_lds_bytes(int64_t ldp, int cap)
+{
+    return 2 * sp_buf_bytes(ldp, cap);
+}
+
+bool predict_sparse_fits(int64_t ldp, int cap)
+{
+    // two blocks per compute unit
+    return cap > 0 && predict_sparse_lds_bytes(ldp, cap) <= 80 * 1024;
+}
+
+template <int NOUT>
+__global__ __launch_bounds__(kSpThreads) void k_predict_sparse(PredictArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x;
+    const int64_t ldp = a.ldp, nsv = a.nsv;
+    const int cap = a.ch_cap, n_out = a.n_out;
+    const int64_t nchunk = (nsv + 15) / 16;
+    const size_t per = sp_buf_bytes(ldp, cap);
+    auto map_of = [&](int p) {
+        return reinterpret_cast<int2*>(smem + p * per);
+    };
+    auto tab_of = [&](int p) {
+        return reinterpret_cast<float*>(smem + p * per + ldp * 8);
+    };
+    auto sq_of = [&](int p) {
+        return reinterpret_cast<float*>(smem + p * per + ldp * 8 + cap * 64);
+    };
+    auto tix_of = [&](int p) {
+        return reinterpret_cast<int32_t*>(smem + p * per + ldp * 8 +
+                                          cap * 64 + 64);
+    };
+    auto coef_of = [&](int p) {
+        return reinterpret_cast<double*>(smem + p * per + ldp * 8 +
+                                         cap * 64 + 128);
+    };
+
+    for (int64_t c = tid; c < 2 * ldp; c += kSpThreads) {
+        const int p = c >= ldp;
+        map_of(p)[c - p * ldp] = make_int2(-1, 0);
+    }
+    __syncthreads();
+
+    auto stage = [&](int64_t k, int p) {
+        const int E = a.ch_ncol[k];
+        const int32_t* cols = a.ch_cols + k * cap;
+        int2* mp = map_of(p);
+        for (int e = tid; e < E; e += kSpThreads)
+            mp[cols[e]] = make_int2((int)k, e);
+        const float* src = a.ch_tab + k * cap * 16;
+        float* dst = tab_of(p);
+        for (int e = tid; e < E * 4; e += kSpThreads)
+            *reinterpret_cast<float4*>(dst + 4 * e) = ld4(src + 4 * e);
+        if (tid < 16) {
+            const int64_t j = k * 16 + tid;
+            const bool ok = j < nsv;
+            sq_of(p)[tid] = ok ? a.sqsv[j] : 0.0f;
+            tix_of(p)[tid] = (ok && a.self_match) ? a.sv_train_idx[j] : -1;
+        }
+        for (int e = tid; e < 16 * NOUT; e += kSpThreads) {
+            const int s = e / NOUT, o = e - s * NOUT;
+            const int64_t j = k * 16 + s;
+            coef_of(p)[e] =
+                (j < nsv && o < n_out) ? a.coef[j * n_out + o] : 0.0;
+        }
+    };
+    if (nchunk > 0) stage(0, 0);
+
+    // this lane's query row
+    const int64_t r = (int64_t)blockIdx.x * kSpThreads + tid;
+    const bool rv = r < a.m;
+    const int64_t k0 = rv ? a.rpt[r] : 0, k1 = rv ? a.rpt[r + 1] : 0;
+    const int nz = (int)(k1 - k0);
+    int32_t qc[kSpRegNz];
+    float qv[kSpRegNz];
+#pragma unroll
+    for (int i = 0; i < kSpRegNz; ++i) {
+        const bool ok = i < nz;
+        qc[i] = ok ? a.cit[k0 + i] : 0;
+        qv[i] = ok ? a.cvt[k0 + i] : 0.0f;
+    }
+    int mx = min(nz, kSpRegNz);  // wave-uniform bound of the register part
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
+    const float sqr = rv ? a.sqt[r] : 0.0f;
+    const int64_t self = r + a.row_base;
+    double outv[NOUT];
+#pragma unroll
+    for (int o = 0; o < NOUT; ++o) outv[o] = 0.0;
+    __syncthreads();
+
+    for (int64_t k = 0; k < nchunk; ++k) {
+        const int p = (int)(k & 1);
+        if (k + 1 < nchunk) stage(k + 1, p ^ 1);
+        const int2* mp = map_of(p);
+        const float* tb = tab_of(p);
+        float acc[16];
+#pragma unroll
+        for (int s = 0; s < 16; ++s) acc[s] = 0.0f;
+        auto add = [&](int32_t c, float v) {
+            const int2 t = mp[c];
+            if (t.x == (int)k) {
+                const float* xr = tb + t.y * 16;
+#pragma unroll
+                for (int s = 0; s < 16; s += 4) {
+                    const float4 x = ld4(xr + s);
+                    acc[s + 0] = fmaf(v, x.x, acc[s + 0]);
+                    acc[s + 1] = fmaf(v, x.y, acc[s + 1]);
+                    acc[s + 2] = fmaf(v, x.z, acc[s + 2]);
+                    acc[s + 3] = fmaf(v, x.w, acc[s + 3]);
+                }
+            }
+        };
+#pragma unroll
+        for (int i = 0; i < kSpRegNz; ++i) {
+            if (i >= mx) break;
+            if (i < nz) add(qc[i], qv[i]);
+        }
+        for (int64_t q = k0 + kSpRegNz; q < k1; ++q) add(a.cit[q], a.cvt[q]);
+        const float* sq = sq_of(p);
+        const int32_t* tix = tix_of(p);
+        const double* cf = coef_of(p);
+#pragma unroll
+        for (int s = 0; s < 16; ++s) {
+            float kv = rbf_from_dot(sqr, sq[s], acc[s], a.gexp);
+            if ((int64_t)tix[s] == self) kv = 1.0f;
+#pragma unroll
+            for (int o = 0; o < NOUT; ++o)
+                outv[o] = fma(cf[s * NOUT + o], (double)kv, outv[o]);
+        }
+        __syncthreads();
+    }
+
+    if (rv) {
+#pragma unroll
+        for (int o = 0; o < NOUT; ++o)
+            if (o < n_out)
+                a.out[r * n_out + o] = outv[o] + (a.b ? a.b[o] : 0.0);
+    }
+}
+
+void launch_predict_sparse(const PredictArgs& a, hipStream_t s)
+{
+    if (a.m <= 0) return;
+    if (!predict_sparse_fits(a.ldp, a.ch_cap))
+        throw Error{SVM_E_INTERNAL, "sparse decision tables exceed LDS"};
+    const unsigned blocks = (unsigned)((a.m + kSpThreads - 1) / kSpThreads);
+    const size_t lds = predict_sparse_lds_bytes(a.ldp, a.ch_cap);
+    if (a.n_out <= 1)
+        k_predict_sparse<1><<<blocks, kSpThreads, lds, s>>>(a);
+    else if (a.n_out <= 4)
+        k_predict_sparse<4><<<blocks, kSpThreads, lds, s>>>(a);
+    else if (a.n_out <= kSpOutMax)
+        k_predict_sparse<16><<<blocks, kSpThreads, lds, s>>>(a);
+    else
+        throw Error{SVM_E_UNSUPPORTED, "more than 16 outputs"};
+}
+
+// One block per chunk of 16 support rows: flag the columns the rows hold,
+// number them in increasing order (block scan), scatter the values into an
+// LDS table and write it out with the columns.
+__global__ __launch_bounds__(256) void k_sv_chunks(ChunkArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ int wsum[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t ldp = a.ldp, k = blockIdx.x;
+    const int cap = a.cap;
+    int* fl = reinterpret_cast<int*>(smem);
+    float* tl = reinterpret_cast<float*>(smem + ((ldp * 4 + 15) & ~15));
+    for (int64_t c = tid; c < ldp; c += 256) fl[c] = 0;
+    for (int e = tid; e < cap * 16; e += 256) tl[e] = 0.0f;
+    __syncthreads();
+    // the nonzeros of the chunk's rows: wave w takes slots w, w + 4, ...
+    auto each = [&](auto fn) {
+        for (int s = wave; s < 16; s += 4) {
+            const int64_t j = k * 16 + s;
+            if (j >= a.nsv) break;
+            const int64_t row = a.idx ? (int64_t)a.idx[j] : j;
+            const int64_t p0 = a.rp[row], p1 = a.rp[row + 1];
+            for (int64_t q = p0 + lane; q < p1; q += 64)
+                fn(s, a.ci[q], a.cv[q]);
+        }
+    };
+    each([&](int, int32_t c, float) { fl[c] = 1; });
+    __syncthreads();
+    const int E = block_exclusive_scan<256>(fl, ldp, wsum);
+    each([&](int s, int32_t c, float v) {
+        const int e = fl[c];
+        if (e < cap) tl[e * 16 + s] = v;
+    });
+    for (int64_t c = tid; c < ldp; c += 256) {
+        const int e = fl[c];
+        const bool used = (c + 1 < ldp ? fl[c + 1] : E) > e;
+        if (used && e < cap) a.cols[k * cap + e] = (int32_t)c;
+    }
+    if (a.sq_out && tid < 16 && k * 16 + tid < a.nsv) {
+        const int64_t j = k * 16 + tid;
+        a.sq_out[j] = a.sq[a.idx ? (int64_t)a.idx[j] : j];
+    }
+    __syncthreads();
+    const int Ec = min(E, cap);
+    float* dst = a.tab + k * cap * 16;
+    for (int e = tid; e < Ec * 4; e += 256)
+        *reinterpret_cast<float4*>(dst + 4 * e) = ld4(tl + 4 * e);
+    if (tid == 0) a.ncol[k] = Ec;
+}
+
+void launch_sv_chunks(const ChunkArgs& a, hipStream_t s)
+{
+    const int64_t nchunk = (a.nsv + 15) / 16;
+    if (nchunk <= 0) return;
+    const size_t lds = (size_t)((a.ldp * 4 + 15) & ~15) + (size_t)a.cap * 64;
+    k_sv_chunks<<<(unsigned)nchunk, 256, lds, s>>>(a);
+}
+
+}  // namespace msvm

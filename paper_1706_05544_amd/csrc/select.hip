@@ -307,40 +307,6 @@ static size_t select_csr_lds_bytes(int nblk_cols, int64_t ldp, int csr_cols)
            (size_t)(csr_cols + 1) * nblk_cols * 16 * 4;
 }
 
-// In-place exclusive prefix sum of v[0..L) (non-negative ints) by the whole
-// block; returns the total.  Thread t sums a contiguous chunk.
-__device__ int block_exclusive_scan(int* v, int64_t L, int* wsum)
-{
-    constexpr int NW = kSelThreads / 64;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t K = (L + kSelThreads - 1) / kSelThreads;
-    const int64_t b0 = min((int64_t)tid * K, L), b1 = min(b0 + K, L);
-    int loc = 0;
-    for (int64_t i = b0; i < b1; ++i) loc += v[i];
-    int inc = loc;  // inclusive over the wave
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int u = __shfl_up(inc, o);
-        if (lane >= o) inc += u;
-    }
-    if (lane == 63) wsum[wave] = inc;
-    __syncthreads();
-    int off = 0, tot = 0;
-    for (int w = 0; w < NW; ++w) {
-        const int x = wsum[w];
-        off += w < wave ? x : 0;
-        tot += x;
-    }
-    int run = off + inc - loc;
-    for (int64_t i = b0; i < b1; ++i) {
-        const int x = v[i];
-        v[i] = run;
-        run += x;
-    }
-    __syncthreads();
-    return tot;
-}
-
 static size_t select_lds_bytes(int nblk_cols, int slice)
 {
     return (size_t)nblk_cols * 16 * (slice + 4) * sizeof(float);
@@ -925,7 +891,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
                 if (hp0[k] + lane + 64 * j < hp1[k]) cidx[hc[k][j]] = 1;
         for_rest([&](int, int32_t c, float) { cidx[c] = 1; });
         __syncthreads();
-        const int E = block_exclusive_scan(cidx, ldp, ri[0]);
+        const int E = block_exclusive_scan<kSelThreads>(cidx, ldp, ri[0]);
 #pragma unroll
         for (int k = 0; k < 2; ++k)
 #pragma unroll

@@ -230,6 +230,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
         throw Error{SVM_E_UNSUPPORTED,
                     "training set too large for the dense row kernel"};
     nb_ = (int)nb;
+    ch_cap_ = sparse_chunk_cap(f);
 
     F_.alloc((size_t)n_);
     alpha_.alloc((size_t)N_);
@@ -525,13 +526,21 @@ void Solver::recompute_responses()
         HIP_TRY(hipMemsetAsync(F_.p, 0, F_.bytes(), s));
         return;
     }
-    if (sv_rows_.count < (size_t)(nsv * f_.ldp)) {
-        sv_rows_.alloc((size_t)(nsv * f_.ldp));
-        sv_sq_.alloc((size_t)nsv);
-    }
-    gather_rows(f_, sv_idx_.p, nsv, sv_rows_.p, sv_sq_.p, s);
     PredictArgs a{};
-    a.SV = sv_rows_.p;
+    if (sv_sq_.count < (size_t)nsv) sv_sq_.alloc((size_t)nsv);
+    if (ch_cap_ > 0) {
+        build_sv_chunks(f_, sv_idx_.p, nsv, ch_cap_, ch_ncol_, ch_cols_,
+                        ch_tab_, sv_sq_.p, s);
+        a.ch_ncol = ch_ncol_.p;
+        a.ch_cols = ch_cols_.p;
+        a.ch_tab = ch_tab_.p;
+        a.ch_cap = ch_cap_;
+    } else {
+        if (sv_rows_.count < (size_t)(nsv * f_.ldp))
+            sv_rows_.alloc((size_t)(nsv * f_.ldp));
+        gather_rows(f_, sv_idx_.p, nsv, sv_rows_.p, sv_sq_.p, s);
+        a.SV = sv_rows_.p;
+    }
     a.sqsv = sv_sq_.p;
     a.nsv = nsv;
     a.coef = sv_coef_.p;
@@ -895,6 +904,10 @@ void build_model(svm_model& m, Context& cx, const Features& f,
     m.coef_dev.alloc((size_t)(nsv * n_out));
     m.b_dev.alloc((size_t)n_out);
     gather_rows(f, idx.p, nsv, m.SV.p, m.sqsv.p, s);
+    m.ch_cap = sparse_chunk_cap(f);
+    if (m.ch_cap > 0)
+        build_sv_chunks(f, idx.p, nsv, m.ch_cap, m.ch_ncol, m.ch_cols,
+                        m.ch_tab, nullptr, s);
     m.sv_idx.resize((size_t)nsv);
     m.coef.resize((size_t)(nsv * n_out));
     if (nsv > 0) {
@@ -928,7 +941,46 @@ void predict_device(const svm_model& mdl, Context& cx, const Features& t,
     a.self_match = 0;
     a.out = out;
     a.gexp = mdl.gexp;
+    if (mdl.ch_cap > 0) {
+        a.ch_ncol = mdl.ch_ncol.p;
+        a.ch_cols = mdl.ch_cols.p;
+        a.ch_tab = mdl.ch_tab.p;
+        a.ch_cap = mdl.ch_cap;
+    }
     predict_rows(a, t, cx.stream);
+}
+
+int sparse_chunk_cap(const Features& f)
+{
+    if (!f.csr || f.n <= 0 || f.nnz > 32 * f.n) return 0;
+    const int64_t cap =
+        std::min<int64_t>(f.ldp, 16 * std::max<int64_t>(1, f.maxnz));
+    return predict_sparse_fits(f.ldp, (int)cap) ? (int)cap : 0;
+}
+
+void build_sv_chunks(const Features& f, const int32_t* idx, int64_t nsv,
+                     int cap, DevBuf<int32_t>& ncol, DevBuf<int32_t>& cols,
+                     DevBuf<float>& tab, float* sq_out, hipStream_t s)
+{
+    const int64_t nch = (nsv + 15) / 16;
+    if (ncol.count < (size_t)nch) ncol.alloc((size_t)nch);
+    if (cols.count < (size_t)(nch * cap)) cols.alloc((size_t)(nch * cap));
+    if (tab.count < (size_t)(nch * cap * 16))
+        tab.alloc((size_t)(nch * cap * 16));
+    ChunkArgs c{};
+    c.rp = f.rp.p;
+    c.ci = f.ci.p;
+    c.cv = f.cv.p;
+    c.sq = f.sq.p;
+    c.idx = idx;
+    c.nsv = nsv;
+    c.ldp = f.ldp;
+    c.cap = cap;
+    c.ncol = ncol.p;
+    c.cols = cols.p;
+    c.tab = tab.p;
+    c.sq_out = sq_out;
+    launch_sv_chunks(c, s);
 }
 
 void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
@@ -952,6 +1004,18 @@ void predict_rows(PredictArgs a, const Features& t, hipStream_t s)
         launch_predict(a, s);
         return;
     }
+    if (a.ch_tab && t.nnz <= 32 * t.n) {
+        a.rpt = t.rp.p;
+        a.cit = t.ci.p;
+        a.cvt = t.cv.p;
+        a.sqt = t.sq.p;
+        a.m = t.n;
+        a.row_base = 0;
+        launch_predict_sparse(a, s);
+        return;
+    }
+    if (!a.SV)
+        throw Error{SVM_E_INTERNAL, "no dense support rows for this input"};
     // CSR rows: dense chunks of up to 256 MB
     const int64_t row_bytes = t.ldp * (int64_t)sizeof(float);
     int64_t chunk = std::max<int64_t>(64, ((int64_t)256 << 20) / row_bytes);

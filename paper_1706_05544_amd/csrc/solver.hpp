@@ -192,6 +192,10 @@ private:
     DevBuf<int64_t> sv_cnt_;
     DevBuf<float> sv_rows_, sv_sq_;
     DevBuf<float> rows_out_;
+    // sparse decision path of the recompute: support rows by column
+    int ch_cap_ = 0;
+    DevBuf<int32_t> ch_ncol_, ch_cols_;
+    DevBuf<float> ch_tab_;
     RowCache* cache_ = nullptr;
     double row_ms_ = 0, cached_ms_ = 0, row_bytes_ = 0, cached_bytes_ = 0;
     int64_t row_launches_ = 0, row_rows_ = 0, cached_launches_ = 0;
@@ -210,6 +214,11 @@ struct svm_model {
     int64_t n_sv = 0;
     msvm::DevBuf<float> SV, sqsv;
     msvm::DevBuf<double> coef_dev, b_dev;
+    // CSR training set with sparse rows: the support rows by column in
+    // chunks of 16, for the sparse decision path (ch_cap == 0: none)
+    int32_t ch_cap = 0;
+    msvm::DevBuf<int32_t> ch_ncol, ch_cols;
+    msvm::DevBuf<float> ch_tab;
     std::vector<int32_t> sv_idx;             // union, increasing
     std::vector<double> coef;                // n_sv x n_out
     std::vector<double> b;                   // n_out
@@ -224,8 +233,22 @@ void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
                  float* sq_out, hipStream_t s);
 
 // Decision sums of a (support rows, coefficients, outputs set) for every
-// row of t: dense rows directly, CSR rows through dense chunks of rows.
+// row of t: dense rows directly; sparse CSR rows through the sparse path
+// when a carries the support rows by column; other CSR rows through dense
+// chunks of rows.
 void predict_rows(PredictArgs a, const Features& t, hipStream_t s);
+
+// Capacity (columns per chunk of 16 rows) of the by-column support rows of
+// the sparse decision path for a CSR training set, or 0 when its rows are
+// not sparse enough (more than 32 nonzeros a row on average) or a chunk's
+// table would not fit the kernel's LDS.
+int sparse_chunk_cap(const Features& f);
+
+// Builds the by-column support rows: support row j is row idx[j] of f, and
+// its norm goes to sq_out[j] (when given).  Sizes the buffers.
+void build_sv_chunks(const Features& f, const int32_t* idx, int64_t nsv,
+                     int cap, DevBuf<int32_t>& ncol, DevBuf<int32_t>& cols,
+                     DevBuf<float>& tab, float* sq_out, hipStream_t s);
 
 // Builds the model arrays from the n x n_out coefficient matrix (device).
 void build_model(svm_model& m, Context& cx, const Features& f,

@@ -119,6 +119,34 @@ def test_ovr_c4_csr_against_oracle():
     assert np.mean(L == np.argmax(Dref, axis=1)) >= 0.999
 
 
+def test_sparse_decision_path_against_oracle():
+    # ragged rows (0 to 40 nonzeros, some past the 32 the kernel holds in
+    # registers) and three one-vs-rest outputs: a CSR model's predictions on
+    # CSR rows go through the support rows by column; the oracle sums c K
+    # directly over the GPU's support vectors
+    X, _ = _ragged(1200, 500, 21)
+    labels = np.random.default_rng(5).integers(0, 3, 1200).astype(np.int32)
+    m = nv.svm_train_ovr(X, labels, 3, C=1.0, gamma=0.05, tol=1e-3)
+    Xt, _ = _ragged(700, 500, 22)
+    D = nv.svm_predict(m, Xt)
+    for c in range(3):
+        idx, coef, _ = nv.svm_model_get(m, c, with_alpha=True)
+        SV = oracle.Matrix(X).rows(idx)
+        Dsame = oracle.decision(SV, coef, m.info(c)["b"], Xt, 0.05)
+        Kabs = oracle.decision(SV, np.abs(coef), 0.0, Xt, 0.05)
+        assert np.max(np.abs(D[:, c] - Dsame) / (Kabs + 1.0)) <= 1e-6
+    # empty query set, and a query set of only empty rows
+    assert nv.svm_predict(m, sp.csr_matrix((0, 500), dtype=np.float32)
+                          ).shape == (0, 3)
+    Z = sp.csr_matrix((5, 500), dtype=np.float32)
+    Dz = nv.svm_predict(m, Z)
+    for c in range(3):
+        idx, coef, _ = nv.svm_model_get(m, c)
+        Dref = oracle.decision(oracle.Matrix(X).rows(idx), coef,
+                               m.info(c)["b"], Z, 0.05)
+        np.testing.assert_allclose(Dz[:, c], Dref, rtol=1e-6, atol=1e-9)
+
+
 def test_csr_and_dense_give_the_same_model():
     X, y = _ragged(1500, 300, 7)
     kw = dict(type=C_SVC, C=1.0, gamma=0.02, tol=1e-3)
