@@ -11,6 +11,13 @@ namespace msvm {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
+// s_waitcnt immediate (gfx9 encoding): vmcnt 0, expcnt and lgkmcnt not
+// waited.  Where the compiler cannot count the loads in flight (a load in
+// a loop or behind a branch) it waits for all of them at the next use of
+// any loaded value; an explicit wait once they are all needed anyway keeps
+// that wait out of the loops that follow.
+constexpr int kVmcnt0 = 0x0f70;
+
 // One 16x16x4 fp32 matrix-core step.  Lane l supplies A[l%16][l/16] and
 // B[l/16][l%16]; lane l, register v of the result holds D[4(l/16)+v][l%16].
 __device__ __forceinline__ floatx4 mfma4(float a, float b, floatx4 c)

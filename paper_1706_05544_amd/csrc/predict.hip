@@ -142,9 +142,10 @@ namespace msvm {
 // stored by column (the columns some row of the chunk holds, increasing,
 // each with the 16 values).  A block owns 256 query rows, one per lane, with
 // the first kSpRegNz nonzeros of each in registers, and walks over all
-// chunks, staging chunk k + 1 in LDS (a map column -> (chunk, table row),
-// the table, the chunk's norms and coefficients) while it computes chunk k,
-// one barrier per chunk.  Per query nonzero at column c the lane looks c up
+// chunks: while it sums chunk k it writes chunk k + 1 into LDS (a map
+// column -> (chunk, table row), the table, the chunk's norms and
+// coefficients) from registers and loads chunk k + 2 into them, one barrier
+// per chunk.  Per query nonzero at column c the lane looks c up
 // and, if the chunk holds it, adds v * x_s[c] to its 16 dot products: the
 // sum over the common nonzeros in the query row's column order, as every
 // CSR kernel of the library sums it (the skipped products are products with
@@ -155,12 +156,17 @@ namespace msvm {
 constexpr int kSpThreads = 256;
 constexpr int kSpRegNz = 32;  // query nonzeros held in registers
 constexpr int kSpOutMax = 16;
+constexpr int kSpTabMax = 512;  // columns of a chunk (fits the registers)
+// LDS table rows: 16 values padded to 20 floats, so that rows start on 8
+// different banks and the 16-byte reads of lanes on different rows rarely
+// conflict
+constexpr int kSpTS = 20;
 
 // one LDS buffer: map (int2 per column), table (cap x 16 floats), 16 norms,
 // 16 training indices, 16 x kSpOutMax coefficients
 __host__ __device__ inline size_t sp_buf_bytes(int64_t ldp, int cap)
 {
-    return (size_t)ldp * 8 + (size_t)cap * 64 + 64 + 64 +
+    return (size_t)ldp * 8 + (size_t)(cap + 1) * kSpTS * 4 + 64 + 64 +
            16 * kSpOutMax * 8;
 }
 
@@ -171,8 +177,9 @@ size_t predict_sparse_lds_bytes(int64_t ldp, int cap)
 
 bool predict_sparse_fits(int64_t ldp, int cap)
 {
-    // two blocks per compute unit
-    return cap > 0 && predict_sparse_lds_bytes(ldp, cap) <= 80 * 1024;
+    // two blocks per compute unit; a chunk's columns fit the prefetch
+    return cap > 0 && cap <= kSpTabMax &&
+           predict_sparse_lds_bytes(ldp, cap) <= 80 * 1024;
 }
 
 template <int NOUT>
@@ -190,48 +197,90 @@ __global__ __launch_bounds__(kSpThreads) void k_predict_sparse(PredictArgs a)
     auto tab_of = [&](int p) {
         return reinterpret_cast<float*>(smem + p * per + ldp * 8);
     };
+    const size_t tb_bytes = (size_t)(cap + 1) * kSpTS * 4;
     auto sq_of = [&](int p) {
-        return reinterpret_cast<float*>(smem + p * per + ldp * 8 + cap * 64);
+        return reinterpret_cast<float*>(smem + p * per + ldp * 8 + tb_bytes);
     };
     auto tix_of = [&](int p) {
         return reinterpret_cast<int32_t*>(smem + p * per + ldp * 8 +
-                                          cap * 64 + 64);
+                                          tb_bytes + 64);
     };
     auto coef_of = [&](int p) {
         return reinterpret_cast<double*>(smem + p * per + ldp * 8 +
-                                         cap * 64 + 128);
+                                         tb_bytes + 128);
     };
 
     for (int64_t c = tid; c < 2 * ldp; c += kSpThreads) {
         const int p = c >= ldp;
         map_of(p)[c - p * ldp] = make_int2(-1, 0);
     }
+    if (tid < 2 * kSpTS) tab_of(tid / kSpTS)[cap * kSpTS + tid % kSpTS] = 0.0f;
     __syncthreads();
 
-    auto stage = [&](int64_t k, int p) {
-        const int E = a.ch_ncol[k];
-        const int32_t* cols = a.ch_cols + k * cap;
-        int2* mp = map_of(p);
-        for (int e = tid; e < E; e += kSpThreads)
-            mp[cols[e]] = make_int2((int)k, e);
-        const float* src = a.ch_tab + k * cap * 16;
-        float* dst = tab_of(p);
-        for (int e = tid; e < E * 4; e += kSpThreads)
-            *reinterpret_cast<float4*>(dst + 4 * e) = ld4(src + 4 * e);
-        if (tid < 16) {
-            const int64_t j = k * 16 + tid;
-            const bool ok = j < nsv;
-            sq_of(p)[tid] = ok ? a.sqsv[j] : 0.0f;
-            tix_of(p)[tid] = (ok && a.self_match) ? a.sv_train_idx[j] : -1;
-        }
-        for (int e = tid; e < 16 * NOUT; e += kSpThreads) {
-            const int s = e / NOUT, o = e - s * NOUT;
-            const int64_t j = k * 16 + s;
-            coef_of(p)[e] =
-                (j < nsv && o < n_out) ? a.coef[j * n_out + o] : 0.0;
-        }
+    // Chunk k + 2 is loaded into registers while chunk k is summed, and
+    // written to LDS (buffer of chunk k + 2) in the next iteration, so that
+    // no barrier waits for a global load.
+    constexpr int kPF = kSpTabMax * 4 / kSpThreads;  // float4 per thread
+    constexpr int kPC = kSpTabMax / kSpThreads;      // columns per thread
+    struct Pre {
+        float4 t[kPF];
+        int32_t c[kPC];
+        int E;
+        float sq;
+        int32_t tix;
+        double cf;
     };
-    if (nchunk > 0) stage(0, 0);
+    auto fetch = [&](int64_t k, Pre& q) {
+        q.E = a.ch_ncol[k];
+        const float* src = a.ch_tab + k * cap * 16;
+#pragma unroll
+        for (int i = 0; i < kPF; ++i) {
+            const int e = tid + i * kSpThreads;
+            q.t[i] = e < q.E * 4 ? ld4(src + 4 * e) : make_float4(0, 0, 0, 0);
+        }
+        const int32_t* cols = a.ch_cols + k * cap;
+#pragma unroll
+        for (int i = 0; i < kPC; ++i) {
+            const int e = tid + i * kSpThreads;
+            q.c[i] = e < q.E ? cols[e] : 0;
+        }
+        const int64_t j = k * 16 + (tid & 15);
+        const bool ok = tid < 16 && j < nsv;
+        q.sq = ok ? a.sqsv[j] : 0.0f;
+        q.tix = (ok && a.self_match) ? a.sv_train_idx[j] : -1;
+        const int s = tid / NOUT, o = tid - s * NOUT;
+        const int64_t jc = k * 16 + s;
+        q.cf = (tid < 16 * NOUT && jc < nsv && o < n_out)
+                   ? a.coef[jc * n_out + o]
+                   : 0.0;
+    };
+    auto put = [&](int64_t k, int p, const Pre& q) {
+        int2* mp = map_of(p);
+#pragma unroll
+        for (int i = 0; i < kPC; ++i) {
+            const int e = tid + i * kSpThreads;
+            if (e < q.E) mp[q.c[i]] = make_int2((int)k, e);
+        }
+        float* dst = tab_of(p);
+#pragma unroll
+        for (int i = 0; i < kPF; ++i) {
+            const int e = tid + i * kSpThreads;
+            if (e < q.E * 4)
+                *reinterpret_cast<float4*>(dst + (e >> 2) * kSpTS +
+                                           4 * (e & 3)) = q.t[i];
+        }
+        if (tid < 16) {
+            sq_of(p)[tid] = q.sq;
+            tix_of(p)[tid] = q.tix;
+        }
+        if (tid < 16 * NOUT) coef_of(p)[tid] = q.cf;
+    };
+    Pre pre;
+    if (nchunk > 0) {
+        fetch(0, pre);
+        put(0, 0, pre);
+    }
+    if (nchunk > 1) fetch(1, pre);
 
     // this lane's query row
     const int64_t r = (int64_t)blockIdx.x * kSpThreads + tid;
@@ -246,44 +295,77 @@ __global__ __launch_bounds__(kSpThreads) void k_predict_sparse(PredictArgs a)
         qc[i] = ok ? a.cit[k0 + i] : 0;
         qv[i] = ok ? a.cvt[k0 + i] : 0.0f;
     }
-    int mx = min(nz, kSpRegNz);  // wave-uniform bound of the register part
+    int mxall = nz;  // the longest row of the wave
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
+    for (int off = 32; off > 0; off >>= 1)
+        mxall = max(mxall, __shfl_xor(mxall, off));
+    const int mx = min(mxall, kSpRegNz);  // its part held in registers
+    const int zrow = cap * kSpTS;         // the zero row of a table
     const float sqr = rv ? a.sqt[r] : 0.0f;
     const int64_t self = r + a.row_base;
     double outv[NOUT];
 #pragma unroll
     for (int o = 0; o < NOUT; ++o) outv[o] = 0.0;
+    // the query nonzeros (and chunk 1) have arrived: no wait on them inside
+    // the chunk loop
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
     __syncthreads();
 
     for (int64_t k = 0; k < nchunk; ++k) {
         const int p = (int)(k & 1);
-        if (k + 1 < nchunk) stage(k + 1, p ^ 1);
+        if (k + 1 < nchunk) put(k + 1, p ^ 1, pre);
+        if (k + 2 < nchunk) fetch(k + 2, pre);
         const int2* mp = map_of(p);
         const float* tb = tab_of(p);
         float acc[16];
 #pragma unroll
         for (int s = 0; s < 16; ++s) acc[s] = 0.0f;
-        auto add = [&](int32_t c, float v) {
-            const int2 t = mp[c];
-            if (t.x == (int)k) {
-                const float* xr = tb + t.y * 16;
+        // four nonzeros at a time: the four lookups, then the four table
+        // rows (a miss reads the zero row; a product with zero changes
+        // nothing), no branch on the lookups
+        auto rows4 = [&](const int32_t (&c)[4], const float (&v)[4]) {
+            int off[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int2 t = mp[c[j]];
+                off[j] = t.x == (int)k ? t.y * kSpTS : zrow;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float* xr = tb + off[j];
 #pragma unroll
                 for (int s = 0; s < 16; s += 4) {
                     const float4 x = ld4(xr + s);
-                    acc[s + 0] = fmaf(v, x.x, acc[s + 0]);
-                    acc[s + 1] = fmaf(v, x.y, acc[s + 1]);
-                    acc[s + 2] = fmaf(v, x.z, acc[s + 2]);
-                    acc[s + 3] = fmaf(v, x.w, acc[s + 3]);
+                    acc[s + 0] = fmaf(v[j], x.x, acc[s + 0]);
+                    acc[s + 1] = fmaf(v[j], x.y, acc[s + 1]);
+                    acc[s + 2] = fmaf(v[j], x.z, acc[s + 2]);
+                    acc[s + 3] = fmaf(v[j], x.w, acc[s + 3]);
                 }
             }
         };
 #pragma unroll
-        for (int i = 0; i < kSpRegNz; ++i) {
-            if (i >= mx) break;
-            if (i < nz) add(qc[i], qv[i]);
+        for (int g = 0; g < kSpRegNz / 4; ++g) {
+            if (4 * g < mx) {  // uniform over the wave
+                const int32_t c[4] = {qc[4 * g], qc[4 * g + 1], qc[4 * g + 2],
+                                      qc[4 * g + 3]};
+                const float v[4] = {qv[4 * g], qv[4 * g + 1], qv[4 * g + 2],
+                                    qv[4 * g + 3]};
+                rows4(c, v);
+            }
         }
-        for (int64_t q = k0 + kSpRegNz; q < k1; ++q) add(a.cit[q], a.cvt[q]);
+        if (mxall > kSpRegNz) {  // uniform: a row of the wave is longer
+            for (int i = kSpRegNz; i < mxall; i += 4) {
+                int32_t c[4];
+                float v[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const bool ok = i + j < nz;
+                    c[j] = ok ? a.cit[k0 + i + j] : 0;
+                    v[j] = ok ? a.cvt[k0 + i + j] : 0.0f;
+                }
+                rows4(c, v);
+            }
+        }
         const float* sq = sq_of(p);
         const int32_t* tix = tix_of(p);
         const double* cf = coef_of(p);

@@ -24,8 +24,6 @@ constexpr int kSlabStride = 68;
 // feature slabs in flight per wave of k_rows
 constexpr int kRing = 4;
 constexpr int kRowWaves = kRowThreads / 64;
-// s_waitcnt immediate (gfx9 encoding): vmcnt 0, expcnt and lgkmcnt not waited
-constexpr int kVmcnt0 = 0x0f70;
 
 // LDS row stride of a staged working-set sample: ldp rounded up to whole
 // 16-feature chunks (zero-filled) plus a pad of 4 against bank conflicts.
@@ -52,14 +50,16 @@ __host__ __device__ inline int rows_wave_buf(int nblk_cols, bool csr)
 // CSR (csr_cols >= 0): a column map (ldp int32: the compact row of a column
 // used by the working set, or -1), then csr_cols + 1 compact rows of
 // nblk_cols * 16 floats (the samples' values at one column; the last row is
-// zero, for the columns the working set does not use).
+// zero, for the columns the working set does not use), each padded by 4
+// floats: rows then start on 8 different banks, and the 16-byte reads of
+// lanes on different rows rarely conflict.
 __host__ __device__ inline size_t rows_stage_bytes(int nblk_cols, int64_t ldp,
                                                    int csr_cols)
 {
     if (csr_cols < 0)
         return (size_t)nblk_cols * 16 * rows_xs_stride(ldp) * sizeof(float);
     return (((size_t)ldp * 4 + 15) & ~(size_t)15) +
-           (size_t)(csr_cols + 1) * nblk_cols * 16 * sizeof(float);
+           (size_t)(csr_cols + 1) * (nblk_cols * 16 + 4) * sizeof(float);
 }
 
 __host__ __device__ inline size_t rows_aux_offset(int nblk_cols, int64_t ldp,
@@ -354,8 +354,9 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             }
         } else if (CSR) {
             // CSR rows.  The working set sits by column in LDS: colmap[j] is
-            // the compact row of column j (-1: no sample has it), xsT[e * QS
-            // + s] = x_s[cols[e]], and row CC is zero.  One lane per row
+            // the compact row of column j (-1: no sample has it), xsT[e * QT
+            // + s] = x_s[cols[e]] (rows padded to QT floats), and row CC is
+            // zero.  One lane per row
             // walks the row's nonzeros in column order and, per nonzero,
             // reads the QS samples' values of its column: K(x_i, x_s) sums
             // the products of the common nonzeros in increasing column order
@@ -363,7 +364,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             // with a zero add nothing, exactly).  The K values of 64 rows go
             // through a wave buffer into the 16-row tile layout of the
             // epilogue.
-            constexpr int QS = NBLK * 16, QP = QS + 1;
+            constexpr int QS = NBLK * 16, QP = QS + 1, QT = QS + 4;
             const int CC = a.csr_cols;
             int32_t* colmap = reinterpret_cast<int32_t*>(smem);
             float* xsT =
@@ -410,6 +411,10 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                         colmap[c[j]] = e0 + j * kRowThreads;
             }
             const int n4 = (CC + 1) * QS / 4;
+            auto xs_at = [&](int e) {  // float4 e of the table in LDS
+                const int row = e / (QS / 4), j = e - row * (QS / 4);
+                return xsT + row * QT + 4 * j;
+            };
             for (int e0 = tid; e0 < n4; e0 += XB * kRowThreads) {
                 float4 v[XB];
 #pragma unroll
@@ -419,7 +424,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 for (int j = 0; j < XB; ++j)
                     if (e0 + j * kRowThreads < n4)
                         *reinterpret_cast<float4*>(
-                            xsT + 4 * (e0 + j * kRowThreads)) = v[j];
+                            xs_at(e0 + j * kRowThreads)) = v[j];
             }
             // nothing stays in flight (a load whose value is unused would
             // make the row loop wait for all loads at every batch)
@@ -478,7 +483,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 #pragma unroll
                     for (int j = 0; j < KB; ++j) {
                         const int m = colmap[cc[j]];
-                        const float* xr = xsT + (m >= 0 ? m : CC) * QS;
+                        const float* xr = xsT + (m >= 0 ? m : CC) * QT;
 #pragma unroll
                         for (int q = 0; q < QS; q += 4) {
                             const float4 x = ld4(xr + q);
