@@ -23,6 +23,7 @@ namespace msvm {
 constexpr int kMaxQ = 64;          // largest working set
 constexpr int kMaxHalf = kMaxQ / 2;
 constexpr int kRowThreads = 256;   // row/update kernel: 4 waves
+constexpr int kSellRows = 16;      // rows per slice of the sliced CSR copy
 constexpr int kSelThreads = 1024;  // select/solve kernel: one block
 constexpr int kBlockTop = 2;       // candidates per side kept per row group
 constexpr int kSelRecords = 2;     // row-group records held per thread
@@ -106,6 +107,11 @@ struct RowArgs {
     const int64_t* rp;    // CSR rows (rp == nullptr: dense)
     const int32_t* ci;
     const float* cv;
+    // CSR rows sliced by kSellRows (so == nullptr: walk rp/ci/cv instead):
+    // nonzero k of row i at so[i / kSellRows] + kSellRows * k + i % kSellRows
+    const int64_t* so;
+    const int32_t* sci;
+    const float* scv;
     const float* sq;
     double* F;
     const uint8_t* st;
@@ -262,6 +268,13 @@ void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,
                             const float* cv, int64_t n, int64_t d,
                             int64_t nnz, float* sq, int32_t* bad,
                             hipStream_t s);
+// sliced copy of CSR rows (kSellRows rows per slice): so[0 .. ns] (the
+// offsets, ns = ceil(n / kSellRows)), then the entries
+void launch_sell_offsets(const int64_t* rp, int64_t n, int64_t* so,
+                         hipStream_t s);
+void launch_sell_fill(const int64_t* rp, const int32_t* ci, const float* cv,
+                      int64_t n, const int64_t* so, int32_t* sci, float* scv,
+                      hipStream_t s);
 // dense copies of CSR rows (idx == nullptr: rows r0 .. r0 + k - 1)
 void launch_gather_rows_csr(const int64_t* rp, const int32_t* ci,
                             const float* cv, const float* sq, int64_t ldp,

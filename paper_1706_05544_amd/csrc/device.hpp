@@ -305,6 +305,26 @@ __device__ __forceinline__ float bld_f32(Rsrc r, uint32_t off)
         float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
 }
 
+// A 64-bit value that is the same on every active lane, in scalar registers.
+__device__ __forceinline__ int64_t uniform_i64(int64_t v)
+{
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ double uniform_f64(double v)
+{
+    return __builtin_bit_cast(double,
+                              uniform_i64(__builtin_bit_cast(int64_t, v)));
+}
+
+__device__ __forceinline__ int32_t bld_i32(Rsrc r, uint32_t off)
+{
+    return __builtin_bit_cast(
+        int32_t, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+
 __device__ __forceinline__ double bld_f64(Rsrc r, uint32_t off)
 {
     return __builtin_bit_cast(

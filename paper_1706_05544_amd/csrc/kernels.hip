@@ -442,6 +442,94 @@ void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,
         rp, ci, cv, n, d, nnz, sq, bad);
 }
 
+// ---------------------------------------------------------------------------
+// Sliced copy of the CSR rows for the row kernel
+// ---------------------------------------------------------------------------
+//
+// Slices of kSellRows consecutive rows.  Slice s holds nonzero k of its row t
+// at so[s] + kSellRows * k + t for k below the slice width (the most
+// nonzeros of its rows); entries past the end of a row are (column 0, value
+// 0).  A row keeps its nonzeros in column order.  The row kernel walks one
+// row per lane: a load of nonzero k of 64 rows then reads four 64-byte runs
+// instead of 64 scattered words.
+
+// so[s] = kSellRows * (width of slice s), for the scan below
+__global__ void k_sell_widths(const int64_t* rp, int64_t n, int64_t* so)
+{
+    const int64_t ns = (n + kSellRows - 1) / kSellRows;
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s >= ns) return;
+    int64_t w = 0;
+    for (int t = 0; t < kSellRows; ++t) {
+        const int64_t i = s * kSellRows + t;
+        if (i < n) w = max(w, rp[i + 1] - rp[i]);
+    }
+    so[s] = kSellRows * max(w, (int64_t)0);
+}
+
+// Exclusive scan of so[0 .. ns) in place; so[ns] = the total.  One block:
+// each thread sums a contiguous run, the run sums are scanned in LDS, then
+// each thread rewrites its run.
+__global__ __launch_bounds__(1024) void k_sell_scan(int64_t* so, int64_t ns)
+{
+    __shared__ int64_t part[1024];
+    const int t = threadIdx.x;
+    const int64_t run = (ns + 1023) / 1024;
+    const int64_t b = min((int64_t)t * run, ns), e = min(b + run, ns);
+    int64_t acc = 0;
+    for (int64_t k = b; k < e; ++k) acc += so[k];
+    part[t] = acc;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int64_t v = t >= off ? part[t - off] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    acc = part[t] - acc;  // exclusive prefix of this run
+    for (int64_t k = b; k < e; ++k) {
+        const int64_t w = so[k];
+        so[k] = acc;
+        acc += w;
+    }
+    if (t == 1023) so[ns] = part[1023];
+}
+
+// One thread per row: its nonzeros, then the padding of its slice.
+__global__ void k_sell_fill(const int64_t* rp, const int32_t* ci,
+                            const float* cv, int64_t n, const int64_t* so,
+                            int32_t* sci, float* scv)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const int64_t s = i / kSellRows, t = i - s * kSellRows;
+    const int64_t w = (so[s + 1] - so[s]) / kSellRows;
+    const int64_t p0 = rp[i], nz = rp[i + 1] - p0;
+    for (int64_t k = 0; k < w; ++k) {
+        const int64_t dst = so[s] + kSellRows * k + t;
+        sci[dst] = k < nz ? ci[p0 + k] : 0;
+        scv[dst] = k < nz ? cv[p0 + k] : 0.0f;
+    }
+}
+
+void launch_sell_offsets(const int64_t* rp, int64_t n, int64_t* so,
+                         hipStream_t s)
+{
+    const int64_t ns = (n + kSellRows - 1) / kSellRows;
+    if (ns > 0)
+        k_sell_widths<<<(unsigned)((ns + 255) / 256), 256, 0, s>>>(rp, n, so);
+    k_sell_scan<<<1, 1024, 0, s>>>(so, ns);
+}
+
+void launch_sell_fill(const int64_t* rp, const int32_t* ci, const float* cv,
+                      int64_t n, const int64_t* so, int32_t* sci, float* scv,
+                      hipStream_t s)
+{
+    if (n > 0)
+        k_sell_fill<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(rp, ci, cv, n,
+                                                              so, sci, scv);
+}
+
 // Dense rows (ldp wide, zero-filled) of CSR rows: row r of the output is
 // source row idx[r] (idx == nullptr: row r0 + r), with its norm.  One block
 // per output row.

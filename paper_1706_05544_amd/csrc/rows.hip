@@ -33,17 +33,21 @@ __host__ __device__ inline int rows_xs_stride(int64_t ldp)
 }
 
 // Per-wave LDS bytes for the row data of 16 * tiles rows: F (fp64), the
-// squared norm, for eps-SVR the target, and the state byte of each copy.
-__host__ __device__ inline int rows_aux_bytes(int tiles, bool svr)
+// squared norm, for eps-SVR the target, and the state byte of each copy
+// (dense path only).
+__host__ __device__ inline int rows_aux_bytes(int tiles, bool svr, bool csr)
 {
-    return ((16 * tiles * (svr ? 18 : 13)) + 15) & ~15;
+    // (the CSR path reads and writes its row data directly, one row per
+    // lane)
+    return csr ? 0 : ((16 * tiles * (svr ? 18 : 13)) + 15) & ~15;
 }
 
-// Floats of the per-wave buffer: a feature slab (dense), or the K values of
-// 64 rows x 16 * nblk_cols slots with one pad column (CSR).
+// Floats of the per-wave buffer: a feature slab (dense); the CSR path needs
+// none.
 __host__ __device__ inline int rows_wave_buf(int nblk_cols, bool csr)
 {
-    return csr ? 64 * (16 * nblk_cols + 1) : 16 * kSlabStride;
+    (void)nblk_cols;
+    return csr ? 0 : 16 * kSlabStride;
 }
 
 // Staged working set.  Dense: nblk_cols * 16 rows of rows_xs_stride floats.
@@ -80,7 +84,8 @@ size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
                       int csr_cols)
 {
     return rows_aux_offset(nblk_cols, ldp, csr_cols) +
-           (size_t)kRowWaves * rows_aux_bytes(tiles, svr) + kBlockRecBytes +
+           (size_t)kRowWaves * rows_aux_bytes(tiles, svr, csr_cols >= 0) +
+           kBlockRecBytes +
            kSlotInfoBytes;
 }
 
@@ -194,18 +199,19 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
     const int nw = (int)(min(b0 + 16 * ((wave + 1) * tb / kRowWaves), b1) - rw0);
     const int Tw = (nw + 15) >> 4;
     unsigned char* aux =
-        smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) + wave * rows_aux_bytes(T, SVR);
+        smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) +
+        wave * rows_aux_bytes(T, SVR, CSR);
     double* Fw = reinterpret_cast<double*>(aux);
     float* sqw = reinterpret_cast<float*>(aux + 8 * RW);
     float* zw = reinterpret_cast<float*>(aux + 12 * RW);
     uint8_t* stw = aux + (SVR ? 16 : 12) * RW;  // copy (i,-) at stw[RW + r]
     unsigned char* brec = smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) +
-                          kRowWaves * rows_aux_bytes(T, SVR);
+                          kRowWaves * rows_aux_bytes(T, SVR, CSR);
     double* brk = reinterpret_cast<double*>(brec);  // [kRowWaves][4]
     int32_t* bri = reinterpret_cast<int32_t*>(brec + kRowWaves * 32);
     // slot table (block-wide): norm, sample and cache slot of every slot
     unsigned char* sinfo = smem + rows_aux_offset(NBLK, ldp, CSR ? a.csr_cols : -1) +
-                           kRowWaves * rows_aux_bytes(T, SVR) + kBlockRecBytes;
+                           kRowWaves * rows_aux_bytes(T, SVR, CSR) + kBlockRecBytes;
     float* sl_sq = reinterpret_cast<float*>(sinfo);
     int32_t* sl_smp = reinterpret_cast<int32_t*>(sinfo + 4 * kMaxQ);
     int32_t* sl_cs = reinterpret_cast<int32_t*>(sinfo + 8 * kMaxQ);
@@ -250,22 +256,43 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
 
     Top2 up, lo;  // this lane's best candidates of each side
     // keys of the variables of row lr (only lanes with own = true hold one)
-    auto push = [&](int lr, double Fn, bool own) {
-        const int32_t row = (int32_t)(rw0 + lr);
-        const uint8_t s0 = stw[lr];
-        const double r0 = SVR ? (double)zw[lr] - a.eps
+    auto push_vals = [&](int32_t row, double Fn, uint8_t s0, uint8_t s1,
+                         float z, bool own) {
+        const double r0 = SVR ? (double)z - a.eps
                               : ((s0 & ST_YPOS) ? 1.0 : -1.0);
         const double v0 = r0 - Fn;
         const bool u0 = own && (s0 & ST_UP), l0 = own && (s0 & ST_LOW);
         if (u0) up.push(v0, row);
         if (l0) lo.push(-v0, row);
         if (SVR) {
-            const uint8_t s1 = stw[RW + lr];
-            const double v1 = ((double)zw[lr] + a.eps) - Fn;
+            const double v1 = ((double)z + a.eps) - Fn;
             const bool u1 = own && (s1 & ST_UP), l1 = own && (s1 & ST_LOW);
             if (u1) up.push(v1, (int32_t)(n + row));
             if (l1) lo.push(-v1, (int32_t)(n + row));
         }
+    };
+    auto push = [&](int lr, double Fn, bool own) {
+        push_vals((int32_t)(rw0 + lr), Fn, stw[lr], SVR ? stw[RW + lr] : 0,
+                  SVR ? zw[lr] : 0.0f, own);
+    };
+    // Row data of one row per lane for the CSR path (loads past the wave's
+    // rows read zero): F, norm, state bytes, target.
+    struct RowVals {
+        double f;
+        float q, z;
+        uint8_t s0, s1;
+    };
+    auto row_vals = [&](int r, RowVals& v) {
+        const Rsrc rQ = make_rsrc(a.sq + rw0, (int64_t)nw * 4);
+        const Rsrc rS0 = make_rsrc(a.st + rw0, nw);
+        const Rsrc rS1 = make_rsrc(a.st + n + rw0, SVR ? nw : 0);
+        const Rsrc rZ = make_rsrc(a.z + rw0, SVR ? (int64_t)nw * 4 : 0);
+        const uint32_t u = (uint32_t)r;
+        v.f = (UPD || CAND) ? bld_f64(rF, 8 * u) : 0.0;
+        v.q = XS ? bld_f32(rQ, 4 * u) : 0.0f;
+        v.s0 = CAND ? bld_u8(rS0, u) : 0;
+        v.s1 = (SVR && CAND) ? bld_u8(rS1, u) : 0;
+        v.z = (SVR && CAND) ? bld_f32(rZ, 4 * u) : 0.0f;
     };
 
     if (XS) {
@@ -303,7 +330,302 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             if (CAND) push(orl, Fn, nl < 4 && orl < nw);
         };
 
-        if (HOT && path == PATH_CACHED) {
+        if (CSR) {
+            // CSR rows, one row per lane in groups of 64 (its row data read
+            // and F written directly).  Computed path: the working set sits
+            // by column in LDS: colmap[j] is the float offset e * QT in xsT
+            // of the compact row e of column j (-1: no sample has it),
+            // xsT[e * QT + s] = x_s[cols[e]] (rows padded to QT floats).
+            // Each lane walks its row's nonzeros in column order and, per
+            // nonzero, reads the QS samples' values of its column: K(x_i,
+            // x_s) sums the products of the common nonzeros in increasing
+            // column order (every CSR kernel of the library sums them so;
+            // the products with a zero add nothing, exactly).  Cached path:
+            // the lane reads K(x_i, x_s) of its row from the cached rows.
+            // Either way the same epilogue and fp64 order.
+            constexpr int QS = NBLK * 16, QT = QS + 4;
+            const int CC = a.csr_cols;
+            const bool CACHED = HOT && path == PATH_CACHED;  // uniform
+            const bool INS = HOT && path == PATH_INSERT;
+            int32_t* colmap = reinterpret_cast<int32_t*>(smem);
+            float* xsT =
+                reinterpret_cast<float*>(smem + ((ldp * 4 + 15) & ~15));
+            float sq0 = 0.0f;
+            int32_t smp0 = -1, cs0 = -1;
+            if (tid < QS) {
+                const float q = ws->sS[tid];
+                const int32_t i = ws->S[tid], c = ws->cslot[tid];
+                sq0 = tid < nS ? q : 0.0f;
+                smp0 = tid < nS ? i : -1;
+                cs0 = (HOT && tid < nS) ? c : -1;
+            }
+            if (done) return;  // uniform over the block
+            if (!CACHED)
+                for (int e = tid; e < ldp; e += kRowThreads) colmap[e] = -1;
+            if (tid < QS) {
+                sl_sq[tid] = sq0;
+                sl_smp[tid] = smp0;
+                sl_cs[tid] = cs0;
+            }
+            __syncthreads();  // column map cleared, slot table written
+            if (!CACHED) {
+                // the compact columns and rows, 8 loads in flight per thread
+                constexpr int XB = 8;
+                for (int e0 = tid; e0 < CC; e0 += XB * kRowThreads) {
+                    int32_t c[XB];
+#pragma unroll
+                    for (int j = 0; j < XB; ++j)
+                        c[j] = a.xsc_cols[min(e0 + j * kRowThreads, CC - 1)];
+#pragma unroll
+                    for (int j = 0; j < XB; ++j)
+                        if (e0 + j * kRowThreads < CC && c[j] >= 0)
+                            colmap[c[j]] = (e0 + j * kRowThreads) * QT;
+                }
+                const int n4 = (CC + 1) * QS / 4;
+                auto xs_at = [&](int e) {  // float4 e of the table in LDS
+                    const int row = e / (QS / 4), j = e - row * (QS / 4);
+                    return xsT + row * QT + 4 * j;
+                };
+                for (int e0 = tid; e0 < n4; e0 += XB * kRowThreads) {
+                    float4 v[XB];
+#pragma unroll
+                    for (int j = 0; j < XB; ++j)
+                        v[j] = ld4(a.xsc +
+                                   4 * min(e0 + j * kRowThreads, n4 - 1));
+#pragma unroll
+                    for (int j = 0; j < XB; ++j)
+                        if (e0 + j * kRowThreads < n4)
+                            *reinterpret_cast<float4*>(
+                                xs_at(e0 + j * kRowThreads)) = v[j];
+                }
+            }
+            // nothing stays in flight (a load whose value is unused would
+            // make the row loop wait for all loads at every batch)
+            __builtin_amdgcn_s_waitcnt(kVmcnt0);
+            __syncthreads();
+
+            // every working-set coefficient (uniform over the wave)
+            double cfa[QS];
+#pragma unroll
+            for (int q = 0; q < QS; ++q) {
+                const double c = ws->coef[q];
+                cfa[q] = uniform_f64((UPD && q < nS) ? c : 0.0);
+            }
+
+            // The epilogue of the row of this lane (local row r) from its K
+            // values: cache fill (insert path), test rows, F_i += sum_s cf_s
+            // K_is in the order of the 16-lane rotation sum of the tiled
+            // epilogue (so the dense and CSR kernels order F's update
+            // alike), then the keys of its variables.
+            auto finish_row = [&](int r, bool rv, const float (&kv)[QS],
+                                  const RowVals& rd) {
+                if (rv) {
+                    if (INS) {
+#pragma unroll
+                        for (int q = 0; q < QS; ++q) {
+                            const int32_t cs = sl_cs[q];
+                            if (cs >= 0)
+                                a.cache[(int64_t)cs * a.ldc + rw0 + r] = kv[q];
+                        }
+                    }
+                    if (ROWS) {
+#pragma unroll
+                        for (int q = 0; q < QS; ++q)
+                            if (q < nS)
+                                a.rows_out[(int64_t)q * n + rw0 + r] = kv[q];
+                    }
+                }
+                double Fn = rd.f;
+                if (UPD) {
+                    // t_s = sum_b cf K (fma from 0, b ascending); then
+                    // ((t_s + t_s+8) + (t_s+4 + t_s+12)) pairwise down to
+                    // one sum: the rotation order, term by term
+                    auto term = [&](int s) {
+                        double t = 0.0;
+#pragma unroll
+                        for (int b = 0; b < NBLK; ++b)
+                            t = fma(cfa[b * 16 + s], (double)kv[b * 16 + s], t);
+                        return t;
+                    };
+                    auto quad = [&](int s) {  // s < 4
+                        return (term(s) + term(s + 8)) +
+                               (term(s + 4) + term(s + 12));
+                    };
+                    Fn += (quad(0) + quad(2)) + (quad(1) + quad(3));
+                    bst_f64(rF, 8 * (uint32_t)r, Fn);  // dropped past nw
+                }
+                if (CAND)
+                    push_vals((int32_t)(rw0 + r), Fn, rd.s0, rd.s1, rd.z, rv);
+            };
+
+            if (CACHED) {
+                // K(x_i, x_s) of this lane's row from the cached rows of the
+                // slots, the next group's requested while this one is done
+                const float* crow[QS];
+#pragma unroll
+                for (int q = 0; q < QS; ++q) {
+                    const int32_t cs = __builtin_amdgcn_readfirstlane(sl_cs[q]);
+                    crow[q] = a.cache + (int64_t)(cs >= 0 ? cs : 0) * a.ldc +
+                              (cs >= 0 ? rw0 : 0);
+                }
+                auto cfetch = [&](int p0, float (&kv)[QS], RowVals& rd) {
+                    const int r = 16 * p0 + lane;
+                    const int rr = r < nw ? r : 0;  // an address in the row
+#pragma unroll
+                    for (int q = 0; q < QS; ++q) kv[q] = crow[q][rr];
+                    row_vals(r, rd);
+                };
+                float nkv[QS];
+                RowVals nrd;
+                cfetch(0, nkv, nrd);
+                for (int p0 = 0; p0 < Tw; p0 += 4) {
+                    const int r = 16 * p0 + lane;
+                    const bool rv = r < nw;
+                    float kv[QS];
+#pragma unroll
+                    for (int q = 0; q < QS; ++q)
+                        kv[q] = sl_cs[q] >= 0 ? nkv[q] : 0.0f;
+                    const RowVals rd = nrd;
+                    cfetch(p0 + 4, nkv, nrd);
+                    finish_row(r, rv, kv, rd);
+                }
+            } else {
+                // The wave's nonzeros through buffer resources based at its
+                // first row: the sliced copy (a.so; nonzero k of a row
+                // kSellRows entries after nonzero k - 1, the row padded with
+                // zeros to its slice's width) or the CSR rows.  Offsets are
+                // below 2^31 (16 * tiles * ldp * 4 is, checked at launch).
+                // A load past the wave's nonzeros reads zero.
+                const bool sell = a.so != nullptr;  // uniform
+                int64_t e_beg, e_end;
+                if (sell) {
+                    const int64_t ns = (n + kSellRows - 1) / kSellRows;
+                    e_beg = a.so[rw0 / kSellRows];
+                    e_end = a.so[min((rw0 + nw + kSellRows - 1) / kSellRows,
+                                     ns)];
+                } else {
+                    e_beg = a.rp[rw0];
+                    e_end = a.rp[rw0 + nw];
+                }
+                // (values the same on every lane: said so, so that the
+                // resources live in scalar registers)
+                e_beg = uniform_i64(e_beg);
+                e_end = uniform_i64(e_end);
+                const Rsrc rCI = make_rsrc((sell ? a.sci : a.ci) + e_beg,
+                                           4 * (e_end - e_beg));
+                const Rsrc rCV = make_rsrc((sell ? a.scv : a.cv) + e_beg,
+                                           4 * (e_end - e_beg));
+                // byte offset of nonzero 0 and the nonzeros (sliced: the
+                // slice width) of this lane's row in the group p0 .. p0 + 3
+                auto row_ptrs = [&](int p0, uint32_t& lo, int& nz) {
+                    const int r = 16 * p0 + lane;
+                    const bool v = r < nw;
+                    const int64_t gr = v ? rw0 + r : 0;
+                    int64_t k0, k1;
+                    if (sell) {
+                        const int64_t sl = gr / kSellRows;
+                        const int64_t o0 = a.so[sl], o1 = a.so[sl + 1];
+                        k0 = o0 + (gr - sl * kSellRows);
+                        k1 = k0 + (o1 - o0) / kSellRows;
+                    } else {
+                        k0 = a.rp[gr];
+                        k1 = a.rp[gr + 1];
+                    }
+                    lo = v ? (uint32_t)(4 * (k0 - e_beg)) : kOob;
+                    nz = v ? (int)(k1 - k0) : 0;
+                };
+
+                // Per nonzero (column c, value v) of the row: acc[s] += v *
+                // x_s[c] from the table row at colmap[c]; a column no sample
+                // holds adds exact zeros, so its lanes sit out (the table
+                // reads are the LDS cost).  Nonzeros come in batches of KB,
+                // two batches in flight (ping-pong registers: a batch is
+                // waited for only when it is summed).
+                auto run = [&](auto stride_tag) {
+                    constexpr uint32_t STR = decltype(stride_tag)::value;
+                    constexpr int KB = 8;
+                    auto issue = [&](uint32_t vo, int32_t (&cc)[KB],
+                                     float (&vv)[KB]) {
+#pragma unroll
+                        for (int j = 0; j < KB; ++j) {
+                            cc[j] = bld_i32(rCI, vo + STR * j);
+                            vv[j] = bld_f32(rCV, vo + STR * j);
+                        }
+                    };
+                    auto consume = [&](int kb, int nz, const int32_t (&cc)[KB],
+                                       const float (&vv)[KB],
+                                       float (&acc)[QS]) {
+                        int m[KB];
+#pragma unroll
+                        for (int j = 0; j < KB; ++j) m[j] = colmap[cc[j]];
+#pragma unroll
+                        for (int j = 0; j < KB; ++j) {
+                            if (kb + j < nz && m[j] >= 0) {
+                                const float* xr = xsT + m[j];
+#pragma unroll
+                                for (int q = 0; q < QS; q += 4) {
+                                    const float4 x = ld4(xr + q);
+                                    acc[q + 0] = fmaf(vv[j], x.x, acc[q + 0]);
+                                    acc[q + 1] = fmaf(vv[j], x.y, acc[q + 1]);
+                                    acc[q + 2] = fmaf(vv[j], x.z, acc[q + 2]);
+                                    acc[q + 3] = fmaf(vv[j], x.w, acc[q + 3]);
+                                }
+                            }
+                        }
+                    };
+                    uint32_t nlo;
+                    int nnz_next;
+                    RowVals nrd;
+                    row_ptrs(0, nlo, nnz_next);
+                    row_vals(lane, nrd);
+                    for (int p0 = 0; p0 < Tw; p0 += 4) {
+                        const int r = 16 * p0 + lane;  // this lane's row
+                        const bool rv = r < nw;
+                        const uint32_t lo = nlo;
+                        const int nz = nnz_next;
+                        const RowVals rd = nrd;
+                        row_ptrs(p0 + 4, nlo, nnz_next);
+                        row_vals(r + 64, nrd);
+                        int mx = nz;
+#pragma unroll
+                        for (int off = 32; off > 0; off >>= 1)
+                            mx = max(mx, __shfl_xor(mx, off));
+                        mx = __builtin_amdgcn_readfirstlane(mx);
+                        float acc[QS];
+#pragma unroll
+                        for (int q = 0; q < QS; ++q) acc[q] = 0.0f;
+                        int32_t ca[KB], cb[KB];
+                        float va[KB], vb[KB];
+                        issue(mx > 0 ? lo : kOob, ca, va);
+                        for (int kb = 0;;) {
+                            issue(kb + KB < mx ? lo + STR * (kb + KB) : kOob,
+                                  cb, vb);
+                            consume(kb, nz, ca, va, acc);
+                            kb += KB;
+                            if (kb >= mx) break;
+                            issue(kb + KB < mx ? lo + STR * (kb + KB) : kOob,
+                                  ca, va);
+                            consume(kb, nz, cb, vb, acc);
+                            kb += KB;
+                            if (kb >= mx) break;
+                        }
+                        float kv[QS];
+#pragma unroll
+                        for (int q = 0; q < QS; ++q) {
+                            float k = rbf_from_dot(rd.q, sl_sq[q], acc[q],
+                                                   a.gexp);
+                            if (rw0 + r == (int64_t)sl_smp[q]) k = 1.0f;
+                            kv[q] = k;
+                        }
+                        finish_row(r, rv, kv, rd);
+                    }
+                };
+                if (sell)
+                    run(std::integral_constant<uint32_t, 4 * kSellRows>{});
+                else
+                    run(std::integral_constant<uint32_t, 4>{});
+            }
+        } else         if (HOT && path == PATH_CACHED) {
             // Every working-set sample is cached: lane (g, nl) reads rows
             // lr .. lr + 3 of its slot's row as one float4, kRing tiles
             // ahead.  Unused slots read a valid address and are zeroed.
@@ -351,177 +673,6 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                     cfetch(t0 + j + kRing, ring[j]);
                     if (t0 + j < Tw) finish_tile(t0 + j, kv);
                 }
-            }
-        } else if (CSR) {
-            // CSR rows.  The working set sits by column in LDS: colmap[j] is
-            // the compact row of column j (-1: no sample has it), xsT[e * QT
-            // + s] = x_s[cols[e]] (rows padded to QT floats), and row CC is
-            // zero.  One lane per row
-            // walks the row's nonzeros in column order and, per nonzero,
-            // reads the QS samples' values of its column: K(x_i, x_s) sums
-            // the products of the common nonzeros in increasing column order
-            // (every CSR kernel of the library sums them so; the products
-            // with a zero add nothing, exactly).  The K values of 64 rows go
-            // through a wave buffer into the 16-row tile layout of the
-            // epilogue.
-            constexpr int QS = NBLK * 16, QP = QS + 1, QT = QS + 4;
-            const int CC = a.csr_cols;
-            int32_t* colmap = reinterpret_cast<int32_t*>(smem);
-            float* xsT =
-                reinterpret_cast<float*>(smem + ((ldp * 4 + 15) & ~15));
-            float* tb = reinterpret_cast<float*>(
-                            smem + rows_stage_bytes(NBLK, ldp, CC)) +
-                        wave * rows_wave_buf(NBLK, true);
-            float sq0 = 0.0f;
-            int32_t smp0 = -1, cs0 = -1;
-            if (tid < NBLK * 16) {
-                const float q = ws->sS[tid];
-                const int32_t i = ws->S[tid], c = ws->cslot[tid];
-                sq0 = tid < nS ? q : 0.0f;
-                smp0 = tid < nS ? i : -1;
-                cs0 = (HOT && tid < nS) ? c : -1;
-            }
-            AuxRegs ar;
-            aux_issue(0, ar);
-            if (done) return;  // uniform over the block
-            for (int e = tid; e < ldp; e += kRowThreads) colmap[e] = -1;
-            aux_store(0, ar);
-            if (tid < NBLK * 16) {
-                sl_sq[tid] = sq0;
-                sl_smp[tid] = smp0;
-                sl_cs[tid] = cs0;
-            }
-            if (RW > 256) {
-                for (int k0 = 256; k0 < RW; k0 += 256) {
-                    aux_issue(k0, ar);
-                    aux_store(k0, ar);
-                }
-            }
-            __syncthreads();  // column map cleared
-            // the compact columns and rows, 8 loads in flight per thread
-            constexpr int XB = 8;
-            for (int e0 = tid; e0 < CC; e0 += XB * kRowThreads) {
-                int32_t c[XB];
-#pragma unroll
-                for (int j = 0; j < XB; ++j)
-                    c[j] = a.xsc_cols[min(e0 + j * kRowThreads, CC - 1)];
-#pragma unroll
-                for (int j = 0; j < XB; ++j)
-                    if (e0 + j * kRowThreads < CC && c[j] >= 0)
-                        colmap[c[j]] = e0 + j * kRowThreads;
-            }
-            const int n4 = (CC + 1) * QS / 4;
-            auto xs_at = [&](int e) {  // float4 e of the table in LDS
-                const int row = e / (QS / 4), j = e - row * (QS / 4);
-                return xsT + row * QT + 4 * j;
-            };
-            for (int e0 = tid; e0 < n4; e0 += XB * kRowThreads) {
-                float4 v[XB];
-#pragma unroll
-                for (int j = 0; j < XB; ++j)
-                    v[j] = ld4(a.xsc + 4 * min(e0 + j * kRowThreads, n4 - 1));
-#pragma unroll
-                for (int j = 0; j < XB; ++j)
-                    if (e0 + j * kRowThreads < n4)
-                        *reinterpret_cast<float4*>(
-                            xs_at(e0 + j * kRowThreads)) = v[j];
-            }
-            // nothing stays in flight (a load whose value is unused would
-            // make the row loop wait for all loads at every batch)
-            __builtin_amdgcn_s_waitcnt(kVmcnt0);
-            __syncthreads();
-
-            const bool INS = HOT && path == PATH_INSERT;
-            constexpr int KB = 8;  // nonzeros loaded per batch
-            // row pointers of the next 64 rows requested one group ahead,
-            // and each batch of nonzeros while the previous one is summed
-            auto row_ptrs = [&](int p0, int64_t& k0, int64_t& k1) {
-                const int r = 16 * p0 + lane;
-                const int64_t gr = r < nw ? rw0 + r : 0;
-                k0 = a.rp[gr];
-                k1 = a.rp[gr + 1];
-            };
-            auto batch = [&](int kb, int nz, int64_t k0, int32_t (&cc)[KB],
-                             float (&vv)[KB]) {
-#pragma unroll
-                for (int j = 0; j < KB; ++j) {
-                    // unconditional loads (a valid entry when unused)
-                    const bool ok = kb + j < nz;
-                    const int64_t pos = ok ? k0 + kb + j : 0;
-                    cc[j] = a.ci[pos];
-                    vv[j] = a.cv[pos];
-                }
-            };
-            int64_t nk0, nk1;
-            row_ptrs(0, nk0, nk1);
-            for (int p0 = 0; p0 < Tw; p0 += 4) {
-                const int r = 16 * p0 + lane;  // this lane's row (local)
-                const bool rv = r < nw;
-                const int64_t k0 = nk0, k1 = nk1;
-                row_ptrs(p0 + 4, nk0, nk1);
-                const int nz = rv ? (int)(k1 - k0) : 0;
-                int mx = nz;
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1)
-                    mx = max(mx, __shfl_xor(mx, off));
-                float acc[QS];
-#pragma unroll
-                for (int q = 0; q < QS; ++q) acc[q] = 0.0f;
-                int32_t ncc[KB];
-                float nvv[KB];
-                batch(0, nz, k0, ncc, nvv);
-                for (int kb = 0; kb < mx; kb += KB) {
-                    int32_t cc[KB];
-                    float vv[KB];
-#pragma unroll
-                    for (int j = 0; j < KB; ++j) {
-                        const bool ok = kb + j < nz;
-                        cc[j] = ok ? ncc[j] : 0;
-                        vv[j] = ok ? nvv[j] : 0.0f;
-                    }
-                    batch(kb + KB, nz, k0, ncc, nvv);
-#pragma unroll
-                    for (int j = 0; j < KB; ++j) {
-                        const int m = colmap[cc[j]];
-                        const float* xr = xsT + (m >= 0 ? m : CC) * QT;
-#pragma unroll
-                        for (int q = 0; q < QS; q += 4) {
-                            const float4 x = ld4(xr + q);
-                            acc[q + 0] = fmaf(vv[j], x.x, acc[q + 0]);
-                            acc[q + 1] = fmaf(vv[j], x.y, acc[q + 1]);
-                            acc[q + 2] = fmaf(vv[j], x.z, acc[q + 2]);
-                            acc[q + 3] = fmaf(vv[j], x.w, acc[q + 3]);
-                        }
-                    }
-                }
-                const float sqr = rv ? sqw[r] : 0.0f;
-#pragma unroll
-                for (int q = 0; q < QS; ++q) {
-                    float kv = rbf_from_dot(sqr, sl_sq[q], acc[q], a.gexp);
-                    if (rw0 + r == (int64_t)sl_smp[q]) kv = 1.0f;
-                    tb[lane * QP + q] = kv;
-                }
-                __builtin_amdgcn_wave_barrier();
-                for (int t = 0; t < 4; ++t) {
-                    const int ti = p0 + t;
-                    if (ti >= Tw) break;
-                    const int lr = 16 * ti + 4 * g;
-                    float kv[NBLK][4];
-#pragma unroll
-                    for (int b = 0; b < NBLK; ++b) {
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            kv[b][v] = tb[(16 * t + 4 * g + v) * QP + b * 16 + nl];
-                        const int32_t csb = INS ? sl_cs[b * 16 + nl] : -1;
-                        if (csb >= 0 && rw0 + lr < n)
-                            *reinterpret_cast<float4*>(
-                                a.cache + (int64_t)csb * a.ldc + rw0 + lr) =
-                                make_float4(kv[b][0], kv[b][1], kv[b][2],
-                                            kv[b][3]);
-                    }
-                    finish_tile(ti, kv);
-                }
-                __builtin_amdgcn_wave_barrier();
             }
         } else {
             // Staged working-set rows: every slot (finite values past nS),
@@ -689,20 +840,30 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 }
             }
         }
-        if (UPD)
+        if (UPD && !CSR)
             for (int r = lane; r < nw; r += 64) bst_f64(rF, 8 * r, Fw[r]);
     } else if (CAND) {
-        AuxRegs ar;
-        for (int k0 = 0; k0 < RW; k0 += 256) {
-            aux_issue(k0, ar);
-            aux_store(k0, ar);
-        }
-        // keys of the wave's variables, one row per lane
-        for (int r0 = 0; r0 < nw; r0 += 64) {
-            const int r = r0 + lane;
-            const bool own = r < nw;
-            const int rr = own ? r : 0;
-            push(rr, Fw[rr], own);
+        if (CSR) {
+            // keys of the wave's variables, one row per lane, read directly
+            for (int r0 = 0; r0 < nw; r0 += 64) {
+                const int r = r0 + lane;
+                RowVals rd;
+                row_vals(r, rd);
+                push_vals((int32_t)(rw0 + r), rd.f, rd.s0, rd.s1, rd.z, r < nw);
+            }
+        } else {
+            AuxRegs ar;
+            for (int k0 = 0; k0 < RW; k0 += 256) {
+                aux_issue(k0, ar);
+                aux_store(k0, ar);
+            }
+            // keys of the wave's variables, one row per lane
+            for (int r0 = 0; r0 < nw; r0 += 64) {
+                const int r = r0 + lane;
+                const bool own = r < nw;
+                const int rr = own ? r : 0;
+                push(rr, Fw[rr], own);
+            }
         }
     }
 

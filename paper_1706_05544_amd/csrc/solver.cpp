@@ -55,8 +55,15 @@ static void load_csr(const svm_matrix* M, Features& f, Context& cx)
     HIP_TRY(hipMemsetAsync(bad.p, 0, 2 * sizeof(int32_t), cx.stream));
     launch_csr_check_norms(f.rp.p, f.ci.p, f.cv.p, f.n, f.d, f.nnz, f.sq.p,
                            bad.p, cx.stream);
+    // slice offsets from the row pointers (used only once these are valid)
+    const int64_t ns = (f.n + kSellRows - 1) / kSellRows;
+    f.so.alloc((size_t)(ns + 1));
+    launch_sell_offsets(f.rp.p, f.n, f.so.p, cx.stream);
     int32_t hbv[2] = {0, 0};
+    int64_t sell_total = 0;
     HIP_TRY(hipMemcpyAsync(hbv, bad.p, 2 * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, cx.stream));
+    HIP_TRY(hipMemcpyAsync(&sell_total, f.so.p + ns, sizeof(int64_t),
                            hipMemcpyDeviceToHost, cx.stream));
     cx.sync();
     const int32_t hb = hbv[0];
@@ -73,6 +80,14 @@ static void load_csr(const svm_matrix* M, Features& f, Context& cx)
         throw Error{SVM_E_INVALID,
                     "X holds a value that is not finite (or whose square "
                     "overflows fp32)"};
+    if (sell_total > 0 && sell_total <= 4 * f.nnz + 64 * kSellRows) {
+        f.sci.alloc((size_t)sell_total);
+        f.scv.alloc((size_t)sell_total);
+        launch_sell_fill(f.rp.p, f.ci.p, f.cv.p, f.n, f.so.p, f.sci.p,
+                         f.scv.p, cx.stream);
+    } else {
+        f.so.release();
+    }
 }
 
 void load_features(const svm_matrix* M, Features& f, Context& cx)
@@ -152,8 +167,13 @@ void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
     const int64_t row = c.ldc * (int64_t)sizeof(float);
     size_t free_b = 0, total_b = 0;
     HIP_TRY(hipMemGetInfo(&free_b, &total_b));
+    // default: a quarter of the free memory, at most 8 GiB; an explicit
+    // budget may use the free memory but 2 GiB (left to the caller)
     int64_t cap = std::min<int64_t>((int64_t)(free_b / 4), (int64_t)8 << 30);
-    if (bytes > 0) cap = std::min<int64_t>(cap, bytes);
+    if (bytes > 0)
+        cap = std::min<int64_t>(bytes,
+                                std::max<int64_t>((int64_t)free_b -
+                                                      ((int64_t)2 << 30), 0));
     const int64_t slots = std::min<int64_t>(n, cap / row);
     // a working set reads up to kMaxQ slots and the replacement needs a
     // free one besides them
@@ -285,6 +305,9 @@ int Solver::csr_cols(int nbc) const
 
 void Solver::set_csr(RowArgs& a, int nbc) const
 {
+    a.so = f_.so.p;
+    a.sci = f_.sci.p;
+    a.scv = f_.scv.p;
     a.csr_cols = csr_cols(nbc);
     a.xsc_cols = xsc_cols_.p;
     a.xsc = xsc_.p;

@@ -92,6 +92,11 @@ struct Features {
     DevBuf<int64_t> rp;
     DevBuf<int32_t> ci;
     DevBuf<float> cv;
+    // the rows again, sliced by kSellRows for the row kernel (empty when the
+    // row lengths are so uneven that the padding would pass 4 x nnz)
+    DevBuf<int64_t> so;
+    DevBuf<int32_t> sci;
+    DevBuf<float> scv;
 };
 
 // Uploads X (host or device) into the padded layout and computes norms.

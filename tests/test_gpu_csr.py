@@ -65,6 +65,32 @@ def test_kernel_rows_csr(n, d, seed):
         assert K[j, i] == 1.0
 
 
+def test_kernel_rows_csr_skewed_rows():
+    # every 16th row holds 600 nonzeros, the others 1: padding the rows to
+    # their slice's longest would pass 4 x nnz, so the row kernel walks the
+    # CSR rows themselves (the other tests take the sliced copy)
+    rng = np.random.default_rng(7)
+    n, d = 160, 1000
+    rows, cols = [], []
+    for i in range(n):
+        k = 600 if i % 16 == 0 else 1
+        rows.append(np.full(k, i))
+        cols.append(np.sort(rng.choice(d, size=k, replace=False)))
+    r, c = np.concatenate(rows), np.concatenate(cols)
+    v = (0.1 * rng.standard_normal(r.size)).astype(np.float32)
+    X = sp.csr_matrix((v, (r, c)), shape=(n, d), dtype=np.float32)
+    X.sort_indices()
+    y = np.where(np.arange(n) % 2 == 0, 1.0, -1.0).astype(np.float32)
+    gamma = 0.05
+    s = nv.Solver(X, y, type=C_SVC, C=1.0, gamma=gamma, tol=1e-3)
+    idx = np.array([0, 1, 16, 17, 31, 32, 63, 64, 100, 128, 144, 159,
+                    2, 48, 80, 96])
+    K = s.rows(idx)
+    ref = oracle.kernel_rows(X, gamma, idx)
+    err = np.abs(K - ref) - (1e-5 * np.abs(ref) + 1e-12)
+    assert np.max(err) <= 0, np.max(np.abs(K - ref) / (np.abs(ref) + 1e-30))
+
+
 def _check(w, m, ref, p):
     info = m.info()
     assert info["status"] == nv.SVM_OK
