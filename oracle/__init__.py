@@ -24,6 +24,11 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 C_SVC = 0
 EPS_SVR = 1
+# kernels (Section 3's list, e1071 parameterisation)
+LINEAR = 0
+POLY = 1
+RBF = 2
+SIGMOID = 3
 
 
 def build(force: bool = True) -> str:
@@ -46,7 +51,9 @@ class _Mat(ct.Structure):
 class _Params(ct.Structure):
     _fields_ = [("type", ct.c_int32), ("C", ct.c_double), ("eps", ct.c_double),
                 ("gamma", ct.c_double), ("tol", ct.c_double),
-                ("max_iter", ct.c_int64), ("threads", ct.c_int32)]
+                ("max_iter", ct.c_int64), ("threads", ct.c_int32),
+                ("kernel", ct.c_int32), ("degree", ct.c_int32),
+                ("coef0", ct.c_double)]
 
 
 class _Result(ct.Structure):
@@ -66,8 +73,8 @@ def _load():
             build(force=False)
         lib = ct.CDLL(_LIB)
         P = ct.POINTER
-        lib.orc_kernel.argtypes = [P(_Mat), P(_Mat), ct.c_double, ct.c_void_p]
-        lib.orc_kernel_rows.argtypes = [P(_Mat), ct.c_double, ct.c_void_p,
+        lib.orc_kernel.argtypes = [P(_Mat), P(_Mat), P(_Params), ct.c_void_p]
+        lib.orc_kernel_rows.argtypes = [P(_Mat), P(_Params), ct.c_void_p,
                                         ct.c_int64, ct.c_int32, ct.c_void_p]
         lib.orc_num_vars.restype = ct.c_int64
         lib.orc_num_vars.argtypes = [ct.c_int32, ct.c_int64]
@@ -88,7 +95,7 @@ def _load():
                                        ct.c_void_p, ct.c_void_p, ct.c_double,
                                        ct.c_int32, ct.c_void_p, P(ct.c_int32)]
         lib.orc_decision.argtypes = [P(_Mat), ct.c_void_p, ct.c_double,
-                                     P(_Mat), ct.c_double, ct.c_int32,
+                                     P(_Mat), P(_Params), ct.c_int32,
                                      ct.c_void_p]
         _lib = lib
     return _lib
@@ -142,11 +149,19 @@ class Params:
     tol: float = 1e-3
     max_iter: int = 0
     threads: int = 0
+    kernel: int = RBF
+    degree: int = 3
+    coef0: float = 0.0
 
     def c(self, d: int) -> _Params:
         g = self.gamma if self.gamma > 0 else 1.0 / d
         return _Params(self.type, self.C, self.eps, g, self.tol,
-                       self.max_iter, self.threads)
+                       self.max_iter, self.threads, self.kernel, self.degree,
+                       self.coef0)
+
+
+def _kparams(gamma: float, kind: int, degree: int, coef0: float) -> _Params:
+    return _Params(C_SVC, 1.0, 0.0, gamma, 1.0, 0, 0, kind, degree, coef0)
 
 
 @dataclass
@@ -173,22 +188,27 @@ def num_vars(type_: int, n: int) -> int:
     return 2 * n if type_ == EPS_SVR else n
 
 
-def kernel(A, B, gamma: float) -> np.ndarray:
+def kernel(A, B, gamma: float, kind: int = RBF, degree: int = 3,
+           coef0: float = 0.0) -> np.ndarray:
     """Full kernel matrix K(a_i, b_j), fp64, by the direct definition."""
     A, B = _as_mat(A), _as_mat(B)
     out = np.empty((A.n, B.n), dtype=np.float64)
-    rc = _load().orc_kernel(ct.byref(A.s), ct.byref(B.s), gamma, _ptr(out))
+    kp = _kparams(gamma, kind, degree, coef0)
+    rc = _load().orc_kernel(ct.byref(A.s), ct.byref(B.s), ct.byref(kp),
+                            _ptr(out))
     assert rc == 0
     return out
 
 
-def kernel_rows(X, gamma: float, idx, threads: int = 0) -> np.ndarray:
+def kernel_rows(X, gamma: float, idx, threads: int = 0, kind: int = RBF,
+                degree: int = 3, coef0: float = 0.0) -> np.ndarray:
     """Kernel rows K(x_idx[j], X) -> (len(idx), n) fp64."""
     X = _as_mat(X)
     idx = np.ascontiguousarray(idx, dtype=np.int64)
     out = np.empty((len(idx), X.n), dtype=np.float64)
-    rc = _load().orc_kernel_rows(ct.byref(X.s), gamma, _ptr(idx), len(idx),
-                                 threads, _ptr(out))
+    kp = _kparams(gamma, kind, degree, coef0)
+    rc = _load().orc_kernel_rows(ct.byref(X.s), ct.byref(kp), _ptr(idx),
+                                 len(idx), threads, _ptr(out))
     assert rc == 0
     return out
 
@@ -276,7 +296,7 @@ def subproblem(X, y, p: Params, alpha, F, B, inner_tol: float,
     if KBB is None:
         sB = sample_of(p.type, X.n, B)
         XB = X.rows(sB)
-        KBB = kernel(XB, XB, p.c(X.d).gamma)
+        KBB = kernel(XB, XB, p.c(X.d).gamma, p.kernel, p.degree, p.coef0)
     KBB = np.ascontiguousarray(KBB, dtype=np.float64)
     out = np.empty(len(B), dtype=np.float64)
     steps = ct.c_int32()
@@ -296,13 +316,15 @@ def coefficients(type_: int, n: int, y, alpha) -> np.ndarray:
     return np.where(np.asarray(y) > 0, 1.0, -1.0) * alpha
 
 
-def decision(SV, coef, b: float, Xt, gamma: float, threads: int = 0):
+def decision(SV, coef, b: float, Xt, gamma: float, threads: int = 0,
+             kind: int = RBF, degree: int = 3, coef0: float = 0.0):
     """D(x) = sum_i coef_i K(sv_i, x) + b, fp64 direct sums."""
     SV, Xt = _as_mat(SV), _as_mat(Xt)
     coef = np.ascontiguousarray(coef, dtype=np.float64)
     out = np.empty(Xt.n, dtype=np.float64)
+    kp = _kparams(gamma, kind, degree, coef0)
     rc = _load().orc_decision(ct.byref(SV.s), _ptr(coef), b, ct.byref(Xt.s),
-                              gamma, threads, _ptr(out))
+                              ct.byref(kp), threads, _ptr(out))
     assert rc == 0
     return out
 
@@ -314,7 +336,8 @@ def model_decision(X, y, p: Params, res: Result, Xt, threads: int = 0):
     sv = np.nonzero(c)[0]
     if len(sv) == 0:
         return np.full(_as_mat(Xt).n, res.b)
-    return decision(X.rows(sv), c[sv], res.b, Xt, p.c(X.d).gamma, threads)
+    return decision(X.rows(sv), c[sv], res.b, Xt, p.c(X.d).gamma, threads,
+                    p.kernel, p.degree, p.coef0)
 
 
 def train_ovr(X, labels, n_classes: int, p: Params):

@@ -8,7 +8,8 @@
  * arXiv 1706.05544, Section 3, Eq. 1 and Eq. 2) and the maximal-violating-
  * pair decomposition of LIBSVM (Chang & Lin 2011, the solver the paper
  * extends).  No blocking, fusion or reordering: kernel values come from the
- * direct definition exp(-gamma * sum (a_k - b_k)^2) in fp64, one pair of
+ * direct definitions in fp64 (RBF: exp(-gamma * sum (a_k - b_k)^2); the
+ * others from the dot product sum a_k b_k), one pair of
  * variables is optimised per step, and the responses F are updated with two
  * full kernel rows per step.  OpenMP parallelism is only over independent
  * rows (each output element is computed by one thread in a fixed order), so
@@ -19,7 +20,10 @@
  * active-set enumeration), tests/test_oracle_invariants.py (constraints, KKT,
  * monotone objective), tests/test_oracle_vs_libsvm.py (scikit-learn's LIBSVM
  * endpoint).  The subproblem and working-set helpers are pinned by
- * tests/test_oracle_select.py.
+ * tests/test_oracle_select.py.  The linear, polynomial and sigmoid kernels
+ * are pinned by tests/test_oracle_kernels.py (scikit-learn's pairwise
+ * kernels, worked numbers, the 2-point closed form and its single step,
+ * the exact QP optimum, LIBSVM's endpoint).
  */
 #include "svm_oracle.h"
 
@@ -75,11 +79,63 @@ static double sqdist(const orc_mat *A, int64_t i, const orc_mat *B, int64_t j)
     return sum;
 }
 
-/* RBF kernel, e1071/LIBSVM parameterisation (Section 3, kernel list). */
-static double rbf(const orc_mat *A, int64_t i, const orc_mat *B, int64_t j,
-                  double gamma)
+/* Dot product of row i of A and row j of B, over the columns in increasing
+ * order (the products of columns only one row holds are zero). */
+static double dotp(const orc_mat *A, int64_t i, const orc_mat *B, int64_t j)
 {
-    return exp(-gamma * sqdist(A, i, B, j));
+    double sum = 0.0;
+    if (!A->csr && !B->csr) {
+        const float *a = A->val + i * A->ld;
+        const float *b = B->val + j * B->ld;
+        for (int64_t k = 0; k < A->d; ++k) sum += (double)a[k] * (double)b[k];
+        return sum;
+    }
+    int64_t pa = 0, ea, pb = 0, eb;
+    if (A->csr) { pa = A->row_ptr[i]; ea = A->row_ptr[i + 1]; } else { ea = A->d; }
+    if (B->csr) { pb = B->row_ptr[j]; eb = B->row_ptr[j + 1]; } else { eb = B->d; }
+    while (pa < ea && pb < eb) {
+        const int64_t ca = A->csr ? A->col[pa] : pa;
+        const int64_t cb = B->csr ? B->col[pb] : pb;
+        if (ca == cb) {
+            const double va = A->csr ? (double)A->val[pa]
+                                     : (double)A->val[i * A->ld + pa];
+            const double vb = B->csr ? (double)B->val[pb]
+                                     : (double)B->val[j * B->ld + pb];
+            sum += va * vb;
+            ++pa;
+            ++pb;
+        } else if (ca < cb) {
+            ++pa;
+        } else {
+            ++pb;
+        }
+    }
+    return sum;
+}
+
+/* The kernel of p, e1071/LIBSVM parameterisation (Section 3, kernel list). */
+static double kval(const orc_params *p, const orc_mat *A, int64_t i,
+                   const orc_mat *B, int64_t j)
+{
+    switch (p->kernel) {
+    case ORC_LINEAR:
+        return dotp(A, i, B, j);
+    case ORC_POLY:
+        return pow(p->gamma * dotp(A, i, B, j) + p->coef0, (double)p->degree);
+    case ORC_SIGMOID:
+        return tanh(p->gamma * dotp(A, i, B, j) + p->coef0);
+    default:
+        return exp(-p->gamma * sqdist(A, i, B, j));
+    }
+}
+
+static int check_kernel(const orc_params *p)
+{
+    if (!p || p->kernel < ORC_LINEAR || p->kernel > ORC_SIGMOID) return 0;
+    if (p->kernel != ORC_LINEAR && !(p->gamma > 0)) return 0;
+    if (p->kernel == ORC_POLY && p->degree < 1) return 0;
+    if (!isfinite(p->coef0)) return 0;
+    return 1;
 }
 
 static void set_threads(int32_t threads)
@@ -91,25 +147,26 @@ static void set_threads(int32_t threads)
 #endif
 }
 
-int orc_kernel(const orc_mat *A, const orc_mat *B, double gamma, double *out)
+int orc_kernel(const orc_mat *A, const orc_mat *B, const orc_params *p,
+               double *out)
 {
-    if (!A || !B || !out || A->d != B->d) return ORC_EINVAL;
+    if (!A || !B || !out || A->d != B->d || !check_kernel(p)) return ORC_EINVAL;
     for (int64_t i = 0; i < A->n; ++i)
         for (int64_t j = 0; j < B->n; ++j)
-            out[i * B->n + j] = rbf(A, i, B, j, gamma);
+            out[i * B->n + j] = kval(p, A, i, B, j);
     return ORC_OK;
 }
 
-int orc_kernel_rows(const orc_mat *X, double gamma, const int64_t *idx,
+int orc_kernel_rows(const orc_mat *X, const orc_params *p, const int64_t *idx,
                     int64_t q, int32_t threads, double *out)
 {
-    if (!X || !idx || !out) return ORC_EINVAL;
+    if (!X || !idx || !out || !check_kernel(p)) return ORC_EINVAL;
     set_threads(threads);
     for (int64_t j = 0; j < q; ++j) {
         int64_t s = idx[j];
         double *row = out + j * X->n;
 #pragma omp parallel for schedule(static)
-        for (int64_t r = 0; r < X->n; ++r) row[r] = rbf(X, s, X, r, gamma);
+        for (int64_t r = 0; r < X->n; ++r) row[r] = kval(p, X, s, X, r);
     }
     return ORC_OK;
 }
@@ -250,7 +307,7 @@ int orc_state_summary(int64_t n, const float *y, const orc_params *p,
 static int check_params(const orc_mat *X, const float *y, const orc_params *p)
 {
     if (!X || !y || !p || X->n < 1 || X->d < 1) return ORC_EINVAL;
-    if (!(p->C > 0) || !(p->gamma > 0) || !(p->tol > 0) || !(p->eps >= 0))
+    if (!(p->C > 0) || !(p->tol > 0) || !(p->eps >= 0) || !check_kernel(p))
         return ORC_EINVAL;
     if (p->type != ORC_C_SVC && p->type != ORC_EPS_SVR) return ORC_EINVAL;
     return ORC_OK;
@@ -284,9 +341,12 @@ int orc_solve(const orc_mat *X, const float *y, const orc_params *p,
 
         const int64_t si = smp(p->type, n, i), sj = smp(p->type, n, j);
         const double yi = yv(p->type, n, y, i), yj = yv(p->type, n, y, j);
-        /* second derivative along the pair direction (K_ii = K_jj = 1) */
-        double kij = (si == sj) ? 1.0 : rbf(X, si, X, sj, p->gamma);
-        double a = 1.0 + 1.0 - 2.0 * kij;
+        /* second derivative along the pair direction, K_ii + K_jj - 2 K_ij
+         * (0 for the two copies of one sample) */
+        double a = 0.0;
+        if (si != sj)
+            a = kval(p, X, si, X, si) + kval(p, X, sj, X, sj) -
+                2.0 * kval(p, X, si, X, sj);
         if (a <= 0.0) a = TAU;
         double s = (m - M) / a;
         /* largest feasible move of each variable */
@@ -304,8 +364,8 @@ int orc_solve(const orc_mat *X, const float *y, const orc_params *p,
         if (si != sj) {
 #pragma omp parallel for schedule(static)
             for (int64_t r = 0; r < n; ++r) {
-                Ki[r] = rbf(X, si, X, r, p->gamma);
-                Kj[r] = rbf(X, sj, X, r, p->gamma);
+                Ki[r] = kval(p, X, si, X, r);
+                Kj[r] = kval(p, X, sj, X, r);
             }
             for (int64_t r = 0; r < n; ++r) F[r] += s * (Ki[r] - Kj[r]);
         }
@@ -343,7 +403,7 @@ int orc_responses(const orc_mat *X, const float *y, const orc_params *p,
         for (int64_t t = 0; t < N; ++t) {
             if (alpha[t] == 0.0) continue;
             acc += yv(p->type, n, y, t) * alpha[t] *
-                   rbf(X, r, X, smp(p->type, n, t), p->gamma);
+                   kval(p, X, r, X, smp(p->type, n, t));
         }
         F[r] = acc;
     }
@@ -467,15 +527,17 @@ int orc_subproblem(int64_t n, const float *y, const orc_params *p,
 /* ---------------------------------------------------------------------- */
 
 int orc_decision(const orc_mat *SV, const double *coef, double b,
-                 const orc_mat *Xt, double gamma, int32_t threads, double *out)
+                 const orc_mat *Xt, const orc_params *p, int32_t threads,
+                 double *out)
 {
-    if (!SV || !coef || !Xt || !out || SV->d != Xt->d) return ORC_EINVAL;
+    if (!SV || !coef || !Xt || !out || SV->d != Xt->d || !check_kernel(p))
+        return ORC_EINVAL;
     set_threads(threads);
 #pragma omp parallel for schedule(static)
     for (int64_t r = 0; r < Xt->n; ++r) {
         double acc = 0.0;
         for (int64_t s = 0; s < SV->n; ++s)
-            acc += coef[s] * rbf(SV, s, Xt, r, gamma);
+            acc += coef[s] * kval(p, SV, s, Xt, r);
         out[r] = acc + b;
     }
     return ORC_OK;

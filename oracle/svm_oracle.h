@@ -17,8 +17,13 @@
  *     copy"), copy (i,+) has y = +1 and p = eps - z_i, copy (i,-) has
  *     y = -1 and p = eps + z_i (Eq. 1 substituted into Eq. 2; the only
  *     assignment under which a free positive copy lies on f(x) = z - eps);
- *   - RBF kernel K(a,b) = exp(-gamma * sum_k (a_k - b_k)^2)  (Section 3,
- *     "radial basis function", e1071 parameterisation).
+ *   - the four kernels of Section 3's feature list, in the e1071 (LIBSVM)
+ *     parameterisation the paper's interface follows (the paper names them
+ *     without formulas):
+ *       linear      K(a,b) = a.b
+ *       polynomial  K(a,b) = (gamma a.b + coef0)^degree
+ *       RBF         K(a,b) = exp(-gamma * sum_k (a_k - b_k)^2)
+ *       sigmoid     K(a,b) = tanh(gamma a.b + coef0)
  *
  * Solver: maximal-violating-pair SMO (Chang & Lin 2011, cited in Section 1
  * and Section 3 for Eq. 1), no shrinking, kernel values from the direct
@@ -51,6 +56,7 @@ typedef struct {
 } orc_mat;
 
 enum { ORC_C_SVC = 0, ORC_EPS_SVR = 1 };
+enum { ORC_LINEAR = 0, ORC_POLY = 1, ORC_RBF = 2, ORC_SIGMOID = 3 };
 enum { ORC_OK = 0, ORC_MAX_ITER = 1, ORC_EINVAL = -1 };
 
 typedef struct {
@@ -58,6 +64,9 @@ typedef struct {
     double C, eps, gamma, tol;
     int64_t max_iter;   /* <= 0: max(1e7, 100*N) */
     int32_t threads;    /* OpenMP threads for kernel rows (<=0: default) */
+    int32_t kernel;     /* ORC_LINEAR, ORC_POLY, ORC_RBF or ORC_SIGMOID */
+    int32_t degree;     /* polynomial degree (>= 1) */
+    double coef0;       /* polynomial and sigmoid offset */
 } orc_params;
 
 typedef struct {
@@ -71,11 +80,13 @@ typedef struct {
     int32_t status;     /* ORC_OK or ORC_MAX_ITER */
 } orc_result;
 
-/* out[i*B->n + j] = K(a_i, b_j) for all pairs. */
-int orc_kernel(const orc_mat *A, const orc_mat *B, double gamma, double *out);
+/* out[i*B->n + j] = K(a_i, b_j) for all pairs (kernel, gamma, degree and
+ * coef0 of p). */
+int orc_kernel(const orc_mat *A, const orc_mat *B, const orc_params *p,
+               double *out);
 
 /* out[j*X->n + r] = K(x_idx[j], x_r): q kernel rows against the whole set. */
-int orc_kernel_rows(const orc_mat *X, double gamma, const int64_t *idx,
+int orc_kernel_rows(const orc_mat *X, const orc_params *p, const int64_t *idx,
                     int64_t q, int32_t threads, double *out);
 
 /* Number of dual variables: n (C-SVC) or 2n (eps-SVR). */
@@ -119,7 +130,7 @@ int orc_subproblem(int64_t n, const float *y, const orc_params *p,
 
 /* Decision values D(x) = sum_i coef_i K(sv_i, x) + b, summed in fp64. */
 int orc_decision(const orc_mat *SV, const double *coef, double b,
-                 const orc_mat *Xt, double gamma, int32_t threads,
+                 const orc_mat *Xt, const orc_params *p, int32_t threads,
                  double *out);
 
 #ifdef __cplusplus
