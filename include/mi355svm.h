@@ -2,15 +2,16 @@
  * mi355svm.h -- C ABI of a kernel-SVM dual solver for one AMD Instinct
  * MI355X (gfx950).
  *
- * The library trains C-SVC and eps-SVR models with the RBF kernel by the
- * working-set decomposition of Wang et al., "Rgtsvm: Support Vector Machines
- * on a GPU in R" (arXiv 1706.05544), and evaluates their decision function.
+ * The library trains C-SVC and eps-SVR models with the linear, polynomial,
+ * RBF or sigmoid kernel by the working-set decomposition of Wang et al.,
+ * "Rgtsvm: Support Vector Machines on a GPU in R" (arXiv 1706.05544), and
+ * evaluates their decision function.
  * Everything that computes runs in hand-written HIP kernels; this header
  * only moves pointers and sizes.
  *
  * Problem (Section 3, Eq. 2):
  *     min_a  1/2 a^T Q a + p^T a   s.t.  y^T a = 0,  0 <= a_t <= C,
- *     Q_ts = y_t y_s K(x_smp(t), x_smp(s)),  K(u,v) = exp(-gamma |u - v|^2).
+ *     Q_ts = y_t y_s K(x_smp(t), x_smp(s)),  K one of the kernels below.
  *   C-SVC:   one variable per sample, y_t = label in {+1,-1}, p_t = -1.
  *   eps-SVR: two variables per sample (Section 3, "positive and negative
  *            copy"; Eq. 1): copy (i,+) with y = +1, p = eps - z_i and copy
@@ -52,8 +53,15 @@ typedef enum {
 
 typedef enum { SVM_C_SVC = 0, SVM_EPS_SVR = 1 } svm_type;
 
-/* Section 3 lists four kernels; RBF is implemented, the others return
- * SVM_E_UNSUPPORTED. */
+/* The four kernels of Section 3's list, in the e1071 (LIBSVM)
+ * parameterisation (the paper names them without formulas):
+ *   linear      K(u,v) = u.v
+ *   polynomial  K(u,v) = (gamma u.v + coef0)^degree
+ *   RBF         K(u,v) = exp(-gamma |u - v|^2)
+ *   sigmoid     K(u,v) = tanh(gamma u.v + coef0)
+ * Kernel values are computed in fp32 from an fp32 dot product; the
+ * sigmoid kernel is not positive semidefinite in general (a pair of
+ * non-positive curvature gets the floor 1e-12, as in LIBSVM). */
 typedef enum {
     SVM_KERNEL_LINEAR = 0,
     SVM_KERNEL_POLY = 1,
@@ -97,6 +105,8 @@ typedef struct {
                               global gap, tol/2); 0: 0.3 */
     int32_t max_inner;     /* subproblem step cap; 0: 8 q */
     int32_t profile;       /* 1: time the row/update kernel with events */
+    double coef0;          /* polynomial and sigmoid offset (finite; 0) */
+    int32_t degree;        /* polynomial degree, in [1, 64] (3) */
 } svm_params;
 
 /* Per-output statistics of a trained model. */
@@ -107,6 +117,9 @@ typedef struct {
     int64_t n_features;
     int64_t n_sv;          /* support rows stored (union over outputs) */
     double gamma;          /* resolved gamma */
+    int32_t kernel;        /* svm_kernel of the model */
+    int32_t degree;        /* its polynomial degree */
+    double coef0;          /* its polynomial / sigmoid offset */
     /* the rest refers to the output asked for */
     int32_t status;        /* SVM_OK or SVM_W_MAX_ITER */
     int64_t n_sv_output;   /* samples with non-zero coefficient */
@@ -132,8 +145,8 @@ typedef struct {
 
 typedef struct svm_model svm_model;  /* opaque, owned by the library */
 
-/* Defaults: C-SVC, RBF, C = 1, eps = 0.1, gamma = 0 (1/d), tol = 1e-3,
- * working_set = 16, device 0, NULL stream. */
+/* Defaults: C-SVC, RBF, C = 1, eps = 0.1, gamma = 0 (1/d), coef0 = 0,
+ * degree = 3, tol = 1e-3, working_set = 16, device 0, NULL stream. */
 void svm_params_default(svm_params *p);
 
 /* Train a binary C-SVC (y = labels, each +1 or -1, both present) or an

@@ -26,11 +26,12 @@ svm_status check_params(const svm_params* p)
     if (!p) return fail(SVM_E_INVALID, "params is NULL");
     if (p->type != SVM_C_SVC && p->type != SVM_EPS_SVR)
         return fail(SVM_E_INVALID, "type must be SVM_C_SVC or SVM_EPS_SVR");
-    if (p->kernel != SVM_KERNEL_RBF) {
-        if (p->kernel >= SVM_KERNEL_LINEAR && p->kernel <= SVM_KERNEL_SIGMOID)
-            return fail(SVM_E_UNSUPPORTED, "only the RBF kernel is implemented");
+    if (p->kernel < SVM_KERNEL_LINEAR || p->kernel > SVM_KERNEL_SIGMOID)
         return fail(SVM_E_INVALID, "unknown kernel");
-    }
+    if (!std::isfinite(p->coef0))
+        return fail(SVM_E_INVALID, "coef0 must be finite");
+    if (p->kernel == SVM_KERNEL_POLY && (p->degree < 1 || p->degree > 64))
+        return fail(SVM_E_INVALID, "degree must be in [1, 64]");
     if (!finite_pos(p->C)) return fail(SVM_E_INVALID, "C must be finite and > 0");
     if (!std::isfinite(p->epsilon) || p->epsilon < 0)
         return fail(SVM_E_INVALID, "epsilon must be finite and >= 0");
@@ -112,6 +113,9 @@ void fill_info(svm_model_info& in, const svm_model& m,
     in.n_train = m.n_train;
     in.n_features = m.d;
     in.gamma = m.gamma;
+    in.kernel = m.kf.kind;
+    in.degree = m.kf.degree;
+    in.coef0 = m.coef0;
     in.status = r.status;
     in.n_sv_output = r.n_sv;
     in.n_bounded = r.n_bounded;
@@ -191,6 +195,8 @@ void svm_params_default(svm_params* p)
     p->inner_ratio = 0.0;
     p->max_inner = 0;
     p->profile = 0;
+    p->coef0 = 0.0;
+    p->degree = 3;
 }
 
 svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
@@ -227,7 +233,8 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
     m->d = X->d;
     m->ldp = f.ldp;
     m->gamma = o.gamma;
-    m->gexp = (float)(o.gamma * 1.4426950408889634);
+    m->kf = msvm::kernel_fn(o);
+    m->coef0 = o.coef0;
     m->device = p->device;
     m->b.assign(1, r.b);
     msvm::DevBuf<double> coef((size_t)X->n);
@@ -299,7 +306,8 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     m->d = X->d;
     m->ldp = f.ldp;
     m->gamma = o.gamma;
-    m->gexp = (float)(o.gamma * 1.4426950408889634);
+    m->kf = msvm::kernel_fn(o);
+    m->coef0 = o.coef0;
     m->device = p->device;
     m->b.assign((size_t)n_classes, 0.0);
     m->alpha.resize((size_t)n_classes);

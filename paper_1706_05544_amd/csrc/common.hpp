@@ -102,6 +102,18 @@ enum : int32_t {
     SS_SET_ALPHA = 16   // alpha_B taken from ws->alphaB instead of solved
 };
 
+// The kernel function (Section 3's list, e1071 parameterisation):
+// kind = svm_kernel; RBF exp(-gamma |u - v|^2) = 2^(-gexp |u - v|^2) with
+// gexp = gamma log2(e); linear u.v; polynomial (gamma u.v + coef0)^degree;
+// sigmoid tanh(gamma u.v + coef0).
+struct KernelFn {
+    int32_t kind;
+    int32_t degree;
+    float gexp;
+    float gamma;
+    float coef0;
+};
+
 struct RowArgs {
     const float* X;       // dense rows, or nullptr for CSR
     const int64_t* rp;    // CSR rows (rp == nullptr: dense)
@@ -131,7 +143,7 @@ struct RowArgs {
     int64_t ldc;
     int64_t n, ldp;
     double eps;
-    float gexp;           // gamma * log2(e)
+    KernelFn kf;
     int32_t half;
     int32_t tiles;        // 16-row tiles per wave
     int32_t mode;
@@ -158,7 +170,7 @@ struct SelArgs {
     int32_t csr_cols;
     int64_t n, ldp;
     double C, eps, tol;
-    float gexp;
+    KernelFn kf;
     double inner_ratio;
     double inner_tol_override;  // >= 0: fixed inner tolerance (tests)
     int32_t max_inner;
@@ -188,7 +200,7 @@ struct PredictArgs {
     int32_t self_match;
     int64_t row_base;     // training-set index of query row 0 (self_match)
     double* out;          // m x n_out
-    float gexp;
+    KernelFn kf;
     // sparse path: CSR query rows, and the support rows by column in
     // chunks of 16 (chunk k: support rows 16k .. 16k + 15)
     const int64_t* rpt;

@@ -51,6 +51,48 @@ __device__ __forceinline__ float rbf_from_dot(float sa, float sb, float dot,
     return __builtin_amdgcn_exp2f(-gexp * d2);
 }
 
+// b^e for an integer e >= 1 by binary exponentiation (the same product
+// order wherever a kernel value is computed)
+__device__ __forceinline__ float powi_f32(float b, int e)
+{
+    float r = 1.0f;
+    while (e > 0) {
+        if (e & 1) r *= b;
+        b *= b;
+        e >>= 1;
+    }
+    return r;
+}
+
+// Kernel value of a pair from its dot product for the kernels other than
+// RBF (linear, polynomial, sigmoid).
+__device__ __forceinline__ float kernel_of_dot(const KernelFn& kf, float dot)
+{
+    if (kf.kind == SVM_KERNEL_LINEAR) return dot;
+    const float t = fmaf(kf.gamma, dot, kf.coef0);
+    if (kf.kind == SVM_KERNEL_POLY) return powi_f32(t, kf.degree);
+    return tanhf(t);
+}
+
+// Kernel value of a pair from its dot product and squared norms (the norms
+// enter the RBF kernel only).  kf.kind is uniform over a launch; the hot
+// loops test it once around a whole tile (kf.kind == SVM_KERNEL_RBF ?
+// rbf_from_dot : kernel_of_dot) instead of per value.
+__device__ __forceinline__ float kernel_from_dot(const KernelFn& kf, float sa,
+                                                 float sb, float dot)
+{
+    if (kf.kind == SVM_KERNEL_RBF) return rbf_from_dot(sa, sb, dot, kf.gexp);
+    return kernel_of_dot(kf, dot);
+}
+
+// K(x, x) := 1 exactly for the RBF kernel when both sides are the same
+// training row (its expansion |x|^2 + |x|^2 - 2 x.x cancels in fp32 to a
+// small non-zero); the other kernels have no cancellation there.
+__device__ __forceinline__ bool kernel_self_is_one(const KernelFn& kf)
+{
+    return kf.kind == SVM_KERNEL_RBF;
+}
+
 // Order "largest key first, lowest index on ties".
 __device__ __forceinline__ bool better(double k1, int32_t i1, double k2,
                                        int32_t i2)

@@ -83,13 +83,23 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
 #pragma unroll
             for (int o = 0; o < NOUT; ++o)
                 cf[o] = (ok && o < n_out) ? a.coef[sv * n_out + o] : 0.0;
+            float kv[4];
+            if (a.kf.kind == SVM_KERNEL_RBF) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    kv[v] = rbf_from_dot(sqr[v], ssv, acc[cb][v], a.kf.gexp);
+                    if (st == rid[v] + a.row_base) kv[v] = 1.0f;
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    kv[v] = kernel_of_dot(a.kf, acc[cb][v]);
+            }
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                float kv = rbf_from_dot(sqr[v], ssv, acc[cb][v], a.gexp);
-                if (st == rid[v] + a.row_base) kv = 1.0f;
 #pragma unroll
                 for (int o = 0; o < NOUT; ++o)
-                    part[o][v] = fma(cf[o], (double)kv, part[o][v]);
+                    part[o][v] = fma(cf[o], (double)kv[v], part[o][v]);
             }
         }
     }
@@ -369,13 +379,22 @@ __global__ __launch_bounds__(kSpThreads) void k_predict_sparse(PredictArgs a)
         const float* sq = sq_of(p);
         const int32_t* tix = tix_of(p);
         const double* cf = coef_of(p);
+        float kv[16];
+        if (a.kf.kind == SVM_KERNEL_RBF) {
+#pragma unroll
+            for (int s = 0; s < 16; ++s) {
+                kv[s] = rbf_from_dot(sqr, sq[s], acc[s], a.kf.gexp);
+                if ((int64_t)tix[s] == self) kv[s] = 1.0f;
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < 16; ++s) kv[s] = kernel_of_dot(a.kf, acc[s]);
+        }
 #pragma unroll
         for (int s = 0; s < 16; ++s) {
-            float kv = rbf_from_dot(sqr, sq[s], acc[s], a.gexp);
-            if ((int64_t)tix[s] == self) kv = 1.0f;
 #pragma unroll
             for (int o = 0; o < NOUT; ++o)
-                outv[o] = fma(cf[s * NOUT + o], (double)kv, outv[o]);
+                outv[o] = fma(cf[s * NOUT + o], (double)kv[s], outv[o]);
         }
         __syncthreads();
     }

@@ -610,12 +610,18 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                             if (kb >= mx) break;
                         }
                         float kv[QS];
+                        if (a.kf.kind == SVM_KERNEL_RBF) {
 #pragma unroll
-                        for (int q = 0; q < QS; ++q) {
-                            float k = rbf_from_dot(rd.q, sl_sq[q], acc[q],
-                                                   a.gexp);
-                            if (rw0 + r == (int64_t)sl_smp[q]) k = 1.0f;
-                            kv[q] = k;
+                            for (int q = 0; q < QS; ++q) {
+                                float k = rbf_from_dot(rd.q, sl_sq[q], acc[q],
+                                                       a.kf.gexp);
+                                if (rw0 + r == (int64_t)sl_smp[q]) k = 1.0f;
+                                kv[q] = k;
+                            }
+                        } else {
+#pragma unroll
+                            for (int q = 0; q < QS; ++q)
+                                kv[q] = kernel_of_dot(a.kf, acc[q]);
                         }
                         finish_row(r, rv, kv, rd);
                     }
@@ -809,17 +815,31 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                                 *reinterpret_cast<const float4*>(sqw + lr);
                             const float qv[4] = {q4v.x, q4v.y, q4v.z, q4v.w};
                             float kv[NBLK][4];
+                            if (a.kf.kind == SVM_KERNEL_RBF) {
+#pragma unroll
+                                for (int b = 0; b < NBLK; ++b) {
+                                    const float ssb = sl_sq[b * 16 + nl];
+                                    const int32_t smb = sl_smp[b * 16 + nl];
+#pragma unroll
+                                    for (int v = 0; v < 4; ++v) {
+                                        float k = rbf_from_dot(qv[v], ssb,
+                                                               acc[b][v],
+                                                               a.kf.gexp);
+                                        if (rw0 + lr + v == (int64_t)smb)
+                                            k = 1.0f;
+                                        kv[b][v] = k;
+                                    }
+                                }
+                            } else {
+#pragma unroll
+                                for (int b = 0; b < NBLK; ++b)
+#pragma unroll
+                                    for (int v = 0; v < 4; ++v)
+                                        kv[b][v] = kernel_of_dot(a.kf,
+                                                                 acc[b][v]);
+                            }
 #pragma unroll
                             for (int b = 0; b < NBLK; ++b) {
-                                const float ssb = sl_sq[b * 16 + nl];
-                                const int32_t smb = sl_smp[b * 16 + nl];
-#pragma unroll
-                                for (int v = 0; v < 4; ++v) {
-                                    float k = rbf_from_dot(qv[v], ssb,
-                                                           acc[b][v], a.gexp);
-                                    if (rw0 + lr + v == (int64_t)smb) k = 1.0f;
-                                    kv[b][v] = k;
-                                }
                                 // rows lr .. lr+3 of a row stored padded to
                                 // ldc (a multiple of 4): in bounds when row
                                 // lr is

@@ -905,13 +905,13 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
         for (int e = tid; e < nS * nS; e += kSelThreads) {
             const int ia = e / nS, ib = e - ia * nS;
             float k = 1.0f;
-            if (ia != ib) {
+            if (ia != ib || !kernel_self_is_one(a.kf)) {
                 float acc = 0.0f;
                 for (int r = 0; r < E; ++r)
                     acc = fmaf(tab[r * QS + ia], tab[r * QS + ib], acc);
                 const float qa = e == tid ? sqa : a.sq[shS[ia]];
                 const float qb = e == tid ? sqb : a.sq[shS[ib]];
-                k = rbf_from_dot(qa, qb, acc, a.gexp);
+                k = kernel_from_dot(a.kf, qa, qb, acc);
             }
             KSS[ia][ib] = k;
         }
@@ -1027,9 +1027,10 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
             for (int vv = 0; vv < 4; ++vv) {
                 const int ia = bi * 16 + 4 * g + vv, ib = bj * 16 + nl;
                 if (ia < nS && ib < nS)
-                    KSS[ia][ib] = ia == ib ? 1.0f
-                                           : rbf_from_dot(sqa[vv], sqb, acc[vv],
-                                                          a.gexp);
+                    KSS[ia][ib] = (ia == ib && kernel_self_is_one(a.kf))
+                                      ? 1.0f
+                                      : kernel_from_dot(a.kf, sqa[vv], sqb,
+                                                        acc[vv]);
             }
             if (bi == 0 && g == 0 && vb) shsS[sb] = sqb;
         }

@@ -138,6 +138,9 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
     o.type = p->type;
     o.C = p->C;
     o.eps = p->type == SVM_EPS_SVR ? p->epsilon : 0.0;
+    o.kernel = p->kernel;
+    o.degree = p->kernel == SVM_KERNEL_POLY ? p->degree : 1;
+    o.coef0 = p->coef0;
     o.gamma = p->gamma > 0 ? p->gamma : 1.0 / (double)d;
     o.tol = p->tol;
     const int64_t N = p->type == SVM_EPS_SVR ? 2 * n : n;
@@ -151,6 +154,17 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
     o.max_inner = p->max_inner > 0 ? p->max_inner : 8 * p->working_set;
     o.profile = p->profile != 0;
     return o;
+}
+
+KernelFn kernel_fn(const SolveOptions& o)
+{
+    KernelFn k{};
+    k.kind = o.kernel;
+    k.degree = o.degree;
+    k.gexp = (float)(o.gamma * 1.4426950408889634);  // gamma log2(e)
+    k.gamma = (float)o.gamma;
+    k.coef0 = (float)o.coef0;
+    return k;
 }
 
 // ---------------------------------------------------------------------------
@@ -197,7 +211,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
 {
     n_ = f.n;
     N_ = o.type == SVM_EPS_SVR ? 2 * n_ : n_;
-    gexp_ = (float)(o.gamma * 1.4426950408889634);
+    kf_ = kernel_fn(o);
     half_ = o.q / 2;
     nblk_cols_ = o.q <= 16 ? 1 : (o.q <= 32 ? 2 : 4);
     // Grid: every block of k_rows resident at once (occupancy from the
@@ -339,7 +353,7 @@ void Solver::launch_keys()
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
-    a.gexp = gexp_;
+    a.kf = kf_;
     a.half = half_;
     a.tiles = tiles_;
     a.mode = RU_CAND;
@@ -366,7 +380,7 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
-    a.gexp = gexp_;
+    a.kf = kf_;
     a.half = half_;
     a.tiles = tiles_;
     a.mode = RU_UPDATE | RU_CAND | RU_CHECK_DONE;
@@ -403,7 +417,7 @@ void Solver::launch_solve(int32_t mode)
     a.C = o_.C;
     a.eps = o_.eps;
     a.tol = o_.tol;
-    a.gexp = gexp_;
+    a.kf = kf_;
     a.inner_ratio = o_.inner_ratio;
     a.inner_tol_override = -1.0;
     a.max_inner = o_.max_inner;
@@ -572,7 +586,7 @@ void Solver::recompute_responses()
     a.sv_train_idx = sv_idx_.p;
     a.self_match = 1;
     a.out = F_.p;
-    a.gexp = gexp_;
+    a.kf = kf_;
     predict_rows(a, f_, s);
 }
 
@@ -758,7 +772,7 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     a.n = n_;
     a.ldp = f_.ldp;
     a.eps = o_.eps;
-    a.gexp = gexp_;
+    a.kf = kf_;
     a.half = half_;
     a.tiles = tiles_;
     a.mode = RU_ROWS;
@@ -804,7 +818,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.C = o_.C;
     a.eps = o_.eps;
     a.tol = o_.tol;
-    a.gexp = gexp_;
+    a.kf = kf_;
     a.inner_ratio = o_.inner_ratio;
     a.inner_tol_override = inner_tol;
     a.max_inner = max_inner;
@@ -851,7 +865,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.C = o_.C;
     a.eps = o_.eps;
     a.tol = o_.tol;
-    a.gexp = gexp_;
+    a.kf = kf_;
     a.inner_ratio = o_.inner_ratio;
     a.inner_tol_override = 0.0;
     a.max_inner = 0;
@@ -878,7 +892,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     r.n = n_;
     r.ldp = f_.ldp;
     r.eps = o_.eps;
-    r.gexp = gexp_;
+    r.kf = kf_;
     r.half = half_;
     r.tiles = tiles_;
     r.mode = RU_UPDATE;
@@ -963,7 +977,7 @@ void predict_device(const svm_model& mdl, Context& cx, const Features& t,
     a.sv_train_idx = nullptr;
     a.self_match = 0;
     a.out = out;
-    a.gexp = mdl.gexp;
+    a.kf = mdl.kf;
     if (mdl.ch_cap > 0) {
         a.ch_ncol = mdl.ch_ncol.p;
         a.ch_cols = mdl.ch_cols.p;

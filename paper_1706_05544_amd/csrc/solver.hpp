@@ -107,7 +107,8 @@ int64_t padded_ld(int64_t d);
 
 struct SolveOptions {
     int32_t type;
-    double C, eps, gamma, tol;
+    int32_t kernel, degree;
+    double C, eps, gamma, coef0, tol;
     int64_t max_iter;
     int32_t q;
     int32_t check_every;
@@ -117,6 +118,9 @@ struct SolveOptions {
 };
 
 SolveOptions make_options(const svm_params* p, int64_t n, int64_t d);
+
+// The kernel of the options as the kernels take it.
+KernelFn kernel_fn(const SolveOptions& o);
 
 // Result of one binary (or SVR) solve.
 struct SolveResult {
@@ -179,7 +183,7 @@ private:
     const Features& f_;
     SolveOptions o_;
     int64_t n_, N_;
-    float gexp_;
+    KernelFn kf_;
     int half_, nblk_cols_, tiles_, nb_;
     DevBuf<double> F_, alpha_;
     DevBuf<uint8_t> st_;
@@ -213,8 +217,8 @@ struct svm_model {
     int32_t type = 0;
     int32_t n_out = 1;
     int64_t n_train = 0, d = 0, ldp = 0;
-    double gamma = 0;
-    float gexp = 0;
+    double gamma = 0, coef0 = 0;
+    msvm::KernelFn kf{};
     int device = 0;
     int64_t n_sv = 0;
     msvm::DevBuf<float> SV, sqsv;

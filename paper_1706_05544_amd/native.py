@@ -64,13 +64,16 @@ class svm_params(ct.Structure):
                 ("device", ct.c_int32), ("cache_bytes", ct.c_int64),
                 ("stream", ct.c_void_p), ("check_every", ct.c_int32),
                 ("inner_ratio", ct.c_double), ("max_inner", ct.c_int32),
-                ("profile", ct.c_int32)]
+                ("profile", ct.c_int32), ("coef0", ct.c_double),
+                ("degree", ct.c_int32)]
 
 
 class svm_model_info(ct.Structure):
     _fields_ = [("type", ct.c_int32), ("n_outputs", ct.c_int32),
                 ("n_train", ct.c_int64), ("n_features", ct.c_int64),
                 ("n_sv", ct.c_int64), ("gamma", ct.c_double),
+                ("kernel", ct.c_int32), ("degree", ct.c_int32),
+                ("coef0", ct.c_double),
                 ("status", ct.c_int32), ("n_sv_output", ct.c_int64),
                 ("n_bounded", ct.c_int64), ("iters", ct.c_int64),
                 ("gap", ct.c_double), ("b", ct.c_double),

@@ -45,9 +45,10 @@ def test_struct_layout_matches_header(tmp_path):
 int main(void) {
   printf("%zu %zu %zu\n", sizeof(svm_matrix), sizeof(svm_params),
          sizeof(svm_model_info));
-  printf("%zu %zu %zu %zu\n", offsetof(svm_params, stream),
+  printf("%zu %zu %zu %zu %zu %zu %zu\n", offsetof(svm_params, stream),
          offsetof(svm_params, profile), offsetof(svm_model_info, train_ms),
-         offsetof(svm_matrix, nnz));
+         offsetof(svm_matrix, nnz), offsetof(svm_params, coef0),
+         offsetof(svm_params, degree), offsetof(svm_model_info, coef0));
   return 0;
 }
 ''')
@@ -62,7 +63,9 @@ int main(void) {
         ct.sizeof(nv.svm_model_info)]
     assert [int(x) for x in b.split()] == [
         nv.svm_params.stream.offset, nv.svm_params.profile.offset,
-        nv.svm_model_info.train_ms.offset, nv.svm_matrix.nnz.offset]
+        nv.svm_model_info.train_ms.offset, nv.svm_matrix.nnz.offset,
+        nv.svm_params.coef0.offset, nv.svm_params.degree.offset,
+        nv.svm_model_info.coef0.offset]
 
 
 def test_params_default():
@@ -70,6 +73,7 @@ def test_params_default():
     assert p.type == nv.SVM_C_SVC and p.kernel == nv.SVM_KERNEL_RBF
     assert p.C == 1.0 and p.epsilon == 0.1 and p.gamma == 0.0
     assert p.tol == 1e-3 and p.working_set == 16 and p.device == 0
+    assert p.coef0 == 0.0 and p.degree == 3
 
 
 def _x(n=8, d=3):
@@ -90,8 +94,12 @@ def _y(n=8):
     (dict(working_set=66), nv.SVM_E_INVALID),
     (dict(working_set=0), nv.SVM_E_INVALID),
     (dict(type=7), nv.SVM_E_INVALID),
-    (dict(kernel=nv.SVM_KERNEL_POLY), nv.SVM_E_UNSUPPORTED),
     (dict(kernel=9), nv.SVM_E_INVALID),
+    (dict(kernel=-1), nv.SVM_E_INVALID),
+    (dict(kernel=nv.SVM_KERNEL_POLY, degree=0), nv.SVM_E_INVALID),
+    (dict(kernel=nv.SVM_KERNEL_POLY, degree=65), nv.SVM_E_INVALID),
+    (dict(kernel=nv.SVM_KERNEL_SIGMOID, coef0=float("inf")),
+     nv.SVM_E_INVALID),
     (dict(inner_ratio=1.5), nv.SVM_E_INVALID),
 ])
 def test_invalid_params(kw, code):
