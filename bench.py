@@ -78,7 +78,8 @@ def measured_traffic(workload: str):
         return None
 
 
-def cpu_baseline(w, target_s: float) -> dict:
+def cpu_baseline(w, target_s: float, kernel: int, gamma: float, degree: int,
+                 coef0: float) -> dict:
     """The oracle (untuned) on a bounded sample: maximal-violating-pair SMO
     steps from alpha = 0 on the full training set; 2 kernel rows per step."""
     import numpy as np
@@ -87,8 +88,9 @@ def cpu_baseline(w, target_s: float) -> dict:
     threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
     if threads <= 0:
         threads = len(os.sched_getaffinity(0))
-    p = oracle.Params(w.type, C=w.C, eps=w.eps, gamma=w.gamma, tol=w.tol,
-                      threads=threads)
+    p = oracle.Params(w.type, C=w.C, eps=w.eps, gamma=gamma, tol=w.tol,
+                      threads=threads, kernel=kernel, degree=degree,
+                      coef0=coef0)
     N = oracle.num_vars(w.type, w.n)
     X = oracle.Matrix(w.X)
     a0 = np.zeros(N)
@@ -123,6 +125,13 @@ def main() -> int:
                     help="feature layout of workloads that offer both "
                          "(C4: dense or csr)")
     ap.add_argument("--working-set", type=int, default=16)
+    ap.add_argument("--kernel", default="rbf",
+                    choices=["linear", "poly", "rbf", "sigmoid"],
+                    help="kernel function (e1071 parameterisation)")
+    ap.add_argument("--gamma", type=float, default=None,
+                    help="kernel gamma (default: the workload's)")
+    ap.add_argument("--degree", type=int, default=3)
+    ap.add_argument("--coef0", type=float, default=0.0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -164,8 +173,13 @@ def main() -> int:
     y = torch.from_numpy(w.y).to(dev)
     Xt = to_device(w.Xt)
     torch.cuda.synchronize()
-    kw = dict(type=w.type, C=w.C, epsilon=w.eps, gamma=w.gamma, tol=w.tol,
-              working_set=args.working_set)
+    kernel = {"linear": nv.SVM_KERNEL_LINEAR, "poly": nv.SVM_KERNEL_POLY,
+              "rbf": nv.SVM_KERNEL_RBF,
+              "sigmoid": nv.SVM_KERNEL_SIGMOID}[args.kernel]
+    gamma = args.gamma if args.gamma is not None else w.gamma
+    kw = dict(type=w.type, C=w.C, epsilon=w.eps, gamma=gamma, tol=w.tol,
+              working_set=args.working_set, kernel=kernel,
+              degree=args.degree, coef0=args.coef0)
 
     multi = w.n_classes > 2
     if multi:
@@ -251,6 +265,10 @@ def main() -> int:
     else:
         quality = {"test_mse": float(np.mean((Dn - w.yt) ** 2))}
 
+    kernel_desc = {"rbf": "RBF", "linear": "linear",
+                   "poly": "polynomial (degree %d, coef0 %g)"
+                           % (args.degree, args.coef0),
+                   "sigmoid": "sigmoid (coef0 %g)" % args.coef0}[args.kernel]
     out = {
         "metric": METRIC,
         "value": rows / wall,
@@ -265,15 +283,17 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "%s: %s RBF, %s n=%d d=%d, C=%g, gamma=%g, "
+            "workload": "%s: %s %s, %s n=%d d=%d, C=%g, gamma=%g, "
                         "tol=%g, q=%d; predict %d points"
                         % (w.name, ("one-vs-rest %d-class C-SVC" % w.n_classes)
                            if multi else
                            ("C-SVC" if w.type == 0 else "eps-SVR"),
+                           kernel_desc,
                            ("CSR (%d nonzeros)" % w.X.nnz)
                            if hasattr(w.X, "indptr") else "dense",
-                           w.n, w.d, w.C, w.gamma, w.tol, args.working_set,
+                           w.n, w.d, w.C, gamma, w.tol, args.working_set,
                            w.Xt.shape[0]),
+            "kernel": args.kernel,
             "n": w.n, "d": w.d, "n_test": int(w.Xt.shape[0]),
             "working_set": args.working_set,
         },
@@ -309,7 +329,8 @@ def main() -> int:
         },
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, kernel, gamma,
+                                           args.degree, args.coef0)
     print(json.dumps(out), flush=True)
     return 0
 
