@@ -348,3 +348,92 @@ def train_ovr(X, labels, n_classes: int, p: Params):
         yc = np.where(labels == c, 1.0, -1.0).astype(np.float32)
         out.append(train(X, yc, p))
     return out
+
+
+# ---------------------------------------------------------------------------
+# Scaling, k-fold cross-validation and metrics (Section 3's feature list:
+# "scaling training data", "K-fold cross validation", "accuracy or
+# correlation, mean square error"), by their definitions in fp64.
+# ---------------------------------------------------------------------------
+
+def scale_stats(X):
+    """Per-column mean and sample standard deviation (n - 1 divisor), fp64.
+    A constant column has sd 0 (it is left as it is)."""
+    A = np.asarray(X, dtype=np.float64)
+    mu = A.mean(axis=0)
+    sd = np.sqrt(((A - mu) ** 2).sum(axis=0) / (A.shape[0] - 1))
+    return mu, sd
+
+
+def scale_apply(X, mu, sd):
+    """(x - mu) / sd per column in fp64, rounded once to fp32; columns with
+    sd 0 unchanged."""
+    A = np.asarray(X, dtype=np.float64)
+    s = np.where(sd > 0, sd, 1.0)
+    m = np.where(sd > 0, mu, 0.0)
+    return ((A - m) / s).astype(np.float32)
+
+
+def train_scaled(X, y, p: Params, Xt):
+    """Training on standardised features (and, for eps-SVR, targets) and the
+    decision values of Xt in the units of the targets: (result, D)."""
+    mu, sd = scale_stats(X)
+    Xs, Xts = scale_apply(X, mu, sd), scale_apply(Xt, mu, sd)
+    ys, y_mu, y_sd = np.asarray(y, np.float32), 0.0, 0.0
+    if p.type == EPS_SVR:
+        (y_mu,), (y_sd,) = scale_stats(np.asarray(y)[:, None])
+        if y_sd > 0:
+            ys = scale_apply(np.asarray(y)[:, None], np.array([y_mu]),
+                             np.array([y_sd]))[:, 0]
+    r = train(Xs, ys, p)
+    D = model_decision(Xs, ys, p, r, Xts)
+    if p.type == EPS_SVR and y_sd > 0:
+        D = D * y_sd + y_mu
+    return r, D
+
+
+def _rows(X, idx):
+    return X[idx] if not hasattr(X, "indptr") else X[idx]
+
+
+def cross_validate(X, y, p: Params, k: int, fold=None, labels=None,
+                   n_classes: int = 0):
+    """Decision values of every row from the model trained on the rows of
+    the other folds (fold[i] in [0, k); None: i mod k).  labels with
+    n_classes: one-vs-rest, D is n x n_classes."""
+    n = X.shape[0]
+    fold = np.arange(n) % k if fold is None else np.asarray(fold)
+    n_out = n_classes if labels is not None else 1
+    D = np.zeros((n, n_out))
+    for f in range(k):
+        tr, te = np.nonzero(fold != f)[0], np.nonzero(fold == f)[0]
+        Xtr, Xte = _rows(X, tr), _rows(X, te)
+        for c in range(n_out):
+            if labels is not None:
+                yc = np.where(np.asarray(labels)[tr] == c, 1.0,
+                              -1.0).astype(np.float32)
+            else:
+                yc = np.asarray(y, np.float32)[tr]
+            r = train(Xtr, yc, p)
+            D[te, c] = model_decision(Xtr, yc, p, r, Xte)
+    return D[:, 0] if n_out == 1 else D
+
+
+def metrics(type_: int, D, y=None, labels=None):
+    """accuracy (C-SVC: D >= 0 is +1; one-vs-rest: argmax, ties to the
+    lowest class), mse and squared correlation (eps-SVR), and the error
+    that tuning minimises (1 - accuracy, or mse)."""
+    D = np.asarray(D, dtype=np.float64)
+    if labels is not None:
+        acc = float(np.mean(np.argmax(D, axis=1) == np.asarray(labels)))
+        return {"accuracy": acc, "error": 1.0 - acc}
+    t = np.asarray(y, dtype=np.float64)
+    if type_ == C_SVC:
+        acc = float(np.mean(np.where(D >= 0, 1.0, -1.0) == t))
+        return {"accuracy": acc, "error": 1.0 - acc}
+    mse = float(np.mean((D - t) ** 2))
+    n = len(t)
+    num = n * (D @ t) - D.sum() * t.sum()
+    den = (n * (D @ D) - D.sum() ** 2) * (n * (t @ t) - t.sum() ** 2)
+    scc = float(num * num / den) if den > 0 else 0.0
+    return {"mse": mse, "scc": scc, "error": mse}

@@ -45,10 +45,13 @@ def test_struct_layout_matches_header(tmp_path):
 int main(void) {
   printf("%zu %zu %zu\n", sizeof(svm_matrix), sizeof(svm_params),
          sizeof(svm_model_info));
-  printf("%zu %zu %zu %zu %zu %zu %zu\n", offsetof(svm_params, stream),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\n",
+         offsetof(svm_params, stream),
          offsetof(svm_params, profile), offsetof(svm_model_info, train_ms),
          offsetof(svm_matrix, nnz), offsetof(svm_params, coef0),
-         offsetof(svm_params, degree), offsetof(svm_model_info, coef0));
+         offsetof(svm_params, degree), offsetof(svm_model_info, coef0),
+         offsetof(svm_params, scale), sizeof(svm_cv_stats),
+         offsetof(svm_cv_stats, error));
   return 0;
 }
 ''')
@@ -65,7 +68,8 @@ int main(void) {
         nv.svm_params.stream.offset, nv.svm_params.profile.offset,
         nv.svm_model_info.train_ms.offset, nv.svm_matrix.nnz.offset,
         nv.svm_params.coef0.offset, nv.svm_params.degree.offset,
-        nv.svm_model_info.coef0.offset]
+        nv.svm_model_info.coef0.offset, nv.svm_params.scale.offset,
+        ct.sizeof(nv.svm_cv_stats), nv.svm_cv_stats.error.offset]
 
 
 def test_params_default():
@@ -101,6 +105,7 @@ def _y(n=8):
     (dict(kernel=nv.SVM_KERNEL_SIGMOID, coef0=float("inf")),
      nv.SVM_E_INVALID),
     (dict(inner_ratio=1.5), nv.SVM_E_INVALID),
+    (dict(scale=2), nv.SVM_E_INVALID),
 ])
 def test_invalid_params(kw, code):
     with pytest.raises(nv.SvmError) as e:
@@ -172,3 +177,26 @@ def test_no_device_is_a_clean_error():
         nv.svm_train(_x(), _y())
     assert e.value.status == nv.SVM_E_DEVICE
     assert "device" in nv.svm_last_error()
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=1), nv.SVM_E_INVALID),
+    (dict(k=9), nv.SVM_E_INVALID),                      # more folds than rows
+    (dict(k=2, fold=[0, 1, 2, 0, 1, 0, 1, 0]), nv.SVM_E_INVALID),
+    (dict(k=3, fold=[0, 1, 0, 1, 0, 1, 0, 1]), nv.SVM_E_INVALID),  # empty fold
+    (dict(k=2, scale=3), nv.SVM_E_INVALID),
+])
+def test_cross_validate_invalid(kw, code):
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_cross_validate(_x(), _y(), **kw)
+    assert e.value.status == code
+
+
+def test_cross_validate_needs_exactly_one_truth():
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_cross_validate(_x(), _y(), labels=np.zeros(8, np.int32),
+                              n_classes=2, k=2)
+    assert e.value.status == nv.SVM_E_INVALID
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_tune(_x(), _y(), k=2, C=[1.0, -1.0])  # C <= 0 in the grid
+    assert e.value.status == nv.SVM_E_INVALID
