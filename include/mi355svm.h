@@ -107,7 +107,25 @@ typedef struct {
     int32_t profile;       /* 1: time the row/update kernel with events */
     double coef0;          /* polynomial and sigmoid offset (finite; 0) */
     int32_t degree;        /* polynomial degree, in [1, 64] (3) */
+    int32_t scale;         /* 1: standardise each feature (and eps-SVR
+                              targets) to mean 0 and sample sd 1 before
+                              training, as e1071 does; dense X only; the
+                              model applies the same statistics to the rows
+                              it predicts (0: inputs used as given) */
 } svm_params;
+
+/* Result of a k-fold cross-validation. */
+typedef struct {
+    int32_t folds;
+    int32_t status;        /* SVM_OK or SVM_W_MAX_ITER (some fold) */
+    int64_t n;             /* rows, each predicted by the model of the folds
+                              it is not in */
+    int64_t iters;         /* outer iterations over all trainings */
+    double accuracy;       /* C-SVC / one-vs-rest: share of correct labels */
+    double mse;            /* eps-SVR: mean squared error */
+    double scc;            /* eps-SVR: squared correlation of D and targets */
+    double error;          /* 1 - accuracy (C-SVC), or mse (eps-SVR) */
+} svm_cv_stats;
 
 /* Per-output statistics of a trained model. */
 typedef struct {
@@ -181,6 +199,37 @@ svm_status svm_model_get(const svm_model *m, int32_t output, int32_t *sv_idx,
                          double *coef, double *alpha);
 
 void svm_model_free(svm_model *m);
+
+/* k-fold cross-validation (Section 3's feature list: "K-fold cross
+ * validation", "accuracy or correlation, mean square error").  Give either
+ * y (n labels +-1 for C-SVC, or n targets for eps-SVR) with labels = NULL,
+ * or labels (n class indices in [0, n_classes)) with y = NULL for
+ * one-vs-rest.  fold: n host entries in [0, k), every fold non-empty, or
+ * NULL for fold i mod k.  For each fold the model is trained on the other
+ * rows (their dual restricted to those rows: the held-out variables stay
+ * at 0) and predicts the held-out rows: decision (host, n x n_outputs,
+ * nullable) receives every row's decision value from the model that did
+ * not see it; stats the metrics over all rows.  With params->scale the
+ * data are standardised once over all rows.  X, y and labels in host
+ * memory only.  Returns SVM_W_MAX_ITER when some training stopped at
+ * max_iter (results still written). */
+svm_status svm_cross_validate(const svm_matrix *X, const float *y,
+                              const int32_t *labels, int32_t n_classes,
+                              const svm_params *params, int32_t k,
+                              const int32_t *fold, double *decision,
+                              svm_cv_stats *stats);
+
+/* Grid tuning by cross-validation (Section 3: "tuning parameters ... (C,
+ * eps)", e1071's tune): for grid point g the parameters are params with C
+ * = C[g], gamma = gamma[g] and epsilon = epsilon[g] (each array nullable:
+ * then params' value), and cv_error[g] the k-fold error (1 - accuracy, or
+ * the MSE for eps-SVR) on the given folds; *best = the first g of least
+ * error.  Same inputs as svm_cross_validate. */
+svm_status svm_tune(const svm_matrix *X, const float *y,
+                    const int32_t *labels, int32_t n_classes,
+                    const svm_params *params, int32_t k, const int32_t *fold,
+                    int32_t n_grid, const double *C, const double *gamma,
+                    const double *epsilon, double *cv_error, int32_t *best);
 
 const char *svm_last_error(void);
 

@@ -47,6 +47,8 @@ svm_status check_params(const svm_params* p)
         p->inner_ratio >= 1)
         return fail(SVM_E_INVALID, "inner_ratio must be in [0, 1)");
     if (p->max_inner < 0) return fail(SVM_E_INVALID, "max_inner must be >= 0");
+    if (p->scale != 0 && p->scale != 1)
+        return fail(SVM_E_INVALID, "scale must be 0 or 1");
     return SVM_OK;
 }
 
@@ -199,6 +201,27 @@ void svm_params_default(svm_params* p)
     p->degree = 3;
 }
 
+// Standardises the training features (and, for eps-SVR, the targets) in
+// place, keeping the statistics in the model for prediction.
+static void scale_training(svm_model& m, msvm::Features& f, float* y_dev,
+                           int32_t type, msvm::Context& cx)
+{
+    msvm::scale_fit(f, cx, m.x_mu, m.x_sd);
+    msvm::scale_apply(f, cx, m.x_mu.p, m.x_sd.p);
+    m.x_mu_h.resize((size_t)f.d);
+    m.x_sd_h.resize((size_t)f.d);
+    HIP_TRY(hipMemcpyAsync(m.x_mu_h.data(), m.x_mu.p,
+                           (size_t)f.d * sizeof(double), hipMemcpyDeviceToHost,
+                           cx.stream));
+    HIP_TRY(hipMemcpyAsync(m.x_sd_h.data(), m.x_sd.p,
+                           (size_t)f.d * sizeof(double), hipMemcpyDeviceToHost,
+                           cx.stream));
+    cx.sync();
+    if (type == SVM_EPS_SVR && y_dev)
+        msvm::scale_targets(y_dev, f.n, cx, &m.y_mu, &m.y_sd);
+    m.scaled = true;
+}
+
 svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
                      svm_model** out)
 {
@@ -220,13 +243,14 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
                            X->on_device ? hipMemcpyDeviceToDevice
                                         : hipMemcpyHostToDevice,
                            cx.stream));
+    auto m = std::make_unique<svm_model>();
+    if (p->scale) scale_training(*m, f, yd.p, p->type, cx);
     msvm::SolveOptions o = msvm::make_options(p, X->n, X->d);
     msvm::RowCache rc;
     msvm::cache_init(rc, X->n, p->cache_bytes, cx);
     msvm::Solver s(cx, f, yd.p, o, &rc);
     msvm::SolveResult r = s.train();
 
-    auto m = std::make_unique<svm_model>();
     m->type = p->type;
     m->n_out = 1;
     m->n_train = X->n;
@@ -298,8 +322,9 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
         cx.sync();
         if (hb) return fail(SVM_E_INVALID, "labels must be in [0, n_classes)");
     }
-    msvm::SolveOptions o = msvm::make_options(p, n, X->d);
     auto m = std::make_unique<svm_model>();
+    if (p->scale) scale_training(*m, f, nullptr, SVM_C_SVC, cx);
+    msvm::SolveOptions o = msvm::make_options(p, n, X->d);
     m->type = SVM_C_SVC;
     m->n_out = n_classes;
     m->n_train = n;
@@ -394,6 +419,223 @@ svm_status svm_predict_labels(const svm_model* m, const svm_matrix* X,
     if (m && m->type == SVM_EPS_SVR)
         return fail(SVM_E_INVALID, "labels are undefined for eps-SVR");
     return predict_impl(m, X, nullptr, labels);
+}
+
+// ---------------------------------------------------------------------------
+// k-fold cross-validation and grid tuning (Section 3's feature list)
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Validation shared by cross-validation and tuning: exactly one of y
+// (C-SVC / eps-SVR) and labels (one-vs-rest over n_classes), and the folds.
+svm_status check_cv(const svm_matrix* X, const float* y,
+                    const int32_t* labels, int32_t n_classes,
+                    const svm_params* p, int32_t k, const int32_t* fold)
+{
+    svm_status st;
+    if ((st = check_params(p)) != SVM_OK) return st;
+    if ((st = check_matrix(X, 2)) != SVM_OK) return st;
+    if ((y != nullptr) == (labels != nullptr))
+        return fail(SVM_E_INVALID, "give exactly one of y and labels");
+    if (labels) {
+        if (p->type != SVM_C_SVC)
+            return fail(SVM_E_INVALID, "one-vs-rest needs type SVM_C_SVC");
+        if (n_classes < 2 || n_classes > 16)
+            return fail(SVM_E_INVALID, "n_classes must be in [2, 16]");
+        if (X->on_device)
+            return fail(SVM_E_UNSUPPORTED,
+                        "cross-validation takes host labels");
+        for (int64_t i = 0; i < X->n; ++i)
+            if (labels[i] < 0 || labels[i] >= n_classes)
+                return fail(SVM_E_INVALID, "labels must be in [0, n_classes)");
+    } else {
+        if (X->on_device)
+            return fail(SVM_E_UNSUPPORTED,
+                        "cross-validation takes host labels or targets");
+        if ((st = check_host_labels(y, X->n, p->type)) != SVM_OK) return st;
+    }
+    if (k < 2 || (int64_t)k > X->n)
+        return fail(SVM_E_INVALID, "folds must be in [2, n]");
+    if (fold) {
+        std::vector<int64_t> cnt((size_t)k, 0);
+        for (int64_t i = 0; i < X->n; ++i) {
+            if (fold[i] < 0 || fold[i] >= k)
+                return fail(SVM_E_INVALID, "fold entries must be in [0, k)");
+            cnt[(size_t)fold[i]]++;
+        }
+        for (int32_t f = 0; f < k; ++f)
+            if (cnt[(size_t)f] == 0)
+                return fail(SVM_E_INVALID, "every fold needs a row");
+    }
+    return check_device(p->device);
+}
+
+// Everything a run of cross-validations over one data set shares: the
+// feature store (scaled once, as for a training on all rows), the labels
+// or targets, the folds and the truth for the metrics.
+struct CvData {
+    msvm::Features f;
+    msvm::DevBuf<float> y;        // targets (scaled for eps-SVR), or +-1
+    msvm::DevBuf<float> y_true;   // the targets or labels as given
+    msvm::DevBuf<int32_t> labels; // one-vs-rest
+    msvm::DevBuf<int32_t> fold;
+    double y_mu = 0.0, y_sd = 0.0;
+    int32_t n_out = 1;
+};
+
+void cv_load(CvData& c, const svm_matrix* X, const float* y,
+             const int32_t* labels, int32_t n_classes, const svm_params* p,
+             int32_t k, const int32_t* fold, msvm::Context& cx)
+{
+    const int64_t n = X->n;
+    msvm::load_features(X, c.f, cx);
+    if (p->scale) {
+        msvm::DevBuf<double> mu, sd;
+        msvm::scale_fit(c.f, cx, mu, sd);
+        msvm::scale_apply(c.f, cx, mu.p, sd.p);
+    }
+    std::vector<int32_t> fh((size_t)n);
+    for (int64_t i = 0; i < n; ++i)
+        fh[(size_t)i] = fold ? fold[i] : (int32_t)(i % k);
+    c.fold.alloc((size_t)n);
+    HIP_TRY(hipMemcpyAsync(c.fold.p, fh.data(), (size_t)n * sizeof(int32_t),
+                           hipMemcpyHostToDevice, cx.stream));
+    c.y.alloc((size_t)n);
+    if (labels) {
+        c.n_out = n_classes;
+        c.labels.alloc((size_t)n);
+        HIP_TRY(hipMemcpyAsync(c.labels.p, labels, (size_t)n * sizeof(int32_t),
+                               hipMemcpyHostToDevice, cx.stream));
+    } else {
+        c.y_true.alloc((size_t)n);
+        HIP_TRY(hipMemcpyAsync(c.y_true.p, y, (size_t)n * sizeof(float),
+                               hipMemcpyHostToDevice, cx.stream));
+        HIP_TRY(hipMemcpyAsync(c.y.p, y, (size_t)n * sizeof(float),
+                               hipMemcpyHostToDevice, cx.stream));
+        if (p->scale && p->type == SVM_EPS_SVR)
+            msvm::scale_targets(c.y.p, n, cx, &c.y_mu, &c.y_sd);
+    }
+    cx.sync();
+}
+
+// k trainings (per class for one-vs-rest), each on the rows outside one
+// fold; the decision values of the held-out rows into D (device, n x
+// n_out), then the metrics.
+svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
+                  svm_cv_stats* stats, msvm::Context& cx)
+{
+    const int64_t n = c.f.n;
+    msvm::SolveOptions o = msvm::make_options(p, n, c.f.d);
+    msvm::RowCache rc;  // K rows do not depend on the fold or the class
+    msvm::cache_init(rc, n, p->cache_bytes, cx);
+    svm_status worst = SVM_OK;
+    int64_t iters = 0;
+    for (int32_t fo = 0; fo < k; ++fo) {
+        for (int32_t cl = 0; cl < c.n_out; ++cl) {
+            if (c.labels.p)
+                msvm::launch_ovr_labels(c.labels.p, n, cl, c.y.p, cx.stream);
+            msvm::Solver s(cx, c.f, c.y.p, o, &rc, c.fold.p, fo);
+            msvm::SolveResult r = s.train();
+            s.cv_decision(D, c.n_out, cl, c.fold.p, fo, r.b);
+            iters += r.iters;
+            if (r.status != SVM_OK) worst = r.status;
+        }
+    }
+    if (p->type == SVM_EPS_SVR && c.y_sd > 0.0)
+        msvm::launch_affine(D, n, c.y_sd, c.y_mu, cx.stream);
+    msvm::DevBuf<double> sums(7);
+    msvm::launch_metrics(p->type, c.n_out, D, c.y_true.p, c.labels.p, n,
+                         sums.p, cx.stream);
+    double h[7];
+    HIP_TRY(hipMemcpyAsync(h, sums.p, sizeof(h), hipMemcpyDeviceToHost,
+                           cx.stream));
+    cx.sync();
+    std::memset(stats, 0, sizeof(*stats));
+    stats->folds = k;
+    stats->n = n;
+    stats->status = worst;
+    stats->iters = iters;
+    const double nn = (double)n;
+    if (p->type == SVM_C_SVC) {
+        stats->accuracy = h[0] / nn;
+        stats->error = 1.0 - stats->accuracy;
+    } else {
+        stats->mse = h[1] / nn;
+        const double num = nn * h[6] - h[2] * h[3];
+        const double den = (nn * h[4] - h[2] * h[2]) * (nn * h[5] - h[3] * h[3]);
+        stats->scc = den > 0.0 ? num * num / den : 0.0;
+        stats->error = stats->mse;
+    }
+    return worst;
+}
+
+}  // namespace
+
+svm_status svm_cross_validate(const svm_matrix* X, const float* y,
+                              const int32_t* labels, int32_t n_classes,
+                              const svm_params* p, int32_t k,
+                              const int32_t* fold, double* decision,
+                              svm_cv_stats* stats)
+{
+    if (!stats) return fail(SVM_E_INVALID, "stats is NULL");
+    svm_status st;
+    if ((st = check_cv(X, y, labels, n_classes, p, k, fold)) != SVM_OK)
+        return st;
+    GUARD_BEGIN
+    msvm::Context cx(p->device, p->stream);
+    CvData c;
+    cv_load(c, X, y, labels, n_classes, p, k, fold, cx);
+    msvm::DevBuf<double> D((size_t)(X->n * c.n_out));
+    st = cv_run(c, p, k, D.p, stats, cx);
+    if (decision) {
+        HIP_TRY(hipMemcpyAsync(decision, D.p,
+                               (size_t)(X->n * c.n_out) * sizeof(double),
+                               hipMemcpyDeviceToHost, cx.stream));
+        cx.sync();
+    }
+    if (st == SVM_W_MAX_ITER)
+        return fail(SVM_W_MAX_ITER, "max_iter reached in at least one fold");
+    return SVM_OK;
+    GUARD_END
+}
+
+svm_status svm_tune(const svm_matrix* X, const float* y,
+                    const int32_t* labels, int32_t n_classes,
+                    const svm_params* p, int32_t k, const int32_t* fold,
+                    int32_t n_grid, const double* C, const double* gamma,
+                    const double* epsilon, double* cv_error, int32_t* best)
+{
+    if (n_grid < 1) return fail(SVM_E_INVALID, "n_grid must be >= 1");
+    if (!cv_error || !best) return fail(SVM_E_INVALID, "outputs are NULL");
+    svm_status st;
+    if ((st = check_cv(X, y, labels, n_classes, p, k, fold)) != SVM_OK)
+        return st;
+    std::vector<svm_params> grid((size_t)n_grid, *p);
+    for (int32_t g = 0; g < n_grid; ++g) {
+        if (C) grid[(size_t)g].C = C[g];
+        if (gamma) grid[(size_t)g].gamma = gamma[g];
+        if (epsilon) grid[(size_t)g].epsilon = epsilon[g];
+        if ((st = check_params(&grid[(size_t)g])) != SVM_OK) return st;
+    }
+    GUARD_BEGIN
+    msvm::Context cx(p->device, p->stream);
+    CvData c;
+    cv_load(c, X, y, labels, n_classes, p, k, fold, cx);
+    msvm::DevBuf<double> D((size_t)(X->n * c.n_out));
+    svm_status worst = SVM_OK;
+    *best = 0;
+    for (int32_t g = 0; g < n_grid; ++g) {
+        svm_cv_stats cs;
+        if (cv_run(c, &grid[(size_t)g], k, D.p, &cs, cx) != SVM_OK)
+            worst = SVM_W_MAX_ITER;
+        cv_error[g] = cs.error;
+        if (cs.error < cv_error[*best]) *best = g;  // ties: the first
+    }
+    if (worst == SVM_W_MAX_ITER)
+        return fail(SVM_W_MAX_ITER, "max_iter reached in at least one fold");
+    return SVM_OK;
+    GUARD_END
 }
 
 svm_status svm_model_get_info(const svm_model* m, int32_t output,

@@ -234,8 +234,25 @@ void launch_pad_copy(const float* src, int64_t ld, int64_t n, int64_t d,
                      float* dst, int64_t ldp, hipStream_t s);
 void launch_norms(const float* X, int64_t n, int64_t ldp, float* sq,
                   int32_t* bad_flag, hipStream_t s);
-void launch_init_state(int32_t type, const float* y, int64_t n, uint8_t* st,
+// fold == nullptr: every row trains; else rows with fold[i] == held are
+// held out (alpha = 0, outside I_up and I_low)
+void launch_init_state(int32_t type, const float* y, int64_t n,
+                       const int32_t* fold, int32_t held, uint8_t* st,
                        int32_t* bad_flag, hipStream_t s);
+void launch_cv_decision(const double* F, int64_t n, double b,
+                        const int32_t* fold, int32_t held, double* out,
+                        int32_t stride, int32_t off, hipStream_t s);
+// per-column mean and sample standard deviation (n - 1) of n x d (leading
+// dimension ld) in fp64; part holds col_stats_partials(n, d) doubles
+void launch_col_stats(const float* X, int64_t n, int64_t ld, int64_t d,
+                      double* part, double* mu, double* sd, hipStream_t s);
+int64_t col_stats_partials(int64_t n, int64_t d);
+void launch_scale_apply(float* X, int64_t n, int64_t ld, int64_t d,
+                        const double* mu, const double* sd, hipStream_t s);
+void launch_affine(double* D, int64_t m, double a, double b, hipStream_t s);
+void launch_metrics(int32_t type, int32_t n_out, const double* D,
+                    const float* y, const int32_t* labels, int64_t n,
+                    double* out, hipStream_t s);
 void launch_ovr_labels(const int32_t* labels, int64_t n, int32_t cls,
                        float* y, hipStream_t s);
 void launch_check_labels(const int32_t* labels, int64_t n, int32_t ncls,

@@ -2,6 +2,8 @@
 // extraction of the working-set dual solve (gfx950).
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+
 #include "common.hpp"
 #include "device.hpp"
 
@@ -78,35 +80,213 @@ void launch_check_finite(const float* v, int64_t n, int32_t* bad,
 // Initial state bytes for alpha = 0.  C-SVC: label +1 -> I_up, -1 -> I_low;
 // a label other than +-1 sets bit 0 of *bad, each class seen sets bit 1
 // (+1) or bit 2 (-1).  eps-SVR: positive copies in I_up, negative in I_low.
+// State bytes at alpha = 0.  A row held out of the training (fold[i] ==
+// held, cross-validation) keeps only its label bit: its variables stay at
+// 0 outside I_up and I_low, so no working set takes them and the solve is
+// the dual restricted to the other rows.  bad: 1 an invalid label or
+// target, 2 / 4 a positive / negative training row seen.
 __global__ void k_init_state(int32_t type, const float* y, int64_t n,
-                             uint8_t* st, int32_t* bad)
+                             const int32_t* fold, int32_t held, uint8_t* st,
+                             int32_t* bad)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
+    const bool train = !fold || fold[i] != held;
+    const uint8_t up = train ? ST_UP : 0, low = train ? ST_LOW : 0;
     if (type == SVM_C_SVC) {
         float v = y[i];
         if (v == 1.0f) {
-            st[i] = ST_YPOS | ST_UP;
-            atomicOr(bad, 2);
+            st[i] = ST_YPOS | up;
+            if (train) atomicOr(bad, 2);
         } else if (v == -1.0f) {
-            st[i] = ST_LOW;
-            atomicOr(bad, 4);
+            st[i] = low;
+            if (train) atomicOr(bad, 4);
         } else {
             st[i] = 0;
             atomicOr(bad, 1);
         }
     } else {
-        st[i] = ST_YPOS | ST_UP;
-        st[n + i] = ST_LOW;
+        st[i] = ST_YPOS | up;
+        st[n + i] = low;
         if (!isfinite(y[i])) atomicOr(bad, 1);
     }
 }
 
-void launch_init_state(int32_t type, const float* y, int64_t n, uint8_t* st,
+void launch_init_state(int32_t type, const float* y, int64_t n,
+                       const int32_t* fold, int32_t held, uint8_t* st,
                        int32_t* bad, hipStream_t s)
 {
-    k_init_state<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(type, y, n, st,
-                                                             bad);
+    k_init_state<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(type, y, n, fold,
+                                                             held, st, bad);
+}
+
+// Decision values of the rows held out of a training: out[i * stride +
+// off] = F_i + b for fold[i] == held (F_i = sum_j c_j K(x_j, x_i) over the
+// trained coefficients, recomputed from alpha at the end of the solve).
+__global__ void k_cv_decision(const double* F, int64_t n, double b,
+                              const int32_t* fold, int32_t held, double* out,
+                              int32_t stride, int32_t off)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n && fold[i] == held) out[i * stride + off] = F[i] + b;
+}
+
+void launch_cv_decision(const double* F, int64_t n, double b,
+                        const int32_t* fold, int32_t held, double* out,
+                        int32_t stride, int32_t off, hipStream_t s)
+{
+    if (n > 0)
+        k_cv_decision<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(
+            F, n, b, fold, held, out, stride, off);
+}
+
+// ---------------------------------------------------------------------------
+// scaling (standardisation of the features and, for eps-SVR, the targets)
+// ---------------------------------------------------------------------------
+
+constexpr int kStatRows = 256;  // rows of one partial sum
+
+// part[b * d + c] = sum over rows b * kStatRows .. of x_rc (mu == nullptr)
+// or of (x_rc - mu_c)^2, in fp64 and row order.
+__global__ void k_col_partial(const float* X, int64_t n, int64_t ld,
+                              int64_t d, const double* mu, double* part)
+{
+    const int64_t r0 = (int64_t)blockIdx.x * kStatRows;
+    const int64_t r1 = min(r0 + kStatRows, n);
+    for (int64_t c = threadIdx.x; c < d; c += blockDim.x) {
+        const double m = mu ? mu[c] : 0.0;
+        double acc = 0.0;
+        for (int64_t r = r0; r < r1; ++r) {
+            const double v = (double)X[r * ld + c];
+            if (mu) {
+                const double e = v - m;
+                acc += e * e;
+            } else {
+                acc += v;
+            }
+        }
+        part[(int64_t)blockIdx.x * d + c] = acc;
+    }
+}
+
+// mode 0: mu_c = (sum of the partials) / n; mode 1: sd_c = sqrt(sum / (n-1))
+// (the partials summed in block order)
+__global__ void k_col_finish(const double* part, int64_t nblk, int64_t d,
+                             int64_t n, int32_t mode, double* out)
+{
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= d) return;
+    double s = 0.0;
+    for (int64_t b = 0; b < nblk; ++b) s += part[b * d + c];
+    out[c] = mode == 0 ? s / (double)n : sqrt(s / (double)(n - 1));
+}
+
+void launch_col_stats(const float* X, int64_t n, int64_t ld, int64_t d,
+                      double* part, double* mu, double* sd, hipStream_t s)
+{
+    const int64_t nblk = (n + kStatRows - 1) / kStatRows;
+    const unsigned g = (unsigned)((d + 255) / 256);
+    k_col_partial<<<(unsigned)nblk, 256, 0, s>>>(X, n, ld, d, nullptr, part);
+    k_col_finish<<<g, 256, 0, s>>>(part, nblk, d, n, 0, mu);
+    k_col_partial<<<(unsigned)nblk, 256, 0, s>>>(X, n, ld, d, mu, part);
+    k_col_finish<<<g, 256, 0, s>>>(part, nblk, d, n, 1, sd);
+}
+
+int64_t col_stats_partials(int64_t n, int64_t d)
+{
+    return (n + kStatRows - 1) / kStatRows * d;
+}
+
+// x_rc = (x_rc - mu_c) / sd_c in fp64, rounded once to fp32; a constant
+// column (sd_c = 0) is left as it is.
+__global__ void k_scale_apply(float* X, int64_t n, int64_t ld, int64_t d,
+                              const double* mu, const double* sd)
+{
+    const int64_t total = n * d;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = e / d, c = e - r * d;
+        const double s = sd[c];
+        if (s > 0.0) {
+            float* x = X + r * ld + c;
+            *x = (float)(((double)*x - mu[c]) / s);
+        }
+    }
+}
+
+void launch_scale_apply(float* X, int64_t n, int64_t ld, int64_t d,
+                        const double* mu, const double* sd, hipStream_t s)
+{
+    const int64_t total = n * d;
+    if (total <= 0) return;
+    const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+    k_scale_apply<<<(unsigned)blocks, 256, 0, s>>>(X, n, ld, d, mu, sd);
+}
+
+// D = D * a + b (the decision values of a model trained on scaled targets,
+// back in the units of the targets)
+__global__ void k_affine(double* D, int64_t m, double a, double b)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < m) D[i] = fma(D[i], a, b);
+}
+
+void launch_affine(double* D, int64_t m, double a, double b, hipStream_t s)
+{
+    if (m > 0)
+        k_affine<<<(unsigned)((m + 255) / 256), 256, 0, s>>>(D, m, a, b);
+}
+
+// Quality of decision values against the truth (cross-validation):
+// out[0] correct labels (C-SVC: sign, D >= 0 is +1, against y; one-vs-rest:
+// argmax, ties to the lowest class, against labels), out[1] sum (D - y)^2,
+// out[2..6] sum D, sum y, sum D^2, sum y^2, sum D y.  One block, fp64,
+// a fixed reduction order.
+__global__ __launch_bounds__(1024) void k_metrics(int32_t type, int32_t n_out,
+                                                  const double* D,
+                                                  const float* y,
+                                                  const int32_t* labels,
+                                                  int64_t n, double* out)
+{
+    __shared__ double sh[7][1024];
+    const int tid = threadIdx.x;
+    double acc[7] = {0, 0, 0, 0, 0, 0, 0};
+    for (int64_t i = tid; i < n; i += 1024) {
+        if (n_out > 1) {
+            int best = 0;
+            double bv = D[i * n_out];
+            for (int o = 1; o < n_out; ++o)
+                if (D[i * n_out + o] > bv) {
+                    bv = D[i * n_out + o];
+                    best = o;
+                }
+            acc[0] += best == labels[i] ? 1.0 : 0.0;
+            continue;
+        }
+        const double d = D[i], t = (double)y[i];
+        if (type == SVM_C_SVC) acc[0] += (d >= 0.0 ? 1.0 : -1.0) == t ? 1.0 : 0.0;
+        acc[1] += (d - t) * (d - t);
+        acc[2] += d;
+        acc[3] += t;
+        acc[4] += d * d;
+        acc[5] += t * t;
+        acc[6] += d * t;
+    }
+    for (int k = 0; k < 7; ++k) sh[k][tid] = acc[k];
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+        if (tid < w)
+            for (int k = 0; k < 7; ++k) sh[k][tid] += sh[k][tid + w];
+        __syncthreads();
+    }
+    if (tid < 7) out[tid] = sh[tid][0];
+}
+
+void launch_metrics(int32_t type, int32_t n_out, const double* D,
+                    const float* y, const int32_t* labels, int64_t n,
+                    double* out, hipStream_t s)
+{
+    k_metrics<<<1, 1024, 0, s>>>(type, n_out, D, y, labels, n, out);
 }
 
 __global__ void k_ovr_labels(const int32_t* labels, int64_t n, int32_t cls,

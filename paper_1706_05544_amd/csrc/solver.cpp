@@ -206,7 +206,8 @@ void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
 }
 
 Solver::Solver(Context& cx, const Features& f, const float* y_dev,
-               const SolveOptions& o, RowCache* cache)
+               const SolveOptions& o, RowCache* cache, const int32_t* fold,
+               int32_t held)
     : cx_(cx), f_(f), o_(o), cache_(cache && cache->slots > 0 ? cache : nullptr)
 {
     n_ = f.n;
@@ -294,7 +295,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     HIP_TRY(hipMemsetAsync(xS_.p, 0, xS_.bytes(), s));
     DevBuf<int32_t> bad(1);
     HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), s));
-    launch_init_state(o.type, y_.p, n_, st_.p, bad.p, s);
+    launch_init_state(o.type, y_.p, n_, fold, held, st_.p, bad.p, s);
     int32_t hb = 0;
     HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t), hipMemcpyDeviceToHost,
                            s));
@@ -688,6 +689,12 @@ void Solver::coefficients(double* c, int32_t stride, int32_t off)
                         cx_.stream);
 }
 
+void Solver::cv_decision(double* out, int32_t stride, int32_t off,
+                         const int32_t* fold, int32_t held, double b)
+{
+    launch_cv_decision(F_.p, n_, b, fold, held, out, stride, off, cx_.stream);
+}
+
 void Solver::get_alpha(double* out)
 {
     HIP_TRY(hipMemcpyAsync(out, alpha_.p, (size_t)N_ * sizeof(double),
@@ -964,9 +971,57 @@ void build_model(svm_model& m, Context& cx, const Features& f,
     cx.sync();
 }
 
-void predict_device(const svm_model& mdl, Context& cx, const Features& t,
+void scale_fit(const Features& f, Context& cx, DevBuf<double>& mu,
+               DevBuf<double>& sd)
+{
+    if (f.csr)
+        throw Error{SVM_E_UNSUPPORTED,
+                    "scaling needs dense features (centring a sparse matrix "
+                    "would fill it)"};
+    mu.alloc((size_t)f.d);
+    sd.alloc((size_t)f.d);
+    DevBuf<double> part((size_t)col_stats_partials(f.n, f.d));
+    launch_col_stats(f.X.p, f.n, f.ldp, f.d, part.p, mu.p, sd.p, cx.stream);
+    cx.sync();
+}
+
+void scale_apply(Features& f, Context& cx, const double* mu, const double* sd)
+{
+    if (f.csr)
+        throw Error{SVM_E_UNSUPPORTED,
+                    "a model trained on scaled data predicts dense rows only"};
+    launch_scale_apply(f.X.p, f.n, f.ldp, f.d, mu, sd, cx.stream);
+    DevBuf<int32_t> bad(1);
+    HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
+    launch_norms(f.X.p, f.n, f.ldp, f.sq.p, bad.p, cx.stream);
+    int32_t hb = 0;
+    HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t), hipMemcpyDeviceToHost,
+                           cx.stream));
+    cx.sync();
+    if (hb)
+        throw Error{SVM_E_INVALID,
+                    "a scaled value is not finite (or its square overflows "
+                    "fp32)"};
+}
+
+void scale_targets(float* y_dev, int64_t n, Context& cx, double* mu,
+                   double* sd)
+{
+    DevBuf<double> m(1), s(1), part((size_t)col_stats_partials(n, 1));
+    launch_col_stats(y_dev, n, 1, 1, part.p, m.p, s.p, cx.stream);
+    launch_scale_apply(y_dev, n, 1, 1, m.p, s.p, cx.stream);
+    HIP_TRY(hipMemcpyAsync(mu, m.p, sizeof(double), hipMemcpyDeviceToHost,
+                           cx.stream));
+    HIP_TRY(hipMemcpyAsync(sd, s.p, sizeof(double), hipMemcpyDeviceToHost,
+                           cx.stream));
+    cx.sync();
+    if (!(*sd > 0.0)) *sd = 0.0;  // constant targets: left as they are
+}
+
+void predict_device(const svm_model& mdl, Context& cx, Features& t,
                     double* out)
 {
+    if (mdl.scaled) scale_apply(t, cx, mdl.x_mu.p, mdl.x_sd.p);
     PredictArgs a{};
     a.SV = mdl.SV.p;
     a.sqsv = mdl.sqsv.p;
@@ -985,6 +1040,8 @@ void predict_device(const svm_model& mdl, Context& cx, const Features& t,
         a.ch_cap = mdl.ch_cap;
     }
     predict_rows(a, t, cx.stream);
+    if (mdl.scaled && mdl.type == SVM_EPS_SVR && mdl.y_sd > 0.0)
+        launch_affine(out, t.n * mdl.n_out, mdl.y_sd, mdl.y_mu, cx.stream);
 }
 
 int sparse_chunk_cap(const Features& f)

@@ -140,8 +140,11 @@ struct SolveResult {
 class Solver {
 public:
     // y: device pointer to n labels (+-1) or targets.  Features are shared.
+    // fold (device, n entries) and held: rows with fold[i] == held are held
+    // out of the training (cross-validation); fold == nullptr: none.
     Solver(Context& cx, const Features& f, const float* y_dev,
-           const SolveOptions& o, RowCache* cache = nullptr);
+           const SolveOptions& o, RowCache* cache = nullptr,
+           const int32_t* fold = nullptr, int32_t held = -1);
 
     // Full training run: initial keys, iterations, final recompute, bias.
     SolveResult train();
@@ -152,6 +155,11 @@ public:
 
     // Host copy of alpha (N values).
     void get_alpha(double* out);
+
+    // After train(): decision values F_i + b of the rows with fold[i] ==
+    // held, to out[i * stride + off] (device).
+    void cv_decision(double* out, int32_t stride, int32_t off,
+                     const int32_t* fold, int32_t held, double b);
 
     // ---- test hooks ----
     void set_state(const double* alpha_h, const double* F_h);
@@ -217,6 +225,13 @@ struct svm_model {
     int32_t type = 0;
     int32_t n_out = 1;
     int64_t n_train = 0, d = 0, ldp = 0;
+    // trained on standardised data: the features' means and standard
+    // deviations (a constant column has sd 0 and is left as it is), and
+    // for eps-SVR the targets' (decision values are mapped back)
+    bool scaled = false;
+    msvm::DevBuf<double> x_mu, x_sd;
+    std::vector<double> x_mu_h, x_sd_h;
+    double y_mu = 0.0, y_sd = 1.0;
     double gamma = 0, coef0 = 0;
     msvm::KernelFn kf{};
     int device = 0;
@@ -263,8 +278,20 @@ void build_sv_chunks(const Features& f, const int32_t* idx, int64_t nsv,
 void build_model(svm_model& m, Context& cx, const Features& f,
                  const double* coef_dev, int32_t n_out);
 
-// Decision values for X (m x n_out) into `out` (device).
-void predict_device(const svm_model& mdl, Context& cx, const Features& t,
+// Decision values for X (m x n_out) into `out` (device); t is scaled with
+// the model's statistics first when the model was trained on scaled data.
+void predict_device(const svm_model& mdl, Context& cx, Features& t,
                     double* out);
+
+// Standardisation (dense features only): per-feature mean and sample
+// standard deviation of f (device, d values each), and their application
+// to a feature store (its norms recomputed).  Targets: the same for the n
+// values of y (mean and sd returned on the host).
+void scale_fit(const Features& f, Context& cx, DevBuf<double>& mu,
+               DevBuf<double>& sd);
+void scale_apply(Features& f, Context& cx, const double* mu,
+                 const double* sd);
+void scale_targets(float* y_dev, int64_t n, Context& cx, double* mu,
+                   double* sd);
 
 }  // namespace msvm

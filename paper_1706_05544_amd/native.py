@@ -35,7 +35,8 @@ SVM_CSR = 1
 EXPORTS = [
     "svm_params_default", "svm_train", "svm_train_ovr", "svm_predict",
     "svm_predict_labels", "svm_model_get_info", "svm_model_get",
-    "svm_model_free", "svm_last_error", "svm_test_solver_create",
+    "svm_model_free", "svm_last_error", "svm_cross_validate", "svm_tune",
+    "svm_test_solver_create",
     "svm_test_solver_free", "svm_test_set_state", "svm_test_get_state",
     "svm_test_select", "svm_test_rows", "svm_test_subproblem",
     "svm_test_apply", "svm_test_iterate",
@@ -65,7 +66,17 @@ class svm_params(ct.Structure):
                 ("stream", ct.c_void_p), ("check_every", ct.c_int32),
                 ("inner_ratio", ct.c_double), ("max_inner", ct.c_int32),
                 ("profile", ct.c_int32), ("coef0", ct.c_double),
-                ("degree", ct.c_int32)]
+                ("degree", ct.c_int32), ("scale", ct.c_int32)]
+
+
+class svm_cv_stats(ct.Structure):
+    _fields_ = [("folds", ct.c_int32), ("status", ct.c_int32),
+                ("n", ct.c_int64), ("iters", ct.c_int64),
+                ("accuracy", ct.c_double), ("mse", ct.c_double),
+                ("scc", ct.c_double), ("error", ct.c_double)]
+
+    def as_dict(self) -> dict:
+        return {k: getattr(self, k) for k, _ in self._fields_}
 
 
 class svm_model_info(ct.Structure):
@@ -126,6 +137,12 @@ def load(path: Optional[str] = None):
     lib.svm_model_get.argtypes = [vp, ct.c_int32, vp, vp, vp]
     lib.svm_model_free.argtypes = [vp]
     lib.svm_model_free.restype = None
+    lib.svm_cross_validate.argtypes = [P(svm_matrix), vp, vp, ct.c_int32,
+                                       P(svm_params), ct.c_int32, vp, vp,
+                                       P(svm_cv_stats)]
+    lib.svm_tune.argtypes = [P(svm_matrix), vp, vp, ct.c_int32,
+                             P(svm_params), ct.c_int32, vp, ct.c_int32, vp, vp,
+                             vp, vp, P(ct.c_int32)]
     lib.svm_last_error.restype = ct.c_char_p
     lib.svm_last_error.argtypes = []
     lib.svm_test_solver_create.argtypes = [P(svm_matrix), vp, P(svm_params),
@@ -327,6 +344,55 @@ def svm_model_get_info(model: Model, output: int = 0) -> dict:
     info = svm_model_info()
     _check(load().svm_model_get_info(model.ptr, output, ct.byref(info)))
     return info.as_dict()
+
+
+def _cv_inputs(X, y, labels, fold):
+    M = _Mat(X)
+    if M.device:
+        raise ValueError("cross-validation takes host inputs")
+    yv = None if y is None else np.ascontiguousarray(y, dtype=np.float32)
+    lv = None if labels is None else np.ascontiguousarray(labels,
+                                                          dtype=np.int32)
+    fv = None if fold is None else np.ascontiguousarray(fold, dtype=np.int32)
+    return (M, yv, lv, fv,
+            None if yv is None else _np_ptr(yv),
+            None if lv is None else _np_ptr(lv),
+            None if fv is None else _np_ptr(fv))
+
+
+def svm_cross_validate(X, y=None, labels=None, n_classes: int = 0,
+                       k: int = 10, fold=None,
+                       params: Optional[svm_params] = None, **kw):
+    """k-fold cross-validation -> (decision values n x n_outputs, stats)."""
+    p = params or svm_params_default(**kw)
+    M, yv, lv, fv, yp, lp, fp = _cv_inputs(X, y, labels, fold)
+    n_out = n_classes if labels is not None else 1
+    D = np.empty((M.s.n, n_out), dtype=np.float64)
+    st = svm_cv_stats()
+    rc = _check(load().svm_cross_validate(ct.byref(M.s), yp, lp, n_classes,
+                                          ct.byref(p), k, fp, _np_ptr(D),
+                                          ct.byref(st)))
+    out = st.as_dict()
+    out["rc"] = rc
+    return (D[:, 0] if n_out == 1 else D), out
+
+
+def svm_tune(X, y=None, labels=None, n_classes: int = 0, k: int = 10,
+             fold=None, C=None, gamma=None, epsilon=None,
+             params: Optional[svm_params] = None, **kw):
+    """Grid tuning by k-fold cross-validation -> (errors, best index)."""
+    p = params or svm_params_default(**kw)
+    M, yv, lv, fv, yp, lp, fp = _cv_inputs(X, y, labels, fold)
+    arrs = [None if a is None else np.ascontiguousarray(a, dtype=np.float64)
+            for a in (C, gamma, epsilon)]
+    n_grid = max(len(a) for a in arrs if a is not None)
+    err = np.empty(n_grid, dtype=np.float64)
+    best = ct.c_int32()
+    _check(load().svm_tune(ct.byref(M.s), yp, lp, n_classes, ct.byref(p), k,
+                           fp, n_grid,
+                           *[None if a is None else _np_ptr(a) for a in arrs],
+                           _np_ptr(err), ct.byref(best)))
+    return err, best.value
 
 
 def svm_model_get(model: Model, output: int = 0, with_alpha: bool = False):
