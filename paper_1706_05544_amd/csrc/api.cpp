@@ -609,8 +609,7 @@ svm_status svm_tune(const svm_matrix* X, const float* y,
     if (n_grid < 1) return fail(SVM_E_INVALID, "n_grid must be >= 1");
     if (!cv_error || !best) return fail(SVM_E_INVALID, "outputs are NULL");
     svm_status st;
-    if ((st = check_cv(X, y, labels, n_classes, p, k, fold)) != SVM_OK)
-        return st;
+    if ((st = check_params(p)) != SVM_OK) return st;
     std::vector<svm_params> grid((size_t)n_grid, *p);
     for (int32_t g = 0; g < n_grid; ++g) {
         if (C) grid[(size_t)g].C = C[g];
@@ -618,6 +617,8 @@ svm_status svm_tune(const svm_matrix* X, const float* y,
         if (epsilon) grid[(size_t)g].epsilon = epsilon[g];
         if ((st = check_params(&grid[(size_t)g])) != SVM_OK) return st;
     }
+    if ((st = check_cv(X, y, labels, n_classes, p, k, fold)) != SVM_OK)
+        return st;
     GUARD_BEGIN
     msvm::Context cx(p->device, p->stream);
     CvData c;
