@@ -24,11 +24,12 @@ from paper_1706_05544_amd import workloads
 def _skewed(n, seed):
     # features of very different scales and offsets, one constant column
     rng = np.random.default_rng(seed)
-    X = rng.standard_normal((n, 6)) * np.array([1, 10, 0.01, 100, 1, 1]) + \
-        np.array([0, 5, -3, 1000, 0, 0])
+    G = rng.standard_normal((n, 6))
+    X = G * np.array([1, 10, 0.01, 100, 1, 1]) + np.array([0, 5, -3, 1000, 0, 0])
     X[:, 4] = 2.5
-    y = np.where(X[:, 0] + 0.1 * X[:, 1] + 100 * X[:, 2] +
-                 0.3 * rng.standard_normal(n) > 0.5, 1.0, -1.0)
+    y = np.where(G[:, 0] + G[:, 1] - G[:, 2] + 0.5 * rng.standard_normal(n)
+                 > 0.3, 1.0, -1.0)
+    assert 0.2 < np.mean(y > 0) < 0.8  # both classes, well mixed
     return X.astype(np.float32), y.astype(np.float32)
 
 
