@@ -132,6 +132,12 @@ def main() -> int:
                     help="kernel gamma (default: the workload's)")
     ap.add_argument("--degree", type=int, default=3)
     ap.add_argument("--coef0", type=float, default=0.0)
+    ap.add_argument("--cv", type=int, default=0,
+                    help="K > 1: one step is a K-fold cross-validation of "
+                         "the training set instead of a training + "
+                         "prediction")
+    ap.add_argument("--scale", action="store_true",
+                    help="standardise the features (and eps-SVR targets)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -179,14 +185,49 @@ def main() -> int:
     gamma = args.gamma if args.gamma is not None else w.gamma
     kw = dict(type=w.type, C=w.C, epsilon=w.eps, gamma=gamma, tol=w.tol,
               working_set=args.working_set, kernel=kernel,
-              degree=args.degree, coef0=args.coef0)
+              degree=args.degree, coef0=args.coef0,
+              scale=1 if args.scale else 0)
 
     multi = w.n_classes > 2
     if multi:
         kw.pop("type")
         kw.pop("epsilon")
 
+    class CvRun:
+        """One cross-validation in the shape of a model's statistics."""
+        n_outputs = 1
+
+        def __init__(self, st, ms):
+            self.st, self.ms = st, ms
+
+        def info(self, c=0):
+            st = self.st
+            return {"train_ms": self.ms, "iters": st["iters"],
+                    "kernel_rows": st["kernel_rows"],
+                    "row_kernel_ms": st["row_kernel_ms"],
+                    "row_kernel_launches": st["row_kernel_launches"],
+                    "row_kernel_bytes": st["row_kernel_bytes"],
+                    "cached_kernel_ms": 0.0, "cached_kernel_launches": 0,
+                    "cached_kernel_bytes": 0.0, "cache_hits": 0,
+                    "cache_fills": 0, "n_sv_output": 0, "dual_obj": 0.0,
+                    "gap": 0.0}
+
+    y_host = w.y
+    cv_stats = {}
+
     def step(profile: int):
+        if args.cv > 1:
+            t = time.perf_counter()
+            if multi:
+                D, st = nv.svm_cross_validate(X, labels=y_host,
+                                              n_classes=w.n_classes, k=args.cv,
+                                              profile=profile, **kw)
+            else:
+                D, st = nv.svm_cross_validate(X, y_host, k=args.cv,
+                                              profile=profile, **kw)
+            t1 = time.perf_counter()
+            cv_stats.update(st)
+            return CvRun(st, 1e3 * (t1 - t)), torch.from_numpy(D), t1
         if multi:
             m = nv.svm_train_ovr(X, y, w.n_classes, profile=profile, **kw)
         else:
@@ -256,7 +297,11 @@ def main() -> int:
 
     last = infos[-1]
     Dn = D.cpu().numpy()
-    if multi:
+    if args.cv > 1:
+        quality = ({"cv_accuracy": cv_stats["accuracy"]}
+                   if w.type == workloads.C_SVC else
+                   {"cv_mse": cv_stats["mse"], "cv_scc": cv_stats["scc"]})
+    elif multi:
         acc = float(np.mean(np.argmax(Dn, axis=1) == w.yt))
         quality = {"test_accuracy": acc}
     elif w.type == workloads.C_SVC:
@@ -284,7 +329,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {
             "workload": "%s: %s %s, %s n=%d d=%d, C=%g, gamma=%g, "
-                        "tol=%g, q=%d; predict %d points"
+                        "tol=%g, q=%d; %s"
                         % (w.name, ("one-vs-rest %d-class C-SVC" % w.n_classes)
                            if multi else
                            ("C-SVC" if w.type == 0 else "eps-SVR"),
@@ -292,7 +337,10 @@ def main() -> int:
                            ("CSR (%d nonzeros)" % w.X.nnz)
                            if hasattr(w.X, "indptr") else "dense",
                            w.n, w.d, w.C, gamma, w.tol, args.working_set,
-                           w.Xt.shape[0]),
+                           ("%d-fold cross-validation" % args.cv)
+                           if args.cv > 1 else
+                           "predict %d points" % w.Xt.shape[0])
+                        + ("; features standardised" if args.scale else ""),
             "kernel": args.kernel,
             "n": w.n, "d": w.d, "n_test": int(w.Xt.shape[0]),
             "working_set": args.working_set,

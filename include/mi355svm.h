@@ -125,6 +125,12 @@ typedef struct {
     double mse;            /* eps-SVR: mean squared error */
     double scc;            /* eps-SVR: squared correlation of D and targets */
     double error;          /* 1 - accuracy (C-SVC), or mse (eps-SVR) */
+    int64_t kernel_rows;   /* kernel rows used over all trainings */
+    /* params->profile = 1: the row/update launches that computed rows from
+     * X, over all trainings (as in svm_model_info) */
+    double row_kernel_ms;
+    int64_t row_kernel_launches;
+    double row_kernel_bytes;
 } svm_cv_stats;
 
 /* Per-output statistics of a trained model. */
@@ -210,9 +216,9 @@ void svm_model_free(svm_model *m);
  * at 0) and predicts the held-out rows: decision (host, n x n_outputs,
  * nullable) receives every row's decision value from the model that did
  * not see it; stats the metrics over all rows.  With params->scale the
- * data are standardised once over all rows.  X, y and labels in host
- * memory only.  Returns SVM_W_MAX_ITER when some training stopped at
- * max_iter (results still written). */
+ * data are standardised once over all rows.  y, labels and fold in host
+ * memory (X may be on the device).  Returns SVM_W_MAX_ITER when some
+ * training stopped at max_iter (results still written). */
 svm_status svm_cross_validate(const svm_matrix *X, const float *y,
                               const int32_t *labels, int32_t n_classes,
                               const svm_params *params, int32_t k,

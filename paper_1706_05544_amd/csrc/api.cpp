@@ -443,16 +443,10 @@ svm_status check_cv(const svm_matrix* X, const float* y,
             return fail(SVM_E_INVALID, "one-vs-rest needs type SVM_C_SVC");
         if (n_classes < 2 || n_classes > 16)
             return fail(SVM_E_INVALID, "n_classes must be in [2, 16]");
-        if (X->on_device)
-            return fail(SVM_E_UNSUPPORTED,
-                        "cross-validation takes host labels");
         for (int64_t i = 0; i < X->n; ++i)
             if (labels[i] < 0 || labels[i] >= n_classes)
                 return fail(SVM_E_INVALID, "labels must be in [0, n_classes)");
     } else {
-        if (X->on_device)
-            return fail(SVM_E_UNSUPPORTED,
-                        "cross-validation takes host labels or targets");
         if ((st = check_host_labels(y, X->n, p->type)) != SVM_OK) return st;
     }
     if (k < 2 || (int64_t)k > X->n)
@@ -530,7 +524,8 @@ svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
     msvm::RowCache rc;  // K rows do not depend on the fold or the class
     msvm::cache_init(rc, n, p->cache_bytes, cx);
     svm_status worst = SVM_OK;
-    int64_t iters = 0;
+    int64_t iters = 0, kernel_rows = 0, row_launches = 0;
+    double row_ms = 0.0, row_bytes = 0.0;
     for (int32_t fo = 0; fo < k; ++fo) {
         for (int32_t cl = 0; cl < c.n_out; ++cl) {
             if (c.labels.p)
@@ -539,6 +534,10 @@ svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
             msvm::SolveResult r = s.train();
             s.cv_decision(D, c.n_out, cl, c.fold.p, fo, r.b);
             iters += r.iters;
+            kernel_rows += r.kernel_rows;
+            row_ms += r.row_ms;
+            row_bytes += r.row_bytes;
+            row_launches += r.row_launches;
             if (r.status != SVM_OK) worst = r.status;
         }
     }
@@ -556,6 +555,10 @@ svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
     stats->n = n;
     stats->status = worst;
     stats->iters = iters;
+    stats->kernel_rows = kernel_rows;
+    stats->row_kernel_ms = row_ms;
+    stats->row_kernel_launches = row_launches;
+    stats->row_kernel_bytes = row_bytes;
     const double nn = (double)n;
     if (p->type == SVM_C_SVC) {
         stats->accuracy = h[0] / nn;

@@ -73,7 +73,10 @@ class svm_cv_stats(ct.Structure):
     _fields_ = [("folds", ct.c_int32), ("status", ct.c_int32),
                 ("n", ct.c_int64), ("iters", ct.c_int64),
                 ("accuracy", ct.c_double), ("mse", ct.c_double),
-                ("scc", ct.c_double), ("error", ct.c_double)]
+                ("scc", ct.c_double), ("error", ct.c_double),
+                ("kernel_rows", ct.c_int64), ("row_kernel_ms", ct.c_double),
+                ("row_kernel_launches", ct.c_int64),
+                ("row_kernel_bytes", ct.c_double)]
 
     def as_dict(self) -> dict:
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -347,9 +350,12 @@ def svm_model_get_info(model: Model, output: int = 0) -> dict:
 
 
 def _cv_inputs(X, y, labels, fold):
+    # X host or device; labels, targets and folds on the host
     M = _Mat(X)
-    if M.device:
-        raise ValueError("cross-validation takes host inputs")
+    if hasattr(y, "cpu"):
+        y = y.cpu().numpy()
+    if hasattr(labels, "cpu"):
+        labels = labels.cpu().numpy()
     yv = None if y is None else np.ascontiguousarray(y, dtype=np.float32)
     lv = None if labels is None else np.ascontiguousarray(labels,
                                                           dtype=np.int32)
@@ -366,6 +372,8 @@ def svm_cross_validate(X, y=None, labels=None, n_classes: int = 0,
     """k-fold cross-validation -> (decision values n x n_outputs, stats)."""
     p = params or svm_params_default(**kw)
     M, yv, lv, fv, yp, lp, fp = _cv_inputs(X, y, labels, fold)
+    if M.device and not kw.get("stream") and not (params and params.stream):
+        p.stream = _stream_of(True)
     n_out = n_classes if labels is not None else 1
     D = np.empty((M.s.n, n_out), dtype=np.float64)
     st = svm_cv_stats()
@@ -383,6 +391,8 @@ def svm_tune(X, y=None, labels=None, n_classes: int = 0, k: int = 10,
     """Grid tuning by k-fold cross-validation -> (errors, best index)."""
     p = params or svm_params_default(**kw)
     M, yv, lv, fv, yp, lp, fp = _cv_inputs(X, y, labels, fold)
+    if M.device and not kw.get("stream") and not (params and params.stream):
+        p.stream = _stream_of(True)
     arrs = [None if a is None else np.ascontiguousarray(a, dtype=np.float64)
             for a in (C, gamma, epsilon)]
     n_grid = max(len(a) for a in arrs if a is not None)

@@ -171,3 +171,14 @@ def test_tune_grid():
     np.testing.assert_allclose(err, ref, atol=2.0 / w.n)
     assert best == int(np.argmin(err))
     assert err[best] <= ref.min() + 2.0 / w.n
+
+
+def test_cv_device_features_same_as_host():
+    import torch
+    w = workloads.c1(n=900, n_test=10)
+    D, st = nv.svm_cross_validate(w.X, w.y, k=3, C=w.C, gamma=w.gamma,
+                                  tol=w.tol)
+    Dd, std = nv.svm_cross_validate(torch.from_numpy(w.X).to("cuda:0"), w.y,
+                                    k=3, C=w.C, gamma=w.gamma, tol=w.tol)
+    np.testing.assert_array_equal(D, Dd)
+    assert st["accuracy"] == std["accuracy"] and st["iters"] == std["iters"]
