@@ -112,6 +112,12 @@ typedef struct {
                               training, as e1071 does; dense X only; the
                               model applies the same statistics to the rows
                               it predicts (0: inputs used as given) */
+    const double *alpha0;  /* warm start for svm_train: N host values (n for
+                              C-SVC, 2n for eps-SVR: copy (i,+) then (i,-))
+                              with 0 <= a <= C and y^T a = 0 (checked to
+                              1e-9 C N when y is in host memory); the solve
+                              starts there instead of at 0.  NULL: 0.  Not
+                              for one-vs-rest or cross-validation */
 } svm_params;
 
 /* Result of a k-fold cross-validation. */

@@ -201,6 +201,25 @@ void svm_params_default(svm_params* p)
     p->degree = 3;
 }
 
+// A warm start: N finite values in [0, C] with y^T a = 0 (labels in host
+// memory only; y == nullptr skips that test).
+static svm_status check_warm_start(const double* a, const float* y, int64_t n,
+                                   const svm_params* p)
+{
+    const int64_t N = p->type == SVM_EPS_SVR ? 2 * n : n;
+    double s = 0.0;
+    for (int64_t t = 0; t < N; ++t) {
+        if (!std::isfinite(a[t]) || a[t] < 0.0 || a[t] > p->C)
+            return fail(SVM_E_INVALID, "alpha0 must lie in [0, C]");
+        if (p->type == SVM_EPS_SVR) s += t < n ? a[t] : -a[t];
+        else if (y) s += y[t] > 0 ? a[t] : -a[t];
+    }
+    if ((p->type == SVM_EPS_SVR || y) &&
+        std::fabs(s) > 1e-9 * p->C * (double)N)
+        return fail(SVM_E_INVALID, "alpha0 must satisfy y^T alpha = 0");
+    return SVM_OK;
+}
+
 // Standardises the training features (and, for eps-SVR, the targets) in
 // place, keeping the statistics in the model for prediction.
 static void scale_training(svm_model& m, msvm::Features& f, float* y_dev,
@@ -233,6 +252,10 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
     if (!y) return fail(SVM_E_INVALID, "y is NULL");
     if (!X->on_device && (st = check_host_labels(y, X->n, p->type)) != SVM_OK)
         return st;
+    if (p->alpha0 &&
+        (st = check_warm_start(p->alpha0, X->on_device ? nullptr : y, X->n,
+                               p)) != SVM_OK)
+        return st;
     if ((st = check_device(p->device)) != SVM_OK) return st;
     GUARD_BEGIN
     msvm::Context cx(p->device, p->stream);
@@ -249,6 +272,7 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
     msvm::RowCache rc;
     msvm::cache_init(rc, X->n, p->cache_bytes, cx);
     msvm::Solver s(cx, f, yd.p, o, &rc);
+    if (p->alpha0) s.warm_start(p->alpha0);
     msvm::SolveResult r = s.train();
 
     m->type = p->type;
@@ -286,6 +310,8 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     if ((st = check_params(p)) != SVM_OK) return st;
     if (p->type != SVM_C_SVC)
         return fail(SVM_E_INVALID, "one-vs-rest needs type SVM_C_SVC");
+    if (p->alpha0)
+        return fail(SVM_E_INVALID, "alpha0 is for svm_train only");
     if ((st = check_matrix(X, 2)) != SVM_OK) return st;
     if (!labels) return fail(SVM_E_INVALID, "labels is NULL");
     if (n_classes < 2 || n_classes > 16)
@@ -435,6 +461,8 @@ svm_status check_cv(const svm_matrix* X, const float* y,
 {
     svm_status st;
     if ((st = check_params(p)) != SVM_OK) return st;
+    if (p->alpha0)
+        return fail(SVM_E_INVALID, "alpha0 is for svm_train only");
     if ((st = check_matrix(X, 2)) != SVM_OK) return st;
     if ((y != nullptr) == (labels != nullptr))
         return fail(SVM_E_INVALID, "give exactly one of y and labels");

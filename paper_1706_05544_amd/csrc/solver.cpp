@@ -716,6 +716,17 @@ void Solver::set_state(const double* alpha_h, const double* F_h)
     cx_.sync();
 }
 
+void Solver::warm_start(const double* alpha_h)
+{
+    hipStream_t s = cx_.stream;
+    HIP_TRY(hipMemcpyAsync(alpha_.p, alpha_h, (size_t)N_ * sizeof(double),
+                           hipMemcpyHostToDevice, s));
+    launch_state_from_alpha(o_.type, y_.p, alpha_.p, n_, o_.C, st_.p, s);
+    recompute_responses();
+    HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
+    cx_.sync();
+}
+
 void Solver::get_state(double* alpha_h, double* F_h)
 {
     if (alpha_h)

@@ -156,6 +156,10 @@ public:
     // Host copy of alpha (N values).
     void get_alpha(double* out);
 
+    // Start the next train() from alpha (N host values, feasible): the
+    // state bytes and F are derived from it.
+    void warm_start(const double* alpha_h);
+
     // After train(): decision values F_i + b of the rows with fold[i] ==
     // held, to out[i * stride + off] (device).
     void cv_decision(double* out, int32_t stride, int32_t off,

@@ -66,7 +66,8 @@ class svm_params(ct.Structure):
                 ("stream", ct.c_void_p), ("check_every", ct.c_int32),
                 ("inner_ratio", ct.c_double), ("max_inner", ct.c_int32),
                 ("profile", ct.c_int32), ("coef0", ct.c_double),
-                ("degree", ct.c_int32), ("scale", ct.c_int32)]
+                ("degree", ct.c_int32), ("scale", ct.c_int32),
+                ("alpha0", ct.c_void_p)]
 
 
 class svm_cv_stats(ct.Structure):
@@ -289,8 +290,13 @@ def _stream_of(device: bool):
     return torch.cuda.current_stream().cuda_stream
 
 
-def svm_train(X, y, params: Optional[svm_params] = None, **kw) -> Model:
+def svm_train(X, y, params: Optional[svm_params] = None, alpha0=None,
+              **kw) -> Model:
     p = params or svm_params_default(**kw)
+    a0 = None
+    if alpha0 is not None:  # warm start (host values, kept alive here)
+        a0 = np.ascontiguousarray(alpha0, dtype=np.float64)
+        p.alpha0 = _np_ptr(a0)
     M = _Mat(X)
     if M.device and not kw.get("stream") and not (params and params.stream):
         p.stream = _stream_of(True)

@@ -200,3 +200,16 @@ def test_cross_validate_needs_exactly_one_truth():
     with pytest.raises(nv.SvmError) as e:
         nv.svm_tune(_x(), _y(), k=2, C=[1.0, -1.0])  # C <= 0 in the grid
     assert e.value.status == nv.SVM_E_INVALID
+
+
+@pytest.mark.parametrize("a0", [
+    [-0.1, 0.1, 0, 0, 0, 0, 0, 0],        # below 0
+    [2.0, 2.0, 0, 0, 0, 0, 0, 0],         # above C = 1
+    [0.5, 0.0, 0, 0, 0, 0, 0, 0],         # y^T a != 0 (labels +1, -1, ...)
+    [float("nan"), 0, 0, 0, 0, 0, 0, 0],
+])
+def test_warm_start_invalid(a0):
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train(_x(), _y(), alpha0=np.array(a0, np.float64))
+    assert e.value.status == nv.SVM_E_INVALID
+    assert "alpha0" in str(e.value)
