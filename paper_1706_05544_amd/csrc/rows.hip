@@ -573,30 +573,42 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                             }
                         }
                     };
+                    auto wave_max = [&](int v) {
+#pragma unroll
+                        for (int off = 32; off > 0; off >>= 1)
+                            v = max(v, __shfl_xor(v, off));
+                        return __builtin_amdgcn_readfirstlane(v);
+                    };
                     uint32_t nlo;
                     int nnz_next;
                     RowVals nrd;
                     row_ptrs(0, nlo, nnz_next);
                     row_vals(lane, nrd);
+                    // the first batch of the next group, requested before
+                    // this group's epilogue (which then covers its latency)
+                    int32_t cn[KB];
+                    float vn[KB];
+                    int mx_next = wave_max(nnz_next);
+                    issue(mx_next > 0 ? nlo : kOob, cn, vn);
                     for (int p0 = 0; p0 < Tw; p0 += 4) {
                         const int r = 16 * p0 + lane;  // this lane's row
                         const bool rv = r < nw;
                         const uint32_t lo = nlo;
                         const int nz = nnz_next;
+                        const int mx = mx_next;
                         const RowVals rd = nrd;
                         row_ptrs(p0 + 4, nlo, nnz_next);
                         row_vals(r + 64, nrd);
-                        int mx = nz;
-#pragma unroll
-                        for (int off = 32; off > 0; off >>= 1)
-                            mx = max(mx, __shfl_xor(mx, off));
-                        mx = __builtin_amdgcn_readfirstlane(mx);
                         float acc[QS];
 #pragma unroll
                         for (int q = 0; q < QS; ++q) acc[q] = 0.0f;
                         int32_t ca[KB], cb[KB];
                         float va[KB], vb[KB];
-                        issue(mx > 0 ? lo : kOob, ca, va);
+#pragma unroll
+                        for (int j = 0; j < KB; ++j) {
+                            ca[j] = cn[j];
+                            va[j] = vn[j];
+                        }
                         for (int kb = 0;;) {
                             issue(kb + KB < mx ? lo + STR * (kb + KB) : kOob,
                                   cb, vb);
@@ -609,6 +621,8 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                             kb += KB;
                             if (kb >= mx) break;
                         }
+                        mx_next = p0 + 4 < Tw ? wave_max(nnz_next) : 0;
+                        issue(mx_next > 0 ? nlo : kOob, cn, vn);
                         float kv[QS];
                         if (a.kf.kind == SVM_KERNEL_RBF) {
 #pragma unroll
