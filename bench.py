@@ -29,6 +29,7 @@ if ROOT not in sys.path:
 
 METRIC = ("train time to KKT tol 1e-3; kernel rows/s and % of HBM/MFMA peak")
 HBM_PEAK_GBS = 8000.0
+MFMA_FP32_PEAK_TFS = 157.3  # dense fp32 matrix-core peak of the MI355X
 
 
 def log(msg: str) -> None:
@@ -44,6 +45,7 @@ def row_bytes_per_launch(n: int, d: int, svr: bool) -> int:
 
 
 KERNEL_SOURCES = ("paper_1706_05544_amd/csrc/rows.hip",
+                  "paper_1706_05544_amd/csrc/rowtile.hpp",
                   "paper_1706_05544_amd/csrc/device.hpp",
                   "paper_1706_05544_amd/csrc/common.hpp")
 
@@ -136,6 +138,10 @@ def main() -> int:
                     help="K > 1: one step is a K-fold cross-validation of "
                          "the training set instead of a training + "
                          "prediction")
+    ap.add_argument("--lockstep", type=int, default=0,
+                    help="P > 1: one-vs-rest classes and cross-validation "
+                         "folds train P at a time in lockstep (one pass "
+                         "over X serves P working sets; no row cache)")
     ap.add_argument("--scale", action="store_true",
                     help="standardise the features (and eps-SVR targets)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -187,6 +193,8 @@ def main() -> int:
               working_set=args.working_set, kernel=kernel,
               degree=args.degree, coef0=args.coef0,
               scale=1 if args.scale else 0)
+    if args.lockstep > 1:
+        kw["lockstep"] = args.lockstep
 
     multi = w.n_classes > 2
     if multi:
@@ -291,6 +299,8 @@ def main() -> int:
     avg_ms = row_ms / max(launches, 1)
     bytes_launch = row_bytes / max(launches, 1)
     achieved = row_bytes / (row_ms * 1e-3) / 1e9 if row_ms > 0 else 0.0
+    lock_tflops = (launches * 2.0 * w.n * w.d * 16 / (row_ms * 1e-3) / 1e12
+                   if row_ms > 0 else 0.0)
     c_launches = sum(i["cached_kernel_launches"] for i in infos)
     c_ms = sum(i["cached_kernel_ms"] for i in infos)
     c_bytes = sum(i["cached_kernel_bytes"] for i in infos)
@@ -340,7 +350,9 @@ def main() -> int:
                            ("%d-fold cross-validation" % args.cv)
                            if args.cv > 1 else
                            "predict %d points" % w.Xt.shape[0])
-                        + ("; features standardised" if args.scale else ""),
+                        + ("; features standardised" if args.scale else "")
+                        + ("; %d problems in lockstep" % args.lockstep
+                           if args.lockstep > 1 else ""),
             "kernel": args.kernel,
             "n": w.n, "d": w.d, "n_test": int(w.Xt.shape[0]),
             "working_set": args.working_set,
@@ -366,6 +378,21 @@ def main() -> int:
                 row_bytes_per_launch(w.n, w.d, w.type == workloads.EPS_SVR)
                 if not hasattr(w.X, "indptr") else None),
             "launches_timed": launches,
+        } if args.lockstep <= 1 else {
+            # k_lock: each pass computes the dot products of every row with
+            # the P working sets on the matrix cores; the statistics split
+            # each pass's time over its problems, so the sum over problems
+            # of 2 n d 16 flops over the summed time is the pass's rate
+            "kernel": "k_lock (P working sets over one pass of X)",
+            "bound": "mfma",
+            "achieved": lock_tflops,
+            "peak": MFMA_FP32_PEAK_TFS,
+            "unit": "TFLOP/s",
+            "frac": lock_tflops / MFMA_FP32_PEAK_TFS,
+            "traffic": None,
+            "hbm_GBps": achieved,
+            "problem_launches_timed": launches,
+            "us_per_problem_launch": 1e3 * avg_ms,
         },
         "row_cache": {
             "rows_served": last["cache_hits"],

@@ -118,6 +118,19 @@ typedef struct {
                               1e-9 C N when y is in host memory); the solve
                               starts there instead of at 0.  NULL: 0.  Not
                               for one-vs-rest or cross-validation */
+    int32_t lockstep;      /* one-vs-rest and cross-validation (also inside
+                              svm_tune): up to this many binary problems
+                              (classes, folds) train in lockstep, their outer
+                              iterations together, one selection launch (a
+                              block per problem) and one pass over X per
+                              iteration; each problem's result is the one
+                              it has when trained alone without the row
+                              cache, which lockstep does not use.  In [0, 4];
+                              0 or 1: one problem after another.  Fewer
+                              when the working-set rows of more would not
+                              fit the row kernel's LDS (2 at d = 784).  > 1
+                              needs dense X and working_set = 16, else
+                              SVM_E_UNSUPPORTED.  No effect on svm_train */
 } svm_params;
 
 /* Result of a k-fold cross-validation. */

@@ -17,7 +17,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmi355svm.so")
 
 ARCH = "gfx950"
-DEVICE_SOURCES = ["kernels.hip", "rows.hip", "select.hip", "predict.hip"]
+DEVICE_SOURCES = ["kernels.hip", "rows.hip", "lockstep.hip", "select.hip",
+                  "predict.hip"]
 HOST_SOURCES = ["solver.cpp", "api.cpp"]
 
 # Packed fp32 instructions are disabled for every compilation that has a

@@ -1,6 +1,7 @@
 // C ABI of the MI355X kernel-SVM library: argument validation, status codes,
 // the thread-local error message, and dispatch to the solver.  Nothing here
 // computes on the data; all arithmetic runs in the HIP kernels.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <memory>
@@ -49,6 +50,25 @@ svm_status check_params(const svm_params* p)
     if (p->max_inner < 0) return fail(SVM_E_INVALID, "max_inner must be >= 0");
     if (p->scale != 0 && p->scale != 1)
         return fail(SVM_E_INVALID, "scale must be 0 or 1");
+    if (p->lockstep < 0 || p->lockstep > msvm::kLockMax)
+        return fail(SVM_E_INVALID, "lockstep must be in [0, 4]");
+    return SVM_OK;
+}
+
+// Lockstep group size for these features (1: one problem after another).
+static int lock_group(const svm_params* p, const msvm::Features& f)
+{
+    if (p->lockstep <= 1) return 1;
+    return std::min<int>(p->lockstep, msvm::Solver::lock_capacity(f, p->type));
+}
+
+// lockstep > 1 needs dense features and working sets of 16
+static svm_status check_lockstep(const svm_params* p, const svm_matrix* X)
+{
+    if (p->lockstep > 1 && (X->layout != SVM_DENSE ||
+                            p->working_set != 16))
+        return fail(SVM_E_UNSUPPORTED,
+                    "lockstep needs dense features and working_set = 16");
     return SVM_OK;
 }
 
@@ -313,6 +333,7 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     if (p->alpha0)
         return fail(SVM_E_INVALID, "alpha0 is for svm_train only");
     if ((st = check_matrix(X, 2)) != SVM_OK) return st;
+    if ((st = check_lockstep(p, X)) != SVM_OK) return st;
     if (!labels) return fail(SVM_E_INVALID, "labels is NULL");
     if (n_classes < 2 || n_classes > 16)
         return fail(SVM_E_INVALID, "n_classes must be in [2, 16]");
@@ -370,15 +391,33 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     // one row cache for all classes: the kernel rows do not depend on labels
     msvm::RowCache rc;
     msvm::cache_init(rc, n, p->cache_bytes, cx);
-    for (int32_t c = 0; c < n_classes; ++c) {
-        msvm::launch_ovr_labels(ld.p, n, c, yc.p, cx.stream);
-        msvm::Solver s(cx, f, yc.p, o, &rc);
-        res[(size_t)c] = s.train();
+    auto collect = [&](int32_t c, msvm::Solver& s, const msvm::SolveResult& r) {
+        res[(size_t)c] = r;
         s.coefficients(coef.p, n_classes, c);
-        m->b[(size_t)c] = res[(size_t)c].b;
+        m->b[(size_t)c] = r.b;
         m->alpha[(size_t)c].resize((size_t)s.N());
         s.get_alpha(m->alpha[(size_t)c].data());
-        if (res[(size_t)c].status != SVM_OK) worst = res[(size_t)c].status;
+        if (r.status != SVM_OK) worst = r.status;
+    };
+    const int L = lock_group(p, f);
+    for (int32_t c0 = 0; c0 < n_classes; c0 += L) {
+        const int G = std::min<int>(L, n_classes - c0);
+        if (G == 1) {
+            msvm::launch_ovr_labels(ld.p, n, c0, yc.p, cx.stream);
+            msvm::Solver s(cx, f, yc.p, o, L > 1 ? nullptr : &rc);
+            collect(c0, s, s.train());
+            continue;
+        }
+        std::vector<std::unique_ptr<msvm::Solver>> ss;
+        std::vector<msvm::Solver*> gp;
+        for (int j = 0; j < G; ++j) {
+            msvm::launch_ovr_labels(ld.p, n, c0 + j, yc.p, cx.stream);
+            ss.emplace_back(new msvm::Solver(cx, f, yc.p, o));
+            gp.push_back(ss.back().get());
+        }
+        const std::vector<msvm::SolveResult> rr =
+            msvm::Solver::train_lockstep(gp);
+        for (int j = 0; j < G; ++j) collect(c0 + j, *gp[j], rr[(size_t)j]);
     }
     msvm::build_model(*m, cx, f, coef.p, n_classes);
     for (int32_t c = 0; c < n_classes; ++c)
@@ -464,6 +503,7 @@ svm_status check_cv(const svm_matrix* X, const float* y,
     if (p->alpha0)
         return fail(SVM_E_INVALID, "alpha0 is for svm_train only");
     if ((st = check_matrix(X, 2)) != SVM_OK) return st;
+    if ((st = check_lockstep(p, X)) != SVM_OK) return st;
     if ((y != nullptr) == (labels != nullptr))
         return fail(SVM_E_INVALID, "give exactly one of y and labels");
     if (labels) {
@@ -554,20 +594,40 @@ svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
     svm_status worst = SVM_OK;
     int64_t iters = 0, kernel_rows = 0, row_launches = 0;
     double row_ms = 0.0, row_bytes = 0.0;
-    for (int32_t fo = 0; fo < k; ++fo) {
-        for (int32_t cl = 0; cl < c.n_out; ++cl) {
+    auto collect = [&](int32_t fo, int32_t cl, msvm::Solver& s,
+                       const msvm::SolveResult& r) {
+        s.cv_decision(D, c.n_out, cl, c.fold.p, fo, r.b);
+        iters += r.iters;
+        kernel_rows += r.kernel_rows;
+        row_ms += r.row_ms;
+        row_bytes += r.row_bytes;
+        row_launches += r.row_launches;
+        if (r.status != SVM_OK) worst = r.status;
+    };
+    // the trainings (fold, class), in groups of L in lockstep
+    const int L = lock_group(p, c.f);
+    const int32_t T = k * c.n_out;
+    for (int32_t t0 = 0; t0 < T; t0 += L) {
+        const int G = std::min<int>(L, T - t0);
+        std::vector<std::unique_ptr<msvm::Solver>> ss;
+        std::vector<msvm::Solver*> gp;
+        for (int j = 0; j < G; ++j) {
+            const int32_t fo = (t0 + j) / c.n_out, cl = (t0 + j) % c.n_out;
             if (c.labels.p)
                 msvm::launch_ovr_labels(c.labels.p, n, cl, c.y.p, cx.stream);
-            msvm::Solver s(cx, c.f, c.y.p, o, &rc, c.fold.p, fo);
-            msvm::SolveResult r = s.train();
-            s.cv_decision(D, c.n_out, cl, c.fold.p, fo, r.b);
-            iters += r.iters;
-            kernel_rows += r.kernel_rows;
-            row_ms += r.row_ms;
-            row_bytes += r.row_bytes;
-            row_launches += r.row_launches;
-            if (r.status != SVM_OK) worst = r.status;
+            ss.emplace_back(new msvm::Solver(cx, c.f, c.y.p, o,
+                                             L > 1 ? nullptr : &rc,
+                                             c.fold.p, fo));
+            gp.push_back(ss.back().get());
         }
+        std::vector<msvm::SolveResult> rr;
+        if (G == 1)
+            rr.push_back(gp[0]->train());
+        else
+            rr = msvm::Solver::train_lockstep(gp);
+        for (int j = 0; j < G; ++j)
+            collect((t0 + j) / c.n_out, (t0 + j) % c.n_out, *gp[j],
+                    rr[(size_t)j]);
     }
     if (p->type == SVM_EPS_SVR && c.y_sd > 0.0)
         msvm::launch_affine(D, n, c.y_sd, c.y_mu, cx.stream);

@@ -212,6 +212,26 @@ struct PredictArgs {
     int32_t ch_cap;
 };
 
+// Several problems over one stream of X (k_lock): problem p's working set
+// is staged at rows 16p .. 16p + 15 of xS; the rest is per problem.  Every
+// problem has the same n, features and kernel kind.
+constexpr int kLockMax = 4;
+struct LockArgs {
+    const float* X;       // dense rows
+    const float* sq;
+    const float* xS;      // P x 16 rows of ldp floats
+    int64_t n, ldp;
+    int32_t tiles;        // 16-row tiles per wave
+    double* F[kLockMax];
+    const uint8_t* st[kLockMax];
+    const float* z[kLockMax];
+    const WorkingSet* ws[kLockMax];
+    double* cand_key[kLockMax];  // as RowArgs, one table per problem
+    int32_t* cand_idx[kLockMax];
+    KernelFn kf[kLockMax];
+    double eps[kLockMax];
+};
+
 // Building the support rows by column (see PredictArgs), from CSR rows:
 // support row j is CSR row idx[j] (idx == nullptr: row j).  cap bounds the
 // columns of a chunk (16 times the longest row, at most ldp).
@@ -267,6 +287,17 @@ size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
                       int csr_cols);
 int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
+// one block per problem; `host` (P entries, each with working sets of 16;
+// their slice is set here) is copied to `dev` first when `upload` is set,
+// and must stay unchanged until the stream has passed the copy
+void launch_select_group(SelArgs* host, SelArgs* dev, int P, bool upload,
+                         bool svr, hipStream_t s);
+// lockstep row/update kernel of P problems (dense features, q = 16 each)
+void launch_lock(const LockArgs& a, int P, int nblocks, bool svr,
+                 hipStream_t s, hipEvent_t e0 = nullptr,
+                 hipEvent_t e1 = nullptr);
+size_t lock_lds_bytes(int P, int64_t ldp, int tiles, bool svr);
+int lock_blocks_per_cu(int P, bool svr, size_t lds);
 void launch_state_from_alpha(int32_t type, const float* y, const double* a,
                              int64_t n, double C, uint8_t* st, hipStream_t s);
 void launch_coef(int32_t type, const double* a, const uint8_t* st, int64_t n,

@@ -313,7 +313,7 @@ static size_t select_lds_bytes(int nblk_cols, int slice)
 }
 
 template <bool SVR, int NBLK>
-__global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
+__device__ __forceinline__ void select_body(const SelArgs& a)
 {
     WorkingSet* ws = a.ws;
     // (SS_CHECK_DONE) ws->done is tested once the record loads are in flight
@@ -1228,6 +1228,22 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 }
 
 template <bool SVR, int NBLK>
+__global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
+{
+    select_body<SVR, NBLK>(a);
+}
+
+// One problem per block: several selections of problems that advance in
+// lockstep (working sets of 16 each).
+template <bool SVR>
+__global__ __launch_bounds__(kSelThreads) void k_select_group(
+    const SelArgs* __restrict__ args)
+{
+    const SelArgs a = args[blockIdx.x];
+    select_body<SVR, 1>(a);
+}
+
+template <bool SVR, int NBLK>
 static void select_dispatch(const SelArgs& a, hipStream_t s)
 {
     const size_t lds = a.rp ? select_csr_lds_bytes(NBLK, a.ldp, a.csr_cols)
@@ -1245,6 +1261,42 @@ static void select_dispatch(const SelArgs& a, hipStream_t s)
         lds_allowed = lds;
     }
     k_select<SVR, NBLK><<<1, kSelThreads, lds, s>>>(a);
+}
+
+void launch_select_group(SelArgs* host, SelArgs* dev, int P, bool upload,
+                         bool svr, hipStream_t s)
+{
+    if (P <= 0) return;
+    const int slice =
+        host[0].slice > 0 ? host[0].slice : select_slice(1, host[0].ldp);
+    if (upload) {
+        for (int p = 0; p < P; ++p) {
+            if (host[p].rp || host[p].ldp != host[0].ldp)
+                throw Error{SVM_E_INTERNAL, "bad lockstep selection"};
+            host[p].slice = slice;
+        }
+        // (host stays untouched until the stream has passed this copy)
+        HIP_TRY(hipMemcpyAsync(dev, host, sizeof(SelArgs) * P,
+                               hipMemcpyHostToDevice, s));
+    }
+    const size_t lds = select_lds_bytes(1, slice);
+    static size_t lds_allowed[2] = {32 * 1024, 32 * 1024};
+    const void* fn = svr ? (const void*)k_select_group<true>
+                         : (const void*)k_select_group<false>;
+    if (lds > lds_allowed[svr]) {
+        hipError_t e = hipFuncSetAttribute(
+            fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            throw Error{SVM_E_UNSUPPORTED,
+                        "select tile needs more LDS than the device allows"};
+        }
+        lds_allowed[svr] = lds;
+    }
+    if (svr)
+        k_select_group<true><<<P, kSelThreads, lds, s>>>(dev);
+    else
+        k_select_group<false><<<P, kSelThreads, lds, s>>>(dev);
 }
 
 void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)

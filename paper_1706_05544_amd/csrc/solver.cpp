@@ -594,13 +594,25 @@ void Solver::recompute_responses()
 SolveResult Solver::train()
 {
     SolveResult r;
-    hipEvent_t t0, t1;
-    HIP_TRY(hipEventCreate(&t0));
-    HIP_TRY(hipEventCreate(&t1));
-    HIP_TRY(hipEventRecord(t0, cx_.stream));
+    hipEvent_t t0 = start(true);
+    const bool conv = run_loop(r);
+    finish(r, conv, t0);
+    return r;
+}
 
-    launch_keys();
-    bool conv = run_loop(r);
+hipEvent_t Solver::start(bool keys)
+{
+    hipEvent_t t0;
+    HIP_TRY(hipEventCreate(&t0));
+    HIP_TRY(hipEventRecord(t0, cx_.stream));
+    if (keys) launch_keys();
+    return t0;
+}
+
+void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0)
+{
+    hipEvent_t t1;
+    HIP_TRY(hipEventCreate(&t1));
     // The incremental responses accumulate rounding over many updates:
     // recompute them from alpha and re-test the gap before accepting.
     for (int pass = 0; pass < 4 && conv; ++pass) {
@@ -680,7 +692,277 @@ SolveResult Solver::train()
                     (long long)cached_launches_);
         }
     }
-    return r;
+}
+
+int Solver::lock_capacity(const Features& f, int32_t type)
+{
+    constexpr size_t kLdsMax = 160 * 1024;
+    const bool svr = type == SVM_EPS_SVR;
+    int P = kLockMax;
+    while (P > 1 && lock_lds_bytes(P, f.ldp, 1, svr) > kLdsMax) --P;
+    return P;
+}
+
+std::vector<SolveResult> Solver::train_lockstep(
+    const std::vector<Solver*>& g)
+{
+    const int G = (int)g.size();
+    std::vector<SolveResult> res(G);
+    if (G == 0) return res;
+    Solver& s0 = *g[0];
+    Context& cx = s0.cx_;
+    const Features& f = s0.f_;
+    const bool svr = s0.o_.type == SVM_EPS_SVR;
+    const int64_t n = s0.n_;
+    if (G > lock_capacity(f, s0.o_.type))
+        throw Error{SVM_E_INTERNAL, "lockstep group too large"};
+    for (Solver* s : g) {
+        if (&s->f_ != &f || &s->cx_ != &cx || s->o_.type != s0.o_.type ||
+            s->kf_.kind != s0.kf_.kind || s->o_.q != 16 || f.csr ||
+            s->cache_ != nullptr)
+            throw Error{SVM_E_INTERNAL, "solvers cannot run in lockstep"};
+    }
+    hipStream_t st = cx.stream;
+
+    // Grid of the lockstep pass for all G problems (as the constructor
+    // does for k_rows): every block resident, units of 32 rows shared out
+    // evenly; fewer problems later reuse it (their LDS is smaller).
+    constexpr int kWaves = kRowThreads / 64;
+    constexpr size_t kLdsMax = 160 * 1024;
+    int cus = 0;
+    HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
+                                  cx.device));
+    const int64_t units = (n + 31) / 32, tiles_total = (n + 15) / 16;
+    auto wave_tiles = [&](int64_t nb) {
+        const int64_t block_tiles = 2 * ((units + nb - 1) / nb);
+        return (int)((block_tiles + kWaves - 1) / kWaves);
+    };
+    int tiles = 1;
+    int64_t cap_blocks = 1;
+    for (int it = 0; it < 8; ++it) {
+        const size_t lds = lock_lds_bytes(G, f.ldp, tiles, svr);
+        cap_blocks = (int64_t)cus * lock_blocks_per_cu(G, svr, lds);
+        const int t = wave_tiles(std::min(cap_blocks, units));
+        if (t <= tiles) break;
+        tiles = t;
+    }
+    int64_t nb = std::min(cap_blocks, (tiles_total + kWaves - 1) / kWaves);
+    nb = std::max<int64_t>(
+        1, std::min({nb, (int64_t)kSelThreads * kSelRecords, units}));
+    tiles = wave_tiles(nb);
+    if (lock_lds_bytes(G, f.ldp, tiles, svr) > kLdsMax ||
+        (int64_t)16 * tiles * f.ldp * 4 >= ((int64_t)1 << 31))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "training set too large for the lockstep row kernel"};
+
+    // the group's working-set rows (problem at position p: rows 16p ..),
+    // candidate tables of the lockstep grid, selection arguments
+    DevBuf<float> xs((size_t)kLockMax * 16 * f.ldp);
+    HIP_TRY(hipMemsetAsync(xs.p, 0, xs.bytes(), st));
+    std::vector<DevBuf<double>> ck(G);
+    std::vector<DevBuf<int32_t>> ci(G);
+    for (int p = 0; p < G; ++p) {
+        ck[p].alloc((size_t)nb * 2 * kBlockTop);
+        ci[p].alloc((size_t)nb * 2 * kBlockTop);
+    }
+    DevBuf<SelArgs> dsel(kLockMax);
+    HostBuf<SelArgs> hsel(kLockMax);
+    HostBuf<WorkingSet> hws((size_t)2 * G);
+    std::vector<int> act(G);
+    for (int p = 0; p < G; ++p) act[p] = p;
+    LockArgs la{};
+
+    // arguments of the active problems, by position
+    auto build = [&]() {
+        la = LockArgs{};
+        la.X = f.X.p;
+        la.sq = f.sq.p;
+        la.xS = xs.p;
+        la.n = n;
+        la.ldp = f.ldp;
+        la.tiles = tiles;
+        for (int q = 0; q < (int)act.size(); ++q) {
+            Solver& s = *g[act[q]];
+            la.F[q] = s.F_.p;
+            la.st[q] = s.st_.p;
+            la.z[q] = s.y_.p;
+            la.ws[q] = s.ws_.p;
+            la.cand_key[q] = ck[act[q]].p;
+            la.cand_idx[q] = ci[act[q]].p;
+            la.kf[q] = s.kf_;
+            la.eps[q] = s.o_.eps;
+            SelArgs a{};
+            a.cand_key = ck[act[q]].p;
+            a.cand_idx = ci[act[q]].p;
+            a.nb = (int32_t)nb;
+            a.half = s.half_;
+            a.ws = s.ws_.p;
+            a.alpha = s.alpha_.p;
+            a.st = s.st_.p;
+            a.F = s.F_.p;
+            a.z = s.y_.p;
+            a.X = f.X.p;
+            a.sq = f.sq.p;
+            a.xS = xs.p + (size_t)q * 16 * f.ldp;
+            a.csr_cols = -1;
+            a.n = n;
+            a.ldp = f.ldp;
+            a.C = s.o_.C;
+            a.eps = s.o_.eps;
+            a.tol = s.o_.tol;
+            a.kf = s.kf_;
+            a.inner_ratio = s.o_.inner_ratio;
+            a.inner_tol_override = -1.0;
+            a.max_inner = s.o_.max_inner;
+            a.max_iter = s.o_.max_iter;
+            a.mode = SS_SOLVE | SS_CHECK_DONE;
+            a.group_rows = kWaves * 16 * tiles;  // most rows of a block
+            hsel.p[q] = a;
+        }
+    };
+
+    std::vector<hipEvent_t> t0(G);
+    for (int p = 0; p < G; ++p) t0[p] = g[p]->start(false);
+    // the first candidates: a pass with empty working sets (F + 0)
+    build();
+    launch_lock(la, G, (int)nb, svr, st);
+
+    const int K = s0.o_.check_every;
+    const bool prof = s0.o_.profile;
+    hipEvent_t ev[2];
+    HIP_TRY(hipEventCreateWithFlags(&ev[0], hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&ev[1], hipEventDisableTiming));
+    std::vector<hipEvent_t> pe;
+    if (prof) {
+        pe.resize((size_t)4 * K);
+        for (auto& e : pe)
+            HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+    }
+    auto cleanup = [&]() {
+        for (auto& e : pe) (void)hipEventDestroy(e);
+        (void)hipEventDestroy(ev[0]);
+        (void)hipEventDestroy(ev[1]);
+    };
+    std::vector<int64_t> last(G, 0);
+    std::vector<int> ran(2, 0);  // problems in each chunk
+    auto enqueue = [&](int slot, bool upload) {
+        const int P = (int)act.size();
+        ran[slot] = P;
+        for (int k = 0; k < K; ++k) {
+            launch_select_group(hsel.p, dsel.p, P, upload && k == 0, svr, st);
+            if (prof)
+                launch_lock(la, P, (int)nb, svr, st,
+                            pe[(size_t)(slot * K + k) * 2],
+                            pe[(size_t)(slot * K + k) * 2 + 1]);
+            else
+                launch_lock(la, P, (int)nb, svr, st);
+        }
+        for (int q = 0; q < P; ++q)
+            HIP_TRY(hipMemcpyAsync(&hws.p[(size_t)slot * G + act[q]],
+                                   g[act[q]]->ws_.p, sizeof(WorkingSet),
+                                   hipMemcpyDeviceToHost, st));
+        HIP_TRY(hipEventRecord(ev[slot], st));
+    };
+
+    // Algorithmic bytes of a lockstep launch: X and the norms once, and
+    // each problem's F (read and written) and state bytes (eps-SVR: and
+    // its targets); shared bytes and the time are split evenly over the
+    // problems of the launch.
+    const double own = 16.0 + (svr ? 6.0 : 1.0);
+    const double shared = 4.0 * (double)f.d * (double)n + 4.0 * (double)n;
+    auto account = [&](int slot, const std::vector<int64_t>& adv) {
+        if (!prof) return;
+        const int P = ran[slot];
+        for (int k = 0; k < K; ++k) {
+            int pk = 0;
+            for (int q = 0; q < P; ++q) pk += adv[act[q]] > k;
+            if (pk == 0) continue;
+            float ms = 0.f;
+            HIP_TRY(hipEventElapsedTime(&ms, pe[(size_t)(slot * K + k) * 2],
+                                        pe[(size_t)(slot * K + k) * 2 + 1]));
+            for (int q = 0; q < P; ++q) {
+                if (adv[act[q]] <= k) continue;
+                Solver& s = *g[act[q]];
+                s.row_ms_ += ms / pk;
+                s.row_launches_ += 1;
+                s.row_rows_ += n;
+                s.row_bytes_ += shared / pk + (double)n * own;
+            }
+        }
+    };
+
+    try {
+        enqueue(0, true);
+        enqueue(1, false);
+        int cur = 0;
+        for (;;) {
+            HIP_TRY(hipEventSynchronize(ev[cur]));
+            std::vector<int64_t> adv(G, 0);
+            bool moved = false, changed = false;
+            std::vector<int> next;
+            for (int p : act) {
+                const WorkingSet& w = hws.p[(size_t)cur * G + p];
+                adv[p] = w.iter - last[p];
+                moved |= adv[p] > 0;
+                last[p] = w.iter;
+                if (w.done)
+                    changed = true;
+                else
+                    next.push_back(p);
+            }
+            account(cur, adv);
+            if (next.empty()) break;
+            if (!moved) throw Error{SVM_E_INTERNAL,
+                                    "solver state made no progress"};
+            if (changed) {
+                // drain the chunk in flight (its problem set is the old
+                // one), then restart the pipeline with the rest
+                cx.sync();
+                const int o = cur ^ 1;
+                std::vector<int64_t> adv2(G, 0);
+                next.clear();
+                for (int p : act) {
+                    const WorkingSet& w = hws.p[(size_t)o * G + p];
+                    adv2[p] = w.iter - last[p];
+                    last[p] = w.iter;
+                    if (!w.done) next.push_back(p);
+                }
+                account(o, adv2);
+                if (next.empty()) break;
+                act = next;
+                build();
+                enqueue(0, true);
+                enqueue(1, false);
+                cur = 0;
+                continue;
+            }
+            enqueue(cur, false);
+            cur ^= 1;
+        }
+        cx.sync();
+    } catch (...) {
+        cx.sync();
+        cleanup();
+        for (auto& e : t0) (void)hipEventDestroy(e);
+        throw;
+    }
+    cleanup();
+
+    std::vector<char> conv(G);
+    for (int p = 0; p < G; ++p) {
+        WorkingSet w;
+        g[p]->read_ws(w);
+        SolveResult& r = res[p];
+        r.iters = w.iter;
+        r.gap = w.gap;
+        r.m = w.m;
+        r.M = w.M;
+        r.kernel_rows = w.rows;
+        r.status = w.done == 2 ? SVM_W_MAX_ITER : SVM_OK;
+        conv[p] = w.done == 1;
+    }
+    for (int p = 0; p < G; ++p) g[p]->finish(res[p], conv[p], t0[p]);
+    return res;
 }
 
 void Solver::coefficients(double* c, int32_t stride, int32_t off)

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <memory>
+#include <vector>
 
 #include "common.hpp"
 
@@ -149,6 +150,19 @@ public:
     // Full training run: initial keys, iterations, final recompute, bias.
     SolveResult train();
 
+    // Training of several solvers in lockstep (one-vs-rest classes,
+    // cross-validation folds, grid points): their outer iterations advance
+    // together, one selection launch (a block per solver) and one pass over
+    // X per iteration (k_lock).  Each result is the one train() gives
+    // without the row cache.  The solvers share the features and the
+    // stream, are of one type and kernel kind, have working sets of 16,
+    // dense features and no row cache; at most lock_capacity() of them.
+    static std::vector<SolveResult> train_lockstep(
+        const std::vector<Solver*>& group);
+    // Problems one lockstep pass can carry for these features (their
+    // working-set rows share the row kernel's LDS): 1 .. kLockMax.
+    static int lock_capacity(const Features& f, int32_t type);
+
     // Expansion coefficients c_i over all n samples, written to
     // c[i * stride + off] (device).
     void coefficients(double* c, int32_t stride, int32_t off);
@@ -178,6 +192,8 @@ public:
     int64_t N() const { return N_; }
 
 private:
+    hipEvent_t start(bool keys);
+    void finish(SolveResult& r, bool conv, hipEvent_t t0);
     void launch_keys();
     void launch_hot_rows(hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
     void launch_solve(int32_t mode);

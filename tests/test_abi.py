@@ -45,13 +45,13 @@ def test_struct_layout_matches_header(tmp_path):
 int main(void) {
   printf("%zu %zu %zu\n", sizeof(svm_matrix), sizeof(svm_params),
          sizeof(svm_model_info));
-  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\n",
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\n",
          offsetof(svm_params, stream),
          offsetof(svm_params, profile), offsetof(svm_model_info, train_ms),
          offsetof(svm_matrix, nnz), offsetof(svm_params, coef0),
          offsetof(svm_params, degree), offsetof(svm_model_info, coef0),
          offsetof(svm_params, scale), sizeof(svm_cv_stats),
-         offsetof(svm_cv_stats, error));
+         offsetof(svm_cv_stats, error), offsetof(svm_params, lockstep));
   return 0;
 }
 ''')
@@ -69,7 +69,8 @@ int main(void) {
         nv.svm_model_info.train_ms.offset, nv.svm_matrix.nnz.offset,
         nv.svm_params.coef0.offset, nv.svm_params.degree.offset,
         nv.svm_model_info.coef0.offset, nv.svm_params.scale.offset,
-        ct.sizeof(nv.svm_cv_stats), nv.svm_cv_stats.error.offset]
+        ct.sizeof(nv.svm_cv_stats), nv.svm_cv_stats.error.offset,
+        nv.svm_params.lockstep.offset]
 
 
 def test_params_default():
@@ -185,6 +186,9 @@ def test_no_device_is_a_clean_error():
     (dict(k=2, fold=[0, 1, 2, 0, 1, 0, 1, 0]), nv.SVM_E_INVALID),
     (dict(k=3, fold=[0, 1, 0, 1, 0, 1, 0, 1]), nv.SVM_E_INVALID),  # empty fold
     (dict(k=2, scale=3), nv.SVM_E_INVALID),
+    (dict(k=2, lockstep=5), nv.SVM_E_INVALID),
+    (dict(k=2, lockstep=-1), nv.SVM_E_INVALID),
+    (dict(k=2, lockstep=2, working_set=32), nv.SVM_E_UNSUPPORTED),
 ])
 def test_cross_validate_invalid(kw, code):
     with pytest.raises(nv.SvmError) as e:
@@ -213,3 +217,19 @@ def test_warm_start_invalid(a0):
         nv.svm_train(_x(), _y(), alpha0=np.array(a0, np.float64))
     assert e.value.status == nv.SVM_E_INVALID
     assert "alpha0" in str(e.value)
+
+
+def test_lockstep_needs_dense_features():
+    # checked before the device: the same error with or without a GPU
+    import scipy.sparse as sp
+    X = sp.csr_matrix(_x())
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_cross_validate(X, _y(), k=2, lockstep=2)
+    assert e.value.status == nv.SVM_E_UNSUPPORTED
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train_ovr(X, np.arange(8, dtype=np.int32) % 2, 2, lockstep=3)
+    assert e.value.status == nv.SVM_E_UNSUPPORTED
+    with pytest.raises(nv.SvmError) as e:
+        nv.svm_train_ovr(_x(), np.arange(8, dtype=np.int32) % 2, 2,
+                         lockstep=9)
+    assert e.value.status == nv.SVM_E_INVALID
