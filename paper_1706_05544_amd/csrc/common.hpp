@@ -305,6 +305,9 @@ void launch_coef(int32_t type, const double* a, const uint8_t* st, int64_t n,
 void launch_coef_strided(int32_t type, const double* a, const uint8_t* st,
                          int64_t n, double* c, int32_t stride, int32_t off,
                          hipStream_t s);
+// out: 1 + kSummaryBlocks entries (the result at out[0], partial sums
+// after it)
+constexpr int kSummaryBlocks = 256;
 void launch_summary(int32_t type, const double* a, const uint8_t* st,
                     const double* F, const float* z, int64_t n, double C,
                     double eps, Summary* out, hipStream_t s);

@@ -89,27 +89,33 @@ __global__ void k_init_state(int32_t type, const float* y, int64_t n,
                              const int32_t* fold, int32_t held, uint8_t* st,
                              int32_t* bad)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    const bool train = !fold || fold[i] != held;
-    const uint8_t up = train ? ST_UP : 0, low = train ? ST_LOW : 0;
-    if (type == SVM_C_SVC) {
-        float v = y[i];
-        if (v == 1.0f) {
-            st[i] = ST_YPOS | up;
-            if (train) atomicOr(bad, 2);
-        } else if (v == -1.0f) {
-            st[i] = low;
-            if (train) atomicOr(bad, 4);
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int flags = 0;  // 1 bad value, 2 a training +1, 4 a training -1
+    if (i < n) {
+        const bool train = !fold || fold[i] != held;
+        const uint8_t up = train ? ST_UP : 0, low = train ? ST_LOW : 0;
+        if (type == SVM_C_SVC) {
+            const float v = y[i];
+            if (v == 1.0f) {
+                st[i] = ST_YPOS | up;
+                flags = train ? 2 : 0;
+            } else if (v == -1.0f) {
+                st[i] = low;
+                flags = train ? 4 : 0;
+            } else {
+                st[i] = 0;
+                flags = 1;
+            }
         } else {
-            st[i] = 0;
-            atomicOr(bad, 1);
+            st[i] = ST_YPOS | up;
+            st[n + i] = low;
+            flags = isfinite(y[i]) ? 0 : 1;
         }
-    } else {
-        st[i] = ST_YPOS | up;
-        st[n + i] = low;
-        if (!isfinite(y[i])) atomicOr(bad, 1);
     }
+    // one atomic per wave
+    const int w = (__ballot(flags & 1) ? 1 : 0) | (__ballot(flags & 2) ? 2 : 0) |
+                  (__ballot(flags & 4) ? 4 : 0);
+    if ((threadIdx.x & 63) == 0 && w) atomicOr(bad, w);
 }
 
 void launch_init_state(int32_t type, const float* y, int64_t n,
@@ -383,21 +389,26 @@ void launch_coef_strided(int32_t type, const double* a, const uint8_t* st,
 }
 
 // Bias and objective ingredients, one block, fixed reduction order.
+// Per-block partial sums of a state (bias and objective terms) over a
+// fixed split of the N variables, then their sum in a fixed tree order:
+// the same bits on every run.
 __global__ __launch_bounds__(1024) void k_summary(int32_t type,
                                                   const double* a,
                                                   const uint8_t* st,
                                                   const double* F,
                                                   const float* z, int64_t n,
                                                   double C, double eps,
-                                                  Summary* out)
+                                                  Summary* part)
 {
     __shared__ double s_v[1024], s_o[1024];
     __shared__ int64_t s_f[1024], s_b[1024];
     const int tid = threadIdx.x;
     const int64_t N = type == SVM_EPS_SVR ? 2 * n : n;
+    const int64_t t0 = (int64_t)blockIdx.x * N / gridDim.x;
+    const int64_t t1 = ((int64_t)blockIdx.x + 1) * N / gridDim.x;
     double sv = 0.0, so = 0.0;
     int64_t nf = 0, nbd = 0;
-    for (int64_t t = tid; t < N; t += 1024) {
+    for (int64_t t = t0 + tid; t < t1; t += 1024) {
         const int64_t sm = t >= n ? t - n : t;
         double yv, rv;
         if (type == SVM_EPS_SVR) {
@@ -431,6 +442,36 @@ __global__ __launch_bounds__(1024) void k_summary(int32_t type,
         __syncthreads();
     }
     if (tid == 0) {
+        Summary& o = part[blockIdx.x];
+        o.sum_free_v = s_v[0];
+        o.obj2 = s_o[0];
+        o.n_free = s_f[0];
+        o.n_bounded = s_b[0];
+    }
+}
+
+__global__ __launch_bounds__(kSummaryBlocks) void k_summary_finish(
+    const Summary* part, int nb, Summary* out)
+{
+    __shared__ double s_v[kSummaryBlocks], s_o[kSummaryBlocks];
+    __shared__ int64_t s_f[kSummaryBlocks], s_b[kSummaryBlocks];
+    const int tid = threadIdx.x;
+    const bool in = tid < nb;
+    s_v[tid] = in ? part[tid].sum_free_v : 0.0;
+    s_o[tid] = in ? part[tid].obj2 : 0.0;
+    s_f[tid] = in ? part[tid].n_free : 0;
+    s_b[tid] = in ? part[tid].n_bounded : 0;
+    __syncthreads();
+    for (int w = kSummaryBlocks / 2; w > 0; w >>= 1) {
+        if (tid < w) {
+            s_v[tid] += s_v[tid + w];
+            s_o[tid] += s_o[tid + w];
+            s_f[tid] += s_f[tid + w];
+            s_b[tid] += s_b[tid + w];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
         out->sum_free_v = s_v[0];
         out->obj2 = s_o[0];
         out->n_free = s_f[0];
@@ -442,7 +483,11 @@ void launch_summary(int32_t type, const double* a, const uint8_t* st,
                     const double* F, const float* z, int64_t n, double C,
                     double eps, Summary* out, hipStream_t s)
 {
-    k_summary<<<1, 1024, 0, s>>>(type, a, st, F, z, n, C, eps, out);
+    const int64_t N = type == SVM_EPS_SVR ? 2 * n : n;
+    const int nb = (int)std::max<int64_t>(
+        1, std::min<int64_t>(kSummaryBlocks, (N + 4095) / 4096));
+    k_summary<<<nb, 1024, 0, s>>>(type, a, st, F, z, n, C, eps, out + 1);
+    k_summary_finish<<<1, kSummaryBlocks, 0, s>>>(out + 1, nb, out);
 }
 
 constexpr int kCompactThreads = 1024;
@@ -476,17 +521,13 @@ __global__ __launch_bounds__(kCompactThreads) void k_compact_count(
     }
 }
 
-__global__ void k_compact_scan(int32_t* blk_cnt, int64_t nblk,
-                               int64_t* total)
+__global__ __launch_bounds__(1024) void k_compact_scan(int32_t* blk_cnt,
+                                                      int64_t nblk,
+                                                      int64_t* total)
 {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    int64_t acc = 0;
-    for (int64_t b = 0; b < nblk; ++b) {
-        int32_t c = blk_cnt[b];
-        blk_cnt[b] = (int32_t)acc;
-        acc += c;
-    }
-    *total = acc;
+    __shared__ int wsum[1024 / 64];
+    const int tot = block_exclusive_scan<1024>(blk_cnt, nblk, wsum);
+    if (threadIdx.x == 0) *total = tot;
 }
 
 __global__ __launch_bounds__(kCompactThreads) void k_compact_scatter(
@@ -520,7 +561,7 @@ void launch_compact(const double* coef, int64_t n, int32_t n_out,
     if (nblk == 0) return;
     k_compact_count<<<(unsigned)nblk, kCompactThreads, 0, s>>>(coef, n, n_out,
                                                                blk_cnt);
-    k_compact_scan<<<1, 64, 0, s>>>(blk_cnt, nblk, count_out);
+    k_compact_scan<<<1, 1024, 0, s>>>(blk_cnt, nblk, count_out);
     k_compact_scatter<<<(unsigned)nblk, kCompactThreads, 0, s>>>(
         coef, n, n_out, blk_cnt, idx_out, coef_out);
 }

@@ -279,7 +279,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     }
     ckey_.alloc((size_t)nb_ * 2 * kBlockTop);
     cidx_.alloc((size_t)nb_ * 2 * kBlockTop);
-    sum_.alloc(1);
+    sum_.alloc(1 + kSummaryBlocks);
     cvec_.alloc((size_t)n_);
     cblk_.alloc((size_t)compact_blocks(n_));
     sv_idx_.alloc((size_t)n_);
