@@ -118,9 +118,10 @@ typedef struct {
                               1e-9 C N when y is in host memory); the solve
                               starts there instead of at 0.  NULL: 0.  Not
                               for one-vs-rest or cross-validation */
-    int32_t lockstep;      /* one-vs-rest and cross-validation (also inside
-                              svm_tune): up to this many binary problems
-                              (classes, folds) train in lockstep, their outer
+    int32_t lockstep;      /* one-vs-rest, cross-validation and svm_tune:
+                              up to this many binary problems (classes,
+                              folds; in svm_tune also of different grid
+                              points) train in lockstep, their outer
                               iterations together, one selection launch (a
                               block per problem) and one pass over X per
                               iteration; each problem's result is the one

@@ -581,54 +581,19 @@ void cv_load(CvData& c, const svm_matrix* X, const float* y,
     cx.sync();
 }
 
-// k trainings (per class for one-vs-rest), each on the rows outside one
-// fold; the decision values of the held-out rows into D (device, n x
-// n_out), then the metrics.
-svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
-                  svm_cv_stats* stats, msvm::Context& cx)
-{
-    const int64_t n = c.f.n;
-    msvm::SolveOptions o = msvm::make_options(p, n, c.f.d);
-    msvm::RowCache rc;  // K rows do not depend on the fold or the class
-    msvm::cache_init(rc, n, p->cache_bytes, cx);
-    svm_status worst = SVM_OK;
+// Totals of the trainings of one cross-validation.
+struct CvAcc {
     int64_t iters = 0, kernel_rows = 0, row_launches = 0;
     double row_ms = 0.0, row_bytes = 0.0;
-    auto collect = [&](int32_t fo, int32_t cl, msvm::Solver& s,
-                       const msvm::SolveResult& r) {
-        s.cv_decision(D, c.n_out, cl, c.fold.p, fo, r.b);
-        iters += r.iters;
-        kernel_rows += r.kernel_rows;
-        row_ms += r.row_ms;
-        row_bytes += r.row_bytes;
-        row_launches += r.row_launches;
-        if (r.status != SVM_OK) worst = r.status;
-    };
-    // the trainings (fold, class), in groups of L in lockstep
-    const int L = lock_group(p, c.f);
-    const int32_t T = k * c.n_out;
-    for (int32_t t0 = 0; t0 < T; t0 += L) {
-        const int G = std::min<int>(L, T - t0);
-        std::vector<std::unique_ptr<msvm::Solver>> ss;
-        std::vector<msvm::Solver*> gp;
-        for (int j = 0; j < G; ++j) {
-            const int32_t fo = (t0 + j) / c.n_out, cl = (t0 + j) % c.n_out;
-            if (c.labels.p)
-                msvm::launch_ovr_labels(c.labels.p, n, cl, c.y.p, cx.stream);
-            ss.emplace_back(new msvm::Solver(cx, c.f, c.y.p, o,
-                                             L > 1 ? nullptr : &rc,
-                                             c.fold.p, fo));
-            gp.push_back(ss.back().get());
-        }
-        std::vector<msvm::SolveResult> rr;
-        if (G == 1)
-            rr.push_back(gp[0]->train());
-        else
-            rr = msvm::Solver::train_lockstep(gp);
-        for (int j = 0; j < G; ++j)
-            collect((t0 + j) / c.n_out, (t0 + j) % c.n_out, *gp[j],
-                    rr[(size_t)j]);
-    }
+    svm_status worst = SVM_OK;
+};
+
+// Metrics of one cross-validation's decision values D (device, n x n_out)
+// into stats.
+void cv_finish(CvData& c, const svm_params* p, int32_t k, double* D,
+               const CvAcc& a, svm_cv_stats* stats, msvm::Context& cx)
+{
+    const int64_t n = c.f.n;
     if (p->type == SVM_EPS_SVR && c.y_sd > 0.0)
         msvm::launch_affine(D, n, c.y_sd, c.y_mu, cx.stream);
     msvm::DevBuf<double> sums(7);
@@ -641,12 +606,12 @@ svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
     std::memset(stats, 0, sizeof(*stats));
     stats->folds = k;
     stats->n = n;
-    stats->status = worst;
-    stats->iters = iters;
-    stats->kernel_rows = kernel_rows;
-    stats->row_kernel_ms = row_ms;
-    stats->row_kernel_launches = row_launches;
-    stats->row_kernel_bytes = row_bytes;
+    stats->status = a.worst;
+    stats->iters = a.iters;
+    stats->kernel_rows = a.kernel_rows;
+    stats->row_kernel_ms = a.row_ms;
+    stats->row_kernel_launches = a.row_launches;
+    stats->row_kernel_bytes = a.row_bytes;
     const double nn = (double)n;
     if (p->type == SVM_C_SVC) {
         stats->accuracy = h[0] / nn;
@@ -657,6 +622,86 @@ svm_status cv_run(CvData& c, const svm_params* p, int32_t k, double* D,
         const double den = (nn * h[4] - h[2] * h[2]) * (nn * h[5] - h[3] * h[3]);
         stats->scc = den > 0.0 ? num * num / den : 0.0;
         stats->error = stats->mse;
+    }
+}
+
+// Cross-validations of the parameter sets ps (one D and stats each): k
+// trainings each (per class for one-vs-rest), each on the rows outside one
+// fold; the decision values of the held-out rows into D[g] (device, n x
+// n_out), then the metrics.  One after another with a row cache per
+// parameter set, or every (parameter set, fold, class) training in
+// lockstep groups.
+svm_status cv_run_many(CvData& c, const std::vector<svm_params>& ps,
+                       int32_t k, const std::vector<double*>& D,
+                       std::vector<svm_cv_stats>& stats, msvm::Context& cx)
+{
+    const int64_t n = c.f.n;
+    const int NG = (int)ps.size();
+    std::vector<msvm::SolveOptions> opts;
+    for (const auto& p : ps) opts.push_back(msvm::make_options(&p, n, c.f.d));
+    std::vector<CvAcc> acc((size_t)NG);
+    auto collect = [&](int g, int32_t fo, int32_t cl, msvm::Solver& s,
+                       const msvm::SolveResult& r) {
+        s.cv_decision(D[(size_t)g], c.n_out, cl, c.fold.p, fo, r.b);
+        CvAcc& a = acc[(size_t)g];
+        a.iters += r.iters;
+        a.kernel_rows += r.kernel_rows;
+        a.row_ms += r.row_ms;
+        a.row_bytes += r.row_bytes;
+        a.row_launches += r.row_launches;
+        if (r.status != SVM_OK) a.worst = r.status;
+    };
+    const int L = lock_group(&ps[0], c.f);
+    const int32_t per = k * c.n_out;  // trainings of one parameter set
+    if (L == 1) {
+        for (int g = 0; g < NG; ++g) {
+            msvm::RowCache rc;  // K rows do not depend on fold or class
+            msvm::cache_init(rc, n, ps[(size_t)g].cache_bytes, cx);
+            for (int32_t t = 0; t < per; ++t) {
+                const int32_t fo = t / c.n_out, cl = t % c.n_out;
+                if (c.labels.p)
+                    msvm::launch_ovr_labels(c.labels.p, n, cl, c.y.p,
+                                            cx.stream);
+                msvm::Solver s(cx, c.f, c.y.p, opts[(size_t)g], &rc,
+                               c.fold.p, fo);
+                collect(g, fo, cl, s, s.train());
+            }
+        }
+    } else {
+        const int32_t T = NG * per;
+        for (int32_t t0 = 0; t0 < T; t0 += L) {
+            const int G = std::min<int>(L, T - t0);
+            std::vector<std::unique_ptr<msvm::Solver>> ss;
+            std::vector<msvm::Solver*> gp;
+            for (int j = 0; j < G; ++j) {
+                const int32_t t = t0 + j, g = t / per, r = t % per;
+                const int32_t fo = r / c.n_out, cl = r % c.n_out;
+                if (c.labels.p)
+                    msvm::launch_ovr_labels(c.labels.p, n, cl, c.y.p,
+                                            cx.stream);
+                ss.emplace_back(new msvm::Solver(cx, c.f, c.y.p,
+                                                 opts[(size_t)g], nullptr,
+                                                 c.fold.p, fo));
+                gp.push_back(ss.back().get());
+            }
+            std::vector<msvm::SolveResult> rr;
+            if (G == 1)
+                rr.push_back(gp[0]->train());
+            else
+                rr = msvm::Solver::train_lockstep(gp);
+            for (int j = 0; j < G; ++j) {
+                const int32_t t = t0 + j, g = t / per, r = t % per;
+                collect(g, r / c.n_out, r % c.n_out, *gp[(size_t)j],
+                        rr[(size_t)j]);
+            }
+        }
+    }
+    stats.assign((size_t)NG, svm_cv_stats{});
+    svm_status worst = SVM_OK;
+    for (int g = 0; g < NG; ++g) {
+        cv_finish(c, &ps[(size_t)g], k, D[(size_t)g], acc[(size_t)g],
+                  &stats[(size_t)g], cx);
+        if (acc[(size_t)g].worst != SVM_OK) worst = acc[(size_t)g].worst;
     }
     return worst;
 }
@@ -678,7 +723,10 @@ svm_status svm_cross_validate(const svm_matrix* X, const float* y,
     CvData c;
     cv_load(c, X, y, labels, n_classes, p, k, fold, cx);
     msvm::DevBuf<double> D((size_t)(X->n * c.n_out));
-    st = cv_run(c, p, k, D.p, stats, cx);
+    std::vector<svm_cv_stats> sv;
+    st = cv_run_many(c, std::vector<svm_params>(1, *p), k,
+                     std::vector<double*>(1, D.p), sv, cx);
+    *stats = sv[0];
     if (decision) {
         HIP_TRY(hipMemcpyAsync(decision, D.p,
                                (size_t)(X->n * c.n_out) * sizeof(double),
@@ -714,15 +762,18 @@ svm_status svm_tune(const svm_matrix* X, const float* y,
     msvm::Context cx(p->device, p->stream);
     CvData c;
     cv_load(c, X, y, labels, n_classes, p, k, fold, cx);
-    msvm::DevBuf<double> D((size_t)(X->n * c.n_out));
-    svm_status worst = SVM_OK;
+    // the decision values of every grid point (their trainings may share
+    // lockstep groups)
+    const size_t per = (size_t)(X->n * c.n_out);
+    msvm::DevBuf<double> D(per * (size_t)n_grid);
+    std::vector<double*> Dg;
+    for (int32_t g = 0; g < n_grid; ++g) Dg.push_back(D.p + per * (size_t)g);
+    std::vector<svm_cv_stats> cs;
+    const svm_status worst = cv_run_many(c, grid, k, Dg, cs, cx);
     *best = 0;
     for (int32_t g = 0; g < n_grid; ++g) {
-        svm_cv_stats cs;
-        if (cv_run(c, &grid[(size_t)g], k, D.p, &cs, cx) != SVM_OK)
-            worst = SVM_W_MAX_ITER;
-        cv_error[g] = cs.error;
-        if (cs.error < cv_error[*best]) *best = g;  // ties: the first
+        cv_error[g] = cs[(size_t)g].error;
+        if (cv_error[g] < cv_error[*best]) *best = g;  // ties: the first
     }
     if (worst == SVM_W_MAX_ITER)
         return fail(SVM_W_MAX_ITER, "max_iter reached in at least one fold");

@@ -52,11 +52,8 @@ def test_ovr_lockstep_equals_sequential(lockstep):
 
 def test_ovr_lockstep_few_features_four_problems():
     # 10 classes in groups of 4, 4 and 2; 40 features: four problems a pass
-    rng = np.random.default_rng(11)
-    n, d, k = 2003, 40, 10
-    P = rng.standard_normal((k, d)) * 1.5
-    lab = rng.integers(0, k, n).astype(np.int32)
-    X = (P[lab] + rng.standard_normal((n, d))).astype(np.float32)
+    X, lab = _ten_classes()
+    k = 10
     kw = dict(C=2.0, gamma=0.02, tol=1e-3, cache_bytes=-1)
     seq = nv.svm_train_ovr(X, lab, k, **kw)
     lock = nv.svm_train_ovr(X, lab, k, lockstep=4, **kw)
@@ -121,14 +118,52 @@ def test_cv_lockstep_against_oracle():
 
 
 def test_tune_lockstep_equals_sequential():
+    # 3 grid points x 3 folds in groups of 4: groups mix grid points with
+    # different C and gamma
     w = workloads.c1(n=900, n_test=10)
     Cs = np.array([0.1, 1.0, 10.0])
     gs = np.array([0.05, 0.05, 0.2])
     kw = dict(k=3, C=Cs, gamma=gs, tol=w.tol, cache_bytes=-1)
     e0, b0 = nv.svm_tune(w.X, w.y, **kw)
-    e1, b1 = nv.svm_tune(w.X, w.y, lockstep=3, **kw)
+    e1, b1 = nv.svm_tune(w.X, w.y, lockstep=4, **kw)
     np.testing.assert_array_equal(e0, e1)
     assert b0 == b1
+
+
+def test_tune_svr_epsilon_grid_lockstep():
+    w = workloads.c2(n=800, n_test=10)
+    eps = np.array([0.05, 0.1, 0.3])
+    kw = dict(k=2, type=EPS_SVR, C=np.full(3, w.C), gamma=np.full(3, w.gamma),
+              epsilon=eps, tol=w.tol, cache_bytes=-1)
+    e0, b0 = nv.svm_tune(w.X, w.y, **kw)
+    e1, b1 = nv.svm_tune(w.X, w.y, lockstep=4, **kw)
+    np.testing.assert_array_equal(e0, e1)
+    assert b0 == b1
+
+
+def _ten_classes(n=2003, d=40, seed=11):
+    rng = np.random.default_rng(seed)
+    P = rng.standard_normal((10, d)) * 1.5
+    lab = rng.integers(0, 10, n).astype(np.int32)
+    X = (P[lab] + rng.standard_normal((n, d))).astype(np.float32)
+    return X, lab
+
+
+def test_lockstep_iteration_cap():
+    # max_iter between the classes' iteration counts: some classes stop at
+    # the cap (warning) while the others of their group converge; the same
+    # states as one class after another
+    X, lab = _ten_classes()
+    kw = dict(C=2.0, gamma=0.02, tol=1e-3, cache_bytes=-1)
+    free = nv.svm_train_ovr(X, lab, 10, **kw)
+    its = sorted(free.info(c)["iters"] for c in range(10))
+    cap = its[5]
+    assert its[0] < cap < its[-1]
+    seq = nv.svm_train_ovr(X, lab, 10, max_iter=cap, **kw)
+    lock = nv.svm_train_ovr(X, lab, 10, max_iter=cap, lockstep=4, **kw)
+    _same_ovr(seq, lock, 10)
+    st = [lock.info(c)["status"] for c in range(10)]
+    assert nv.SVM_W_MAX_ITER in st and nv.SVM_OK in st
 
 
 def test_lockstep_profile_splits_the_pass():
