@@ -85,45 +85,55 @@ void launch_check_finite(const float* v, int64_t n, int32_t* bad,
 // 0 outside I_up and I_low, so no working set takes them and the solve is
 // the dual restricted to the other rows.  bad: 1 an invalid label or
 // target, 2 / 4 a positive / negative training row seen.
-__global__ void k_init_state(int32_t type, const float* y, int64_t n,
-                             const int32_t* fold, int32_t held, uint8_t* st,
-                             int32_t* bad)
+__global__ __launch_bounds__(256) void k_init_state(int32_t type,
+                                                   const float* y, int64_t n,
+                                                   const int32_t* fold,
+                                                   int32_t held, uint8_t* st,
+                                                   int32_t* bad)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    __shared__ int wflags[4];
     int flags = 0;  // 1 bad value, 2 a training +1, 4 a training -1
-    if (i < n) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * 256) {
         const bool train = !fold || fold[i] != held;
         const uint8_t up = train ? ST_UP : 0, low = train ? ST_LOW : 0;
         if (type == SVM_C_SVC) {
             const float v = y[i];
             if (v == 1.0f) {
                 st[i] = ST_YPOS | up;
-                flags = train ? 2 : 0;
+                flags |= train ? 2 : 0;
             } else if (v == -1.0f) {
                 st[i] = low;
-                flags = train ? 4 : 0;
+                flags |= train ? 4 : 0;
             } else {
                 st[i] = 0;
-                flags = 1;
+                flags |= 1;
             }
         } else {
             st[i] = ST_YPOS | up;
             st[n + i] = low;
-            flags = isfinite(y[i]) ? 0 : 1;
+            flags |= isfinite(y[i]) ? 0 : 1;
         }
     }
-    // one atomic per wave
+    // one atomic per block (atomics on one address serialise)
     const int w = (__ballot(flags & 1) ? 1 : 0) | (__ballot(flags & 2) ? 2 : 0) |
                   (__ballot(flags & 4) ? 4 : 0);
-    if ((threadIdx.x & 63) == 0 && w) atomicOr(bad, w);
+    if ((threadIdx.x & 63) == 0) wflags[threadIdx.x >> 6] = w;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int f = wflags[0] | wflags[1] | wflags[2] | wflags[3];
+        if (f) atomicOr(bad, f);
+    }
 }
 
 void launch_init_state(int32_t type, const float* y, int64_t n,
                        const int32_t* fold, int32_t held, uint8_t* st,
                        int32_t* bad, hipStream_t s)
 {
-    k_init_state<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(type, y, n, fold,
-                                                             held, st, bad);
+    const int64_t nb = std::max<int64_t>(
+        1, std::min<int64_t>(512, (n + 255) / 256));
+    k_init_state<<<(unsigned)nb, 256, 0, s>>>(type, y, n, fold, held, st,
+                                              bad);
 }
 
 // Decision values of the rows held out of a training: out[i * stride +

@@ -746,10 +746,17 @@ std::vector<SolveResult> Solver::train_lockstep(
         if (t <= tiles) break;
         tiles = t;
     }
+    const int64_t rec_cap = (int64_t)kSelThreads * kSelRecords;
     int64_t nb = std::min(cap_blocks, (tiles_total + kWaves - 1) / kWaves);
-    nb = std::max<int64_t>(
-        1, std::min({nb, (int64_t)kSelThreads * kSelRecords, units}));
+    nb = std::max<int64_t>(1, std::min({nb, rec_cap, units}));
     tiles = wave_tiles(nb);
+    // the staged rows of many features leave little LDS for the row data:
+    // more blocks (not all resident at once), fewer tiles per wave
+    while (lock_lds_bytes(G, f.ldp, tiles, svr) > kLdsMax &&
+           nb < std::min(rec_cap, units)) {
+        nb = std::min({2 * nb, rec_cap, units});
+        tiles = wave_tiles(nb);
+    }
     if (lock_lds_bytes(G, f.ldp, tiles, svr) > kLdsMax ||
         (int64_t)16 * tiles * f.ldp * 4 >= ((int64_t)1 << 31))
         throw Error{SVM_E_UNSUPPORTED,
