@@ -131,7 +131,9 @@ typedef struct {
                               when the working-set rows of more would not
                               fit the row kernel's LDS (2 at d = 784).  > 1
                               needs dense X and working_set = 16, else
-                              SVM_E_UNSUPPORTED.  No effect on svm_train */
+                              SVM_E_UNSUPPORTED.  No effect on svm_train.
+                              train_ms of a problem then spans its group's
+                              run (the groups' problems overlap in time) */
 } svm_params;
 
 /* Result of a k-fold cross-validation. */

@@ -178,3 +178,15 @@ def test_lockstep_profile_splits_the_pass():
     assert s1["row_kernel_ms"] > 0
     # X is read once per pass instead of once per problem
     assert s1["row_kernel_bytes"] < s0["row_kernel_bytes"]
+
+
+def test_fullsize_c3_cv10_lockstep4():
+    # the configuration `bench.py --cv 10 --lockstep 4` times: C3 at full
+    # size (n = 100000, d = 128), 10 folds in groups of 4, 4 and 2
+    w = workloads.make("C3")
+    kw = dict(k=10, C=w.C, gamma=w.gamma, tol=w.tol, cache_bytes=-1)
+    D0, s0 = nv.svm_cross_validate(w.X, w.y, **kw)
+    D1, s1 = nv.svm_cross_validate(w.X, w.y, lockstep=4, **kw)
+    np.testing.assert_array_equal(D0, D1)
+    assert s0["iters"] == s1["iters"] and s0["accuracy"] == s1["accuracy"]
+    assert s1["rc"] == nv.SVM_OK and 0.98 < s1["accuracy"] < 1.0
