@@ -287,11 +287,9 @@ size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
                       int csr_cols);
 int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
-// one block per problem; `host` (P entries, each with working sets of 16;
-// their slice is set here) is copied to `dev` first when `upload` is set,
-// and must stay unchanged until the stream has passed the copy
-void launch_select_group(SelArgs* host, SelArgs* dev, int P, bool upload,
-                         bool svr, hipStream_t s);
+// one block per problem (P <= kLockMax entries, each with working sets of
+// 16), the arguments passed by value in the launch
+void launch_select_group(const SelArgs* args, int P, bool svr, hipStream_t s);
 // lockstep row/update kernel of P problems (dense features, q = 16 each)
 void launch_lock(const LockArgs& a, int P, int nblocks, bool svr,
                  hipStream_t s, hipEvent_t e0 = nullptr,

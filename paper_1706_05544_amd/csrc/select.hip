@@ -1234,13 +1234,15 @@ __global__ __launch_bounds__(kSelThreads) void k_select(SelArgs a)
 }
 
 // One problem per block: several selections of problems that advance in
-// lockstep (working sets of 16 each).
+// lockstep (working sets of 16 each).  The arguments travel in the launch.
+struct SelGroup {
+    SelArgs a[kLockMax];
+};
+
 template <bool SVR>
-__global__ __launch_bounds__(kSelThreads) void k_select_group(
-    const SelArgs* __restrict__ args)
+__global__ __launch_bounds__(kSelThreads) void k_select_group(SelGroup g)
 {
-    const SelArgs a = args[blockIdx.x];
-    select_body<SVR, 1>(a);
+    select_body<SVR, 1>(g.a[blockIdx.x]);
 }
 
 template <bool SVR, int NBLK>
@@ -1263,21 +1265,18 @@ static void select_dispatch(const SelArgs& a, hipStream_t s)
     k_select<SVR, NBLK><<<1, kSelThreads, lds, s>>>(a);
 }
 
-void launch_select_group(SelArgs* host, SelArgs* dev, int P, bool upload,
-                         bool svr, hipStream_t s)
+void launch_select_group(const SelArgs* args, int P, bool svr, hipStream_t s)
 {
-    if (P <= 0) return;
+    if (P <= 0 || P > kLockMax)
+        throw Error{SVM_E_INTERNAL, "bad lockstep selection"};
+    SelGroup g{};
     const int slice =
-        host[0].slice > 0 ? host[0].slice : select_slice(1, host[0].ldp);
-    if (upload) {
-        for (int p = 0; p < P; ++p) {
-            if (host[p].rp || host[p].ldp != host[0].ldp)
-                throw Error{SVM_E_INTERNAL, "bad lockstep selection"};
-            host[p].slice = slice;
-        }
-        // (host stays untouched until the stream has passed this copy)
-        HIP_TRY(hipMemcpyAsync(dev, host, sizeof(SelArgs) * P,
-                               hipMemcpyHostToDevice, s));
+        args[0].slice > 0 ? args[0].slice : select_slice(1, args[0].ldp);
+    for (int p = 0; p < P; ++p) {
+        if (args[p].rp || args[p].ldp != args[0].ldp)
+            throw Error{SVM_E_INTERNAL, "bad lockstep selection"};
+        g.a[p] = args[p];
+        g.a[p].slice = slice;
     }
     const size_t lds = select_lds_bytes(1, slice);
     static size_t lds_allowed[2] = {32 * 1024, 32 * 1024};
@@ -1294,9 +1293,9 @@ void launch_select_group(SelArgs* host, SelArgs* dev, int P, bool upload,
         lds_allowed[svr] = lds;
     }
     if (svr)
-        k_select_group<true><<<P, kSelThreads, lds, s>>>(dev);
+        k_select_group<true><<<P, kSelThreads, lds, s>>>(g);
     else
-        k_select_group<false><<<P, kSelThreads, lds, s>>>(dev);
+        k_select_group<false><<<P, kSelThreads, lds, s>>>(g);
 }
 
 void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)

@@ -772,8 +772,7 @@ std::vector<SolveResult> Solver::train_lockstep(
         ck[p].alloc((size_t)nb * 2 * kBlockTop);
         ci[p].alloc((size_t)nb * 2 * kBlockTop);
     }
-    DevBuf<SelArgs> dsel(kLockMax);
-    HostBuf<SelArgs> hsel(kLockMax);
+    std::vector<SelArgs> hsel(kLockMax);
     HostBuf<WorkingSet> hws((size_t)2 * G);
     std::vector<int> act(G);
     for (int p = 0; p < G; ++p) act[p] = p;
@@ -824,7 +823,7 @@ std::vector<SolveResult> Solver::train_lockstep(
             a.max_iter = s.o_.max_iter;
             a.mode = SS_SOLVE | SS_CHECK_DONE;
             a.group_rows = kWaves * 16 * tiles;  // most rows of a block
-            hsel.p[q] = a;
+            hsel[q] = a;
         }
     };
 
@@ -852,11 +851,11 @@ std::vector<SolveResult> Solver::train_lockstep(
     };
     std::vector<int64_t> last(G, 0);
     std::vector<int> ran(2, 0);  // problems in each chunk
-    auto enqueue = [&](int slot, bool upload) {
+    auto enqueue = [&](int slot) {
         const int P = (int)act.size();
         ran[slot] = P;
         for (int k = 0; k < K; ++k) {
-            launch_select_group(hsel.p, dsel.p, P, upload && k == 0, svr, st);
+            launch_select_group(hsel.data(), P, svr, st);
             if (prof)
                 launch_lock(la, P, (int)nb, svr, st,
                             pe[(size_t)(slot * K + k) * 2],
@@ -899,8 +898,8 @@ std::vector<SolveResult> Solver::train_lockstep(
     };
 
     try {
-        enqueue(0, true);
-        enqueue(1, false);
+        enqueue(0);
+        enqueue(1);
         int cur = 0;
         for (;;) {
             HIP_TRY(hipEventSynchronize(ev[cur]));
@@ -938,12 +937,12 @@ std::vector<SolveResult> Solver::train_lockstep(
                 if (next.empty()) break;
                 act = next;
                 build();
-                enqueue(0, true);
-                enqueue(1, false);
+                enqueue(0);
+                enqueue(1);
                 cur = 0;
                 continue;
             }
-            enqueue(cur, false);
+            enqueue(cur);
             cur ^= 1;
         }
         cx.sync();
