@@ -320,7 +320,6 @@ __global__ __launch_bounds__(kRowThreads) void k_lock(LockArgs a)
                         part[v] = row_sum_f64(fma(cf[p], (double)kv[v], 0.0));
                     const double Fn = Fw0[p * RW + orl] + pick4(part, nl & 3);
                     if (nl < 4) Fw0[p * RW + orl] = Fn;
-                    push(p, orl, Fn, nl < 4 && orl < nw);
                 }
             }
             if (++psl == nslab) {
@@ -329,11 +328,21 @@ __global__ __launch_bounds__(kRowThreads) void k_lock(LockArgs a)
             }
         }
     }
+    // the new F back, and the keys of the wave's variables, one row per
+    // lane (the candidates do not depend on which lane saw a row)
+    __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int p = 0; p < P; ++p) {
         if (!live[p]) continue;
         const Rsrc rF = make_rsrc(a.F[p] + rw0, (int64_t)nw * 8);
-        for (int r = lane; r < nw; r += 64) bst_f64(rF, 8 * r, Fw0[p * RW + r]);
+        for (int r0 = 0; r0 < nw; r0 += 64) {
+            const int r = r0 + lane;
+            const bool own = r < nw;
+            const int rr = own ? r : 0;
+            const double Fn = Fw0[p * RW + rr];
+            if (own) bst_f64(rF, 8 * r, Fn);
+            push(p, rr, Fn, own);
+        }
     }
 
     // each problem's best two of each side over the block's rows (as k_rows)
