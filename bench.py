@@ -152,8 +152,9 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only; --gpus %d is not "
-              "supported (the multi-GPU design is described in DESIGN.md)"
+        print("bench.py: the library runs on one GPU; --gpus %d is not "
+              "supported (the training rows would be sharded over GPUs, "
+              "with one exchange of selection candidates per iteration)"
               % args.gpus, file=sys.stderr)
         return 2
 
@@ -193,10 +194,12 @@ def main() -> int:
               working_set=args.working_set, kernel=kernel,
               degree=args.degree, coef0=args.coef0,
               scale=1 if args.scale else 0)
-    if args.lockstep > 1:
-        kw["lockstep"] = args.lockstep
-
     multi = w.n_classes > 2
+    # lockstep applies to one-vs-rest classes and cross-validation folds
+    lock = args.lockstep if (args.lockstep > 1 and (multi or args.cv > 1)) \
+        else 0
+    if lock:
+        kw["lockstep"] = lock
     if multi:
         kw.pop("type")
         kw.pop("epsilon")
@@ -351,8 +354,8 @@ def main() -> int:
                            if args.cv > 1 else
                            "predict %d points" % w.Xt.shape[0])
                         + ("; features standardised" if args.scale else "")
-                        + ("; %d problems in lockstep" % args.lockstep
-                           if args.lockstep > 1 else ""),
+                        + ("; %d problems in lockstep" % lock
+                           if lock else ""),
             "kernel": args.kernel,
             "n": w.n, "d": w.d, "n_test": int(w.Xt.shape[0]),
             "working_set": args.working_set,
@@ -378,7 +381,7 @@ def main() -> int:
                 row_bytes_per_launch(w.n, w.d, w.type == workloads.EPS_SVR)
                 if not hasattr(w.X, "indptr") else None),
             "launches_timed": launches,
-        } if args.lockstep <= 1 else {
+        } if not lock else {
             # k_lock: each pass computes the dot products of every row with
             # the P working sets on the matrix cores; the statistics split
             # each pass's time over its problems, so the sum over problems
