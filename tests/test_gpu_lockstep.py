@@ -190,3 +190,18 @@ def test_fullsize_c3_cv10_lockstep4():
     np.testing.assert_array_equal(D0, D1)
     assert s0["iters"] == s1["iters"] and s0["accuracy"] == s1["accuracy"]
     assert s1["rc"] == nv.SVM_OK and 0.98 < s1["accuracy"] < 1.0
+
+
+@pytest.mark.parametrize("d", [900, 2000])
+def test_lockstep_many_features(d):
+    # d = 900: two problems fill the LDS of a pass; d = 2000: not even two
+    # fit, so the folds run one after another (without the cache)
+    rng = np.random.default_rng(d)
+    n = 603
+    y = np.where(rng.standard_normal(n) > 0, 1.0, -1.0).astype(np.float32)
+    X = (rng.standard_normal((n, d)) + 0.05 * y[:, None]).astype(np.float32)
+    kw = dict(k=3, C=1.0, gamma=1.0 / d, tol=1e-3, cache_bytes=-1)
+    D0, s0 = nv.svm_cross_validate(X, y, **kw)
+    D1, s1 = nv.svm_cross_validate(X, y, lockstep=4, **kw)
+    np.testing.assert_array_equal(D0, D1)
+    assert s0["iters"] == s1["iters"] and s1["rc"] == nv.SVM_OK
