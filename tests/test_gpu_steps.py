@@ -35,10 +35,16 @@ def _work(name, n, d):
 
 
 def _oracle_state(w, steps):
+    """The oracle's state after `steps` pair steps from alpha = 0; steps = 0
+    is the start state (alpha = 0, F = 0) itself, where every C-SVC key
+    ties at +1 or -1 (the oracle's max_steps = 0 would mean no cap)."""
     p = Params(w.type, C=w.C, eps=w.eps, gamma=w.gamma, tol=w.tol)
     N = oracle.num_vars(w.type, w.n)
+    if steps == 0:
+        return p, np.zeros(N), np.zeros(w.n)
     r = oracle.solve(w.X, w.y, p, np.zeros(N), np.zeros(w.n),
                      max_steps=steps)
+    assert r.iters == steps
     return p, r.alpha, r.F
 
 
@@ -74,6 +80,51 @@ def test_select_matches_oracle(name, n, d, steps, q):
     Be, me, Me = oracle.select(w.y, p, alpha, F, q, d=w.d)
     assert m == me and M == Me
     assert list(B) == list(Be)
+
+
+def _interleave(U, L):
+    B = []
+    for k in range(max(len(U), len(L))):
+        for side in (U, L):
+            if k < len(side) and side[k] not in B:
+                B.append(side[k])
+    return B
+
+
+@pytest.mark.parametrize("n", [333, 5000])
+@pytest.mark.parametrize("q", [2, 6, 16, 32])
+def test_select_alpha0_takes_lowest_indices(n, q):
+    # alpha = 0, F = 0: every up key is +1 (the +1 class), every low key -1
+    # (the -1 class), so the working set is the q/2 lowest indices of each
+    # class, interleaved.  Thousands of tied candidates spread over all the
+    # row kernel's blocks: the merge must keep the lowest indices.
+    w = workloads.c1(n=n, n_test=10)
+    s = _solver(w, q)
+    s.set_state(np.zeros(n), np.zeros(n))
+    B, m, M = s.select()
+    pos = [int(i) for i in np.nonzero(w.y > 0)[0][: q // 2]]
+    neg = [int(i) for i in np.nonzero(w.y < 0)[0][: q // 2]]
+    assert list(B) == _interleave(pos, neg)
+    assert (m, M) == (1.0, -1.0)
+
+
+@pytest.mark.parametrize("q", [2, 16])
+def test_select_alpha0_svr_ties(q):
+    # eps-SVR at alpha = 0 with targets in {0, 1}: the up side is the copies
+    # (i,+) with z_i = 1, the low side the copies (i,-) = n + i with z_i =
+    # 0, each in increasing index order.
+    rng = np.random.default_rng(5)
+    n, d = 3000, 9
+    X = rng.normal(size=(n, d)).astype(np.float32)
+    z = (rng.random(n) < 0.4).astype(np.float32)
+    s = nv.Solver(X, z, type=EPS_SVR, C=1.0, epsilon=0.1, gamma=0.5,
+                  tol=1e-3, working_set=q)
+    s.set_state(np.zeros(2 * n), np.zeros(n))
+    B, m, M = s.select()
+    up = [int(i) for i in np.nonzero(z == 1)[0][: q // 2]]
+    lo = [int(n + i) for i in np.nonzero(z == 0)[0][: q // 2]]
+    assert list(B) == _interleave(up, lo)
+    assert m == np.float64(np.float32(1.0)) - 0.1 and M == 0.0 + 0.1
 
 
 @pytest.mark.parametrize("name,n,d", SHAPES[:4])

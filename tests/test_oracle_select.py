@@ -30,9 +30,15 @@ def _vars(w):
 
 
 def _state(orc, w, steps):
+    """The state after `steps` pair steps from alpha = 0; steps = 0 is the
+    start state itself (alpha = 0, F = 0), built here: solve's max_steps = 0
+    means "no cap"."""
     p = Params(w.type, C=w.C, eps=w.eps, gamma=w.gamma, tol=w.tol)
     N = orc.num_vars(w.type, w.n)
+    if steps == 0:
+        return p, np.zeros(N), np.zeros(w.n)
     res = orc.solve(w.X, w.y, p, np.zeros(N), np.zeros(w.n), max_steps=steps)
+    assert res.iters == steps
     return p, res.alpha, res.F
 
 
@@ -136,3 +142,91 @@ def test_subproblem_reaches_restricted_optimum(orc, name, steps, q):
     assert f_or == pytest.approx(f_star, rel=1e-8, abs=1e-10)
     assert abs(yy[B] @ dd) < 1e-10
     assert np.all(aB >= 0) and np.all(aB <= w.C)
+
+
+# ---------------------------------------------------------------------------
+# Tie-break (lowest variable index among equal keys) pinned by states whose
+# working set follows from the labels alone.
+# ---------------------------------------------------------------------------
+
+def _interleave(U, L):
+    B = []
+    for k in range(max(len(U), len(L))):
+        for side in (U, L):
+            if k < len(side) and side[k] not in B:
+                B.append(side[k])
+    return B
+
+
+@pytest.mark.parametrize("q", [2, 6, 16])
+def test_select_alpha0_svc_takes_lowest_indices(orc, q):
+    # At alpha = 0 and F = 0 every C-SVC key is v_t = y_t: I_up is the +1
+    # class with key +1, I_low the -1 class with key -1.  Every key of a
+    # side ties, so the q/2 largest (smallest) are the q/2 lowest indices
+    # of each class, and m = 1, M = -1.
+    w = workloads.c1(n=400, n_test=10)
+    p = Params(C_SVC, C=w.C, gamma=w.gamma, tol=w.tol)
+    B, m, M = orc.select(w.y, p, np.zeros(w.n), np.zeros(w.n), q, d=w.d)
+    pos = [int(i) for i in np.nonzero(w.y > 0)[0][: q // 2]]
+    neg = [int(i) for i in np.nonzero(w.y < 0)[0][: q // 2]]
+    assert list(B) == _interleave(pos, neg)
+    assert (m, M) == (1.0, -1.0)
+
+
+@pytest.mark.parametrize("q", [2, 6, 16])
+def test_select_alpha0_svr_ties_on_targets(orc, q):
+    # eps-SVR at alpha = 0, F = 0: copy (i,+) is in I_up with key z_i - eps,
+    # copy (i,-) (variable n + i) in I_low with key z_i + eps.  Targets in
+    # {0, 1}: the largest up keys are the copies (i,+) with z_i = 1, the
+    # smallest low keys the copies (i,-) with z_i = 0, each in increasing
+    # index order.
+    rng = np.random.default_rng(5)
+    n = 300
+    z = (rng.random(n) < 0.4).astype(np.float32)
+    eps = 0.1
+    p = Params(EPS_SVR, C=1.0, eps=eps, gamma=0.5, tol=1e-3)
+    B, m, M = orc.select(z, p, np.zeros(2 * n), np.zeros(n), q, d=4)
+    up = [int(i) for i in np.nonzero(z == 1)[0][: q // 2]]
+    lo = [int(n + i) for i in np.nonzero(z == 0)[0][: q // 2]]
+    assert list(B) == _interleave(up, lo)
+    assert m == np.float64(1.0) - eps and M == 0.0 + eps
+
+
+@pytest.mark.parametrize("q", [4, 16])
+def test_select_tied_keys_by_counting(orc, q):
+    # A state with bounded and free variables and keys on a coarse grid
+    # (many ties): the working set by brute force, each entry's place in a
+    # side being the number of entries that precede it (larger key for
+    # I_up, smaller for I_low, equal keys ordered by index).
+    w = workloads.c1(n=240, n_test=10)
+    rng = np.random.default_rng(11)
+    C = w.C
+    alpha = rng.choice([0.0, 0.5 * C, C], size=w.n)
+    F = np.round(rng.normal(size=w.n) * 2) / 4  # keys on a 0.25 grid
+    p = Params(C_SVC, C=C, gamma=w.gamma, tol=w.tol)
+    B, m, M = orc.select(w.y, p, alpha, F, q, d=w.d)
+    yy = np.where(w.y > 0, 1.0, -1.0)
+    v = yy - F
+    up = [t for t in range(w.n)
+          if (yy[t] > 0 and alpha[t] < C) or (yy[t] < 0 and alpha[t] > 0)]
+    lo = [t for t in range(w.n)
+          if (yy[t] > 0 and alpha[t] > 0) or (yy[t] < 0 and alpha[t] < C)]
+
+    def place(side, t, sign):
+        return sum(1 for u in side
+                   if sign * v[u] > sign * v[t] or (v[u] == v[t] and u < t))
+
+    U = [None] * (q // 2)
+    for t in up:
+        k = place(up, t, 1.0)
+        if k < q // 2:
+            U[k] = t
+    L = [None] * (q // 2)
+    for t in lo:
+        k = place(lo, t, -1.0)
+        if k < q // 2:
+            L[k] = t
+    assert list(B) == _interleave(U, L)
+    assert m == max(v[up]) and M == min(v[lo])
+    # the grid really ties entries inside the selected prefix
+    assert len(set(v[U])) < len(U) or len(set(v[L])) < len(L)
