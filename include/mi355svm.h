@@ -44,6 +44,10 @@ extern "C" {
 typedef enum {
     SVM_OK = 0,
     SVM_W_MAX_ITER = 1,        /* max_iter reached; model valid, gap > tol */
+    SVM_W_NOT_CONVERGED = 2,   /* the gap met tol on the incrementally
+                                  updated responses but not, after 3
+                                  re-runs, on responses recomputed from
+                                  alpha; model valid, gap (recomputed) > tol */
     SVM_E_INVALID = -1,        /* bad argument (message says which) */
     SVM_E_UNSUPPORTED = -2,    /* valid but not implemented (e.g. kernel) */
     SVM_E_NOMEM = -3,          /* device or host allocation failed */
@@ -300,6 +304,15 @@ svm_status svm_test_apply(svm_solver *s, const int32_t *B, int32_t nB,
 /* Run up to k full outer iterations; *iters gets the count, *gap the gap. */
 svm_status svm_test_iterate(svm_solver *s, int64_t k, int64_t *iters,
                             double *gap);
+
+/* End a training on the current state as svm_train ends it: recompute F
+ * from alpha, re-test the gap and, while it exceeds tol, run the loop again
+ * and re-test, at most max_passes (>= 0) times (svm_train uses 3).  *gap,
+ * *b (bias, reading R6: mean key over free variables, else (m + M) / 2) and
+ * *obj (f(a)) come from the recomputed responses; *status is SVM_OK,
+ * SVM_W_MAX_ITER or SVM_W_NOT_CONVERGED (the gap still above tol). */
+svm_status svm_test_finish(svm_solver *s, int32_t max_passes, double *gap,
+                           double *b, double *obj, int32_t *status);
 
 #ifdef __cplusplus
 }

@@ -22,6 +22,20 @@ svm_status fail(svm_status st, const std::string& msg)
 
 bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
 
+// The warning status of a training whose model was written, with its
+// message (SVM_OK: nothing to say).
+svm_status warn(svm_status st, const char* where)
+{
+    if (st == SVM_W_MAX_ITER)
+        return fail(st, std::string("max_iter reached before the gap met tol") +
+                            where);
+    if (st == SVM_W_NOT_CONVERGED)
+        return fail(st, std::string("the gap on the responses recomputed from "
+                                    "alpha stayed above tol") +
+                            where);
+    return SVM_OK;
+}
+
 svm_status check_params(const svm_params* p)
 {
     if (!p) return fail(SVM_E_INVALID, "params is NULL");
@@ -314,9 +328,7 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
     m->info.resize(1);
     fill_info(m->info[0], *m, r);
     *out = m.release();
-    if (r.status == SVM_W_MAX_ITER)
-        return fail(SVM_W_MAX_ITER, "max_iter reached before the gap met tol");
-    return SVM_OK;
+    return warn(r.status, "");
     GUARD_END
 }
 
@@ -423,9 +435,7 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     for (int32_t c = 0; c < n_classes; ++c)
         fill_info(m->info[(size_t)c], *m, res[(size_t)c]);
     *out = m.release();
-    if (worst == SVM_W_MAX_ITER)
-        return fail(SVM_W_MAX_ITER, "max_iter reached for at least one class");
-    return SVM_OK;
+    return warn(worst, " (at least one class)");
     GUARD_END
 }
 
@@ -733,9 +743,7 @@ svm_status svm_cross_validate(const svm_matrix* X, const float* y,
                                hipMemcpyDeviceToHost, cx.stream));
         cx.sync();
     }
-    if (st == SVM_W_MAX_ITER)
-        return fail(SVM_W_MAX_ITER, "max_iter reached in at least one fold");
-    return SVM_OK;
+    return warn(st, " (at least one fold)");
     GUARD_END
 }
 
@@ -775,9 +783,7 @@ svm_status svm_tune(const svm_matrix* X, const float* y,
         cv_error[g] = cs[(size_t)g].error;
         if (cv_error[g] < cv_error[*best]) *best = g;  // ties: the first
     }
-    if (worst == SVM_W_MAX_ITER)
-        return fail(SVM_W_MAX_ITER, "max_iter reached in at least one fold");
-    return SVM_OK;
+    return warn(worst, " (at least one fold)");
     GUARD_END
 }
 
@@ -910,6 +916,23 @@ svm_status svm_test_iterate(svm_solver* s, int64_t k, int64_t* iters,
 {
     if (!iters || !gap || k < 0) return fail(SVM_E_INVALID, "bad arguments");
     SOLVER_CALL(s->s->iterate(k, iters, gap))
+}
+
+svm_status svm_test_finish(svm_solver* s, int32_t max_passes, double* gap,
+                           double* b, double* obj, int32_t* status)
+{
+    if (!gap || !b || !obj || !status || max_passes < 0)
+        return fail(SVM_E_INVALID, "bad arguments");
+    if (!s) return fail(SVM_E_INVALID, "solver is NULL");
+    GUARD_BEGIN
+    msvm::SolveResult r;
+    s->s->finish_state(max_passes, r);
+    *gap = r.gap;
+    *b = r.b;
+    *obj = r.obj;
+    *status = r.status;
+    return SVM_OK;
+    GUARD_END
 }
 
 }  // extern "C"

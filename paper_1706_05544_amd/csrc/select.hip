@@ -1053,8 +1053,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
                 int64_t clk = clk0;
                 // rows stop going to a cache that serves almost nothing (a
                 // working set whose samples rarely all recur): the fills
-                // cost HBM writes and the two paths give the same bits
-                const bool fill = iter0 < 512 || c_served * 8 >= c_filled;
+                // cost HBM writes and the two paths give the same bits.  A
+                // cache with a slot for every sample never evicts, so it
+                // keeps filling: every working set whose samples have all
+                // been used before is then served.
+                const bool fill = a.cache_slots >= a.n || iter0 < 512 ||
+                                  c_served * 8 >= c_filled;
                 if (missm == 0) {
                     path = PATH_CACHED;
                     cslot = hs;

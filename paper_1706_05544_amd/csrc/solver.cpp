@@ -609,13 +609,17 @@ hipEvent_t Solver::start(bool keys)
     return t0;
 }
 
-void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0)
+void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0, int max_passes)
 {
     hipEvent_t t1;
     HIP_TRY(hipEventCreate(&t1));
-    // The incremental responses accumulate rounding over many updates:
-    // recompute them from alpha and re-test the gap before accepting.
-    for (int pass = 0; pass < 4 && conv; ++pass) {
+    // The incremental responses accumulate rounding over many updates: F is
+    // recomputed from alpha and the gap re-tested on it.  A solve that met
+    // tol only on the incremental responses continues from the recomputed
+    // ones, at most max_passes times; the gap, m and M reported (and the
+    // bias and objective below) always come from recomputed responses, and
+    // SVM_OK only from a gap measured on them.
+    for (int pass = 0;; ++pass) {
         recompute_responses();
         launch_keys();
         launch_select_only();
@@ -624,12 +628,14 @@ void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0)
         r.gap = w.gap;
         r.m = w.m;
         r.M = w.M;
-        if (w.gap <= o_.tol) break;
+        if (!conv || w.gap <= o_.tol) break;  // (max_iter: status stands)
+        if (pass >= max_passes) {
+            r.status = SVM_W_NOT_CONVERGED;
+            break;
+        }
         launch_fill_i32(&ws_.p->done, 0, 1, cx_.stream);
         conv = run_loop(r);
-        if (!conv) break;
     }
-    if (!conv) recompute_responses();
 
     launch_summary(o_.type, alpha_.p, st_.p, F_.p, y_.p, n_, o_.C, o_.eps,
                    sum_.p, cx_.stream);
@@ -1209,6 +1215,12 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
         throw Error{SVM_E_UNSUPPORTED, "too many features for the row tile"};
     launch_rows(r, nb_, nbc, o_.type == SVM_EPS_SVR, s);
     cx_.sync();
+}
+
+void Solver::finish_state(int max_passes, SolveResult& r)
+{
+    hipEvent_t t0 = start(false);
+    finish(r, true, t0, max_passes);
 }
 
 void Solver::iterate(int64_t k, int64_t* iters, double* gap)

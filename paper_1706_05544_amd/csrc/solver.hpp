@@ -188,12 +188,17 @@ public:
                     int32_t max_inner, double* alpha_B, int32_t* steps);
     void apply(const int32_t* B, int32_t nB, const double* alpha_B);
     void iterate(int64_t k, int64_t* iters, double* gap);
+    // The end of a training on the current state: F recomputed from alpha,
+    // the gap re-tested and the loop re-run at most max_passes times, then
+    // bias, objective and counts.
+    void finish_state(int max_passes, SolveResult& r);
 
     int64_t N() const { return N_; }
 
 private:
     hipEvent_t start(bool keys);
-    void finish(SolveResult& r, bool conv, hipEvent_t t0);
+    void finish(SolveResult& r, bool conv, hipEvent_t t0,
+                int max_passes = 3);
     void launch_keys();
     void launch_hot_rows(hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
     void launch_solve(int32_t mode);

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libmi355svm.so")
 
 SVM_OK = 0
 SVM_W_MAX_ITER = 1
+SVM_W_NOT_CONVERGED = 2
 SVM_E_INVALID = -1
 SVM_E_UNSUPPORTED = -2
 SVM_E_NOMEM = -3
@@ -39,7 +40,7 @@ EXPORTS = [
     "svm_test_solver_create",
     "svm_test_solver_free", "svm_test_set_state", "svm_test_get_state",
     "svm_test_select", "svm_test_rows", "svm_test_subproblem",
-    "svm_test_apply", "svm_test_iterate",
+    "svm_test_apply", "svm_test_iterate", "svm_test_finish",
 ]
 
 
@@ -163,6 +164,9 @@ def load(path: Optional[str] = None):
     lib.svm_test_apply.argtypes = [vp, vp, ct.c_int32, vp]
     lib.svm_test_iterate.argtypes = [vp, ct.c_int64, P(ct.c_int64),
                                      P(ct.c_double)]
+    lib.svm_test_finish.argtypes = [vp, ct.c_int32, P(ct.c_double),
+                                    P(ct.c_double), P(ct.c_double),
+                                    P(ct.c_int32)]
     for name in EXPORTS:  # fail now, not at first use, if one is missing
         getattr(lib, name)
     _lib = lib
@@ -493,3 +497,12 @@ class Solver:
         _check(load().svm_test_iterate(self.ptr, k, ct.byref(it),
                                        ct.byref(gap)))
         return it.value, gap.value
+
+    def finish(self, max_passes: int = 3):
+        """End a training on the current state: (gap, b, obj, status)."""
+        gap, b, obj = ct.c_double(), ct.c_double(), ct.c_double()
+        st = ct.c_int32()
+        _check(load().svm_test_finish(self.ptr, max_passes, ct.byref(gap),
+                                      ct.byref(b), ct.byref(obj),
+                                      ct.byref(st)))
+        return gap.value, b.value, obj.value, st.value
