@@ -217,6 +217,26 @@ svm_status svm_train_ovr(const svm_matrix *X, const int32_t *labels,
 svm_status svm_predict(const svm_model *m, const svm_matrix *X,
                        double *decision);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * decision values of svm_predict (bitwise the same kernels and values) for
+ * the m dense rows of X, which must be in device memory (layout SVM_DENSE,
+ * on_device = 1, any ld >= d), into `decision` (device, m x n_outputs,
+ * row-major fp64, caller-owned), queued on `stream` (hipStream_t; NULL:
+ * the null stream) and NOT waited for: the values are there when the
+ * stream's work up to this call has finished.  The call allocates nothing,
+ * frees nothing and does not synchronise with the host: the rows are
+ * staged, chunk by chunk, in a static array of 32 MiB per device (held by
+ * each GPU the library runs on until the process ends), which every call
+ * on that GPU shares, so calls that overlap in time on one GPU race.  X is
+ * not checked for finite values (a non-finite row gives non-finite
+ * decision values).  Errors: SVM_E_UNSUPPORTED for CSR or host rows, or a
+ * row too long for the staging array (over about 8.3 million features);
+ * SVM_E_INVALID for a NULL model or output or a different number of
+ * features. */
+svm_status svm_predict_noalloc(const svm_model *m, const svm_matrix *X,
+                               double *decision, void *stream);
+
 /* Labels: +1 / -1 (D >= 0 gives +1) for C-SVC, argmax over classes (ties to
  * the lowest class) for one-vs-rest.  eps-SVR models: SVM_E_INVALID. */
 svm_status svm_predict_labels(const svm_model *m, const svm_matrix *X,

@@ -487,6 +487,32 @@ svm_status svm_predict(const svm_model* m, const svm_matrix* X,
     return predict_impl(m, X, decision, nullptr);
 }
 
+svm_status svm_predict_noalloc(const svm_model* m, const svm_matrix* X,
+                               double* decision, void* stream)
+{
+    if (!m) return fail(SVM_E_INVALID, "model is NULL");
+    svm_status st;
+    if ((st = check_matrix(X, 0)) != SVM_OK) return st;
+    if (X->layout != SVM_DENSE || !X->on_device)
+        return fail(SVM_E_UNSUPPORTED,
+                    "svm_predict_noalloc takes dense rows in device memory");
+    if (X->d != m->d)
+        return fail(SVM_E_INVALID, "X has a different number of features");
+    if (X->n == 0) return SVM_OK;
+    if (!decision) return fail(SVM_E_INVALID, "decision is NULL");
+    if (msvm::noalloc_rows_per_chunk(*m, X->values, X->ld) < 1)
+        return fail(SVM_E_UNSUPPORTED,
+                    "a row of X does not fit the staging array of "
+                    "svm_predict_noalloc (32 MiB)");
+    if ((st = check_device(m->device)) != SVM_OK) return st;
+    GUARD_BEGIN
+    HIP_TRY(hipSetDevice(m->device));
+    msvm::predict_noalloc(*m, X->values, X->n, X->ld, decision,
+                          (hipStream_t)stream);
+    return SVM_OK;
+    GUARD_END
+}
+
 svm_status svm_predict_labels(const svm_model* m, const svm_matrix* X,
                               int32_t* labels)
 {

@@ -308,6 +308,20 @@ void build_model(svm_model& m, Context& cx, const Features& f,
 void predict_device(const svm_model& mdl, Context& cx, Features& t,
                     double* out);
 
+// Allocation-free decision values (noalloc.hip): the m dense rows of X
+// (device, leading dimension ld) staged in a static per-device array of
+// noalloc_scratch_bytes(), chunk by chunk, decision values to out
+// (device, m x n_out), all on stream s with no allocation and no host
+// synchronisation.
+void predict_noalloc(const svm_model& mdl, const float* X, int64_t m,
+                     int64_t ld, double* out, hipStream_t s);
+// whether the rows are copied (padded, scaled) into the array, and how many
+// rows one chunk takes (< 1: a row does not fit)
+bool noalloc_needs_copy(const svm_model& mdl, const float* X, int64_t ld);
+int64_t noalloc_rows_per_chunk(const svm_model& mdl, const float* X,
+                               int64_t ld);
+size_t noalloc_scratch_bytes();
+
 // Standardisation (dense features only): per-feature mean and sample
 // standard deviation of f (device, d values each), and their application
 // to a feature store (its norms recomputed).  Targets: the same for the n

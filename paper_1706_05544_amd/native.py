@@ -41,6 +41,7 @@ EXPORTS = [
     "svm_test_solver_free", "svm_test_set_state", "svm_test_get_state",
     "svm_test_select", "svm_test_rows", "svm_test_subproblem",
     "svm_test_apply", "svm_test_iterate", "svm_test_finish",
+    "svm_predict_noalloc",
 ]
 
 
@@ -164,6 +165,7 @@ def load(path: Optional[str] = None):
     lib.svm_test_apply.argtypes = [vp, vp, ct.c_int32, vp]
     lib.svm_test_iterate.argtypes = [vp, ct.c_int64, P(ct.c_int64),
                                      P(ct.c_double)]
+    lib.svm_predict_noalloc.argtypes = [vp, P(svm_matrix), vp, vp]
     lib.svm_test_finish.argtypes = [vp, ct.c_int32, P(ct.c_double),
                                     P(ct.c_double), P(ct.c_double),
                                     P(ct.c_int32)]
@@ -337,6 +339,29 @@ def svm_predict(model: Model, X):
         ptr = _np_ptr(D) if m else None
     _check(load().svm_predict(model.ptr, ct.byref(M.s), ptr))
     return D[:, 0] if n_out == 1 else D
+
+
+def svm_predict_noalloc(model: Model, X, out=None, stream=None):
+    """svm_predict_noalloc: X a dense torch tensor on the GPU; the decision
+    values go to `out` (a float64 tensor of m x n_outputs, allocated here
+    when None) on `stream` (torch's current stream when None), not waited
+    for.  Returns out."""
+    import torch
+    M = _Mat(X)
+    if not M.device:
+        raise SvmError(SVM_E_UNSUPPORTED, "svm_predict_noalloc takes a "
+                       "tensor in device memory")
+    n_out = model.n_outputs
+    m = M.s.n
+    if out is None:
+        out = torch.empty((m, n_out), dtype=torch.float64, device=X.device)
+    assert out.dtype == torch.float64 and out.is_contiguous()
+    assert out.numel() == m * n_out
+    st = stream if stream is not None else torch.cuda.current_stream()
+    _check(load().svm_predict_noalloc(model.ptr, ct.byref(M.s),
+                                      out.data_ptr() if m else None,
+                                      st.cuda_stream))
+    return out
 
 
 def svm_predict_labels(model: Model, X):
