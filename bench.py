@@ -209,6 +209,10 @@ def main() -> int:
                     help="P > 1: one-vs-rest classes and cross-validation "
                          "folds train P at a time in lockstep (one pass "
                          "over X serves P working sets; no row cache)")
+    ap.add_argument("--fused", type=int, default=0, choices=[0, 1],
+                    help="1: every outer iteration as one launch (dense, "
+                         "q <= 16, no row cache); 0: selection and row "
+                         "update as two launches")
     ap.add_argument("--scale", action="store_true",
                     help="standardise the features (and eps-SVR targets)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -261,7 +265,7 @@ def main() -> int:
     kw = dict(type=w.type, C=w.C, epsilon=w.eps, gamma=gamma, tol=w.tol,
               working_set=args.working_set, kernel=kernel,
               degree=args.degree, coef0=args.coef0,
-              scale=1 if args.scale else 0)
+              scale=1 if args.scale else 0, fused=args.fused)
     multi = w.n_classes > 2
     # lockstep applies to one-vs-rest classes and cross-validation folds
     lock = args.lockstep if (args.lockstep > 1 and (multi or args.cv > 1)) \

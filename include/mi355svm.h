@@ -138,6 +138,16 @@ typedef struct {
                               SVM_E_UNSUPPORTED.  No effect on svm_train.
                               train_ms of a problem then spans its group's
                               run (the groups' problems overlap in time) */
+    int32_t fused;         /* 1: every outer iteration as one launch, in
+                              which each block merges the selection
+                              candidates and solves the subproblem itself
+                              while its rows stream (Section 3's loop);
+                              dense X and working_set <= 16 only, no row
+                              cache.  0 (default): selection and row update
+                              as two launches.  The result is the same bit
+                              for bit; one launch has been the slower so far
+                              (its blocks' selection chains run longer than
+                              the stream they hide) */
 } svm_params;
 
 /* Result of a k-fold cross-validation. */

@@ -66,6 +66,8 @@ svm_status check_params(const svm_params* p)
         return fail(SVM_E_INVALID, "scale must be 0 or 1");
     if (p->lockstep < 0 || p->lockstep > msvm::kLockMax)
         return fail(SVM_E_INVALID, "lockstep must be in [0, 4]");
+    if (p->fused != 0 && p->fused != 1)
+        return fail(SVM_E_INVALID, "fused must be 0 or 1");
     return SVM_OK;
 }
 
@@ -304,7 +306,8 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
     if (p->scale) scale_training(*m, f, yd.p, p->type, cx);
     msvm::SolveOptions o = msvm::make_options(p, X->n, X->d);
     msvm::RowCache rc;
-    msvm::cache_init(rc, X->n, p->cache_bytes, cx);
+    msvm::cache_init(rc, X->n, msvm::one_launch_loop(o, f) ? -1 : p->cache_bytes,
+                     cx);
     msvm::Solver s(cx, f, yd.p, o, &rc);
     if (p->alpha0) s.warm_start(p->alpha0);
     msvm::SolveResult r = s.train();
@@ -402,7 +405,8 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     svm_status worst = SVM_OK;
     // one row cache for all classes: the kernel rows do not depend on labels
     msvm::RowCache rc;
-    msvm::cache_init(rc, n, p->cache_bytes, cx);
+    msvm::cache_init(rc, n, msvm::one_launch_loop(o, f) ? -1 : p->cache_bytes,
+                     cx);
     auto collect = [&](int32_t c, msvm::Solver& s, const msvm::SolveResult& r) {
         res[(size_t)c] = r;
         s.coefficients(coef.p, n_classes, c);
@@ -692,7 +696,11 @@ svm_status cv_run_many(CvData& c, const std::vector<svm_params>& ps,
     if (L == 1) {
         for (int g = 0; g < NG; ++g) {
             msvm::RowCache rc;  // K rows do not depend on fold or class
-            msvm::cache_init(rc, n, ps[(size_t)g].cache_bytes, cx);
+            msvm::cache_init(rc, n,
+                             msvm::one_launch_loop(opts[(size_t)g], c.f)
+                                 ? -1
+                                 : ps[(size_t)g].cache_bytes,
+                             cx);
             for (int32_t t = 0; t < per; ++t) {
                 const int32_t fo = t / c.n_out, cl = t % c.n_out;
                 if (c.labels.p)

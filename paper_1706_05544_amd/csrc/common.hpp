@@ -212,6 +212,38 @@ struct PredictArgs {
     int32_t ch_cap;
 };
 
+// One outer iteration per launch (k_iter, dense features, q <= 16): every
+// block merges the previous launch's candidate records, solves the
+// subproblem and updates its rows; F and the records are double-buffered by
+// launch parity; the last block (ticket) writes alpha_B, the state bytes of
+// B and the working-set record.
+constexpr int kIterMaxRecords = 1024;  // blocks (candidate records) at most
+struct IterArgs {
+    const float* X;       // dense rows
+    const float* sq;
+    const float* z;       // labels (C-SVC) or targets (eps-SVR)
+    const double* F_in;   // responses after the previous launch
+    double* F_out;        // responses after this one
+    double* alpha;
+    uint8_t* st;
+    const double* rk_in;  // candidate records of the previous launch
+    const int32_t* ri_in;
+    double* rk_out;       // this launch's (one per block)
+    int32_t* ri_out;
+    WorkingSet* ws;
+    uint32_t* ticket;     // 0 between launches
+    int64_t n, ldp;
+    int32_t nb;           // blocks = candidate records
+    int32_t half;
+    int32_t tiles;        // 16-row tiles per row wave
+    int32_t group_rows;   // most rows of a block
+    double C, eps, tol;
+    KernelFn kf;
+    double inner_ratio;
+    int32_t max_inner;
+    int64_t max_iter;
+};
+
 // Several problems over one stream of X (k_lock): problem p's working set
 // is staged at rows 16p .. 16p + 15 of xS; the rest is per problem.  Every
 // problem has the same n, features and kernel kind.
@@ -296,6 +328,11 @@ void launch_lock(const LockArgs& a, int P, int nblocks, bool svr,
                  hipEvent_t e1 = nullptr);
 size_t lock_lds_bytes(int P, int64_t ldp, int tiles, bool svr);
 int lock_blocks_per_cu(int P, bool svr, size_t lds);
+// one outer iteration (k_iter): nblocks = a.nb blocks
+void launch_iter(const IterArgs& a, int nblocks, bool svr, hipStream_t s,
+                 hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+size_t iter_lds_bytes(int64_t ldp, int tiles, bool svr);
+int iter_blocks_per_cu(bool svr, size_t lds);
 void launch_state_from_alpha(int32_t type, const float* y, const double* a,
                              int64_t n, double C, uint8_t* st, hipStream_t s);
 void launch_coef(int32_t type, const double* a, const uint8_t* st, int64_t n,

@@ -153,7 +153,17 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
     o.inner_ratio = p->inner_ratio > 0 ? p->inner_ratio : 0.3;
     o.max_inner = p->max_inner > 0 ? p->max_inner : 8 * p->working_set;
     o.profile = p->profile != 0;
+    o.fused = p->fused;
+    o.cache_req = p->cache_bytes;
     return o;
+}
+
+bool one_launch_loop(const SolveOptions& o, const Features& f)
+{
+    // (asked for only: on the shapes measured so far it is slower, the
+    // selection chain of a block under 512 concurrent ones taking longer
+    // than the stream it hides)
+    return o.fused > 0 && !f.csr && o.q <= 16;
 }
 
 KernelFn kernel_fn(const SolveOptions& o)
@@ -267,6 +277,44 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     nb_ = (int)nb;
     ch_cap_ = sparse_chunk_cap(f);
 
+    // One launch per outer iteration: as many k_iter blocks as are
+    // resident (at most kIterMaxRecords, one candidate record each), the
+    // rows of a block over its 3 row waves.
+    if (one_launch_loop(o, f)) {
+        auto iter_tiles = [&](int64_t nbk) {
+            const int64_t block_tiles = 2 * ((units + nbk - 1) / nbk);
+            return (int)((block_tiles + 2) / 3);
+        };
+        int T = 1;
+        int64_t nbk = 1;
+        bool ok = true;
+        for (int it = 0; it < 8; ++it) {
+            const size_t lds = iter_lds_bytes(f.ldp, T, svr);
+            if (lds > kLdsMax) {
+                ok = false;
+                break;
+            }
+            const int64_t cap =
+                (int64_t)cus * iter_blocks_per_cu(svr, lds);
+            nbk = std::max<int64_t>(
+                1, std::min<int64_t>({cap, units, (int64_t)kIterMaxRecords}));
+            const int t = iter_tiles(nbk);
+            if (t <= T) break;
+            T = t;
+        }
+        T = iter_tiles(nbk);
+        const int tk = wave_tiles(nbk);  // the k_rows launch on that grid
+        if (ok && iter_lds_bytes(f.ldp, T, svr) <= kLdsMax &&
+            rows_lds_bytes(1, f.ldp, tk, svr, -1) <= kLdsMax &&
+            (int64_t)16 * std::max(T, tk) * f.ldp * 4 < ((int64_t)1 << 31)) {
+            fused_ = true;
+            nbi_ = (int)nbk;
+            tilesi_ = T;
+            tilesk_ = tk;
+            cache_ = nullptr;  // (the row cache serves the two-launch loop)
+        }
+    }
+
     F_.alloc((size_t)n_);
     alpha_.alloc((size_t)N_);
     st_.alloc((size_t)N_);
@@ -279,6 +327,12 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     }
     ckey_.alloc((size_t)nb_ * 2 * kBlockTop);
     cidx_.alloc((size_t)nb_ * 2 * kBlockTop);
+    if (fused_) {
+        F2_.alloc((size_t)n_);
+        irk_.alloc((size_t)2 * nbi_ * 2 * kBlockTop);
+        iri_.alloc((size_t)2 * nbi_ * 2 * kBlockTop);
+        ticket_.alloc(1);
+    }
     sum_.alloc(1 + kSummaryBlocks);
     cvec_.alloc((size_t)n_);
     cblk_.alloc((size_t)compact_blocks(n_));
@@ -293,6 +347,7 @@ Solver::Solver(Context& cx, const Features& f, const float* y_dev,
     HIP_TRY(hipMemsetAsync(alpha_.p, 0, alpha_.bytes(), s));
     HIP_TRY(hipMemsetAsync(ws_.p, 0, sizeof(WorkingSet), s));
     HIP_TRY(hipMemsetAsync(xS_.p, 0, xS_.bytes(), s));
+    if (fused_) HIP_TRY(hipMemsetAsync(ticket_.p, 0, ticket_.bytes(), s));
     DevBuf<int32_t> bad(1);
     HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), s));
     launch_init_state(o.type, y_.p, n_, fold, held, st_.p, bad.p, s);
@@ -360,6 +415,33 @@ void Solver::launch_keys()
     a.mode = RU_CAND;
     a.nS_override = 0;
     launch_rows(a, nb_, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
+}
+
+// The first candidate records of the one-launch loop (k_rows, keys only,
+// on k_iter's grid: the same row range per block, so the records belong to
+// the row groups k_iter's rescans assume), into parity 0.
+void Solver::launch_keys_fused()
+{
+    RowArgs a{};
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.F = F_.p;
+    a.st = st_.p;
+    a.z = y_.p;
+    a.ws = ws_.p;
+    a.xS = xS_.p;
+    a.csr_cols = -1;
+    a.cand_key = irk_.p;
+    a.cand_idx = iri_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.eps = o_.eps;
+    a.kf = kf_;
+    a.half = half_;
+    a.tiles = tilesk_;
+    a.mode = RU_CAND;
+    a.nS_override = 0;
+    launch_rows(a, nbi_, 1, o_.type == SVM_EPS_SVR, cx_.stream);
 }
 
 void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
@@ -550,6 +632,136 @@ bool Solver::run_loop(SolveResult& r)
     return w.done == 1;
 }
 
+// The one-launch loop: chunks of `check_every` k_iter launches, two chunks
+// in flight, the done flag of the older chunk polled.  Launch k of the
+// chunk sequence reads the responses and records of parity k % 2 and writes
+// the other; the responses end in F_ (copied there when the number of
+// iterations was odd).
+bool Solver::run_loop_fused(SolveResult& r)
+{
+    const int K = o_.check_every;
+    HostBuf<WorkingSet> hs(2);
+    hipEvent_t ev[2];
+    HIP_TRY(hipEventCreateWithFlags(&ev[0], hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&ev[1], hipEventDisableTiming));
+    std::vector<hipEvent_t> pe;
+    if (o_.profile) {
+        pe.resize((size_t)4 * K);
+        for (auto& e : pe)
+            HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
+    }
+    WorkingSet w0;
+    read_ws(w0);
+    const int64_t iter_start = w0.iter;
+    int64_t last_iter = w0.iter;
+    const int64_t units = (n_ + 31) / 32;
+    IterArgs a{};
+    a.X = f_.X.p;
+    a.sq = f_.sq.p;
+    a.z = y_.p;
+    a.alpha = alpha_.p;
+    a.st = st_.p;
+    a.ws = ws_.p;
+    a.ticket = ticket_.p;
+    a.n = n_;
+    a.ldp = f_.ldp;
+    a.nb = nbi_;
+    a.half = half_;
+    a.tiles = tilesi_;
+    a.group_rows = (int32_t)std::min<int64_t>(
+        n_, 32 * ((units + nbi_ - 1) / nbi_));
+    a.C = o_.C;
+    a.eps = o_.eps;
+    a.tol = o_.tol;
+    a.kf = kf_;
+    a.inner_ratio = o_.inner_ratio;
+    a.max_inner = o_.max_inner;
+    a.max_iter = o_.max_iter;
+    const size_t rec = (size_t)nbi_ * 2 * kBlockTop;
+    int64_t launched = 0;
+    const bool svr = o_.type == SVM_EPS_SVR;
+
+    auto enqueue = [&](int slot) {
+        for (int k = 0; k < K; ++k) {
+            const int par = (int)(launched & 1);
+            a.F_in = par ? F2_.p : F_.p;
+            a.F_out = par ? F_.p : F2_.p;
+            a.rk_in = irk_.p + par * rec;
+            a.ri_in = iri_.p + par * rec;
+            a.rk_out = irk_.p + (1 - par) * rec;
+            a.ri_out = iri_.p + (1 - par) * rec;
+            if (o_.profile)
+                launch_iter(a, nbi_, svr, cx_.stream,
+                            pe[(size_t)(slot * K + k) * 2],
+                            pe[(size_t)(slot * K + k) * 2 + 1]);
+            else
+                launch_iter(a, nbi_, svr, cx_.stream);
+            ++launched;
+        }
+        HIP_TRY(hipMemcpyAsync(&hs.p[slot], ws_.p, sizeof(WorkingSet),
+                               hipMemcpyDeviceToHost, cx_.stream));
+        HIP_TRY(hipEventRecord(ev[slot], cx_.stream));
+    };
+
+    enqueue(0);
+    enqueue(1);
+    int cur = 0;
+    for (;;) {
+        HIP_TRY(hipEventSynchronize(ev[cur]));
+        const WorkingSet& w = hs.p[cur];
+        if (o_.profile) {
+            const int64_t real = std::min<int64_t>(w.iter - last_iter, K);
+            const double per_row = 16.0 + (svr ? 6.0 : 1.0);
+            for (int64_t k = 0; k < real; ++k) {
+                float ms = 0.f;
+                HIP_TRY(hipEventElapsedTime(
+                    &ms, pe[(size_t)(cur * K + k) * 2],
+                    pe[(size_t)(cur * K + k) * 2 + 1]));
+                row_ms_ += ms;
+                row_launches_ += 1;
+                row_rows_ += n_;
+                row_bytes_ += 4.0 * (double)f_.d * (double)n_ +
+                              (double)n_ * (per_row + 4.0);
+            }
+        }
+        if (w.done) break;
+        if (w.iter == last_iter) {
+            cx_.sync();
+            for (auto& e : pe) (void)hipEventDestroy(e);
+            (void)hipEventDestroy(ev[0]);
+            (void)hipEventDestroy(ev[1]);
+            throw Error{SVM_E_INTERNAL, "solver state made no progress"};
+        }
+        last_iter = w.iter;
+        enqueue(cur);
+        cur ^= 1;
+    }
+    cx_.sync();
+    for (auto& e : pe) (void)hipEventDestroy(e);
+    (void)hipEventDestroy(ev[0]);
+    (void)hipEventDestroy(ev[1]);
+    WorkingSet w;
+    read_ws(w);
+    // iteration k (counted from this call's start) wrote F2_ when odd
+    if ((w.iter - iter_start) & 1)
+        HIP_TRY(hipMemcpyAsync(F_.p, F2_.p, (size_t)n_ * sizeof(double),
+                               hipMemcpyDeviceToDevice, cx_.stream));
+    r.iters = w.iter;
+    r.gap = w.gap;
+    r.m = w.m;
+    r.M = w.M;
+    r.kernel_rows = w.rows;
+    r.status = w.done == 2 ? SVM_W_MAX_ITER : SVM_OK;
+    return w.done == 1;
+}
+
+bool Solver::loop(SolveResult& r)
+{
+    if (!fused_) return run_loop(r);  // (candidates from launch_keys)
+    launch_keys_fused();
+    return run_loop_fused(r);
+}
+
 void Solver::recompute_responses()
 {
     hipStream_t s = cx_.stream;
@@ -594,8 +806,8 @@ void Solver::recompute_responses()
 SolveResult Solver::train()
 {
     SolveResult r;
-    hipEvent_t t0 = start(true);
-    const bool conv = run_loop(r);
+    hipEvent_t t0 = start(!fused_);
+    const bool conv = loop(r);
     finish(r, conv, t0);
     return r;
 }
@@ -634,7 +846,7 @@ void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0, int max_passes)
             break;
         }
         launch_fill_i32(&ws_.p->done, 0, 1, cx_.stream);
-        conv = run_loop(r);
+        conv = loop(r);
     }
 
     launch_summary(o_.type, alpha_.p, st_.p, F_.p, y_.p, n_, o_.C, o_.eps,
@@ -673,7 +885,22 @@ void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0, int max_passes)
     r.cache_filled = w.cache_filled;
     r.iters = w.iter;
     if (const char* e = getenv("SVM_LOG")) {
-        if (atoi(e) > 0 && w.prof[4] > 0) {
+        if (atoi(e) > 0 && fused_ && w.prof[4] > 0) {
+            const double k = 10.0 / (double)w.prof[4];  // 100 MHz ticks -> ns
+            fprintf(stderr,
+                    "[mi355svm] one launch per iteration: iters=%lld "
+                    "blocks=%d tiles=%d rescans=%lld; phases of the last "
+                    "block (us): merge %.2f rescans %.2f build %.2f stage "
+                    "%.2f solve %.2f rows %.2f tail %.2f; kernel %.2f "
+                    "us/launch (%lld timed)\n",
+                    (long long)w.iter, nbi_, tilesi_, (long long)w.rescans,
+                    1e-3 * k * w.prof[0], 1e-3 * k * w.prof[1],
+                    1e-3 * k * w.prof[2], 1e-3 * k * w.prof[3],
+                    1e-3 * k * w.prof[5], 1e-3 * k * w.prof[6],
+                    1e-3 * k * w.prof[7],
+                    row_launches_ ? 1e3 * row_ms_ / row_launches_ : 0.0,
+                    (long long)row_launches_);
+        } else if (atoi(e) > 0 && w.prof[4] > 0) {
             const double k = 10.0 / (double)w.prof[4];  // 100 MHz ticks -> ns
             fprintf(stderr,
                     "[mi355svm] iters=%lld rows=%lld (cache: served %lld "

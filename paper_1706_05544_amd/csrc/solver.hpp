@@ -116,12 +116,19 @@ struct SolveOptions {
     double inner_ratio;
     int32_t max_inner;
     bool profile;
+    int32_t fused;       // svm_params.fused
+    int64_t cache_req;   // svm_params.cache_bytes
 };
 
 SolveOptions make_options(const svm_params* p, int64_t n, int64_t d);
 
 // The kernel of the options as the kernels take it.
 KernelFn kernel_fn(const SolveOptions& o);
+
+// Whether a solve of these options on these features runs one launch per
+// outer iteration (k_iter) instead of a selection launch and a row launch
+// (the row cache serves only the latter).
+bool one_launch_loop(const SolveOptions& o, const Features& f);
 
 // Result of one binary (or SVR) solve.
 struct SolveResult {
@@ -204,6 +211,11 @@ private:
     void launch_solve(int32_t mode);
     void launch_select_only();
     bool run_loop(SolveResult& r);
+    // one launch per outer iteration: initial records, the loop
+    void launch_keys_fused();
+    bool run_loop_fused(SolveResult& r);
+    // the loop of the solver's kind, from the current state
+    bool loop(SolveResult& r);
     void recompute_responses();
     void read_ws(WorkingSet& w);
     // CSR: compact working-set columns of a launch with nbc column blocks
@@ -218,6 +230,14 @@ private:
     int64_t n_, N_;
     KernelFn kf_;
     int half_, nblk_cols_, tiles_, nb_;
+    // one launch per outer iteration: blocks (= candidate records), tiles
+    // per row wave, tiles of the record-writing k_rows launch on that grid;
+    // the second responses buffer, the double-buffered records, the ticket
+    bool fused_ = false;
+    int nbi_ = 0, tilesi_ = 0, tilesk_ = 0;
+    DevBuf<double> F2_, irk_;
+    DevBuf<int32_t> iri_;
+    DevBuf<uint32_t> ticket_;
     DevBuf<double> F_, alpha_;
     DevBuf<uint8_t> st_;
     DevBuf<float> y_;

@@ -69,7 +69,8 @@ class svm_params(ct.Structure):
                 ("inner_ratio", ct.c_double), ("max_inner", ct.c_int32),
                 ("profile", ct.c_int32), ("coef0", ct.c_double),
                 ("degree", ct.c_int32), ("scale", ct.c_int32),
-                ("alpha0", ct.c_void_p), ("lockstep", ct.c_int32)]
+                ("alpha0", ct.c_void_p), ("lockstep", ct.c_int32),
+                ("fused", ct.c_int32)]
 
 
 class svm_cv_stats(ct.Structure):
