@@ -49,6 +49,34 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
         floatx4 acc[4];
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // the epilogue's data of the tile's support rows, requested now so
+        // that it lands during the tile's matrix-core work (buffer loads:
+        // a row past the end reads 0, and so does the index table when
+        // self_match is off)
+        float ssv[4];
+        int64_t stn[4];
+        double cf[4][NOUT];
+        {
+            const Rsrc rQ = make_rsrc(a.sqsv + sv0, (nsv - sv0) * 4);
+            const Rsrc rT =
+                make_rsrc(a.sv_train_idx + (a.self_match ? sv0 : 0),
+                          a.self_match ? (nsv - sv0) * 4 : 0);
+            const Rsrc rC = make_rsrc(a.coef + sv0 * n_out,
+                                      (nsv - sv0) * n_out * 8);
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                const uint32_t j = (uint32_t)(cb * 16 + nl);
+                ssv[cb] = bld_f32(rQ, 4 * j);
+                const int32_t t = bld_i32(rT, 4 * j);
+                stn[cb] = (a.self_match && sv0 + j < nsv) ? t : -1;
+#pragma unroll
+                for (int o = 0; o < NOUT; ++o)
+                    cf[cb][o] = o < n_out
+                                    ? bld_f64(rC, 8 * (j * (uint32_t)n_out +
+                                                       (uint32_t)o))
+                                    : 0.0;
+            }
+        }
         for (int64_t c0 = 0; c0 < ldp; c0 += kPredDK) {
             __syncthreads();
             for (int e = tid; e < 64 * q4c; e += 256) {
@@ -75,20 +103,13 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
         }
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) {
-            const int64_t sv = sv0 + cb * 16 + nl;
-            const bool ok = sv < nsv;
-            const float ssv = ok ? a.sqsv[sv] : 0.0f;
-            const int64_t st = (ok && a.self_match) ? a.sv_train_idx[sv] : -1;
-            double cf[NOUT];
-#pragma unroll
-            for (int o = 0; o < NOUT; ++o)
-                cf[o] = (ok && o < n_out) ? a.coef[sv * n_out + o] : 0.0;
             float kv[4];
             if (a.kf.kind == SVM_KERNEL_RBF) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    kv[v] = rbf_from_dot(sqr[v], ssv, acc[cb][v], a.kf.gexp);
-                    if (st == rid[v] + a.row_base) kv[v] = 1.0f;
+                    kv[v] = rbf_from_dot(sqr[v], ssv[cb], acc[cb][v],
+                                         a.kf.gexp);
+                    if (stn[cb] == rid[v] + a.row_base) kv[v] = 1.0f;
                 }
             } else {
 #pragma unroll
@@ -99,7 +120,166 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
             for (int v = 0; v < 4; ++v) {
 #pragma unroll
                 for (int o = 0; o < NOUT; ++o)
-                    part[o][v] = fma(cf[o], (double)kv[v], part[o][v]);
+                    part[o][v] = fma(cf[cb][o], (double)kv[v], part[o][v]);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int o = 0; o < NOUT; ++o)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+            for (int off = 8; off > 0; off >>= 1)
+                part[o][v] += __shfl_xor(part[o][v], off, 16);
+
+    if (nl < 4) {
+        const int64_t row = row0 + wave * 16 + 4 * g + nl;
+        if (row < m) {
+#pragma unroll
+            for (int o = 0; o < NOUT; ++o) {
+                if (o < n_out) {
+                    double bias = a.b ? a.b[o] : 0.0;
+                    a.out[row * n_out + o] = pick4(part[o], nl) + bias;
+                }
+            }
+        }
+    }
+}
+
+// The same decision sums for rows of at most kRaMaxLdp features: each wave's
+// 16 test rows stay in registers, in the matrix-core operand layout, for the
+// whole kernel, and only the support tiles pass through LDS, whole (64
+// support rows x ldp features a step): half the staging of k_predict and
+// all of a tile's matrix-core work between one pair of barriers.  Same
+// chunk order, so the same K bits.
+constexpr int kRaMaxLdp = 128;
+constexpr int kRaLS = kRaMaxLdp + 4;  // padded LDS row stride
+
+template <int NOUT>
+__global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
+{
+    __shared__ __align__(16) float Bs[64 * kRaLS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, nl = lane & 15;
+    const int64_t m = a.m, ldp = a.ldp, nsv = a.nsv;
+    const int64_t row0 = (int64_t)blockIdx.x * 64;
+    const int n_out = a.n_out;
+    const int kch = (int)((ldp + 15) / 16);  // 16-feature chunks (<= 8)
+
+    float sqr[4];
+    int64_t rid[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        rid[v] = row0 + wave * 16 + 4 * g + v;
+        sqr[v] = rid[v] < m ? a.sqt[rid[v]] : 0.0f;
+    }
+    // this lane's A operand: row wave*16 + nl, features 16c + 4g .. + 3
+    float4 ar[kRaMaxLdp / 16];
+    {
+        const int64_t r = row0 + wave * 16 + nl;
+        const Rsrc rA = make_rsrc(a.Xt + (r < m ? r : 0) * ldp,
+                                  r < m ? ldp * 4 : 0);
+#pragma unroll
+        for (int c = 0; c < kRaMaxLdp / 16; ++c) {
+            const int col = 16 * c + 4 * g;
+            ar[c] = bld_f4(rA, col < ldp ? (uint32_t)(4 * col) : kOob);
+        }
+    }
+    double part[NOUT][4];
+#pragma unroll
+    for (int o = 0; o < NOUT; ++o)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) part[o][v] = 0.0;
+
+    const int q4 = (int)(ldp / 4);  // float4 per support row
+    // A support tile: 64 rows x ldp features; thread t holds float4 t +
+    // 256 j of it (a fixed count, all issued before any store: the ones
+    // past the tile, or past ldp in a row, are sent past the end and read
+    // zero).  (Issuing the next tile's loads before this tile's matrix-core
+    // work costs registers, and so occupancy, and measured slower.)
+    constexpr int kLd = 64 * (kRaMaxLdp / 4) / 256;
+    const int tot = 64 * 4 * kch;
+    for (int64_t sv0 = 0; sv0 < nsv; sv0 += 64) {
+        // the tile's epilogue data (it lands during the work below)
+        float ssv[4];
+        int64_t stn[4];
+        double cf[4][NOUT];
+        {
+            const Rsrc rQ = make_rsrc(a.sqsv + sv0, (nsv - sv0) * 4);
+            const Rsrc rT =
+                make_rsrc(a.sv_train_idx + (a.self_match ? sv0 : 0),
+                          a.self_match ? (nsv - sv0) * 4 : 0);
+            const Rsrc rC = make_rsrc(a.coef + sv0 * n_out,
+                                      (nsv - sv0) * n_out * 8);
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                const uint32_t j = (uint32_t)(cb * 16 + nl);
+                ssv[cb] = bld_f32(rQ, 4 * j);
+                const int32_t t = bld_i32(rT, 4 * j);
+                stn[cb] = (a.self_match && sv0 + j < nsv) ? t : -1;
+#pragma unroll
+                for (int o = 0; o < NOUT; ++o)
+                    cf[cb][o] = o < n_out
+                                    ? bld_f64(rC, 8 * (j * (uint32_t)n_out +
+                                                       (uint32_t)o))
+                                    : 0.0;
+            }
+        }
+        const Rsrc rB = make_rsrc(a.SV + sv0 * ldp,
+                                  min((int64_t)64, nsv - sv0) * ldp * 4);
+        float4 bvl[kLd];
+#pragma unroll
+        for (int j = 0; j < kLd; ++j) {
+            const int e = tid + 256 * j;
+            const int r = e / (4 * kch), c4 = e - r * (4 * kch);
+            bvl[j] = bld_f4(rB, (e < tot && c4 < q4)
+                                    ? (uint32_t)((r * ldp + 4 * c4) * 4)
+                                    : kOob);
+        }
+        __syncthreads();  // the previous tile's reads are done
+#pragma unroll
+        for (int j = 0; j < kLd; ++j) {
+            const int e = tid + 256 * j;
+            const int r = e / (4 * kch), c4 = e - r * (4 * kch);
+            if (e < tot)
+                *reinterpret_cast<float4*>(Bs + r * kRaLS + 4 * c4) = bvl[j];
+        }
+        __syncthreads();
+        floatx4 acc[4];
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < kRaMaxLdp / 16; ++c) {
+            if (c < kch) {  // uniform
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) {
+                    const float4 bv =
+                        ld4(Bs + (cb * 16 + nl) * kRaLS + 16 * c + 4 * g);
+                    acc[cb] = mfma_chunk(acc[cb], ar[c], bv);
+                }
+            }
+        }
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+            float kv[4];
+            if (a.kf.kind == SVM_KERNEL_RBF) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    kv[v] = rbf_from_dot(sqr[v], ssv[cb], acc[cb][v],
+                                         a.kf.gexp);
+                    if (stn[cb] == rid[v] + a.row_base) kv[v] = 1.0f;
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    kv[v] = kernel_of_dot(a.kf, acc[cb][v]);
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+#pragma unroll
+                for (int o = 0; o < NOUT; ++o)
+                    part[o][v] = fma(cf[cb][o], (double)kv[v], part[o][v]);
             }
         }
     }
@@ -130,6 +310,13 @@ void launch_predict(const PredictArgs& a, hipStream_t s)
 {
     if (a.m <= 0) return;
     unsigned blocks = (unsigned)((a.m + 63) / 64);
+    if (a.ldp <= kRaMaxLdp && a.n_out <= 4) {
+        if (a.n_out <= 1)
+            k_predict_ra<1><<<blocks, 256, 0, s>>>(a);
+        else
+            k_predict_ra<4><<<blocks, 256, 0, s>>>(a);
+        return;
+    }
     if (a.n_out <= 1)
         k_predict<1><<<blocks, 256, 0, s>>>(a);
     else if (a.n_out <= 4)
