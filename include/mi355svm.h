@@ -338,7 +338,7 @@ svm_status svm_test_iterate(svm_solver *s, int64_t k, int64_t *iters,
 /* End a training on the current state as svm_train ends it: recompute F
  * from alpha, re-test the gap and, while it exceeds tol, run the loop again
  * and re-test, at most max_passes (>= 0) times (svm_train uses 3).  *gap,
- * *b (bias, reading R6: mean key over free variables, else (m + M) / 2) and
+ * *b (bias: the mean key over free variables, else (m + M) / 2) and
  * *obj (f(a)) come from the recomputed responses; *status is SVM_OK,
  * SVM_W_MAX_ITER or SVM_W_NOT_CONVERGED (the gap still above tol). */
 svm_status svm_test_finish(svm_solver *s, int32_t max_passes, double *gap,

@@ -1,5 +1,6 @@
 """The end of a training on the GPU: responses recomputed from alpha, the gap
-re-tested on them, bias (reading R6) and objective, and the status when the
+re-tested on them, bias (free-key mean, else the
+midpoint) and objective, and the status when the
 gap stays above tol.
 
 Through the svm_test_finish hook, from states the oracle reaches in a given

@@ -1,5 +1,5 @@
-"""Pins for the bias rule of the oracle (reading R6; the paper does not
-define b).
+"""Pins for the bias rule of the oracle (the paper does not define b; the
+rule below is LIBSVM's).
 
 b is the mean of the keys v_t over the free variables (0 < a_t < C); when
 no variable is free, the midpoint (m + M) / 2 of the largest I_up key and

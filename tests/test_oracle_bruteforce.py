@@ -120,7 +120,8 @@ def test_bias_matches_free_multiplier(orc, kind, n, d, C, eps, gamma, seed):
 
 
 def test_duplicate_points_degenerate_pair(orc):
-    # x_2 == x_0: the pair curvature K00 + K22 - 2K02 is 0 (reading R7)
+    # x_2 == x_0: the pair curvature K00 + K22 - 2K02 is 0 (it is
+    # floored at tau = 1e-12)
     X, y = tiny(6, 3, 31, "svc", duplicates=True)
     y[2] = -y[0]
     Q, p, yy, _ = _problem(X, y, C_SVC, 1.0, 0.0, 0.5)

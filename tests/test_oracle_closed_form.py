@@ -81,7 +81,8 @@ def test_three_point_symmetric_svc(orc, C):
 def test_two_point_svr(orc, z, C):
     # c1 = -c2 = clip((z1 - z2 - 2 eps) / (2 (1-k)), 0, C), b = (z1 + z2)/2
     # (for z1 >= z2; mirrored otherwise).  This pins the sign of the SVR
-    # linear term and which copy carries y = +1 (Eq. 1 read as R2).
+    # linear term and which copy carries y = +1 (Eq. 1 substituted
+    # into Eq. 2).
     X = np.array([[0.0, 0.0], [1.0, 0.5]], np.float32)
     zz = np.array(z, np.float32)
     g, eps = 0.5, 0.1
