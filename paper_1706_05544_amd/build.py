@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libmi355svm.so")
 
 ARCH = "gfx950"
 DEVICE_SOURCES = ["kernels.hip", "rows.hip", "lockstep.hip", "select.hip",
-                  "predict.hip", "noalloc.hip", "iterate.hip"]
+                  "predict.hip", "noalloc.hip", "iterate.hip", "factor.hip"]
 HOST_SOURCES = ["solver.cpp", "api.cpp"]
 
 # Packed fp32 instructions are disabled for every compilation that has a

@@ -199,6 +199,8 @@ struct PredictArgs {
     const int32_t* sv_train_idx;  // with self_match: K(x_i, x_i) = 1 exactly
     int32_t self_match;
     int64_t row_base;     // training-set index of query row 0 (self_match)
+    const int32_t* self_sv;  // factored sparse path: training row -> its
+                             // support row or -1 (nullptr: no self pairs)
     double* out;          // m x n_out
     KernelFn kf;
     // sparse path: CSR query rows, and the support rows by column in
@@ -281,6 +283,70 @@ struct ChunkArgs {
     float* sq_out;         // nsv: norms of the support rows (or nullptr)
 };
 
+// The sparse decision path by column (factor.hip).  With s_x = |x|^2, the
+// RBF value of a pair factors as K(x, v) = e^(-g s_x) e^(-g s_v) e^(2g x.v),
+// and x.v = 0 for every pair of rows with no column in common, so
+//   D(x) = e^(-g s_x) C0 + sum over the support rows v sharing a column
+//          with x of (c_v K(x, v) - e^(-g s_x) w_v),
+// with w_v = c_v e^(-g s_v) and C0 = sum_v w_v (the other kernels:
+// e^(-g s) -> 1 and w_v = c_v K of a zero dot product).  The support rows
+// are split into chunks of consecutive rows (at most kFcSvMax); a chunk holds
+// its nonzeros by column (CSC: for every column the chunk's rows that hold
+// it, in increasing order, as (local row, value)), and a dense map from
+// column to (first entry << kFcLenBits | count).  A wave takes query rows
+// one at a time: it adds each product x_c v_c into an LDS accumulator of the
+// chunk's rows (walk 1), then reads back and clears the accumulator at every
+// row it touched (walk 2), which visits each overlapping pair once.
+constexpr int kFcSvMax = 2048;     // support rows of a chunk
+constexpr int kFcLenBits = 12;     // bits of the count in a map entry
+constexpr int64_t kFcEntMax = (int64_t)1 << 20;  // entries of a chunk
+// bound on gexp |x|^2 of the factored RBF form (rows above it, or a model
+// with a support row above it, take the direct formula)
+constexpr float kFcSafe = 63.0f;
+// the factored path serves query rows that share fewer columns than this
+// with a support row on average (measured on the C5 shape, 20 of 1000
+// columns per row: 0.4 shared columns a pair, both paths 103 ms for 1M
+// rows against 44k support rows)
+constexpr double kFcMatchMax = 0.3;
+struct FactArgs {
+    const int64_t* rpt;   // m query rows (CSR)
+    const int32_t* cit;
+    const float* cvt;
+    const float* sqt;
+    int64_t m;
+    int64_t row_base;     // index of query row 0 in self_sv
+    const int32_t* self_sv;  // query row -> its own support row, or -1
+                             // (recompute of F: K(x_i, x_i) = 1), or nullptr
+    int32_t nch;          // chunks
+    int32_t ldpm;         // columns of a map row
+    const int32_t* ch_sv0;   // nch + 1: first support row of each chunk
+    const int64_t* ch_e0;    // nch + 1: first entry of each chunk
+    const uint32_t* map;     // nch x ldpm
+    const int2* ent;         // (local support row, value bits)
+    const float* sqsv;       // nsv norms
+    const double* coef;      // nsv x n_out
+    const double* w;         // nsv x n_out (see above)
+    const float* wf;         // nsv: w of output 0 in fp32
+    const double* c0;        // n_out
+    const double* b;         // n_out or nullptr
+    int32_t n_out;
+    int32_t fast;         // 1: e^(-g s) of every support row is in range
+    double* out;          // m x n_out
+    KernelFn kf;
+};
+// Building the chunks: support row j is CSR row idx[j] of (rp, ci, cv).
+struct FactBuildArgs {
+    const int64_t* rp;
+    const int32_t* ci;
+    const float* cv;
+    const int32_t* idx;
+    int32_t nch, ldpm;
+    const int32_t* ch_sv0;
+    const int64_t* ch_e0;
+    uint32_t* map;
+    int2* ent;
+};
+
 // ---- launch wrappers (kernels.hip / predict.hip) ----
 void launch_pad_copy(const float* src, int64_t ld, int64_t n, int64_t d,
                      float* dst, int64_t ldp, hipStream_t s);
@@ -359,6 +425,21 @@ void launch_predict_sparse(const PredictArgs& a, hipStream_t s);
 // LDS of the sparse decision kernel, and whether it fits
 size_t predict_sparse_lds_bytes(int64_t ldp, int cap);
 bool predict_sparse_fits(int64_t ldp, int cap);
+// sparse decision path by column (factor.hip)
+// nonzeros of each support row, and its norm (sq_out[j] = sq[idx[j]])
+void launch_fc_nnz(const int64_t* rp, const float* sq, const int32_t* idx,
+                   int64_t nsv, int32_t* nz, float* sq_out, hipStream_t s);
+void launch_fc_build(const FactBuildArgs& a, hipStream_t s);
+// w = coef x (RBF: 2^(-gexp s_v); else K of a zero dot), wf = its first
+// column in fp32, c0 = column sums
+// of w (fixed order), and the largest gexp s_v into *gs_max (float bits)
+void launch_fc_weights(const double* coef, const float* sqsv, int64_t nsv,
+                       int32_t n_out, const KernelFn& kf, double* w,
+                       float* wf, double* c0, uint32_t* gs_max, hipStream_t s);
+void launch_fc_self(const int32_t* sv_idx, int64_t nsv, int64_t n,
+                    int32_t* self_sv, hipStream_t s);
+void launch_predict_fact(const FactArgs& a, hipStream_t s);
+size_t fc_map_bytes_limit();
 void launch_csr_compact(const float* xS, int32_t nS, int64_t ldp,
                         int32_t qs, int32_t csr_cols, int32_t* xsc_cols,
                         float* xsc, hipStream_t s);

@@ -778,7 +778,14 @@ void Solver::recompute_responses()
     }
     PredictArgs a{};
     if (sv_sq_.count < (size_t)nsv) sv_sq_.alloc((size_t)nsv);
-    if (ch_cap_ > 0) {
+    if (f_.csr)
+        build_fact(fc_, f_, sv_idx_.p, nsv, sv_coef_.p, 1, kf_, cx_,
+                   sv_sq_.p, &f_);
+    if (fc_.ok) {
+        if (self_sv_.count < (size_t)n_) self_sv_.alloc((size_t)n_);
+        launch_fc_self(sv_idx_.p, nsv, n_, self_sv_.p, s);
+        a.self_sv = self_sv_.p;
+    } else if (ch_cap_ > 0) {
         build_sv_chunks(f_, sv_idx_.p, nsv, ch_cap_, ch_ncol_, ch_cols_,
                         ch_tab_, sv_sq_.p, s);
         a.ch_ncol = ch_ncol_.p;
@@ -800,7 +807,7 @@ void Solver::recompute_responses()
     a.self_match = 1;
     a.out = F_.p;
     a.kf = kf_;
-    predict_rows(a, f_, s);
+    predict_rows(a, f_, s, fc_.ok ? &fc_ : nullptr);
 }
 
 SolveResult Solver::train()
@@ -1490,6 +1497,8 @@ void build_model(svm_model& m, Context& cx, const Features& f,
     if (m.ch_cap > 0)
         build_sv_chunks(f, idx.p, nsv, m.ch_cap, m.ch_ncol, m.ch_cols,
                         m.ch_tab, nullptr, s);
+    if (f.csr)
+        build_fact(m.fc, f, idx.p, nsv, cc.p, n_out, m.kf, cx, m.sqsv.p);
     m.sv_idx.resize((size_t)nsv);
     m.coef.resize((size_t)(nsv * n_out));
     if (nsv > 0) {
@@ -1577,7 +1586,7 @@ void predict_device(const svm_model& mdl, Context& cx, Features& t,
         a.ch_tab = mdl.ch_tab.p;
         a.ch_cap = mdl.ch_cap;
     }
-    predict_rows(a, t, cx.stream);
+    predict_rows(a, t, cx.stream, mdl.fc.ok ? &mdl.fc : nullptr);
     if (mdl.scaled && mdl.type == SVM_EPS_SVR && mdl.y_sd > 0.0)
         launch_affine(out, t.n * mdl.n_out, mdl.y_sd, mdl.y_mu, cx.stream);
 }
@@ -1625,7 +1634,115 @@ void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
         launch_gather_rows(f.X.p, f.sq.p, f.ldp, idx, k, out, sq_out, s);
 }
 
-void predict_rows(PredictArgs a, const Features& t, hipStream_t s)
+// SVM_SPARSE_PATH: 1 = "table" (the factored path is not built), 2 =
+// "factor" (taken whenever built), 0 = unset (chosen by the rule)
+static int sparse_path_switch()
+{
+    const char* e = getenv("SVM_SPARSE_PATH");  // developer switch
+    if (!e) return 0;
+    const std::string v(e);
+    return v == "table" ? 1 : v == "factor" ? 2 : 0;
+}
+
+static bool use_fact(const FactSV* fc, const Features& t)
+{
+    if (!fc || !fc->ok || t.n <= 0) return false;
+    if (sparse_path_switch() == 2) return true;
+    const double shared = (double)t.nnz / (double)t.n * fc->sv_nnz /
+                          (double)std::max<int64_t>(fc->d, 1);
+    return shared < kFcMatchMax;
+}
+
+void build_fact(FactSV& fc, const Features& f, const int32_t* idx,
+                int64_t nsv, const double* coef, int32_t n_out,
+                const KernelFn& kf, Context& cx, float* sqsv,
+                const Features* query)
+{
+    fc.ok = false;
+    if (!f.csr || nsv <= 0 || n_out < 1 || n_out > 4) return;
+    if (sparse_path_switch() == 1) return;
+    hipStream_t s = cx.stream;
+    DevBuf<int32_t> nzd((size_t)nsv);
+    launch_fc_nnz(f.rp.p, f.sq.p, idx, nsv, nzd.p, sqsv, s);
+    std::vector<int32_t> nz((size_t)nsv);
+    HIP_TRY(hipMemcpyAsync(nz.data(), nzd.p, (size_t)nsv * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, s));
+    cx.sync();
+    // chunks of consecutive support rows: at most kFcSvMax rows and
+    // kFcEntMax nonzeros each
+    std::vector<int32_t> sv0{0};
+    std::vector<int64_t> e0{0};
+    int64_t tot = 0, ce = 0;
+    int32_t cs = 0;
+    for (int64_t j = 0; j < nsv; ++j) {
+        const int64_t z = nz[(size_t)j];
+        if (z > kFcEntMax) return;
+        if (cs == kFcSvMax || ce + z > kFcEntMax) {
+            sv0.push_back((int32_t)j);
+            e0.push_back(e0.back() + ce);
+            ce = 0;
+            cs = 0;
+        }
+        ce += z;
+        ++cs;
+        tot += z;
+    }
+    sv0.push_back((int32_t)nsv);
+    e0.push_back(e0.back() + ce);
+    // the factored path pays per entry that a query row meets; rows that
+    // hold a large share of the columns are cheaper through the table path
+    if ((double)tot > 0.1 * (double)f.d * (double)nsv) return;
+    fc.sv_nnz = (double)tot / (double)nsv;
+    fc.d = f.d;
+    fc.ok = true;  // (for the rule only)
+    const bool take = !query || use_fact(&fc, *query);
+    fc.ok = false;
+    if (!take) return;
+    const int32_t nch = (int32_t)(sv0.size() - 1);
+    const int64_t ldpm = (f.ldp + 3) & ~(int64_t)3;
+    if ((size_t)nch * (size_t)ldpm * 4 > fc_map_bytes_limit()) return;
+    fc.sv0.alloc((size_t)nch + 1);
+    fc.e0.alloc((size_t)nch + 1);
+    fc.map.alloc((size_t)nch * (size_t)ldpm);
+    fc.ent.alloc((size_t)std::max<int64_t>(tot, 1));
+    fc.w.alloc((size_t)(nsv * n_out));
+    fc.wf.alloc((size_t)nsv);
+    fc.c0.alloc((size_t)n_out);
+    HIP_TRY(hipMemcpyAsync(fc.sv0.p, sv0.data(), sv0.size() * sizeof(int32_t),
+                           hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(fc.e0.p, e0.data(), e0.size() * sizeof(int64_t),
+                           hipMemcpyHostToDevice, s));
+    FactBuildArgs b{};
+    b.rp = f.rp.p;
+    b.ci = f.ci.p;
+    b.cv = f.cv.p;
+    b.idx = idx;
+    b.nch = nch;
+    b.ldpm = (int32_t)ldpm;
+    b.ch_sv0 = fc.sv0.p;
+    b.ch_e0 = fc.e0.p;
+    b.map = fc.map.p;
+    b.ent = fc.ent.p;
+    launch_fc_build(b, s);
+    DevBuf<uint32_t> gs(1);
+    HIP_TRY(hipMemsetAsync(gs.p, 0, sizeof(uint32_t), s));
+    launch_fc_weights(coef, sqsv, nsv, n_out, kf, fc.w.p, fc.wf.p, fc.c0.p,
+                      gs.p, s);
+    uint32_t gsh = 0;
+    HIP_TRY(hipMemcpyAsync(&gsh, gs.p, sizeof(uint32_t),
+                           hipMemcpyDeviceToHost, s));
+    cx.sync();
+    float gmax = 0.0f;
+    std::memcpy(&gmax, &gsh, sizeof(float));
+    fc.nch = nch;
+    fc.ldpm = (int32_t)ldpm;
+    fc.n_out = n_out;
+    fc.fast = gmax <= kFcSafe ? 1 : 0;
+    fc.ok = true;
+}
+
+void predict_rows(PredictArgs a, const Features& t, hipStream_t s,
+                  const FactSV* fc)
 {
     a.ldp = t.ldp;
     if (!t.csr) {
@@ -1634,6 +1751,36 @@ void predict_rows(PredictArgs a, const Features& t, hipStream_t s)
         a.m = t.n;
         a.row_base = 0;
         launch_predict(a, s);
+        return;
+    }
+    if (t.nnz <= 32 * t.n && use_fact(fc, t)) {
+        FactArgs f{};
+        f.rpt = t.rp.p;
+        f.cit = t.ci.p;
+        f.cvt = t.cv.p;
+        f.sqt = t.sq.p;
+        f.m = t.n;
+        f.row_base = 0;
+        f.self_sv = a.self_sv;
+        f.nch = fc->nch;
+        f.ldpm = fc->ldpm;
+        f.ch_sv0 = fc->sv0.p;
+        f.ch_e0 = fc->e0.p;
+        f.map = fc->map.p;
+        f.ent = fc->ent.p;
+        f.sqsv = a.sqsv;
+        f.coef = a.coef;
+        f.w = fc->w.p;
+        f.wf = fc->wf.p;
+        f.c0 = fc->c0.p;
+        f.b = a.b;
+        f.n_out = a.n_out;
+        f.fast = fc->fast;
+        f.out = a.out;
+        f.kf = a.kf;
+        if (fc->ldpm < ((t.ldp + 3) & ~(int64_t)3))
+            throw Error{SVM_E_INTERNAL, "query rows wider than the model"};
+        launch_predict_fact(f, s);
         return;
     }
     if (a.ch_tab && t.nnz <= 32 * t.n) {

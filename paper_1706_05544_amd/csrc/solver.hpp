@@ -51,6 +51,20 @@ struct HostBuf {
     }
 };
 
+// The support rows in chunks by column for the factored sparse decision
+// path (factor.hip); ok == false: not built.
+struct FactSV {
+    bool ok = false;
+    int32_t nch = 0, ldpm = 0, n_out = 0, fast = 0;
+    double sv_nnz = 0.0;  // nonzeros of a support row, on average
+    int64_t d = 0;
+    DevBuf<int32_t> sv0;
+    DevBuf<int64_t> e0;
+    DevBuf<uint32_t> map;
+    DevBuf<int2> ent;
+    DevBuf<double> w, c0;
+    DevBuf<float> wf;
+};
 struct Context;
 
 // HBM-resident cache of kernel rows K(x_s, .) over all n samples, rows
@@ -258,6 +272,8 @@ private:
     int ch_cap_ = 0;
     DevBuf<int32_t> ch_ncol_, ch_cols_;
     DevBuf<float> ch_tab_;
+    FactSV fc_;
+    DevBuf<int32_t> self_sv_;
     RowCache* cache_ = nullptr;
     double row_ms_ = 0, cached_ms_ = 0, row_bytes_ = 0, cached_bytes_ = 0;
     int64_t row_launches_ = 0, row_rows_ = 0, cached_launches_ = 0;
@@ -288,6 +304,9 @@ struct svm_model {
     int32_t ch_cap = 0;
     msvm::DevBuf<int32_t> ch_ncol, ch_cols;
     msvm::DevBuf<float> ch_tab;
+    // the same rows in chunks by column for the factored path (CSR models
+    // whose rows are sparse enough)
+    msvm::FactSV fc;
     std::vector<int32_t> sv_idx;             // union, increasing
     std::vector<double> coef;                // n_sv x n_out
     std::vector<double> b;                   // n_out
@@ -305,7 +324,26 @@ void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
 // row of t: dense rows directly; sparse CSR rows through the sparse path
 // when a carries the support rows by column; other CSR rows through dense
 // chunks of rows.
-void predict_rows(PredictArgs a, const Features& t, hipStream_t s);
+void predict_rows(PredictArgs a, const Features& t, hipStream_t s,
+                  const FactSV* fc = nullptr);
+
+// Builds fc for support rows idx[0..nsv) of the CSR features f, with
+// coefficients coef (device, nsv x n_out), and writes their norms to sqsv
+// (device, nsv).  Leaves fc.ok false where the factored path does not apply:
+// dense features, more than 4 outputs, support rows holding on average more
+// than a tenth of the columns, a row longer than a chunk, a map over
+// fc_map_bytes_limit(), or SVM_SPARSE_PATH=table in the environment.
+// With query rows given, it is built only if the rule below takes it for
+// them.  predict_rows takes the factored path for query rows t when a
+// query row and a support row share fewer than kFcMatchMax columns on
+// average (nnz(t)/n(t) * fc.sv_nnz / d), else the table path (the
+// factored path pays per shared column about what the table path pays per
+// pair); SVM_SPARSE_PATH=factor takes it whenever it is built (a developer
+// switch for comparing the two paths).
+void build_fact(FactSV& fc, const Features& f, const int32_t* idx,
+                int64_t nsv, const double* coef, int32_t n_out,
+                const KernelFn& kf, Context& cx, float* sqsv,
+                const Features* query = nullptr);
 
 // Capacity (columns per chunk of 16 rows) of the by-column support rows of
 // the sparse decision path for a CSR training set, or 0 when its rows are
