@@ -201,6 +201,13 @@ struct PredictArgs {
     int64_t row_base;     // training-set index of query row 0 (self_match)
     const int32_t* self_sv;  // factored sparse path: training row -> its
                              // support row or -1 (nullptr: no self pairs)
+    // dense paths: the support rows are split into nrange ranges of whole
+    // 64-row tiles (predict_ranges(nsv), so a row's value does not depend
+    // on the batch it comes in); with nrange > 1 each range's sums go to
+    // part (nrange x m x n_out) and a second kernel adds them in range
+    // order, with b
+    int32_t nrange;
+    double* part;
     double* out;          // m x n_out
     KernelFn kf;
     // sparse path: CSR query rows, and the support rows by column in
@@ -420,6 +427,10 @@ void launch_gather_rows(const float* X, const float* sq, int64_t ldp,
                         const int32_t* idx, int64_t k, float* out,
                         float* sq_out, hipStream_t s);
 void launch_predict(const PredictArgs& a, hipStream_t s);
+// ranges of support rows of the dense decision kernels (1 to 8, set by the
+// number of support rows only), and the doubles of part they need for m rows
+int32_t predict_ranges(int64_t nsv);
+int64_t predict_part_doubles(int64_t nsv, int64_t m, int32_t n_out);
 void launch_sv_chunks(const ChunkArgs& a, hipStream_t s);
 void launch_predict_sparse(const PredictArgs& a, hipStream_t s);
 // LDS of the sparse decision kernel, and whether it fits

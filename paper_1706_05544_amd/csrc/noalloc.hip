@@ -2,11 +2,12 @@
 // allocate (code under HIP graph capture, tight serving loops).
 //
 // svm_predict stages the query rows in buffers it allocates (a padded copy
-// of X, their norms, the decision values).  This variant stages what it
-// needs in one static per-device array instead and writes the decision
-// values straight to the caller's buffer; the kernels are the same
-// (k_pad_copy, k_scale_apply, k_norms, k_predict, k_affine), so the values
-// are bitwise those of svm_predict.
+// of X, their norms, the partial sums over ranges of support rows, the
+// decision values).  This variant stages what it needs in one static
+// per-device array instead and writes the decision values straight to the
+// caller's buffer; the kernels are the same (k_pad_copy, k_scale_apply,
+// k_norms, the decision kernels), so the values are bitwise those of
+// svm_predict.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -58,8 +59,10 @@ int64_t noalloc_rows_per_chunk(const svm_model& mdl, const float* X,
                                int64_t ld)
 {
     const bool copy = noalloc_needs_copy(mdl, X, ld);
-    const int64_t row = (copy ? mdl.ldp * 4 : 0) + 4;
-    int64_t rows = (int64_t)(kScratchBytes - kScratchHead - 256) / row;
+    // a staged row, its norm and its partial sums over the support ranges
+    const int64_t row = (copy ? mdl.ldp * 4 : 0) + 4 +
+                        predict_part_doubles(mdl.n_sv, 1, mdl.n_out) * 8;
+    int64_t rows = (int64_t)(kScratchBytes - kScratchHead - 512) / row;
     if (rows >= 64) rows &= ~(int64_t)63;
     return rows;
 }
@@ -80,9 +83,16 @@ void predict_noalloc(const svm_model& mdl, const float* X, int64_t m,
     int32_t* bad = reinterpret_cast<int32_t*>(base);  // never read
     float* sq = reinterpret_cast<float*>(base + kScratchHead);
     const size_t sq_bytes = ((size_t)chunk * 4 + 255) & ~(size_t)255;
-    float* rows = reinterpret_cast<float*>(base + kScratchHead + sq_bytes);
-    if (copy && kScratchHead + sq_bytes + (size_t)chunk * ldp * 4 >
-                    kScratchBytes)
+    const size_t part_bytes =
+        ((size_t)predict_part_doubles(mdl.n_sv, chunk, mdl.n_out) * 8 + 255) &
+        ~(size_t)255;
+    double* part =
+        reinterpret_cast<double*>(base + kScratchHead + sq_bytes);
+    float* rows = reinterpret_cast<float*>(base + kScratchHead + sq_bytes +
+                                           part_bytes);
+    if (kScratchHead + sq_bytes + part_bytes +
+            (copy ? (size_t)chunk * ldp * 4 : 0) >
+        kScratchBytes)
         throw Error{SVM_E_INTERNAL, "staging layout"};
 
     PredictArgs a{};
@@ -96,6 +106,8 @@ void predict_noalloc(const svm_model& mdl, const float* X, int64_t m,
     a.self_match = 0;
     a.kf = mdl.kf;
     a.ldp = ldp;
+    a.nrange = predict_ranges(mdl.n_sv);
+    a.part = a.nrange > 1 ? part : nullptr;
     for (int64_t r0 = 0; r0 < m; r0 += chunk) {
         const int64_t k = m - r0 < chunk ? m - r0 : chunk;
         const float* src = X + r0 * ld;

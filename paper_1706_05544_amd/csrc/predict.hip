@@ -12,6 +12,8 @@
 // applies the RBF epilogue and accumulates c_j K in fp64 per lane.  The
 // per-lane partial sums are reduced across the 16 support columns at the
 // end, so each output is written once, without atomics.
+#include <algorithm>
+
 #include "common.hpp"
 #include "device.hpp"
 
@@ -19,6 +21,37 @@ namespace msvm {
 
 constexpr int kPredDK = 64;            // features per LDS chunk
 constexpr int kPredLS = kPredDK + 4;   // padded LDS row stride
+
+// Support rows [lo, hi) of range r of nrange: whole 64-row tiles, split as
+// evenly as the tiles allow.
+__device__ __forceinline__ void predict_range_of(int64_t nsv, int nrange,
+                                                 int r, int64_t& lo,
+                                                 int64_t& hi)
+{
+    const int64_t tiles = (nsv + 63) / 64;
+    lo = 64 * (tiles * r / nrange);
+    hi = min(nsv, 64 * (tiles * (r + 1) / nrange));
+}
+
+// A row's sums: the decision values (one range), or the range's partial
+// sums (several ranges; k_predict_sum adds them with b).
+template <int NOUT>
+__device__ __forceinline__ void predict_store(const PredictArgs& a,
+                                              int64_t row,
+                                              const double (&part)[NOUT][4],
+                                              int nl)
+{
+    const int n_out = a.n_out;
+#pragma unroll
+    for (int o = 0; o < NOUT; ++o) {
+        if (o >= n_out) continue;
+        const double v = pick4(part[o], nl);
+        if (a.nrange <= 1)
+            a.out[row * n_out + o] = v + (a.b ? a.b[o] : 0.0);
+        else
+            a.part[((int64_t)blockIdx.y * a.m + row) * n_out + o] = v;
+    }
+}
 
 template <int NOUT>
 __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
@@ -45,7 +78,9 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
         for (int v = 0; v < 4; ++v) part[o][v] = 0.0;
 
     const int q4c = kPredDK / 4;
-    for (int64_t sv0 = 0; sv0 < nsv; sv0 += 64) {
+    int64_t sv_lo, sv_hi;
+    predict_range_of(nsv, a.nrange, (int)blockIdx.y, sv_lo, sv_hi);
+    for (int64_t sv0 = sv_lo; sv0 < sv_hi; sv0 += 64) {
         floatx4 acc[4];
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -135,15 +170,7 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
 
     if (nl < 4) {
         const int64_t row = row0 + wave * 16 + 4 * g + nl;
-        if (row < m) {
-#pragma unroll
-            for (int o = 0; o < NOUT; ++o) {
-                if (o < n_out) {
-                    double bias = a.b ? a.b[o] : 0.0;
-                    a.out[row * n_out + o] = pick4(part[o], nl) + bias;
-                }
-            }
-        }
+        if (row < m) predict_store<NOUT>(a, row, part, nl);
     }
 }
 
@@ -200,7 +227,9 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
     // work costs registers, and so occupancy, and measured slower.)
     constexpr int kLd = 64 * (kRaMaxLdp / 4) / 256;
     const int tot = 64 * 4 * kch;
-    for (int64_t sv0 = 0; sv0 < nsv; sv0 += 64) {
+    int64_t sv_lo, sv_hi;
+    predict_range_of(nsv, a.nrange, (int)blockIdx.y, sv_lo, sv_hi);
+    for (int64_t sv0 = sv_lo; sv0 < sv_hi; sv0 += 64) {
         // the tile's epilogue data (it lands during the work below)
         float ssv[4];
         int64_t stn[4];
@@ -294,37 +323,63 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
 
     if (nl < 4) {
         const int64_t row = row0 + wave * 16 + 4 * g + nl;
-        if (row < m) {
-#pragma unroll
-            for (int o = 0; o < NOUT; ++o) {
-                if (o < n_out) {
-                    double bias = a.b ? a.b[o] : 0.0;
-                    a.out[row * n_out + o] = pick4(part[o], nl) + bias;
-                }
-            }
-        }
+        if (row < m) predict_store<NOUT>(a, row, part, nl);
     }
+}
+
+// out = the ranges' partial sums added in range order, + b
+__global__ void k_predict_sum(const double* part, int nrange, int64_t mn,
+                              int n_out, const double* b, double* out)
+{
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < mn;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        double v = 0.0;
+        for (int r = 0; r < nrange; ++r) v += part[(int64_t)r * mn + e];
+        out[e] = v + (b ? b[e % n_out] : 0.0);
+    }
+}
+
+int32_t predict_ranges(int64_t nsv)
+{
+    // about 1600 support rows a range: 64-row work items of 25 tiles, which
+    // fill the chip's block slots in whole rounds for a wide range of m
+    const int64_t r = (nsv + 1599) / 1600;
+    return (int32_t)std::max<int64_t>(1, std::min<int64_t>(8, r));
+}
+
+int64_t predict_part_doubles(int64_t nsv, int64_t m, int32_t n_out)
+{
+    const int32_t r = predict_ranges(nsv);
+    return r > 1 ? (int64_t)r * m * n_out : 0;
 }
 
 void launch_predict(const PredictArgs& a, hipStream_t s)
 {
     if (a.m <= 0) return;
-    unsigned blocks = (unsigned)((a.m + 63) / 64);
+    if (a.nrange < 1 || a.nrange > 8 || (a.nrange > 1 && !a.part))
+        throw Error{SVM_E_INTERNAL, "decision ranges"};
+    const dim3 grid((unsigned)((a.m + 63) / 64), (unsigned)a.nrange);
     if (a.ldp <= kRaMaxLdp && a.n_out <= 4) {
         if (a.n_out <= 1)
-            k_predict_ra<1><<<blocks, 256, 0, s>>>(a);
+            k_predict_ra<1><<<grid, 256, 0, s>>>(a);
         else
-            k_predict_ra<4><<<blocks, 256, 0, s>>>(a);
-        return;
-    }
-    if (a.n_out <= 1)
-        k_predict<1><<<blocks, 256, 0, s>>>(a);
-    else if (a.n_out <= 4)
-        k_predict<4><<<blocks, 256, 0, s>>>(a);
-    else if (a.n_out <= 16)
-        k_predict<16><<<blocks, 256, 0, s>>>(a);
-    else
+            k_predict_ra<4><<<grid, 256, 0, s>>>(a);
+    } else if (a.n_out <= 1) {
+        k_predict<1><<<grid, 256, 0, s>>>(a);
+    } else if (a.n_out <= 4) {
+        k_predict<4><<<grid, 256, 0, s>>>(a);
+    } else if (a.n_out <= 16) {
+        k_predict<16><<<grid, 256, 0, s>>>(a);
+    } else {
         throw Error{SVM_E_UNSUPPORTED, "more than 16 outputs"};
+    }
+    if (a.nrange > 1) {
+        const int64_t mn = a.m * a.n_out;
+        const unsigned blocks =
+            (unsigned)std::min<int64_t>((mn + 255) / 256, 4096);
+        k_predict_sum<<<blocks, 256, 0, s>>>(a.part, a.nrange, mn, a.n_out,
+                                             a.b, a.out);
+    }
 }
 
 }  // namespace msvm

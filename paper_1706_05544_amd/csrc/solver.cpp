@@ -1745,12 +1745,20 @@ void predict_rows(PredictArgs a, const Features& t, hipStream_t s,
                   const FactSV* fc)
 {
     a.ldp = t.ldp;
+    a.nrange = predict_ranges(a.nsv);
     if (!t.csr) {
         a.Xt = t.X.p;
         a.sqt = t.sq.p;
         a.m = t.n;
         a.row_base = 0;
+        DevBuf<double> part;
+        if (a.nrange > 1 && t.n > 0) {
+            part.alloc((size_t)predict_part_doubles(a.nsv, t.n, a.n_out));
+            a.part = part.p;
+        }
         launch_predict(a, s);
+        // the partial sums are freed when the stream has used them
+        if (part.p) HIP_TRY(hipStreamSynchronize(s));
         return;
     }
     if (t.nnz <= 32 * t.n && use_fact(fc, t)) {
@@ -1801,6 +1809,11 @@ void predict_rows(PredictArgs a, const Features& t, hipStream_t s,
     chunk = std::min<int64_t>(chunk, t.n);
     if (chunk <= 0) return;
     DevBuf<float> buf((size_t)(chunk * t.ldp));
+    DevBuf<double> part;
+    if (a.nrange > 1) {
+        part.alloc((size_t)predict_part_doubles(a.nsv, chunk, a.n_out));
+        a.part = part.p;
+    }
     double* out0 = a.out;
     for (int64_t r0 = 0; r0 < t.n; r0 += chunk) {
         const int64_t k = std::min<int64_t>(chunk, t.n - r0);
@@ -1813,7 +1826,7 @@ void predict_rows(PredictArgs a, const Features& t, hipStream_t s,
         a.out = out0 + r0 * a.n_out;
         launch_predict(a, s);
     }
-    // the chunk buffer is freed when the stream has used it
+    // the chunk buffers are freed when the stream has used them
     HIP_TRY(hipStreamSynchronize(s));
 }
 
