@@ -182,12 +182,24 @@ __global__ __launch_bounds__(256) void k_predict(PredictArgs a)
 // chunk order, so the same K bits.
 constexpr int kRaMaxLdp = 128;
 constexpr int kRaLS = kRaMaxLdp + 4;  // padded LDS row stride
+// The support tile goes from memory straight into LDS (buffer loads to LDS:
+// lane l of a wave's load writes 16 bytes at the wave's base + 16 l), in
+// float4 slots of the padded layout: slot S holds row S / 33, float4
+// S % 33 (the 33rd of a row is padding).  4 waves x 9 loads x 64 lanes
+// cover the 64 x 33 slots; slots past the tile, past ldp or past the last
+// support row are written with zeros (range-checked offsets).
+constexpr int kRaSlotsRow = kRaLS / 4;                 // 33
+constexpr int kRaLoads = 9;                            // per wave
+constexpr int kRaSlots = 4 * kRaLoads * 64;            // 2304 >= 64 x 33
+static_assert(kRaSlots >= 64 * kRaSlotsRow, "support tile slots");
+typedef __attribute__((address_space(3))) void* LdsPtr;
 
 template <int NOUT>
-__global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
+__device__ __forceinline__ void predict_ra_body(const PredictArgs& a)
 {
-    __shared__ __align__(16) float Bs[64 * kRaLS];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ __align__(16) float Bs[kRaSlots * 4];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, nl = lane & 15;
     const int64_t m = a.m, ldp = a.ldp, nsv = a.nsv;
     const int64_t row0 = (int64_t)blockIdx.x * 64;
@@ -195,11 +207,12 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
     const int kch = (int)((ldp + 15) / 16);  // 16-feature chunks (<= 8)
 
     float sqr[4];
-    int64_t rid[4];
+    int32_t rself[4];  // training index of the row (self_match), int32
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-        rid[v] = row0 + wave * 16 + 4 * g + v;
-        sqr[v] = rid[v] < m ? a.sqt[rid[v]] : 0.0f;
+        const int64_t r = row0 + wave * 16 + 4 * g + v;
+        sqr[v] = r < m ? a.sqt[r] : 0.0f;
+        rself[v] = (int32_t)(r + a.row_base);
     }
     // this lane's A operand: row wave*16 + nl, features 16c + 4g .. + 3
     float4 ar[kRaMaxLdp / 16];
@@ -220,19 +233,12 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
         for (int v = 0; v < 4; ++v) part[o][v] = 0.0;
 
     const int q4 = (int)(ldp / 4);  // float4 per support row
-    // A support tile: 64 rows x ldp features; thread t holds float4 t +
-    // 256 j of it (a fixed count, all issued before any store: the ones
-    // past the tile, or past ldp in a row, are sent past the end and read
-    // zero).  (Issuing the next tile's loads before this tile's matrix-core
-    // work costs registers, and so occupancy, and measured slower.)
-    constexpr int kLd = 64 * (kRaMaxLdp / 4) / 256;
-    const int tot = 64 * 4 * kch;
     int64_t sv_lo, sv_hi;
     predict_range_of(nsv, a.nrange, (int)blockIdx.y, sv_lo, sv_hi);
     for (int64_t sv0 = sv_lo; sv0 < sv_hi; sv0 += 64) {
         // the tile's epilogue data (it lands during the work below)
         float ssv[4];
-        int64_t stn[4];
+        int32_t stn[4];
         double cf[4][NOUT];
         {
             const Rsrc rQ = make_rsrc(a.sqsv + sv0, (nsv - sv0) * 4);
@@ -257,23 +263,22 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
         }
         const Rsrc rB = make_rsrc(a.SV + sv0 * ldp,
                                   min((int64_t)64, nsv - sv0) * ldp * 4);
-        float4 bvl[kLd];
-#pragma unroll
-        for (int j = 0; j < kLd; ++j) {
-            const int e = tid + 256 * j;
-            const int r = e / (4 * kch), c4 = e - r * (4 * kch);
-            bvl[j] = bld_f4(rB, (e < tot && c4 < q4)
-                                    ? (uint32_t)((r * ldp + 4 * c4) * 4)
-                                    : kOob);
-        }
         __syncthreads();  // the previous tile's reads are done
 #pragma unroll
-        for (int j = 0; j < kLd; ++j) {
-            const int e = tid + 256 * j;
-            const int r = e / (4 * kch), c4 = e - r * (4 * kch);
-            if (e < tot)
-                *reinterpret_cast<float4*>(Bs + r * kRaLS + 4 * c4) = bvl[j];
+        for (int j = 0; j < kRaLoads; ++j) {
+            // this lane's slot of the load, and its offset (kOob: a zero)
+            const int S = (wave * kRaLoads + j) * 64 + lane;
+            const int r = S / kRaSlotsRow, c4 = S - r * kRaSlotsRow;
+            const uint32_t off = (r < 64 && c4 < q4)
+                                     ? (uint32_t)((r * (int)ldp + 4 * c4) * 4)
+                                     : kOob;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rB, (LdsPtr)(Bs + (wave * kRaLoads + j) * 64 * 4), 16,
+                (int)off, 0, 0, 0);
         }
+        // the loads write LDS behind the compiler's back: wait for all of
+        // them (and the epilogue data above) before the barrier
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         floatx4 acc[4];
 #pragma unroll
@@ -297,7 +302,7 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
                 for (int v = 0; v < 4; ++v) {
                     kv[v] = rbf_from_dot(sqr[v], ssv[cb], acc[cb][v],
                                          a.kf.gexp);
-                    if (stn[cb] == rid[v] + a.row_base) kv[v] = 1.0f;
+                    if (stn[cb] == rself[v]) kv[v] = 1.0f;
                 }
             } else {
 #pragma unroll
@@ -325,6 +330,20 @@ __global__ __launch_bounds__(256) void k_predict_ra(PredictArgs a)
         const int64_t row = row0 + wave * 16 + 4 * g + nl;
         if (row < m) predict_store<NOUT>(a, row, part, nl);
     }
+}
+
+// One output: 120 VGPRs, so four waves a SIMD fit (the 64 x 33-slot tile
+// takes 36 KB of LDS, four blocks a CU).  Four outputs keep the default
+// (asking them for four waves spills).
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+void k_predict_ra1(PredictArgs a)
+{
+    predict_ra_body<1>(a);
+}
+
+__global__ __launch_bounds__(256) void k_predict_ra4(PredictArgs a)
+{
+    predict_ra_body<4>(a);
 }
 
 // out = the ranges' partial sums added in range order, + b
@@ -361,9 +380,9 @@ void launch_predict(const PredictArgs& a, hipStream_t s)
     const dim3 grid((unsigned)((a.m + 63) / 64), (unsigned)a.nrange);
     if (a.ldp <= kRaMaxLdp && a.n_out <= 4) {
         if (a.n_out <= 1)
-            k_predict_ra<1><<<grid, 256, 0, s>>>(a);
+            k_predict_ra1<<<grid, 256, 0, s>>>(a);
         else
-            k_predict_ra<4><<<grid, 256, 0, s>>>(a);
+            k_predict_ra4<<<grid, 256, 0, s>>>(a);
     } else if (a.n_out <= 1) {
         k_predict<1><<<grid, 256, 0, s>>>(a);
     } else if (a.n_out <= 4) {
