@@ -1497,8 +1497,9 @@ void build_model(svm_model& m, Context& cx, const Features& f,
     if (m.ch_cap > 0)
         build_sv_chunks(f, idx.p, nsv, m.ch_cap, m.ch_ncol, m.ch_cols,
                         m.ch_tab, nullptr, s);
+    // (the training rows stand in for the query rows in the path rule)
     if (f.csr)
-        build_fact(m.fc, f, idx.p, nsv, cc.p, n_out, m.kf, cx, m.sqsv.p);
+        build_fact(m.fc, f, idx.p, nsv, cc.p, n_out, m.kf, cx, m.sqsv.p, &f);
     m.sv_idx.resize((size_t)nsv);
     m.coef.resize((size_t)(nsv * n_out));
     if (nsv > 0) {
