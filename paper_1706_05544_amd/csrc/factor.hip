@@ -27,7 +27,6 @@ namespace msvm {
 constexpr int kFcWaves = 4;     // waves of a block (independent)
 constexpr int kFcRW = 16;       // query rows of a wave
 constexpr int kFcGroup = 8;     // entry loads issued together
-constexpr int kFcSpa = kFcSvMax;  // accumulator slots of a wave
 constexpr uint32_t kFcLenMask = (1u << kFcLenBits) - 1;
 // Rows with gexp * |x|^2 above kFcSafe take the direct formula, so that
 // e^(-g s_x) and the factor 2^(2 gexp x.v) stay inside fp64 and fp32 range
@@ -272,11 +271,11 @@ __global__ __launch_bounds__(kFcWaves * 64) void k_predict_fact(FactArgs a)
     extern __shared__ __align__(16) unsigned char smem[];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    float* sp = reinterpret_cast<float*>(smem) + wave * kFcSpa;
-    double* rs = reinterpret_cast<double*>(smem + kFcWaves * kFcSpa * 4) +
+    float* sp = reinterpret_cast<float*>(smem) + wave * kFcSvMax;
+    double* rs = reinterpret_cast<double*>(smem + kFcWaves * kFcSvMax * 4) +
                  wave * kFcRW * (NOUT + 1);
     double* rA = rs + kFcRW * NOUT;  // per row: e^(-g s_x) (RBF), else 1
-    for (int i = lane; i < kFcSpa; i += 64) sp[i] = 0.0f;
+    for (int i = lane; i < kFcSvMax; i += 64) sp[i] = 0.0f;
     const int64_t r0 = ((int64_t)blockIdx.x * kFcWaves + wave) * kFcRW;
     const int rows = (int)min<int64_t>(kFcRW, a.m - r0);
     if (rows <= 0) return;  // (no barrier in this kernel)
@@ -352,7 +351,7 @@ __global__ __launch_bounds__(kFcWaves * 64) void k_predict_fact(FactArgs a)
 
 static size_t fc_lds_bytes(int nout)
 {
-    return (size_t)kFcWaves * kFcSpa * 4 +
+    return (size_t)kFcWaves * kFcSvMax * 4 +
            (size_t)kFcWaves * kFcRW * (nout + 1) * 8;
 }
 

@@ -5,13 +5,19 @@
 // scratch once the incremental solve has converged.
 //
 // Tiling: a block of 4 waves owns 64 test rows (16 per wave, the MFMA row
-// tile) and walks over the support rows 64 at a time.  For every 64-feature
-// chunk both operand tiles are staged in LDS (row stride padded by 4 floats
-// against bank conflicts); each wave accumulates its 16 x 64 dot products on
-// the matrix cores in the feature order shared with the training kernels,
-// applies the RBF epilogue and accumulates c_j K in fp64 per lane.  The
-// per-lane partial sums are reduced across the 16 support columns at the
-// end, so each output is written once, without atomics.
+// tile) and one range of the support rows (up to 8 ranges of whole 64-row
+// tiles, set by the number of support rows), which it walks 64 rows at a
+// time.  Each wave accumulates its 16 x 64 dot products on the matrix cores
+// in the feature order shared with the training kernels, applies the RBF
+// epilogue and accumulates c_j K in fp64 per lane; the per-lane partial sums
+// are reduced across the 16 support columns at the end of the range.  With
+// one range that is the output (+ b); with several, each range's sums go to
+// a buffer that k_predict_sum adds in range order, so each output is
+// written once, without atomics, and the same bits whatever the batch.
+// k_predict stages both operand tiles in LDS by 64-feature chunks (row
+// stride padded by 4 floats against bank conflicts); for rows of at most
+// 128 features k_predict_ra keeps the query rows in registers and loads
+// each support tile straight into LDS.
 #include <algorithm>
 
 #include "common.hpp"
