@@ -20,10 +20,15 @@
  * active-set enumeration), tests/test_oracle_invariants.py (constraints, KKT,
  * monotone objective), tests/test_oracle_vs_libsvm.py (scikit-learn's LIBSVM
  * endpoint).  The subproblem and working-set helpers are pinned by
- * tests/test_oracle_select.py.  The linear, polynomial and sigmoid kernels
+ * tests/test_oracle_select.py, the tie-break to the lowest index among
+ * equal keys included (the alpha = 0 state, where all keys of a side tie).
+ * The bias rule (mean key over the free variables, else the midpoint of m
+ * and M) is pinned by tests/test_oracle_bias.py on hand-worked states where
+ * the two differ.  The linear, polynomial and sigmoid kernels
  * are pinned by tests/test_oracle_kernels.py (scikit-learn's pairwise
  * kernels, worked numbers, the 2-point closed form and its single step,
- * the exact QP optimum, LIBSVM's endpoint).
+ * the exact QP optimum, LIBSVM's endpoint).  tests/test_sanitizers.py
+ * runs every function under AddressSanitizer and UndefinedBehaviorSanitizer.
  */
 #include "svm_oracle.h"
 
