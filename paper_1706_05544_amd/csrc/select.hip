@@ -906,8 +906,21 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             const int ia = e / nS, ib = e - ia * nS;
             float k = 1.0f;
             if (ia != ib || !kernel_self_is_one(a.kf)) {
+                // the sum in column order (the row kernel's order), eight
+                // columns' loads issued ahead of their fmas
                 float acc = 0.0f;
-                for (int r = 0; r < E; ++r)
+                int r = 0;
+                for (; r + 8 <= E; r += 8) {
+                    float va[8], vb[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        va[u] = tab[(r + u) * QS + ia];
+                        vb[u] = tab[(r + u) * QS + ib];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) acc = fmaf(va[u], vb[u], acc);
+                }
+                for (; r < E; ++r)
                     acc = fmaf(tab[r * QS + ia], tab[r * QS + ib], acc);
                 const float qa = e == tid ? sqa : a.sq[shS[ia]];
                 const float qb = e == tid ? sqb : a.sq[shS[ib]];
