@@ -102,7 +102,10 @@ typedef struct {
     int64_t max_iter;      /* outer iterations; <= 0: max(1e7, 100 N) */
     int32_t working_set;   /* q, even, in [2, 64]; 16 as in Section 3 */
     int32_t device;        /* HIP device ordinal */
-    int64_t cache_bytes;   /* kernel-row cache budget; 0 default, < 0 off */
+    int64_t cache_bytes;   /* kernel-row cache budget; < 0 off; 0 default:
+                              the whole K if it fits a quarter of the free
+                              device memory, else a quarter of it, at most
+                              8 GiB */
     void *stream;          /* hipStream_t; NULL: a stream of the library */
     int32_t check_every;   /* outer iterations between host polls (0: 64) */
     double inner_ratio;    /* subproblem stops at local gap <= max(ratio *

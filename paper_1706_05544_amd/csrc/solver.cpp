@@ -191,9 +191,12 @@ void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
     const int64_t row = c.ldc * (int64_t)sizeof(float);
     size_t free_b = 0, total_b = 0;
     HIP_TRY(hipMemGetInfo(&free_b, &total_b));
-    // default: a quarter of the free memory, at most 8 GiB; an explicit
-    // budget may use the free memory but 2 GiB (left to the caller)
+    // default: the whole K when it fits a quarter of the free memory (the
+    // cache then keeps every row it computes); otherwise a quarter of the
+    // free memory, at most 8 GiB.  An explicit budget may use the free
+    // memory but 2 GiB (left to the caller).
     int64_t cap = std::min<int64_t>((int64_t)(free_b / 4), (int64_t)8 << 30);
+    if (n * row <= (int64_t)(free_b / 4)) cap = n * row;
     if (bytes > 0)
         cap = std::min<int64_t>(bytes,
                                 std::max<int64_t>((int64_t)free_b -

@@ -17,6 +17,14 @@ shared structure (prototypes, weight vector) 1000k.
   C5  C-SVC   n=2e6,    d=1000, CSR, 20 distinct columns per row, N(0,1)
       values, y = sign(w.x + N(0,0.5^2)) with sign(0) = +1
 
+Two more take the shapes of the paper's own data sets, with the C2 and C3
+recipes (the paper gives no value distributions), and 10 % more points as
+the test set:
+
+  PSVR  eps-SVR n=113978, d=120, the C2 recipe (the target uses x0, x1, x2;
+        the other 117 features are U[-1,1] noise), gamma = 1/120
+  PSVC  C-SVC   n=68971,  d=501, the C3 recipe (means +-0.2*1), gamma = 1/501
+
 Sizes can be overridden (``n=``, ``n_test=``) to get a smaller problem with
 the same recipe; the data then differ from the full-size draw.
 """
@@ -79,8 +87,8 @@ def c1(n: int = 2000, n_test: int = 1000) -> Workload:
     return _gauss_pair(1, n, n_test, 20, 0.5, 1.0, 1.0 / 20, "C1")
 
 
-def c2(n: int = 20000, n_test: int = 5000) -> Workload:
-    d = 50
+def c2(n: int = 20000, n_test: int = 5000, d: int = 50, k: int = 2,
+       name: str = "C2") -> Workload:
 
     def draw(rng, m):
         X = rng.uniform(-1.0, 1.0, (m, d))
@@ -88,18 +96,26 @@ def c2(n: int = 20000, n_test: int = 5000) -> Workload:
              + rng.normal(0.0, 0.1, m))
         return X, z
 
-    rng = _rng(2001)
+    rng = _rng(1000 * k + 1)
     X, z = draw(rng, n)
     perm = rng.permutation(n)
     X, z = X[perm], z[perm]
-    Xt, zt = draw(_rng(2002), n_test)
-    return Workload("C2", EPS_SVR, X.astype(np.float32), z.astype(np.float32),
+    Xt, zt = draw(_rng(1000 * k + 2), n_test)
+    return Workload(name, EPS_SVR, X.astype(np.float32), z.astype(np.float32),
                     Xt.astype(np.float32), zt.astype(np.float32), C=10.0,
                     gamma=1.0 / d, eps=0.1)
 
 
 def c3(n: int = 100000, n_test: int = 20000) -> Workload:
     return _gauss_pair(3, n, n_test, 128, 0.2, 1.0, 1.0 / 128, "C3")
+
+
+def psvr(n: int = 113978, n_test: int = 11398) -> Workload:
+    return c2(n, n_test, d=120, k=6, name="PSVR")
+
+
+def psvc(n: int = 68971, n_test: int = 6897) -> Workload:
+    return _gauss_pair(7, n, n_test, 501, 0.2, 1.0, 1.0 / 501, "PSVC")
 
 
 def _c4_prototypes(d: int, n_classes: int, support: int):
@@ -183,7 +199,8 @@ def c5(n: int = 2000000, n_test: int = 1000000) -> Workload:
 
 def make(name: str, n: Optional[int] = None, n_test: Optional[int] = None,
          **kw) -> Workload:
-    gen = {"C1": c1, "C2": c2, "C3": c3, "C4": c4, "C5": c5}[name.upper()]
+    gen = {"C1": c1, "C2": c2, "C3": c3, "C4": c4, "C5": c5,
+           "PSVR": psvr, "PSVC": psvc}[name.upper().replace("-", "")]
     args = dict(kw)
     if n is not None:
         args["n"] = n

@@ -1,49 +1,82 @@
-"""Seeded generators: determinism, shapes and the stated structure."""
+"""The seeded input generators: shapes, parameters, determinism and the
+recipe of each workload (small sizes; the full-size draws follow the same
+code)."""
 import numpy as np
+import pytest
+import scipy.sparse as sp
 
-from paper_1706_05544_amd import workloads
-
-
-def test_deterministic_and_shapes():
-    a = workloads.c1()
-    b = workloads.c1()
-    assert np.array_equal(a.X, b.X) and np.array_equal(a.y, b.y)
-    assert a.X.shape == (2000, 20) and a.X.dtype == np.float32
-    assert a.Xt.shape == (1000, 20)
-    assert np.sum(a.y == 1) == 1000 and np.sum(a.y == -1) == 1000
-    assert a.gamma == 1.0 / 20 and a.C == 1.0
+from paper_1706_05544_amd import workloads as wl
 
 
-def test_class_means_c3_small():
-    w = workloads.c3(n=20000, n_test=100)
-    assert w.X.shape == (20000, 128)
-    mp = w.X[w.y > 0].mean()
-    mn = w.X[w.y < 0].mean()
-    assert abs(mp - 0.2) < 0.01 and abs(mn + 0.2) < 0.01
+@pytest.mark.parametrize("name,d,typ,gamma", [
+    ("C1", 20, wl.C_SVC, 1 / 20), ("C2", 50, wl.EPS_SVR, 1 / 50),
+    ("C3", 128, wl.C_SVC, 1 / 128), ("PSVR", 120, wl.EPS_SVR, 1 / 120),
+    ("PSVC", 501, wl.C_SVC, 1 / 501)])
+def test_dense_shapes_and_parameters(name, d, typ, gamma):
+    w = wl.make(name, n=300, n_test=40)
+    assert w.X.shape == (300, d) and w.Xt.shape == (40, d)
+    assert w.X.dtype == np.float32 and w.y.dtype == np.float32
+    assert w.type == typ and w.gamma == pytest.approx(gamma)
+    if typ == wl.C_SVC:
+        assert set(np.unique(w.y)) <= {-1.0, 1.0}
+        assert (w.y > 0).sum() == 150  # equal class sizes, shuffled
+    else:
+        assert np.all(np.abs(w.X) <= 1.0)  # U[-1, 1] features
+    again = wl.make(name, n=300, n_test=40)
+    assert np.array_equal(w.X, again.X) and np.array_equal(w.yt, again.yt)
 
 
-def test_c2_targets():
-    w = workloads.c2(n=3000, n_test=100)
-    assert w.type == workloads.EPS_SVR
-    assert w.X.min() >= -1 and w.X.max() <= 1
-    resid = w.y - (np.sin(3 * w.X[:, 0]) + 0.5 * w.X[:, 1] * w.X[:, 2])
-    assert abs(np.std(resid) - 0.1) < 0.01
+def test_full_size_defaults():
+    # the sizes of the data sets of Section 5 (not drawn: only the
+    # generators' defaults are read)
+    import inspect
+    assert inspect.signature(wl.psvr).parameters["n"].default == 113978
+    assert inspect.signature(wl.psvc).parameters["n"].default == 68971
 
 
-def test_c4_density_and_classes():
-    w = workloads.c4(n=2000, n_test=200)
-    dens = np.count_nonzero(w.X) / w.X.size
-    assert 0.15 < dens < 0.25
-    assert set(np.unique(w.y)) == set(range(10))
-    assert w.X.min() >= 0 and w.X.max() <= 1
+def test_names_are_case_and_dash_insensitive():
+    a = wl.make("p-svr", n=50, n_test=5)
+    b = wl.make("PSVR", n=50, n_test=5)
+    assert a.name == "PSVR" and np.array_equal(a.X, b.X)
 
 
-def test_c5_structure():
-    w = workloads.c5(n=5000, n_test=100)
-    X = w.X
-    assert X.shape == (5000, 1000)
-    assert np.all(np.diff(X.indptr) == 20)
-    for i in range(0, 5000, 97):
-        cols = X.indices[X.indptr[i]:X.indptr[i + 1]]
-        assert np.all(np.diff(cols) > 0)
-    assert set(np.unique(w.y)) == {-1.0, 1.0}
+def test_c2_recipe_target():
+    # z = sin(3 x0) + 0.5 x1 x2 + N(0, 0.1^2): the residual has sd 0.1
+    w = wl.c2(n=4000, n_test=10)
+    X = w.X.astype(np.float64)
+    r = w.y - (np.sin(3 * X[:, 0]) + 0.5 * X[:, 1] * X[:, 2])
+    assert abs(r.mean()) < 0.01 and 0.09 < r.std() < 0.11
+    # the same recipe at d = 120 with its own seeds
+    p = wl.psvr(n=4000, n_test=10)
+    Xp = p.X.astype(np.float64)
+    rp = p.y - (np.sin(3 * Xp[:, 0]) + 0.5 * Xp[:, 1] * Xp[:, 2])
+    assert 0.09 < rp.std() < 0.11
+    assert not np.array_equal(p.X[:, :50], w.X)
+
+
+def test_gaussian_pair_means():
+    # x = y * 0.2 * 1 + N(0, I): the class means sit at +-0.2
+    w = wl.psvc(n=4000, n_test=10)
+    X = w.X.astype(np.float64)
+    m_pos = X[w.y > 0].mean()
+    m_neg = X[w.y < 0].mean()
+    assert abs(m_pos - 0.2) < 0.01 and abs(m_neg + 0.2) < 0.01
+
+
+def test_c5_rows_have_twenty_distinct_sorted_columns():
+    w = wl.c5(n=2000, n_test=100)
+    assert sp.isspmatrix_csr(w.X) and w.X.shape == (2000, 1000)
+    nnz = np.diff(w.X.indptr)
+    assert np.all(nnz == 20)
+    cols = w.X.indices.reshape(2000, 20)
+    assert np.all(np.diff(cols, axis=1) > 0)
+
+
+def test_c4_one_vs_rest_labels():
+    w = wl.c4(n=500, n_test=50)
+    assert w.n_classes == 10 and w.y.dtype == np.int32
+    assert np.bincount(w.y, minlength=10).tolist() == [50] * 10
+    assert np.all((w.X >= 0) & (w.X <= 1))
+    c = wl.c4(n=500, n_test=50, layout="csr")
+    assert sp.isspmatrix_csr(c.X)
+    assert np.array_equal(c.X.toarray(), w.X)
