@@ -17,6 +17,10 @@ shared structure (prototypes, weight vector) 1000k.
   C5  C-SVC   n=2e6,    d=1000, CSR, 20 distinct columns per row, N(0,1)
       values, y = sign(w.x + N(0,0.5^2)) with sign(0) = +1
 
+C3B is C3 with the class means at +-0.1133*1 (10 % Bayes error instead of
+1.2 %; the same seeds): the same bytes per iteration, more iterations and
+support vectors.
+
 Two more take the shapes of the paper's own data sets, with the C2 and C3
 recipes (the paper gives no value distributions), and 10 % more points as
 the test set:
@@ -110,6 +114,12 @@ def c3(n: int = 100000, n_test: int = 20000) -> Workload:
     return _gauss_pair(3, n, n_test, 128, 0.2, 1.0, 1.0 / 128, "C3")
 
 
+def c3b(n: int = 100000, n_test: int = 20000) -> Workload:
+    # C3's draw at the offset that gives a 10 % Bayes error:
+    # Phi(-0.1133 sqrt(128)) = 0.10
+    return _gauss_pair(3, n, n_test, 128, 0.1133, 1.0, 1.0 / 128, "C3B")
+
+
 def psvr(n: int = 113978, n_test: int = 11398) -> Workload:
     return c2(n, n_test, d=120, k=6, name="PSVR")
 
@@ -199,7 +209,7 @@ def c5(n: int = 2000000, n_test: int = 1000000) -> Workload:
 
 def make(name: str, n: Optional[int] = None, n_test: Optional[int] = None,
          **kw) -> Workload:
-    gen = {"C1": c1, "C2": c2, "C3": c3, "C4": c4, "C5": c5,
+    gen = {"C1": c1, "C2": c2, "C3": c3, "C3B": c3b, "C4": c4, "C5": c5,
            "PSVR": psvr, "PSVC": psvc}[name.upper().replace("-", "")]
     args = dict(kw)
     if n is not None:

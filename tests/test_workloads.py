@@ -10,7 +10,8 @@ from paper_1706_05544_amd import workloads as wl
 
 @pytest.mark.parametrize("name,d,typ,gamma", [
     ("C1", 20, wl.C_SVC, 1 / 20), ("C2", 50, wl.EPS_SVR, 1 / 50),
-    ("C3", 128, wl.C_SVC, 1 / 128), ("PSVR", 120, wl.EPS_SVR, 1 / 120),
+    ("C3", 128, wl.C_SVC, 1 / 128), ("C3B", 128, wl.C_SVC, 1 / 128),
+    ("PSVR", 120, wl.EPS_SVR, 1 / 120),
     ("PSVC", 501, wl.C_SVC, 1 / 501)])
 def test_dense_shapes_and_parameters(name, d, typ, gamma):
     w = wl.make(name, n=300, n_test=40)
@@ -61,6 +62,15 @@ def test_gaussian_pair_means():
     m_pos = X[w.y > 0].mean()
     m_neg = X[w.y < 0].mean()
     assert abs(m_pos - 0.2) < 0.01 and abs(m_neg + 0.2) < 0.01
+
+
+def test_c3b_is_c3_at_a_smaller_offset():
+    # the same seeds: the noise is C3's, the means move from 0.2 to 0.1133
+    a = wl.c3(n=1000, n_test=10)
+    b = wl.c3b(n=1000, n_test=10)
+    assert np.array_equal(a.y, b.y)
+    diff = (a.X.astype(np.float64) - b.X) * a.y[:, None]
+    assert np.allclose(diff, 0.2 - 0.1133, atol=1e-6)
 
 
 def test_c5_rows_have_twenty_distinct_sorted_columns():
