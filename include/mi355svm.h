@@ -105,7 +105,8 @@ typedef struct {
     int64_t cache_bytes;   /* kernel-row cache budget; < 0 off; 0 default:
                               the whole K if it fits a quarter of the free
                               device memory, else a quarter of it, at most
-                              8 GiB */
+                              8 GiB (the memory is kept for the next
+                              training: svm_cache_release) */
     void *stream;          /* hipStream_t; NULL: a stream of the library */
     int32_t check_every;   /* outer iterations between host polls (0: 64) */
     double inner_ratio;    /* subproblem stops at local gap <= max(ratio *
@@ -264,6 +265,18 @@ svm_status svm_model_get(const svm_model *m, int32_t output, int32_t *sv_idx,
                          double *coef, double *alpha);
 
 void svm_model_free(svm_model *m);
+
+/* Memory management of the library, not an operation of the method.  The
+ * device memory of the kernel-row cache (svm_params.cache_bytes) is kept
+ * per device between trainings, one block as large as the largest cache
+ * used so far on that device, and lent to one training at a time (a
+ * training that finds it in use allocates its own): allocating and freeing
+ * tens of GB per training would make later allocations wait while the
+ * driver clears the freed memory.  This frees the kept block of `device`
+ * (device < 0: of every device) unless a training holds it, and writes
+ * the bytes freed to *freed (nullable).  Errors: SVM_E_INVALID for a
+ * device ordinal out of range, SVM_E_DEVICE without a HIP device. */
+svm_status svm_cache_release(int32_t device, int64_t *freed);
 
 /* k-fold cross-validation (Section 3's feature list: "K-fold cross
  * validation", "accuracy or correlation, mean square error").  Give either

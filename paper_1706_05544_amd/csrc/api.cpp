@@ -855,6 +855,18 @@ svm_status svm_model_get(const svm_model* m, int32_t output, int32_t* sv_idx,
 
 void svm_model_free(svm_model* m) { delete m; }
 
+svm_status svm_cache_release(int32_t device, int64_t* freed)
+{
+    if (freed) *freed = 0;
+    svm_status st;
+    if (device >= 0 && (st = check_device(device)) != SVM_OK) return st;
+    GUARD_BEGIN
+    const size_t b = msvm::cache_pool_trim(device);
+    if (freed) *freed = (int64_t)b;
+    return SVM_OK;
+    GUARD_END
+}
+
 svm_status svm_test_solver_create(const svm_matrix* X, const float* y,
                                   const svm_params* p, svm_solver** out)
 {

@@ -391,6 +391,10 @@ void launch_rows(const RowArgs& a, int nblocks, int nblk_cols, bool svr,
 size_t rows_lds_bytes(int nblk_cols, int64_t ldp, int tiles, bool svr,
                       int csr_cols);
 int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
+// Resident blocks per compute unit of (kernel, block size, dynamic LDS)
+// from the runtime, at least 1; asked once per process and kept (the
+// library builds for one architecture).
+int occupancy_memo(const void* kernel, int threads, size_t lds);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
 // one block per problem (P <= kLockMax entries, each with working sets of
 // 16), the arguments passed by value in the launch

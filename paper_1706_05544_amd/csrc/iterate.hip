@@ -988,14 +988,8 @@ void launch_iter(const IterArgs& a, int nblocks, bool svr, hipStream_t s,
 
 int iter_blocks_per_cu(bool svr, size_t lds)
 {
-    int bpc = 0;
     const void* f = svr ? (const void*)k_iter<true> : (const void*)k_iter<false>;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&bpc, f, kIterThreads,
-                                                     lds) != hipSuccess) {
-        (void)hipGetLastError();
-        return 1;
-    }
-    return bpc > 0 ? bpc : 1;
+    return occupancy_memo(f, kIterThreads, lds);
 }
 
 }  // namespace msvm

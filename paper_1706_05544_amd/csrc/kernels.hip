@@ -3,6 +3,9 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 #include "common.hpp"
 #include "device.hpp"
@@ -343,6 +346,25 @@ void launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s)
 {
     if (n <= 0) return;
     k_fill_i32<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p, v, n);
+}
+
+int occupancy_memo(const void* kernel, int threads, size_t lds)
+{
+    static std::mutex mu;
+    static std::map<std::tuple<const void*, int, size_t>, int> memo;
+    const auto key = std::make_tuple(kernel, threads, lds);
+    std::lock_guard<std::mutex> g(mu);
+    const auto it = memo.find(key);
+    if (it != memo.end()) return it->second;
+    int bpc = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&bpc, kernel, threads,
+                                                     lds) != hipSuccess) {
+        (void)hipGetLastError();
+        bpc = 0;
+    }
+    const int r = bpc > 0 ? bpc : 1;
+    memo[key] = r;
+    return r;
 }
 
 // State bytes from a given alpha (test hooks).

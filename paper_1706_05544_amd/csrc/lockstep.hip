@@ -403,14 +403,7 @@ static void lock_dispatch(const LockArgs& a, int nblocks, hipStream_t s,
 template <bool SVR, int P>
 static int lock_occupancy(size_t lds)
 {
-    int bpc = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &bpc, (const void*)k_lock<SVR, P>, kRowThreads, lds) !=
-        hipSuccess) {
-        (void)hipGetLastError();
-        return 1;
-    }
-    return bpc > 0 ? bpc : 1;
+    return occupancy_memo((const void*)k_lock<SVR, P>, kRowThreads, lds);
 }
 
 int lock_blocks_per_cu(int P, bool svr, size_t lds)

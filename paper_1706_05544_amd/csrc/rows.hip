@@ -923,14 +923,8 @@ static void rows_mode(const RowArgs& a, int nblocks, hipStream_t s,
 template <bool SVR, int NBLK, bool CSR>
 static int rows_occupancy(size_t lds)
 {
-    int bpc = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &bpc, (const void*)k_rows<SVR, NBLK, kModeHot, CSR>, kRowThreads,
-            lds) != hipSuccess) {
-        (void)hipGetLastError();
-        return 1;
-    }
-    return bpc > 0 ? bpc : 1;
+    return occupancy_memo(
+        (const void*)k_rows<SVR, NBLK, kModeHot, CSR>, kRowThreads, lds);
 }
 
 // The CSR row kernel covers up to 32 working-set slots (its per-lane

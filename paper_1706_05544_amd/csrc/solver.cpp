@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 namespace msvm {
 
@@ -181,6 +182,107 @@ KernelFn kernel_fn(const SolveOptions& o)
 // solver
 // ---------------------------------------------------------------------------
 
+namespace {
+
+struct CachePool {
+    std::mutex mu;
+    float* p = nullptr;
+    size_t bytes = 0;
+    bool lent = false;
+};
+
+constexpr int kPoolDevices = 64;
+
+CachePool& pool_of(int dev)
+{
+    static CachePool pools[kPoolDevices];
+    if (dev < 0 || dev >= kPoolDevices)
+        throw Error{SVM_E_INVALID, "device ordinal out of range"};
+    return pools[dev];
+}
+
+// wait for the device's work (on its own current-device setting)
+void sync_device(int dev)
+{
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) cur = -1;
+    if (cur != dev) (void)hipSetDevice(dev);
+    (void)hipDeviceSynchronize();
+    if (cur >= 0 && cur != dev) (void)hipSetDevice(cur);
+}
+
+}  // namespace
+
+void CacheRows::alloc(size_t n, int dev)
+{
+    release();
+    if (n == 0) n = 1;
+    const size_t b = n * sizeof(float);
+    CachePool& pl = pool_of(dev);
+    std::lock_guard<std::mutex> g(pl.mu);
+    if (!pl.lent) {
+        if (pl.bytes < b) {
+            if (pl.p) (void)hipFree(pl.p);
+            pl.p = nullptr;
+            pl.bytes = 0;
+            HIP_TRY(hipMalloc((void**)&pl.p, b));
+            pl.bytes = b;
+        }
+        pl.lent = true;
+        p = pl.p;
+        lent = true;
+    } else {
+        HIP_TRY(hipMalloc((void**)&p, b));
+    }
+    count = n;
+    device = dev;
+}
+
+void CacheRows::release()
+{
+    if (!p) return;
+    if (lent) {
+        // no kernel of this cache may still read the block when the next
+        // cache gets it
+        sync_device(device);
+        CachePool& pl = pool_of(device);
+        std::lock_guard<std::mutex> g(pl.mu);
+        pl.lent = false;
+    } else {
+        (void)hipFree(p);
+    }
+    p = nullptr;
+    count = 0;
+    lent = false;
+}
+
+size_t cache_pool_idle_bytes(int device)
+{
+    CachePool& pl = pool_of(device);
+    std::lock_guard<std::mutex> g(pl.mu);
+    return pl.lent ? 0 : pl.bytes;
+}
+
+size_t cache_pool_trim(int device)
+{
+    size_t freed = 0;
+    for (int d = device < 0 ? 0 : device;
+         d < (device < 0 ? kPoolDevices : device + 1); ++d) {
+        CachePool& pl = pool_of(d);
+        std::lock_guard<std::mutex> g(pl.mu);
+        if (pl.lent || !pl.p) continue;
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) cur = -1;
+        if (cur != d) (void)hipSetDevice(d);
+        (void)hipFree(pl.p);
+        if (cur >= 0 && cur != d) (void)hipSetDevice(cur);
+        freed += pl.bytes;
+        pl.p = nullptr;
+        pl.bytes = 0;
+    }
+    return freed;
+}
+
 void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
 {
     c.slots = 0;
@@ -191,6 +293,7 @@ void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
     const int64_t row = c.ldc * (int64_t)sizeof(float);
     size_t free_b = 0, total_b = 0;
     HIP_TRY(hipMemGetInfo(&free_b, &total_b));
+    free_b += cache_pool_idle_bytes(cx.device);  // kept for the cache
     // default: the whole K when it fits a quarter of the free memory (the
     // cache then keeps every row it computes); otherwise a quarter of the
     // free memory, at most 8 GiB.  An explicit budget may use the free
@@ -208,7 +311,7 @@ void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx)
     if (slots < 2) return;
     // (+16 floats: the row kernel reads whole 16-row tiles, up to 15 rows
     // past the last sample, and the last row has nothing after it)
-    c.rows.alloc((size_t)(slots * c.ldc + 16));
+    c.rows.alloc((size_t)(slots * c.ldc + 16), cx.device);
     c.slot_of.alloc((size_t)n);
     c.owner.alloc((size_t)slots);
     c.clock.alloc(1);

@@ -67,20 +67,47 @@ struct FactSV {
 };
 struct Context;
 
+// Device memory of a kernel-row cache.  The library keeps one block per
+// device between trainings and lends it to one cache at a time (grown when
+// a cache needs more): freeing and allocating tens of GB per training makes
+// a later allocation wait while the driver clears the freed memory.  A
+// cache that finds its device's block lent out allocates its own.  The
+// block is returned after a device synchronisation, as hipFree would do.
+struct CacheRows {
+    float* p = nullptr;
+    size_t count = 0;
+    int device = -1;
+    bool lent = false;
+    CacheRows() = default;
+    CacheRows(const CacheRows&) = delete;
+    CacheRows& operator=(const CacheRows&) = delete;
+    ~CacheRows() { release(); }
+    void alloc(size_t n, int dev);
+    void release();
+};
+
+// Bytes of the device's kept block while no cache holds it (0 otherwise).
+size_t cache_pool_idle_bytes(int device);
+
+// Frees the kept block of a device (every device: device < 0) unless a
+// cache holds it; returns the bytes freed.
+size_t cache_pool_trim(int device);
+
 // HBM-resident cache of kernel rows K(x_s, .) over all n samples, rows
 // padded to ldc floats.  The rows do not depend on the labels, so the
 // outputs of a one-vs-rest model share one cache.  Replacement is FIFO and
 // decided on the device (slot_of / owner maps, clock).
 struct RowCache {
     int64_t slots = 0, ldc = 0;
-    DevBuf<float> rows;
+    CacheRows rows;
     DevBuf<int32_t> slot_of, owner;
     DevBuf<int64_t> clock;
 };
 
 // Sizes and clears the cache for n samples.  bytes: 0 = default (the full
-// kernel matrix if it fits a quarter of the free device memory, at most
-// 8 GiB), > 0 = at most that many bytes (clamped likewise), < 0 = no cache.
+// kernel matrix if it fits a quarter of the free device memory, else a
+// quarter of it, at most 8 GiB; the device's idle kept block counts as
+// free), > 0 = at most that many bytes (clamped likewise), < 0 = no cache.
 // Leaves slots = 0 when fewer rows than a working set needs would fit.
 void cache_init(RowCache& c, int64_t n, int64_t bytes, Context& cx);
 

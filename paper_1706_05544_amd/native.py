@@ -41,7 +41,7 @@ EXPORTS = [
     "svm_test_solver_free", "svm_test_set_state", "svm_test_get_state",
     "svm_test_select", "svm_test_rows", "svm_test_subproblem",
     "svm_test_apply", "svm_test_iterate", "svm_test_finish",
-    "svm_predict_noalloc",
+    "svm_predict_noalloc", "svm_cache_release",
 ]
 
 
@@ -144,6 +144,7 @@ def load(path: Optional[str] = None):
     lib.svm_model_get.argtypes = [vp, ct.c_int32, vp, vp, vp]
     lib.svm_model_free.argtypes = [vp]
     lib.svm_model_free.restype = None
+    lib.svm_cache_release.argtypes = [ct.c_int32, P(ct.c_int64)]
     lib.svm_cross_validate.argtypes = [P(svm_matrix), vp, vp, ct.c_int32,
                                        P(svm_params), ct.c_int32, vp, vp,
                                        P(svm_cv_stats)]
@@ -377,6 +378,14 @@ def svm_predict_labels(model: Model, X):
         ptr = _np_ptr(L) if m else None
     _check(load().svm_predict_labels(model.ptr, ct.byref(M.s), ptr))
     return L
+
+
+def svm_cache_release(device: int = -1) -> int:
+    """Frees the row-cache memory the library keeps between trainings on
+    `device` (-1: every device); returns the bytes freed."""
+    freed = ct.c_int64(0)
+    _check(load().svm_cache_release(device, ct.byref(freed)))
+    return freed.value
 
 
 def svm_model_get_info(model: Model, output: int = 0) -> dict:

@@ -229,6 +229,21 @@ int main(void)
         svm_cross_validate(&X, y, NULL, 0, &q, 2, NULL, NULL, &st), __LINE__);
     expect_no_device(svm_test_solver_create(&X, y, &q, &s), __LINE__);
 
+    /* the kept row-cache memory: nothing kept, nothing freed (every device
+       of the process: no device call when no block is kept); an ordinal
+       out of range is refused */
+    {
+        int64_t freed = -1;
+        EXPECT(svm_cache_release(-1, &freed), SVM_OK);
+        if (freed != 0) {
+            fprintf(stderr, "line %d: freed %lld, expected 0\n", __LINE__,
+                    (long long)freed);
+            ++failures;
+        }
+        EXPECT(svm_cache_release(-1, NULL), SVM_OK);
+        expect_no_device(svm_cache_release(1000, &freed), __LINE__);
+    }
+
     if (failures) {
         fprintf(stderr, "%d checks failed\n", failures);
         return 1;

@@ -77,3 +77,26 @@ def test_cache_shared_by_ovr_classes():
         np.testing.assert_array_equal(a_on, a_off)
         served += m_on.info(c)["cache_hits"]
     assert served > 0
+
+
+def test_kept_cache_memory_is_reused_and_released():
+    # The cache's device memory is kept between trainings and lent to one
+    # cache at a time.  A training that reuses it after a training on other
+    # data gives the bits of the first (the maps are reset per training and
+    # a row is written before it is read); svm_cache_release frees it.
+    wa = workloads.make("C3", n=6000)
+    wb = workloads.make("C2", n=6000)
+    nv.svm_cache_release(-1)
+    first, a_first = _train(wa, 0)
+    other, _ = _train(wb, 0)
+    again, a_again = _train(wa, 0)
+    assert first["cache_hits"] > 0 and other["cache_hits"] > 0
+    np.testing.assert_array_equal(a_again, a_first)
+    for k in ("iters", "b", "dual_obj", "kernel_rows", "cache_hits",
+              "cache_fills"):
+        assert again[k] == first[k], k
+    # the whole K of 6000 rows (the default when it fits) is what is kept
+    freed = nv.svm_cache_release(0)
+    assert freed >= 6000 * 6000 * 4
+    assert nv.svm_cache_release(0) == 0
+    assert nv.svm_cache_release(-1) == 0
