@@ -112,7 +112,9 @@ typedef struct {
     double inner_ratio;    /* subproblem stops at local gap <= max(ratio *
                               global gap, tol/2); 0: 0.3 */
     int32_t max_inner;     /* subproblem step cap; 0: 8 q */
-    int32_t profile;       /* 1: time the row/update kernel with events */
+    int32_t profile;       /* 1: time the row/update kernel with events
+                              (a sample: the launches of one chunk of
+                              check_every iterations in four) */
     double coef0;          /* polynomial and sigmoid offset (finite; 0) */
     int32_t degree;        /* polynomial degree, in [1, 64] (3) */
     int32_t scale;         /* 1: standardise each feature (and eps-SVR

@@ -27,6 +27,8 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",
           "--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang",
           "-packed-fp32-ops", "-I" + INCLUDE]
 DEVICE_FLAGS = ["-x", "hip", "-munsafe-fp-atomics"]
+# roctx ranges of the host phases (rocprofv3 --marker-trace)
+LINK = ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"]
 
 
 def _hipcc() -> str:
@@ -61,7 +63,7 @@ def build(verbose: bool = False) -> str:
         objs = list(ex.map(lambda j: _compile(j[0], j[1], verbose), jobs))
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [_hipcc(), "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp
-           ] + objs
+           ] + objs + LINK
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -488,6 +488,7 @@ svm_status svm_predict(const svm_model* m, const svm_matrix* X,
 {
     if (X && X->n > 0 && !decision)
         return fail(SVM_E_INVALID, "decision is NULL");
+    msvm::Range rg("svm_predict");
     return predict_impl(m, X, decision, nullptr);
 }
 

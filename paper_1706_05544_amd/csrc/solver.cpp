@@ -93,6 +93,7 @@ static void load_csr(const svm_matrix* M, Features& f, Context& cx)
 
 void load_features(const svm_matrix* M, Features& f, Context& cx)
 {
+    Range rg("svm features (copy, norms, checks)");
     f.n = M->n;
     f.d = M->d;
     f.ldp = padded_ld(M->d);
@@ -633,6 +634,10 @@ void Solver::read_ws(WorkingSet& w)
     cx_.sync();
 }
 
+// Chunks of the iteration loop whose row launches are timed in profiling
+// mode: one in kProfileEvery.
+constexpr int64_t kProfileEvery = 4;
+
 // Queue chunks of `check_every` iterations, two chunks in flight, and poll
 // the done flag of the older chunk.  Iterations queued after convergence
 // return at their first instruction.
@@ -655,12 +660,19 @@ bool Solver::run_loop(SolveResult& r)
     read_ws(w0);
     int64_t last_iter = w0.iter;
 
+    // profiling: the row launches of one chunk in kProfileEvery carry the
+    // events (a launch with events costs the loop about 1.4 us more), so
+    // the timed launches are a sample spread over the whole solve
+    int64_t chunk_no = 0;
+    bool timed[2] = {false, false};
     auto enqueue = [&](int slot) {
+        timed[slot] = o_.profile && chunk_no % kProfileEvery == 0;
+        ++chunk_no;
         for (int k = 0; k < K; ++k) {
             launch_solve(SS_SOLVE | SS_CHECK_DONE);
-            // profiling: the events are part of the kernel's own dispatch,
-            // so they bracket its execution, not the queue around it
-            if (o_.profile)
+            // the events are part of the kernel's own dispatch, so they
+            // bracket its execution, not the queue around it
+            if (timed[slot])
                 launch_hot_rows(pe[(size_t)(slot * K + k) * 2],
                                 pe[(size_t)(slot * K + k) * 2 + 1]);
             else
@@ -677,7 +689,7 @@ bool Solver::run_loop(SolveResult& r)
     for (;;) {
         HIP_TRY(hipEventSynchronize(ev[cur]));
         const WorkingSet& w = hs.p[cur];
-        if (o_.profile) {
+        if (timed[cur]) {
             int64_t real = std::min<int64_t>(w.iter - last_iter, K);
             // algorithmic bytes of a launch: computed from X, the features,
             // norm, F read and written and the state byte(s) (eps-SVR: and
@@ -787,7 +799,11 @@ bool Solver::run_loop_fused(SolveResult& r)
     int64_t launched = 0;
     const bool svr = o_.type == SVM_EPS_SVR;
 
+    int64_t chunk_no = 0;  // (profiling: one chunk in kProfileEvery)
+    bool timed[2] = {false, false};
     auto enqueue = [&](int slot) {
+        timed[slot] = o_.profile && chunk_no % kProfileEvery == 0;
+        ++chunk_no;
         for (int k = 0; k < K; ++k) {
             const int par = (int)(launched & 1);
             a.F_in = par ? F2_.p : F_.p;
@@ -796,7 +812,7 @@ bool Solver::run_loop_fused(SolveResult& r)
             a.ri_in = iri_.p + par * rec;
             a.rk_out = irk_.p + (1 - par) * rec;
             a.ri_out = iri_.p + (1 - par) * rec;
-            if (o_.profile)
+            if (timed[slot])
                 launch_iter(a, nbi_, svr, cx_.stream,
                             pe[(size_t)(slot * K + k) * 2],
                             pe[(size_t)(slot * K + k) * 2 + 1]);
@@ -815,7 +831,7 @@ bool Solver::run_loop_fused(SolveResult& r)
     for (;;) {
         HIP_TRY(hipEventSynchronize(ev[cur]));
         const WorkingSet& w = hs.p[cur];
-        if (o_.profile) {
+        if (timed[cur]) {
             const int64_t real = std::min<int64_t>(w.iter - last_iter, K);
             const double per_row = 16.0 + (svr ? 6.0 : 1.0);
             for (int64_t k = 0; k < real; ++k) {
@@ -920,7 +936,12 @@ SolveResult Solver::train()
 {
     SolveResult r;
     hipEvent_t t0 = start(!fused_);
-    const bool conv = loop(r);
+    bool conv;
+    {
+        Range rg("svm solve loop");
+        conv = loop(r);
+    }
+    Range rg("svm finish (recompute, gap, bias, objective)");
     finish(r, conv, t0);
     return r;
 }
@@ -1197,12 +1218,19 @@ std::vector<SolveResult> Solver::train_lockstep(
     };
     std::vector<int64_t> last(G, 0);
     std::vector<int> ran(2, 0);  // problems in each chunk
+    // (profiling: one chunk in kProfileEvery, chunk j being iterations
+    // [jK, (j + 1)K) of every problem of the group, as in a problem's own
+    // loop)
+    int64_t chunk_no = 0;
+    bool timed[2] = {false, false};
     auto enqueue = [&](int slot) {
         const int P = (int)act.size();
         ran[slot] = P;
+        timed[slot] = prof && chunk_no % kProfileEvery == 0;
+        ++chunk_no;
         for (int k = 0; k < K; ++k) {
             launch_select_group(hsel.data(), P, svr, st);
-            if (prof)
+            if (timed[slot])
                 launch_lock(la, P, (int)nb, svr, st,
                             pe[(size_t)(slot * K + k) * 2],
                             pe[(size_t)(slot * K + k) * 2 + 1]);
@@ -1223,7 +1251,7 @@ std::vector<SolveResult> Solver::train_lockstep(
     const double own = 16.0 + (svr ? 6.0 : 1.0);
     const double shared = 4.0 * (double)f.d * (double)n + 4.0 * (double)n;
     auto account = [&](int slot, const std::vector<int64_t>& adv) {
-        if (!prof) return;
+        if (!timed[slot]) return;
         const int P = ran[slot];
         for (int k = 0; k < K; ++k) {
             int pk = 0;
@@ -1583,6 +1611,7 @@ void Solver::iterate(int64_t k, int64_t* iters, double* gap)
 void build_model(svm_model& m, Context& cx, const Features& f,
                  const double* coef_dev, int32_t n_out)
 {
+    Range rg("svm model (support vectors)");
     hipStream_t s = cx.stream;
     const int64_t n = f.n;
     DevBuf<int32_t> blk((size_t)compact_blocks(n)), idx((size_t)n);

@@ -1,12 +1,24 @@
 // Host-side solver state of the MI355X kernel-SVM library.
 #pragma once
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include <memory>
 #include <vector>
 
 #include "common.hpp"
 
 namespace msvm {
+
+// A named host range for `rocprofv3 --marker-trace` (phases of a call:
+// features, solve loop, finish, model, prediction); without a profiler the
+// push and pop do nothing measurable.
+struct Range {
+    explicit Range(const char* name) { roctxRangePush(name); }
+    ~Range() { roctxRangePop(); }
+    Range(const Range&) = delete;
+    Range& operator=(const Range&) = delete;
+};
 
 // RAII device buffer.
 template <class T>

@@ -77,6 +77,6 @@ def test_abi_validation_under_asan_ubsan(tmp_path):
     exe = str(tmp_path / "abi_asan")
     _run([os.path.join(llvm, "clang++")] + SAN[:1] +
          ["-o", exe, drv] + objs + _device_objects() +
-         ["-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib"])
+         ["-L/opt/rocm/lib", "-lamdhip64"] + b.LINK)
     r = _run([exe], env=ENV, timeout=300)
     assert "all checks passed" in r.stdout
