@@ -218,6 +218,10 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="length of each bounded oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--time-select", action="store_true",
+                    help="also time the select/solve kernel with events in "
+                         "the sampled iterations (costs the loop ~5 us per "
+                         "timed launch; reported under 'iteration')")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of 256 MiB (the "
                          "reference kernel for the HBM byte counters)")
@@ -293,7 +297,8 @@ def main() -> int:
                     "cached_kernel_ms": 0.0, "cached_kernel_launches": 0,
                     "cached_kernel_bytes": 0.0, "cache_hits": 0,
                     "cache_fills": 0, "n_sv_output": 0, "dual_obj": 0.0,
-                    "gap": 0.0}
+                    "gap": 0.0, "select_kernel_ms": 0.0,
+                    "select_kernel_launches": 0}
 
     y_host = w.y
     cv_stats = {}
@@ -342,7 +347,7 @@ def main() -> int:
     t0 = time.perf_counter()
     for i in range(args.steps):
         ts = time.perf_counter()
-        m, D, t1 = step(1)
+        m, D, t1 = step(2 if args.time_select else 1)
         torch.cuda.synchronize()
         te = time.perf_counter()
         per = infos_of(m)
@@ -351,7 +356,8 @@ def main() -> int:
                   "row_kernel_launches", "row_kernel_bytes",
                   "cached_kernel_ms", "cached_kernel_launches",
                   "cached_kernel_bytes", "cache_hits", "cache_fills",
-                  "n_sv_output"):
+                  "n_sv_output", "select_kernel_ms",
+                  "select_kernel_launches"):
             info[k] = sum(x[k] for x in per)
         info["dual_obj"] = sum(x["dual_obj"] for x in per)
         info["gap"] = max(x["gap"] for x in per)
@@ -376,6 +382,8 @@ def main() -> int:
     achieved = row_bytes / (row_ms * 1e-3) / 1e9 if row_ms > 0 else 0.0
     lock_tflops = (launches * 2.0 * w.n * w.d * 16 / (row_ms * 1e-3) / 1e12
                    if row_ms > 0 else 0.0)
+    s_launches = sum(i["select_kernel_launches"] for i in infos)
+    s_ms = sum(i["select_kernel_ms"] for i in infos)
     c_launches = sum(i["cached_kernel_launches"] for i in infos)
     c_ms = sum(i["cached_kernel_ms"] for i in infos)
     c_bytes = sum(i["cached_kernel_bytes"] for i in infos)
@@ -468,6 +476,19 @@ def main() -> int:
             "hbm_GBps": achieved,
             "problem_launches_timed": launches,
             "us_per_problem_launch": 1e3 * avg_ms,
+        },
+        # the per-iteration chain: device time per outer iteration; with
+        # --time-select the single-block select/solve kernel (latency-bound:
+        # merge of the block records, K_BB, subproblem) and the row kernel
+        # of the same timed iterations, computed or cached
+        "iteration": {
+            "us_per_iteration": 1e3 * sum(i["train_ms"] for i in infos)
+                                / max(sum(i["iters"] for i in infos), 1),
+            "k_select_avg_us": 1e3 * s_ms / s_launches if s_launches else None,
+            "k_rows_avg_us": (1e3 * (row_ms + c_ms) / (launches + c_launches)
+                              if s_launches and launches + c_launches
+                              else None),
+            "launches_timed": s_launches,
         },
         "row_cache": {
             "rows_served": last["cache_hits"],

@@ -114,7 +114,9 @@ typedef struct {
     int32_t max_inner;     /* subproblem step cap; 0: 8 q */
     int32_t profile;       /* 1: time the row/update kernel with events
                               (a sample: the launches of one chunk of
-                              check_every iterations in four) */
+                              check_every iterations in four); 2: also the
+                              select/solve kernel of those iterations (a
+                              timed launch of it costs the loop ~5 us) */
     double coef0;          /* polynomial and sigmoid offset (finite; 0) */
     int32_t degree;        /* polynomial degree, in [1, 64] (3) */
     int32_t scale;         /* 1: standardise each feature (and eps-SVR
@@ -207,6 +209,10 @@ typedef struct {
     double cached_kernel_ms;
     int64_t cached_kernel_launches;
     double cached_kernel_bytes;
+    /* profile = 2: the select/solve kernel of the same iterations (one
+       block: merge, K_BB, subproblem; latency-bound) */
+    double select_kernel_ms;
+    int64_t select_kernel_launches;
 } svm_model_info;
 
 typedef struct svm_model svm_model;  /* opaque, owned by the library */

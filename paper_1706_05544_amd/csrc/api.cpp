@@ -172,6 +172,8 @@ void fill_info(svm_model_info& in, const svm_model& m,
     in.cached_kernel_ms = r.cached_ms;
     in.cached_kernel_launches = r.cached_launches;
     in.cached_kernel_bytes = r.cached_bytes;
+    in.select_kernel_ms = r.select_ms;
+    in.select_kernel_launches = r.select_launches;
 }
 
 // Leaves HIP's per-thread last-error slot clean on every exit, so that an

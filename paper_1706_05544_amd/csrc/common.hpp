@@ -395,7 +395,8 @@ int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
 // from the runtime, at least 1; asked once per process and kept (the
 // library builds for one architecture).
 int occupancy_memo(const void* kernel, int threads, size_t lds);
-void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s);
+void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s,
+                   hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // one block per problem (P <= kLockMax entries, each with working sets of
 // 16), the arguments passed by value in the launch
 void launch_select_group(const SelArgs* args, int P, bool svr, hipStream_t s);

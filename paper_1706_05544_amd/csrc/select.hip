@@ -1263,7 +1263,8 @@ __global__ __launch_bounds__(kSelThreads) void k_select_group(SelGroup g)
 }
 
 template <bool SVR, int NBLK>
-static void select_dispatch(const SelArgs& a, hipStream_t s)
+static void select_dispatch(const SelArgs& a, hipStream_t s, hipEvent_t e0,
+                            hipEvent_t e1)
 {
     const size_t lds = a.rp ? select_csr_lds_bytes(NBLK, a.ldp, a.csr_cols)
                             : select_lds_bytes(NBLK, a.slice);
@@ -1279,7 +1280,11 @@ static void select_dispatch(const SelArgs& a, hipStream_t s)
         }
         lds_allowed = lds;
     }
-    k_select<SVR, NBLK><<<1, kSelThreads, lds, s>>>(a);
+    if (e0 || e1)  // timed: the events are part of the dispatch
+        hipExtLaunchKernelGGL(k_select<SVR, NBLK>, dim3(1), dim3(kSelThreads),
+                              lds, s, e0, e1, 0, a);
+    else
+        k_select<SVR, NBLK><<<1, kSelThreads, lds, s>>>(a);
 }
 
 void launch_select_group(const SelArgs* args, int P, bool svr, hipStream_t s)
@@ -1315,7 +1320,8 @@ void launch_select_group(const SelArgs* args, int P, bool svr, hipStream_t s)
         k_select_group<false><<<P, kSelThreads, lds, s>>>(g);
 }
 
-void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)
+void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s,
+                   hipEvent_t e0, hipEvent_t e1)
 {
     SelArgs a = a0;
     if (a.slice <= 0) a.slice = select_slice(nblk_cols, a.ldp);
@@ -1327,12 +1333,12 @@ void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s)
                         "too many features for a CSR working set in LDS"};
     }
     switch (nblk_cols * 2 + (svr ? 1 : 0)) {
-        case 2: select_dispatch<false, 1>(a, s); break;
-        case 3: select_dispatch<true, 1>(a, s); break;
-        case 4: select_dispatch<false, 2>(a, s); break;
-        case 5: select_dispatch<true, 2>(a, s); break;
-        case 8: select_dispatch<false, 4>(a, s); break;
-        case 9: select_dispatch<true, 4>(a, s); break;
+        case 2: select_dispatch<false, 1>(a, s, e0, e1); break;
+        case 3: select_dispatch<true, 1>(a, s, e0, e1); break;
+        case 4: select_dispatch<false, 2>(a, s, e0, e1); break;
+        case 5: select_dispatch<true, 2>(a, s, e0, e1); break;
+        case 8: select_dispatch<false, 4>(a, s, e0, e1); break;
+        case 9: select_dispatch<true, 4>(a, s, e0, e1); break;
         default: throw Error{SVM_E_INTERNAL, "bad column-block count"};
     }
 }

@@ -154,7 +154,7 @@ SolveOptions make_options(const svm_params* p, int64_t n, int64_t d)
                                        : 64;
     o.inner_ratio = p->inner_ratio > 0 ? p->inner_ratio : 0.3;
     o.max_inner = p->max_inner > 0 ? p->max_inner : 8 * p->working_set;
-    o.profile = p->profile != 0;
+    o.profile = p->profile < 0 ? 0 : (p->profile > 2 ? 2 : p->profile);
     o.fused = p->fused;
     o.cache_req = p->cache_bytes;
     return o;
@@ -583,7 +583,7 @@ void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
                 e1);
 }
 
-void Solver::launch_solve(int32_t mode)
+void Solver::launch_solve(int32_t mode, hipEvent_t e0, hipEvent_t e1)
 {
     SelArgs a{};
     a.cand_key = ckey_.p;
@@ -622,7 +622,7 @@ void Solver::launch_solve(int32_t mode)
         a.owner = cache_->owner.p;
         a.clock = cache_->clock.p;
     }
-    launch_select(a, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream);
+    launch_select(a, nblk_cols_, o_.type == SVM_EPS_SVR, cx_.stream, e0, e1);
 }
 
 void Solver::launch_select_only() { launch_solve(0); }
@@ -650,7 +650,9 @@ bool Solver::run_loop(SolveResult& r)
     HIP_TRY(hipEventCreateWithFlags(&ev[1], hipEventDisableTiming));
     std::vector<hipEvent_t> pe;
     if (o_.profile) {
-        pe.resize((size_t)4 * K);
+        // per iteration of the two chunks in flight: the row launch's two
+        // events, then the select launch's two
+        pe.resize((size_t)8 * K);
         // device-scope release only: the events time the kernel, not a
         // flush of the caches to host-visible memory
         for (auto& e : pe)
@@ -669,14 +671,20 @@ bool Solver::run_loop(SolveResult& r)
         timed[slot] = o_.profile && chunk_no % kProfileEvery == 0;
         ++chunk_no;
         for (int k = 0; k < K; ++k) {
-            launch_solve(SS_SOLVE | SS_CHECK_DONE);
             // the events are part of the kernel's own dispatch, so they
             // bracket its execution, not the queue around it
-            if (timed[slot])
-                launch_hot_rows(pe[(size_t)(slot * K + k) * 2],
-                                pe[(size_t)(slot * K + k) * 2 + 1]);
-            else
+            const size_t e = (size_t)(slot * K + k) * 4;
+            if (timed[slot]) {
+                if (o_.profile >= 2)
+                    launch_solve(SS_SOLVE | SS_CHECK_DONE, pe[e + 2],
+                                 pe[e + 3]);
+                else
+                    launch_solve(SS_SOLVE | SS_CHECK_DONE);
+                launch_hot_rows(pe[e], pe[e + 1]);
+            } else {
+                launch_solve(SS_SOLVE | SS_CHECK_DONE);
                 launch_hot_rows();
+            }
         }
         HIP_TRY(hipMemcpyAsync(&hs.p[slot], ws_.p, sizeof(WorkingSet),
                                hipMemcpyDeviceToHost, cx_.stream));
@@ -699,10 +707,15 @@ bool Solver::run_loop(SolveResult& r)
             const bool svr = o_.type == SVM_EPS_SVR;
             const double per_row = 16.0 + (svr ? 6.0 : 1.0);
             for (int64_t k = 0; k < real; ++k) {
+                const size_t e = (size_t)(cur * K + k) * 4;
                 float ms = 0.f;
-                HIP_TRY(hipEventElapsedTime(
-                    &ms, pe[(size_t)(cur * K + k) * 2],
-                    pe[(size_t)(cur * K + k) * 2 + 1]));
+                HIP_TRY(hipEventElapsedTime(&ms, pe[e], pe[e + 1]));
+                if (o_.profile >= 2) {
+                    float sms = 0.f;
+                    HIP_TRY(hipEventElapsedTime(&sms, pe[e + 2], pe[e + 3]));
+                    select_ms_ += sms;
+                    select_launches_ += 1;
+                }
                 const int64_t t = (last_iter + k + 1) % kPathLog;
                 if (w.path_log[t] == PATH_CACHED) {
                     cached_ms_ += ms;
@@ -1012,6 +1025,8 @@ void Solver::finish(SolveResult& r, bool conv, hipEvent_t t0, int max_passes)
     r.cached_ms = cached_ms_;
     r.cached_launches = cached_launches_;
     r.cached_bytes = cached_bytes_;
+    r.select_ms = select_ms_;
+    r.select_launches = select_launches_;
     WorkingSet w;
     read_ws(w);
     r.kernel_rows = w.rows;

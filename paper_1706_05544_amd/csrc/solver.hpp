@@ -168,7 +168,7 @@ struct SolveOptions {
     int32_t check_every;
     double inner_ratio;
     int32_t max_inner;
-    bool profile;
+    int32_t profile;  // 0 none, 1 row launches, 2 also the select launches
     int32_t fused;       // svm_params.fused
     int64_t cache_req;   // svm_params.cache_bytes
 };
@@ -196,6 +196,9 @@ struct SolveResult {
     double row_ms = 0, cached_ms = 0;
     int64_t row_launches = 0, row_rows = 0, cached_launches = 0;
     double row_bytes = 0, cached_bytes = 0;
+    // profiled select/solve launches of the same iterations
+    double select_ms = 0;
+    int64_t select_launches = 0;
 };
 
 class Solver {
@@ -261,7 +264,8 @@ private:
                 int max_passes = 3);
     void launch_keys();
     void launch_hot_rows(hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
-    void launch_solve(int32_t mode);
+    void launch_solve(int32_t mode, hipEvent_t e0 = nullptr,
+                      hipEvent_t e1 = nullptr);
     void launch_select_only();
     bool run_loop(SolveResult& r);
     // one launch per outer iteration: initial records, the loop
@@ -316,6 +320,8 @@ private:
     RowCache* cache_ = nullptr;
     double row_ms_ = 0, cached_ms_ = 0, row_bytes_ = 0, cached_bytes_ = 0;
     int64_t row_launches_ = 0, row_rows_ = 0, cached_launches_ = 0;
+    double select_ms_ = 0;
+    int64_t select_launches_ = 0;
 };
 
 }  // namespace msvm

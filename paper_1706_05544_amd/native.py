@@ -104,7 +104,9 @@ class svm_model_info(ct.Structure):
                 ("row_kernel_bytes", ct.c_double),
                 ("cached_kernel_ms", ct.c_double),
                 ("cached_kernel_launches", ct.c_int64),
-                ("cached_kernel_bytes", ct.c_double)]
+                ("cached_kernel_bytes", ct.c_double),
+                ("select_kernel_ms", ct.c_double),
+                ("select_kernel_launches", ct.c_int64)]
 
     def as_dict(self) -> dict:
         return {k: getattr(self, k) for k, _ in self._fields_}
