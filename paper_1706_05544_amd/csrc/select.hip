@@ -301,10 +301,25 @@ int select_slice(int nblk_cols, int64_t ldp)
 // Dynamic LDS of the CSR working set in the selection: the column index
 // (ldp int32) and the by-column table ((csr_cols + 1) rows of 16 * nblk_cols
 // floats).
-static size_t select_csr_lds_bytes(int nblk_cols, int64_t ldp, int csr_cols)
+__host__ __device__ inline size_t select_csr_lds_bytes(int nblk_cols,
+                                                       int64_t ldp,
+                                                       int csr_cols)
 {
     return (size_t)((ldp + 3) & ~(int64_t)3) * 4 +
            (size_t)(csr_cols + 1) * nblk_cols * 16 * 4;
+}
+
+// LDS limit of the CSR working set in the selection.
+constexpr size_t kSelCsrLds = 112 * 1024;
+
+// The slots' nonzero lists (csr_cols int32 after the table: csr_cols /
+// (16 nblk_cols) entries a slot) when they fit the limit besides it.
+__host__ __device__ inline bool select_csr_lists(int nblk_cols, int64_t ldp,
+                                                 int csr_cols)
+{
+    return select_csr_lds_bytes(nblk_cols, ldp, csr_cols) +
+               (size_t)csr_cols * 4 <=
+           kSelCsrLds;
 }
 
 static size_t select_lds_bytes(int nblk_cols, int slice)
@@ -345,6 +360,8 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     __shared__ float KSS[QS][QS + 1];
     __shared__ double shDc[kMaxQ];
     __shared__ int32_t shNB, shNS, shGo, shDone;
+    __shared__ int32_t shNoList;       // CSR: a slot's row is longer than LM
+    __shared__ int32_t shLen[kMaxQ];   // CSR: nonzeros of each slot's row
 
     __shared__ double shGap, shMx, shMn;
     extern __shared__ __align__(16) float xst[];  // QS x (slice + 4)
@@ -835,6 +852,7 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     // slices: every thread loads a piece into LDS; then the NBLK^2
     // matrix-core waves accumulate the slice while the other waves copy it
     // to xS (the rows of the next k_rows).
+    int csrE = 0;  // CSR: the columns of the working set's table
     if (a.rp) {
         // CSR: the working set by column.  cidx[c] flags, then numbers in
         // increasing column order, the columns some sample holds; tab[e *
@@ -846,6 +864,16 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         int* cidx = reinterpret_cast<int*>(xst);
         float* tab = xst + ((ldp + 3) & ~(int64_t)3);
         const int CC = a.csr_cols;
+        // Per slot, the table rows of its nonzeros in column order (LM
+        // entries a slot): K_SS[a][b] then runs over the nonzeros of sample
+        // a, the row kernel's own fma sequence for row a and slot b, instead
+        // of over every column of the table.  Used when every slot's row
+        // fits LM entries (csr_cols = 16 nblk_cols x the longest row when
+        // that is below d).
+        const int LM = CC / QS;
+        int* lst = reinterpret_cast<int*>(tab + (int64_t)(CC + 1) * QS);
+        const bool lfit = select_csr_lists(NBLK, ldp, CC) && LM > 0;
+        if (tid == 0) shNoList = lfit ? 0 : 1;
         for (int64_t c = tid; c < ldp; c += kSelThreads) cidx[c] = 0;
         for (int64_t e = tid; e < (int64_t)(CC + 1) * QS; e += kSelThreads)
             tab[e] = 0.0f;
@@ -885,10 +913,16 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         }
         __syncthreads();
 #pragma unroll
-        for (int k = 0; k < 2; ++k)
+        for (int k = 0; k < 2; ++k) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 if (hp0[k] + lane + 64 * j < hp1[k]) cidx[hc[k][j]] = 1;
+            const int slot = wave + k * NW;
+            if (lane == 0 && slot < nS) {
+                shLen[slot] = (int32_t)(hp1[k] - hp0[k]);
+                if (hp1[k] - hp0[k] > LM) shNoList = 1;
+            }
+        }
         for_rest([&](int, int32_t c, float) { cidx[c] = 1; });
         __syncthreads();
         const int E = block_exclusive_scan<kSelThreads>(cidx, ldp, ri[0]);
@@ -901,11 +935,54 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         for_rest([&](int slot, int32_t c, float v) {
             tab[(int64_t)cidx[c] * QS + slot] = v;
         });
+        const bool lists = shNoList == 0;  // uniform: set before a barrier
+        if (lists) {
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int slot = wave + k * NW;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t q = hp0[k] + lane + 64 * j;
+                    if (q < hp1[k])
+                        lst[slot * LM + (int)(q - hp0[k])] = cidx[hc[k][j]];
+                }
+                for (int64_t q = hp0[k] + 256 + lane; q < hp1[k]; q += 64)
+                    lst[slot * LM + (int)(q - hp0[k])] = cidx[a.ci[q]];
+            }
+        }
         __syncthreads();
         for (int e = tid; e < nS * nS; e += kSelThreads) {
             const int ia = e / nS, ib = e - ia * nS;
             float k = 1.0f;
-            if (ia != ib || !kernel_self_is_one(a.kf)) {
+            if ((ia != ib || !kernel_self_is_one(a.kf)) && lists) {
+                // over the nonzeros of sample ia in column order: the row
+                // kernel's fma sequence for row ia and slot ib (eight
+                // nonzeros' loads issued ahead of their fmas)
+                const int* la = lst + ia * LM;
+                const int na = shLen[ia];
+                float acc = 0.0f;
+                int j = 0;
+                for (; j + 8 <= na; j += 8) {
+                    int e8[8];
+                    float va[8], vb[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) e8[u] = la[j + u];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        va[u] = tab[e8[u] * QS + ia];
+                        vb[u] = tab[e8[u] * QS + ib];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) acc = fmaf(va[u], vb[u], acc);
+                }
+                for (; j < na; ++j) {
+                    const int r = la[j];
+                    acc = fmaf(tab[r * QS + ia], tab[r * QS + ib], acc);
+                }
+                const float qa = e == tid ? sqa : a.sq[shS[ia]];
+                const float qb = e == tid ? sqb : a.sq[shS[ib]];
+                k = kernel_from_dot(a.kf, qa, qb, acc);
+            } else if (ia != ib || !kernel_self_is_one(a.kf)) {
                 // the sum in column order (the row kernel's order), eight
                 // columns' loads issued ahead of their fmas
                 float acc = 0.0f;
@@ -928,19 +1005,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             }
             KSS[ia][ib] = k;
         }
-        if (a.xsc) {
-            // the table and its columns for the row kernel
-            for (int64_t c = tid; c < ldp; c += kSelThreads) {
-                const int e = cidx[c];
-                const bool used = (c + 1 < ldp ? cidx[c + 1] : E) > e;
-                if (used && e < CC) a.xsc_cols[e] = (int32_t)c;
-            }
-            for (int e = E + tid; e < CC; e += kSelThreads) a.xsc_cols[e] = -1;
-            const int64_t n4 = (int64_t)(CC + 1) * QS / 4;
-            for (int64_t e = tid; e < n4; e += kSelThreads)
-                *reinterpret_cast<float4*>(a.xsc + 4 * e) = ld4(tab + 4 * e);
-        }
-        if (tid < nS) shsS[tid] = a.sq[shS[tid]];
+        // (the table and its columns go to the row kernel after the last
+        // barrier, from the waves that do not solve: a barrier waits for
+        // the stores before it)
+        csrE = E;
+        // norm of slot tid: the sqb of pair (0, tid), loaded above
+        if (tid < nS) shsS[tid] = sqb;
         t_stage = wall_clock64();
     } else {
         const int g = lane >> 4, nl = lane & 15;
@@ -1110,6 +1180,23 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
                 ws->cache_filled = c_filled + nfill;
             }
         }
+        if (a.rp && a.xsc) {
+            // the CSR table and its columns for the row kernel (cidx and
+            // tab are still in LDS)
+            const int* cidx = reinterpret_cast<const int*>(xst);
+            const float* tab = xst + ((ldp + 3) & ~(int64_t)3);
+            const int CC = a.csr_cols, E = csrE;
+            constexpr int CT = kSelThreads - 64;  // copying threads
+            for (int64_t c = tid - 64; c < ldp; c += CT) {
+                const int e = cidx[c];
+                const bool used = (c + 1 < ldp ? cidx[c + 1] : E) > e;
+                if (used && e < CC) a.xsc_cols[e] = (int32_t)c;
+            }
+            for (int e = E + tid - 64; e < CC; e += CT) a.xsc_cols[e] = -1;
+            const int64_t n4 = (int64_t)(CC + 1) * QS / 4;
+            for (int64_t e = tid - 64; e < n4; e += CT)
+                *reinterpret_cast<float4*>(a.xsc + 4 * e) = ld4(tab + 4 * e);
+        }
         const int ldp16 = (int)((ldp + 15) & ~(int64_t)15);
         const int W = a.slice;
         if (!a.rp && W >= ldp16) {
@@ -1266,8 +1353,12 @@ template <bool SVR, int NBLK>
 static void select_dispatch(const SelArgs& a, hipStream_t s, hipEvent_t e0,
                             hipEvent_t e1)
 {
-    const size_t lds = a.rp ? select_csr_lds_bytes(NBLK, a.ldp, a.csr_cols)
-                            : select_lds_bytes(NBLK, a.slice);
+    const size_t lds =
+        a.rp ? select_csr_lds_bytes(NBLK, a.ldp, a.csr_cols) +
+                   (select_csr_lists(NBLK, a.ldp, a.csr_cols)
+                        ? (size_t)a.csr_cols * 4
+                        : 0)
+             : select_lds_bytes(NBLK, a.slice);
     static size_t lds_allowed = 32 * 1024;
     if (lds > lds_allowed) {
         hipError_t e = hipFuncSetAttribute(
@@ -1328,7 +1419,7 @@ void launch_select(const SelArgs& a0, int nblk_cols, bool svr, hipStream_t s,
     if (a.rp) {
         // CSR: the working set by column is whole in LDS
         a.slice = (int)((a.ldp + 15) & ~(int64_t)15);
-        if (select_csr_lds_bytes(nblk_cols, a.ldp, a.csr_cols) > 112 * 1024)
+        if (select_csr_lds_bytes(nblk_cols, a.ldp, a.csr_cols) > kSelCsrLds)
             throw Error{SVM_E_UNSUPPORTED,
                         "too many features for a CSR working set in LDS"};
     }
