@@ -395,6 +395,9 @@ int rows_blocks_per_cu(int nblk_cols, bool svr, size_t lds, bool csr);
 // from the runtime, at least 1; asked once per process and kept (the
 // library builds for one architecture).
 int occupancy_memo(const void* kernel, int threads, size_t lds);
+// Raises a kernel's dynamic LDS limit to at least lds bytes (never lowers
+// it; thread-safe); false when the device refuses.
+bool raise_dynamic_lds(const void* kernel, size_t lds);
 void launch_select(const SelArgs& a, int nblk_cols, bool svr, hipStream_t s,
                    hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 // one block per problem (P <= kLockMax entries, each with working sets of

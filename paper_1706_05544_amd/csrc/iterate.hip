@@ -955,19 +955,9 @@ static void iter_dispatch(const IterArgs& a, int nblocks, hipStream_t s,
                           hipEvent_t e0, hipEvent_t e1)
 {
     const size_t lds = iter_lds_bytes(a.ldp, a.tiles, SVR);
-    static size_t lds_allowed = 64 * 1024;
-    if (lds > lds_allowed) {
-        hipError_t e = hipFuncSetAttribute(
-            (const void*)k_iter<SVR>,
-            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            throw Error{SVM_E_UNSUPPORTED,
-                        "iteration kernel needs more LDS than the device "
-                        "allows"};
-        }
-        lds_allowed = lds;
-    }
+    if (!raise_dynamic_lds((const void*)k_iter<SVR>, lds))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "iteration kernel needs more LDS than the device allows"};
     if (e0)
         hipExtLaunchKernelGGL(k_iter<SVR>, dim3(nblocks), dim3(kIterThreads),
                               (uint32_t)lds, s, e0, e1, 0, a);

@@ -348,6 +348,22 @@ void launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s)
     k_fill_i32<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(p, v, n);
 }
 
+bool raise_dynamic_lds(const void* kernel, size_t lds)
+{
+    static std::mutex mu;
+    static std::map<const void*, size_t> lim;
+    std::lock_guard<std::mutex> g(mu);
+    size_t& cur = lim[kernel];
+    if (lds <= cur) return true;
+    if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    cur = lds;
+    return true;
+}
+
 int occupancy_memo(const void* kernel, int threads, size_t lds)
 {
     static std::mutex mu;

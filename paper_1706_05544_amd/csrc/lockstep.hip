@@ -379,19 +379,9 @@ static void lock_dispatch(const LockArgs& a, int nblocks, hipStream_t s,
                           hipEvent_t e0, hipEvent_t e1)
 {
     const size_t lds = lock_lds_bytes(P, a.ldp, a.tiles, SVR);
-    static size_t lds_allowed = 64 * 1024;
-    if (lds > lds_allowed) {
-        hipError_t e = hipFuncSetAttribute(
-            (const void*)k_lock<SVR, P>,
-            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            throw Error{SVM_E_UNSUPPORTED,
-                        "lockstep row tile needs more LDS than the device "
-                        "allows"};
-        }
-        lds_allowed = lds;
-    }
+    if (!raise_dynamic_lds((const void*)k_lock<SVR, P>, lds))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "lockstep row tile needs more LDS than the device allows"};
     if (e0) {
         hipExtLaunchKernelGGL(k_lock<SVR, P>, dim3(nblocks), dim3(kRowThreads),
                               (uint32_t)lds, s, e0, e1, 0, a);

@@ -876,18 +876,9 @@ static void rows_dispatch(const RowArgs& a, int nblocks, hipStream_t s,
 {
     const size_t lds = rows_lds_bytes(NBLK, a.ldp, a.tiles, SVR,
                                       CSR ? a.csr_cols : -1);
-    static size_t lds_allowed = 64 * 1024;
-    if (lds > lds_allowed) {
-        hipError_t e = hipFuncSetAttribute(
-            (const void*)k_rows<SVR, NBLK, MODE, CSR>,
-            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            throw Error{SVM_E_UNSUPPORTED,
-                        "row tile needs more LDS than the device allows"};
-        }
-        lds_allowed = lds;
-    }
+    if (!raise_dynamic_lds((const void*)k_rows<SVR, NBLK, MODE, CSR>, lds))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "row tile needs more LDS than the device allows"};
     if (e0) {
         hipExtLaunchKernelGGL(k_rows<SVR, NBLK, MODE, CSR>, dim3(nblocks),
                               dim3(kRowThreads), (uint32_t)lds, s, e0, e1, 0,

@@ -1359,18 +1359,9 @@ static void select_dispatch(const SelArgs& a, hipStream_t s, hipEvent_t e0,
                         ? (size_t)a.csr_cols * 4
                         : 0)
              : select_lds_bytes(NBLK, a.slice);
-    static size_t lds_allowed = 32 * 1024;
-    if (lds > lds_allowed) {
-        hipError_t e = hipFuncSetAttribute(
-            (const void*)k_select<SVR, NBLK>,
-            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            throw Error{SVM_E_UNSUPPORTED,
-                        "select tile needs more LDS than the device allows"};
-        }
-        lds_allowed = lds;
-    }
+    if (!raise_dynamic_lds((const void*)k_select<SVR, NBLK>, lds))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "select tile needs more LDS than the device allows"};
     if (e0 || e1)  // timed: the events are part of the dispatch
         hipExtLaunchKernelGGL(k_select<SVR, NBLK>, dim3(1), dim3(kSelThreads),
                               lds, s, e0, e1, 0, a);
@@ -1392,19 +1383,11 @@ void launch_select_group(const SelArgs* args, int P, bool svr, hipStream_t s)
         g.a[p].slice = slice;
     }
     const size_t lds = select_lds_bytes(1, slice);
-    static size_t lds_allowed[2] = {32 * 1024, 32 * 1024};
     const void* fn = svr ? (const void*)k_select_group<true>
                          : (const void*)k_select_group<false>;
-    if (lds > lds_allowed[svr]) {
-        hipError_t e = hipFuncSetAttribute(
-            fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            throw Error{SVM_E_UNSUPPORTED,
-                        "select tile needs more LDS than the device allows"};
-        }
-        lds_allowed[svr] = lds;
-    }
+    if (!raise_dynamic_lds(fn, lds))
+        throw Error{SVM_E_UNSUPPORTED,
+                    "select tile needs more LDS than the device allows"};
     if (svr)
         k_select_group<true><<<P, kSelThreads, lds, s>>>(g);
     else
