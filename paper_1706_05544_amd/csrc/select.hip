@@ -416,6 +416,17 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         for (int k = 0; k < 12; ++k) c_prof[k] = ws->prof[k];
     }
     if (tid == 0) shDone = 0;
+    // Wave 1's cache state (used after K_SS), read now: a scalar load
+    // issued later would be waited for by the next barrier, while here its
+    // round trip overlaps the records'.
+    const bool use_cache =
+        a.cache_slots > 0 && (a.mode & SS_SOLVE) && !given && wave == 1;
+    int64_t clk0 = 0, c_served = 0, c_filled = 0;
+    if (use_cache) clk0 = *a.clock;
+    if (wave == 1) {
+        c_served = ws->cache_served;
+        c_filled = ws->cache_filled;
+    }
     // (7) prefetch (dense input): waves 1.. stage the first feature slice
     // of the winners' rows in LDS, row c for candidate c, and their norms,
     // while wave 0 builds the working set
@@ -818,34 +829,22 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     const int32_t t = act ? shB[bpos] : INT_MAX;
     const int sl = act ? shSlot[bpos] : 0;
     const int64_t sm = act ? sample_of(SVR, t, n) : 0;
-    double al = act ? a.alpha[t] : 0.0;
-    double yv = 1.0, rv = 0.0, v = 0.0;
-    if (act) {
-        if (SVR) {
-            yv = t < n ? 1.0 : -1.0;
-            rv = t < n ? (double)a.z[sm] - a.eps : (double)a.z[sm] + a.eps;
-        } else {
-            yv = (a.st[t] & ST_YPOS) ? 1.0 : -1.0;
-            rv = yv;
-        }
-        v = rv - a.F[sm];
-    }
+    // The state of B is loaded here and used only by the subproblem: the
+    // loads are unconditional (index 0 for lanes without a variable) and
+    // their values pass an empty asm at the subproblem, so that the
+    // compiler neither branches around them nor computes from them early
+    // (either makes wave 0 wait for them before the next barrier).
+    const int64_t t_l = act ? t : 0, sm_l = act ? sm : 0;
+    double al_b = a.alpha[t_l];
+    double F_b = a.F[sm_l];
+    float z_b = SVR ? a.z[sm_l] : 0.0f;
+    uint32_t st_b = SVR ? 0u : (uint32_t)a.st[t_l];
 
     uint64_t t_stage = 0;
     // Kernel-row cache (wave 1): the slot of each working-set sample,
     // looked up while the working-set rows load.
-    const bool use_cache =
-        a.cache_slots > 0 && (a.mode & SS_SOLVE) && !given && wave == 1;
     int32_t hslot = -1;
-    int64_t clk0 = 0, c_served = 0, c_filled = 0;
-    if (use_cache) {
-        if (lane < nS) hslot = a.slot_of[shS[lane]];
-        clk0 = *a.clock;
-    }
-    if (wave == 1) {
-        c_served = ws->cache_served;
-        c_filled = ws->cache_filled;
-    }
+    if (use_cache && lane < nS) hslot = a.slot_of[shS[lane]];
 
     // (10) K_SS.  CSR input: the working set by column (below).  Dense input: on the matrix cores (same operand
     // order as k_rows): the working-set rows pass through LDS in feature
@@ -1214,6 +1213,19 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     }
 
     // (11) subproblem: maximal-violating-pair steps restricted to B
+    asm volatile("" : "+v"(al_b), "+v"(F_b), "+v"(z_b), "+v"(st_b));
+    double al = act ? al_b : 0.0;
+    double yv = 1.0, rv = 0.0, v = 0.0;
+    if (act) {
+        if (SVR) {
+            yv = t < n ? 1.0 : -1.0;
+            rv = t < n ? (double)z_b - a.eps : (double)z_b + a.eps;
+        } else {
+            yv = (st_b & ST_YPOS) ? 1.0 : -1.0;
+            rv = yv;
+        }
+        v = rv - F_b;
+    }
     const double a0 = al;
     if ((a.mode & SS_SET_ALPHA) && act) al = ws->alphaB[bpos];
     const double C = a.C;
