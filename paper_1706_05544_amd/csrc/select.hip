@@ -110,7 +110,10 @@ __device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
     constexpr int E = kSelThreads / LPE;  // entries covered
     constexpr int F = E / LPE;            // comparisons per thread
     const int tid = threadIdx.x;
-    const int e = tid / LPE, f0 = (tid % LPE) * F;
+    // thread (e, l) compares entry e with entries l, l + LPE, ...: the
+    // LPE lanes of an entry read consecutive entries (no LDS bank
+    // conflicts), and the count does not depend on the split
+    const int e = tid / LPE, f0 = tid % LPE;
 #pragma unroll
     for (int side = 0; side < 2; ++side) {
         const int M = side ? M1 : M0;
@@ -120,7 +123,7 @@ __device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
         int c = 0;
 #pragma unroll 8
         for (int j = 0; j < F; ++j) {
-            const int f = f0 + j;
+            const int f = f0 + LPE * j;
             const double kf = k[side][f];
             const int32_t iff = i[side][f];
             c += (f < M && better(kf, iff, ke, ie)) ? 1 : 0;
