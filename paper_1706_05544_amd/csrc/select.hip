@@ -461,10 +461,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         }
         if (tid < 2) nsv[tid] = 0;
         __syncthreads();
-        if (wave == 0) {
-            // lane l holds row maximum l; theta = the largest x_l with at
-            // least `half` row maxima >= x_l (-inf if there is none)
-            for (int side = 0; side < 2; ++side) {
+        if (wave < 2) {
+            // wave `side`, lane l: row maximum l of that side; theta = the
+            // largest x_l with at least `half` row maxima >= x_l (-inf if
+            // there is none)
+            {
+                const int side = wave;
                 const double x = rmax[side][lane];
                 int c = 0;
 #pragma unroll 16
