@@ -114,9 +114,13 @@ __device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
     // LPE lanes of an entry read consecutive entries (no LDS bank
     // conflicts), and the count does not depend on the split
     const int e = tid / LPE, f0 = tid % LPE;
+    // first entry of this wave: a wave whose entries are all past a side's
+    // list skips that side
+    const int e_wave = (tid & ~63) / LPE;
 #pragma unroll
     for (int side = 0; side < 2; ++side) {
         const int M = side ? M1 : M0;
+        if (e_wave >= M) continue;  // uniform over the wave
         const bool ve = e < M;
         const double ke = k[side][ve ? e : 0];
         const int32_t ie = i[side][ve ? e : 0];
@@ -148,7 +152,7 @@ __device__ __forceinline__ void pair_rank_top(const double (*k)[kSurv],
 // entries at or above it (at least `half` of them) hold the top `half`;
 // they are compacted in place and ranked.  Run by the whole block; k and i
 // are overwritten.
-__device__ void top_half(double (*k)[kSurv], int32_t (*i)[kSurv], int M0,
+__device__ __forceinline__ void top_half(double (*k)[kSurv], int32_t (*i)[kSurv], int M0,
                          int M1, int half, double* ku, int32_t* iu, double* kl,
                          int32_t* il, int32_t* shM)
 {
