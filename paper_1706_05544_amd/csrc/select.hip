@@ -1241,6 +1241,16 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     const double itol = a.inner_tol_override >= 0.0
                             ? a.inner_tol_override
                             : fmax(a.inner_ratio * shGap, 0.5 * a.tol);
+    // q <= 16: each lane holds the K_SS row of its slot in registers, and
+    // a step takes K(s, s_i), K(s, s_j) from there (uniform register
+    // index) and K_ii, K_jj, K_ij from lanes i and j: the same stored
+    // values as the LDS reads, without an LDS round trip on the step's
+    // chain
+    float krow[DUP ? QS : 1];
+    if (DUP) {
+#pragma unroll
+        for (int c = 0; c < QS; ++c) krow[c] = KSS[sl][c];
+    }
     int steps = 0;
     for (; steps < a.max_inner; ++steps) {
         const bool up = act && ((yv > 0 && al < C) || (yv < 0 && al > 0));
@@ -1273,9 +1283,22 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         const double ali = rl_f64(al, Li), alj = rl_f64(al, Lj);
         const double yi = rl_f64(yv, Li), yj = rl_f64(yv, Lj);
         const int si = rl_i32(sl, Li), sj = rl_i32(sl, Lj);
-        const double kij = (double)KSS[si][sj];
-        const double kai = (double)KSS[sl][si], kaj = (double)KSS[sl][sj];
-        double a2 = (double)KSS[si][si] + (double)KSS[sj][sj] - 2.0 * kij;
+        double kij, kai, kaj, kii, kjj;
+        if (DUP) {
+            const float fi = krow[si], fj = krow[sj];  // K(s, s_i), K(s, s_j)
+            kai = (double)fi;
+            kaj = (double)fj;
+            kij = (double)__int_as_float(rl_i32(__float_as_int(fj), Li));
+            kii = (double)__int_as_float(rl_i32(__float_as_int(fi), Li));
+            kjj = (double)__int_as_float(rl_i32(__float_as_int(fj), Lj));
+        } else {
+            kij = (double)KSS[si][sj];
+            kai = (double)KSS[sl][si];
+            kaj = (double)KSS[sl][sj];
+            kii = (double)KSS[si][si];
+            kjj = (double)KSS[sj][sj];
+        }
+        double a2 = kii + kjj - 2.0 * kij;
         if (a2 <= 0.0) a2 = kTau;
         double s = (vi - vj) / a2;
         const double Ui = yi > 0 ? C - ali : ali;
