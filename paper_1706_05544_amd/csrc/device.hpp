@@ -126,10 +126,12 @@ __device__ __forceinline__ void wave_best(double& k, int32_t& i)
 constexpr int kDppRor1 = 0x121, kDppRor2 = 0x122, kDppRor4 = 0x124,
               kDppRor8 = 0x128;
 
+// (a row rotate has a source lane for every lane, so no lane keeps the old
+// value, and the result needs no copy of the source first)
 template <int CTRL>
 __device__ __forceinline__ int dpp_i32(int v)
 {
-    return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xF, 0xF, false);
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, false);
 }
 
 template <int CTRL>
