@@ -122,7 +122,7 @@ struct RowArgs {
     // CSR rows sliced by kSellRows (so == nullptr: walk rp/ci/cv instead):
     // nonzero k of row i at so[i / kSellRows] + kSellRows * k + i % kSellRows
     const int64_t* so;
-    const int32_t* sci;
+    const uint16_t* sci;  // column indices (below 65536) of the sliced copy
     const float* scv;
     const float* sq;
     double* F;
@@ -471,7 +471,7 @@ void launch_csr_check_norms(const int64_t* rp, const int32_t* ci,
 void launch_sell_offsets(const int64_t* rp, int64_t n, int64_t* so,
                          hipStream_t s);
 void launch_sell_fill(const int64_t* rp, const int32_t* ci, const float* cv,
-                      int64_t n, const int64_t* so, int32_t* sci, float* scv,
+                      int64_t n, const int64_t* so, uint16_t* sci, float* scv,
                       hipStream_t s);
 // dense copies of CSR rows (idx == nullptr: rows r0 .. r0 + k - 1)
 void launch_gather_rows_csr(const int64_t* rp, const int32_t* ci,

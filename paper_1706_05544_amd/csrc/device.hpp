@@ -380,6 +380,11 @@ __device__ __forceinline__ uint8_t bld_u8(Rsrc r, uint32_t off)
     return __builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
 }
 
+__device__ __forceinline__ uint16_t bld_u16(Rsrc r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+}
+
 __device__ __forceinline__ void bst_f64(Rsrc r, uint32_t off, double v)
 {
     typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));

@@ -767,7 +767,7 @@ __global__ __launch_bounds__(1024) void k_sell_scan(int64_t* so, int64_t ns)
 // One thread per row: its nonzeros, then the padding of its slice.
 __global__ void k_sell_fill(const int64_t* rp, const int32_t* ci,
                             const float* cv, int64_t n, const int64_t* so,
-                            int32_t* sci, float* scv)
+                            uint16_t* sci, float* scv)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
@@ -776,7 +776,7 @@ __global__ void k_sell_fill(const int64_t* rp, const int32_t* ci,
     const int64_t p0 = rp[i], nz = rp[i + 1] - p0;
     for (int64_t k = 0; k < w; ++k) {
         const int64_t dst = so[s] + kSellRows * k + t;
-        sci[dst] = k < nz ? ci[p0 + k] : 0;
+        sci[dst] = k < nz ? (uint16_t)ci[p0 + k] : (uint16_t)0;
         scv[dst] = k < nz ? cv[p0 + k] : 0.0f;
     }
 }
@@ -791,7 +791,7 @@ void launch_sell_offsets(const int64_t* rp, int64_t n, int64_t* so,
 }
 
 void launch_sell_fill(const int64_t* rp, const int32_t* ci, const float* cv,
-                      int64_t n, const int64_t* so, int32_t* sci, float* scv,
+                      int64_t n, const int64_t* so, uint16_t* sci, float* scv,
                       hipStream_t s)
 {
     if (n > 0)

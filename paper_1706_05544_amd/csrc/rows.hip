@@ -438,9 +438,12 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 // The wave's nonzeros through buffer resources based at its
                 // first row: the sliced copy (a.so; nonzero k of a row
                 // kSellRows entries after nonzero k - 1, the row padded with
-                // zeros to its slice's width) or the CSR rows.  Offsets are
-                // below 2^31 (16 * tiles * ldp * 4 is, checked at launch).
-                // A load past the wave's nonzeros reads zero.
+                // zeros to its slice's width; 16-bit columns) or the CSR
+                // rows.  Offsets are below 2^31 (16 * tiles * ldp * 4 is,
+                // checked at launch), so a 16-bit column's offset (half the
+                // value's) is below 2^30, and so is its range: half of kOob
+                // still lies past it.  A load past the wave's nonzeros reads
+                // zero.
                 const bool sell = a.so != nullptr;  // uniform
                 int64_t e_beg, e_end;
                 if (sell) {
@@ -456,8 +459,9 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                 // resources live in scalar registers)
                 e_beg = uniform_i64(e_beg);
                 e_end = uniform_i64(e_end);
-                const Rsrc rCI = make_rsrc((sell ? a.sci : a.ci) + e_beg,
-                                           4 * (e_end - e_beg));
+                const Rsrc rCI =
+                    sell ? make_rsrc(a.sci + e_beg, 2 * (e_end - e_beg))
+                         : make_rsrc(a.ci + e_beg, 4 * (e_end - e_beg));
                 const Rsrc rCV = make_rsrc((sell ? a.scv : a.cv) + e_beg,
                                            4 * (e_end - e_beg));
                 // byte offset of nonzero 0 and the nonzeros (sliced: the
@@ -493,7 +497,10 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
                                      float (&vv)[KB]) {
 #pragma unroll
                         for (int j = 0; j < KB; ++j) {
-                            cc[j] = bld_i32(rCI, vo + STR * j);
+                            // (sliced copy: 16-bit columns, half the offset)
+                            cc[j] = STR == 4 ? bld_i32(rCI, vo + STR * j)
+                                             : (int32_t)bld_u16(
+                                                   rCI, (vo >> 1) + (STR >> 1) * j);
                             vv[j] = bld_f32(rCV, vo + STR * j);
                         }
                     };

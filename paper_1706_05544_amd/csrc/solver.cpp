@@ -81,7 +81,8 @@ static void load_csr(const svm_matrix* M, Features& f, Context& cx)
         throw Error{SVM_E_INVALID,
                     "X holds a value that is not finite (or whose square "
                     "overflows fp32)"};
-    if (sell_total > 0 && sell_total <= 4 * f.nnz + 64 * kSellRows) {
+    if (sell_total > 0 && sell_total <= 4 * f.nnz + 64 * kSellRows &&
+        f.d <= 65536) {
         f.sci.alloc((size_t)sell_total);
         f.scv.alloc((size_t)sell_total);
         launch_sell_fill(f.rp.p, f.ci.p, f.cv.p, f.n, f.so.p, f.sci.p,
@@ -723,11 +724,16 @@ bool Solver::run_loop(SolveResult& r)
                     cached_bytes_ +=
                         (double)n_ * (per_row + 4.0 * (double)w.ns_log[t]);
                 } else {
-                    // the features: dense 4d per row, CSR 8 per nonzero and
-                    // the row pointers
+                    // the features: dense 4d per row; CSR 8 per nonzero
+                    // and the row pointers, or in the sliced copy 6 per
+                    // nonzero (16-bit column) and the slice offsets
+                    const bool sl = f_.csr && f_.so.p != nullptr;
                     const double feat =
-                        f_.csr ? 8.0 * (double)f_.nnz + 8.0 * (double)(n_ + 1)
-                               : 4.0 * (double)f_.d * (double)n_;
+                        !f_.csr ? 4.0 * (double)f_.d * (double)n_
+                        : sl    ? 6.0 * (double)f_.nnz +
+                                   8.0 * (double)((n_ + kSellRows - 1) /
+                                                      kSellRows + 1)
+                                : 8.0 * (double)f_.nnz + 8.0 * (double)(n_ + 1);
                     row_ms_ += ms;
                     row_launches_ += 1;
                     row_rows_ += n_;

@@ -147,9 +147,10 @@ struct Features {
     DevBuf<int32_t> ci;
     DevBuf<float> cv;
     // the rows again, sliced by kSellRows for the row kernel (empty when the
-    // row lengths are so uneven that the padding would pass 4 x nnz)
+    // row lengths are so uneven that the padding would pass 4 x nnz, or when
+    // d > 65536)
     DevBuf<int64_t> so;
-    DevBuf<int32_t> sci;
+    DevBuf<uint16_t> sci;  // 16-bit column indices (d <= 65536)
     DevBuf<float> scv;
 };
 
