@@ -334,6 +334,32 @@ static size_t select_lds_bytes(int nblk_cols, int slice)
     return (size_t)nblk_cols * 16 * (slice + 4) * sizeof(float);
 }
 
+// Exclusive scan in place of the 0/1 flags v[0..L), L <= kSelThreads, by
+// the whole block (one flag a thread: a ballot and a count of the lanes
+// below, no shuffle chain); returns the number of flags set.  Longer lists
+// take the general block scan.
+__device__ __forceinline__ int flag_exclusive_scan(int* v, int64_t L,
+                                                   int* wsum)
+{
+    if (L > kSelThreads) return block_exclusive_scan<kSelThreads>(v, L, wsum);
+    constexpr int NW = kSelThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool in = tid < L;
+    const unsigned long long m = __ballot(in && v[in ? tid : 0] != 0);
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        const int x = wsum[w];
+        off += w < wave ? x : 0;
+        tot += x;
+    }
+    if (in) v[tid] = off + lanes_below(m);
+    __syncthreads();
+    return tot;
+}
+
 template <bool SVR, int NBLK>
 __device__ __forceinline__ void select_body(const SelArgs& a)
 {
@@ -360,6 +386,7 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     __shared__ int32_t ri[2][NW];
     __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
     __shared__ int32_t shCandPos[kMaxQ], shSlotCand[kMaxQ];
+    __shared__ int64_t shRpC[kMaxQ][2];  // CSR: row pointers of candidate c
     __shared__ float shSqCand[kMaxQ];  // squared norm of each candidate
     __shared__ int shCnt;
     __shared__ int32_t shPos[kMaxQ];  // position in B of the i-th smallest
@@ -663,6 +690,21 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     }
     const uint64_t t_merge = wall_clock64();
 
+    // CSR input: wave 1 reads the row pointers of the winners (candidate
+    // c: up winner c for c < half, else low winner c - half) while wave 0
+    // builds the working set, so that the staging of the working-set rows
+    // starts from them
+    const bool pfr = !given && a.rp && (a.mode & SS_SOLVE);  // uniform
+    if (pfr && wave == 1 && lane < 2 * half) {
+        const int c = lane;
+        const double key = c < half ? upk[c] : lok[c - half];
+        const int32_t idx = c < half ? upi[c] : loi[c - half];
+        const int64_t smp =
+            key != -INFINITY ? sample_of(SVR, idx, n) : 0;
+        const int64_t r0 = a.rp[smp], r1 = a.rp[smp + 1];
+        shRpC[c][0] = r0;
+        shRpC[c][1] = r1;
+    }
     // candidate c: up winner c (c < half) or low winner c - half
     pf = !given && !a.rp && (a.mode & SS_SOLVE) && 2 * half * pq4 <= 4 * PT;
     if (pf && wave != 0) {
@@ -895,9 +937,16 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             const int slot = wave + k * NW;
-            const int64_t smp = slot < nS ? shS[slot] : 0;
-            hp0[k] = a.rp[smp];
-            hp1[k] = slot < nS ? a.rp[smp + 1] : hp0[k];
+            if (pfr) {
+                // those of a candidate of the slot, read during the build
+                const int c = slot < nS ? shSlotCand[slot] : 0;
+                hp0[k] = slot < nS ? shRpC[c][0] : 0;
+                hp1[k] = slot < nS ? shRpC[c][1] : hp0[k];
+            } else {
+                const int64_t smp = slot < nS ? shS[slot] : 0;
+                hp0[k] = a.rp[smp];
+                hp1[k] = slot < nS ? a.rp[smp + 1] : hp0[k];
+            }
         }
 #pragma unroll
         for (int k = 0; k < 2; ++k)
@@ -933,7 +982,7 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         }
         for_rest([&](int, int32_t c, float) { cidx[c] = 1; });
         __syncthreads();
-        const int E = block_exclusive_scan<kSelThreads>(cidx, ldp, ri[0]);
+        const int E = flag_exclusive_scan(cidx, ldp, ri[0]);
 #pragma unroll
         for (int k = 0; k < 2; ++k)
 #pragma unroll
