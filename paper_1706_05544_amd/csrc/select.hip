@@ -564,6 +564,7 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         // b) holds the units [b TU / nb, (b + 1) TU / nb) of the TU units
         // of 32 rows; it has at most grows rows.
         const uint32_t grows = (uint32_t)a.group_rows;
+        int32_t wgrp = -1;  // wave 0: the group of this lane's winner
         const int64_t TU = (n + 31) >> 5, NB = a.nb;
         // group of a row: floor(((row / 32 + 1) NB - 1) / TU), through an
         // fp64 quotient corrected to the exact integer
@@ -585,6 +586,7 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             const bool valid = k < half && kk[k] != -INFINITY;
             const int32_t b =
                 valid ? group_of(sample_of(SVR, ii[k], n)) : -1 - lane;
+            wgrp = b;
             int c = 0;
             bool first = true;
             for (int j = 0; j < half; ++j) {
@@ -608,24 +610,26 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             // ranked like the survivors when they fit, else by rounds.
             const uint32_t NV = SVR ? 2 : 1;
             const uint32_t per = grows * NV;
-            if (tid < 2) {
-                const int side = tid;
+            if (wave == 0) {
+                // the winners outside the exhausted groups, in order (lane
+                // layout and groups as in (5))
+                const int side = lane >> 5, k = lane & 31;
                 const int ne = nex[side];
                 const double* kk = side ? lok : upk;
                 const int32_t* ii = side ? loi : upi;
-                int c = 0;
-                for (int k = 0; k < half; ++k) {
-                    if (kk[k] == -INFINITY) continue;
-                    const int32_t b = group_of(sample_of(SVR, ii[k], n));
-                    bool ex = false;
-                    for (int x = 0; x < ne; ++x) ex |= exb[side][x] == b;
-                    if (!ex) {
-                        svk[side][c] = kk[k];
-                        svi[side][c] = ii[k];
-                        ++c;
-                    }
+                const bool valid = k < half && kk[k] != -INFINITY;
+                bool ex = false;
+                for (int x = 0; x < ne; ++x) ex |= exb[side][x] == wgrp;
+                const bool keep = valid && !ex;
+                const unsigned long long m = __ballot(keep);
+                const unsigned long long ms =
+                    side ? (m >> 32) : (m & 0xffffffffull);
+                if (keep) {
+                    const int pos = __popcll(ms & ((1ull << k) - 1ull));
+                    svk[side][pos] = kk[k];
+                    svi[side][pos] = ii[k];
                 }
-                nsv[side] = c;
+                if (k == 0) nsv[side] = __popcll(ms);
             }
             __syncthreads();
             const int nk0 = nsv[0], nk1 = nsv[1];

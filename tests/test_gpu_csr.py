@@ -116,6 +116,20 @@ def test_train_c5_recipe_against_oracle(n):
     _check(w, m, ref, p)
 
 
+def test_train_wide_ragged_csr_against_oracle():
+    # d = 2000: more columns than the selection block has threads (its
+    # column numbering takes the general scan), rows of 0 to 40 nonzeros
+    from types import SimpleNamespace
+    X, y = _ragged(1600, 2000, 7)
+    w = SimpleNamespace(X=X[:1300], y=y[:1300], Xt=X[1300:], yt=y[1300:],
+                        d=2000, type=C_SVC, C=1.0, eps=0.0, gamma=0.05,
+                        tol=1e-3)
+    p = Params(C_SVC, C=w.C, gamma=w.gamma, tol=w.tol)
+    ref = oracle.train(w.X, w.y, p)
+    m = nv.svm_train(w.X, w.y, type=C_SVC, C=w.C, gamma=w.gamma, tol=w.tol)
+    _check(w, m, ref, p)
+
+
 def test_train_svr_csr_against_oracle():
     w = workloads.make("C2", n=2000, n_test=300)
     w.X[np.abs(w.X) < 0.5] = 0.0  # about half the entries zero
