@@ -334,6 +334,26 @@ static size_t select_lds_bytes(int nblk_cols, int slice)
     return (size_t)nblk_cols * 16 * (slice + 4) * sizeof(float);
 }
 
+// Value of the lane R places along this lane's 16-lane row (a row rotate:
+// every lane has a source, so none keeps its old value); R = 1 .. 15 meet
+// every other lane of the row once.  Needs the whole row active.
+template <int R>
+__device__ __forceinline__ int row_rot(int v)
+{
+    return __builtin_amdgcn_mov_dpp(v, 0x120 + R, 0xF, 0xF, false);
+}
+
+template <int R = 1, class Fn>
+__device__ __forceinline__ void for_row_rotations(Fn&& fn)
+{
+    if constexpr (R < 16) {
+        fn(std::integral_constant<int, R>{});
+        // one rotation at a time (hoisting them all would hold 15 values)
+        __builtin_amdgcn_sched_barrier(0);
+        for_row_rotations<R + 1>(fn);
+    }
+}
+
 // Exclusive scan in place of the 0/1 flags v[0..L), L <= kSelThreads, by
 // the whole block (one flag a thread: a ballot and a count of the lanes
 // below, no shuffle chain); returns the number of flags set.  Longer lists
@@ -814,6 +834,7 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             const int32_t t = act ? shB[lane] : INT_MAX;
             const int32_t s = act ? (int32_t)sample_of(SVR, t, n) : -1;
             int firstpos = lane;
+            const bool row16 = nB <= 16;  // B in the first 16-lane row
             if (SVR)
                 for (int j = 0; j < nB; ++j) {
                     const int32_t sj = rl_i32(s, j);
@@ -827,7 +848,16 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             // its variables in increasing index order: lowest lane = lowest
             // index on ties)
             int p = 0;
-            for (int j = 0; j < nB; ++j) p += rl_i32(t, j) < t ? 1 : 0;
+            if (row16) {
+                for_row_rotations([&](auto r) {
+                    constexpr int R = decltype(r)::value;
+                    const int m = row_rot<R>(lane & 15);
+                    const int32_t tm = row_rot<R>(t);
+                    p += (m < nB && tm < t) ? 1 : 0;
+                });
+            } else {
+                for (int j = 0; j < nB; ++j) p += rl_i32(t, j) < t ? 1 : 0;
+            }
             if (act) {
                 shSlot[lane] = slot;
                 if (firstpos == lane) shS[slot] = s;
