@@ -801,10 +801,27 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
                 // drop a variable already placed earlier in the order: up
                 // entry k follows low entries 0..k-1, low entry k follows up
                 // entries 0..k (entries compared through registers)
-                for (int j = 0; j < half; ++j) {
-                    const int32_t uj = rl_i32(idx, j), lj = rl_i32(idx, half + j);
-                    if (isU && j < k && lj == idx) keep = false;
-                    if (inL && j <= k && uj == idx) keep = false;
+                if (2 * half <= 16) {
+                    // both lists in the first 16-lane row: each lane meets
+                    // every other entry by the 15 row rotations (no chain
+                    // of readlanes)
+                    int dup = 0;
+                    const int lo = isU ? half : 0;  // partners it checks:
+                    const int hi = isU ? half + k : k + 1;  // lanes [lo, hi)
+                    for_row_rotations([&](auto r) {
+                        constexpr int R = decltype(r)::value;
+                        const int m = row_rot<R>(lane & 15);
+                        const int32_t im = row_rot<R>(idx);
+                        dup |= (m >= lo && m < hi && im == idx) ? 1 : 0;
+                    });
+                    if (dup) keep = false;
+                } else {
+                    for (int j = 0; j < half; ++j) {
+                        const int32_t uj = rl_i32(idx, j),
+                                      lj = rl_i32(idx, half + j);
+                        if (isU && j < k && lj == idx) keep = false;
+                        if (inL && j <= k && uj == idx) keep = false;
+                    }
                 }
                 const unsigned long long m = __ballot(keep);
                 const unsigned long long mu = m & ((1ull << half) - 1ull);
@@ -835,11 +852,22 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             const int32_t s = act ? (int32_t)sample_of(SVR, t, n) : -1;
             int firstpos = lane;
             const bool row16 = nB <= 16;  // B in the first 16-lane row
-            if (SVR)
+            if (SVR && row16) {
+                // the lanes of B holding the same sample, by row rotations
+                uint32_t same = 0;
+                for_row_rotations([&](auto r) {
+                    constexpr int R = decltype(r)::value;
+                    const int m = row_rot<R>(lane & 15);
+                    const int32_t sm = row_rot<R>(s);
+                    same |= (m < nB && sm == s) ? (1u << m) : 0u;
+                });
+                if (act) firstpos = __builtin_ctz(same | (1u << lane));
+            } else if (SVR) {
                 for (int j = 0; j < nB; ++j) {
                     const int32_t sj = rl_i32(s, j);
                     if (act && j < firstpos && sj == s) firstpos = j;
                 }
+            }
             const unsigned long long fm = __ballot(act && firstpos == lane);
             const unsigned long long bl =
                 firstpos >= 64 ? ~0ull : ((1ull << firstpos) - 1ull);
