@@ -609,11 +609,25 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             wgrp = b;
             int c = 0;
             bool first = true;
-            for (int j = 0; j < half; ++j) {
-                const int32_t bu = rl_i32(b, j), bl = rl_i32(b, 32 + j);
-                const int32_t bj = side ? bl : bu;
-                c += bj == b;
-                first &= !(j < k && bj == b);
+            if (half <= 16) {
+                // a side's winners sit in one 16-lane row (rows 0 and 2):
+                // the row rotations meet every other winner of the side
+                uint32_t same = k < half ? (1u << k) : 0u;
+                for_row_rotations([&](auto r) {
+                    constexpr int R = decltype(r)::value;
+                    const int m = row_rot<R>(lane & 15);
+                    const int32_t bm = row_rot<R>(b);
+                    same |= (m < half && bm == b) ? (1u << m) : 0u;
+                });
+                c = __popc(same);
+                first = (same & ((1u << k) - 1u)) == 0u;
+            } else {
+                for (int j = 0; j < half; ++j) {
+                    const int32_t bu = rl_i32(b, j), bl = rl_i32(b, 32 + j);
+                    const int32_t bj = side ? bl : bu;
+                    c += bj == b;
+                    first &= !(j < k && bj == b);
+                }
             }
             const bool ex = valid && c >= kBlockTop && first;
             const unsigned long long m = __ballot(ex);
