@@ -1461,9 +1461,21 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         // the change of the coefficient of each slot: the one variable of
         // the slot, or (eps-SVR) the sum of both copies of its sample
         int partner = -1;
-        if (SVR)
+        if (SVR && DUP) {
+            // variable p sits in lane p of its row: the row rotations meet
+            // every other variable (a sample has at most one twin)
+            uint32_t pm = 0;
+            for_row_rotations([&](auto r) {
+                constexpr int R = decltype(r)::value;
+                const int m = row_rot<R>(lane & 15);
+                const int slm = row_rot<R>(sl);
+                pm |= (m < nB && slm == sl) ? (1u << m) : 0u;
+            });
+            partner = pm ? __builtin_ctz(pm) : -1;
+        } else if (SVR) {
             for (int j = 0; j < nB; ++j)
                 if (j != p && rl_i32(sl, j) == sl) partner = j;
+        }
         __builtin_amdgcn_wave_barrier();
         if (own && (partner < 0 || p < partner))
             ws->coef[sl] = dc + (partner >= 0 ? shDc[partner] : 0.0);
