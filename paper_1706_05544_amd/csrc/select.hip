@@ -1405,8 +1405,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         if (bu == -INFINITY || bl == -INFINITY) break;
         const double vi = bu, vj = -bl;
         if (!(vi - vj > itol)) break;
-        const double ali = rl_f64(al, Li), alj = rl_f64(al, Lj);
-        const double yi = rl_f64(yv, Li), yj = rl_f64(yv, Lj);
+        // the room of each lane's variable as the up one (ucap) and as the
+        // low one (lcap), taken from lanes i and j; lanes i and j update
+        // their own alpha with their own label
+        const double ucap = yv > 0 ? C - al : al;
+        const double lcap = yv > 0 ? al : C - al;
+        const double Ui = rl_f64(ucap, Li), Lb = rl_f64(lcap, Lj);
         const int si = rl_i32(sl, Li), sj = rl_i32(sl, Lj);
         double kij, kai, kaj, kii, kjj;
         if (DUP) {
@@ -1426,8 +1430,6 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
         double a2 = kii + kjj - 2.0 * kij;
         if (a2 <= 0.0) a2 = kTau;
         double s = (vi - vj) / a2;
-        const double Ui = yi > 0 ? C - ali : ali;
-        const double Lb = yj > 0 ? alj : C - alj;
         bool ci = false, cj = false;
         if (Ui <= s) {
             s = Ui;
@@ -1439,12 +1441,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
             ci = (Ui == s);
         }
         if (act && p == Li) {
-            al += yi * s;
-            if (ci) al = yi > 0 ? C : 0.0;
+            al += yv * s;
+            if (ci) al = yv > 0 ? C : 0.0;
         }
         if (act && p == Lj) {
-            al -= yj * s;
-            if (cj) al = yj > 0 ? 0.0 : C;
+            al -= yv * s;
+            if (cj) al = yv > 0 ? 0.0 : C;
         }
         if (act) v -= s * (kai - kaj);
     }
