@@ -401,14 +401,12 @@ __device__ __forceinline__ void select_body(const SelArgs& a)
     __shared__ int32_t nex[2];
     __shared__ double keepk[kMaxHalf];
     __shared__ int32_t keepi[kMaxHalf];
-    __shared__ int32_t nkeep;
     __shared__ double rk[2][NW];
     __shared__ int32_t ri[2][NW];
     __shared__ int32_t shB[kMaxQ], shSlot[kMaxQ], shS[kMaxQ];
     __shared__ int32_t shCandPos[kMaxQ], shSlotCand[kMaxQ];
     __shared__ int64_t shRpC[kMaxQ][2];  // CSR: row pointers of candidate c
     __shared__ float shSqCand[kMaxQ];  // squared norm of each candidate
-    __shared__ int shCnt;
     __shared__ int32_t shPos[kMaxQ];  // position in B of the i-th smallest
     __shared__ float shsS[kMaxQ];
     __shared__ float KSS[QS][QS + 1];
