@@ -245,6 +245,15 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
         // always computed from X) and the cache slot of this lane's
         // working-set slots.
         const int32_t path = HOT ? ws->path : PATH_STREAM;
+        // (dense, hot mode) the cache slot of this lane's working-set slots,
+        // requested with the path and waited for with it: issued inside the
+        // cached branch, it would be a second round trip after the path's
+        int32_t cs_in[NBLK];
+#pragma unroll
+        for (int b = 0; b < NBLK; ++b) {
+            cs_in[b] = (HOT && !CSR) ? ws->cslot[b * 16 + nl] : -1;
+            if (HOT && !CSR) asm volatile("" ::"v"(cs_in[b]));
+        }
 
         // F_i += sum_s cf_s K(x_i, x_s) for the 16 rows of tile ti, given
         // this lane's K values kv[b][v] (row lr + v of slot b * 16 + nl),
@@ -603,10 +612,7 @@ __global__ __launch_bounds__(kRowThreads) void k_rows(RowArgs a)
             // ahead.  Unused slots read a valid address and are zeroed.
             int32_t cs[NBLK];
 #pragma unroll
-            for (int b = 0; b < NBLK; ++b) {
-                const int32_t c = ws->cslot[b * 16 + nl];
-                cs[b] = b * 16 + nl < nS ? c : -1;
-            }
+            for (int b = 0; b < NBLK; ++b) cs[b] = b * 16 + nl < nS ? cs_in[b] : -1;
             const float* crow[NBLK];
 #pragma unroll
             for (int b = 0; b < NBLK; ++b)
