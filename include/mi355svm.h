@@ -27,7 +27,9 @@
  *     arguments are reported even on a machine without a GPU.
  *   - Host inputs are read during the call and copied once to the device;
  *     they are never retained.  Device inputs (on_device = 1) are borrowed
- *     for the duration of the call and used on params->stream.
+ *     for the duration of the call and used on params->stream (dense ones
+ *     with ld = d, d a multiple of 4 and 16-byte aligned values are read
+ *     in place, not copied; they are never written).
  *   - Calls are synchronous: they return after the device work they queued
  *     has finished.  Models and solvers are not shared between threads
  *     without external locking.

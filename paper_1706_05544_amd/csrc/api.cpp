@@ -298,7 +298,7 @@ svm_status svm_train(const svm_matrix* X, const float* y, const svm_params* p,
     GUARD_BEGIN
     msvm::Context cx(p->device, p->stream);
     msvm::Features f;
-    msvm::load_features(X, f, cx);
+    msvm::load_features(X, f, cx, true);
     msvm::DevBuf<float> yd((size_t)X->n);
     HIP_TRY(hipMemcpyAsync(yd.p, y, (size_t)X->n * sizeof(float),
                            X->on_device ? hipMemcpyDeviceToDevice
@@ -369,7 +369,7 @@ svm_status svm_train_ovr(const svm_matrix* X, const int32_t* labels,
     GUARD_BEGIN
     msvm::Context cx(p->device, p->stream);
     msvm::Features f;
-    msvm::load_features(X, f, cx);
+    msvm::load_features(X, f, cx, true);
     const int64_t n = X->n;
     msvm::DevBuf<int32_t> ld((size_t)n);
     HIP_TRY(hipMemcpyAsync(ld.p, labels, (size_t)n * sizeof(int32_t),
@@ -462,7 +462,7 @@ static svm_status predict_impl(const svm_model* mdl, const svm_matrix* X,
     GUARD_BEGIN
     msvm::Context cx(mdl->device, nullptr);
     msvm::Features t;
-    msvm::load_features(X, t, cx);
+    msvm::load_features(X, t, cx, true);
     const int64_t m = X->n;
     msvm::DevBuf<double> D((size_t)(m * mdl->n_out));
     msvm::predict_device(*mdl, cx, t, D.p);
@@ -594,7 +594,7 @@ void cv_load(CvData& c, const svm_matrix* X, const float* y,
              int32_t k, const int32_t* fold, msvm::Context& cx)
 {
     const int64_t n = X->n;
-    msvm::load_features(X, c.f, cx);
+    msvm::load_features(X, c.f, cx, true);
     if (p->scale) {
         msvm::DevBuf<double> mu, sd;
         msvm::scale_fit(c.f, cx, mu, sd);

@@ -92,7 +92,7 @@ static void load_csr(const svm_matrix* M, Features& f, Context& cx)
     }
 }
 
-void load_features(const svm_matrix* M, Features& f, Context& cx)
+void load_features(const svm_matrix* M, Features& f, Context& cx, bool borrow)
 {
     Range rg("svm features (copy, norms, checks)");
     f.n = M->n;
@@ -102,11 +102,18 @@ void load_features(const svm_matrix* M, Features& f, Context& cx)
         load_csr(M, f, cx);
         return;
     }
-    f.X.alloc((size_t)(f.n * f.ldp));
     f.sq.alloc((size_t)f.n);
     const hipMemcpyKind kind =
         M->on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
-    if (f.n > 0) {
+    f.Xb = nullptr;
+    if (borrow && M->on_device && f.n > 0 && f.ldp == f.d && M->ld == f.d &&
+        ((uintptr_t)M->values & 15) == 0) {
+        f.Xb = static_cast<const float*>(M->values);
+        f.X.release();
+    } else {
+        f.X.alloc((size_t)(f.n * f.ldp));
+    }
+    if (f.n > 0 && !f.Xb) {
         if (f.ldp == f.d && M->ld == f.d) {
             HIP_TRY(hipMemcpyAsync(f.X.p, M->values,
                                    (size_t)(f.n * f.d) * sizeof(float), kind,
@@ -124,7 +131,7 @@ void load_features(const svm_matrix* M, Features& f, Context& cx)
     }
     DevBuf<int32_t> bad(1);
     HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
-    launch_norms(f.X.p, f.n, f.ldp, f.sq.p, bad.p, cx.stream);
+    launch_norms(f.x(), f.n, f.ldp, f.sq.p, bad.p, cx.stream);
     int32_t hb = 0;
     HIP_TRY(hipMemcpyAsync(&hb, bad.p, sizeof(int32_t),
                            hipMemcpyDeviceToHost, cx.stream));
@@ -501,7 +508,7 @@ void Solver::set_csr(SelArgs& a, int nbc)
 void Solver::launch_keys()
 {
     RowArgs a{};
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.rp = f_.rp.p;
     a.ci = f_.ci.p;
     a.cv = f_.cv.p;
@@ -531,7 +538,7 @@ void Solver::launch_keys()
 void Solver::launch_keys_fused()
 {
     RowArgs a{};
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.sq = f_.sq.p;
     a.F = F_.p;
     a.st = st_.p;
@@ -555,7 +562,7 @@ void Solver::launch_keys_fused()
 void Solver::launch_hot_rows(hipEvent_t e0, hipEvent_t e1)
 {
     RowArgs a{};
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.rp = f_.rp.p;
     a.ci = f_.ci.p;
     a.cv = f_.cv.p;
@@ -596,7 +603,7 @@ void Solver::launch_solve(int32_t mode, hipEvent_t e0, hipEvent_t e1)
     a.st = st_.p;
     a.F = F_.p;
     a.z = y_.p;
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.rp = f_.rp.p;
     a.ci = f_.ci.p;
     a.cv = f_.cv.p;
@@ -793,7 +800,7 @@ bool Solver::run_loop_fused(SolveResult& r)
     int64_t last_iter = w0.iter;
     const int64_t units = (n_ + 31) / 32;
     IterArgs a{};
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.sq = f_.sq.p;
     a.z = y_.p;
     a.alpha = alpha_.p;
@@ -1169,7 +1176,7 @@ std::vector<SolveResult> Solver::train_lockstep(
     // arguments of the active problems, by position
     auto build = [&]() {
         la = LockArgs{};
-        la.X = f.X.p;
+        la.X = f.x();
         la.sq = f.sq.p;
         la.xS = xs.p;
         la.n = n;
@@ -1195,7 +1202,7 @@ std::vector<SolveResult> Solver::train_lockstep(
             a.st = s.st_.p;
             a.F = s.F_.p;
             a.z = s.y_.p;
-            a.X = f.X.p;
+            a.X = f.x();
             a.sq = f.sq.p;
             a.xS = xs.p + (size_t)q * 16 * f.ldp;
             a.csr_cols = -1;
@@ -1458,7 +1465,7 @@ void Solver::rows(const int32_t* samples, int32_t k, float* out_h)
     cx_.sync();
     if (rows_out_.count < (size_t)(k * n_)) rows_out_.alloc((size_t)(k * n_));
     RowArgs a{};
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.rp = f_.rp.p;
     a.ci = f_.ci.p;
     a.cv = f_.cv.p;
@@ -1507,7 +1514,7 @@ void Solver::subproblem(const int32_t* B, int32_t nB, double inner_tol,
     a.st = st_.p;
     a.F = F_.p;
     a.z = y_.p;
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.rp = f_.rp.p;
     a.ci = f_.ci.p;
     a.cv = f_.cv.p;
@@ -1554,7 +1561,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     a.st = st_.p;
     a.F = F_.p;
     a.z = y_.p;
-    a.X = f_.X.p;
+    a.X = f_.x();
     a.rp = f_.rp.p;
     a.ci = f_.ci.p;
     a.cv = f_.cv.p;
@@ -1577,7 +1584,7 @@ void Solver::apply(const int32_t* B, int32_t nB, const double* alpha_B)
     int nbc = nB <= 16 ? 1 : (nB <= 32 ? 2 : 4);
     launch_select(a, nbc, o_.type == SVM_EPS_SVR, s);
     RowArgs r{};
-    r.X = f_.X.p;
+    r.X = f_.x();
     r.rp = f_.rp.p;
     r.ci = f_.ci.p;
     r.cv = f_.cv.p;
@@ -1685,7 +1692,7 @@ void scale_fit(const Features& f, Context& cx, DevBuf<double>& mu,
     mu.alloc((size_t)f.d);
     sd.alloc((size_t)f.d);
     DevBuf<double> part((size_t)col_stats_partials(f.n, f.d));
-    launch_col_stats(f.X.p, f.n, f.ldp, f.d, part.p, mu.p, sd.p, cx.stream);
+    launch_col_stats(f.x(), f.n, f.ldp, f.d, part.p, mu.p, sd.p, cx.stream);
     cx.sync();
 }
 
@@ -1694,6 +1701,12 @@ void scale_apply(Features& f, Context& cx, const double* mu, const double* sd)
     if (f.csr)
         throw Error{SVM_E_UNSUPPORTED,
                     "a model trained on scaled data predicts dense rows only"};
+    if (f.Xb) {  // scaled in place: the caller's rows are copied first
+        f.X.alloc((size_t)(f.n * f.ldp));
+        HIP_TRY(hipMemcpyAsync(f.X.p, f.Xb, f.X.bytes(),
+                               hipMemcpyDeviceToDevice, cx.stream));
+        f.Xb = nullptr;
+    }
     launch_scale_apply(f.X.p, f.n, f.ldp, f.d, mu, sd, cx.stream);
     DevBuf<int32_t> bad(1);
     HIP_TRY(hipMemsetAsync(bad.p, 0, sizeof(int32_t), cx.stream));
@@ -1788,7 +1801,7 @@ void gather_rows(const Features& f, const int32_t* idx, int64_t k, float* out,
         launch_gather_rows_csr(f.rp.p, f.ci.p, f.cv.p, f.sq.p, f.ldp, idx, 0,
                                k, out, sq_out, s);
     else
-        launch_gather_rows(f.X.p, f.sq.p, f.ldp, idx, k, out, sq_out, s);
+        launch_gather_rows(f.x(), f.sq.p, f.ldp, idx, k, out, sq_out, s);
 }
 
 // SVM_SPARSE_PATH: 1 = "table" (the factored path is not built), 2 =
@@ -1904,7 +1917,7 @@ void predict_rows(PredictArgs a, const Features& t, hipStream_t s,
     a.ldp = t.ldp;
     a.nrange = predict_ranges(a.nsv);
     if (!t.csr) {
-        a.Xt = t.X.p;
+        a.Xt = t.x();
         a.sqt = t.sq.p;
         a.m = t.n;
         a.row_base = 0;

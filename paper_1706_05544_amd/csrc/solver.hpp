@@ -143,6 +143,10 @@ struct Features {
     int64_t maxnz = 0;  // CSR: nonzeros of the longest row
     bool csr = false;
     DevBuf<float> X, sq;
+    // dense device input already in the padded layout (ld = ldp = d, 16-byte
+    // aligned): used in place for the duration of the call, not copied
+    const float* Xb = nullptr;
+    const float* x() const { return Xb ? Xb : X.p; }
     DevBuf<int64_t> rp;
     DevBuf<int32_t> ci;
     DevBuf<float> cv;
@@ -156,7 +160,11 @@ struct Features {
 
 // Uploads X (host or device) into the padded layout and computes norms.
 // Throws Error{SVM_E_INVALID} if a value is not finite.
-void load_features(const svm_matrix* M, Features& f, Context& cx);
+// borrow: dense device input already in the padded layout is used in place
+// (the caller's buffer must outlive f; only for calls that return before
+// the caller regains it).
+void load_features(const svm_matrix* M, Features& f, Context& cx,
+                   bool borrow = false);
 
 int64_t padded_ld(int64_t d);
 
