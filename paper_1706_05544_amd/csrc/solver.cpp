@@ -675,10 +675,14 @@ bool Solver::run_loop(SolveResult& r)
     // the timed launches are a sample spread over the whole solve
     int64_t chunk_no = 0;
     bool timed[2] = {false, false};
-    auto enqueue = [&](int slot) {
+    int kc[2] = {K, K};  // iterations queued in each chunk
+    double gmin = -1.0;  // smallest gap polled so far, and its iteration
+    int64_t it_min = 0;
+    auto enqueue = [&](int slot, int kk) {
         timed[slot] = o_.profile && chunk_no % kProfileEvery == 0;
         ++chunk_no;
-        for (int k = 0; k < K; ++k) {
+        kc[slot] = kk;
+        for (int k = 0; k < kk; ++k) {
             // the events are part of the kernel's own dispatch, so they
             // bracket its execution, not the queue around it
             const size_t e = (size_t)(slot * K + k) * 4;
@@ -699,14 +703,14 @@ bool Solver::run_loop(SolveResult& r)
         HIP_TRY(hipEventRecord(ev[slot], cx_.stream));
     };
 
-    enqueue(0);
-    enqueue(1);
+    enqueue(0, K);
+    enqueue(1, K);
     int cur = 0;
     for (;;) {
         HIP_TRY(hipEventSynchronize(ev[cur]));
         const WorkingSet& w = hs.p[cur];
         if (timed[cur]) {
-            int64_t real = std::min<int64_t>(w.iter - last_iter, K);
+            int64_t real = std::min<int64_t>(w.iter - last_iter, kc[cur]);
             // algorithmic bytes of a launch: computed from X, the features,
             // norm, F read and written and the state byte(s) (eps-SVR: and
             // the target) of every row, plus the rows written to the cache;
@@ -758,7 +762,27 @@ bool Solver::run_loop(SolveResult& r)
             throw Error{SVM_E_INTERNAL, "solver state made no progress"};
         }
         last_iter = w.iter;
-        enqueue(cur);
+        // Near the end the chunks shrink: the launches queued behind the
+        // converged iteration return at once but still cost a launch each
+        // (about 5 us a pair), and a whole chunk is in flight when the host
+        // sees convergence.  The iterations still to go are estimated from
+        // the rate at which the smallest gap seen so far has been falling
+        // (log scale); a chunk is then about half of them, at least K / 8.
+        // The device stops at the same iteration whatever the chunking.
+        int next = K;
+        if (w.gap > o_.tol && gmin > 0.0 && w.gap < gmin) {
+            const double rate = std::log(gmin / w.gap) /
+                                (double)std::max<int64_t>(w.iter - it_min, 1);
+            const double togo = std::log(w.gap / o_.tol) / rate;
+            if (togo < 2.0 * K)
+                next = std::max(std::max(K / 8, 1),
+                                std::min(K, (int)(0.5 * togo)));
+        }
+        if (gmin <= 0.0 || w.gap < gmin) {
+            gmin = w.gap;
+            it_min = w.iter;
+        }
+        enqueue(cur, next);
         cur ^= 1;
     }
     cx_.sync();
