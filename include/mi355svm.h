@@ -111,8 +111,8 @@ typedef struct {
                               training: svm_cache_release) */
     void *stream;          /* hipStream_t; NULL: a stream of the library */
     int32_t check_every;   /* outer iterations between host polls (0: 64;
-                              an eighth to a quarter of it once the gap is
-                              within 8 tol) */
+                              fewer near convergence, down to an eighth,
+                              from the rate at which the gap falls) */
     double inner_ratio;    /* subproblem stops at local gap <= max(ratio *
                               global gap, tol/2); 0: 0.3 */
     int32_t max_inner;     /* subproblem step cap; 0: 8 q */
